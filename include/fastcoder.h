@@ -1,0 +1,213 @@
+/*
+ * fastcoder.h - C ABI of the MI355X (gfx950) draft-stage library for
+ * retrieval-based speculative decoding after FastCoder (arXiv 2502.17139).
+ *
+ * The library implements the data-parallel hot path of the draft stage:
+ * suffix-array construction over token datastores, longest-suffix retrieval
+ * over prioritised stores with continuation gather, the frequency-weighted
+ * draft trie pruned to c nodes with its tree-attention mask and position ids,
+ * and greedy acceptance of the longest matching root-to-leaf path.
+ *
+ * Conventions shared by every entry point:
+ *  - Buffers named in a signature are DEVICE pointers (HBM) owned by the
+ *    caller, unless marked "host".  The library never allocates or frees
+ *    device memory; scratch space comes from a caller-provided workspace whose
+ *    size the matching *_workspace_bytes function reports.
+ *  - Calls enqueue work on `stream` and return without waiting, except
+ *    fc_datastore_build, which synchronises `stream` between its rounds.
+ *  - Arguments are validated on the host before anything is launched; a
+ *    failed check returns its status and writes nothing.  FC_ERR_DEVICE
+ *    reports a HIP launch or runtime error.  No exception crosses the ABI,
+ *    nothing calls exit/abort, and there is no global mutable state: calls on
+ *    different streams may run concurrently when their buffers do not overlap.
+ *  - Arrays are row-major and densely packed; [B][k] means B rows of k.
+ *  - Tokens are uint16.  Token 0 separates files: a context never reaches
+ *    back past a 0, so no match straddles two files.
+ */
+#ifndef FASTCODER_H
+#define FASTCODER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum fc_status {
+  FC_OK = 0,
+  FC_ERR_INVALID = 1,     /* null pointer, size or parameter out of range */
+  FC_ERR_WORKSPACE = 2,   /* workspace pointer null or smaller than required */
+  FC_ERR_DEVICE = 3,      /* HIP launch/runtime error, or a device-side check failed */
+  FC_ERR_UNSUPPORTED = 4  /* valid request outside what this build handles */
+} fc_status;
+
+#define FC_MAX_SOURCES 4     /* stores per retrieval */
+#define FC_MAX_NMAX 16       /* longest context suffix searched (n_max) */
+#define FC_MAX_TREE_ROWS 256 /* c + 1 (root + kept nodes) */
+#define FC_BUCKETS 65537     /* entries of a store's first-token table */
+
+/* ABI revision; bumped on any incompatible change. */
+int32_t fc_abi_version(void);
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* fc_status_string(fc_status s);
+
+/* ------------------------------------------------------------------------ */
+/* Datastore index                                                           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Suffix array of a token datastore (Section III-A: exact suffix matching
+ * over a suffix array after Manber and Myers; Section IV-A: every position of
+ * a file splits it into a context and a continuation).
+ *
+ * tokens [n]   : the datastore text, files joined by single 0 tokens.
+ * sa_out [n]   : receives the start positions 0..n-1 sorted by suffix order:
+ *                token by token by numeric id, a suffix that ends first
+ *                (a proper prefix) sorting lower.  The order is total, so the
+ *                result is unique.
+ * ws, ws_bytes : workspace of at least fc_datastore_build_workspace_bytes(n).
+ * Built by prefix doubling: suffixes are sorted by their first 3 tokens, then
+ * by (rank of the first h tokens, rank of the h tokens after them) with h
+ * doubling, each round an LSD radix sort restricted to still-tied suffixes.
+ * Synchronises `stream` once per round (it reads the number of tied
+ * suffixes).  Requires n < 2^32 - 1.  n == 0 is a no-op.
+ */
+size_t fc_datastore_build_workspace_bytes(uint64_t n);
+fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint32_t* sa_out, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/*
+ * First-token table of a store: bucket_out[t] (t = 0..65536) = number of
+ * suffixes whose first token is below t, i.e. the suffix-array index where
+ * suffixes starting with token t begin (the bucket table Manber and Myers
+ * use to shorten the search).  bucket_out has FC_BUCKETS entries.
+ */
+fc_status fc_store_prepare(const uint16_t* tokens, const uint32_t* sa, uint64_t n, uint32_t* bucket_out,
+                           hipStream_t stream);
+
+/* A read-only view of one store; all pointers are device pointers. */
+typedef struct fc_store {
+  const uint16_t* tokens; /* [n] text */
+  const uint32_t* sa;     /* [n] suffix array of tokens */
+  const uint32_t* bucket; /* [FC_BUCKETS] table from fc_store_prepare */
+  uint64_t n;             /* tokens in the store, < 2^32 - 1 */
+} fc_store;
+
+/* ------------------------------------------------------------------------ */
+/* Retrieval                                                                 */
+/* ------------------------------------------------------------------------ */
+
+typedef struct fc_retrieve_params {
+  int32_t n_max; /* longest context suffix tried, 1..16 (paper: 16) */
+  int32_t n_min; /* shortest suffix tried, 1..n_max */
+  int32_t k;     /* continuation slots per query (retrieval cap), >= 1 */
+  int32_t m;     /* tokens per continuation, 1..255 */
+} fc_retrieve_params;
+
+/*
+ * Batched longest-suffix retrieval over S stores in priority order
+ * (Section III-A; two stores, the repository store first and the common store
+ * second, searched side by side: Section IV-A, Section IV-C).
+ *
+ * stores (host) [S] : store views, S in 1..FC_MAX_SOURCES.
+ * ctx [B][L]        : the last L context tokens of each query.
+ * For each query and store: n_hi = min(n_max, L, trailing non-zero tokens of
+ * the context); for n = n_hi down to n_min the suffix q = ctx[L-n..L) is
+ * searched and the first n with an occurrence wins.
+ * match_n   [B][S] : that n, or 0 when no n in [n_min, n_hi] occurs.
+ * range_lo  [B][S] : suffix-array index of the first suffix starting with q
+ *                    (0 when there is no match).
+ * range_cnt [B][S] : number of occurrences of q.
+ * taken     [B][S] : slots store s fills: min(k - slots of stores before it,
+ *                    range_cnt).  When range_cnt exceeds that budget b, the
+ *                    occurrences at range offsets floor(i*range_cnt/b),
+ *                    i = 0..b-1, are kept (a strided sample that keeps every
+ *                    continuation prefix's share to within one); otherwise
+ *                    all are kept, in suffix-array order.
+ * Slot i of a query: store 0's kept occurrences first, then store 1's, ...;
+ * slots at or past the query's total taken are not written (their contents
+ * are whatever the buffers held), which saves writing k slots per query.
+ * cont_pos [B][k]    : text position where the continuation starts (match
+ *                      start + match_n).
+ * cont_src [B][k]    : store index.
+ * cont_len [B][k]    : continuation length 0..m: up to m tokens, cut before
+ *                      the first 0 and at the end of the store.
+ * cont_tok [B][k][m] : continuation tokens, 0 past cont_len.
+ * Within one store's slots the continuations come out in lexicographic order
+ * (suffix order), which fc_build_tree relies on.
+ * ws may be NULL when fc_retrieve_workspace_bytes returns 0.
+ */
+size_t fc_retrieve_workspace_bytes(int32_t B, int32_t S, fc_retrieve_params p);
+fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
+                      fc_retrieve_params p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
+                      int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len, uint16_t* cont_tok,
+                      void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Draft tree                                                                */
+/* ------------------------------------------------------------------------ */
+
+typedef struct fc_tree_params {
+  int32_t c;                       /* kept nodes (draft tokens), 1..255 (paper: 64) */
+  uint32_t alpha[FC_MAX_SOURCES];  /* weight of one occurrence per store (paper: alpha = beta = 1) */
+} fc_tree_params;
+
+/*
+ * Frequency-weighted draft trie pruned to c nodes (Section IV-D, eq. (3));
+ * tree-attention mask and position ids (Section IV-D, eq. (4)).
+ *
+ * Inputs are fc_retrieve's outputs: taken [B][S], cont_len [B][k],
+ * cont_tok [B][k][m], and ctx [B][L] for the root token ctx[L-1].
+ * Precondition: within each store's slots the continuations are in
+ * lexicographic order (a prefix first), as fc_retrieve produces them; a query
+ * that violates it gets num_nodes = -1 and padding rows.
+ * Every non-empty continuation enters a trie; node weight = sum of alpha[s]
+ * over the continuations through the node.  The c highest nodes are kept,
+ * ranked by weight, ties by path (token by token, a prefix first); this set
+ * is closed under ancestors.  Rows: 0 is the root (token ctx[L-1], parent -1,
+ * weight = sum of alpha over non-empty continuations, position 0), then the
+ * kept nodes in preorder with children in token order.
+ * num_nodes [B]           : 1 + kept nodes.
+ * node_tok, parent [B][c+1], weight [B][c+1] (uint32), pos_ids [B][c+1]
+ *                         : token, parent row, weight, depth of each row.
+ * mask [B][c+1][c+1]      : 1 where column j is row i or an ancestor of i
+ *                           (root included), else 0.
+ * Rows past num_nodes: token 0, parent -1, weight 0, position 0, mask 0.
+ * Limits: S <= FC_MAX_SOURCES, k <= 65535, and the per-query working set
+ * (about k*(2m+9) bytes) must fit one workgroup's LDS (FC_ERR_UNSUPPORTED).
+ */
+fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok,
+                        const uint16_t* ctx, int32_t B, int32_t L, int32_t S, int32_t k, int32_t m, fc_tree_params t,
+                        int32_t* num_nodes, int32_t* node_tok, int32_t* parent, uint32_t* weight, int32_t* pos_ids,
+                        int32_t* mask, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Acceptance                                                                */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Greedy acceptance (Section IV-D: every correct draft token from the start
+ * is accepted, everything after the first error rejected).
+ * target [B][c+1]: the target model's next token after each tree row, -1
+ * when there is none.  From the root, step to the child whose token equals
+ * the current row's target while one exists.  With u the row reached:
+ * accept_len [B]    : depth(u) + 1 (the path plus target[u]), or depth(u)
+ *                     when target[u] is -1.
+ * accept_tok [B][m+1]: the path tokens then target[u]; -1 past accept_len.
+ * last_node [B]     : u.
+ * The tree arrays are fc_build_tree's outputs; a query with num_nodes < 1 is
+ * treated as a bare root.
+ */
+fc_status fc_verify_accept(const int32_t* num_nodes, const int32_t* node_tok, const int32_t* parent,
+                           const int32_t* pos_ids, const int32_t* target, int32_t B, int32_t c, int32_t m,
+                           int32_t* accept_len, int32_t* accept_tok, int32_t* last_node, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FASTCODER_H */

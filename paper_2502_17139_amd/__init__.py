@@ -1,0 +1,244 @@
+"""MI355X (gfx950) draft-stage retrieval library for retrieval-based
+speculative decoding after FastCoder (arXiv 2502.17139).
+
+The compute lives in libfastcoder.so (hand-written HIP kernels behind the C
+ABI of include/fastcoder.h).  This module is the thin Python binding: the
+functions carry the C entry points' names, take torch tensors on the GPU for
+device memory and the current torch stream for ordering, and only marshal
+arguments.  There is no CPU path: without the built library every call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import functools
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfastcoder.so")
+
+FC_MAX_SOURCES = 4
+FC_MAX_NMAX = 16
+FC_MAX_TREE_ROWS = 256
+FC_BUCKETS = 65537
+
+STATUS = {0: "FC_OK", 1: "FC_ERR_INVALID", 2: "FC_ERR_WORKSPACE", 3: "FC_ERR_DEVICE", 4: "FC_ERR_UNSUPPORTED"}
+
+# Names of every entry point the header declares.
+EXPORTS = (
+    "fc_abi_version", "fc_status_string",
+    "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_store_prepare",
+    "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree", "fc_verify_accept",
+)
+
+
+class FcError(RuntimeError):
+    """A non-OK status from the library."""
+
+    def __init__(self, fn: str, code: int, text: str):
+        super().__init__(f"{fn} failed: {text}")
+        self.code = code
+
+
+class FcStore(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_void_p), ("sa", ctypes.c_void_p), ("bucket", ctypes.c_void_p),
+                ("n", ctypes.c_uint64)]
+
+
+class FcRetrieveParams(ctypes.Structure):
+    _fields_ = [("n_max", ctypes.c_int32), ("n_min", ctypes.c_int32), ("k", ctypes.c_int32), ("m", ctypes.c_int32)]
+
+
+class FcTreeParams(ctypes.Structure):
+    _fields_ = [("c", ctypes.c_int32), ("alpha", ctypes.c_uint32 * FC_MAX_SOURCES)]
+
+
+@functools.lru_cache(maxsize=1)
+def lib() -> ctypes.CDLL:
+    """Load libfastcoder.so (torch is imported first so its HIP runtime is the
+    one the library binds to)."""
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(hipcc --offload-arch=gfx950); there is no CPU fallback")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, u32, u64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_size_t
+    L.fc_abi_version.restype = i32
+    L.fc_abi_version.argtypes = []
+    L.fc_status_string.restype = ctypes.c_char_p
+    L.fc_status_string.argtypes = [ctypes.c_int]
+    L.fc_datastore_build_workspace_bytes.restype = sz
+    L.fc_datastore_build_workspace_bytes.argtypes = [u64]
+    L.fc_datastore_build.restype = ctypes.c_int
+    L.fc_datastore_build.argtypes = [vp, u64, vp, vp, sz, vp]
+    L.fc_store_prepare.restype = ctypes.c_int
+    L.fc_store_prepare.argtypes = [vp, vp, u64, vp, vp]
+    L.fc_retrieve_workspace_bytes.restype = sz
+    L.fc_retrieve_workspace_bytes.argtypes = [i32, i32, FcRetrieveParams]
+    L.fc_retrieve.restype = ctypes.c_int
+    L.fc_retrieve.argtypes = [ctypes.POINTER(FcStore), i32, vp, i32, i32, FcRetrieveParams,
+                              vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.fc_build_tree.restype = ctypes.c_int
+    L.fc_build_tree.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, FcTreeParams,
+                                vp, vp, vp, vp, vp, vp, vp]
+    L.fc_verify_accept.restype = ctypes.c_int
+    L.fc_verify_accept.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp]
+    return L
+
+
+def _check(fn: str, code: int) -> None:
+    if code != 0:
+        raise FcError(fn, code, lib().fc_status_string(code).decode())
+
+
+def _ptr(t: torch.Tensor | None) -> ctypes.c_void_p:
+    if t is None:
+        return ctypes.c_void_p(0)
+    if not t.is_cuda:
+        raise ValueError("device tensor expected")
+    if not t.is_contiguous():
+        raise ValueError("contiguous tensor expected")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _empty(shape, dtype, device) -> torch.Tensor:
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+# ---------------------------------------------------------------- index ----
+
+def fc_datastore_build_workspace_bytes(n: int) -> int:
+    return int(lib().fc_datastore_build_workspace_bytes(n))
+
+
+def fc_datastore_build(tokens: torch.Tensor, sa_out: torch.Tensor | None = None,
+                       workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Suffix array (uint32[n]) of a uint16 token tensor on the GPU."""
+    if tokens.dtype != torch.uint16 or tokens.dim() != 1:
+        raise ValueError("tokens must be a 1-D uint16 tensor")
+    n = tokens.numel()
+    if sa_out is None:
+        sa_out = _empty(n, torch.uint32, tokens.device)
+    need = fc_datastore_build_workspace_bytes(n)
+    if workspace is None:
+        workspace = _empty(max(need, 1), torch.uint8, tokens.device)
+    _check("fc_datastore_build", lib().fc_datastore_build(_ptr(tokens), n, _ptr(sa_out), _ptr(workspace),
+                                                         workspace.numel(), _stream(stream)))
+    return sa_out
+
+
+def fc_store_prepare(tokens: torch.Tensor, sa: torch.Tensor, bucket_out: torch.Tensor | None = None,
+                     stream=None) -> torch.Tensor:
+    """First-token table (uint32[FC_BUCKETS]) of a store."""
+    if bucket_out is None:
+        bucket_out = _empty(FC_BUCKETS, torch.uint32, tokens.device)
+    _check("fc_store_prepare", lib().fc_store_prepare(_ptr(tokens), _ptr(sa), tokens.numel(), _ptr(bucket_out),
+                                                     _stream(stream)))
+    return bucket_out
+
+
+class Store:
+    """A datastore resident on the GPU: tokens, suffix array, bucket table."""
+
+    def __init__(self, tokens: torch.Tensor, sa: torch.Tensor | None = None, bucket: torch.Tensor | None = None,
+                 stream=None):
+        self.tokens = tokens
+        self.sa = fc_datastore_build(tokens, stream=stream) if sa is None else sa
+        self.bucket = fc_store_prepare(tokens, self.sa, stream=stream) if bucket is None else bucket
+
+    @property
+    def n(self) -> int:
+        return self.tokens.numel()
+
+    def view(self) -> FcStore:
+        return FcStore(self.tokens.data_ptr(), self.sa.data_ptr(), self.bucket.data_ptr(), self.n)
+
+
+# ------------------------------------------------------------ retrieval ----
+
+RETRIEVE_FIELDS = ("match_n", "range_lo", "range_cnt", "taken", "cont_pos", "cont_src", "cont_len", "cont_tok")
+
+
+def retrieve_outputs(B: int, S: int, k: int, m: int, device) -> dict:
+    return dict(
+        match_n=_empty((B, S), torch.int32, device), range_lo=_empty((B, S), torch.uint32, device),
+        range_cnt=_empty((B, S), torch.uint32, device), taken=_empty((B, S), torch.int32, device),
+        cont_pos=_empty((B, k), torch.uint32, device), cont_src=_empty((B, k), torch.uint8, device),
+        cont_len=_empty((B, k), torch.uint8, device), cont_tok=_empty((B, k, m), torch.uint16, device))
+
+
+def fc_retrieve(stores, ctx: torch.Tensor, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int = 10,
+                out: dict | None = None, workspace: torch.Tensor | None = None, stream=None) -> dict:
+    """Batched longest-suffix retrieval; ctx is uint16 [B][L] on the GPU."""
+    if ctx.dtype != torch.uint16 or ctx.dim() != 2:
+        raise ValueError("ctx must be a 2-D uint16 tensor")
+    B, L = ctx.shape
+    S = len(stores)
+    views = (FcStore * max(S, 1))(*[s.view() for s in stores])
+    p = FcRetrieveParams(n_max, n_min, k, m)
+    if out is None:
+        out = retrieve_outputs(B, S, k, m, ctx.device)
+    need = int(lib().fc_retrieve_workspace_bytes(B, S, p))
+    if workspace is None and need > 0:
+        workspace = _empty(need, torch.uint8, ctx.device)
+    _check("fc_retrieve", lib().fc_retrieve(
+        views, S, _ptr(ctx), B, L, p, *[_ptr(out[f]) for f in RETRIEVE_FIELDS],
+        _ptr(workspace), 0 if workspace is None else workspace.numel(), _stream(stream)))
+    return out
+
+
+# ----------------------------------------------------------------- tree ----
+
+TREE_FIELDS = ("num_nodes", "node_tok", "parent", "weight", "pos_ids", "mask")
+
+
+def tree_outputs(B: int, c: int, device) -> dict:
+    R = c + 1
+    return dict(num_nodes=_empty(B, torch.int32, device), node_tok=_empty((B, R), torch.int32, device),
+                parent=_empty((B, R), torch.int32, device), weight=_empty((B, R), torch.uint32, device),
+                pos_ids=_empty((B, R), torch.int32, device), mask=_empty((B, R, R), torch.int32, device))
+
+
+def fc_build_tree(taken: torch.Tensor, cont_len: torch.Tensor, cont_tok: torch.Tensor, ctx: torch.Tensor,
+                  c: int = 64, alpha=(1, 1), out: dict | None = None, stream=None) -> dict:
+    """Weighted draft trie pruned to c nodes, with mask and position ids."""
+    B, S = taken.shape
+    k, m = cont_tok.shape[1], cont_tok.shape[2]
+    L = ctx.shape[1]
+    a = list(alpha)[:S]
+    if len(a) != S:
+        raise ValueError("need one alpha per store")
+    tp = FcTreeParams(c, (ctypes.c_uint32 * FC_MAX_SOURCES)(*(a + [0] * (FC_MAX_SOURCES - S))))
+    if out is None:
+        out = tree_outputs(B, c, ctx.device)
+    _check("fc_build_tree", lib().fc_build_tree(
+        _ptr(taken), _ptr(cont_len), _ptr(cont_tok), _ptr(ctx), B, L, S, k, m, tp,
+        *[_ptr(out[f]) for f in TREE_FIELDS], _stream(stream)))
+    return out
+
+
+# ----------------------------------------------------------- acceptance ----
+
+ACCEPT_FIELDS = ("accept_len", "accept_tok", "last_node")
+
+
+def accept_outputs(B: int, m: int, device) -> dict:
+    return dict(accept_len=_empty(B, torch.int32, device), accept_tok=_empty((B, m + 1), torch.int32, device),
+                last_node=_empty(B, torch.int32, device))
+
+
+def fc_verify_accept(tree: dict, target: torch.Tensor, m: int = 10, out: dict | None = None, stream=None) -> dict:
+    """Longest accepted root path against per-row target tokens ([B][c+1])."""
+    B, R = tree["node_tok"].shape
+    if out is None:
+        out = accept_outputs(B, m, target.device)
+    _check("fc_verify_accept", lib().fc_verify_accept(
+        _ptr(tree["num_nodes"]), _ptr(tree["node_tok"]), _ptr(tree["parent"]), _ptr(tree["pos_ids"]),
+        _ptr(target), B, R - 1, m, *[_ptr(out[f]) for f in ACCEPT_FIELDS], _stream(stream)))
+    return out

@@ -1,0 +1,237 @@
+// Longest-suffix retrieval with continuation gather on gfx950 (fc_retrieve).
+//
+// For every query and store the method looks for the longest suffix of the
+// context, from n_max tokens down, that occurs in the datastore, and returns
+// what follows each occurrence (Section III-A; the repository store and the
+// common store are searched side by side, Section IV-A and Section IV-C).
+//
+// k_search: one wave per query.  The wave's lanes take the (store, n, bound)
+// triples - 2 stores x 15 lengths x {lower, upper} = 60 lanes at the paper's
+// n_max = 16, n_min = 2 - so every candidate length is searched at once and
+// the dependent probe chain is one binary search long instead of fifteen.
+// Each search starts from the first-token bucket of the store (one table
+// read replaces the top ~15 levels of the search) and compares from the
+// second token on.  The wave then keeps, per store, the longest n whose range
+// is non-empty and fills the k slots in store priority order.
+//
+// k_gather: one thread per (query, slot).  A slot maps to its store and
+// range offset (strided floor(i*cnt/b) when the range exceeds the store's
+// budget b), reads the suffix-array entry and copies up to m continuation
+// tokens, cut before a 0 and at the end of the store.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fastcoder.h"
+#include "fc_device.h"
+#include "fc_host.h"
+
+namespace {
+
+constexpr int kSearchThreads = 256;
+constexpr int kQueriesPerBlock = kSearchThreads / fc::kWave;
+constexpr int kGatherThreads = 256;
+
+struct StoreArgs {
+  const uint16_t* tok[FC_MAX_SOURCES];
+  const uint32_t* sa[FC_MAX_SOURCES];
+  const uint32_t* bucket[FC_MAX_SOURCES];
+  uint32_t n[FC_MAX_SOURCES];
+};
+
+// Suffix j against pattern q[0..n) from token `from` on: -1 below (a suffix
+// that ends first is below), 0 starts with q, +1 above.
+__device__ __forceinline__ int cmp_suffix(const uint16_t* __restrict__ T, uint32_t N, uint32_t j,
+                                          const uint16_t* q, int n, int from) {
+  for (int x = from; x < n; ++x) {
+    const uint64_t p = (uint64_t)j + (uint64_t)x;
+    if (p >= N) return -1;
+    const uint16_t a = T[p];
+    const uint16_t b = q[x];
+    if (a != b) return a < b ? -1 : 1;
+  }
+  return 0;
+}
+
+__global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, const uint16_t* __restrict__ ctx,
+                                                           int B, int L, int n_max, int n_min, int k,
+                                                           int32_t* __restrict__ match_n,
+                                                           uint32_t* __restrict__ range_lo,
+                                                           uint32_t* __restrict__ range_cnt,
+                                                           int32_t* __restrict__ taken) {
+  __shared__ uint16_t s_q[kQueriesPerBlock][FC_MAX_NMAX];
+  __shared__ uint32_t s_lo[kQueriesPerBlock][FC_MAX_SOURCES][FC_MAX_NMAX];
+  __shared__ uint32_t s_hi[kQueriesPerBlock][FC_MAX_SOURCES][FC_MAX_NMAX];
+  __shared__ int s_nhi[kQueriesPerBlock];
+
+  const int w = threadIdx.x / fc::kWave;
+  const int lane = fc::lane_id();
+  const int b = blockIdx.x * kQueriesPerBlock + w;
+  const bool active = b < B;
+  const int nq = L < FC_MAX_NMAX ? L : FC_MAX_NMAX;  // tokens of the context kept
+
+  if (active && lane < nq) s_q[w][FC_MAX_NMAX - nq + lane] = ctx[(int64_t)b * L + (L - nq + lane)];
+  if (active && lane < FC_MAX_SOURCES * FC_MAX_NMAX) {
+    (&s_lo[w][0][0])[lane] = 0;
+    (&s_hi[w][0][0])[lane] = 0;
+  }
+  __syncthreads();
+  if (active && lane == 0) {
+    int tail = 0;
+    while (tail < nq && s_q[w][FC_MAX_NMAX - 1 - tail] != 0) ++tail;
+    int h = n_max < L ? n_max : L;
+    s_nhi[w] = tail < h ? tail : h;
+  }
+  __syncthreads();
+
+  const int NN = n_max - n_min + 1;
+  const int tasks = S * NN * 2;
+  if (active) {
+    const int n_hi = s_nhi[w];
+    for (int t = lane; t < tasks; t += fc::kWave) {
+      const int s = t / (2 * NN);
+      const int rem = t - s * 2 * NN;
+      const int ni = rem >> 1;
+      const int upper = rem & 1;
+      const int n = n_max - ni;
+      if (n > n_hi || n < n_min) continue;
+      const uint16_t* q = &s_q[w][FC_MAX_NMAX - n];
+      const uint16_t* T = st.tok[s];
+      const uint32_t* SA = st.sa[s];
+      const uint32_t N = st.n[s];
+      uint32_t lo = 0, hi = 0;
+      if (N > 0) {
+        lo = st.bucket[s][q[0]];
+        hi = st.bucket[s][q[0] + 1];
+      }
+      while (lo < hi) {
+        const uint32_t mid = lo + ((hi - lo) >> 1);
+        const int c = cmp_suffix(T, N, SA[mid], q, n, 1);
+        if (upper ? (c <= 0) : (c < 0)) lo = mid + 1; else hi = mid;
+      }
+      if (upper) s_hi[w][s][ni] = lo; else s_lo[w][s][ni] = lo;
+    }
+  }
+  __syncthreads();
+  if (active && lane == 0) {
+    const int n_hi = s_nhi[w];
+    int64_t used = 0;
+    for (int s = 0; s < S; ++s) {
+      int mn = 0;
+      uint32_t lo = 0, cnt = 0;
+      for (int n = n_hi; n >= n_min; --n) {
+        const int ni = n_max - n;
+        const uint32_t c = s_hi[w][s][ni] - s_lo[w][s][ni];
+        if (c > 0) {
+          mn = n;
+          lo = s_lo[w][s][ni];
+          cnt = c;
+          break;
+        }
+      }
+      const int64_t budget = (int64_t)k - used;
+      const int64_t tk = (int64_t)cnt < budget ? (int64_t)cnt : budget;
+      const int64_t o = (int64_t)b * S + s;
+      match_n[o] = mn;
+      range_lo[o] = lo;
+      range_cnt[o] = cnt;
+      taken[o] = (int32_t)tk;
+      used += tk;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, int k, int m,
+                                                           const int32_t* __restrict__ match_n,
+                                                           const uint32_t* __restrict__ range_lo,
+                                                           const uint32_t* __restrict__ range_cnt,
+                                                           const int32_t* __restrict__ taken,
+                                                           uint32_t* __restrict__ cont_pos,
+                                                           uint8_t* __restrict__ cont_src,
+                                                           uint8_t* __restrict__ cont_len,
+                                                           uint16_t* __restrict__ cont_tok) {
+  const uint32_t chunks = fc::div_up(k, kGatherThreads);
+  const int b = (int)(blockIdx.x / chunks);
+  const int i = (int)(blockIdx.x - (uint32_t)b * chunks) * kGatherThreads + (int)threadIdx.x;
+  if (i >= k) return;
+  const int64_t slot = (int64_t)b * k + i;
+  uint16_t* out = cont_tok + slot * m;
+  int64_t before = 0;
+  int src = -1;
+  for (int s = 0; s < S; ++s) {
+    const int64_t t = taken[(int64_t)b * S + s];
+    if (i < before + t) {
+      src = s;
+      break;
+    }
+    before += t;
+  }
+  if (src < 0) return;  // slots past the query's last kept occurrence are not written
+  const int64_t o = (int64_t)b * S + src;
+  const uint64_t cnt = range_cnt[o];
+  const uint64_t budget = (uint64_t)((int64_t)k - before);
+  const uint64_t local = (uint64_t)(i - before);
+  const uint64_t off = cnt > budget ? (local * cnt) / budget : local;
+  const uint32_t j = st.sa[src][(uint64_t)range_lo[o] + off];
+  const uint64_t start = (uint64_t)j + (uint64_t)match_n[o];
+  const uint16_t* T = st.tok[src];
+  const uint64_t N = st.n[src];
+  int len = 0;
+  bool open = true;
+  for (int x = 0; x < m; ++x) {
+    uint16_t v = 0;
+    if (open) {
+      const uint64_t p = start + (uint64_t)x;
+      if (p < N) v = T[p];
+      if (v == 0) open = false; else ++len;
+    }
+    out[x] = open ? v : 0;
+  }
+  cont_pos[slot] = (uint32_t)start;
+  cont_src[slot] = (uint8_t)src;
+  cont_len[slot] = (uint8_t)len;
+}
+
+}  // namespace
+
+extern "C" size_t fc_retrieve_workspace_bytes(int32_t B, int32_t S, fc_retrieve_params p) {
+  (void)B;
+  (void)S;
+  (void)p;
+  return 0;
+}
+
+extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
+                                 fc_retrieve_params p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
+                                 int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len,
+                                 uint16_t* cont_tok, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!stores || S < 1 || S > FC_MAX_SOURCES) return FC_ERR_INVALID;
+  if (B < 0 || L < 1) return FC_ERR_INVALID;
+  if (p.n_max < 1 || p.n_max > FC_MAX_NMAX || p.n_min < 1 || p.n_min > p.n_max) return FC_ERR_INVALID;
+  if (p.k < 1 || p.m < 1 || p.m > 255) return FC_ERR_INVALID;
+  if ((int64_t)S * (p.n_max - p.n_min + 1) * 2 > 4 * fc::kWave) return FC_ERR_INVALID;
+  StoreArgs st = {};
+  for (int s = 0; s < S; ++s) {
+    const fc_store& x = stores[s];
+    if (x.n >= 0xFFFFFFFFull) return FC_ERR_INVALID;
+    if (x.n > 0 && (!x.tokens || !x.sa || !x.bucket)) return FC_ERR_INVALID;
+    st.tok[s] = x.tokens;
+    st.sa[s] = x.sa;
+    st.bucket[s] = x.bucket;
+    st.n[s] = (uint32_t)x.n;
+  }
+  if (B == 0) return FC_OK;
+  if (!ctx || !match_n || !range_lo || !range_cnt || !taken || !cont_pos || !cont_src || !cont_len || !cont_tok)
+    return FC_ERR_INVALID;
+  const uint64_t gather_blocks = (uint64_t)B * fc::div_up(p.k, kGatherThreads);
+  if (gather_blocks > 0x7FFFFFFFull) return FC_ERR_UNSUPPORTED;
+  if (ws_bytes < fc_retrieve_workspace_bytes(B, S, p)) return FC_ERR_WORKSPACE;
+  (void)ws;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(k_search, dim3(fc::div_up(B, kQueriesPerBlock)), dim3(kSearchThreads), 0, stream, st, S, ctx,
+                     B, L, p.n_max, p.n_min, p.k, match_n, range_lo, range_cnt, taken);
+  FC_CHECK_LAUNCH();
+  hipLaunchKernelGGL(k_gather, dim3((uint32_t)gather_blocks), dim3(kGatherThreads), 0, stream, st, S,
+                     p.k, p.m, match_n, range_lo, range_cnt, taken, cont_pos, cont_src, cont_len, cont_tok);
+  FC_CHECK_LAUNCH();
+  return FC_OK;
+}

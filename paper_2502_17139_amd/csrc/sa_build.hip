@@ -1,0 +1,533 @@
+// Suffix-array construction on gfx950 (fc_datastore_build, fc_store_prepare).
+//
+// The datastore is indexed for exact suffix matching with a suffix array
+// (Section III-A, after Manber and Myers; datastore organisation in
+// Section IV-A).  Construction is prefix doubling, which is what Manber and
+// Myers' own construction does, with every round's sort done as an LSD radix
+// sort so it runs at HBM bandwidth:
+//
+//   round 0  key(i) = the first 3 tokens of suffix i, each as token+1 in 17
+//            bits with 0 past the end, so a suffix that ends first sorts
+//            first; all n suffixes are sorted.
+//   round r  (h = 3 * 2^(r-1)) only suffixes still tied with another are
+//            re-sorted, by key(i) = (rank[i], rank[i+h] + 1, or 0 past the
+//            end), where rank[i] is the suffix-array index at which i's group
+//            of equal h-token prefixes starts (Larsson and Sadakane's group
+//            numbering).  Suffixes whose group becomes a singleton drop out.
+//   finally  sa[rank[i]] = i.
+//
+// Each radix sort is a global digit histogram followed by one "onesweep"
+// pass per 8-bit digit (Adinets and Merrill 2022): a workgroup takes a tile
+// of 4096 keys (its tile id from an atomic ticket, so tiles start in order),
+// ranks them stably inside the tile with wave ballots, publishes per-digit
+// tile counts and resolves its global offsets by decoupled look-back over the
+// earlier tiles, stages the tile in LDS in digit order, and writes it out in
+// runs.  Digit passes in which every key has the same digit are skipped.
+//
+// After each sort, head flags of the new and old groups are turned into
+// group starts with a three-phase scan (tile partials, one-workgroup scan of
+// the partials, per-tile apply), which also compacts the still-tied suffixes.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fastcoder.h"
+#include "fc_device.h"
+#include "fc_host.h"
+
+namespace {
+
+constexpr int kSortThreads = 256;
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kSortThreads * kSortItems;  // 4096 keys per tile
+constexpr int kRadix = 256;
+constexpr int kMaxDigits = 8;
+constexpr int kSegThreads = 256;
+constexpr int kSegItems = 16;
+constexpr int kSegTile = kSegThreads * kSegItems;
+constexpr int kScanThreads = 1024;
+constexpr int kMaxPasses = 1024;  // ticket counters per build
+constexpr int kMaxRounds = 40;
+constexpr int kHistBlocks = 1024;
+constexpr uint32_t kSpinLimit = 1u << 22;
+
+constexpr uint64_t kFlagAgg = 1ull << 46;
+constexpr uint64_t kFlagInc = 2ull << 46;
+constexpr uint64_t kFlagMask = 3ull << 46;
+constexpr uint64_t kCountMask = (1ull << 46) - 1;
+
+__device__ __forceinline__ uint64_t pack_status(uint32_t epoch, uint64_t flag, uint64_t count) {
+  return ((uint64_t)epoch << 48) | flag | count;
+}
+
+// ---------------------------------------------------------------- keys ----
+
+__global__ void __launch_bounds__(256) k_init_keys(const uint16_t* __restrict__ tok, uint32_t n,
+                                                     uint64_t* __restrict__ keys, uint32_t* __restrict__ vals) {
+  uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  uint64_t a = (uint64_t)tok[i] + 1;
+  uint64_t b = (i + 1 < n) ? (uint64_t)tok[i + 1] + 1 : 0;
+  uint64_t c = (i + 2 < n) ? (uint64_t)tok[i + 2] + 1 : 0;
+  keys[i] = (a << 34) | (b << 17) | c;
+  vals[i] = i;
+}
+
+__global__ void __launch_bounds__(256) k_pair_keys(const uint32_t* __restrict__ vals, uint32_t U,
+                                                     const uint32_t* __restrict__ rank, uint32_t n, uint64_t h,
+                                                     uint32_t sb, uint64_t* __restrict__ keys) {
+  uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= U) return;
+  uint32_t i = vals[r];
+  uint64_t hi = rank[i];
+  uint64_t lo = ((uint64_t)i + h < n) ? (uint64_t)rank[i + h] + 1 : 0;
+  keys[r] = (hi << sb) | lo;
+}
+
+__global__ void __launch_bounds__(256) k_scatter_sa(const uint32_t* __restrict__ rank, uint32_t n,
+                                                      uint32_t* __restrict__ sa) {
+  uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) {
+    const uint32_t r = rank[i];
+    if (r < n) sa[r] = i;
+  }
+}
+
+// ------------------------------------------------------------ histogram ---
+
+__global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys, uint32_t U, int digits,
+                                                uint32_t* __restrict__ hist) {
+  __shared__ uint32_t s[kMaxDigits][kRadix];
+  for (int i = threadIdx.x; i < kMaxDigits * kRadix; i += blockDim.x) (&s[0][0])[i] = 0;
+  __syncthreads();
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < U; i += gridDim.x * blockDim.x) {
+    uint64_t k = keys[i];
+    for (int d = 0; d < digits; ++d) atomicAdd(&s[d][(k >> (8 * d)) & 0xFF], 1u);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < digits * kRadix; i += blockDim.x) {
+    uint32_t v = (&s[0][0])[i];
+    if (v) atomicAdd(&hist[i], v);
+  }
+}
+
+// One workgroup of 256 threads: digit offsets (exclusive scan per digit) and
+// the "trivial" flag of each digit (all keys share it).
+__global__ void __launch_bounds__(256) k_hist_scan(const uint32_t* __restrict__ hist, uint32_t U, int digits,
+                                                     uint32_t* __restrict__ offsets, uint32_t* __restrict__ trivial) {
+  __shared__ uint32_t scratch[8];
+  for (int d = 0; d < digits; ++d) {
+    uint32_t v = hist[d * kRadix + threadIdx.x];
+    uint32_t total;
+    uint32_t ex = fc::block_excl_sum<uint32_t>(v, scratch, &total);
+    offsets[d * kRadix + threadIdx.x] = ex;
+    uint32_t any_full = fc::block_sum<uint32_t>(v == U ? 1u : 0u, scratch);
+    if (threadIdx.x == 0) trivial[d] = any_full ? 1u : 0u;
+  }
+}
+
+// ------------------------------------------------------------- onesweep ---
+
+__global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __restrict__ kin,
+                                                           const uint32_t* __restrict__ vin,
+                                                           uint64_t* __restrict__ kout, uint32_t* __restrict__ vout,
+                                                           uint32_t U, uint32_t shift,
+                                                           const uint32_t* __restrict__ digit_base,
+                                                           uint64_t* status, uint32_t* ticket, uint32_t epoch,
+                                                           uint32_t* err) {
+  __shared__ uint32_t s_tile;
+  __shared__ uint32_t s_wcnt[kSortThreads / fc::kWave][kRadix];
+  __shared__ uint32_t s_dstart[kRadix];
+  __shared__ uint32_t s_gbase[kRadix];
+  __shared__ uint32_t s_scan[kSortThreads / fc::kWave + 1];
+  __shared__ uint64_t s_keys[kSortTile];
+  __shared__ uint32_t s_vals[kSortTile];
+
+  const int tid = threadIdx.x;
+  const int w = tid / fc::kWave;
+  const int lane = fc::lane_id();
+  for (int i = tid; i < (kSortThreads / fc::kWave) * kRadix; i += kSortThreads) (&s_wcnt[0][0])[i] = 0;
+  if (tid == 0) s_tile = atomicAdd(ticket, 1u);
+  __syncthreads();
+  const uint32_t tile = s_tile;
+  const uint64_t base = (uint64_t)tile * kSortTile;
+  const uint32_t nvalid = (uint32_t)((U - base) < (uint64_t)kSortTile ? (U - base) : (uint64_t)kSortTile);
+
+  uint64_t k[kSortItems];
+  uint32_t v[kSortItems];
+  uint32_t rk[kSortItems];
+#pragma unroll
+  for (int j = 0; j < kSortItems; ++j) {
+    const uint32_t idx = (uint32_t)(w * kSortItems * fc::kWave + j * fc::kWave + lane);
+    const bool valid = idx < nvalid;
+    k[j] = valid ? kin[base + idx] : ~0ull;
+    v[j] = valid ? vin[base + idx] : 0u;
+  }
+  const uint64_t lt = fc::lanemask_lt();
+#pragma unroll
+  for (int j = 0; j < kSortItems; ++j) {
+    const uint32_t idx = (uint32_t)(w * kSortItems * fc::kWave + j * fc::kWave + lane);
+    const bool valid = idx < nvalid;
+    const uint32_t d = (uint32_t)(k[j] >> shift) & 0xFF;
+    uint64_t peers = fc::ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t ones = fc::ballot(valid && bit);
+      peers &= bit ? ones : ~ones;
+    }
+    const uint32_t below = (uint32_t)__popcll(peers & lt);
+    const uint32_t old = s_wcnt[w][d];
+    if (valid && below == 0) s_wcnt[w][d] = old + (uint32_t)__popcll(peers);
+    rk[j] = old + below;
+  }
+  __syncthreads();
+
+  // Per digit: offsets of each wave's elements, tile count, tile-local start.
+  const uint32_t t = (uint32_t)tid;  // this thread's digit
+  uint32_t total = 0;
+#pragma unroll
+  for (int ww = 0; ww < kSortThreads / fc::kWave; ++ww) {
+    uint32_t c = s_wcnt[ww][t];
+    s_wcnt[ww][t] = total;
+    total += c;
+  }
+  uint32_t tile_sum;
+  s_dstart[t] = fc::block_excl_sum<uint32_t>(total, s_scan, &tile_sum);
+
+  // Decoupled look-back for this digit's global offset.
+  uint64_t* mine = status + (uint64_t)tile * kRadix + t;
+  uint64_t excl = 0;
+  if (tile > 0) {
+    __hip_atomic_store(mine, pack_status(epoch, kFlagAgg, total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int64_t p = (int64_t)tile - 1;
+    uint32_t spins = 0;
+    while (p >= 0) {
+      const uint64_t s = __hip_atomic_load(status + (uint64_t)p * kRadix + t, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t fl = s & kFlagMask;
+      if ((uint32_t)(s >> 48) != epoch || fl == 0) {
+        if (++spins > kSpinLimit) {
+          atomicOr(err, 1u);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        continue;
+      }
+      excl += s & kCountMask;
+      if (fl == kFlagInc) break;
+      --p;
+    }
+  }
+  __hip_atomic_store(mine, pack_status(epoch, kFlagInc, excl + total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  s_gbase[t] = digit_base[t] + (uint32_t)excl;
+  __syncthreads();
+
+  // Stage in LDS in digit order.
+#pragma unroll
+  for (int j = 0; j < kSortItems; ++j) {
+    const uint32_t idx = (uint32_t)(w * kSortItems * fc::kWave + j * fc::kWave + lane);
+    if (idx < nvalid) {
+      const uint32_t d = (uint32_t)(k[j] >> shift) & 0xFF;
+      const uint32_t pos = s_dstart[d] + s_wcnt[w][d] + rk[j];
+      s_keys[pos] = k[j];
+      s_vals[pos] = v[j];
+    }
+  }
+  __syncthreads();
+  for (uint32_t i = (uint32_t)tid; i < nvalid; i += kSortThreads) {
+    const uint64_t key = s_keys[i];
+    const uint32_t d = (uint32_t)(key >> shift) & 0xFF;
+    const uint32_t dst = s_gbase[d] + (i - s_dstart[d]);
+    if (dst < U) {  // always true unless a look-back gave up (then err is set)
+      kout[dst] = key;
+      vout[dst] = s_vals[i];
+    }
+  }
+}
+
+// ------------------------------------------------------ group bookkeeping --
+
+struct SegFlags {
+  bool new_head, old_head, keep;
+};
+
+__device__ __forceinline__ SegFlags seg_flags(const uint64_t* __restrict__ keys, uint32_t U, uint32_t r,
+                                              uint32_t sb, bool round0) {
+  const uint64_t kr = keys[r];
+  SegFlags f;
+  if (r == 0) {
+    f.new_head = true;
+    f.old_head = true;
+  } else {
+    const uint64_t kp = keys[r - 1];
+    f.new_head = kr != kp;
+    f.old_head = round0 ? false : ((kr >> sb) != (kp >> sb));
+  }
+  const bool last_of_group = (r + 1 == U) || (keys[r + 1] != kr);
+  f.keep = !(f.new_head && last_of_group);
+  return f;
+}
+
+// Per tile: last new-group head, last old-group head, number kept.
+__global__ void __launch_bounds__(kSegThreads) k_seg_partials(const uint64_t* __restrict__ keys, uint32_t U,
+                                                                uint32_t sb, int round0, uint32_t* __restrict__ part_h,
+                                                                uint32_t* __restrict__ part_g,
+                                                                uint32_t* __restrict__ part_k) {
+  __shared__ uint32_t scratch[kSegThreads / fc::kWave + 1];
+  const uint32_t r0 = blockIdx.x * kSegTile + threadIdx.x * kSegItems;
+  uint32_t mh = 0, mg = 0, kc = 0;
+  for (int j = 0; j < kSegItems; ++j) {
+    const uint32_t r = r0 + j;
+    if (r >= U) break;
+    const SegFlags f = seg_flags(keys, U, r, sb, round0 != 0);
+    if (f.new_head) mh = r;
+    if (f.old_head) mg = r;
+    kc += f.keep ? 1u : 0u;
+  }
+  mh = fc::block_max<uint32_t>(mh, scratch);
+  mg = fc::block_max<uint32_t>(mg, scratch);
+  kc = fc::block_sum<uint32_t>(kc, scratch);
+  if (threadIdx.x == 0) {
+    part_h[blockIdx.x] = mh;
+    part_g[blockIdx.x] = mg;
+    part_k[blockIdx.x] = kc;
+  }
+}
+
+// One workgroup: exclusive max / max / sum scans of the tile partials, in
+// place; *u_next receives the number kept.
+__global__ void __launch_bounds__(kScanThreads) k_seg_scan(uint32_t* __restrict__ part_h,
+                                                             uint32_t* __restrict__ part_g,
+                                                             uint32_t* __restrict__ part_k, uint32_t ntiles,
+                                                             uint32_t* __restrict__ u_next) {
+  __shared__ uint32_t scratch[kScanThreads / fc::kWave + 1];
+  const uint32_t per = fc::div_up(ntiles, kScanThreads);
+  const uint32_t lo = threadIdx.x * per;
+  const uint32_t hi = lo + per < ntiles ? lo + per : ntiles;
+  uint32_t mh = 0, mg = 0, kc = 0;
+  for (uint32_t i = lo; i < hi; ++i) {
+    mh = part_h[i] > mh ? part_h[i] : mh;
+    mg = part_g[i] > mg ? part_g[i] : mg;
+    kc += part_k[i];
+  }
+  uint32_t total;
+  uint32_t eh = fc::block_excl_max<uint32_t>(mh, 0u, scratch);
+  uint32_t eg = fc::block_excl_max<uint32_t>(mg, 0u, scratch);
+  uint32_t ek = fc::block_excl_sum<uint32_t>(kc, scratch, &total);
+  for (uint32_t i = lo; i < hi; ++i) {
+    const uint32_t h = part_h[i], g = part_g[i], kk = part_k[i];
+    part_h[i] = eh;
+    part_g[i] = eg;
+    part_k[i] = ek;
+    eh = h > eh ? h : eh;
+    eg = g > eg ? g : eg;
+    ek += kk;
+  }
+  if (threadIdx.x == 0) *u_next = total;
+}
+
+// Per element: new rank = old group start + (new head index - old head index)
+// in the sorted list; tied suffixes are compacted into vals_next.
+__global__ void __launch_bounds__(kSegThreads) k_seg_apply(const uint64_t* __restrict__ keys,
+                                                             const uint32_t* __restrict__ vals, uint32_t U,
+                                                             uint32_t sb, int round0,
+                                                             const uint32_t* __restrict__ pre_h,
+                                                             const uint32_t* __restrict__ pre_g,
+                                                             const uint32_t* __restrict__ pre_k,
+                                                             uint32_t* __restrict__ rank,
+                                                             uint32_t* __restrict__ vals_next) {
+  __shared__ uint32_t scratch[kSegThreads / fc::kWave + 1];
+  const uint32_t r0 = blockIdx.x * kSegTile + threadIdx.x * kSegItems;
+  uint32_t mh = 0, mg = 0, kc = 0;
+  for (int j = 0; j < kSegItems; ++j) {
+    const uint32_t r = r0 + j;
+    if (r >= U) break;
+    const SegFlags f = seg_flags(keys, U, r, sb, round0 != 0);
+    if (f.new_head) mh = r;
+    if (f.old_head) mg = r;
+    kc += f.keep ? 1u : 0u;
+  }
+  uint32_t eh = fc::block_excl_max<uint32_t>(mh, 0u, scratch);
+  uint32_t eg = fc::block_excl_max<uint32_t>(mg, 0u, scratch);
+  uint32_t ek = fc::block_excl_sum<uint32_t>(kc, scratch, nullptr);
+  const uint32_t th = pre_h[blockIdx.x], tg = pre_g[blockIdx.x];
+  uint32_t hh = eh > th ? eh : th;
+  uint32_t gg = eg > tg ? eg : tg;
+  uint32_t out = pre_k[blockIdx.x] + ek;
+  for (int j = 0; j < kSegItems; ++j) {
+    const uint32_t r = r0 + j;
+    if (r >= U) break;
+    const SegFlags f = seg_flags(keys, U, r, sb, round0 != 0);
+    if (f.new_head) hh = r;
+    if (f.old_head) gg = r;
+    const uint32_t start = round0 ? 0u : (uint32_t)(keys[r] >> sb);
+    const uint32_t i = vals[r];
+    rank[i] = start + (hh - gg);
+    if (f.keep) vals_next[out++] = i;
+  }
+}
+
+// ------------------------------------------------------- first-token table --
+
+__global__ void __launch_bounds__(256) k_bucket(const uint16_t* __restrict__ tok, const uint32_t* __restrict__ sa,
+                                                  uint32_t n, uint32_t* __restrict__ bucket) {
+  const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= FC_BUCKETS) return;
+  // first SA index whose suffix starts with a token >= t
+  uint32_t lo = 0, hi = n;
+  while (lo < hi) {
+    const uint32_t mid = lo + (hi - lo) / 2;
+    if ((uint32_t)tok[sa[mid]] < t) lo = mid + 1; else hi = mid;
+  }
+  bucket[t] = lo;
+}
+
+struct BuildWs {
+  uint32_t* rank;
+  uint64_t* keys[2];
+  uint32_t* vals[2];
+  uint64_t* status;
+  uint32_t *part_h, *part_g, *part_k;
+  uint32_t* hist;
+  uint32_t* offsets;
+  uint32_t* tickets;
+  uint32_t* misc;  // [0] error flag, [1] next U, [2..9] trivial digit flags
+};
+
+size_t carve_build(void* p, uint64_t n, BuildWs* w) {
+  fc::Carver c(p);
+  const uint64_t tiles = (n + kSortTile - 1) / kSortTile;
+  const uint64_t seg_tiles = (n + kSegTile - 1) / kSegTile;
+  BuildWs tmp;
+  tmp.rank = c.take<uint32_t>(n);
+  tmp.keys[0] = c.take<uint64_t>(n);
+  tmp.keys[1] = c.take<uint64_t>(n);
+  tmp.vals[0] = c.take<uint32_t>(n);
+  tmp.vals[1] = c.take<uint32_t>(n);
+  tmp.status = c.take<uint64_t>(tiles * kRadix);
+  tmp.part_h = c.take<uint32_t>(seg_tiles);
+  tmp.part_g = c.take<uint32_t>(seg_tiles);
+  tmp.part_k = c.take<uint32_t>(seg_tiles);
+  tmp.hist = c.take<uint32_t>(kMaxDigits * kRadix);
+  tmp.offsets = c.take<uint32_t>(kMaxDigits * kRadix);
+  tmp.tickets = c.take<uint32_t>(kMaxPasses);
+  tmp.misc = c.take<uint32_t>(16);
+  if (w) *w = tmp;
+  return c.used + 256;
+}
+
+int bit_length(uint64_t x) {
+  int b = 0;
+  while (x) {
+    ++b;
+    x >>= 1;
+  }
+  return b;
+}
+
+struct SortState {
+  uint32_t epoch = 0;
+  uint32_t ticket = 0;
+};
+
+// LSD radix sort of (keys, vals) over the low key_bits bits.  Returns the
+// buffer index (0 or 1) that holds the result.
+fc_status radix_sort(BuildWs& w, int src, uint32_t U, int key_bits, SortState& st, hipStream_t stream,
+                     int* result) {
+  const int digits = (key_bits + 7) / 8;
+  FC_CHECK_HIP(hipMemsetAsync(w.hist, 0, sizeof(uint32_t) * kMaxDigits * kRadix, stream));
+  const uint32_t hist_blocks = fc::div_up(U, 256) < (uint32_t)kHistBlocks ? fc::div_up(U, 256) : kHistBlocks;
+  hipLaunchKernelGGL(k_hist, dim3(hist_blocks), dim3(256), 0, stream, w.keys[src], U, digits, w.hist);
+  FC_CHECK_LAUNCH();
+  hipLaunchKernelGGL(k_hist_scan, dim3(1), dim3(256), 0, stream, w.hist, U, digits, w.offsets, w.misc + 2);
+  FC_CHECK_LAUNCH();
+  uint32_t trivial[kMaxDigits] = {0};
+  FC_CHECK_HIP(hipMemcpyAsync(trivial, w.misc + 2, sizeof(uint32_t) * digits, hipMemcpyDeviceToHost, stream));
+  FC_CHECK_HIP(hipStreamSynchronize(stream));
+  int cur = src;
+  const uint32_t tiles = fc::div_up(U, kSortTile);
+  for (int d = 0; d < digits; ++d) {
+    if (trivial[d]) continue;
+    if (st.ticket >= (uint32_t)kMaxPasses) return FC_ERR_UNSUPPORTED;
+    ++st.epoch;
+    hipLaunchKernelGGL(k_onesweep, dim3(tiles), dim3(kSortThreads), 0, stream, w.keys[cur], w.vals[cur],
+                       w.keys[cur ^ 1], w.vals[cur ^ 1], U, (uint32_t)(8 * d), w.offsets + d * kRadix, w.status,
+                       w.tickets + st.ticket, st.epoch, w.misc);
+    FC_CHECK_LAUNCH();
+    ++st.ticket;
+    cur ^= 1;
+  }
+  *result = cur;
+  return FC_OK;
+}
+
+}  // namespace
+
+extern "C" size_t fc_datastore_build_workspace_bytes(uint64_t n) { return carve_build(nullptr, n, nullptr); }
+
+extern "C" fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint32_t* sa_out, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+  if (n >= 0xFFFFFFFFull) return FC_ERR_INVALID;
+  if (n == 0) return FC_OK;
+  if (!tokens || !sa_out) return FC_ERR_INVALID;
+  if (!ws || ws_bytes < fc_datastore_build_workspace_bytes(n)) return FC_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  BuildWs w;
+  carve_build(ws, n, &w);
+  const uint32_t N = (uint32_t)n;
+  const uint64_t tiles = (n + kSortTile - 1) / kSortTile;
+  FC_CHECK_HIP(hipMemsetAsync(w.status, 0, sizeof(uint64_t) * tiles * kRadix, stream));
+  FC_CHECK_HIP(hipMemsetAsync(w.tickets, 0, sizeof(uint32_t) * kMaxPasses, stream));
+  FC_CHECK_HIP(hipMemsetAsync(w.misc, 0, sizeof(uint32_t) * 16, stream));
+
+  const uint32_t sb = (uint32_t)bit_length(n);  // every rank + 1 <= n fits in sb bits
+  SortState st;
+  hipLaunchKernelGGL(k_init_keys, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, tokens, N, w.keys[0], w.vals[0]);
+  FC_CHECK_LAUNCH();
+  uint32_t U = N;
+  int vin = 0;  // buffer holding the suffixes to sort
+  uint64_t h = 3;
+  for (int round = 0;; ++round) {
+    if (round >= kMaxRounds) return FC_ERR_DEVICE;
+    if (round > 0) {
+      hipLaunchKernelGGL(k_pair_keys, dim3(fc::div_up(U, 256)), dim3(256), 0, stream, w.vals[vin], U, w.rank, N,
+                         h, sb, w.keys[vin]);
+      FC_CHECK_LAUNCH();
+      h *= 2;
+    }
+    int res = vin;
+    fc_status s = radix_sort(w, vin, U, round == 0 ? 51 : (int)(2 * sb), st, stream, &res);
+    if (s != FC_OK) return s;
+    const uint32_t seg_tiles = fc::div_up(U, kSegTile);
+    hipLaunchKernelGGL(k_seg_partials, dim3(seg_tiles), dim3(kSegThreads), 0, stream, w.keys[res], U, sb,
+                       round == 0 ? 1 : 0, w.part_h, w.part_g, w.part_k);
+    FC_CHECK_LAUNCH();
+    hipLaunchKernelGGL(k_seg_scan, dim3(1), dim3(kScanThreads), 0, stream, w.part_h, w.part_g, w.part_k, seg_tiles,
+                       w.misc + 1);
+    FC_CHECK_LAUNCH();
+    hipLaunchKernelGGL(k_seg_apply, dim3(seg_tiles), dim3(kSegThreads), 0, stream, w.keys[res], w.vals[res], U, sb,
+                       round == 0 ? 1 : 0, w.part_h, w.part_g, w.part_k, w.rank, w.vals[res ^ 1]);
+    FC_CHECK_LAUNCH();
+    uint32_t host_misc[2] = {0, 0};
+    FC_CHECK_HIP(hipMemcpyAsync(host_misc, w.misc, sizeof(uint32_t) * 2, hipMemcpyDeviceToHost, stream));
+    FC_CHECK_HIP(hipStreamSynchronize(stream));
+    if (host_misc[0]) return FC_ERR_DEVICE;
+    U = host_misc[1];
+    vin = res ^ 1;
+    if (U == 0) break;
+  }
+  hipLaunchKernelGGL(k_scatter_sa, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, w.rank, N, sa_out);
+  FC_CHECK_LAUNCH();
+  return FC_OK;
+}
+
+extern "C" fc_status fc_store_prepare(const uint16_t* tokens, const uint32_t* sa, uint64_t n, uint32_t* bucket_out,
+                                      hipStream_t stream) {
+  if (n >= 0xFFFFFFFFull || !bucket_out) return FC_ERR_INVALID;
+  if (n > 0 && (!tokens || !sa)) return FC_ERR_INVALID;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(k_bucket, dim3(fc::div_up(FC_BUCKETS, 256)), dim3(256), 0, stream, tokens, sa, (uint32_t)n,
+                     bucket_out);
+  FC_CHECK_LAUNCH();
+  return FC_OK;
+}

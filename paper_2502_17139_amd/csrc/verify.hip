@@ -1,0 +1,68 @@
+// Greedy acceptance of a draft tree on gfx950 (fc_verify_accept).
+//
+// The target model checks every draft in one forward pass; the accepted
+// draft is the longest root path whose tokens all agree with the model, and
+// everything after the first disagreement is discarded (Section IV-D).  One
+// thread per query walks from the root: at row u it looks for the child whose
+// token equals the model's token after u, and stops when there is none; the
+// model's own token at the stopping row is accepted as well.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fastcoder.h"
+#include "fc_device.h"
+#include "fc_host.h"
+
+namespace {
+
+__global__ void __launch_bounds__(256) k_verify(const int32_t* __restrict__ num_nodes,
+                                                  const int32_t* __restrict__ node_tok,
+                                                  const int32_t* __restrict__ parent,
+                                                  const int32_t* __restrict__ target, int B, int c, int m,
+                                                  int32_t* __restrict__ accept_len, int32_t* __restrict__ accept_tok,
+                                                  int32_t* __restrict__ last_node) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int R = c + 1;
+  const int64_t row = (int64_t)b * R;
+  int n = num_nodes[b];
+  n = n < 1 ? 1 : (n > R ? R : n);
+  int32_t* out = accept_tok + (int64_t)b * (m + 1);
+  int u = 0, len = 0;
+  for (;;) {
+    const int32_t want = target[row + u];
+    if (want < 0 || len >= m + 1) break;
+    int next = -1;
+    for (int v = u + 1; v < n; ++v)
+      if (parent[row + v] == u && node_tok[row + v] == want) {
+        next = v;
+        break;
+      }
+    if (next < 0) break;
+    out[len++] = node_tok[row + next];
+    u = next;
+  }
+  const int32_t bonus = target[row + u];
+  if (bonus >= 0 && len < m + 1) out[len++] = bonus;
+  for (int x = len; x < m + 1; ++x) out[x] = -1;
+  accept_len[b] = len;
+  last_node[b] = u;
+}
+
+}  // namespace
+
+extern "C" fc_status fc_verify_accept(const int32_t* num_nodes, const int32_t* node_tok, const int32_t* parent,
+                                      const int32_t* pos_ids, const int32_t* target, int32_t B, int32_t c, int32_t m,
+                                      int32_t* accept_len, int32_t* accept_tok, int32_t* last_node,
+                                      hipStream_t stream) {
+  (void)pos_ids;
+  if (B < 0 || c < 0 || c + 1 > FC_MAX_TREE_ROWS || m < 0 || m > 255) return FC_ERR_INVALID;
+  if (B == 0) return FC_OK;
+  if (!num_nodes || !node_tok || !parent || !target || !accept_len || !accept_tok || !last_node)
+    return FC_ERR_INVALID;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(k_verify, dim3(fc::div_up(B, 256)), dim3(256), 0, stream, num_nodes, node_tok, parent, target,
+                     B, c, m, accept_len, accept_tok, last_node);
+  FC_CHECK_LAUNCH();
+  return FC_OK;
+}

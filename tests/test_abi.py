@@ -1,0 +1,123 @@
+"""The C ABI library loads, exports every entry point include/fastcoder.h
+declares, and rejects bad arguments on the host before touching a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2502_17139_amd as fc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(fc.LIB_PATH):
+        from paper_2502_17139_amd import build
+        build.build()
+    return fc.lib()
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "fastcoder.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fc_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared()
+    assert set(names) == set(fc.EXPORTS)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    assert L.fc_abi_version() == 1
+    for code, name in fc.STATUS.items():
+        assert L.fc_status_string(code).decode().startswith(name)
+    assert L.fc_status_string(99).decode() == "FC_ERR_UNKNOWN"
+
+
+def test_workspace_sizes(L):
+    assert fc.fc_datastore_build_workspace_bytes(1000) < fc.fc_datastore_build_workspace_bytes(2000)
+    # about 28.6 bytes per token for the 1B-token store
+    n = 1_001_999_999
+    assert 28 * n < fc.fc_datastore_build_workspace_bytes(n) < 29 * n
+    assert L.fc_retrieve_workspace_bytes(1024, 2, fc.FcRetrieveParams(16, 2, 5000, 10)) == 0
+
+
+def _retrieve_args(S=1, B=1, L_=4, p=(16, 2, 5000, 10), ws_bytes=0):
+    views = (fc.FcStore * 4)(*[fc.FcStore(1, 1, 1, 10) for _ in range(4)])
+    one = ctypes.c_void_p(8)
+    return [views, S, one, B, L_, fc.FcRetrieveParams(*p)] + [one] * 8 + [None, ws_bytes, None]
+
+
+@pytest.mark.parametrize("change,code", [
+    (dict(S=0), 1), (dict(S=5), 1), (dict(B=-1), 1), (dict(L_=0), 1),
+    (dict(p=(17, 2, 10, 10)), 1), (dict(p=(4, 5, 10, 10)), 1), (dict(p=(4, 0, 10, 10)), 1),
+    (dict(p=(4, 2, 0, 10)), 1), (dict(p=(4, 2, 10, 0)), 1), (dict(p=(4, 2, 10, 256)), 1),
+])
+def test_retrieve_rejects(L, change, code):
+    assert L.fc_retrieve(*_retrieve_args(**change)) == code
+
+
+def test_retrieve_rejects_null_outputs_and_big_store(L):
+    args = _retrieve_args()
+    args[6] = None  # match_n
+    assert L.fc_retrieve(*args) == 1
+    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 1 << 32))
+    args = _retrieve_args()
+    args[0] = views
+    assert L.fc_retrieve(*args) == 1
+    views = (fc.FcStore * 1)(fc.FcStore(1, None, 1, 10))
+    args[0] = views
+    assert L.fc_retrieve(*args) == 1
+
+
+def _tree_args(B=1, L_=2, S=2, k=10, m=4, c=8, alpha=(1, 1, 0, 0)):
+    one = ctypes.c_void_p(8)
+    tp = fc.FcTreeParams(c, (ctypes.c_uint32 * 4)(*alpha))
+    return [one, one, one, one, B, L_, S, k, m, tp] + [one] * 6 + [None]
+
+
+@pytest.mark.parametrize("change,code", [
+    (dict(B=-1), 1), (dict(L_=0), 1), (dict(S=0), 1), (dict(S=5), 1), (dict(k=0), 1), (dict(m=0), 1),
+    (dict(m=256), 1), (dict(c=0), 1), (dict(c=255 + 1), 1), (dict(k=65536), 4),
+    (dict(k=60000, alpha=(1 << 20, 1, 0, 0)), 4), (dict(k=5000, m=255), 4),
+])
+def test_build_tree_rejects(L, change, code):
+    if change == dict(k=5000, m=255):
+        # about 2.6 MB of LDS per query: larger than any workgroup can hold; this
+        # check reads the device's limit, so it needs a GPU
+        pytest.skip("LDS limit check queries the device")
+    assert L.fc_build_tree(*_tree_args(**change)) == code
+
+
+def test_verify_and_build_reject(L):
+    one = ctypes.c_void_p(8)
+    assert L.fc_verify_accept(one, one, one, one, one, 1, -1, 4, one, one, one, None) == 1
+    assert L.fc_verify_accept(one, one, one, one, one, 1, 255 + 1, 4, one, one, one, None) == 1
+    assert L.fc_verify_accept(None, one, one, one, one, 1, 8, 4, one, one, one, None) == 1
+    assert L.fc_datastore_build(one, 1 << 32, one, one, 1 << 40, None) == 1
+    assert L.fc_datastore_build(one, 100, one, None, 0, None) == 2
+    assert L.fc_datastore_build(one, 100, one, one, 16, None) == 2
+    assert L.fc_datastore_build(None, 100, one, one, 1 << 30, None) == 1
+    assert L.fc_store_prepare(one, one, 100, None, None) == 1
+    # empty requests succeed without launching anything
+    assert L.fc_datastore_build(None, 0, None, None, 0, None) == 0
+    assert L.fc_retrieve(*_retrieve_args(B=0)) == 0
+    assert L.fc_verify_accept(None, None, None, None, None, 0, 8, 4, None, None, None, None) == 0
+
+
+def test_binding_has_no_cpu_path(monkeypatch, tmp_path):
+    """Without the built library every call raises instead of computing."""
+    monkeypatch.setattr(fc, "LIB_PATH", str(tmp_path / "missing.so"))
+    fc.lib.cache_clear()
+    try:
+        with pytest.raises(RuntimeError, match="no CPU fallback"):
+            fc.lib()
+    finally:
+        monkeypatch.undo()
+        fc.lib.cache_clear()
