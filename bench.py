@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Draft-stage hot-path benchmark on one MI355X.
+
+One step = one batch of queries through the whole draft-stage path on the
+GPU: fc_retrieve (longest-suffix match in both stores + continuation gather),
+fc_build_tree (weighted trie, top-c, mask, position ids) and fc_verify_accept
+(longest accepted path against the true next tokens).  Stores, suffix arrays,
+bucket tables, query contexts and target tokens are resident in HBM before
+the timed region; the suffix arrays are built once, untimed, with
+fc_datastore_build (the paper builds its datastores offline).
+
+Default workload: the 1,024-query batch over a 10M-token project store and a
+1B-token general store (k = 5000, m = 10, c = 64, n = 16..2).  Prints ONE JSON
+line.  Timing uses HIP events on the stream the kernels run on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
+WORKLOADS = {"headline": 3, "two-store": 2, "single": 1}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(taken, cont_len, match_n, ctx_nhi, store_sizes, k, m, c, n_min):
+    """Bytes the method must move per launch, from the batch's own outputs.
+
+    search (per query, per store): for every suffix length tried, n_hi down
+    to the match (or n_min): one bucket read (8 B) and two binary searches of
+    ceil(log2(bucket size + 1)) probes, each probe a 4-byte suffix-array entry
+    plus up to 2n bytes of text; bucket sizes are taken as n_s / 32256.
+    Plus the context row (32 B) and the four per-store outputs (16 B).
+    gather (per kept slot): 4-byte suffix-array entry + 2*len text bytes
+    read; 4 + 1 + 1 + 2*m bytes written.
+    tree (per query): taken (4*S) + cont_len (1 per kept slot) + cont_tok
+    (2*m per kept slot) + root token (2) read; rows 4*4*(c+1) + num_nodes 4
+    + mask 4*(c+1)^2 written.
+    verify (per query): num_nodes 4 + node_tok/parent/target 3*4*(c+1) read;
+    4 + 4*(m+1) + 4 written.
+    """
+    B, S = taken.shape
+    R = c + 1
+    search = 0.0
+    for b in range(B):
+        search += 32
+        for s in range(S):
+            lo_n = match_n[b, s] if match_n[b, s] > 0 else n_min
+            probes = int(np.ceil(np.log2(store_sizes[s] / 32256.0 + 1)))
+            for n in range(int(ctx_nhi[b]), int(lo_n) - 1, -1):
+                search += 8 + 2 * probes * (4 + 2 * n)
+            search += 16
+    used = taken.sum(axis=1)
+    kept = int(used.sum())
+    lens = sum(int(cont_len[b, :used[b]].astype(np.int64).sum()) for b in range(B))
+    gather = kept * (4 + 4 + 1 + 1 + 2 * m) + 2 * lens
+    tree = B * (4 * S + 2) + kept * (1 + 2 * m) + B * (4 + 16 * R + 4 * R * R)
+    verify = B * (4 + 12 * R + 4 + 4 * (m + 1) + 4)
+    return dict(search=search, gather=float(gather), tree=float(tree), verify=float(verify))
+
+
+def n_hi_of(ctx: np.ndarray, n_max: int) -> np.ndarray:
+    out = np.zeros(ctx.shape[0], np.int64)
+    for b in range(ctx.shape[0]):
+        t = 0
+        while t < ctx.shape[1] and ctx[b, ctx.shape[1] - 1 - t] != 0:
+            t += 1
+        out[b] = min(n_max, ctx.shape[1], t)
+    return out
+
+
+def cpu_baseline(texts, ctx, nxt, p, alpha, c, budget_s):
+    """The oracle (test infrastructure) on a bounded sample of the batch."""
+    import oracle
+    B = ctx.shape[0]
+    n = 4
+    done, spent = 0, 0.0
+    while done < B:
+        q = min(n, B - done)
+        rows = slice(done, done + q)
+        t0 = time.perf_counter()
+        r = oracle.retrieve(texts, ctx[rows], n_max=p["n_max"], n_min=p["n_min"], k=p["k"], m=p["m"])
+        t = oracle.build_tree(r["taken"], r["cont_len"], r["cont_tok"], ctx[rows], c=c, alpha=alpha)
+        tgt = targets_for(t["pos_ids"], t["num_nodes"], nxt[rows])
+        oracle.verify_accept(t, tgt, m=p["m"])
+        spent += time.perf_counter() - t0
+        done += q
+        if spent >= budget_s:
+            break
+        n = min(2 * n, 64)
+    return done, spent
+
+
+def targets_for(pos_ids, num_nodes, nxt):
+    """target[b][i] = the true token after the path to row i (-1 if none)."""
+    B, R = pos_ids.shape
+    out = np.full((B, R), -1, np.int32)
+    for b in range(B):
+        n = int(num_nodes[b])
+        for i in range(max(n, 0)):
+            j = int(pos_ids[b, i])
+            if j < nxt.shape[1]:
+                out[b, i] = int(nxt[b, j])
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="headline")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    import paper_2502_17139_amd as fc
+    import synth
+
+    cfg = WORKLOADS[args.workload]
+    p = dict(synth.PARAMS)
+    c, alpha = p["c"], tuple(p["alpha"])
+    roles = synth.store_roles(cfg)
+    alpha = alpha[:len(roles)]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    t0 = time.perf_counter()
+    texts = [synth.store(cfg, r) for r in roles]
+    ctx_np, nxt_np = synth.queries(cfg, next_tokens=p["m"] + 1)
+    log(f"generated stores {[len(t) for t in texts]} and {ctx_np.shape[0]} queries in {time.perf_counter() - t0:.1f}s")
+
+    stream = torch.cuda.current_stream()
+    stores, build_s = [], []
+    for t in texts:
+        tok = torch.from_numpy(t).to(dev)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        st = fc.Store(tok)
+        torch.cuda.synchronize()
+        build_s.append(time.perf_counter() - t1)
+        stores.append(st)
+    log(f"suffix arrays built in {[round(x, 3) for x in build_s]} s")
+
+    B = ctx_np.shape[0]
+    k, m = p["k"], p["m"]
+    ctx = torch.from_numpy(ctx_np).to(dev)
+    rout = fc.retrieve_outputs(B, len(stores), k, m, dev)
+    tout = fc.tree_outputs(B, c, dev)
+    aout = fc.accept_outputs(B, m, dev)
+
+    def retrieve():
+        fc.fc_retrieve(stores, ctx, n_max=p["n_max"], n_min=p["n_min"], k=k, m=m, out=rout)
+
+    def tree():
+        fc.fc_build_tree(rout["taken"], rout["cont_len"], rout["cont_tok"], ctx, c=c, alpha=alpha, out=tout)
+
+    # first pass: its tree fixes the target tokens (the target model's outputs)
+    retrieve()
+    tree()
+    torch.cuda.synchronize()
+    tgt_np = targets_for(tout["pos_ids"].cpu().numpy(), tout["num_nodes"].cpu().numpy(), nxt_np)
+    target = torch.from_numpy(tgt_np).to(dev)
+
+    def verify():
+        fc.fc_verify_accept(tout, target, m=m, out=aout)
+
+    for _ in range(args.warmup):
+        retrieve()
+        tree()
+        verify()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for i in range(K):
+        ev[i][0].record(stream)
+        retrieve()
+        ev[i][1].record(stream)
+        tree()
+        ev[i][2].record(stream)
+        verify()
+        ev[i][3].record(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(end)
+    phase_ms = {name: float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)]))
+                for j, name in enumerate(("fc_retrieve", "fc_build_tree", "fc_verify_accept"))}
+    ms_step = total_ms / K
+
+    # outputs of the batch, for the byte model and the acceptance statistic
+    taken = rout["taken"].cpu().numpy()
+    cont_len = rout["cont_len"].cpu().numpy()
+    match_n = rout["match_n"].cpu().numpy()
+    acc = aout["accept_len"].cpu().numpy()
+    nb = algorithmic_bytes(taken, cont_len, match_n, n_hi_of(ctx_np, p["n_max"]), [len(t) for t in texts],
+                           k, m, c, p["n_min"])
+    dominant = max(phase_ms, key=phase_ms.get)
+    dom_bytes = {"fc_retrieve": nb["search"] + nb["gather"], "fc_build_tree": nb["tree"],
+                 "fc_verify_accept": nb["verify"]}[dominant]
+    achieved = dom_bytes / (phase_ms[dominant] * 1e-3) / 1e9
+    total_bytes = sum(nb.values())
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        done, spent = cpu_baseline(texts, ctx_np, nxt_np, p, alpha, c, args.cpu_budget)
+        cpu = {"value": done / spent, "unit": "retrievals/s", "cores": oracle.max_threads(), "kind": "oracle",
+               "sample": f"first {done} of the {B} queries (retrieve + tree + accept), {spent:.1f} s"}
+
+    line = {
+        "metric": "draft retrievals/sec (match+gather+trie) at 1B-token datastore; HBM GB/s vs peak",
+        "value": B * K / (total_ms * 1e-3),
+        "unit": "retrievals/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u16/u32 (integer)",
+        "data": "synthetic (seeded template/Zipf/noise token stores; no dataset)",
+        "config": {"workload": synth.CONFIGS[cfg]["name"], "stores_tokens": [len(t) for t in texts],
+                   "batch": B, "n_max": p["n_max"], "n_min": p["n_min"], "k": k, "m": m, "c": c,
+                   "alpha": list(alpha), "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+        "cpu_baseline": cpu,
+        "phases_ms": phase_ms,
+        "algorithmic_bytes_per_step": nb,
+        "step_GBps_algorithmic": total_bytes / (ms_step * 1e-3) / 1e9,
+        "accept_len_mean": float(acc.mean()),
+        "slots_kept_mean": float(taken.sum(axis=1).mean()),
+        "sa_build_s": build_s,
+        "wall_s_timed": wall,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

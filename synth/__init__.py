@@ -147,18 +147,19 @@ def drop_cache() -> None:
     _STORE_CACHE.clear()
 
 
-def _window_random(text_files: int, qseed: int, q: int, src_text: np.ndarray) -> np.ndarray:
+def _window_random(text_files: int, qseed: int, q: int, src_text: np.ndarray, extra: int) -> np.ndarray:
     f, off = uniform(qseed, ROLE_QUERY, q, 2, 0, 0x7FFFFFFF)
     f = int(f) % text_files
     off = int(off) % (FILE_LEN - CTX_LEN + 1)
     start = f * (FILE_LEN + 1) + off
-    return src_text[start:start + CTX_LEN].copy()
+    w = src_text[start:start + CTX_LEN + extra]
+    return np.concatenate([w, np.zeros(CTX_LEN + extra - len(w), np.uint16)])
 
 
-def _window_fresh(p: Pool, qseed: int, q: int) -> np.ndarray:
-    text = p.files(qseed + 1_000_003, 1_000_000_000 + q, 1, FILE_LEN, sep=False)
+def _window_fresh(p: Pool, qseed: int, q: int, extra: int) -> np.ndarray:
+    text = p.files(qseed + 1_000_003, 1_000_000_000 + q, 1, FILE_LEN + extra, sep=False)
     off = int(uniform(qseed, ROLE_FRESH, q, 1, 0, FILE_LEN - CTX_LEN)[0])
-    return text[off:off + CTX_LEN].copy()
+    return text[off:off + CTX_LEN + extra].copy()
 
 
 def query_plan(cfg: int) -> list:
@@ -190,20 +191,28 @@ def query_plan(cfg: int) -> list:
     return plan
 
 
-def queries(cfg: int, count: int | None = None) -> np.ndarray:
-    """Query contexts, uint16 [B][16] (the first `count` of the batch if given)."""
+def queries(cfg: int, count: int | None = None, next_tokens: int = 0):
+    """Query contexts, uint16 [B][16] (the first `count` of the batch if given).
+
+    With next_tokens > 0 also returns the tokens that truly follow each
+    window, uint16 [B][next_tokens] (the store's own text for a random
+    window, 0-padded at the end of the store; the fresh file's continuation
+    for a fresh one): the ground truth a target model would reproduce.
+    """
     c = CONFIGS[cfg]
     plan = query_plan(cfg)
     if count is not None:
         plan = plan[:count]
     stores = {r: (seed, nt, s, nf) for r, seed, nt, s, nf in c["stores"]}
-    out = np.empty((len(plan), CTX_LEN), dtype=np.uint16)
+    out = np.empty((len(plan), CTX_LEN + next_tokens), dtype=np.uint16)
     for q, (kind, role) in enumerate(plan):
         seed, nt, s, nf = stores[role]
         if kind == "random":
-            out[q] = _window_random(nf, c["qseed"], q, store(cfg, role))
+            out[q] = _window_random(nf, c["qseed"], q, store(cfg, role), next_tokens)
         else:
-            out[q] = _window_fresh(pool(seed, nt, s), c["qseed"], q)
+            out[q] = _window_fresh(pool(seed, nt, s), c["qseed"], q, next_tokens)
+    if next_tokens:
+        return np.ascontiguousarray(out[:, :CTX_LEN]), np.ascontiguousarray(out[:, CTX_LEN:])
     return out
 
 
