@@ -27,16 +27,18 @@ import paper_2502_17139_amd as fc  # noqa: E402
 P = dict(synth.PARAMS)
 
 
-def _targets(tree: dict, seed: int) -> np.ndarray:
+def _targets(tree: dict, seed: int, row_ids=None) -> np.ndarray:
     """Seeded targets that follow the tree most of the time; computed from
-    one side's own tree output."""
+    one side's own tree output.  row_ids name each row's query in the full
+    batch, so a sampled subset draws the same targets as the full batch."""
     B, R = tree["node_tok"].shape
     out = np.full((B, R), -1, np.int32)
     for b in range(B):
         n = int(tree["num_nodes"][b])
         par = tree["parent"][b]
+        qid = b if row_ids is None else int(row_ids[b])
         for i in range(max(n, 0)):
-            rng = np.random.default_rng([seed, b, i])
+            rng = np.random.default_rng([seed, qid, i])
             kids = [v for v in range(1, n) if par[v] == i]
             if kids and rng.random() < 0.75:
                 out[b, i] = int(tree["node_tok"][b, kids[int(rng.integers(len(kids)))]])
@@ -165,9 +167,11 @@ def test_headline_workload_sampled():
     tg_ = {f: g[f] for f in ("node_tok", "parent", "num_nodes")}
     targets = _targets(tg_, 3)
     ga = fc.fc_verify_accept(g["_tree_dev"], dev(targets), m=P["m"])
-    oa = oracle.verify_accept(o, _targets({f: o[f] for f in ("node_tok", "parent", "num_nodes")}, 3), m=P["m"])
+    oa = oracle.verify_accept(o, _targets({f: o[f] for f in ("node_tok", "parent", "num_nodes")}, 3, rows),
+                              m=P["m"])
     for i, b in enumerate(rows):
-        assert host(ga["accept_len"])[b] == oa["accept_len"][i]
+        for f in ("accept_len", "accept_tok", "last_node"):
+            assert (host(ga[f])[b] == oa[f][i]).all(), (f, b)
     synth.drop_cache()
 
 
