@@ -14,10 +14,10 @@
 // second token on.  The wave then keeps, per store, the longest n whose range
 // is non-empty and fills the k slots in store priority order.
 //
-// k_gather: one thread per (query, slot).  A slot maps to its store and
-// range offset (strided floor(i*cnt/b) when the range exceeds the store's
-// budget b), reads the suffix-array entry and copies up to m continuation
-// tokens, cut before a 0 and at the end of the store.
+// k_gather: one workgroup per query over its kept slots only.  A slot maps to
+// its store and range offset (strided floor(i*cnt/b) when the range exceeds
+// the store's budget b), reads the suffix-array entry and copies up to m
+// continuation tokens, cut before a 0 and at the end of the store.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -38,16 +38,29 @@ struct StoreArgs {
   uint32_t n[FC_MAX_SOURCES];
 };
 
-// Suffix j against pattern q[0..n) from token `from` on: -1 below (a suffix
-// that ends first is below), 0 starts with q, +1 above.
+// Suffix j against pattern q[0..n), knowing token 0 already matches: -1 below
+// (a suffix that ends first is below), 0 starts with q, +1 above.  Tokens are
+// fetched in two batches of independent loads (1..8, then 9..15 only when the
+// first eight all match), so a probe costs one memory round trip in the
+// common case instead of a chain of dependent loads.
 __device__ __forceinline__ int cmp_suffix(const uint16_t* __restrict__ T, uint32_t N, uint32_t j,
-                                          const uint16_t* q, int n, int from) {
-  for (int x = from; x < n; ++x) {
-    const uint64_t p = (uint64_t)j + (uint64_t)x;
-    if (p >= N) return -1;
-    const uint16_t a = T[p];
-    const uint16_t b = q[x];
-    if (a != b) return a < b ? -1 : 1;
+                                          const uint16_t* q, int n) {
+  constexpr int kBatch = 8;
+  uint16_t t[kBatch];
+  for (int x0 = 1; x0 < n; x0 += kBatch) {
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const uint64_t p = (uint64_t)j + (uint64_t)(x0 + u);
+      t[u] = (x0 + u < n && p < N) ? T[p] : (uint16_t)0;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int x = x0 + u;
+      if (x >= n) return 0;
+      if ((uint64_t)j + (uint64_t)x >= N) return -1;
+      const uint16_t b = q[x];
+      if (t[u] != b) return t[u] < b ? -1 : 1;
+    }
   }
   return 0;
 }
@@ -103,10 +116,29 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
         lo = st.bucket[s][q[0]];
         hi = st.bucket[s][q[0] + 1];
       }
-      while (lo < hi) {
-        const uint32_t mid = lo + ((hi - lo) >> 1);
-        const int c = cmp_suffix(T, N, SA[mid], q, n, 1);
-        if (upper ? (c <= 0) : (c < 0)) lo = mid + 1; else hi = mid;
+      // Binary search; the suffix-array entries of both possible next
+      // midpoints are fetched together with the current probe's text, so
+      // each level costs one dependent round trip.
+      if (lo < hi) {
+        uint32_t mid = lo + ((hi - lo) >> 1);
+        uint32_t j = SA[mid];
+        for (;;) {
+          const uint32_t lmid = lo + ((mid - lo) >> 1);
+          const uint32_t rmid = (mid + 1) + ((hi - mid - 1) >> 1);
+          const uint32_t jl = lo < mid ? SA[lmid] : 0u;
+          const uint32_t jr = mid + 1 < hi ? SA[rmid] : 0u;
+          const int c = cmp_suffix(T, N, j, q, n);
+          if (upper ? (c <= 0) : (c < 0)) {
+            lo = mid + 1;
+            mid = rmid;
+            j = jr;
+          } else {
+            hi = mid;
+            mid = lmid;
+            j = jl;
+          }
+          if (lo >= hi) break;
+        }
       }
       if (upper) s_hi[w][s][ni] = lo; else s_lo[w][s][ni] = lo;
     }
@@ -140,6 +172,11 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
   }
 }
 
+// One workgroup per query walks only the query's kept slots.  Each thread
+// handles two slots per iteration; for each it reads the suffix-array entry,
+// then issues all m token loads at once (they do not depend on each other;
+// the cut at the first 0 is applied afterwards in registers).
+template <int MAXM>
 __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, int k, int m,
                                                            const int32_t* __restrict__ match_n,
                                                            const uint32_t* __restrict__ range_lo,
@@ -149,46 +186,118 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
                                                            uint8_t* __restrict__ cont_src,
                                                            uint8_t* __restrict__ cont_len,
                                                            uint16_t* __restrict__ cont_tok) {
-  const uint32_t chunks = fc::div_up(k, kGatherThreads);
-  const int b = (int)(blockIdx.x / chunks);
-  const int i = (int)(blockIdx.x - (uint32_t)b * chunks) * kGatherThreads + (int)threadIdx.x;
-  if (i >= k) return;
-  const int64_t slot = (int64_t)b * k + i;
-  uint16_t* out = cont_tok + slot * m;
-  int64_t before = 0;
-  int src = -1;
-  for (int s = 0; s < S; ++s) {
-    const int64_t t = taken[(int64_t)b * S + s];
-    if (i < before + t) {
-      src = s;
-      break;
+  __shared__ int64_t s_first[FC_MAX_SOURCES + 1];
+  __shared__ uint64_t s_cnt[FC_MAX_SOURCES], s_budget[FC_MAX_SOURCES], s_lo[FC_MAX_SOURCES];
+  __shared__ uint32_t s_n[FC_MAX_SOURCES];
+  const int b = blockIdx.x;
+  if (threadIdx.x == 0) {
+    int64_t before = 0;
+    for (int s = 0; s < S; ++s) {
+      const int64_t o = (int64_t)b * S + s;
+      const int64_t t = taken[o];
+      s_first[s] = before;
+      s_cnt[s] = range_cnt[o];
+      s_budget[s] = (uint64_t)((int64_t)k - before);
+      s_lo[s] = range_lo[o];
+      s_n[s] = (uint32_t)match_n[o];
+      before += t;
     }
-    before += t;
+    s_first[S] = before;
   }
-  if (src < 0) return;  // slots past the query's last kept occurrence are not written
-  const int64_t o = (int64_t)b * S + src;
-  const uint64_t cnt = range_cnt[o];
-  const uint64_t budget = (uint64_t)((int64_t)k - before);
-  const uint64_t local = (uint64_t)(i - before);
-  const uint64_t off = cnt > budget ? (local * cnt) / budget : local;
-  const uint32_t j = st.sa[src][(uint64_t)range_lo[o] + off];
-  const uint64_t start = (uint64_t)j + (uint64_t)match_n[o];
-  const uint16_t* T = st.tok[src];
-  const uint64_t N = st.n[src];
-  int len = 0;
-  bool open = true;
-  for (int x = 0; x < m; ++x) {
-    uint16_t v = 0;
-    if (open) {
-      const uint64_t p = start + (uint64_t)x;
-      if (p < N) v = T[p];
-      if (v == 0) open = false; else ++len;
+  __syncthreads();
+  const int total = (int)s_first[S];
+  for (int i0 = (int)threadIdx.x; i0 < total; i0 += 2 * kGatherThreads) {
+    uint32_t j[2];
+    int src[2];
+    bool ok[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int i = i0 + h * kGatherThreads;
+      ok[h] = i < total;
+      int s = 0;
+      while (s + 1 < S && i >= s_first[s + 1]) ++s;
+      src[h] = s;
+      const uint64_t local = ok[h] ? (uint64_t)(i - s_first[s]) : 0;
+      const uint64_t off = (ok[h] && s_cnt[s] > s_budget[s]) ? (local * s_cnt[s]) / s_budget[s] : local;
+      j[h] = ok[h] ? st.sa[s][s_lo[s] + off] : 0u;
     }
-    out[x] = open ? v : 0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (!ok[h]) continue;
+      const int i = i0 + h * kGatherThreads;
+      const int s = src[h];
+      const uint64_t start = (uint64_t)j[h] + s_n[s];
+      const uint16_t* T = st.tok[s];
+      const uint64_t N = st.n[s];
+      uint16_t v[MAXM];
+#pragma unroll
+      for (int x = 0; x < MAXM; ++x) v[x] = (x < m && start + x < N) ? T[start + x] : (uint16_t)0;
+      int len = m;
+#pragma unroll
+      for (int x = MAXM - 1; x >= 0; --x)
+        if (x < m && v[x] == 0) len = x;
+      const int64_t slot = (int64_t)b * k + i;
+      uint16_t* out = cont_tok + slot * m;
+#pragma unroll
+      for (int x = 0; x < MAXM; ++x)
+        if (x < m) out[x] = x < len ? v[x] : (uint16_t)0;
+      cont_pos[slot] = (uint32_t)start;
+      cont_src[slot] = (uint8_t)s;
+      cont_len[slot] = (uint8_t)len;
+    }
   }
-  cont_pos[slot] = (uint32_t)start;
-  cont_src[slot] = (uint8_t)src;
-  cont_len[slot] = (uint8_t)len;
+}
+
+// Any m up to 255: the token copy loops over m with a cut flag.
+__global__ void __launch_bounds__(kGatherThreads) k_gather_any(StoreArgs st, int S, int k, int m,
+                                                               const int32_t* __restrict__ match_n,
+                                                               const uint32_t* __restrict__ range_lo,
+                                                               const uint32_t* __restrict__ range_cnt,
+                                                               const int32_t* __restrict__ taken,
+                                                               uint32_t* __restrict__ cont_pos,
+                                                               uint8_t* __restrict__ cont_src,
+                                                               uint8_t* __restrict__ cont_len,
+                                                               uint16_t* __restrict__ cont_tok) {
+  const int b = blockIdx.x;
+  int64_t total = 0;
+  for (int s = 0; s < S; ++s) total += taken[(int64_t)b * S + s];
+  for (int i = (int)threadIdx.x; i < total; i += kGatherThreads) {
+    int64_t before = 0;
+    int src = 0;
+    for (int s = 0; s < S; ++s) {
+      const int64_t t = taken[(int64_t)b * S + s];
+      if (i < before + t) {
+        src = s;
+        break;
+      }
+      before += t;
+    }
+    const int64_t o = (int64_t)b * S + src;
+    const uint64_t cnt = range_cnt[o];
+    const uint64_t budget = (uint64_t)((int64_t)k - before);
+    const uint64_t local = (uint64_t)(i - before);
+    const uint64_t off = cnt > budget ? (local * cnt) / budget : local;
+    const uint32_t jj = st.sa[src][(uint64_t)range_lo[o] + off];
+    const uint64_t start = (uint64_t)jj + (uint64_t)match_n[o];
+    const uint16_t* T = st.tok[src];
+    const uint64_t N = st.n[src];
+    const int64_t slot = (int64_t)b * k + i;
+    uint16_t* out = cont_tok + slot * m;
+    int len = 0;
+    bool open = true;
+    for (int x = 0; x < m; ++x) {
+      uint16_t v = 0;
+      if (open) {
+        const uint64_t p = start + (uint64_t)x;
+        if (p < N) v = T[p];
+        if (v == 0) open = false; else ++len;
+      }
+      out[x] = open ? v : 0;
+    }
+    cont_pos[slot] = (uint32_t)start;
+    cont_src[slot] = (uint8_t)src;
+    cont_len[slot] = (uint8_t)len;
+  }
 }
 
 }  // namespace
@@ -222,16 +331,19 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
   if (B == 0) return FC_OK;
   if (!ctx || !match_n || !range_lo || !range_cnt || !taken || !cont_pos || !cont_src || !cont_len || !cont_tok)
     return FC_ERR_INVALID;
-  const uint64_t gather_blocks = (uint64_t)B * fc::div_up(p.k, kGatherThreads);
-  if (gather_blocks > 0x7FFFFFFFull) return FC_ERR_UNSUPPORTED;
   if (ws_bytes < fc_retrieve_workspace_bytes(B, S, p)) return FC_ERR_WORKSPACE;
   (void)ws;
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_search, dim3(fc::div_up(B, kQueriesPerBlock)), dim3(kSearchThreads), 0, stream, st, S, ctx,
                      B, L, p.n_max, p.n_min, p.k, match_n, range_lo, range_cnt, taken);
   FC_CHECK_LAUNCH();
-  hipLaunchKernelGGL(k_gather, dim3((uint32_t)gather_blocks), dim3(kGatherThreads), 0, stream, st, S,
-                     p.k, p.m, match_n, range_lo, range_cnt, taken, cont_pos, cont_src, cont_len, cont_tok);
+  if (p.m <= 16) {
+    hipLaunchKernelGGL(k_gather<16>, dim3(B), dim3(kGatherThreads), 0, stream, st, S, p.k, p.m, match_n, range_lo,
+                       range_cnt, taken, cont_pos, cont_src, cont_len, cont_tok);
+  } else {
+    hipLaunchKernelGGL(k_gather_any, dim3(B), dim3(kGatherThreads), 0, stream, st, S, p.k, p.m, match_n, range_lo,
+                       range_cnt, taken, cont_pos, cont_src, cont_len, cont_tok);
+  }
   FC_CHECK_LAUNCH();
   return FC_OK;
 }

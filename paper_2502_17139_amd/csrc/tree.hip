@@ -38,6 +38,7 @@ namespace {
 
 constexpr int kTreeThreads = 512;
 constexpr int kMaskWords = FC_MAX_TREE_ROWS / 32;
+constexpr int kSmallClass = 1024;  // kept slots handled by the small-LDS launch
 
 struct Alpha {
   uint32_t a[FC_MAX_SOURCES];
@@ -91,7 +92,7 @@ __device__ __forceinline__ int src_of(const int* seg, int S, int i) {
   return s;
 }
 
-__global__ void __launch_bounds__(kTreeThreads) k_tree(const int32_t* __restrict__ taken,
+__global__ void __launch_bounds__(kTreeThreads) k_tree_any(const int32_t* __restrict__ taken,
                                                        const uint8_t* __restrict__ cont_len,
                                                        const uint16_t* __restrict__ cont_tok,
                                                        const uint16_t* __restrict__ ctx, int L, int S, int k, int m,
@@ -380,6 +381,412 @@ __global__ void __launch_bounds__(kTreeThreads) k_tree(const int32_t* __restrict
   if (tid == 0) num_nodes[b] = err ? -1 : num;
 }
 
+
+// ---------------------------------------------------------------------------
+// Fast path (m <= 16).  One workgroup of NT threads per query; queries are
+// split into two launches by their kept-slot count T, each with an LDS
+// layout sized for its class, so light queries run several workgroups per CU.
+// Every thread owns a contiguous chunk of merged positions; per-chunk
+// summaries are combined with wave shuffles and one LDS exchange, which keeps
+// the number of barriers per query small.
+// ---------------------------------------------------------------------------
+
+template <int NT>
+struct Scan2 {
+  // Exclusive prefix sums of (x, y) over the block plus their totals.
+  __device__ static void run(uint32_t x, uint32_t y, uint32_t* sx, uint32_t* sy, uint32_t* ex, uint32_t* ey,
+                             uint32_t* tx, uint32_t* ty) {
+    constexpr int NW = NT / fc::kWave;
+    const int w = (int)threadIdx.x / fc::kWave;
+    const uint32_t ix = fc::wave_incl_sum(x), iy = fc::wave_incl_sum(y);
+    if (fc::lane_id() == fc::kWave - 1) {
+      sx[w] = ix;
+      sy[w] = iy;
+    }
+    __syncthreads();
+    uint32_t px = 0, py = 0, ax = 0, ay = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const uint32_t vx = sx[i], vy = sy[i];
+      if (i < w) {
+        px += vx;
+        py += vy;
+      }
+      ax += vx;
+      ay += vy;
+    }
+    *ex = px + ix - x;
+    *ey = py + iy - y;
+    *tx = ax;
+    *ty = ay;
+    __syncthreads();
+  }
+};
+
+template <int NT, int MAXM>
+__global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ taken,
+                                                  const uint8_t* __restrict__ cont_len,
+                                                  const uint16_t* __restrict__ cont_tok,
+                                                  const uint16_t* __restrict__ ctx, int L, int S, int k, int m, int c,
+                                                  Alpha alpha, int t_lo, int t_hi, int words,
+                                                  int32_t* __restrict__ num_nodes, int32_t* __restrict__ node_tok,
+                                                  int32_t* __restrict__ parent, uint32_t* __restrict__ weight,
+                                                  int32_t* __restrict__ pos_ids, int32_t* __restrict__ mask) {
+  constexpr int NW = NT / fc::kWave;
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ int s_seg[FC_MAX_SOURCES + 1];
+  __shared__ int s_err;
+  __shared__ uint32_t s_x[NW + 1], s_y[NW + 1], s_z[NW + 1];
+  __shared__ uint16_t s_wmin[NW][MAXM + 1];
+  __shared__ uint32_t s_hist[256];
+  __shared__ uint32_t s_sel_w[FC_MAX_TREE_ROWS];
+  __shared__ uint16_t s_sel_p[FC_MAX_TREE_ROWS];
+  __shared__ uint8_t s_sel_d[FC_MAX_TREE_ROWS];
+  __shared__ int16_t s_par[FC_MAX_TREE_ROWS];
+  __shared__ uint32_t s_pick[2];
+
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = fc::lane_id();
+  const int w = tid / fc::kWave;
+  const int R = c + 1;
+  const int64_t row0 = (int64_t)b * k;
+
+  // Class check: this launch owns queries with t_lo < T <= t_hi.  Malformed
+  // rows (a negative count or more than k slots) count as T = 0, so the
+  // small-class launch (t_lo = -1) reports them.
+  int T_raw = 0, bad = 0;
+  for (int s = 0; s < S; ++s) {
+    const int t = taken[(int64_t)b * S + s];
+    bad |= t < 0;
+    T_raw += t > 0 ? t : 0;
+  }
+  bad |= T_raw > k;
+  if (bad) T_raw = 0;
+  if (T_raw <= t_lo || T_raw > t_hi) return;  // uniform over the workgroup
+
+  const TreeLayout lay = tree_layout(t_hi, m);
+  uint16_t* str = (uint16_t*)(smem + lay.str);
+  uint16_t* E = str;
+  uint32_t* anc = (uint32_t*)(smem + lay.str);
+  uint32_t* A = (uint32_t*)(smem + lay.A);
+  uint16_t* perm = (uint16_t*)(smem + lay.perm);
+  uint8_t* len = smem + lay.len;
+  uint8_t* lcp = smem + lay.lcp;
+  uint8_t* mlen = smem + lay.mlen;
+
+  if (tid == 0) {
+    int acc = 0;
+    for (int s = 0; s < S; ++s) {
+      s_seg[s] = acc;
+      const int t = taken[(int64_t)b * S + s];
+      acc += bad ? 0 : t;
+    }
+    s_seg[S] = acc;
+    s_err = bad;
+    s_pick[0] = 0;
+    s_pick[1] = 0;
+  }
+  __syncthreads();
+  const int T = T_raw;
+
+  // 1. load lengths and tokens (32-bit words when the rows are aligned)
+  for (int i = tid; i < T; i += NT) {
+    const uint8_t l = cont_len[row0 + i];
+    len[i] = l;
+    if (l > m) s_err = 1;
+  }
+  if (words) {
+    const uint32_t* src = (const uint32_t*)(cont_tok + row0 * m);
+    uint32_t* dst = (uint32_t*)str;
+    const int nw = (T * m + 1) >> 1;
+    for (int e = tid; e < nw; e += NT) dst[e] = src[e];
+  } else {
+    for (int e = tid; e < T * m; e += NT) str[e] = cont_tok[row0 * m + e];
+  }
+  __syncthreads();
+
+  // 2. precondition (each store's slots sorted) and merged order
+  for (int i = tid; i < T; i += NT) {
+    const int s = src_of(s_seg, S, i);
+    if (i > s_seg[s] && len[i - 1] <= m && len[i] <= m &&
+        str_cmp(str + (i - 1) * m, len[i - 1], str + i * m, len[i]) > 0)
+      s_err = 1;
+  }
+  const int per = (T + NT - 1) / NT;
+  const int p0 = tid * per < T ? tid * per : T;
+  const int p1 = p0 + per < T ? p0 + per : T;
+  const int na = s_seg[1] - s_seg[0];
+  if (S == 1) {
+    for (int p = p0; p < p1; ++p) perm[p] = (uint16_t)p;
+  } else if (S == 2 || s_seg[2] == T) {
+    // merge path over two sorted lists (store 0 first on equal strings)
+    const int nb = T - na;
+    int lo = p0 - nb > 0 ? p0 - nb : 0;
+    int hi = p0 < na ? p0 : na;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      const int jb = na + (p0 - mid - 1);
+      if (str_cmp(str + mid * m, len[mid], str + jb * m, len[jb]) <= 0) lo = mid + 1; else hi = mid;
+    }
+    int ia = lo, ib = p0 - lo;
+    for (int p = p0; p < p1; ++p) {
+      bool take_a;
+      if (ia >= na) take_a = false;
+      else if (ib >= nb) take_a = true;
+      else take_a = str_cmp(str + ia * m, len[ia], str + (na + ib) * m, len[na + ib]) <= 0;
+      perm[p] = (uint16_t)(take_a ? ia++ : na + ib++);
+    }
+  } else {
+    for (int i = tid; i < T; i += NT) {
+      const int s = src_of(s_seg, S, i);
+      const uint16_t* x = str + i * m;
+      const int lx = len[i];
+      int mp = i - s_seg[s];
+      for (int s2 = 0; s2 < S; ++s2) {
+        if (s2 == s) continue;
+        int lo2 = s_seg[s2], hi2 = s_seg[s2 + 1];
+        const int base = lo2;
+        while (lo2 < hi2) {
+          const int mid = (lo2 + hi2) >> 1;
+          const int cc = str_cmp(str + mid * m, len[mid], x, lx);
+          if (s2 < s ? (cc <= 0) : (cc < 0)) lo2 = mid + 1; else hi2 = mid;
+        }
+        mp += lo2 - base;
+      }
+      perm[mp] = (uint16_t)i;
+    }
+  }
+  __syncthreads();
+  const bool err = s_err != 0;
+
+  int nsel = 0;
+  uint32_t root_w = 0;
+  if (!err) {
+    // 3. merged lengths, adjacent LCPs, alpha sums, node counts, and each
+    //    chunk's first head per depth (first q with lcp[q] < d)
+    uint32_t asum = 0, rw = 0, nodes = 0;
+    uint16_t f[MAXM + 1];
+#pragma unroll
+    for (int d = 0; d <= MAXM; ++d) f[d] = (uint16_t)T;
+    for (int p = p1 - 1; p >= p0; --p) {
+      const int i = perm[p];
+      const int li = len[i];
+      int l = 0;
+      if (p > 0) {
+        const int i2 = perm[p - 1];
+        l = str_lcp(str + i2 * m, len[i2], str + i * m, li);
+      }
+      mlen[p] = (uint8_t)li;
+      lcp[p] = (uint8_t)l;
+      const uint32_t a = alpha.a[src_of(s_seg, S, i)];
+      asum += a;
+      if (li > 0) rw += a;
+      nodes += (uint32_t)(li - l);
+#pragma unroll
+      for (int d = 1; d <= MAXM; ++d)
+        if (l < d) f[d] = (uint16_t)p;
+    }
+    uint32_t a_ex, dummy, a_tot, n_tot;
+    Scan2<NT>::run(asum, nodes, s_x, s_y, &a_ex, &dummy, &a_tot, &n_tot);
+    root_w = fc::block_sum<uint32_t>(rw, s_z);
+    // suffix minimum of f over later chunks (wave shuffles, then waves)
+    uint16_t nh[MAXM + 1];
+#pragma unroll
+    for (int d = 1; d <= MAXM; ++d) {
+      uint32_t v = f[d];
+      uint32_t inc = v;
+#pragma unroll
+      for (int off = 1; off < fc::kWave; off <<= 1) {
+        const uint32_t o = __shfl_down(inc, off, fc::kWave);
+        if (lane + off < fc::kWave && o < inc) inc = o;
+      }
+      uint32_t ex = __shfl_down(inc, 1, fc::kWave);
+      if (lane == fc::kWave - 1) ex = (uint32_t)T;
+      if (lane == 0) s_wmin[w][d] = (uint16_t)inc;
+      nh[d] = (uint16_t)ex;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int d = 1; d <= MAXM; ++d) {
+      uint32_t v = nh[d];
+      for (int ww = w + 1; ww < NW; ++ww) v = s_wmin[ww][d] < v ? s_wmin[ww][d] : v;
+      nh[d] = (uint16_t)v;
+    }
+    // alpha prefix sums
+    {
+      uint32_t run = a_ex;
+      for (int p = p0; p < p1; ++p) {
+        A[p] = run;
+        run += alpha.a[src_of(s_seg, S, perm[p])];
+      }
+      if (tid == 0) A[T] = a_tot;
+    }
+    __syncthreads();  // str is dead from here on: E reuses it
+
+    // 4. run ends, right to left through the chunk
+    for (int q = p1 - 1; q >= p0; --q) {
+      const int l = lcp[q], ml = mlen[q];
+#pragma unroll
+      for (int d = 1; d <= MAXM; ++d) {
+        if (d > l && d <= ml) E[q * m + d - 1] = nh[d];
+        if (d > l) nh[d] = (uint16_t)q;
+      }
+    }
+    __syncthreads();
+
+    // 5. radix select: the need-th largest weight W*, and how many nodes of
+    //    weight W* to take (in (p, d) order)
+    const uint32_t need = n_tot < (uint32_t)c ? n_tot : (uint32_t)c;
+    uint32_t wmax = 0;
+    for (int p = p0; p < p1; ++p) {
+      const int d = lcp[p] + 1;  // the shallowest own node is the heaviest
+      if (d <= mlen[p]) {
+        const uint32_t W = A[E[p * m + d - 1]] - A[p];
+        wmax = W > wmax ? W : wmax;
+      }
+    }
+    wmax = fc::block_max<uint32_t>(wmax, s_z);
+    uint32_t prefix = 0, remaining = need;
+    int bits = 0;
+    for (uint32_t x = wmax; x; x >>= 1) ++bits;
+    if (need > 0 && bits > 0) {
+      for (int shift = ((bits - 1) / 8) * 8; shift >= 0; shift -= 8) {
+        for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
+        __syncthreads();
+        const uint64_t hi_mask = shift + 8 >= 32 ? 0ull : (uint64_t)prefix >> (shift + 8);
+        for (int p = p0; p < p1; ++p) {
+          const uint32_t ap = A[p];
+          for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
+            const uint32_t W = A[E[p * m + d - 1]] - ap;
+            if ((shift + 8 >= 32 ? 0ull : (uint64_t)(W >> (shift + 8))) == hi_mask)
+              atomicAdd(&s_hist[(W >> shift) & 0xFF], 1u);
+          }
+        }
+        __syncthreads();
+        if (tid < fc::kWave) {
+          // wave 0 finds the bin holding the remaining-th largest
+          uint32_t cnt[4];
+          uint32_t lsum = 0;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            cnt[u] = s_hist[255 - (lane * 4 + u)];
+            lsum += cnt[u];
+          }
+          const uint32_t incl = fc::wave_incl_sum(lsum);
+          const uint32_t before = incl - lsum;
+          if (before < remaining && incl >= remaining) {
+            uint32_t acc = before;
+            int bin = 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              if (acc + cnt[u] >= remaining) {
+                bin = 255 - (lane * 4 + u);
+                break;
+              }
+              acc += cnt[u];
+            }
+            s_pick[0] = prefix | ((uint32_t)bin << shift);
+            s_pick[1] = remaining - acc;
+          }
+        }
+        __syncthreads();
+        prefix = s_pick[0];
+        remaining = s_pick[1];
+      }
+    }
+    const uint32_t wstar = prefix;
+    const uint32_t take_eq = remaining;
+
+    // 6. kept nodes in (p, d) order = preorder
+    uint32_t gt = 0, eq = 0;
+    if (need > 0) {
+      for (int p = p0; p < p1; ++p) {
+        const uint32_t ap = A[p];
+        for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
+          const uint32_t W = A[E[p * m + d - 1]] - ap;
+          gt += W > wstar;
+          eq += W == wstar;
+        }
+      }
+    }
+    uint32_t gt_ex, eq_ex, gt_tot, eq_tot;
+    Scan2<NT>::run(gt, eq, s_x, s_y, &gt_ex, &eq_ex, &gt_tot, &eq_tot);
+    if (need > 0 && (gt + eq) > 0) {
+      uint32_t o = 1 + gt_ex + (eq_ex < take_eq ? eq_ex : take_eq);
+      uint32_t r = eq_ex;
+      for (int p = p0; p < p1; ++p) {
+        const uint32_t ap = A[p];
+        for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
+          const uint32_t W = A[E[p * m + d - 1]] - ap;
+          bool keep = W > wstar;
+          if (W == wstar) keep = r++ < take_eq;
+          if (keep && o < (uint32_t)FC_MAX_TREE_ROWS) {
+            s_sel_p[o] = (uint16_t)p;
+            s_sel_d[o] = (uint8_t)d;
+            s_sel_w[o] = W;
+            ++o;
+          }
+        }
+      }
+    }
+    const uint32_t total_sel = need > 0 ? gt_tot + (eq_tot < take_eq ? eq_tot : take_eq) : 0;
+    nsel = (int)(total_sel < (uint32_t)c ? total_sel : (uint32_t)c);
+    if (tid == 0) s_sel_d[0] = 0;
+    __syncthreads();
+    for (int r = tid + 1; r <= nsel; r += NT) {
+      const int d = s_sel_d[r];
+      int q = r - 1;
+      while (q > 0 && s_sel_d[q] != d - 1) --q;
+      s_par[r] = (int16_t)q;
+    }
+    if (tid == 0) s_par[0] = -1;
+    __syncthreads();
+  }
+
+  // 7. rows, then the mask from ancestor bitsets (E is dead by now)
+  const int num = err ? 0 : 1 + nsel;
+  for (int r = tid; r < R; r += NT) {
+    const int64_t out = (int64_t)b * R + r;
+    int32_t tk = 0, pr = -1, ps = 0;
+    uint32_t wt = 0;
+    if (r < num) {
+      if (r == 0) {
+        tk = ctx[(int64_t)b * L + L - 1];
+        wt = root_w;
+      } else {
+        const int p = s_sel_p[r];
+        const int d = s_sel_d[r];
+        tk = cont_tok[(row0 + perm[p]) * m + d - 1];
+        pr = s_par[r];
+        wt = s_sel_w[r];
+        ps = d;
+      }
+    }
+    node_tok[out] = tk;
+    parent[out] = pr;
+    weight[out] = wt;
+    pos_ids[out] = ps;
+  }
+  const int words_per_row = (R + 31) >> 5;
+  for (int i = tid; i < R * words_per_row; i += NT) anc[i] = 0;
+  __syncthreads();
+  for (int r = tid; r < num; r += NT) {
+    int j = r;
+    while (j >= 0) {
+      anc[r * words_per_row + (j >> 5)] |= 1u << (j & 31);
+      j = (j == 0) ? -1 : s_par[j];
+    }
+  }
+  __syncthreads();
+  const int64_t mbase = (int64_t)b * R * R;
+  for (int e = tid; e < R * R; e += NT) {
+    const int i = e / R, j = e - (e / R) * R;
+    mask[mbase + e] = (i < num) ? (int32_t)((anc[i * words_per_row + (j >> 5)] >> (j & 31)) & 1u) : 0;
+  }
+  if (tid == 0) num_nodes[b] = err ? -1 : num;
+}
+
 }  // namespace
 
 extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok,
@@ -394,20 +801,44 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
   if (B == 0) return FC_OK;
   if (!taken || !cont_len || !cont_tok || !ctx || !num_nodes || !node_tok || !parent || !weight || !pos_ids || !mask)
     return FC_ERR_INVALID;
-  const TreeLayout lay = tree_layout(k, m);
   int dev = 0, max_lds = 0;
   FC_CHECK_HIP(hipGetDevice(&dev));
   FC_CHECK_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
-  const size_t static_lds = 6 * 1024;
-  if (lay.total + static_lds > (size_t)max_lds) return FC_ERR_UNSUPPORTED;
-  (void)hipGetLastError();
-  if (lay.total > 64 * 1024)
-    (void)hipFuncSetAttribute((const void*)k_tree, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lay.total);
-  (void)hipGetLastError();
+  const size_t static_lds = 7 * 1024;
   Alpha a = {};
   for (int s = 0; s < S; ++s) a.a[s] = t.alpha[s];
-  hipLaunchKernelGGL(k_tree, dim3(B), dim3(kTreeThreads), lay.total, stream, taken, cont_len, cont_tok, ctx, L, S, k,
-                     m, t.c, a, num_nodes, node_tok, parent, weight, pos_ids, mask);
+  const TreeLayout full = tree_layout(k, m);
+  if (full.total + static_lds > (size_t)max_lds) return FC_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  if (m <= 16) {
+    // light queries (T <= 1024) in small-LDS workgroups, the rest in full-LDS ones
+    const int t_small = k < kSmallClass ? k : kSmallClass;
+    const int words = ((((uintptr_t)cont_tok) & 3) == 0 && ((size_t)k * m) % 2 == 0) ? 1 : 0;
+    const TreeLayout small = tree_layout(t_small, m);
+    if (small.total > 64 * 1024)
+      (void)hipFuncSetAttribute((const void*)k_tree_fast<256, 16>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)small.total);
+    hipLaunchKernelGGL((k_tree_fast<256, 16>), dim3(B), dim3(256), small.total, stream, taken, cont_len, cont_tok,
+                       ctx, L, S, k, m, t.c, a, -1, t_small, words, num_nodes, node_tok, parent, weight, pos_ids,
+                       mask);
+    FC_CHECK_LAUNCH();
+    if (k > t_small) {
+      if (full.total > 64 * 1024)
+        (void)hipFuncSetAttribute((const void*)k_tree_fast<512, 16>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)full.total);
+      (void)hipGetLastError();
+      hipLaunchKernelGGL((k_tree_fast<512, 16>), dim3(B), dim3(512), full.total, stream, taken, cont_len, cont_tok,
+                         ctx, L, S, k, m, t.c, a, t_small, k, words, num_nodes, node_tok, parent, weight, pos_ids,
+                         mask);
+      FC_CHECK_LAUNCH();
+    }
+    return FC_OK;
+  }
+  if (full.total > 64 * 1024)
+    (void)hipFuncSetAttribute((const void*)k_tree_any, hipFuncAttributeMaxDynamicSharedMemorySize, (int)full.total);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(k_tree_any, dim3(B), dim3(kTreeThreads), full.total, stream, taken, cont_len, cont_tok, ctx, L,
+                     S, k, m, t.c, a, num_nodes, node_tok, parent, weight, pos_ids, mask);
   FC_CHECK_LAUNCH();
   return FC_OK;
 }

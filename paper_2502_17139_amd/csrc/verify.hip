@@ -2,10 +2,10 @@
 //
 // The target model checks every draft in one forward pass; the accepted
 // draft is the longest root path whose tokens all agree with the model, and
-// everything after the first disagreement is discarded (Section IV-D).  One
-// thread per query walks from the root: at row u it looks for the child whose
-// token equals the model's token after u, and stops when there is none; the
-// model's own token at the stopping row is accepted as well.
+// everything after the first disagreement is discarded (Section IV-D).  From
+// the root, at row u the walk moves to the child whose token equals the
+// model's token after u, and stops when there is none; the model's own token
+// at the stopping row is accepted as well.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -15,38 +15,61 @@
 
 namespace {
 
-__global__ void __launch_bounds__(256) k_verify(const int32_t* __restrict__ num_nodes,
-                                                  const int32_t* __restrict__ node_tok,
-                                                  const int32_t* __restrict__ parent,
-                                                  const int32_t* __restrict__ target, int B, int c, int m,
-                                                  int32_t* __restrict__ accept_len, int32_t* __restrict__ accept_tok,
-                                                  int32_t* __restrict__ last_node) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
+constexpr int kVerifyThreads = 256;
+constexpr int kQueriesPerBlock = kVerifyThreads / fc::kWave;
+
+// One wave per query.  Lane l holds rows l, l+64, l+128, l+192 (parent and
+// token); each step is one ballot over "my row is a child of u carrying the
+// target token", so a path of depth d costs d ballots.
+__global__ void __launch_bounds__(kVerifyThreads) k_verify(const int32_t* __restrict__ num_nodes,
+                                                           const int32_t* __restrict__ node_tok,
+                                                           const int32_t* __restrict__ parent,
+                                                           const int32_t* __restrict__ target, int B, int c, int m,
+                                                           int32_t* __restrict__ accept_len,
+                                                           int32_t* __restrict__ accept_tok,
+                                                           int32_t* __restrict__ last_node) {
+  constexpr int kChunks = FC_MAX_TREE_ROWS / fc::kWave;
+  const int b = blockIdx.x * kQueriesPerBlock + (int)(threadIdx.x / fc::kWave);
+  const int lane = fc::lane_id();
+  if (b >= B) return;  // whole wave leaves together
   const int R = c + 1;
   const int64_t row = (int64_t)b * R;
   int n = num_nodes[b];
   n = n < 1 ? 1 : (n > R ? R : n);
+  int32_t par[kChunks], tok[kChunks];
+#pragma unroll
+  for (int h = 0; h < kChunks; ++h) {
+    const int v = lane + h * fc::kWave;
+    const bool in = v >= 1 && v < n;
+    par[h] = in ? parent[row + v] : -2;
+    tok[h] = in ? node_tok[row + v] : -1;
+  }
   int32_t* out = accept_tok + (int64_t)b * (m + 1);
   int u = 0, len = 0;
   for (;;) {
     const int32_t want = target[row + u];
     if (want < 0 || len >= m + 1) break;
     int next = -1;
-    for (int v = u + 1; v < n; ++v)
-      if (parent[row + v] == u && node_tok[row + v] == want) {
-        next = v;
-        break;
-      }
+#pragma unroll
+    for (int h = 0; h < kChunks; ++h) {
+      const uint64_t hit = fc::ballot(par[h] == u && tok[h] == want);
+      if (next < 0 && hit) next = h * fc::kWave + (int)__builtin_ctzll(hit);
+    }
     if (next < 0) break;
-    out[len++] = node_tok[row + next];
+    if (lane == 0) out[len] = want;
+    ++len;
     u = next;
   }
   const int32_t bonus = target[row + u];
-  if (bonus >= 0 && len < m + 1) out[len++] = bonus;
-  for (int x = len; x < m + 1; ++x) out[x] = -1;
-  accept_len[b] = len;
-  last_node[b] = u;
+  if (bonus >= 0 && len < m + 1) {
+    if (lane == 0) out[len] = bonus;
+    ++len;
+  }
+  for (int x = len + lane; x < m + 1; x += fc::kWave) out[x] = -1;
+  if (lane == 0) {
+    accept_len[b] = len;
+    last_node[b] = u;
+  }
 }
 
 }  // namespace
@@ -61,8 +84,8 @@ extern "C" fc_status fc_verify_accept(const int32_t* num_nodes, const int32_t* n
   if (!num_nodes || !node_tok || !parent || !target || !accept_len || !accept_tok || !last_node)
     return FC_ERR_INVALID;
   (void)hipGetLastError();
-  hipLaunchKernelGGL(k_verify, dim3(fc::div_up(B, 256)), dim3(256), 0, stream, num_nodes, node_tok, parent, target,
-                     B, c, m, accept_len, accept_tok, last_node);
+  hipLaunchKernelGGL(k_verify, dim3(fc::div_up(B, kQueriesPerBlock)), dim3(kVerifyThreads), 0, stream, num_nodes,
+                     node_tok, parent, target, B, c, m, accept_len, accept_tok, last_node);
   FC_CHECK_LAUNCH();
   return FC_OK;
 }
