@@ -139,7 +139,9 @@ typedef struct fc_retrieve_params {
  * cont_tok [B][k][m] : continuation tokens, 0 past cont_len.
  * Within one store's slots the continuations come out in lexicographic order
  * (suffix order), which fc_build_tree relies on.
- * ws may be NULL when fc_retrieve_workspace_bytes returns 0.
+ * ws, ws_bytes : workspace of at least fc_retrieve_workspace_bytes(B, S, p)
+ *                (4*(B+1) bytes: the batch's slot offsets); its contents on
+ *                entry do not matter.
  */
 size_t fc_retrieve_workspace_bytes(int32_t B, int32_t S, fc_retrieve_params p);
 fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,

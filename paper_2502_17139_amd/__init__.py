@@ -173,6 +173,11 @@ def retrieve_outputs(B: int, S: int, k: int, m: int, device) -> dict:
         cont_len=_empty((B, k), torch.uint8, device), cont_tok=_empty((B, k, m), torch.uint16, device))
 
 
+def fc_retrieve_workspace_bytes(B: int, S: int, n_max: int = 16, n_min: int = 2, k: int = 5000,
+                                m: int = 10) -> int:
+    return int(lib().fc_retrieve_workspace_bytes(B, S, FcRetrieveParams(n_max, n_min, k, m)))
+
+
 def fc_retrieve(stores, ctx: torch.Tensor, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int = 10,
                 out: dict | None = None, workspace: torch.Tensor | None = None, stream=None) -> dict:
     """Batched longest-suffix retrieval; ctx is uint16 [B][L] on the GPU."""

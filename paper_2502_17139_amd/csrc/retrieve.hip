@@ -14,9 +14,10 @@
 // second token on.  The wave then keeps, per store, the longest n whose range
 // is non-empty and fills the k slots in store priority order.
 //
-// k_gather: one workgroup per query over its kept slots only.  A slot maps to
-// its store and range offset (strided floor(i*cnt/b) when the range exceeds
-// the store's budget b), reads the suffix-array entry and copies up to m
+// k_offsets + k_gather: the kept slots of the whole batch are numbered
+// consecutively and spread evenly over a persistent grid.  A slot maps to its
+// store and range offset (strided floor(i*cnt/b) when the range exceeds the
+// store's budget b), reads the suffix-array entry and copies up to m
 // continuation tokens, cut before a 0 and at the end of the store.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -30,6 +31,9 @@ namespace {
 constexpr int kSearchThreads = 256;
 constexpr int kQueriesPerBlock = kSearchThreads / fc::kWave;
 constexpr int kGatherThreads = 256;
+constexpr int kScanThreads = 1024;
+constexpr int kOffsetsInLds = 4096;
+constexpr int kGatherBlocks = 2048;
 
 struct StoreArgs {
   const uint16_t* tok[FC_MAX_SOURCES];
@@ -172,79 +176,117 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
   }
 }
 
-// One workgroup per query walks only the query's kept slots.  Each thread
-// handles two slots per iteration; for each it reads the suffix-array entry,
-// then issues all m token loads at once (they do not depend on each other;
-// the cut at the first 0 is applied afterwards in registers).
+// Exclusive prefix of kept slots over the batch (one workgroup):
+// offsets[b] = slots kept by queries before b; offsets[B] = total.
+__global__ void __launch_bounds__(kScanThreads) k_offsets(const int32_t* __restrict__ taken, int B, int S,
+                                                          uint32_t* __restrict__ offsets) {
+  __shared__ uint32_t scratch[kScanThreads / fc::kWave + 1];
+  const int per = (B + kScanThreads - 1) / kScanThreads;
+  const int b0 = (int)threadIdx.x * per;
+  const int b1 = b0 + per < B ? b0 + per : B;
+  uint32_t sum = 0;
+  for (int b = b0; b < b1; ++b)
+    for (int s = 0; s < S; ++s) sum += (uint32_t)taken[(int64_t)b * S + s];
+  uint32_t total;
+  uint32_t run = fc::block_excl_sum<uint32_t>(sum, scratch, &total);
+  for (int b = b0; b < b1; ++b) {
+    offsets[b] = run;
+    for (int s = 0; s < S; ++s) run += (uint32_t)taken[(int64_t)b * S + s];
+  }
+  if (threadIdx.x == 0) offsets[B] = total;
+}
+
+// Continuation tokens [start, start + MAXM) of one slot, all loads issued
+// together: 32-bit words from the aligned word at or before start.  Tokens
+// at or past N read as 0.
 template <int MAXM>
-__global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, int k, int m,
+__device__ __forceinline__ void load_window(const uint16_t* __restrict__ T, uint64_t N, uint64_t start,
+                                           uint16_t (&v)[MAXM]) {
+  constexpr int kWords = MAXM / 2 + 1;
+  const uint64_t w0 = start >> 1;
+  const int odd = (int)(start & 1);
+  if (2 * (w0 + kWords) <= N) {
+    const uint32_t* W = (const uint32_t*)T + w0;
+    uint32_t wd[kWords];
+#pragma unroll
+    for (int u = 0; u < kWords; ++u) wd[u] = W[u];
+#pragma unroll
+    for (int x = 0; x < MAXM; ++x) {
+      const uint16_t even_v = (uint16_t)(wd[x >> 1] >> (16 * (x & 1)));
+      const uint16_t odd_v = (uint16_t)(wd[(x + 1) >> 1] >> (16 * ((x + 1) & 1)));
+      v[x] = odd ? odd_v : even_v;
+    }
+  } else {
+#pragma unroll
+    for (int x = 0; x < MAXM; ++x) v[x] = (start + x < N) ? T[start + x] : (uint16_t)0;
+  }
+}
+
+// Kept slots of the whole batch as one flat range, split evenly over a
+// persistent grid: slot g belongs to the query b with offsets[b] <= g <
+// offsets[b+1] (binary search in an LDS copy of the offsets).  For each slot
+// the suffix-array entry is read (consecutive slots of a store read
+// consecutive entries when the whole range is kept), then the continuation
+// window with a few wide loads, cut at the first 0 in registers.
+template <int MAXM>
+__global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, int B, int k, int m,
                                                            const int32_t* __restrict__ match_n,
                                                            const uint32_t* __restrict__ range_lo,
                                                            const uint32_t* __restrict__ range_cnt,
                                                            const int32_t* __restrict__ taken,
+                                                           const uint32_t* __restrict__ offsets, int words,
                                                            uint32_t* __restrict__ cont_pos,
                                                            uint8_t* __restrict__ cont_src,
                                                            uint8_t* __restrict__ cont_len,
                                                            uint16_t* __restrict__ cont_tok) {
-  __shared__ int64_t s_first[FC_MAX_SOURCES + 1];
-  __shared__ uint64_t s_cnt[FC_MAX_SOURCES], s_budget[FC_MAX_SOURCES], s_lo[FC_MAX_SOURCES];
-  __shared__ uint32_t s_n[FC_MAX_SOURCES];
-  const int b = blockIdx.x;
-  if (threadIdx.x == 0) {
+  __shared__ uint32_t s_off[kOffsetsInLds];
+  const bool in_lds = B + 1 <= kOffsetsInLds;
+  if (in_lds)
+    for (int i = (int)threadIdx.x; i <= B; i += kGatherThreads) s_off[i] = offsets[i];
+  __syncthreads();
+  const uint32_t* off_tab = in_lds ? s_off : offsets;
+  const uint32_t total = off_tab[B];
+  for (uint32_t g = blockIdx.x * kGatherThreads + threadIdx.x; g < total; g += gridDim.x * kGatherThreads) {
+    int lo = 0, hi = B;  // last b with offsets[b] <= g
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (off_tab[mid] <= g) lo = mid; else hi = mid;
+    }
+    const int b = lo;
+    const int i = (int)(g - off_tab[b]);
+    int s = 0;
     int64_t before = 0;
-    for (int s = 0; s < S; ++s) {
-      const int64_t o = (int64_t)b * S + s;
-      const int64_t t = taken[o];
-      s_first[s] = before;
-      s_cnt[s] = range_cnt[o];
-      s_budget[s] = (uint64_t)((int64_t)k - before);
-      s_lo[s] = range_lo[o];
-      s_n[s] = (uint32_t)match_n[o];
+    for (; s + 1 < S; ++s) {
+      const int64_t t = taken[(int64_t)b * S + s];
+      if (i < before + t) break;
       before += t;
     }
-    s_first[S] = before;
-  }
-  __syncthreads();
-  const int total = (int)s_first[S];
-  for (int i0 = (int)threadIdx.x; i0 < total; i0 += 2 * kGatherThreads) {
-    uint32_t j[2];
-    int src[2];
-    bool ok[2];
+    const int64_t o = (int64_t)b * S + s;
+    const uint64_t cnt = range_cnt[o];
+    const uint64_t budget = (uint64_t)((int64_t)k - before);
+    const uint64_t local = (uint64_t)(i - before);
+    const uint64_t off = cnt > budget ? (local * cnt) / budget : local;
+    const uint32_t j = st.sa[s][(uint64_t)range_lo[o] + off];
+    const uint64_t start = (uint64_t)j + (uint64_t)match_n[o];
+    const uint64_t N = st.n[s];
+    uint16_t v[MAXM];
+    if (words) load_window<MAXM>(st.tok[s], N, start, v);
+    else {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int i = i0 + h * kGatherThreads;
-      ok[h] = i < total;
-      int s = 0;
-      while (s + 1 < S && i >= s_first[s + 1]) ++s;
-      src[h] = s;
-      const uint64_t local = ok[h] ? (uint64_t)(i - s_first[s]) : 0;
-      const uint64_t off = (ok[h] && s_cnt[s] > s_budget[s]) ? (local * s_cnt[s]) / s_budget[s] : local;
-      j[h] = ok[h] ? st.sa[s][s_lo[s] + off] : 0u;
+      for (int x = 0; x < MAXM; ++x) v[x] = (start + x < N) ? st.tok[s][start + x] : (uint16_t)0;
     }
+    int len = m;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      if (!ok[h]) continue;
-      const int i = i0 + h * kGatherThreads;
-      const int s = src[h];
-      const uint64_t start = (uint64_t)j[h] + s_n[s];
-      const uint16_t* T = st.tok[s];
-      const uint64_t N = st.n[s];
-      uint16_t v[MAXM];
+    for (int x = MAXM - 1; x >= 0; --x)
+      if (x < m && v[x] == 0) len = x;
+    const int64_t slot = (int64_t)b * k + i;
+    uint16_t* out = cont_tok + slot * m;
 #pragma unroll
-      for (int x = 0; x < MAXM; ++x) v[x] = (x < m && start + x < N) ? T[start + x] : (uint16_t)0;
-      int len = m;
-#pragma unroll
-      for (int x = MAXM - 1; x >= 0; --x)
-        if (x < m && v[x] == 0) len = x;
-      const int64_t slot = (int64_t)b * k + i;
-      uint16_t* out = cont_tok + slot * m;
-#pragma unroll
-      for (int x = 0; x < MAXM; ++x)
-        if (x < m) out[x] = x < len ? v[x] : (uint16_t)0;
-      cont_pos[slot] = (uint32_t)start;
-      cont_src[slot] = (uint8_t)s;
-      cont_len[slot] = (uint8_t)len;
-    }
+    for (int x = 0; x < MAXM; ++x)
+      if (x < m) out[x] = x < len ? v[x] : (uint16_t)0;
+    cont_pos[slot] = (uint32_t)start;
+    cont_src[slot] = (uint8_t)s;
+    cont_len[slot] = (uint8_t)len;
   }
 }
 
@@ -303,10 +345,9 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather_any(StoreArgs st, int
 }  // namespace
 
 extern "C" size_t fc_retrieve_workspace_bytes(int32_t B, int32_t S, fc_retrieve_params p) {
-  (void)B;
   (void)S;
   (void)p;
-  return 0;
+  return B > 0 ? ((size_t)B + 1) * sizeof(uint32_t) : 0;
 }
 
 extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
@@ -331,15 +372,25 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
   if (B == 0) return FC_OK;
   if (!ctx || !match_n || !range_lo || !range_cnt || !taken || !cont_pos || !cont_src || !cont_len || !cont_tok)
     return FC_ERR_INVALID;
-  if (ws_bytes < fc_retrieve_workspace_bytes(B, S, p)) return FC_ERR_WORKSPACE;
-  (void)ws;
+  if (!ws || ws_bytes < fc_retrieve_workspace_bytes(B, S, p)) return FC_ERR_WORKSPACE;
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_search, dim3(fc::div_up(B, kQueriesPerBlock)), dim3(kSearchThreads), 0, stream, st, S, ctx,
                      B, L, p.n_max, p.n_min, p.k, match_n, range_lo, range_cnt, taken);
   FC_CHECK_LAUNCH();
   if (p.m <= 16) {
-    hipLaunchKernelGGL(k_gather<16>, dim3(B), dim3(kGatherThreads), 0, stream, st, S, p.k, p.m, match_n, range_lo,
-                       range_cnt, taken, cont_pos, cont_src, cont_len, cont_tok);
+    uint32_t* offsets = (uint32_t*)ws;
+    hipLaunchKernelGGL(k_offsets, dim3(1), dim3(kScanThreads), 0, stream, taken, B, S, offsets);
+    FC_CHECK_LAUNCH();
+    int words = 1;
+    for (int s = 0; s < S; ++s) words &= (((uintptr_t)st.tok[s]) & 3) == 0;
+    const uint64_t want = ((uint64_t)B * p.k + kGatherThreads - 1) / kGatherThreads;
+    const uint32_t blocks = (uint32_t)(want < (uint64_t)kGatherBlocks ? want : (uint64_t)kGatherBlocks);
+    if (p.m <= 10)
+      hipLaunchKernelGGL(k_gather<10>, dim3(blocks), dim3(kGatherThreads), 0, stream, st, S, B, p.k, p.m, match_n,
+                         range_lo, range_cnt, taken, offsets, words, cont_pos, cont_src, cont_len, cont_tok);
+    else
+      hipLaunchKernelGGL(k_gather<16>, dim3(blocks), dim3(kGatherThreads), 0, stream, st, S, B, p.k, p.m, match_n,
+                         range_lo, range_cnt, taken, offsets, words, cont_pos, cont_src, cont_len, cont_tok);
   } else {
     hipLaunchKernelGGL(k_gather_any, dim3(B), dim3(kGatherThreads), 0, stream, st, S, p.k, p.m, match_n, range_lo,
                        range_cnt, taken, cont_pos, cont_src, cont_len, cont_tok);

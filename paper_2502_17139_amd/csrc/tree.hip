@@ -86,6 +86,12 @@ __device__ __forceinline__ int str_lcp(const uint16_t* a, int la, const uint16_t
   return x;
 }
 
+// alpha[s] without indexing the argument struct at run time (which would
+// place it in scratch memory).
+__device__ __forceinline__ uint32_t alpha_of(const Alpha& a, int s) {
+  return s == 0 ? a.a[0] : s == 1 ? a.a[1] : s == 2 ? a.a[2] : a.a[3];
+}
+
 __device__ __forceinline__ int src_of(const int* seg, int S, int i) {
   int s = 0;
   while (s + 1 < S && i >= seg[s + 1]) ++s;
@@ -393,18 +399,22 @@ __global__ void __launch_bounds__(kTreeThreads) k_tree_any(const int32_t* __rest
 
 template <int NT>
 struct Scan2 {
-  // Exclusive prefix sums of (x, y) over the block plus their totals.
+  // Exclusive prefix sums of (x, y) over the block plus their totals, and
+  // optionally the block total of z; two barriers.
   __device__ static void run(uint32_t x, uint32_t y, uint32_t* sx, uint32_t* sy, uint32_t* ex, uint32_t* ey,
-                             uint32_t* tx, uint32_t* ty) {
+                             uint32_t* tx, uint32_t* ty, uint32_t z = 0, uint32_t* sz = nullptr,
+                             uint32_t* tz = nullptr) {
     constexpr int NW = NT / fc::kWave;
     const int w = (int)threadIdx.x / fc::kWave;
     const uint32_t ix = fc::wave_incl_sum(x), iy = fc::wave_incl_sum(y);
+    const uint32_t iz = sz ? fc::wave_sum(z) : 0u;
     if (fc::lane_id() == fc::kWave - 1) {
       sx[w] = ix;
       sy[w] = iy;
+      if (sz) sz[w] = iz;
     }
     __syncthreads();
-    uint32_t px = 0, py = 0, ax = 0, ay = 0;
+    uint32_t px = 0, py = 0, ax = 0, ay = 0, az = 0;
 #pragma unroll
     for (int i = 0; i < NW; ++i) {
       const uint32_t vx = sx[i], vy = sy[i];
@@ -414,11 +424,13 @@ struct Scan2 {
       }
       ax += vx;
       ay += vy;
+      if (sz) az += sz[i];
     }
     *ex = px + ix - x;
     *ey = py + iy - y;
     *tx = ax;
     *ty = ay;
+    if (tz) *tz = az;
     __syncthreads();
   }
 };
@@ -496,7 +508,14 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     len[i] = l;
     if (l > m) s_err = 1;
   }
-  if (words) {
+  if (words == 2) {
+    // 16-byte rows: 8 tokens per load, four loads in flight per thread
+    const uint4* src = (const uint4*)(cont_tok + row0 * m);
+    uint4* dst = (uint4*)str;
+    const int nv = (T * m + 7) >> 3;
+#pragma unroll 4
+    for (int e = tid; e < nv; e += NT) dst[e] = src[e];
+  } else if (words == 1) {
     const uint32_t* src = (const uint32_t*)(cont_tok + row0 * m);
     uint32_t* dst = (uint32_t*)str;
     const int nw = (T * m + 1) >> 1;
@@ -579,7 +598,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       }
       mlen[p] = (uint8_t)li;
       lcp[p] = (uint8_t)l;
-      const uint32_t a = alpha.a[src_of(s_seg, S, i)];
+      const uint32_t a = alpha_of(alpha, src_of(s_seg, S, i));
       asum += a;
       if (li > 0) rw += a;
       nodes += (uint32_t)(li - l);
@@ -588,8 +607,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
         if (l < d) f[d] = (uint16_t)p;
     }
     uint32_t a_ex, dummy, a_tot, n_tot;
-    Scan2<NT>::run(asum, nodes, s_x, s_y, &a_ex, &dummy, &a_tot, &n_tot);
-    root_w = fc::block_sum<uint32_t>(rw, s_z);
+    Scan2<NT>::run(asum, nodes, s_x, s_y, &a_ex, &dummy, &a_tot, &n_tot, rw, s_z, &root_w);
     // suffix minimum of f over later chunks (wave shuffles, then waves)
     uint16_t nh[MAXM + 1];
 #pragma unroll
@@ -618,22 +636,31 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       uint32_t run = a_ex;
       for (int p = p0; p < p1; ++p) {
         A[p] = run;
-        run += alpha.a[src_of(s_seg, S, perm[p])];
+        run += alpha_of(alpha, src_of(s_seg, S, perm[p]));
       }
       if (tid == 0) A[T] = a_tot;
     }
     __syncthreads();  // str is dead from here on: E reuses it
 
-    // 4. run ends, right to left through the chunk
+    // 4. run ends, right to left through the chunk.  The node weight
+    //    A[end] - A[q] is stored directly when every weight fits 16 bits
+    //    (weights never exceed the root's); otherwise the run end is stored
+    //    and the weight recomputed where needed.
+    const bool wide = root_w > 0xFFFFu;
     for (int q = p1 - 1; q >= p0; --q) {
       const int l = lcp[q], ml = mlen[q];
+      const uint32_t aq = A[q];
 #pragma unroll
       for (int d = 1; d <= MAXM; ++d) {
-        if (d > l && d <= ml) E[q * m + d - 1] = nh[d];
+        if (d > l && d <= ml) E[q * m + d - 1] = wide ? nh[d] : (uint16_t)(A[nh[d]] - aq);
         if (d > l) nh[d] = (uint16_t)q;
       }
     }
     __syncthreads();
+    auto node_w = [&](int p, int d, uint32_t ap) -> uint32_t {
+      const uint16_t e = E[p * m + d - 1];
+      return wide ? A[e] - ap : (uint32_t)e;
+    };
 
     // 5. radix select: the need-th largest weight W*, and how many nodes of
     //    weight W* to take (in (p, d) order)
@@ -642,7 +669,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     for (int p = p0; p < p1; ++p) {
       const int d = lcp[p] + 1;  // the shallowest own node is the heaviest
       if (d <= mlen[p]) {
-        const uint32_t W = A[E[p * m + d - 1]] - A[p];
+        const uint32_t W = node_w(p, d, A[p]);
         wmax = W > wmax ? W : wmax;
       }
     }
@@ -656,9 +683,9 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
         __syncthreads();
         const uint64_t hi_mask = shift + 8 >= 32 ? 0ull : (uint64_t)prefix >> (shift + 8);
         for (int p = p0; p < p1; ++p) {
-          const uint32_t ap = A[p];
+          const uint32_t ap = wide ? A[p] : 0u;
           for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
-            const uint32_t W = A[E[p * m + d - 1]] - ap;
+            const uint32_t W = node_w(p, d, ap);
             if ((shift + 8 >= 32 ? 0ull : (uint64_t)(W >> (shift + 8))) == hi_mask)
               atomicAdd(&s_hist[(W >> shift) & 0xFF], 1u);
           }
@@ -702,9 +729,9 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     uint32_t gt = 0, eq = 0;
     if (need > 0) {
       for (int p = p0; p < p1; ++p) {
-        const uint32_t ap = A[p];
+        const uint32_t ap = wide ? A[p] : 0u;
         for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
-          const uint32_t W = A[E[p * m + d - 1]] - ap;
+          const uint32_t W = node_w(p, d, ap);
           gt += W > wstar;
           eq += W == wstar;
         }
@@ -716,9 +743,9 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       uint32_t o = 1 + gt_ex + (eq_ex < take_eq ? eq_ex : take_eq);
       uint32_t r = eq_ex;
       for (int p = p0; p < p1; ++p) {
-        const uint32_t ap = A[p];
+        const uint32_t ap = wide ? A[p] : 0u;
         for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
-          const uint32_t W = A[E[p * m + d - 1]] - ap;
+          const uint32_t W = node_w(p, d, ap);
           bool keep = W > wstar;
           if (W == wstar) keep = r++ < take_eq;
           if (keep && o < (uint32_t)FC_MAX_TREE_ROWS) {
@@ -813,7 +840,11 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
   if (m <= 16) {
     // light queries (T <= 1024) in small-LDS workgroups, the rest in full-LDS ones
     const int t_small = k < kSmallClass ? k : kSmallClass;
-    const int words = ((((uintptr_t)cont_tok) & 3) == 0 && ((size_t)k * m) % 2 == 0) ? 1 : 0;
+    // row loads: 16-byte vectors when every query's row is 16-byte aligned,
+    // else 32-bit words when 4-byte aligned, else single tokens
+    int words = 0;
+    if ((((uintptr_t)cont_tok) & 15) == 0 && ((size_t)k * m) % 8 == 0) words = 2;
+    else if ((((uintptr_t)cont_tok) & 3) == 0 && ((size_t)k * m) % 2 == 0) words = 1;
     const TreeLayout small = tree_layout(t_small, m);
     if (small.total > 64 * 1024)
       (void)hipFuncSetAttribute((const void*)k_tree_fast<256, 16>, hipFuncAttributeMaxDynamicSharedMemorySize,

@@ -45,7 +45,9 @@ def test_workspace_sizes(L):
     # about 28.6 bytes per token for the 1B-token store
     n = 1_001_999_999
     assert 28 * n < fc.fc_datastore_build_workspace_bytes(n) < 29 * n
-    assert L.fc_retrieve_workspace_bytes(1024, 2, fc.FcRetrieveParams(16, 2, 5000, 10)) == 0
+    # the batch's slot offsets
+    assert L.fc_retrieve_workspace_bytes(1024, 2, fc.FcRetrieveParams(16, 2, 5000, 10)) == 4 * 1025
+    assert L.fc_retrieve_workspace_bytes(0, 2, fc.FcRetrieveParams(16, 2, 5000, 10)) == 0
 
 
 def _retrieve_args(S=1, B=1, L_=4, p=(16, 2, 5000, 10), ws_bytes=0):
@@ -61,6 +63,13 @@ def _retrieve_args(S=1, B=1, L_=4, p=(16, 2, 5000, 10), ws_bytes=0):
 ])
 def test_retrieve_rejects(L, change, code):
     assert L.fc_retrieve(*_retrieve_args(**change)) == code
+
+
+def test_retrieve_rejects_missing_workspace(L):
+    assert L.fc_retrieve(*_retrieve_args(ws_bytes=0)) == 2
+    args = _retrieve_args(ws_bytes=4)  # 4*(B+1) = 8 needed
+    args[-3] = ctypes.c_void_p(8)
+    assert L.fc_retrieve(*args) == 2
 
 
 def test_retrieve_rejects_null_outputs_and_big_store(L):
