@@ -165,13 +165,15 @@ def main():
     rws = torch.empty(max(fc.fc_retrieve_workspace_bytes(B, len(stores), p["n_max"], p["n_min"], k, m), 1),
                       dtype=torch.uint8, device=dev)
     tout = fc.tree_outputs(B, c, dev)
+    tws = torch.empty(max(fc.fc_build_tree_workspace_bytes(B), 1), dtype=torch.uint8, device=dev)
     aout = fc.accept_outputs(B, m, dev)
 
     def retrieve():
         fc.fc_retrieve(stores, ctx, n_max=p["n_max"], n_min=p["n_min"], k=k, m=m, out=rout, workspace=rws)
 
     def tree():
-        fc.fc_build_tree(rout["taken"], rout["cont_len"], rout["cont_tok"], ctx, c=c, alpha=alpha, out=tout)
+        fc.fc_build_tree(rout["taken"], rout["cont_len"], rout["cont_tok"], ctx, c=c, alpha=alpha, out=tout,
+                         workspace=tws)
 
     # first pass: its tree fixes the target tokens (the target model's outputs)
     retrieve()

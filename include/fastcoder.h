@@ -179,13 +179,17 @@ typedef struct fc_tree_params {
  * mask [B][c+1][c+1]      : 1 where column j is row i or an ancestor of i
  *                           (root included), else 0.
  * Rows past num_nodes: token 0, parent -1, weight 0, position 0, mask 0.
- * Limits: S <= FC_MAX_SOURCES, k <= 65535, and the per-query working set
- * (about k*(2m+9) bytes) must fit one workgroup's LDS (FC_ERR_UNSUPPORTED).
+ * ws, ws_bytes           : workspace of at least fc_build_tree_workspace_bytes(B)
+ *                           (the batch split into light and heavy queries).
+ * Limits: S <= FC_MAX_SOURCES, k <= 65535, alpha[s]*k < 2^32, and the
+ * per-query working set (about k*(2m+9) bytes) must fit one workgroup's LDS
+ * (FC_ERR_UNSUPPORTED).
  */
+size_t fc_build_tree_workspace_bytes(int32_t B);
 fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok,
                         const uint16_t* ctx, int32_t B, int32_t L, int32_t S, int32_t k, int32_t m, fc_tree_params t,
                         int32_t* num_nodes, int32_t* node_tok, int32_t* parent, uint32_t* weight, int32_t* pos_ids,
-                        int32_t* mask, hipStream_t stream);
+                        int32_t* mask, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Acceptance                                                                */

@@ -30,7 +30,8 @@ STATUS = {0: "FC_OK", 1: "FC_ERR_INVALID", 2: "FC_ERR_WORKSPACE", 3: "FC_ERR_DEV
 EXPORTS = (
     "fc_abi_version", "fc_status_string",
     "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_store_prepare",
-    "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree", "fc_verify_accept",
+    "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
+    "fc_verify_accept",
 )
 
 
@@ -79,9 +80,11 @@ def lib() -> ctypes.CDLL:
     L.fc_retrieve.restype = ctypes.c_int
     L.fc_retrieve.argtypes = [ctypes.POINTER(FcStore), i32, vp, i32, i32, FcRetrieveParams,
                               vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.fc_build_tree_workspace_bytes.restype = sz
+    L.fc_build_tree_workspace_bytes.argtypes = [i32]
     L.fc_build_tree.restype = ctypes.c_int
     L.fc_build_tree.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, FcTreeParams,
-                                vp, vp, vp, vp, vp, vp, vp]
+                                vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.fc_verify_accept.restype = ctypes.c_int
     L.fc_verify_accept.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp]
     return L
@@ -210,8 +213,13 @@ def tree_outputs(B: int, c: int, device) -> dict:
                 pos_ids=_empty((B, R), torch.int32, device), mask=_empty((B, R, R), torch.int32, device))
 
 
+def fc_build_tree_workspace_bytes(B: int) -> int:
+    return int(lib().fc_build_tree_workspace_bytes(B))
+
+
 def fc_build_tree(taken: torch.Tensor, cont_len: torch.Tensor, cont_tok: torch.Tensor, ctx: torch.Tensor,
-                  c: int = 64, alpha=(1, 1), out: dict | None = None, stream=None) -> dict:
+                  c: int = 64, alpha=(1, 1), out: dict | None = None, workspace: torch.Tensor | None = None,
+                  stream=None) -> dict:
     """Weighted draft trie pruned to c nodes, with mask and position ids."""
     B, S = taken.shape
     k, m = cont_tok.shape[1], cont_tok.shape[2]
@@ -222,9 +230,13 @@ def fc_build_tree(taken: torch.Tensor, cont_len: torch.Tensor, cont_tok: torch.T
     tp = FcTreeParams(c, (ctypes.c_uint32 * FC_MAX_SOURCES)(*(a + [0] * (FC_MAX_SOURCES - S))))
     if out is None:
         out = tree_outputs(B, c, ctx.device)
+    need = fc_build_tree_workspace_bytes(B)
+    if workspace is None and need > 0:
+        workspace = _empty(need, torch.uint8, ctx.device)
     _check("fc_build_tree", lib().fc_build_tree(
         _ptr(taken), _ptr(cont_len), _ptr(cont_tok), _ptr(ctx), B, L, S, k, m, tp,
-        *[_ptr(out[f]) for f in TREE_FIELDS], _stream(stream)))
+        *[_ptr(out[f]) for f in TREE_FIELDS], _ptr(workspace), 0 if workspace is None else workspace.numel(),
+        _stream(stream)))
     return out
 
 

@@ -435,12 +435,47 @@ struct Scan2 {
   }
 };
 
+// Splits the batch into light (T <= t_small kept slots; malformed rows too)
+// and heavy queries, each list in query order: lists[0..B) light ids,
+// lists[B..2B) heavy ids, counts[0], counts[1] their lengths.
+__global__ void __launch_bounds__(1024) k_tree_classify(const int32_t* __restrict__ taken, int B, int S, int k,
+                                                        int t_small, int32_t* __restrict__ lists,
+                                                        int32_t* __restrict__ counts) {
+  __shared__ uint32_t s_a[1024 / fc::kWave + 1], s_b[1024 / fc::kWave + 1];
+  const int per = (B + 1023) / 1024;
+  const int b0 = (int)threadIdx.x * per;
+  const int b1 = b0 + per < B ? b0 + per : B;
+  auto heavy = [&](int b) {
+    int T = 0, bad = 0;
+    for (int s = 0; s < S; ++s) {
+      const int t = taken[(int64_t)b * S + s];
+      bad |= t < 0;
+      T += t > 0 ? t : 0;
+    }
+    return !bad && T <= k && T > t_small;
+  };
+  uint32_t nh = 0;
+  for (int b = b0; b < b1; ++b) nh += heavy(b) ? 1u : 0u;
+  const uint32_t nl = (uint32_t)(b1 > b0 ? b1 - b0 : 0) - nh;
+  uint32_t el, eh, tl, th;
+  Scan2<1024>::run(nl, nh, s_a, s_b, &el, &eh, &tl, &th);
+  for (int b = b0; b < b1; ++b) {
+    if (heavy(b)) lists[B + (eh++)] = b;
+    else lists[el++] = b;
+  }
+  if (threadIdx.x == 0) {
+    counts[0] = (int32_t)tl;
+    counts[1] = (int32_t)th;
+  }
+}
+
 template <int NT, int MAXM>
 __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ taken,
                                                   const uint8_t* __restrict__ cont_len,
                                                   const uint16_t* __restrict__ cont_tok,
                                                   const uint16_t* __restrict__ ctx, int L, int S, int k, int m, int c,
-                                                  Alpha alpha, int t_lo, int t_hi, int words,
+                                                  Alpha alpha, const int32_t* __restrict__ list,
+                                                  const int32_t* __restrict__ list_count, int t_hi, int words,
                                                   int32_t* __restrict__ num_nodes, int32_t* __restrict__ node_tok,
                                                   int32_t* __restrict__ parent, uint32_t* __restrict__ weight,
                                                   int32_t* __restrict__ pos_ids, int32_t* __restrict__ mask) {
@@ -455,18 +490,21 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
   __shared__ uint16_t s_sel_p[FC_MAX_TREE_ROWS];
   __shared__ uint8_t s_sel_d[FC_MAX_TREE_ROWS];
   __shared__ int16_t s_par[FC_MAX_TREE_ROWS];
-  __shared__ uint32_t s_pick[2];
+  __shared__ uint32_t s_pick[3];
 
-  const int b = blockIdx.x;
+  // This launch owns the queries in `list` (built by k_tree_classify);
+  // workgroups past the list's length leave at once, after every real one
+  // has been dispatched.
+  if ((int)blockIdx.x >= *list_count) return;
+  const int b = list[blockIdx.x];
   const int tid = threadIdx.x;
   const int lane = fc::lane_id();
   const int w = tid / fc::kWave;
   const int R = c + 1;
   const int64_t row0 = (int64_t)b * k;
 
-  // Class check: this launch owns queries with t_lo < T <= t_hi.  Malformed
-  // rows (a negative count or more than k slots) count as T = 0, so the
-  // small-class launch (t_lo = -1) reports them.
+  // Malformed rows (a negative count or more than k slots) count as T = 0
+  // and are reported with num_nodes = -1.
   int T_raw = 0, bad = 0;
   for (int s = 0; s < S; ++s) {
     const int t = taken[(int64_t)b * S + s];
@@ -474,8 +512,8 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     T_raw += t > 0 ? t : 0;
   }
   bad |= T_raw > k;
+  bad |= T_raw > t_hi;  // cannot happen: k_tree_classify routes queries by T
   if (bad) T_raw = 0;
-  if (T_raw <= t_lo || T_raw > t_hi) return;  // uniform over the workgroup
 
   const TreeLayout lay = tree_layout(t_hi, m);
   uint16_t* str = (uint16_t*)(smem + lay.str);
@@ -662,22 +700,84 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       return wide ? A[e] - ap : (uint32_t)e;
     };
 
-    // 5. radix select: the need-th largest weight W*, and how many nodes of
-    //    weight W* to take (in (p, d) order)
+    // 5. the need-th largest weight W* and how many nodes of weight W* to
+    //    take (in (p, d) order).  Most nodes are light, so weights below 8
+    //    are counted in registers, 8..255 in an LDS histogram, and heavier
+    //    ones lumped; only when W* itself is heavy does a radix select over
+    //    the (few) heavy nodes follow.
     const uint32_t need = n_tot < (uint32_t)c ? n_tot : (uint32_t)c;
-    uint32_t wmax = 0;
-    for (int p = p0; p < p1; ++p) {
-      const int d = lcp[p] + 1;  // the shallowest own node is the heaviest
-      if (d <= mlen[p]) {
-        const uint32_t W = node_w(p, d, A[p]);
-        wmax = W > wmax ? W : wmax;
-      }
-    }
-    wmax = fc::block_max<uint32_t>(wmax, s_z);
     uint32_t prefix = 0, remaining = need;
-    int bits = 0;
-    for (uint32_t x = wmax; x; x >>= 1) ++bits;
-    if (need > 0 && bits > 0) {
+    for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
+    if (tid == 0) s_pick[2] = 0;
+    __syncthreads();
+    if (need > 0) {
+      uint32_t r[8], rbig = 0;
+#pragma unroll
+      for (int v = 0; v < 8; ++v) r[v] = 0;
+      for (int p = p0; p < p1; ++p) {
+        const uint32_t ap = wide ? A[p] : 0u;
+        for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
+          const uint32_t W = node_w(p, d, ap);
+#pragma unroll
+          for (int v = 0; v < 8; ++v) r[v] += (W == (uint32_t)v);
+          if (W >= 256) ++rbig;
+          else if (W >= 8) atomicAdd(&s_hist[W], 1u);
+        }
+      }
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const uint32_t x = fc::wave_sum(r[v]);
+        if (lane == 0 && x) atomicAdd(&s_hist[v], x);
+      }
+      const uint32_t xb = fc::wave_sum(rbig);
+      if (lane == 0 && xb) atomicAdd(&s_pick[2], xb);
+    }
+    __syncthreads();
+    const uint32_t n_heavy = s_pick[2];
+    if (need > 0 && n_heavy < need) {
+      // W* < 256: wave 0 walks the histogram from the top
+      if (tid < fc::kWave) {
+        const uint32_t want = need - n_heavy;
+        uint32_t cnt[4];
+        uint32_t lsum = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          cnt[u] = s_hist[255 - (lane * 4 + u)];
+          lsum += cnt[u];
+        }
+        const uint32_t incl = fc::wave_incl_sum(lsum);
+        const uint32_t before = incl - lsum;
+        if (before < want && incl >= want) {
+          uint32_t acc = before;
+          int bin = 0;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            if (acc + cnt[u] >= want) {
+              bin = 255 - (lane * 4 + u);
+              break;
+            }
+            acc += cnt[u];
+          }
+          s_pick[0] = (uint32_t)bin;
+          s_pick[1] = want - acc;
+        }
+      }
+      __syncthreads();
+      prefix = s_pick[0];
+      remaining = s_pick[1];
+    } else if (need > 0) {
+      // W* >= 256: radix select over the heavy nodes only
+      uint32_t wmax = 0;
+      for (int p = p0; p < p1; ++p) {
+        const int d = lcp[p] + 1;  // the shallowest own node is the heaviest
+        if (d <= mlen[p]) {
+          const uint32_t W = node_w(p, d, A[p]);
+          wmax = W > wmax ? W : wmax;
+        }
+      }
+      wmax = fc::block_max<uint32_t>(wmax, s_z);
+      int bits = 0;
+      for (uint32_t x = wmax; x; x >>= 1) ++bits;
       for (int shift = ((bits - 1) / 8) * 8; shift >= 0; shift -= 8) {
         for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
         __syncthreads();
@@ -686,13 +786,13 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
           const uint32_t ap = wide ? A[p] : 0u;
           for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
             const uint32_t W = node_w(p, d, ap);
+            if (W < 256) break;  // own nodes get lighter with depth
             if ((shift + 8 >= 32 ? 0ull : (uint64_t)(W >> (shift + 8))) == hi_mask)
               atomicAdd(&s_hist[(W >> shift) & 0xFF], 1u);
           }
         }
         __syncthreads();
         if (tid < fc::kWave) {
-          // wave 0 finds the bin holding the remaining-th largest
           uint32_t cnt[4];
           uint32_t lsum = 0;
 #pragma unroll
@@ -816,10 +916,15 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
 
 }  // namespace
 
+extern "C" size_t fc_build_tree_workspace_bytes(int32_t B) {
+  return B > 0 ? (2 * (size_t)B + 2) * sizeof(int32_t) : 0;
+}
+
 extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok,
                                    const uint16_t* ctx, int32_t B, int32_t L, int32_t S, int32_t k, int32_t m,
                                    fc_tree_params t, int32_t* num_nodes, int32_t* node_tok, int32_t* parent,
-                                   uint32_t* weight, int32_t* pos_ids, int32_t* mask, hipStream_t stream) {
+                                   uint32_t* weight, int32_t* pos_ids, int32_t* mask, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
   if (B < 0 || L < 1 || S < 1 || S > FC_MAX_SOURCES) return FC_ERR_INVALID;
   if (k < 1 || m < 1 || m > 255 || t.c < 1 || t.c + 1 > FC_MAX_TREE_ROWS) return FC_ERR_INVALID;
   if (k > 65535) return FC_ERR_UNSUPPORTED;
@@ -828,6 +933,7 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
   if (B == 0) return FC_OK;
   if (!taken || !cont_len || !cont_tok || !ctx || !num_nodes || !node_tok || !parent || !weight || !pos_ids || !mask)
     return FC_ERR_INVALID;
+  if (!ws || ws_bytes < fc_build_tree_workspace_bytes(B)) return FC_ERR_WORKSPACE;
   int dev = 0, max_lds = 0;
   FC_CHECK_HIP(hipGetDevice(&dev));
   FC_CHECK_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
@@ -838,8 +944,13 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
   if (full.total + static_lds > (size_t)max_lds) return FC_ERR_UNSUPPORTED;
   (void)hipGetLastError();
   if (m <= 16) {
-    // light queries (T <= 1024) in small-LDS workgroups, the rest in full-LDS ones
+    // light queries (T <= 1024) in small-LDS workgroups, the rest in full-LDS
+    // ones, each launch walking its own list of queries
     const int t_small = k < kSmallClass ? k : kSmallClass;
+    int32_t* lists = (int32_t*)ws;
+    int32_t* counts = lists + 2 * (size_t)B;
+    hipLaunchKernelGGL(k_tree_classify, dim3(1), dim3(1024), 0, stream, taken, B, S, k, t_small, lists, counts);
+    FC_CHECK_LAUNCH();
     // row loads: 16-byte vectors when every query's row is 16-byte aligned,
     // else 32-bit words when 4-byte aligned, else single tokens
     int words = 0;
@@ -849,18 +960,19 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
     if (small.total > 64 * 1024)
       (void)hipFuncSetAttribute((const void*)k_tree_fast<256, 16>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)small.total);
+    (void)hipGetLastError();
     hipLaunchKernelGGL((k_tree_fast<256, 16>), dim3(B), dim3(256), small.total, stream, taken, cont_len, cont_tok,
-                       ctx, L, S, k, m, t.c, a, -1, t_small, words, num_nodes, node_tok, parent, weight, pos_ids,
-                       mask);
+                       ctx, L, S, k, m, t.c, a, lists, counts, t_small, words, num_nodes, node_tok, parent, weight,
+                       pos_ids, mask);
     FC_CHECK_LAUNCH();
     if (k > t_small) {
       if (full.total > 64 * 1024)
-        (void)hipFuncSetAttribute((const void*)k_tree_fast<512, 16>, hipFuncAttributeMaxDynamicSharedMemorySize,
+        (void)hipFuncSetAttribute((const void*)k_tree_fast<1024, 16>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                   (int)full.total);
       (void)hipGetLastError();
-      hipLaunchKernelGGL((k_tree_fast<512, 16>), dim3(B), dim3(512), full.total, stream, taken, cont_len, cont_tok,
-                         ctx, L, S, k, m, t.c, a, t_small, k, words, num_nodes, node_tok, parent, weight, pos_ids,
-                         mask);
+      hipLaunchKernelGGL((k_tree_fast<1024, 16>), dim3(B), dim3(1024), full.total, stream, taken, cont_len,
+                         cont_tok, ctx, L, S, k, m, t.c, a, lists + B, counts + 1, k, words, num_nodes, node_tok,
+                         parent, weight, pos_ids, mask);
       FC_CHECK_LAUNCH();
     }
     return FC_OK;

@@ -88,7 +88,7 @@ def test_retrieve_rejects_null_outputs_and_big_store(L):
 def _tree_args(B=1, L_=2, S=2, k=10, m=4, c=8, alpha=(1, 1, 0, 0)):
     one = ctypes.c_void_p(8)
     tp = fc.FcTreeParams(c, (ctypes.c_uint32 * 4)(*alpha))
-    return [one, one, one, one, B, L_, S, k, m, tp] + [one] * 6 + [None]
+    return [one, one, one, one, B, L_, S, k, m, tp] + [one] * 6 + [one, 1 << 20, None]
 
 
 @pytest.mark.parametrize("change,code", [
@@ -102,6 +102,16 @@ def test_build_tree_rejects(L, change, code):
         # check reads the device's limit, so it needs a GPU
         pytest.skip("LDS limit check queries the device")
     assert L.fc_build_tree(*_tree_args(**change)) == code
+
+
+def test_build_tree_rejects_missing_workspace(L):
+    args = _tree_args()
+    args[-2] = 8  # 4*(2B+2) = 16 needed
+    assert L.fc_build_tree(*args) == 2
+    args = _tree_args()
+    args[-3] = None
+    assert L.fc_build_tree(*args) == 2
+    assert L.fc_build_tree_workspace_bytes(1024) == 4 * 2050
 
 
 def test_verify_and_build_reject(L):
