@@ -18,6 +18,71 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return (uint64_t)__ballot(p); }
 
+// ---- DPP wave primitives (32-bit).  Within each row of 16 lanes values move
+// with DPP row shifts (plain VALU ops); rows are combined with readlane.
+// Lanes whose DPP source falls outside the row take the identity explicitly,
+// so the result does not depend on how out-of-row reads are filled.  Call
+// with the whole wave active.
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+
+constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+constexpr int kRowShl1 = 0x101, kRowShl2 = 0x102, kRowShl4 = 0x104, kRowShl8 = 0x108;
+
+// Inclusive prefix sum over the 64 lanes.
+__device__ __forceinline__ uint32_t wave_incl_sum_u32(uint32_t v) {
+  const int r = lane_id() & 15;
+  uint32_t x = v, y;
+  y = dpp_mov<kRowShr1>(x); x += r >= 1 ? y : 0u;
+  y = dpp_mov<kRowShr2>(x); x += r >= 2 ? y : 0u;
+  y = dpp_mov<kRowShr4>(x); x += r >= 4 ? y : 0u;
+  y = dpp_mov<kRowShr8>(x); x += r >= 8 ? y : 0u;
+  const uint32_t t0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 15);
+  const uint32_t t1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 31);
+  const uint32_t t2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 47);
+  const int row = lane_id() >> 4;
+  return x + (row == 0 ? 0u : row == 1 ? t0 : row == 2 ? t0 + t1 : t0 + t1 + t2);
+}
+
+// Sum over the 64 lanes (every lane gets it).
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+  const int r = lane_id() & 15;
+  uint32_t x = v, y;
+  y = dpp_mov<kRowShr1>(x); x += r >= 1 ? y : 0u;
+  y = dpp_mov<kRowShr2>(x); x += r >= 2 ? y : 0u;
+  y = dpp_mov<kRowShr4>(x); x += r >= 4 ? y : 0u;
+  y = dpp_mov<kRowShr8>(x); x += r >= 8 ? y : 0u;
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 15) + (uint32_t)__builtin_amdgcn_readlane((int)x, 31) +
+         (uint32_t)__builtin_amdgcn_readlane((int)x, 47) + (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+// Minimum over the lanes above this one (ident for lane 63); *total gets
+// the minimum over the whole wave.
+__device__ __forceinline__ uint32_t wave_excl_suffix_min_u32(uint32_t v, uint32_t ident, uint32_t* total) {
+  const int r = lane_id() & 15;
+  uint32_t x = v, y;
+  y = dpp_mov<kRowShl1>(x); x = (r <= 14 && y < x) ? y : x;
+  y = dpp_mov<kRowShl2>(x); x = (r <= 13 && y < x) ? y : x;
+  y = dpp_mov<kRowShl4>(x); x = (r <= 11 && y < x) ? y : x;
+  y = dpp_mov<kRowShl8>(x); x = (r <= 7 && y < x) ? y : x;
+  // x = minimum over lanes r..15 of this row
+  y = dpp_mov<kRowShl1>(x);
+  uint32_t ex = r <= 14 ? y : ident;  // lanes r+1..15 of this row
+  const uint32_t m1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 16);
+  const uint32_t m2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 32);
+  const uint32_t m3 = (uint32_t)__builtin_amdgcn_readlane((int)x, 48);
+  const uint32_t m0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 0);
+  const uint32_t t3 = m3, t2 = m2 < t3 ? m2 : t3, t1 = m1 < t2 ? m1 : t2;
+  const int row = lane_id() >> 4;
+  const uint32_t tail = row == 0 ? t1 : row == 1 ? t2 : row == 2 ? t3 : ident;
+  ex = tail < ex ? tail : ex;
+  *total = m0 < t1 ? m0 : t1;
+  return ex;
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_incl_sum(T v) {
   const int l = lane_id();
@@ -71,9 +136,15 @@ __device__ __forceinline__ T wave_min(T v) {
 // 1024).  scratch holds at least blockDim.x/64 + 1 entries.  Every thread of
 // the block must call it; it contains barriers.  *total receives the sum.
 template <typename T>
+__device__ __forceinline__ T wave_incl_sum_any(T v) {
+  if constexpr (sizeof(T) == 4) return (T)wave_incl_sum_u32((uint32_t)v);
+  else return wave_incl_sum(v);
+}
+
+template <typename T>
 __device__ __forceinline__ T block_excl_sum(T v, T* scratch, T* total) {
   const int nw = (int)(blockDim.x / kWave), w = (int)(threadIdx.x / kWave);
-  T inc = wave_incl_sum(v);
+  T inc = wave_incl_sum_any(v);
   if (lane_id() == kWave - 1) scratch[w] = inc;
   __syncthreads();
   if (threadIdx.x == 0) {

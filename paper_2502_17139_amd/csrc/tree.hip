@@ -406,8 +406,8 @@ struct Scan2 {
                              uint32_t* tz = nullptr) {
     constexpr int NW = NT / fc::kWave;
     const int w = (int)threadIdx.x / fc::kWave;
-    const uint32_t ix = fc::wave_incl_sum(x), iy = fc::wave_incl_sum(y);
-    const uint32_t iz = sz ? fc::wave_sum(z) : 0u;
+    const uint32_t ix = fc::wave_incl_sum_u32(x), iy = fc::wave_incl_sum_u32(y);
+    const uint32_t iz = sz ? fc::wave_sum_u32(z) : 0u;
     if (fc::lane_id() == fc::kWave - 1) {
       sx[w] = ix;
       sy[w] = iy;
@@ -646,25 +646,20 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     }
     uint32_t a_ex, dummy, a_tot, n_tot;
     Scan2<NT>::run(asum, nodes, s_x, s_y, &a_ex, &dummy, &a_tot, &n_tot, rw, s_z, &root_w);
-    // suffix minimum of f over later chunks (wave shuffles, then waves)
+    // first head after the chunk at every depth: minimum of f over later
+    // chunks (DPP within the wave, then over the later waves)
     uint16_t nh[MAXM + 1];
 #pragma unroll
     for (int d = 1; d <= MAXM; ++d) {
-      uint32_t v = f[d];
-      uint32_t inc = v;
-#pragma unroll
-      for (int off = 1; off < fc::kWave; off <<= 1) {
-        const uint32_t o = __shfl_down(inc, off, fc::kWave);
-        if (lane + off < fc::kWave && o < inc) inc = o;
-      }
-      uint32_t ex = __shfl_down(inc, 1, fc::kWave);
-      if (lane == fc::kWave - 1) ex = (uint32_t)T;
-      if (lane == 0) s_wmin[w][d] = (uint16_t)inc;
-      nh[d] = (uint16_t)ex;
+      if (d > m) break;  // uniform
+      uint32_t wave_min;
+      nh[d] = (uint16_t)fc::wave_excl_suffix_min_u32(f[d], (uint32_t)T, &wave_min);
+      if (lane == 0) s_wmin[w][d] = (uint16_t)wave_min;
     }
     __syncthreads();
 #pragma unroll
     for (int d = 1; d <= MAXM; ++d) {
+      if (d > m) break;
       uint32_t v = nh[d];
       for (int ww = w + 1; ww < NW; ++ww) v = s_wmin[ww][d] < v ? s_wmin[ww][d] : v;
       nh[d] = (uint16_t)v;
@@ -726,10 +721,10 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       }
 #pragma unroll
       for (int v = 0; v < 8; ++v) {
-        const uint32_t x = fc::wave_sum(r[v]);
+        const uint32_t x = fc::wave_sum_u32(r[v]);
         if (lane == 0 && x) atomicAdd(&s_hist[v], x);
       }
-      const uint32_t xb = fc::wave_sum(rbig);
+      const uint32_t xb = fc::wave_sum_u32(rbig);
       if (lane == 0 && xb) atomicAdd(&s_pick[2], xb);
     }
     __syncthreads();
@@ -745,7 +740,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
           cnt[u] = s_hist[255 - (lane * 4 + u)];
           lsum += cnt[u];
         }
-        const uint32_t incl = fc::wave_incl_sum(lsum);
+        const uint32_t incl = fc::wave_incl_sum_u32(lsum);
         const uint32_t before = incl - lsum;
         if (before < want && incl >= want) {
           uint32_t acc = before;
@@ -800,7 +795,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
             cnt[u] = s_hist[255 - (lane * 4 + u)];
             lsum += cnt[u];
           }
-          const uint32_t incl = fc::wave_incl_sum(lsum);
+          const uint32_t incl = fc::wave_incl_sum_u32(lsum);
           const uint32_t before = incl - lsum;
           if (before < remaining && incl >= remaining) {
             uint32_t acc = before;
