@@ -397,6 +397,35 @@ __global__ void __launch_bounds__(kTreeThreads) k_tree_any(const int32_t* __rest
 // the number of barriers per query small.
 // ---------------------------------------------------------------------------
 
+// Longest common prefix of two rows of `m` tokens (lengths la, lb), reading
+// the rows as 32-bit words: all word loads are independent, so the result
+// costs one LDS round trip instead of one per token.  Requires even m (rows
+// 4-byte aligned); tokens past a row's length are ignored.
+template <int MAXW>
+__device__ __forceinline__ int row_lcp_w(const uint16_t* a, int la, const uint16_t* b, int lb) {
+  const int n = la < lb ? la : lb;
+  const uint32_t* wa = (const uint32_t*)a;
+  const uint32_t* wb = (const uint32_t*)b;
+  int first = 2 * MAXW;
+#pragma unroll
+  for (int j = MAXW - 1; j >= 0; --j) {
+    if (2 * j < n) {
+      const uint32_t d = wa[j] ^ wb[j];
+      if (d) first = 2 * j + ((d & 0xFFFFu) == 0 ? 1 : 0);
+    }
+  }
+  return first < n ? first : n;
+}
+
+// Lexicographic comparison of two rows (a prefix first), word-wise.
+template <int MAXW>
+__device__ __forceinline__ int row_cmp_w(const uint16_t* a, int la, const uint16_t* b, int lb) {
+  const int x = row_lcp_w<MAXW>(a, la, b, lb);
+  const int n = la < lb ? la : lb;
+  if (x < n) return a[x] < b[x] ? -1 : 1;
+  return la < lb ? -1 : (la > lb ? 1 : 0);
+}
+
 template <int NT>
 struct Scan2 {
   // Exclusive prefix sums of (x, y) over the block plus their totals, and
@@ -539,6 +568,15 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
   }
   __syncthreads();
   const int T = T_raw;
+  const bool even_m = (m & 1) == 0;  // rows are 4-byte aligned in LDS
+  auto rcmp = [&](int i, int j) -> int {
+    return even_m ? row_cmp_w<MAXM / 2>(str + i * m, len[i], str + j * m, len[j])
+                  : str_cmp(str + i * m, len[i], str + j * m, len[j]);
+  };
+  auto rlcp = [&](int i, int j) -> int {
+    return even_m ? row_lcp_w<MAXM / 2>(str + i * m, len[i], str + j * m, len[j])
+                  : str_lcp(str + i * m, len[i], str + j * m, len[j]);
+  };
 
   // 1. load lengths and tokens (32-bit words when the rows are aligned)
   for (int i = tid; i < T; i += NT) {
@@ -566,9 +604,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
   // 2. precondition (each store's slots sorted) and merged order
   for (int i = tid; i < T; i += NT) {
     const int s = src_of(s_seg, S, i);
-    if (i > s_seg[s] && len[i - 1] <= m && len[i] <= m &&
-        str_cmp(str + (i - 1) * m, len[i - 1], str + i * m, len[i]) > 0)
-      s_err = 1;
+    if (i > s_seg[s] && len[i - 1] <= m && len[i] <= m && rcmp(i - 1, i) > 0) s_err = 1;
   }
   const int per = (T + NT - 1) / NT;
   const int p0 = tid * per < T ? tid * per : T;
@@ -584,14 +620,14 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
       const int jb = na + (p0 - mid - 1);
-      if (str_cmp(str + mid * m, len[mid], str + jb * m, len[jb]) <= 0) lo = mid + 1; else hi = mid;
+      if (rcmp(mid, jb) <= 0) lo = mid + 1; else hi = mid;
     }
     int ia = lo, ib = p0 - lo;
     for (int p = p0; p < p1; ++p) {
       bool take_a;
       if (ia >= na) take_a = false;
       else if (ib >= nb) take_a = true;
-      else take_a = str_cmp(str + ia * m, len[ia], str + (na + ib) * m, len[na + ib]) <= 0;
+      else take_a = rcmp(ia, na + ib) <= 0;
       perm[p] = (uint16_t)(take_a ? ia++ : na + ib++);
     }
   } else {
@@ -606,7 +642,8 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
         const int base = lo2;
         while (lo2 < hi2) {
           const int mid = (lo2 + hi2) >> 1;
-          const int cc = str_cmp(str + mid * m, len[mid], x, lx);
+          const int cc = even_m ? row_cmp_w<MAXM / 2>(str + mid * m, len[mid], x, lx)
+                                : str_cmp(str + mid * m, len[mid], x, lx);
           if (s2 < s ? (cc <= 0) : (cc < 0)) lo2 = mid + 1; else hi2 = mid;
         }
         mp += lo2 - base;
@@ -629,11 +666,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     for (int p = p1 - 1; p >= p0; --p) {
       const int i = perm[p];
       const int li = len[i];
-      int l = 0;
-      if (p > 0) {
-        const int i2 = perm[p - 1];
-        l = str_lcp(str + i2 * m, len[i2], str + i * m, li);
-      }
+      const int l = p > 0 ? rlcp(perm[p - 1], i) : 0;
       mlen[p] = (uint8_t)li;
       lcp[p] = (uint8_t)l;
       const uint32_t a = alpha_of(alpha, src_of(s_seg, S, i));
@@ -711,7 +744,10 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       for (int v = 0; v < 8; ++v) r[v] = 0;
       for (int p = p0; p < p1; ++p) {
         const uint32_t ap = wide ? A[p] : 0u;
-        for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
+        const int l = lcp[p], ml = mlen[p];
+#pragma unroll
+        for (int d = 1; d <= MAXM; ++d) {
+          if (d <= l || d > ml) continue;
           const uint32_t W = node_w(p, d, ap);
 #pragma unroll
           for (int v = 0; v < 8; ++v) r[v] += (W == (uint32_t)v);
@@ -825,7 +861,10 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     if (need > 0) {
       for (int p = p0; p < p1; ++p) {
         const uint32_t ap = wide ? A[p] : 0u;
-        for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
+        const int l = lcp[p], ml = mlen[p];
+#pragma unroll
+        for (int d = 1; d <= MAXM; ++d) {
+          if (d <= l || d > ml) continue;
           const uint32_t W = node_w(p, d, ap);
           gt += W > wstar;
           eq += W == wstar;
@@ -839,7 +878,10 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       uint32_t r = eq_ex;
       for (int p = p0; p < p1; ++p) {
         const uint32_t ap = wide ? A[p] : 0u;
-        for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
+        const int l = lcp[p], ml = mlen[p];
+#pragma unroll
+        for (int d = 1; d <= MAXM; ++d) {
+          if (d <= l || d > ml) continue;
           const uint32_t W = node_w(p, d, ap);
           bool keep = W > wstar;
           if (W == wstar) keep = r++ < take_eq;
