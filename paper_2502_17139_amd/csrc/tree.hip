@@ -514,6 +514,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
   __shared__ int s_err;
   __shared__ uint32_t s_x[NW + 1], s_y[NW + 1], s_z[NW + 1];
   __shared__ uint16_t s_wmin[NW][MAXM + 1];
+  __shared__ uint16_t s_wsuf[NW][MAXM + 1];
   __shared__ uint32_t s_hist[256];
   __shared__ uint32_t s_sel_w[FC_MAX_TREE_ROWS];
   __shared__ uint16_t s_sel_p[FC_MAX_TREE_ROWS];
@@ -568,6 +569,12 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
   }
   __syncthreads();
   const int T = T_raw;
+  // store boundaries in registers (no LDS round trip per lookup)
+  const int seg1 = s_seg[1 < S ? 1 : S], seg2 = s_seg[2 < S ? 2 : S], seg3 = s_seg[3 < S ? 3 : S];
+  auto store_of = [&](int i) -> int { return (S > 1 && i >= seg1) + (S > 2 && i >= seg2) + (S > 3 && i >= seg3); };
+  // with one weight for every store the alpha prefix sum is linear
+  const bool alpha_flat = (S < 2 || alpha.a[1] == alpha.a[0]) && (S < 3 || alpha.a[2] == alpha.a[0]) &&
+                          (S < 4 || alpha.a[3] == alpha.a[0]);
   const bool even_m = (m & 1) == 0;  // rows are 4-byte aligned in LDS
   auto rcmp = [&](int i, int j) -> int {
     return even_m ? row_cmp_w<MAXM / 2>(str + i * m, len[i], str + j * m, len[j])
@@ -603,8 +610,9 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
 
   // 2. precondition (each store's slots sorted) and merged order
   for (int i = tid; i < T; i += NT) {
-    const int s = src_of(s_seg, S, i);
-    if (i > s_seg[s] && len[i - 1] <= m && len[i] <= m && rcmp(i - 1, i) > 0) s_err = 1;
+    const int s = store_of(i);
+    const int first = s == 0 ? 0 : s == 1 ? seg1 : s == 2 ? seg2 : seg3;
+    if (i > first && len[i - 1] <= m && len[i] <= m && rcmp(i - 1, i) > 0) s_err = 1;
   }
   const int per = (T + NT - 1) / NT;
   const int p0 = tid * per < T ? tid * per : T;
@@ -669,7 +677,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       const int l = p > 0 ? rlcp(perm[p - 1], i) : 0;
       mlen[p] = (uint8_t)li;
       lcp[p] = (uint8_t)l;
-      const uint32_t a = alpha_of(alpha, src_of(s_seg, S, i));
+      const uint32_t a = alpha_of(alpha, store_of(i));
       asum += a;
       if (li > 0) rw += a;
       nodes += (uint32_t)(li - l);
@@ -684,25 +692,35 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     uint16_t nh[MAXM + 1];
 #pragma unroll
     for (int d = 1; d <= MAXM; ++d) {
-      if (d > m) break;  // uniform
-      uint32_t wave_min;
-      nh[d] = (uint16_t)fc::wave_excl_suffix_min_u32(f[d], (uint32_t)T, &wave_min);
+      uint32_t wave_min = (uint32_t)T;
+      if (d <= m) nh[d] = (uint16_t)fc::wave_excl_suffix_min_u32(f[d], (uint32_t)T, &wave_min);
       if (lane == 0) s_wmin[w][d] = (uint16_t)wave_min;
+    }
+    __syncthreads();
+    // one thread per (wave, depth): minimum over the later waves, every
+    // load issued before any is used
+    if (tid < NW * MAXM) {
+      const int w0 = tid / MAXM, d0 = tid % MAXM + 1;
+      uint32_t v = (uint32_t)T;
+#pragma unroll
+      for (int u = 0; u < NW; ++u) {
+        const uint32_t x = s_wmin[u][d0];
+        v = (u > w0 && x < v) ? x : v;
+      }
+      s_wsuf[w0][d0] = (uint16_t)v;
     }
     __syncthreads();
 #pragma unroll
     for (int d = 1; d <= MAXM; ++d) {
-      if (d > m) break;
-      uint32_t v = nh[d];
-      for (int ww = w + 1; ww < NW; ++ww) v = s_wmin[ww][d] < v ? s_wmin[ww][d] : v;
-      nh[d] = (uint16_t)v;
+      const uint32_t x = s_wsuf[w][d];
+      if (d <= m && x < nh[d]) nh[d] = (uint16_t)x;
     }
     // alpha prefix sums
     {
       uint32_t run = a_ex;
       for (int p = p0; p < p1; ++p) {
         A[p] = run;
-        run += alpha_of(alpha, src_of(s_seg, S, perm[p]));
+        run += alpha_of(alpha, store_of(perm[p]));
       }
       if (tid == 0) A[T] = a_tot;
     }
@@ -718,7 +736,9 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       const uint32_t aq = A[q];
 #pragma unroll
       for (int d = 1; d <= MAXM; ++d) {
-        if (d > l && d <= ml) E[q * m + d - 1] = wide ? nh[d] : (uint16_t)(A[nh[d]] - aq);
+        if (d > l && d <= ml)
+          E[q * m + d - 1] = wide ? nh[d] : alpha_flat ? (uint16_t)(alpha.a[0] * ((uint32_t)nh[d] - (uint32_t)q))
+                                                       : (uint16_t)(A[nh[d]] - aq);
         if (d > l) nh[d] = (uint16_t)q;
       }
     }
