@@ -89,12 +89,31 @@ fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint32_t* sa_ou
 fc_status fc_store_prepare(const uint16_t* tokens, const uint32_t* sa, uint64_t n, uint32_t* bucket_out,
                            hipStream_t stream);
 
+/*
+ * Optional two-token prefix table of a store (the same bucket idea one token
+ * deeper): for every pair (t0, u) with t0 < V and u in [0, V],
+ * pair_out[t0*(V+1) + u] = number of suffixes whose first two tokens sort
+ * below (t0, u), where u = 0 stands for "the suffix ends after t0" and
+ * u = t1 + 1 for a second token t1; the last entry, index V*(V+1), is n.
+ * A search for a pattern starting with (t0, t1) then starts from the range
+ * [pair[t0*(V+1)+t1+1], pair[t0*(V+1)+t1+2]) instead of the whole first-token
+ * bucket.  pair_out holds fc_pair_table_entries(V) entries (4.16 GB at
+ * V = 32256).  V must exceed every token of the store: the call checks it,
+ * which synchronises `stream`, and returns FC_ERR_INVALID otherwise (the
+ * table is then unspecified).  1 <= V <= 65536.
+ */
+uint64_t fc_pair_table_entries(uint32_t V);
+fc_status fc_store_prepare_pairs(const uint16_t* tokens, const uint32_t* sa, uint64_t n, uint32_t V,
+                                 uint32_t* pair_out, hipStream_t stream);
+
 /* A read-only view of one store; all pointers are device pointers. */
 typedef struct fc_store {
   const uint16_t* tokens; /* [n] text */
   const uint32_t* sa;     /* [n] suffix array of tokens */
   const uint32_t* bucket; /* [FC_BUCKETS] table from fc_store_prepare */
   uint64_t n;             /* tokens in the store, < 2^32 - 1 */
+  const uint32_t* pair;   /* optional two-token table from fc_store_prepare_pairs, or NULL */
+  uint32_t pair_vocab;    /* its V (ignored when pair is NULL) */
 } fc_store;
 
 /* ------------------------------------------------------------------------ */

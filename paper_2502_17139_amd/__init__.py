@@ -30,6 +30,7 @@ STATUS = {0: "FC_OK", 1: "FC_ERR_INVALID", 2: "FC_ERR_WORKSPACE", 3: "FC_ERR_DEV
 EXPORTS = (
     "fc_abi_version", "fc_status_string",
     "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_store_prepare",
+    "fc_pair_table_entries", "fc_store_prepare_pairs",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
     "fc_verify_accept",
 )
@@ -45,7 +46,7 @@ class FcError(RuntimeError):
 
 class FcStore(ctypes.Structure):
     _fields_ = [("tokens", ctypes.c_void_p), ("sa", ctypes.c_void_p), ("bucket", ctypes.c_void_p),
-                ("n", ctypes.c_uint64)]
+                ("n", ctypes.c_uint64), ("pair", ctypes.c_void_p), ("pair_vocab", ctypes.c_uint32)]
 
 
 class FcRetrieveParams(ctypes.Structure):
@@ -75,6 +76,10 @@ def lib() -> ctypes.CDLL:
     L.fc_datastore_build.argtypes = [vp, u64, vp, vp, sz, vp]
     L.fc_store_prepare.restype = ctypes.c_int
     L.fc_store_prepare.argtypes = [vp, vp, u64, vp, vp]
+    L.fc_pair_table_entries.restype = u64
+    L.fc_pair_table_entries.argtypes = [u32]
+    L.fc_store_prepare_pairs.restype = ctypes.c_int
+    L.fc_store_prepare_pairs.argtypes = [vp, vp, u64, u32, vp, vp]
     L.fc_retrieve_workspace_bytes.restype = sz
     L.fc_retrieve_workspace_bytes.argtypes = [i32, i32, FcRetrieveParams]
     L.fc_retrieve.restype = ctypes.c_int
@@ -146,21 +151,40 @@ def fc_store_prepare(tokens: torch.Tensor, sa: torch.Tensor, bucket_out: torch.T
     return bucket_out
 
 
+def fc_pair_table_entries(V: int) -> int:
+    return int(lib().fc_pair_table_entries(V))
+
+
+def fc_store_prepare_pairs(tokens: torch.Tensor, sa: torch.Tensor, V: int, pair_out: torch.Tensor | None = None,
+                           stream=None) -> torch.Tensor:
+    """Two-token prefix table (uint32[V*(V+1)+1]) of a store; V > every token."""
+    if pair_out is None:
+        pair_out = _empty(fc_pair_table_entries(V), torch.uint32, tokens.device)
+    _check("fc_store_prepare_pairs", lib().fc_store_prepare_pairs(_ptr(tokens), _ptr(sa), tokens.numel(), V,
+                                                                 _ptr(pair_out), _stream(stream)))
+    return pair_out
+
+
 class Store:
-    """A datastore resident on the GPU: tokens, suffix array, bucket table."""
+    """A datastore resident on the GPU: tokens, suffix array, bucket table and,
+    with pair_vocab = V, the optional two-token table."""
 
     def __init__(self, tokens: torch.Tensor, sa: torch.Tensor | None = None, bucket: torch.Tensor | None = None,
-                 stream=None):
+                 pair_vocab: int | None = None, stream=None):
         self.tokens = tokens
         self.sa = fc_datastore_build(tokens, stream=stream) if sa is None else sa
         self.bucket = fc_store_prepare(tokens, self.sa, stream=stream) if bucket is None else bucket
+        self.pair_vocab = pair_vocab or 0
+        self.pair = (fc_store_prepare_pairs(tokens, self.sa, pair_vocab, stream=stream)
+                     if pair_vocab else None)
 
     @property
     def n(self) -> int:
         return self.tokens.numel()
 
     def view(self) -> FcStore:
-        return FcStore(self.tokens.data_ptr(), self.sa.data_ptr(), self.bucket.data_ptr(), self.n)
+        return FcStore(self.tokens.data_ptr(), self.sa.data_ptr(), self.bucket.data_ptr(), self.n,
+                       None if self.pair is None else self.pair.data_ptr(), self.pair_vocab)
 
 
 # ------------------------------------------------------------ retrieval ----

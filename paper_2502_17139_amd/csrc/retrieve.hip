@@ -9,9 +9,10 @@
 // triples - 2 stores x 15 lengths x {lower, upper} = 60 lanes at the paper's
 // n_max = 16, n_min = 2 - so every candidate length is searched at once and
 // the dependent probe chain is one binary search long instead of fifteen.
-// Each search starts from the first-token bucket of the store (one table
-// read replaces the top ~15 levels of the search) and compares from the
-// second token on.  The wave then keeps, per store, the longest n whose range
+// Each search starts from the store's two-token table when it has one (one
+// table read replaces the top ~25 levels of the search on a 1B-token store)
+// or else from its first-token bucket, and compares only the tokens the
+// table does not already fix.  The wave then keeps, per store, the longest n whose range
 // is non-empty and fills the k slots in store priority order.
 //
 // k_offsets + k_gather: the kept slots of the whole batch are numbered
@@ -39,19 +40,21 @@ struct StoreArgs {
   const uint16_t* tok[FC_MAX_SOURCES];
   const uint32_t* sa[FC_MAX_SOURCES];
   const uint32_t* bucket[FC_MAX_SOURCES];
+  const uint32_t* pair[FC_MAX_SOURCES];
   uint32_t n[FC_MAX_SOURCES];
+  uint32_t pair_vocab[FC_MAX_SOURCES];
 };
 
-// Suffix j against pattern q[0..n), knowing token 0 already matches: -1 below
+// Suffix j against pattern q[0..n), knowing tokens before `from` match: -1 below
 // (a suffix that ends first is below), 0 starts with q, +1 above.  Tokens are
 // fetched in two batches of independent loads (1..8, then 9..15 only when the
 // first eight all match), so a probe costs one memory round trip in the
 // common case instead of a chain of dependent loads.
 __device__ __forceinline__ int cmp_suffix(const uint16_t* __restrict__ T, uint32_t N, uint32_t j,
-                                          const uint16_t* q, int n) {
+                                          const uint16_t* q, int n, int from) {
   constexpr int kBatch = 8;
   uint16_t t[kBatch];
-  for (int x0 = 1; x0 < n; x0 += kBatch) {
+  for (int x0 = from; x0 < n; x0 += kBatch) {
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const uint64_t p = (uint64_t)j + (uint64_t)(x0 + u);
@@ -116,14 +119,27 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
       const uint32_t* SA = st.sa[s];
       const uint32_t N = st.n[s];
       uint32_t lo = 0, hi = 0;
+      int from = 1;
       if (N > 0) {
-        lo = st.bucket[s][q[0]];
-        hi = st.bucket[s][q[0] + 1];
+        const uint32_t V = st.pair_vocab[s];
+        if (n >= 2 && st.pair[s] != nullptr && q[0] < V && q[1] < V) {
+          // two-token table: the range of suffixes starting with q[0] q[1]
+          const uint64_t idx = (uint64_t)q[0] * (V + 1) + q[1] + 1;
+          lo = st.pair[s][idx];
+          hi = st.pair[s][idx + 1];
+          from = 2;
+        } else if (n >= 2 && st.pair[s] != nullptr) {
+          hi = lo = 0;  // a token >= V cannot occur in the store
+        } else {
+          lo = st.bucket[s][q[0]];
+          hi = st.bucket[s][q[0] + 1];
+        }
       }
       // Binary search; the suffix-array entries of both possible next
       // midpoints are fetched together with the current probe's text, so
-      // each level costs one dependent round trip.
-      if (lo < hi) {
+      // each level costs one dependent round trip.  When the table already
+      // covers the whole pattern the range is final.
+      if (from < n && lo < hi) {
         uint32_t mid = lo + ((hi - lo) >> 1);
         uint32_t j = SA[mid];
         for (;;) {
@@ -131,7 +147,7 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
           const uint32_t rmid = (mid + 1) + ((hi - mid - 1) >> 1);
           const uint32_t jl = lo < mid ? SA[lmid] : 0u;
           const uint32_t jr = mid + 1 < hi ? SA[rmid] : 0u;
-          const int c = cmp_suffix(T, N, j, q, n);
+          const int c = cmp_suffix(T, N, j, q, n, from);
           if (upper ? (c <= 0) : (c < 0)) {
             lo = mid + 1;
             mid = rmid;
@@ -143,6 +159,8 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
           }
           if (lo >= hi) break;
         }
+      } else if (upper) {
+        lo = hi;  // range already final: its end is the upper bound
       }
       if (upper) s_hi[w][s][ni] = lo; else s_lo[w][s][ni] = lo;
     }
@@ -368,6 +386,9 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
     st.sa[s] = x.sa;
     st.bucket[s] = x.bucket;
     st.n[s] = (uint32_t)x.n;
+    st.pair[s] = x.pair;
+    st.pair_vocab[s] = x.pair ? x.pair_vocab : 0u;
+    if (x.pair && (x.pair_vocab < 1 || x.pair_vocab > 65536)) return FC_ERR_INVALID;
   }
   if (B == 0) return FC_OK;
   if (!ctx || !match_n || !range_lo || !range_cnt || !taken || !cont_pos || !cont_src || !cont_len || !cont_tok)

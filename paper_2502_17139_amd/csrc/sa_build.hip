@@ -382,6 +382,53 @@ __global__ void __launch_bounds__(256) k_bucket(const uint16_t* __restrict__ tok
   bucket[t] = lo;
 }
 
+// Largest token of a store, for the pair-table precondition (out[0] starts
+// at 0).
+__global__ void __launch_bounds__(256) k_max_token(const uint16_t* __restrict__ tok, uint32_t n,
+                                                   uint32_t* __restrict__ out) {
+  uint32_t mx = 0;
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    mx = tok[i] > mx ? tok[i] : mx;
+  mx = fc::wave_max(mx);
+  if (fc::lane_id() == 0 && mx) atomicMax(out, mx);
+}
+
+// Two-token table: suffix-array position r owns the table entries between
+// the previous suffix's pair key (exclusive) and its own (inclusive); keys
+// never decrease along the suffix array.  r = n owns the rest up to the
+// final entry.  Each wave takes 64 consecutive positions and writes their
+// ranges one after another with all 64 lanes, so long ranges are written
+// in coalesced runs.
+__global__ void __launch_bounds__(256) k_pairs(const uint16_t* __restrict__ tok, const uint32_t* __restrict__ sa,
+                                               uint32_t n, uint32_t V, uint32_t* __restrict__ pair) {
+  const uint64_t base = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) & ~(uint64_t)(fc::kWave - 1);
+  const int lane = fc::lane_id();
+  if (base > n) return;  // whole wave
+  const uint64_t end = (uint64_t)V * (V + 1);
+  auto key = [&](uint64_t rr) -> uint64_t {
+    if (rr >= n) return end;
+    const uint32_t j = sa[rr];
+    const uint64_t t0 = tok[j];
+    const uint64_t u = (uint64_t)j + 1 < n ? (uint64_t)tok[j + 1] + 1 : 0;
+    const uint64_t k = t0 * (V + 1) + u;
+    return k < end ? k : end;  // tokens >= V were rejected before launch
+  };
+  const uint64_t r = base + lane;
+  uint64_t hi = 0, lo = 1;  // empty unless r <= n
+  if (r <= n) {
+    hi = key(r);
+    lo = r == 0 ? 0 : key(r - 1) + 1;
+  }
+  for (int jl = 0; jl < fc::kWave; ++jl) {
+    const uint64_t l2 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(lo >> 32), jl) << 32) |
+                        (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)lo, jl);
+    const uint64_t h2 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(hi >> 32), jl) << 32) |
+                        (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)hi, jl);
+    const uint32_t val = (uint32_t)(base + jl);
+    for (uint64_t k = l2 + lane; k <= h2; k += fc::kWave) pair[k] = val;
+  }
+}
+
 struct BuildWs {
   uint32_t* rank;
   uint64_t* keys[2];
@@ -528,6 +575,35 @@ extern "C" fc_status fc_store_prepare(const uint16_t* tokens, const uint32_t* sa
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_bucket, dim3(fc::div_up(FC_BUCKETS, 256)), dim3(256), 0, stream, tokens, sa, (uint32_t)n,
                      bucket_out);
+  FC_CHECK_LAUNCH();
+  return FC_OK;
+}
+
+extern "C" uint64_t fc_pair_table_entries(uint32_t V) { return (uint64_t)V * ((uint64_t)V + 1) + 1; }
+
+extern "C" fc_status fc_store_prepare_pairs(const uint16_t* tokens, const uint32_t* sa, uint64_t n, uint32_t V,
+                                            uint32_t* pair_out, hipStream_t stream) {
+  if (n >= 0xFFFFFFFFull || !pair_out || V < 1 || V > 65536) return FC_ERR_INVALID;
+  if (n > 0 && (!tokens || !sa)) return FC_ERR_INVALID;
+  (void)hipGetLastError();
+  if (n > 0) {
+    // precondition: every token < V (pair_out[0] serves as the reduction cell)
+    FC_CHECK_HIP(hipMemsetAsync(pair_out, 0, sizeof(uint32_t), stream));
+    const uint32_t blocks = fc::div_up(n, 256) < 4096u ? fc::div_up(n, 256) : 4096u;
+    hipLaunchKernelGGL(k_max_token, dim3(blocks), dim3(256), 0, stream, tokens, (uint32_t)n, pair_out);
+    FC_CHECK_LAUNCH();
+    uint32_t mx = 0;
+    FC_CHECK_HIP(hipMemcpyAsync(&mx, pair_out, sizeof(uint32_t), hipMemcpyDeviceToHost, stream));
+    FC_CHECK_HIP(hipStreamSynchronize(stream));
+    if (mx >= V) return FC_ERR_INVALID;
+  }
+  if (n == 0) {  // every entry is 0
+    FC_CHECK_HIP(hipMemsetAsync(pair_out, 0, sizeof(uint32_t) * fc_pair_table_entries(V), stream));
+    return FC_OK;
+  }
+  const uint64_t threads = n + 1;
+  hipLaunchKernelGGL(k_pairs, dim3((uint32_t)((threads + 255) / 256)), dim3(256), 0, stream, tokens, sa,
+                     (uint32_t)n, V, pair_out);
   FC_CHECK_LAUNCH();
   return FC_OK;
 }

@@ -51,7 +51,7 @@ def test_workspace_sizes(L):
 
 
 def _retrieve_args(S=1, B=1, L_=4, p=(16, 2, 5000, 10), ws_bytes=0):
-    views = (fc.FcStore * 4)(*[fc.FcStore(1, 1, 1, 10) for _ in range(4)])
+    views = (fc.FcStore * 4)(*[fc.FcStore(1, 1, 1, 10, None, 0) for _ in range(4)])
     one = ctypes.c_void_p(8)
     return [views, S, one, B, L_, fc.FcRetrieveParams(*p)] + [one] * 8 + [None, ws_bytes, None]
 
@@ -76,11 +76,14 @@ def test_retrieve_rejects_null_outputs_and_big_store(L):
     args = _retrieve_args()
     args[6] = None  # match_n
     assert L.fc_retrieve(*args) == 1
-    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 1 << 32))
+    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 1 << 32, None, 0))
     args = _retrieve_args()
     args[0] = views
     assert L.fc_retrieve(*args) == 1
-    views = (fc.FcStore * 1)(fc.FcStore(1, None, 1, 10))
+    views = (fc.FcStore * 1)(fc.FcStore(1, None, 1, 10, None, 0))
+    args[0] = views
+    assert L.fc_retrieve(*args) == 1
+    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, 1, 70000))  # pair vocabulary out of range
     args[0] = views
     assert L.fc_retrieve(*args) == 1
 
@@ -112,6 +115,16 @@ def test_build_tree_rejects_missing_workspace(L):
     args[-3] = None
     assert L.fc_build_tree(*args) == 2
     assert L.fc_build_tree_workspace_bytes(1024) == 4 * 2050
+
+
+def test_pair_table_size_and_rejects(L):
+    assert L.fc_pair_table_entries(32256) == 32256 * 32257 + 1
+    assert L.fc_pair_table_entries(3) == 13
+    one = ctypes.c_void_p(8)
+    assert L.fc_store_prepare_pairs(one, one, 10, 0, one, None) == 1
+    assert L.fc_store_prepare_pairs(one, one, 10, 65537, one, None) == 1
+    assert L.fc_store_prepare_pairs(one, one, 10, 5, None, None) == 1
+    assert L.fc_store_prepare_pairs(None, one, 10, 5, one, None) == 1
 
 
 def test_verify_and_build_reject(L):

@@ -112,16 +112,44 @@ def test_bucket_table():
         assert (b == want).all()
 
 
+def _pair_table_expected(t: np.ndarray, V: int) -> np.ndarray:
+    """Number of suffixes whose first two tokens sort below each (t0, u),
+    by counting 2-prefix keys of every suffix (u = 0: suffix of length 1)."""
+    n = len(t)
+    t0 = t.astype(np.int64)
+    u = np.zeros(n, np.int64)
+    u[:-1] = t0[1:] + 1
+    keys = t0 * (V + 1) + u
+    counts = np.bincount(keys, minlength=V * (V + 1))
+    return np.concatenate([[0], np.cumsum(counts)])
+
+
+def test_pair_table():
+    for seed, (n, V) in enumerate([(1, 3), (2, 3), (500, 5), (5000, 40), (70000, 300)]):
+        t = synth.random_text(50 + seed, n, V, 0.05)
+        say(f"pair table n={n} V={V}")
+        st = gpu_store(t, pair_vocab=V)
+        torch.cuda.synchronize()
+        assert (host(st.pair).astype(np.int64) == _pair_table_expected(t, V)).all()
+    # a larger vocabulary than needed is fine; a smaller one is rejected
+    t = synth.random_text(9, 3000, 50, 0.05)
+    st = gpu_store(t, pair_vocab=64)
+    assert (host(st.pair).astype(np.int64) == _pair_table_expected(t, 64)).all()
+    with pytest.raises(fc.FcError, match="INVALID"):
+        fc.fc_store_prepare_pairs(st.tokens, st.sa, 49)
+
+
 # --------------------------------------------------------------- retrieval --
 
 def test_first_workload_full_batch():
     t = synth.store(1, "single")
     ctx = synth.queries(1)
     st = gpu_store(t)
+    st_pairs = fc.Store(st.tokens, st.sa, st.bucket, pair_vocab=synth.VOCAB)
     for (k, m, c) in ((P["k"], P["m"], P["c"]), (1000, 10, 64), (257, 3, 5), (1, 1, 1)):
         say(f"workload 1: k={k} m={m} c={c}")
         p = dict(P, k=k, m=m)
-        g = gpu_pipeline([st], ctx, p, (1,), c)
+        g = gpu_pipeline([st_pairs if k == P["k"] else st], ctx, p, (1,), c)
         o = oracle_pipeline([t], ctx, p, (1,), c)
         compare_retrieve(g, o)
         compare_tree(g, o)
@@ -131,7 +159,7 @@ def test_first_workload_full_batch():
 def test_two_store_workload_full_batch():
     tp, tg = synth.store(2, "project"), synth.store(2, "general")
     ctx = synth.queries(2)
-    stores = [gpu_store(tp), gpu_store(tg)]
+    stores = [gpu_store(tp, synth.VOCAB), gpu_store(tg, synth.VOCAB)]
     say("workload 2: gpu")
     g = gpu_pipeline(stores, ctx, P, (1, 1), P["c"])
     say("workload 2: oracle")
@@ -139,7 +167,8 @@ def test_two_store_workload_full_batch():
     compare_retrieve(g, o)
     compare_tree(g, o)
     _check_accept(g, o, P["m"])
-    # unequal store weights
+    # unequal store weights, first-token tables only
+    stores = [fc.Store(x.tokens, x.sa, x.bucket) for x in stores]
     g = gpu_pipeline(stores, ctx[:64], P, (3, 1), 32)
     o = oracle_pipeline([tp, tg], ctx[:64], P, (3, 1), 32)
     compare_tree(g, o)
@@ -152,7 +181,7 @@ def test_headline_workload_sampled():
     tp, tg = synth.store(3, "project"), synth.store(3, "general")
     ctx = synth.queries(3)
     say("headline: building suffix arrays")
-    stores = [gpu_store(tp), gpu_store(tg)]
+    stores = [gpu_store(tp, synth.VOCAB), gpu_store(tg, synth.VOCAB)]
     torch.cuda.synchronize()
     say("headline: checking suffix arrays")
     for t, st in zip((tp, tg), stores):
@@ -185,7 +214,8 @@ def test_fuzz_small_stores(seed):
     texts = [synth.random_text(100 * seed + s, int(rng.integers(0, 6000)), vocab, 0.02) for s in range(S)]
     if seed == 0:
         texts[0] = np.zeros(0, np.uint16)  # an empty store
-    stores = [gpu_store(t) if len(t) else fc.Store(dev(np.zeros(1, np.uint16))[:0],
+    pv = vocab if seed % 2 else None
+    stores = [gpu_store(t, pv) if len(t) else fc.Store(dev(np.zeros(1, np.uint16))[:0],
                                                     dev(np.zeros(1, np.uint32))[:0],
                                                     fc.fc_store_prepare(dev(np.zeros(1, np.uint16))[:0],
                                                                         dev(np.zeros(1, np.uint32))[:0]))
