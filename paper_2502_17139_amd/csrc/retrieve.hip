@@ -8,7 +8,7 @@
 // k_search: one wave per query.  The wave's lanes take the (store, n, bound)
 // triples - 2 stores x 15 lengths x {lower, upper} = 60 lanes at the paper's
 // n_max = 16, n_min = 2 - so every candidate length is searched at once and
-// the dependent probe chain is one search long instead of fifteen.
+// the dependent probe chain is one binary search long instead of fifteen.
 // Each search starts from the store's two-token table when it has one (one
 // table read replaces the top ~25 levels of the search on a 1B-token store)
 // or else from its first-token bucket, and compares only the tokens the
@@ -46,107 +46,34 @@ struct StoreArgs {
 };
 
 // Suffix j against pattern q[0..n), knowing tokens before `from` match: -1 below
-// (a suffix that ends first is below), 0 starts with q, +1 above.  The
-// tokens j+from .. j+n-1 (at most 15) are fetched as eight 32-bit words
-// from the aligned word at or before j+from, all loads independent, so a
-// probe costs one memory round trip; near the end of the store single
-// tokens are read instead.
+// (a suffix that ends first is below), 0 starts with q, +1 above.  Tokens are
+// fetched in two batches of independent loads (1..8, then 9..15 only when the
+// first eight all match), so a probe costs one memory round trip in the
+// common case instead of a chain of dependent loads.
 __device__ __forceinline__ int cmp_suffix(const uint16_t* __restrict__ T, uint32_t N, uint32_t j,
-                                          const uint16_t* q, int n, int from, bool words) {
-  const uint64_t p0 = (uint64_t)j + (uint64_t)from;
-  const uint64_t w0 = p0 >> 1;
-  const bool odd = (p0 & 1) != 0;
-  // tokens 2*w0 .. 2*w0+15 packed two per word
-  uint32_t w_0, w_1, w_2, w_3, w_4, w_5, w_6, w_7;
-  if (words && 2 * (w0 + 8) <= N) {
-    const uint32_t* W = (const uint32_t*)T + w0;
-    w_0 = W[0]; w_1 = W[1]; w_2 = W[2]; w_3 = W[3];
-    w_4 = W[4]; w_5 = W[5]; w_6 = W[6]; w_7 = W[7];
-  } else {
-    auto tk = [&](uint64_t p) -> uint32_t { return p < N ? (uint32_t)T[p] : 0u; };
-    const uint64_t b = 2 * w0;
-    w_0 = tk(b + 0) | (tk(b + 1) << 16); w_1 = tk(b + 2) | (tk(b + 3) << 16);
-    w_2 = tk(b + 4) | (tk(b + 5) << 16); w_3 = tk(b + 6) | (tk(b + 7) << 16);
-    w_4 = tk(b + 8) | (tk(b + 9) << 16); w_5 = tk(b + 10) | (tk(b + 11) << 16);
-    w_6 = tk(b + 12) | (tk(b + 13) << 16); w_7 = tk(b + 14) | (tk(b + 15) << 16);
-  }
-  // token u of the window (u = 0..15)
-  auto tok_at = [&](int u) -> uint32_t {
-    const uint32_t wv = u < 2 ? w_0 : u < 4 ? w_1 : u < 6 ? w_2 : u < 8 ? w_3 : u < 10 ? w_4 : u < 12 ? w_5
-                      : u < 14 ? w_6 : w_7;
-    return (u & 1) ? (wv >> 16) : (wv & 0xFFFFu);
-  };
+                                          const uint16_t* q, int n, int from) {
+  constexpr int kBatch = 8;
+  uint16_t t[kBatch];
+  for (int x0 = from; x0 < n; x0 += kBatch) {
 #pragma unroll
-  for (int u = 0; u < 15; ++u) {
-    const int x = from + u;
-    if (x >= n) return 0;
-    if (p0 + (uint64_t)u >= N) return -1;
-    const uint32_t a = odd ? tok_at(u + 1) : tok_at(u);
-    const uint32_t b = q[x];
-    if (a != b) return a < b ? -1 : 1;
+    for (int u = 0; u < kBatch; ++u) {
+      const uint64_t p = (uint64_t)j + (uint64_t)(x0 + u);
+      t[u] = (x0 + u < n && p < N) ? T[p] : (uint16_t)0;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int x = x0 + u;
+      if (x >= n) return 0;
+      if ((uint64_t)j + (uint64_t)x >= N) return -1;
+      const uint16_t b = q[x];
+      if (t[u] != b) return t[u] < b ? -1 : 1;
+    }
   }
   return 0;
 }
 
-// First position in [lo, hi) where pred fails (pred: the suffix sorts below
-// the pattern, or for the upper bound below-or-equal; true then false along
-// the range), by a 4-ary search: each level probes the three quartile
-// points at once and, in the same memory round trip, fetches the
-// suffix-array entries of the quartile points of all four possible next
-// ranges, so a level costs one dependent round trip and the range shrinks
-// fourfold.
-__device__ __forceinline__ uint32_t search4(const uint16_t* __restrict__ T, const uint32_t* __restrict__ SA,
-                                            uint32_t N, const uint16_t* q, int n, int from, bool upper, bool words,
-                                            uint32_t lo, uint32_t hi) {
-  auto quart = [](uint32_t a, uint32_t b, int i) -> uint32_t {
-    return a + (uint32_t)(((uint64_t)(b - a) * (uint64_t)i) >> 2);
-  };
-  uint32_t j1 = 0, j2 = 0, j3 = 0;
-  if (lo < hi) {
-    j1 = SA[quart(lo, hi, 1)];
-    j2 = SA[quart(lo, hi, 2)];
-    j3 = SA[quart(lo, hi, 3)];
-  }
-  while (lo < hi) {
-    const uint32_t p1 = quart(lo, hi, 1), p2 = quart(lo, hi, 2), p3 = quart(lo, hi, 3);
-    // the four candidate next ranges and their quartile points' entries
-    const uint32_t a0 = lo, b0 = p1, a1 = p1 + 1, b1 = p2, a2 = p2 + 1, b2 = p3, a3 = p3 + 1, b3 = hi;
-    auto sa_at = [&](uint32_t a, uint32_t b, int i) -> uint32_t { return a < b ? SA[quart(a, b, i)] : 0u; };
-    const uint32_t n01 = sa_at(a0, b0, 1), n02 = sa_at(a0, b0, 2), n03 = sa_at(a0, b0, 3);
-    const uint32_t n11 = sa_at(a1, b1, 1), n12 = sa_at(a1, b1, 2), n13 = sa_at(a1, b1, 3);
-    const uint32_t n21 = sa_at(a2, b2, 1), n22 = sa_at(a2, b2, 2), n23 = sa_at(a2, b2, 3);
-    const uint32_t n31 = sa_at(a3, b3, 1), n32 = sa_at(a3, b3, 2), n33 = sa_at(a3, b3, 3);
-    const int c1 = cmp_suffix(T, N, j1, q, n, from, words);
-    const int c2 = cmp_suffix(T, N, j2, q, n, from, words);
-    const int c3 = cmp_suffix(T, N, j3, q, n, from, words);
-    const bool t1 = upper ? c1 <= 0 : c1 < 0;
-    const bool t2 = upper ? c2 <= 0 : c2 < 0;
-    const bool t3 = upper ? c3 <= 0 : c3 < 0;
-    int c;
-    if (!t1) {
-      c = 0;
-      hi = b0;
-    } else if (!t2) {
-      c = 1;
-      lo = a1;
-      hi = b1;
-    } else if (!t3) {
-      c = 2;
-      lo = a2;
-      hi = b2;
-    } else {
-      c = 3;
-      lo = a3;
-    }
-    j1 = c == 0 ? n01 : c == 1 ? n11 : c == 2 ? n21 : n31;
-    j2 = c == 0 ? n02 : c == 1 ? n12 : c == 2 ? n22 : n32;
-    j3 = c == 0 ? n03 : c == 1 ? n13 : c == 2 ? n23 : n33;
-  }
-  return lo;
-}
-
 __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, const uint16_t* __restrict__ ctx,
-                                                           int B, int L, int n_max, int n_min, int k, int words_i,
+                                                           int B, int L, int n_max, int n_min, int k,
                                                            int32_t* __restrict__ match_n,
                                                            uint32_t* __restrict__ range_lo,
                                                            uint32_t* __restrict__ range_cnt,
@@ -176,7 +103,6 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
   }
   __syncthreads();
 
-  const bool words = words_i != 0;
   const int NN = n_max - n_min + 1;
   const int tasks = S * NN * 2;
   if (active) {
@@ -209,9 +135,33 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
           hi = st.bucket[s][q[0] + 1];
         }
       }
-      // When the table already covers the whole pattern the range is final.
-      if (from < n && lo < hi) lo = search4(T, SA, N, q, n, from, upper != 0, words, lo, hi);
-      else if (upper) lo = hi;
+      // Binary search; the suffix-array entries of both possible next
+      // midpoints are fetched together with the current probe's text, so
+      // each level costs one dependent round trip.  When the table already
+      // covers the whole pattern the range is final.
+      if (from < n && lo < hi) {
+        uint32_t mid = lo + ((hi - lo) >> 1);
+        uint32_t j = SA[mid];
+        for (;;) {
+          const uint32_t lmid = lo + ((mid - lo) >> 1);
+          const uint32_t rmid = (mid + 1) + ((hi - mid - 1) >> 1);
+          const uint32_t jl = lo < mid ? SA[lmid] : 0u;
+          const uint32_t jr = mid + 1 < hi ? SA[rmid] : 0u;
+          const int c = cmp_suffix(T, N, j, q, n, from);
+          if (upper ? (c <= 0) : (c < 0)) {
+            lo = mid + 1;
+            mid = rmid;
+            j = jr;
+          } else {
+            hi = mid;
+            mid = lmid;
+            j = jl;
+          }
+          if (lo >= hi) break;
+        }
+      } else if (upper) {
+        lo = hi;  // range already final: its end is the upper bound
+      }
       if (upper) s_hi[w][s][ni] = lo; else s_lo[w][s][ni] = lo;
     }
   }
@@ -445,15 +395,15 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
     return FC_ERR_INVALID;
   if (!ws || ws_bytes < fc_retrieve_workspace_bytes(B, S, p)) return FC_ERR_WORKSPACE;
   (void)hipGetLastError();
-  int words = 1;  // 32-bit text loads when every store's tokens are 4-byte aligned
-  for (int s = 0; s < S; ++s) words &= (((uintptr_t)st.tok[s]) & 3) == 0;
   hipLaunchKernelGGL(k_search, dim3(fc::div_up(B, kQueriesPerBlock)), dim3(kSearchThreads), 0, stream, st, S, ctx,
-                     B, L, p.n_max, p.n_min, p.k, words, match_n, range_lo, range_cnt, taken);
+                     B, L, p.n_max, p.n_min, p.k, match_n, range_lo, range_cnt, taken);
   FC_CHECK_LAUNCH();
   if (p.m <= 16) {
     uint32_t* offsets = (uint32_t*)ws;
     hipLaunchKernelGGL(k_offsets, dim3(1), dim3(kScanThreads), 0, stream, taken, B, S, offsets);
     FC_CHECK_LAUNCH();
+    int words = 1;
+    for (int s = 0; s < S; ++s) words &= (((uintptr_t)st.tok[s]) & 3) == 0;
     const uint64_t want = ((uint64_t)B * p.k + kGatherThreads - 1) / kGatherThreads;
     const uint32_t blocks = (uint32_t)(want < (uint64_t)kGatherBlocks ? want : (uint64_t)kGatherBlocks);
     if (p.m <= 10)
