@@ -29,7 +29,7 @@ if ROOT not in sys.path:
 import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
-WORKLOADS = {"headline": 3, "two-store": 2, "single": 1}
+WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "build": 3}
 
 
 def log(*a):
@@ -134,6 +134,10 @@ def main():
     import paper_2502_17139_amd as fc
     import synth
 
+    if args.workload == "replay":
+        return run_replay(args)
+    if args.workload == "build":
+        return run_build(args)
     cfg = WORKLOADS[args.workload]
     p = dict(synth.PARAMS)
     c, alpha = p["c"], tuple(p["alpha"])
@@ -260,6 +264,86 @@ def main():
         "slots_kept_mean": float(taken.sum(axis=1).mean()),
         "sa_build_s": build_s,
         "wall_s_timed": wall,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def run_replay(args):
+    """Decode-trace replay: 128 streams of 4096 tokens drawn like the 10M-token
+    project store, over the 10M + 1B stores, up to 512 steps, LRU(32)."""
+    import torch
+    import paper_2502_17139_amd as fc
+    from paper_2502_17139_amd.replay import GpuReplay
+    import synth
+
+    p = dict(synth.PARAMS)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    texts = [synth.store(3, r) for r in synth.store_roles(3)]
+    stores = [fc.Store(torch.from_numpy(t).to(dev), pair_vocab=synth.VOCAB) for t in texts]
+    truth = synth.truth()
+    rp = GpuReplay(stores, truth, **p)
+    rp.run(max_steps=args.warmup)  # warm-up steps, then a fresh replay is timed
+    rp.reset()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    res = rp.run(max_steps=512)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    live = res["accept"] >= 0
+    tokens = int(res["accept"][live].sum())
+    line = {
+        "metric": "decode-trace replay steps/sec (128 streams; retrieve + tree + accept per step)",
+        "value": res["steps"] / wall, "unit": "steps/s", "n_gpus": 1, "steps": res["steps"], "warmup": args.warmup,
+        "ms_per_step": 1e3 * wall / max(res["steps"], 1), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u16/u32 (integer)",
+        "data": "synthetic (seeded streams from the project pool; no dataset)",
+        "config": {"workload": "replay over project 10M + general 1B", "streams": int(truth.shape[0]),
+                   "stream_len": int(truth.shape[1]), "lru": 32, **{kk: p[kk] for kk in ("n_max", "n_min", "k", "m", "c")}},
+        "roofline": None,
+        "accepted_tokens_per_s": tokens / wall,
+        "acc_len": res["acc_len"],
+        "lru_hit_rate": float(res["hits"].sum() / max(res["lookups"].sum(), 1)),
+        "retrievals": int(res["lookups"].sum() - res["hits"].sum()),
+    }
+    print(json.dumps(line), flush=True)
+
+
+def run_build(args):
+    """Suffix-array construction of the 1B-token general store and the
+    10M-token project store (plus both stores' first-token tables)."""
+    import torch
+    import paper_2502_17139_amd as fc
+    import synth
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    out = {}
+    for role in ("project", "general"):
+        t = synth.store(3, role)
+        tok = torch.from_numpy(t).to(dev)
+        sa = torch.empty(len(t), dtype=torch.uint32, device=dev)
+        ws = torch.empty(fc.fc_datastore_build_workspace_bytes(len(t)), dtype=torch.uint8, device=dev)
+        times = []
+        for i in range(max(args.warmup, 1) + args.steps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fc.fc_datastore_build(tok, sa_out=sa, workspace=ws)
+            torch.cuda.synchronize()
+            if i >= max(args.warmup, 1):
+                times.append(time.perf_counter() - t0)
+        sec = float(np.median(times))
+        n = len(t)
+        # floor traffic of any build: read the text, write the array
+        out[role] = {"tokens": n, "seconds": sec, "floor_GBps": (2 * n + 4 * n) / sec / 1e9}
+        del ws, sa, tok
+        torch.cuda.empty_cache()
+    line = {
+        "metric": "suffix-array build seconds (1B-token general store)", "value": out["general"]["seconds"],
+        "unit": "s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": 1e3 * out["general"]["seconds"], "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u16/u32/u64 (integer)", "data": "synthetic (seeded store; no dataset)",
+        "config": {"workload": "SA build, 1B general + 10M project stores"}, "roofline": None, "builds": out,
     }
     print(json.dumps(line), flush=True)
 

@@ -158,6 +158,13 @@ typedef struct fc_retrieve_params {
  * cont_tok [B][k][m] : continuation tokens, 0 past cont_len.
  * Within one store's slots the continuations come out in lexicographic order
  * (suffix order), which fc_build_tree relies on.
+ * rows [B], n_rows : optional row map.  When rows is not NULL, query b's
+ *                per-store results and slots go to row rows[b] of every output
+ *                array, which then has n_rows rows ([n_rows][S], [n_rows][k],
+ *                [n_rows][k][m]) - e.g. straight into the slots of a
+ *                retrieval cache.  Rows must be distinct; a query whose row
+ *                is outside [0, n_rows) is skipped.  When rows is NULL, row b
+ *                is query b and n_rows is ignored.
  * ws, ws_bytes : workspace of at least fc_retrieve_workspace_bytes(B, S, p)
  *                (4*(B+1) bytes: the batch's slot offsets); its contents on
  *                entry do not matter.
@@ -166,7 +173,7 @@ size_t fc_retrieve_workspace_bytes(int32_t B, int32_t S, fc_retrieve_params p);
 fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
                       fc_retrieve_params p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
                       int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len, uint16_t* cont_tok,
-                      void* ws, size_t ws_bytes, hipStream_t stream);
+                      const int32_t* rows, int32_t n_rows, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Draft tree                                                                */
@@ -198,6 +205,10 @@ typedef struct fc_tree_params {
  * mask [B][c+1][c+1]      : 1 where column j is row i or an ancestor of i
  *                           (root included), else 0.
  * Rows past num_nodes: token 0, parent -1, weight 0, position 0, mask 0.
+ * rows [B], n_rows       : optional row map: query b reads row rows[b] of
+ *                           taken, cont_len and cont_tok (n_rows rows each);
+ *                           its outputs stay at b.  A row outside
+ *                           [0, n_rows) gives num_nodes = -1.  NULL: row b.
  * ws, ws_bytes           : workspace of at least fc_build_tree_workspace_bytes(B)
  *                           (the batch split into light and heavy queries).
  * Limits: S <= FC_MAX_SOURCES, k <= 65535, alpha[s]*k < 2^32, and the
@@ -208,7 +219,8 @@ size_t fc_build_tree_workspace_bytes(int32_t B);
 fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok,
                         const uint16_t* ctx, int32_t B, int32_t L, int32_t S, int32_t k, int32_t m, fc_tree_params t,
                         int32_t* num_nodes, int32_t* node_tok, int32_t* parent, uint32_t* weight, int32_t* pos_ids,
-                        int32_t* mask, void* ws, size_t ws_bytes, hipStream_t stream);
+                        int32_t* mask, const int32_t* rows, int32_t n_rows, void* ws, size_t ws_bytes,
+                        hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Acceptance                                                                */
@@ -230,6 +242,26 @@ fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len, const uin
 fc_status fc_verify_accept(const int32_t* num_nodes, const int32_t* node_tok, const int32_t* parent,
                            const int32_t* pos_ids, const int32_t* target, int32_t B, int32_t c, int32_t m,
                            int32_t* accept_len, int32_t* accept_tok, int32_t* last_node, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Decode-trace replay                                                       */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Stand-in for the target model when replaying a known token stream (the
+ * accepted length per forward step is the paper's average acceptance length
+ * metric, Section V-C eq. (7)): after the path to tree row i the model would
+ * produce the true token at position start[b] + pos_ids[b][i].
+ * truth  : stream s starts at truth + s*truth_stride and has truth_len tokens.
+ * seq [B] : stream of query b (NULL: stream b); start [B]: position of the
+ *           token after query b's context in its stream.
+ * target [B][c+1] : truth[seq[b]][start[b] + pos_ids[b][i]] for rows
+ *                   i < num_nodes[b] whose position is below truth_len,
+ *                   else -1.
+ */
+fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_t truth_stride, const int32_t* seq,
+                                const int32_t* start, const int32_t* num_nodes, const int32_t* pos_ids, int32_t B,
+                                int32_t c, int32_t* target, hipStream_t stream);
 
 #ifdef __cplusplus
 }

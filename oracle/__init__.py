@@ -166,3 +166,71 @@ def verify_accept(tree: dict, target, m: int = 10) -> dict:
     _lib().oracle_verify_accept(B, R - 1, m, _p(nn), _p(tok), _p(par), _p(pos), _p(tg),
                                 _p(out["accept_len"]), _p(out["accept_tok"]), _p(out["last_node"]))
     return out
+
+
+def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int = 10, c: int = 64, alpha=(1, 1),
+           lru: int = 32, ctx_len: int = 16, max_steps: int = 512) -> dict:
+    """Decode-trace replay over known streams (reading of the average
+    acceptance length setting, Section V-C eq. (7)).
+
+    Every stream starts with its first ctx_len tokens as context at position
+    p = ctx_len.  Each step, for every stream with p below its length: the
+    key is the last ctx_len tokens; an LRU of `lru` entries per stream maps
+    keys to stored retrieval results (a hit reuses the result and becomes most
+    recent; a miss retrieves, inserts as most recent and drops the least
+    recent beyond `lru`); the draft tree is built; the target after tree row
+    i is truth[p + pos_ids[i]] (-1 past the stream); the accepted length is
+    added to p.  Returns accept [steps][n_streams] (-1 for finished streams),
+    hits and lookups per stream, final positions, the mean accepted length
+    per live step, and the step count.
+    """
+    from collections import OrderedDict
+
+    truth = np.ascontiguousarray(truth, dtype=np.uint16)
+    nseq, tlen = truth.shape
+    pos = [ctx_len] * nseq
+    caches = [OrderedDict() for _ in range(nseq)]
+    hits = [0] * nseq
+    lookups = [0] * nseq
+    fields = ("taken", "cont_len", "cont_tok")
+    steps = []
+    for _ in range(max_steps):
+        act = [b for b in range(nseq) if pos[b] < tlen]
+        if not act:
+            break
+        ctx = np.stack([truth[b, pos[b] - ctx_len:pos[b]] for b in act])
+        keys = [ctx[j].tobytes() for j in range(len(act))]
+        missing = []
+        for j, b in enumerate(act):
+            lookups[b] += 1
+            if keys[j] in caches[b]:
+                caches[b].move_to_end(keys[j])
+                hits[b] += 1
+            else:
+                missing.append(j)
+        if missing:
+            r = retrieve(texts, ctx[missing], n_max=n_max, n_min=n_min, k=k, m=m)
+            for i, j in enumerate(missing):
+                b = act[j]
+                if len(caches[b]) >= lru:
+                    caches[b].popitem(last=False)
+                caches[b][keys[j]] = {f: r[f][i].copy() for f in fields}
+        got = [caches[b][keys[j]] for j, b in enumerate(act)]
+        tree = build_tree(np.stack([g["taken"] for g in got]), np.stack([g["cont_len"] for g in got]),
+                          np.stack([g["cont_tok"] for g in got]), ctx, c=c, alpha=alpha)
+        target = np.full(tree["node_tok"].shape, -1, np.int32)
+        for j, b in enumerate(act):
+            for i in range(int(tree["num_nodes"][j])):
+                at = pos[b] + int(tree["pos_ids"][j, i])
+                if at < tlen:
+                    target[j, i] = int(truth[b, at])
+        acc = verify_accept(tree, target, m=m)["accept_len"]
+        row = np.full(nseq, -1, np.int64)
+        for j, b in enumerate(act):
+            row[b] = int(acc[j])
+            pos[b] += int(acc[j])
+        steps.append(row)
+    accept = np.stack(steps) if steps else np.zeros((0, nseq), np.int64)
+    live = accept >= 0
+    return dict(accept=accept, hits=np.array(hits), lookups=np.array(lookups), pos=np.array(pos),
+                acc_len=float(accept[live].sum() / max(live.sum(), 1)), steps=len(steps))

@@ -32,7 +32,7 @@ EXPORTS = (
     "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_store_prepare",
     "fc_pair_table_entries", "fc_store_prepare_pairs",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
-    "fc_verify_accept",
+    "fc_verify_accept", "fc_targets_from_truth",
 )
 
 
@@ -84,14 +84,16 @@ def lib() -> ctypes.CDLL:
     L.fc_retrieve_workspace_bytes.argtypes = [i32, i32, FcRetrieveParams]
     L.fc_retrieve.restype = ctypes.c_int
     L.fc_retrieve.argtypes = [ctypes.POINTER(FcStore), i32, vp, i32, i32, FcRetrieveParams,
-                              vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+                              vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]
     L.fc_build_tree_workspace_bytes.restype = sz
     L.fc_build_tree_workspace_bytes.argtypes = [i32]
     L.fc_build_tree.restype = ctypes.c_int
     L.fc_build_tree.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, FcTreeParams,
-                                vp, vp, vp, vp, vp, vp, vp, sz, vp]
+                                vp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]
     L.fc_verify_accept.restype = ctypes.c_int
     L.fc_verify_accept.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp]
+    L.fc_targets_from_truth.restype = ctypes.c_int
+    L.fc_targets_from_truth.argtypes = [vp, i32, ctypes.c_int64, vp, vp, vp, vp, i32, i32, vp, vp]
     return L
 
 
@@ -206,8 +208,10 @@ def fc_retrieve_workspace_bytes(B: int, S: int, n_max: int = 16, n_min: int = 2,
 
 
 def fc_retrieve(stores, ctx: torch.Tensor, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int = 10,
-                out: dict | None = None, workspace: torch.Tensor | None = None, stream=None) -> dict:
-    """Batched longest-suffix retrieval; ctx is uint16 [B][L] on the GPU."""
+                out: dict | None = None, workspace: torch.Tensor | None = None, rows: torch.Tensor | None = None,
+                stream=None) -> dict:
+    """Batched longest-suffix retrieval; ctx is uint16 [B][L] on the GPU.
+    With rows (int32 [B]), query b's results go to row rows[b] of `out`."""
     if ctx.dtype != torch.uint16 or ctx.dim() != 2:
         raise ValueError("ctx must be a 2-D uint16 tensor")
     B, L = ctx.shape
@@ -219,8 +223,9 @@ def fc_retrieve(stores, ctx: torch.Tensor, n_max: int = 16, n_min: int = 2, k: i
     need = int(lib().fc_retrieve_workspace_bytes(B, S, p))
     if workspace is None and need > 0:
         workspace = _empty(need, torch.uint8, ctx.device)
+    n_rows = out["taken"].shape[0]
     _check("fc_retrieve", lib().fc_retrieve(
-        views, S, _ptr(ctx), B, L, p, *[_ptr(out[f]) for f in RETRIEVE_FIELDS],
+        views, S, _ptr(ctx), B, L, p, *[_ptr(out[f]) for f in RETRIEVE_FIELDS], _ptr(rows), n_rows,
         _ptr(workspace), 0 if workspace is None else workspace.numel(), _stream(stream)))
     return out
 
@@ -243,9 +248,11 @@ def fc_build_tree_workspace_bytes(B: int) -> int:
 
 def fc_build_tree(taken: torch.Tensor, cont_len: torch.Tensor, cont_tok: torch.Tensor, ctx: torch.Tensor,
                   c: int = 64, alpha=(1, 1), out: dict | None = None, workspace: torch.Tensor | None = None,
-                  stream=None) -> dict:
-    """Weighted draft trie pruned to c nodes, with mask and position ids."""
-    B, S = taken.shape
+                  rows: torch.Tensor | None = None, stream=None) -> dict:
+    """Weighted draft trie pruned to c nodes, with mask and position ids.
+    With rows (int32 [B]), query b reads row rows[b] of taken/cont_*."""
+    n_rows, S = taken.shape
+    B = n_rows if rows is None else rows.numel()
     k, m = cont_tok.shape[1], cont_tok.shape[2]
     L = ctx.shape[1]
     a = list(alpha)[:S]
@@ -259,8 +266,8 @@ def fc_build_tree(taken: torch.Tensor, cont_len: torch.Tensor, cont_tok: torch.T
         workspace = _empty(need, torch.uint8, ctx.device)
     _check("fc_build_tree", lib().fc_build_tree(
         _ptr(taken), _ptr(cont_len), _ptr(cont_tok), _ptr(ctx), B, L, S, k, m, tp,
-        *[_ptr(out[f]) for f in TREE_FIELDS], _ptr(workspace), 0 if workspace is None else workspace.numel(),
-        _stream(stream)))
+        *[_ptr(out[f]) for f in TREE_FIELDS], _ptr(rows), n_rows, _ptr(workspace),
+        0 if workspace is None else workspace.numel(), _stream(stream)))
     return out
 
 
@@ -282,4 +289,16 @@ def fc_verify_accept(tree: dict, target: torch.Tensor, m: int = 10, out: dict | 
     _check("fc_verify_accept", lib().fc_verify_accept(
         _ptr(tree["num_nodes"]), _ptr(tree["node_tok"]), _ptr(tree["parent"]), _ptr(tree["pos_ids"]),
         _ptr(target), B, R - 1, m, *[_ptr(out[f]) for f in ACCEPT_FIELDS], _stream(stream)))
+    return out
+
+
+def fc_targets_from_truth(truth: torch.Tensor, start: torch.Tensor, tree: dict, seq: torch.Tensor | None = None,
+                          out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Target tokens [B][c+1] from true streams (uint16 [n_streams][len])."""
+    B, R = tree["node_tok"].shape
+    if out is None:
+        out = _empty((B, R), torch.int32, truth.device)
+    _check("fc_targets_from_truth", lib().fc_targets_from_truth(
+        _ptr(truth), truth.shape[1], truth.stride(0), _ptr(seq), _ptr(start), _ptr(tree["num_nodes"]),
+        _ptr(tree["pos_ids"]), B, R - 1, _ptr(out), _stream(stream)))
     return out

@@ -242,4 +242,12 @@ __device__ __forceinline__ T block_max(T v, T* scratch) {
 
 __host__ __device__ __forceinline__ uint32_t div_up(uint64_t a, uint64_t b) { return (uint32_t)((a + b - 1) / b); }
 
+// Row of query b under an optional row map: rows[b] when it lies in
+// [0, n_rows), -1 when it does not, b when there is no map.
+__device__ __forceinline__ int map_row(const int32_t* rows, int n_rows, int b) {
+  if (!rows) return b;
+  const int r = rows[b];
+  return (r >= 0 && r < n_rows) ? r : -1;
+}
+
 }  // namespace fc

@@ -74,6 +74,7 @@ __device__ __forceinline__ int cmp_suffix(const uint16_t* __restrict__ T, uint32
 
 __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, const uint16_t* __restrict__ ctx,
                                                            int B, int L, int n_max, int n_min, int k,
+                                                           const int32_t* __restrict__ rows, int n_rows,
                                                            int32_t* __restrict__ match_n,
                                                            uint32_t* __restrict__ range_lo,
                                                            uint32_t* __restrict__ range_cnt,
@@ -166,7 +167,8 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
     }
   }
   __syncthreads();
-  if (active && lane == 0) {
+  const int row = active ? fc::map_row(rows, n_rows, b) : -1;
+  if (active && lane == 0 && row >= 0) {
     const int n_hi = s_nhi[w];
     int64_t used = 0;
     for (int s = 0; s < S; ++s) {
@@ -184,7 +186,7 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
       }
       const int64_t budget = (int64_t)k - used;
       const int64_t tk = (int64_t)cnt < budget ? (int64_t)cnt : budget;
-      const int64_t o = (int64_t)b * S + s;
+      const int64_t o = (int64_t)row * S + s;
       match_n[o] = mn;
       range_lo[o] = lo;
       range_cnt[o] = cnt;
@@ -197,19 +199,26 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
 // Exclusive prefix of kept slots over the batch (one workgroup):
 // offsets[b] = slots kept by queries before b; offsets[B] = total.
 __global__ void __launch_bounds__(kScanThreads) k_offsets(const int32_t* __restrict__ taken, int B, int S,
+                                                          const int32_t* __restrict__ rows, int n_rows,
                                                           uint32_t* __restrict__ offsets) {
   __shared__ uint32_t scratch[kScanThreads / fc::kWave + 1];
   const int per = (B + kScanThreads - 1) / kScanThreads;
   const int b0 = (int)threadIdx.x * per;
   const int b1 = b0 + per < B ? b0 + per : B;
+  auto kept = [&](int b) -> uint32_t {
+    const int r = fc::map_row(rows, n_rows, b);
+    uint32_t t = 0;
+    if (r >= 0)
+      for (int s = 0; s < S; ++s) t += (uint32_t)taken[(int64_t)r * S + s];
+    return t;
+  };
   uint32_t sum = 0;
-  for (int b = b0; b < b1; ++b)
-    for (int s = 0; s < S; ++s) sum += (uint32_t)taken[(int64_t)b * S + s];
+  for (int b = b0; b < b1; ++b) sum += kept(b);
   uint32_t total;
   uint32_t run = fc::block_excl_sum<uint32_t>(sum, scratch, &total);
   for (int b = b0; b < b1; ++b) {
     offsets[b] = run;
-    for (int s = 0; s < S; ++s) run += (uint32_t)taken[(int64_t)b * S + s];
+    run += kept(b);
   }
   if (threadIdx.x == 0) offsets[B] = total;
 }
@@ -253,6 +262,7 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
                                                            const uint32_t* __restrict__ range_cnt,
                                                            const int32_t* __restrict__ taken,
                                                            const uint32_t* __restrict__ offsets, int words,
+                                                           const int32_t* __restrict__ rows, int n_rows,
                                                            uint32_t* __restrict__ cont_pos,
                                                            uint8_t* __restrict__ cont_src,
                                                            uint8_t* __restrict__ cont_len,
@@ -271,15 +281,16 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
       if (off_tab[mid] <= g) lo = mid; else hi = mid;
     }
     const int b = lo;
+    const int row = fc::map_row(rows, n_rows, b);  // >= 0: a skipped query owns no slots
     const int i = (int)(g - off_tab[b]);
     int s = 0;
     int64_t before = 0;
     for (; s + 1 < S; ++s) {
-      const int64_t t = taken[(int64_t)b * S + s];
+      const int64_t t = taken[(int64_t)row * S + s];
       if (i < before + t) break;
       before += t;
     }
-    const int64_t o = (int64_t)b * S + s;
+    const int64_t o = (int64_t)row * S + s;
     const uint64_t cnt = range_cnt[o];
     const uint64_t budget = (uint64_t)((int64_t)k - before);
     const uint64_t local = (uint64_t)(i - before);
@@ -297,7 +308,7 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
 #pragma unroll
     for (int x = MAXM - 1; x >= 0; --x)
       if (x < m && v[x] == 0) len = x;
-    const int64_t slot = (int64_t)b * k + i;
+    const int64_t slot = (int64_t)row * k + i;
     uint16_t* out = cont_tok + slot * m;
 #pragma unroll
     for (int x = 0; x < MAXM; ++x)
@@ -317,8 +328,10 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather_any(StoreArgs st, int
                                                                uint32_t* __restrict__ cont_pos,
                                                                uint8_t* __restrict__ cont_src,
                                                                uint8_t* __restrict__ cont_len,
-                                                               uint16_t* __restrict__ cont_tok) {
-  const int b = blockIdx.x;
+                                                               uint16_t* __restrict__ cont_tok,
+                                                               const int32_t* __restrict__ rows, int n_rows) {
+  const int b = fc::map_row(rows, n_rows, (int)blockIdx.x);  // row of this query
+  if (b < 0) return;
   int64_t total = 0;
   for (int s = 0; s < S; ++s) total += taken[(int64_t)b * S + s];
   for (int i = (int)threadIdx.x; i < total; i += kGatherThreads) {
@@ -371,7 +384,8 @@ extern "C" size_t fc_retrieve_workspace_bytes(int32_t B, int32_t S, fc_retrieve_
 extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
                                  fc_retrieve_params p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
                                  int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len,
-                                 uint16_t* cont_tok, void* ws, size_t ws_bytes, hipStream_t stream) {
+                                 uint16_t* cont_tok, const int32_t* rows, int32_t n_rows, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
   if (!stores || S < 1 || S > FC_MAX_SOURCES) return FC_ERR_INVALID;
   if (B < 0 || L < 1) return FC_ERR_INVALID;
   if (p.n_max < 1 || p.n_max > FC_MAX_NMAX || p.n_min < 1 || p.n_min > p.n_max) return FC_ERR_INVALID;
@@ -393,14 +407,15 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
   if (B == 0) return FC_OK;
   if (!ctx || !match_n || !range_lo || !range_cnt || !taken || !cont_pos || !cont_src || !cont_len || !cont_tok)
     return FC_ERR_INVALID;
+  if (rows && n_rows < 1) return FC_ERR_INVALID;
   if (!ws || ws_bytes < fc_retrieve_workspace_bytes(B, S, p)) return FC_ERR_WORKSPACE;
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_search, dim3(fc::div_up(B, kQueriesPerBlock)), dim3(kSearchThreads), 0, stream, st, S, ctx,
-                     B, L, p.n_max, p.n_min, p.k, match_n, range_lo, range_cnt, taken);
+                     B, L, p.n_max, p.n_min, p.k, rows, n_rows, match_n, range_lo, range_cnt, taken);
   FC_CHECK_LAUNCH();
   if (p.m <= 16) {
     uint32_t* offsets = (uint32_t*)ws;
-    hipLaunchKernelGGL(k_offsets, dim3(1), dim3(kScanThreads), 0, stream, taken, B, S, offsets);
+    hipLaunchKernelGGL(k_offsets, dim3(1), dim3(kScanThreads), 0, stream, taken, B, S, rows, n_rows, offsets);
     FC_CHECK_LAUNCH();
     int words = 1;
     for (int s = 0; s < S; ++s) words &= (((uintptr_t)st.tok[s]) & 3) == 0;
@@ -408,13 +423,15 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
     const uint32_t blocks = (uint32_t)(want < (uint64_t)kGatherBlocks ? want : (uint64_t)kGatherBlocks);
     if (p.m <= 10)
       hipLaunchKernelGGL(k_gather<10>, dim3(blocks), dim3(kGatherThreads), 0, stream, st, S, B, p.k, p.m, match_n,
-                         range_lo, range_cnt, taken, offsets, words, cont_pos, cont_src, cont_len, cont_tok);
+                         range_lo, range_cnt, taken, offsets, words, rows, n_rows, cont_pos, cont_src, cont_len,
+                         cont_tok);
     else
       hipLaunchKernelGGL(k_gather<16>, dim3(blocks), dim3(kGatherThreads), 0, stream, st, S, B, p.k, p.m, match_n,
-                         range_lo, range_cnt, taken, offsets, words, cont_pos, cont_src, cont_len, cont_tok);
+                         range_lo, range_cnt, taken, offsets, words, rows, n_rows, cont_pos, cont_src, cont_len,
+                         cont_tok);
   } else {
     hipLaunchKernelGGL(k_gather_any, dim3(B), dim3(kGatherThreads), 0, stream, st, S, p.k, p.m, match_n, range_lo,
-                       range_cnt, taken, cont_pos, cont_src, cont_len, cont_tok);
+                       range_cnt, taken, cont_pos, cont_src, cont_len, cont_tok, rows, n_rows);
   }
   FC_CHECK_LAUNCH();
   return FC_OK;

@@ -102,7 +102,8 @@ __global__ void __launch_bounds__(kTreeThreads) k_tree_any(const int32_t* __rest
                                                        const uint8_t* __restrict__ cont_len,
                                                        const uint16_t* __restrict__ cont_tok,
                                                        const uint16_t* __restrict__ ctx, int L, int S, int k, int m,
-                                                       int c, Alpha alpha, int32_t* __restrict__ num_nodes,
+                                                       int c, Alpha alpha, const int32_t* __restrict__ rows,
+                                                       int n_rows, int32_t* __restrict__ num_nodes,
                                                        int32_t* __restrict__ node_tok, int32_t* __restrict__ parent,
                                                        uint32_t* __restrict__ weight, int32_t* __restrict__ pos_ids,
                                                        int32_t* __restrict__ mask) {
@@ -131,12 +132,13 @@ __global__ void __launch_bounds__(kTreeThreads) k_tree_any(const int32_t* __rest
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int R = c + 1;
-  const int64_t row0 = (int64_t)b * k;
+  const int in_row = fc::map_row(rows, n_rows, b);
+  const int64_t row0 = (int64_t)(in_row < 0 ? 0 : in_row) * k;
 
   if (tid == 0) {
-    int acc = 0, err = 0;
+    int acc = 0, err = in_row < 0;
     for (int s = 0; s < S; ++s) {
-      const int t = taken[(int64_t)b * S + s];
+      const int t = in_row < 0 ? 0 : taken[(int64_t)in_row * S + s];
       if (t < 0) err = 1;
       s_seg[s] = acc;
       acc += t > 0 ? t : 0;
@@ -468,16 +470,19 @@ struct Scan2 {
 // and heavy queries, each list in query order: lists[0..B) light ids,
 // lists[B..2B) heavy ids, counts[0], counts[1] their lengths.
 __global__ void __launch_bounds__(1024) k_tree_classify(const int32_t* __restrict__ taken, int B, int S, int k,
-                                                        int t_small, int32_t* __restrict__ lists,
+                                                        int t_small, const int32_t* __restrict__ rows, int n_rows,
+                                                        int32_t* __restrict__ lists,
                                                         int32_t* __restrict__ counts) {
   __shared__ uint32_t s_a[1024 / fc::kWave + 1], s_b[1024 / fc::kWave + 1];
   const int per = (B + 1023) / 1024;
   const int b0 = (int)threadIdx.x * per;
   const int b1 = b0 + per < B ? b0 + per : B;
   auto heavy = [&](int b) {
+    const int r = fc::map_row(rows, n_rows, b);
+    if (r < 0) return false;  // reported as malformed by the light launch
     int T = 0, bad = 0;
     for (int s = 0; s < S; ++s) {
-      const int t = taken[(int64_t)b * S + s];
+      const int t = taken[(int64_t)r * S + s];
       bad |= t < 0;
       T += t > 0 ? t : 0;
     }
@@ -505,6 +510,7 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
                                                   const uint16_t* __restrict__ ctx, int L, int S, int k, int m, int c,
                                                   Alpha alpha, const int32_t* __restrict__ list,
                                                   const int32_t* __restrict__ list_count, int t_hi, int words,
+                                                  const int32_t* __restrict__ rows, int n_rows,
                                                   int32_t* __restrict__ num_nodes, int32_t* __restrict__ node_tok,
                                                   int32_t* __restrict__ parent, uint32_t* __restrict__ weight,
                                                   int32_t* __restrict__ pos_ids, int32_t* __restrict__ mask) {
@@ -531,13 +537,14 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
   const int lane = fc::lane_id();
   const int w = tid / fc::kWave;
   const int R = c + 1;
-  const int64_t row0 = (int64_t)b * k;
+  const int in_row = fc::map_row(rows, n_rows, b);
+  const int64_t row0 = (int64_t)(in_row < 0 ? 0 : in_row) * k;
 
-  // Malformed rows (a negative count or more than k slots) count as T = 0
-  // and are reported with num_nodes = -1.
-  int T_raw = 0, bad = 0;
-  for (int s = 0; s < S; ++s) {
-    const int t = taken[(int64_t)b * S + s];
+  // Malformed rows (a row outside the map's range, a negative count or more
+  // than k slots) count as T = 0 and are reported with num_nodes = -1.
+  int T_raw = 0, bad = in_row < 0;
+  for (int s = 0; s < S && in_row >= 0; ++s) {
+    const int t = taken[(int64_t)in_row * S + s];
     bad |= t < 0;
     T_raw += t > 0 ? t : 0;
   }
@@ -559,8 +566,8 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     int acc = 0;
     for (int s = 0; s < S; ++s) {
       s_seg[s] = acc;
-      const int t = taken[(int64_t)b * S + s];
-      acc += bad ? 0 : t;
+      const int t = bad ? 0 : taken[(int64_t)in_row * S + s];
+      acc += t;
     }
     s_seg[S] = acc;
     s_err = bad;
@@ -980,8 +987,8 @@ extern "C" size_t fc_build_tree_workspace_bytes(int32_t B) {
 extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok,
                                    const uint16_t* ctx, int32_t B, int32_t L, int32_t S, int32_t k, int32_t m,
                                    fc_tree_params t, int32_t* num_nodes, int32_t* node_tok, int32_t* parent,
-                                   uint32_t* weight, int32_t* pos_ids, int32_t* mask, void* ws, size_t ws_bytes,
-                                   hipStream_t stream) {
+                                   uint32_t* weight, int32_t* pos_ids, int32_t* mask, const int32_t* rows,
+                                   int32_t n_rows, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (B < 0 || L < 1 || S < 1 || S > FC_MAX_SOURCES) return FC_ERR_INVALID;
   if (k < 1 || m < 1 || m > 255 || t.c < 1 || t.c + 1 > FC_MAX_TREE_ROWS) return FC_ERR_INVALID;
   if (k > 65535) return FC_ERR_UNSUPPORTED;
@@ -990,6 +997,7 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
   if (B == 0) return FC_OK;
   if (!taken || !cont_len || !cont_tok || !ctx || !num_nodes || !node_tok || !parent || !weight || !pos_ids || !mask)
     return FC_ERR_INVALID;
+  if (rows && n_rows < 1) return FC_ERR_INVALID;
   if (!ws || ws_bytes < fc_build_tree_workspace_bytes(B)) return FC_ERR_WORKSPACE;
   int dev = 0, max_lds = 0;
   FC_CHECK_HIP(hipGetDevice(&dev));
@@ -1006,7 +1014,8 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
     const int t_small = k < kSmallClass ? k : kSmallClass;
     int32_t* lists = (int32_t*)ws;
     int32_t* counts = lists + 2 * (size_t)B;
-    hipLaunchKernelGGL(k_tree_classify, dim3(1), dim3(1024), 0, stream, taken, B, S, k, t_small, lists, counts);
+    hipLaunchKernelGGL(k_tree_classify, dim3(1), dim3(1024), 0, stream, taken, B, S, k, t_small, rows, n_rows, lists,
+                       counts);
     FC_CHECK_LAUNCH();
     // row loads: 16-byte vectors when every query's row is 16-byte aligned,
     // else 32-bit words when 4-byte aligned, else single tokens
@@ -1019,8 +1028,8 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
                                 (int)small.total);
     (void)hipGetLastError();
     hipLaunchKernelGGL((k_tree_fast<256, 16>), dim3(B), dim3(256), small.total, stream, taken, cont_len, cont_tok,
-                       ctx, L, S, k, m, t.c, a, lists, counts, t_small, words, num_nodes, node_tok, parent, weight,
-                       pos_ids, mask);
+                       ctx, L, S, k, m, t.c, a, lists, counts, t_small, words, rows, n_rows, num_nodes, node_tok,
+                       parent, weight, pos_ids, mask);
     FC_CHECK_LAUNCH();
     if (k > t_small) {
       if (full.total > 64 * 1024)
@@ -1028,8 +1037,8 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
                                   (int)full.total);
       (void)hipGetLastError();
       hipLaunchKernelGGL((k_tree_fast<1024, 16>), dim3(B), dim3(1024), full.total, stream, taken, cont_len,
-                         cont_tok, ctx, L, S, k, m, t.c, a, lists + B, counts + 1, k, words, num_nodes, node_tok,
-                         parent, weight, pos_ids, mask);
+                         cont_tok, ctx, L, S, k, m, t.c, a, lists + B, counts + 1, k, words, rows, n_rows, num_nodes,
+                         node_tok, parent, weight, pos_ids, mask);
       FC_CHECK_LAUNCH();
     }
     return FC_OK;
@@ -1038,7 +1047,7 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
     (void)hipFuncSetAttribute((const void*)k_tree_any, hipFuncAttributeMaxDynamicSharedMemorySize, (int)full.total);
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_tree_any, dim3(B), dim3(kTreeThreads), full.total, stream, taken, cont_len, cont_tok, ctx, L,
-                     S, k, m, t.c, a, num_nodes, node_tok, parent, weight, pos_ids, mask);
+                     S, k, m, t.c, a, rows, n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
   FC_CHECK_LAUNCH();
   return FC_OK;
 }

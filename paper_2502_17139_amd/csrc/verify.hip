@@ -72,6 +72,26 @@ __global__ void __launch_bounds__(kVerifyThreads) k_verify(const int32_t* __rest
   }
 }
 
+// target[b][i] = truth[b][start[b] + pos_ids[b][i]] for live rows inside
+// the stream, else -1; one thread per (query, row).
+__global__ void __launch_bounds__(256) k_targets(const uint16_t* __restrict__ truth, int truth_len,
+                                                 int64_t stride, const int32_t* __restrict__ seq,
+                                                 const int32_t* __restrict__ start,
+                                                 const int32_t* __restrict__ num_nodes,
+                                                 const int32_t* __restrict__ pos_ids, int B, int R,
+                                                 int32_t* __restrict__ target) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (int64_t)B * R) return;
+  const int b = (int)(e / R), i = (int)(e - (int64_t)b * R);
+  int32_t v = -1;
+  if (i < num_nodes[b]) {
+    const int64_t pos = (int64_t)start[b] + pos_ids[e];
+    const int64_t sq = seq ? seq[b] : b;
+    if (pos >= 0 && pos < truth_len) v = truth[sq * stride + pos];
+  }
+  target[e] = v;
+}
+
 }  // namespace
 
 extern "C" fc_status fc_verify_accept(const int32_t* num_nodes, const int32_t* node_tok, const int32_t* parent,
@@ -86,6 +106,21 @@ extern "C" fc_status fc_verify_accept(const int32_t* num_nodes, const int32_t* n
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_verify, dim3(fc::div_up(B, kQueriesPerBlock)), dim3(kVerifyThreads), 0, stream, num_nodes,
                      node_tok, parent, target, B, c, m, accept_len, accept_tok, last_node);
+  FC_CHECK_LAUNCH();
+  return FC_OK;
+}
+
+extern "C" fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_t truth_stride,
+                                           const int32_t* seq, const int32_t* start, const int32_t* num_nodes,
+                                           const int32_t* pos_ids, int32_t B, int32_t c, int32_t* target,
+                                           hipStream_t stream) {
+  if (B < 0 || c < 0 || c + 1 > FC_MAX_TREE_ROWS || truth_len < 0 || truth_stride < truth_len) return FC_ERR_INVALID;
+  if (B == 0) return FC_OK;
+  if (!truth || !start || !num_nodes || !pos_ids || !target) return FC_ERR_INVALID;
+  (void)hipGetLastError();
+  const int64_t n = (int64_t)B * (c + 1);
+  hipLaunchKernelGGL(k_targets, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, stream, truth, truth_len,
+                     truth_stride, seq, start, num_nodes, pos_ids, B, c + 1, target);
   FC_CHECK_LAUNCH();
   return FC_OK;
 }

@@ -53,7 +53,7 @@ def test_workspace_sizes(L):
 def _retrieve_args(S=1, B=1, L_=4, p=(16, 2, 5000, 10), ws_bytes=0):
     views = (fc.FcStore * 4)(*[fc.FcStore(1, 1, 1, 10, None, 0) for _ in range(4)])
     one = ctypes.c_void_p(8)
-    return [views, S, one, B, L_, fc.FcRetrieveParams(*p)] + [one] * 8 + [None, ws_bytes, None]
+    return [views, S, one, B, L_, fc.FcRetrieveParams(*p)] + [one] * 8 + [None, 0, None, ws_bytes, None]
 
 
 @pytest.mark.parametrize("change,code", [
@@ -91,7 +91,7 @@ def test_retrieve_rejects_null_outputs_and_big_store(L):
 def _tree_args(B=1, L_=2, S=2, k=10, m=4, c=8, alpha=(1, 1, 0, 0)):
     one = ctypes.c_void_p(8)
     tp = fc.FcTreeParams(c, (ctypes.c_uint32 * 4)(*alpha))
-    return [one, one, one, one, B, L_, S, k, m, tp] + [one] * 6 + [one, 1 << 20, None]
+    return [one, one, one, one, B, L_, S, k, m, tp] + [one] * 6 + [None, 0, one, 1 << 20, None]
 
 
 @pytest.mark.parametrize("change,code", [
@@ -115,6 +115,23 @@ def test_build_tree_rejects_missing_workspace(L):
     args[-3] = None
     assert L.fc_build_tree(*args) == 2
     assert L.fc_build_tree_workspace_bytes(1024) == 4 * 2050
+
+
+def test_row_maps_and_targets_reject(L):
+    args = _retrieve_args(ws_bytes=1 << 20)
+    args[-3] = ctypes.c_void_p(8)
+    args[-5] = ctypes.c_void_p(8)  # a row map with no rows
+    args[-4] = 0
+    assert L.fc_retrieve(*args) == 1
+    targs = _tree_args()
+    targs[-5] = ctypes.c_void_p(8)
+    targs[-4] = 0
+    assert L.fc_build_tree(*targs) == 1
+    one = ctypes.c_void_p(8)
+    assert L.fc_targets_from_truth(one, 100, 50, None, one, one, one, 2, 8, one, None) == 1  # stride < len
+    assert L.fc_targets_from_truth(one, 100, 100, None, one, one, one, 2, 256, one, None) == 1
+    assert L.fc_targets_from_truth(None, 100, 100, None, one, one, one, 2, 8, one, None) == 1
+    assert L.fc_targets_from_truth(None, 0, 0, None, None, None, None, 0, 8, None, None) == 0
 
 
 def test_pair_table_size_and_rejects(L):

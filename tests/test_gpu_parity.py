@@ -23,6 +23,7 @@ if not torch.cuda.is_available():  # pragma: no cover - CPU container
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_2502_17139_amd as fc  # noqa: E402
+from paper_2502_17139_amd.replay import GpuReplay  # noqa: E402
 
 P = dict(synth.PARAMS)
 
@@ -201,7 +202,48 @@ def test_headline_workload_sampled():
     for i, b in enumerate(rows):
         for f in ("accept_len", "accept_tok", "last_node"):
             assert (host(ga[f])[b] == oa[f][i]).all(), (f, b)
+    # decode-trace replay over the same stores: a few streams, first steps
+    say("headline: replay")
+    truth = synth.truth(n_seq=4)
+    g = GpuReplay(stores, truth, **P).run(max_steps=6)
+    o = oracle.replay([tp, tg], truth, **P, max_steps=6)
+    for f in ("accept", "hits", "lookups", "pos"):
+        assert (g[f] == o[f]).all(), f
     synth.drop_cache()
+
+
+# ------------------------------------------------------------------ replay --
+
+def test_replay_matches_oracle():
+    """Decode-trace replay: 16 streams from the project pool, 10M-token
+    project store + 1M-token store, first 60 steps; every accepted length,
+    cache hit and final position equal."""
+    tp, t1 = synth.store(3, "project"), synth.store(1, "single")
+    truth = synth.truth(n_seq=16, length=600)
+    stores = [gpu_store(tp, synth.VOCAB), gpu_store(t1)]
+    say("replay: gpu")
+    g = GpuReplay(stores, truth, **P).run(max_steps=60)
+    say("replay: oracle")
+    o = oracle.replay([tp, t1], truth, **P, max_steps=60)
+    for f in ("accept", "hits", "lookups", "pos"):
+        assert (g[f] == o[f]).all(), f
+    assert g["acc_len"] == o["acc_len"] and g["acc_len"] > 2.0
+
+
+def test_replay_cache_eviction():
+    """Periodic streams that never match: one token per step, contexts cycle
+    through 20 keys; LRU sizes above and below the cycle."""
+    store = np.full(5000, 7, np.uint16)
+    period = (np.arange(20) * 13 % 97 + 100).astype(np.uint16)
+    truth = np.stack([np.tile(np.roll(period, r), 12) for r in range(3)])
+    st = gpu_store(store)
+    for lru in (10, 20, 32):
+        p = dict(n_max=16, n_min=2, k=50, m=4, c=8, alpha=(1,))
+        g = GpuReplay([st], truth, lru=lru, **p).run(max_steps=1000)
+        o = oracle.replay([store], truth, lru=lru, **p, max_steps=1000)
+        for f in ("accept", "hits", "lookups", "pos"):
+            assert (g[f] == o[f]).all(), (lru, f)
+        assert (g["hits"] == (truth.shape[1] - 16 - 20 if lru >= 20 else 0)).all()
 
 
 # -------------------------------------------------------------- edge cases --
