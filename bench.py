@@ -29,7 +29,7 @@ if ROOT not in sys.path:
 import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
-WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "build": 3}
+WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "build": 3, "copy": 0}
 
 
 def log(*a):
@@ -138,6 +138,8 @@ def main():
         return run_replay(args)
     if args.workload == "build":
         return run_build(args)
+    if args.workload == "copy":
+        return run_copy(args)
     cfg = WORKLOADS[args.workload]
     p = dict(synth.PARAMS)
     c, alpha = p["c"], tuple(p["alpha"])
@@ -346,6 +348,27 @@ def run_build(args):
         "config": {"workload": "SA build, 1B general + 10M project stores"}, "roofline": None, "builds": out,
     }
     print(json.dumps(line), flush=True)
+
+
+def run_copy(args):
+    """A plain device-to-device copy of 1 GiB: the reference for scaling
+    hardware traffic counters to bytes."""
+    import torch
+
+    dev = torch.device("cuda", 0)
+    src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(args.warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / max(args.steps, 1)
+    print(json.dumps({"metric": "device copy GB/s (1 GiB read + 1 GiB written per copy)", "value": 2 * (1 << 30) / dt / 1e9,
+                      "unit": "GB/s", "bytes_read_per_copy": 1 << 30, "bytes_written_per_copy": 1 << 30,
+                      "steps": args.steps, "warmup": args.warmup, "n_gpus": 1}), flush=True)
 
 
 if __name__ == "__main__":
