@@ -504,7 +504,7 @@ __global__ void __launch_bounds__(1024) k_tree_classify(const int32_t* __restric
 }
 
 template <int NT, int MAXM>
-__global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ taken,
+__global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__ taken,
                                                   const uint8_t* __restrict__ cont_len,
                                                   const uint16_t* __restrict__ cont_tok,
                                                   const uint16_t* __restrict__ ctx, int L, int S, int k, int m, int c,
@@ -754,6 +754,18 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       const uint16_t e = E[p * m + d - 1];
       return wide ? A[e] - ap : (uint32_t)e;
     };
+    // The weights of all depths of string p, fetched together (the depth
+    // bound m is uniform, so every load issues before any is used); depths
+    // that are not p's own nodes hold unused values.
+    auto row_w = [&](int p, uint32_t (&wv)[MAXM + 1]) {
+      const uint32_t ap = wide ? A[p] : 0u;
+#pragma unroll
+      for (int d = 1; d <= MAXM; ++d) wv[d] = d <= m ? (uint32_t)E[p * m + d - 1] : 0u;
+      if (wide) {
+#pragma unroll
+        for (int d = 1; d <= MAXM; ++d) wv[d] = d <= m ? A[wv[d]] - ap : 0u;
+      }
+    };
 
     // 5. the need-th largest weight W* and how many nodes of weight W* to
     //    take (in (p, d) order).  Most nodes are light, so weights below 8
@@ -770,16 +782,17 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
 #pragma unroll
       for (int v = 0; v < 8; ++v) r[v] = 0;
       for (int p = p0; p < p1; ++p) {
-        const uint32_t ap = wide ? A[p] : 0u;
         const int l = lcp[p], ml = mlen[p];
+        uint32_t wv[MAXM + 1];
+        row_w(p, wv);
 #pragma unroll
         for (int d = 1; d <= MAXM; ++d) {
-          if (d <= l || d > ml) continue;
-          const uint32_t W = node_w(p, d, ap);
+          const bool own = d > l && d <= ml;
+          const uint32_t W = wv[d];
 #pragma unroll
-          for (int v = 0; v < 8; ++v) r[v] += (W == (uint32_t)v);
-          if (W >= 256) ++rbig;
-          else if (W >= 8) atomicAdd(&s_hist[W], 1u);
+          for (int v = 0; v < 8; ++v) r[v] += (own && W == (uint32_t)v) ? 1u : 0u;
+          rbig += (own && W >= 256) ? 1u : 0u;
+          if (own && W >= 8 && W < 256) atomicAdd(&s_hist[W], 1u);
         }
       }
 #pragma unroll
@@ -887,14 +900,14 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
     uint32_t gt = 0, eq = 0;
     if (need > 0) {
       for (int p = p0; p < p1; ++p) {
-        const uint32_t ap = wide ? A[p] : 0u;
         const int l = lcp[p], ml = mlen[p];
+        uint32_t wv[MAXM + 1];
+        row_w(p, wv);
 #pragma unroll
         for (int d = 1; d <= MAXM; ++d) {
-          if (d <= l || d > ml) continue;
-          const uint32_t W = node_w(p, d, ap);
-          gt += W > wstar;
-          eq += W == wstar;
+          const bool own = d > l && d <= ml;
+          gt += (own && wv[d] > wstar) ? 1u : 0u;
+          eq += (own && wv[d] == wstar) ? 1u : 0u;
         }
       }
     }
@@ -904,12 +917,13 @@ __global__ void __launch_bounds__(NT) k_tree_fast(const int32_t* __restrict__ ta
       uint32_t o = 1 + gt_ex + (eq_ex < take_eq ? eq_ex : take_eq);
       uint32_t r = eq_ex;
       for (int p = p0; p < p1; ++p) {
-        const uint32_t ap = wide ? A[p] : 0u;
         const int l = lcp[p], ml = mlen[p];
+        uint32_t wv[MAXM + 1];
+        row_w(p, wv);
 #pragma unroll
         for (int d = 1; d <= MAXM; ++d) {
           if (d <= l || d > ml) continue;
-          const uint32_t W = node_w(p, d, ap);
+          const uint32_t W = wv[d];
           bool keep = W > wstar;
           if (W == wstar) keep = r++ < take_eq;
           if (keep && o < (uint32_t)FC_MAX_TREE_ROWS) {
