@@ -778,9 +778,9 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     if (tid == 0) s_pick[2] = 0;
     __syncthreads();
     if (need > 0) {
-      uint32_t r[8], rbig = 0;
-#pragma unroll
-      for (int v = 0; v < 8; ++v) r[v] = 0;
+      // weights 1 and 2 (the bulk: unshared continuation tails) are counted
+      // in registers, other light weights with LDS atomics
+      uint32_t r1 = 0, r2 = 0, rbig = 0;
       for (int p = p0; p < p1; ++p) {
         const int l = lcp[p], ml = mlen[p];
         uint32_t wv[MAXM + 1];
@@ -789,16 +789,16 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
         for (int d = 1; d <= MAXM; ++d) {
           const bool own = d > l && d <= ml;
           const uint32_t W = wv[d];
-#pragma unroll
-          for (int v = 0; v < 8; ++v) r[v] += (own && W == (uint32_t)v) ? 1u : 0u;
-          rbig += (own && W >= 256) ? 1u : 0u;
-          if (own && W >= 8 && W < 256) atomicAdd(&s_hist[W], 1u);
+          r1 += (own && W == 1u) ? 1u : 0u;
+          r2 += (own && W == 2u) ? 1u : 0u;
+          rbig += (own && W >= 256u) ? 1u : 0u;
+          if (own && W != 1u && W != 2u && W < 256u) atomicAdd(&s_hist[W], 1u);
         }
       }
-#pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        const uint32_t x = fc::wave_sum_u32(r[v]);
-        if (lane == 0 && x) atomicAdd(&s_hist[v], x);
+      {
+        const uint32_t x1 = fc::wave_sum_u32(r1), x2 = fc::wave_sum_u32(r2);
+        if (lane == 0 && x1) atomicAdd(&s_hist[1], x1);
+        if (lane == 0 && x2) atomicAdd(&s_hist[2], x2);
       }
       const uint32_t xb = fc::wave_sum_u32(rbig);
       if (lane == 0 && xb) atomicAdd(&s_pick[2], xb);
@@ -992,6 +992,47 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   if (tid == 0) num_nodes[b] = err ? -1 : num;
 }
 
+template <int MAXM>
+fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok, const uint16_t* ctx,
+                      int32_t B, int32_t L, int32_t S, int32_t k, int32_t m, fc_tree_params t, Alpha a,
+                      const TreeLayout& full, int32_t* num_nodes, int32_t* node_tok, int32_t* parent,
+                      uint32_t* weight, int32_t* pos_ids, int32_t* mask, const int32_t* rows, int32_t n_rows, void* ws,
+                      hipStream_t stream) {
+  // light queries (T <= 1024) in small-LDS workgroups, the rest in full-LDS
+  // ones, each launch walking its own list of queries
+  const int t_small = k < kSmallClass ? k : kSmallClass;
+  int32_t* lists = (int32_t*)ws;
+  int32_t* counts = lists + 2 * (size_t)B;
+  hipLaunchKernelGGL(k_tree_classify, dim3(1), dim3(1024), 0, stream, taken, B, S, k, t_small, rows, n_rows, lists,
+                     counts);
+  FC_CHECK_LAUNCH();
+  // row loads: 16-byte vectors when every query's row is 16-byte aligned,
+  // else 32-bit words when 4-byte aligned, else single tokens
+  int words = 0;
+  if ((((uintptr_t)cont_tok) & 15) == 0 && ((size_t)k * m) % 8 == 0) words = 2;
+  else if ((((uintptr_t)cont_tok) & 3) == 0 && ((size_t)k * m) % 2 == 0) words = 1;
+  const TreeLayout small = tree_layout(t_small, m);
+  if (small.total > 64 * 1024)
+    (void)hipFuncSetAttribute((const void*)k_tree_fast<256, MAXM>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)small.total);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL((k_tree_fast<256, MAXM>), dim3(B), dim3(256), small.total, stream, taken, cont_len, cont_tok,
+                     ctx, L, S, k, m, t.c, a, lists, counts, t_small, words, rows, n_rows, num_nodes, node_tok, parent,
+                     weight, pos_ids, mask);
+  FC_CHECK_LAUNCH();
+  if (k > t_small) {
+    if (full.total > 64 * 1024)
+      (void)hipFuncSetAttribute((const void*)k_tree_fast<1024, MAXM>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)full.total);
+    (void)hipGetLastError();
+    hipLaunchKernelGGL((k_tree_fast<1024, MAXM>), dim3(B), dim3(1024), full.total, stream, taken, cont_len, cont_tok,
+                       ctx, L, S, k, m, t.c, a, lists + B, counts + 1, k, words, rows, n_rows, num_nodes, node_tok,
+                       parent, weight, pos_ids, mask);
+    FC_CHECK_LAUNCH();
+  }
+  return FC_OK;
+}
+
 }  // namespace
 
 extern "C" size_t fc_build_tree_workspace_bytes(int32_t B) {
@@ -1022,41 +1063,10 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
   const TreeLayout full = tree_layout(k, m);
   if (full.total + static_lds > (size_t)max_lds) return FC_ERR_UNSUPPORTED;
   (void)hipGetLastError();
-  if (m <= 16) {
-    // light queries (T <= 1024) in small-LDS workgroups, the rest in full-LDS
-    // ones, each launch walking its own list of queries
-    const int t_small = k < kSmallClass ? k : kSmallClass;
-    int32_t* lists = (int32_t*)ws;
-    int32_t* counts = lists + 2 * (size_t)B;
-    hipLaunchKernelGGL(k_tree_classify, dim3(1), dim3(1024), 0, stream, taken, B, S, k, t_small, rows, n_rows, lists,
-                       counts);
-    FC_CHECK_LAUNCH();
-    // row loads: 16-byte vectors when every query's row is 16-byte aligned,
-    // else 32-bit words when 4-byte aligned, else single tokens
-    int words = 0;
-    if ((((uintptr_t)cont_tok) & 15) == 0 && ((size_t)k * m) % 8 == 0) words = 2;
-    else if ((((uintptr_t)cont_tok) & 3) == 0 && ((size_t)k * m) % 2 == 0) words = 1;
-    const TreeLayout small = tree_layout(t_small, m);
-    if (small.total > 64 * 1024)
-      (void)hipFuncSetAttribute((const void*)k_tree_fast<256, 16>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)small.total);
-    (void)hipGetLastError();
-    hipLaunchKernelGGL((k_tree_fast<256, 16>), dim3(B), dim3(256), small.total, stream, taken, cont_len, cont_tok,
-                       ctx, L, S, k, m, t.c, a, lists, counts, t_small, words, rows, n_rows, num_nodes, node_tok,
-                       parent, weight, pos_ids, mask);
-    FC_CHECK_LAUNCH();
-    if (k > t_small) {
-      if (full.total > 64 * 1024)
-        (void)hipFuncSetAttribute((const void*)k_tree_fast<1024, 16>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  (int)full.total);
-      (void)hipGetLastError();
-      hipLaunchKernelGGL((k_tree_fast<1024, 16>), dim3(B), dim3(1024), full.total, stream, taken, cont_len,
-                         cont_tok, ctx, L, S, k, m, t.c, a, lists + B, counts + 1, k, words, rows, n_rows, num_nodes,
-                         node_tok, parent, weight, pos_ids, mask);
-      FC_CHECK_LAUNCH();
-    }
-    return FC_OK;
-  }
+  if (m <= 10) return launch_fast<10>(taken, cont_len, cont_tok, ctx, B, L, S, k, m, t, a, full, num_nodes, node_tok,
+                                      parent, weight, pos_ids, mask, rows, n_rows, ws, stream);
+  if (m <= 16) return launch_fast<16>(taken, cont_len, cont_tok, ctx, B, L, S, k, m, t, a, full, num_nodes, node_tok,
+                                      parent, weight, pos_ids, mask, rows, n_rows, ws, stream);
   if (full.total > 64 * 1024)
     (void)hipFuncSetAttribute((const void*)k_tree_any, hipFuncAttributeMaxDynamicSharedMemorySize, (int)full.total);
   (void)hipGetLastError();

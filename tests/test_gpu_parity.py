@@ -147,7 +147,7 @@ def test_first_workload_full_batch():
     ctx = synth.queries(1)
     st = gpu_store(t)
     st_pairs = fc.Store(st.tokens, st.sa, st.bucket, pair_vocab=synth.VOCAB)
-    for (k, m, c) in ((P["k"], P["m"], P["c"]), (1000, 10, 64), (257, 3, 5), (1, 1, 1)):
+    for (k, m, c) in ((P["k"], P["m"], P["c"]), (1000, 10, 64), (257, 3, 5), (1200, 13, 40), (1, 1, 1)):
         say(f"workload 1: k={k} m={m} c={c}")
         p = dict(P, k=k, m=m)
         g = gpu_pipeline([st_pairs if k == P["k"] else st], ctx, p, (1,), c)
