@@ -5,7 +5,8 @@ One step = one batch of queries through the whole draft-stage path on the
 GPU: fc_retrieve (longest-suffix match in both stores + continuation gather),
 fc_build_tree (weighted trie, top-c, mask, position ids) and fc_verify_accept
 (longest accepted path against the true next tokens).  Stores, suffix arrays,
-first-token and two-token tables, query contexts and target tokens are
+first-token and two-token tables, inline-prefix records, query contexts and
+target tokens are
 resident in HBM before the timed region; the suffix arrays and tables are
 built once, untimed, with fc_datastore_build / fc_store_prepare(_pairs) (the
 paper builds its datastores offline).
@@ -159,7 +160,7 @@ def main():
         tok = torch.from_numpy(t).to(dev)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
-        st = fc.Store(tok, pair_vocab=synth.VOCAB)
+        st = fc.Store(tok, pair_vocab=synth.VOCAB, records=True)
         torch.cuda.synchronize()
         build_s.append(time.perf_counter() - t1)
         stores.append(st)
@@ -282,7 +283,7 @@ def run_replay(args):
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     texts = [synth.store(3, r) for r in synth.store_roles(3)]
-    stores = [fc.Store(torch.from_numpy(t).to(dev), pair_vocab=synth.VOCAB) for t in texts]
+    stores = [fc.Store(torch.from_numpy(t).to(dev), pair_vocab=synth.VOCAB, records=True) for t in texts]
     truth = synth.truth()
     rp = GpuReplay(stores, truth, **p)
     rp.run(max_steps=args.warmup)  # warm-up steps, then a fresh replay is timed

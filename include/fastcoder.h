@@ -106,6 +106,24 @@ uint64_t fc_pair_table_entries(uint32_t V);
 fc_status fc_store_prepare_pairs(const uint16_t* tokens, const uint32_t* sa, uint64_t n, uint32_t V,
                                  uint32_t* pair_out, hipStream_t stream);
 
+/*
+ * Optional inline-prefix records of a store, for the searches that start
+ * from the two-token table.  Record i is FC_RECORD_BYTES = 32 bytes: sa[i]
+ * as a uint32, then the FC_RECORD_TOKENS = 14 tokens T[sa[i]+2 ..
+ * sa[i]+16) as uint16 (0 for positions at or past n).  A suffix search of
+ * Section III-A then reads one record per probe and decides the comparison
+ * from it alone (the table fixes the first two tokens and n_max <= 16), so
+ * a probe costs one memory round trip and no second, dependent read of the
+ * text.  A 0 stored past the end compares exactly like the end itself:
+ * query tokens are never 0.  rec_out is fc_record_bytes(n) bytes (32 GB at
+ * n = 1e9), 32-byte aligned, written on `stream`.
+ */
+#define FC_RECORD_BYTES 32
+#define FC_RECORD_TOKENS 14
+uint64_t fc_record_bytes(uint64_t n);
+fc_status fc_store_prepare_records(const uint16_t* tokens, const uint32_t* sa, uint64_t n, void* rec_out,
+                                   hipStream_t stream);
+
 /* A read-only view of one store; all pointers are device pointers. */
 typedef struct fc_store {
   const uint16_t* tokens; /* [n] text */
@@ -114,6 +132,7 @@ typedef struct fc_store {
   uint64_t n;             /* tokens in the store, < 2^32 - 1 */
   const uint32_t* pair;   /* optional two-token table from fc_store_prepare_pairs, or NULL */
   uint32_t pair_vocab;    /* its V (ignored when pair is NULL) */
+  const void* rec;        /* optional records from fc_store_prepare_records (needs pair), or NULL */
 } fc_store;
 
 /* ------------------------------------------------------------------------ */
@@ -132,7 +151,9 @@ typedef struct fc_retrieve_params {
  * (Section III-A; two stores, the repository store first and the common store
  * second, searched side by side: Section IV-A, Section IV-C).
  *
- * stores (host) [S] : store views, S in 1..FC_MAX_SOURCES.
+ * stores (host) [S] : store views, S in 1..FC_MAX_SOURCES.  A store with
+ *                    records must also have a two-token table, and its
+ *                    records must be 32-byte aligned (FC_ERR_INVALID).
  * ctx [B][L]        : the last L context tokens of each query.
  * For each query and store: n_hi = min(n_max, L, trailing non-zero tokens of
  * the context); for n = n_hi down to n_min the suffix q = ctx[L-n..L) is

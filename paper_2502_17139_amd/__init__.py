@@ -30,7 +30,7 @@ STATUS = {0: "FC_OK", 1: "FC_ERR_INVALID", 2: "FC_ERR_WORKSPACE", 3: "FC_ERR_DEV
 EXPORTS = (
     "fc_abi_version", "fc_status_string",
     "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_store_prepare",
-    "fc_pair_table_entries", "fc_store_prepare_pairs",
+    "fc_pair_table_entries", "fc_store_prepare_pairs", "fc_record_bytes", "fc_store_prepare_records",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
     "fc_verify_accept", "fc_targets_from_truth",
 )
@@ -46,7 +46,8 @@ class FcError(RuntimeError):
 
 class FcStore(ctypes.Structure):
     _fields_ = [("tokens", ctypes.c_void_p), ("sa", ctypes.c_void_p), ("bucket", ctypes.c_void_p),
-                ("n", ctypes.c_uint64), ("pair", ctypes.c_void_p), ("pair_vocab", ctypes.c_uint32)]
+                ("n", ctypes.c_uint64), ("pair", ctypes.c_void_p), ("pair_vocab", ctypes.c_uint32),
+                ("rec", ctypes.c_void_p)]
 
 
 class FcRetrieveParams(ctypes.Structure):
@@ -80,6 +81,10 @@ def lib() -> ctypes.CDLL:
     L.fc_pair_table_entries.argtypes = [u32]
     L.fc_store_prepare_pairs.restype = ctypes.c_int
     L.fc_store_prepare_pairs.argtypes = [vp, vp, u64, u32, vp, vp]
+    L.fc_record_bytes.restype = u64
+    L.fc_record_bytes.argtypes = [u64]
+    L.fc_store_prepare_records.restype = ctypes.c_int
+    L.fc_store_prepare_records.argtypes = [vp, vp, u64, vp, vp]
     L.fc_retrieve_workspace_bytes.restype = sz
     L.fc_retrieve_workspace_bytes.argtypes = [i32, i32, FcRetrieveParams]
     L.fc_retrieve.restype = ctypes.c_int
@@ -167,18 +172,36 @@ def fc_store_prepare_pairs(tokens: torch.Tensor, sa: torch.Tensor, V: int, pair_
     return pair_out
 
 
+def fc_record_bytes(n: int) -> int:
+    return int(lib().fc_record_bytes(n))
+
+
+def fc_store_prepare_records(tokens: torch.Tensor, sa: torch.Tensor, rec_out: torch.Tensor | None = None,
+                             stream=None) -> torch.Tensor:
+    """Inline-prefix records (uint8[32*n]: sa[i] then T[sa[i]+2 .. sa[i]+16))."""
+    if rec_out is None:
+        rec_out = _empty(max(fc_record_bytes(tokens.numel()), 1), torch.uint8, tokens.device)
+    _check("fc_store_prepare_records", lib().fc_store_prepare_records(_ptr(tokens), _ptr(sa), tokens.numel(),
+                                                                     _ptr(rec_out), _stream(stream)))
+    return rec_out
+
+
 class Store:
     """A datastore resident on the GPU: tokens, suffix array, bucket table and,
-    with pair_vocab = V, the optional two-token table."""
+    with pair_vocab = V, the optional two-token table; with records = True
+    (needs pair_vocab) also the inline-prefix records."""
 
     def __init__(self, tokens: torch.Tensor, sa: torch.Tensor | None = None, bucket: torch.Tensor | None = None,
-                 pair_vocab: int | None = None, stream=None):
+                 pair_vocab: int | None = None, records: bool = False, stream=None):
         self.tokens = tokens
         self.sa = fc_datastore_build(tokens, stream=stream) if sa is None else sa
         self.bucket = fc_store_prepare(tokens, self.sa, stream=stream) if bucket is None else bucket
         self.pair_vocab = pair_vocab or 0
         self.pair = (fc_store_prepare_pairs(tokens, self.sa, pair_vocab, stream=stream)
                      if pair_vocab else None)
+        if records and not pair_vocab:
+            raise ValueError("records need the two-token table (pair_vocab)")
+        self.rec = fc_store_prepare_records(tokens, self.sa, stream=stream) if records else None
 
     @property
     def n(self) -> int:
@@ -186,7 +209,8 @@ class Store:
 
     def view(self) -> FcStore:
         return FcStore(self.tokens.data_ptr(), self.sa.data_ptr(), self.bucket.data_ptr(), self.n,
-                       None if self.pair is None else self.pair.data_ptr(), self.pair_vocab)
+                       None if self.pair is None else self.pair.data_ptr(), self.pair_vocab,
+                       None if self.rec is None else self.rec.data_ptr())
 
 
 # ------------------------------------------------------------ retrieval ----

@@ -12,7 +12,10 @@
 // Each search starts from the store's two-token table when it has one (one
 // table read replaces the top ~25 levels of the search on a 1B-token store)
 // or else from its first-token bucket, and compares only the tokens the
-// table does not already fix.  The wave then keeps, per store, the longest n whose range
+// table does not already fix.  With the store's inline-prefix records a
+// probe is one 32-byte record read and two levels are resolved per round
+// trip; without them each probe reads the suffix-array entry (prefetched a
+// level ahead) and then the text.  The wave then keeps, per store, the longest n whose range
 // is non-empty and fills the k slots in store priority order.
 //
 // k_offsets + k_gather: the kept slots of the whole batch are numbered
@@ -41,6 +44,7 @@ struct StoreArgs {
   const uint32_t* sa[FC_MAX_SOURCES];
   const uint32_t* bucket[FC_MAX_SOURCES];
   const uint32_t* pair[FC_MAX_SOURCES];
+  const uint4* rec[FC_MAX_SOURCES];
   uint32_t n[FC_MAX_SOURCES];
   uint32_t pair_vocab[FC_MAX_SOURCES];
 };
@@ -70,6 +74,69 @@ __device__ __forceinline__ int cmp_suffix(const uint16_t* __restrict__ T, uint32
     }
   }
   return 0;
+}
+
+// A pattern's tokens at offsets 2..15 packed two per word like a record's
+// token words (offset 2 + 2x in the low half of word x), each word rotated
+// by 16 bits so that one unsigned compare orders two tokens
+// lexicographically; positions at or past n are masked out on both sides.
+struct RecQuery {
+  uint32_t rot[FC_RECORD_TOKENS / 2];
+  uint32_t mask[FC_RECORD_TOKENS / 2];
+};
+
+__device__ __forceinline__ uint32_t rot16(uint32_t x) { return __builtin_amdgcn_alignbit(x, x, 16); }
+
+__device__ __forceinline__ RecQuery rec_query(const uint16_t* q, int n) {
+  RecQuery r;
+#pragma unroll
+  for (int x = 0; x < FC_RECORD_TOKENS / 2; ++x) {
+    const int o = 2 + 2 * x;
+    const uint32_t a = o < n ? q[o] : 0u;
+    const uint32_t b = o + 1 < n ? q[o + 1] : 0u;
+    r.rot[x] = rot16(a | (b << 16));
+    r.mask[x] = (o < n ? 0xFFFFu : 0u) | (o + 1 < n ? 0xFFFF0000u : 0u);
+  }
+  return r;
+}
+
+// Record (two 16-byte halves) against the pattern: -1 below, 0 starts
+// with it, +1 above.  The first differing word decides.
+__device__ __forceinline__ int rec_cmp(const uint4& h0, const uint4& h1, const RecQuery& r) {
+  const uint32_t t[FC_RECORD_TOKENS / 2] = {h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+  int res = 0;
+#pragma unroll
+  for (int x = FC_RECORD_TOKENS / 2 - 1; x >= 0; --x) {
+    const uint32_t u = rot16(t[x] & r.mask[x]);
+    res = u != r.rot[x] ? (u < r.rot[x] ? -1 : 1) : res;
+  }
+  return res;
+}
+
+// Lower (upper = false) or upper bound of the pattern in suffix-array range
+// [lo, hi) over the records: two levels of the binary search per memory
+// round trip, by loading the midpoint's record together with the records
+// of both possible next midpoints.
+__device__ __forceinline__ uint32_t rec_search(const uint4* __restrict__ R, uint32_t lo, uint32_t hi,
+                                               const RecQuery& rq, bool upper) {
+  while (lo < hi) {
+    const uint32_t mid = lo + ((hi - lo) >> 1);
+    const uint32_t lmid = lo < mid ? lo + ((mid - lo) >> 1) : mid;
+    const uint32_t rmid = mid + 1 < hi ? (mid + 1) + ((hi - mid - 1) >> 1) : mid;
+    const uint4 m0 = R[2 * (uint64_t)mid], m1 = R[2 * (uint64_t)mid + 1];
+    const uint4 l0 = R[2 * (uint64_t)lmid], l1 = R[2 * (uint64_t)lmid + 1];
+    const uint4 r0 = R[2 * (uint64_t)rmid], r1 = R[2 * (uint64_t)rmid + 1];
+    const int c = rec_cmp(m0, m1, rq);
+    const bool right = upper ? c <= 0 : c < 0;
+    if (right) lo = mid + 1; else hi = mid;
+    if (lo < hi) {
+      const uint32_t nm = right ? rmid : lmid;
+      const uint4 a0 = right ? r0 : l0, a1 = right ? r1 : l1;
+      const int c2 = rec_cmp(a0, a1, rq);
+      if (upper ? c2 <= 0 : c2 < 0) lo = nm + 1; else hi = nm;
+    }
+  }
+  return lo;
 }
 
 __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, const uint16_t* __restrict__ ctx,
@@ -136,11 +203,14 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
           hi = st.bucket[s][q[0] + 1];
         }
       }
-      // Binary search; the suffix-array entries of both possible next
-      // midpoints are fetched together with the current probe's text, so
-      // each level costs one dependent round trip.  When the table already
-      // covers the whole pattern the range is final.
-      if (from < n && lo < hi) {
+      // Binary search, over the records when the store has them; else the
+      // suffix-array entries of both possible next midpoints are fetched
+      // together with the current probe's text, so each level costs one
+      // dependent round trip.  When the table already covers the whole
+      // pattern the range is final.
+      if (from < n && lo < hi && from == 2 && st.rec[s] != nullptr) {
+        lo = rec_search(st.rec[s], lo, hi, rec_query(q, n), upper);
+      } else if (from < n && lo < hi) {
         uint32_t mid = lo + ((hi - lo) >> 1);
         uint32_t j = SA[mid];
         for (;;) {
@@ -403,6 +473,8 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
     st.pair[s] = x.pair;
     st.pair_vocab[s] = x.pair ? x.pair_vocab : 0u;
     if (x.pair && (x.pair_vocab < 1 || x.pair_vocab > 65536)) return FC_ERR_INVALID;
+    if (x.rec && (!x.pair || ((uintptr_t)x.rec & (FC_RECORD_BYTES - 1)))) return FC_ERR_INVALID;
+    st.rec[s] = x.n > 0 ? (const uint4*)x.rec : nullptr;
   }
   if (B == 0) return FC_OK;
   if (!ctx || !match_n || !range_lo || !range_cnt || !taken || !cont_pos || !cont_src || !cont_len || !cont_tok)

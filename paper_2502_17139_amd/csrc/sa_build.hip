@@ -429,6 +429,26 @@ __global__ void __launch_bounds__(256) k_pairs(const uint16_t* __restrict__ tok,
   }
 }
 
+// Inline-prefix records: one thread per suffix-array position writes
+// {sa[i], T[sa[i]+2 .. sa[i]+16)} as two 16-byte stores (0 past the end).
+__global__ void __launch_bounds__(256) k_records(const uint16_t* __restrict__ tok, const uint32_t* __restrict__ sa,
+                                                 uint32_t n, uint4* __restrict__ rec) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t j = sa[i];
+  uint32_t w[8];
+  w[0] = j;
+#pragma unroll
+  for (int x = 0; x < FC_RECORD_TOKENS / 2; ++x) {
+    const uint64_t p = (uint64_t)j + 2 + 2 * x;
+    const uint32_t a = p < n ? tok[p] : 0u;
+    const uint32_t b = p + 1 < n ? tok[p + 1] : 0u;
+    w[1 + x] = a | (b << 16);
+  }
+  rec[2 * i] = make_uint4(w[0], w[1], w[2], w[3]);
+  rec[2 * i + 1] = make_uint4(w[4], w[5], w[6], w[7]);
+}
+
 struct BuildWs {
   uint32_t* rank;
   uint64_t* keys[2];
@@ -604,6 +624,20 @@ extern "C" fc_status fc_store_prepare_pairs(const uint16_t* tokens, const uint32
   const uint64_t threads = n + 1;
   hipLaunchKernelGGL(k_pairs, dim3((uint32_t)((threads + 255) / 256)), dim3(256), 0, stream, tokens, sa,
                      (uint32_t)n, V, pair_out);
+  FC_CHECK_LAUNCH();
+  return FC_OK;
+}
+
+extern "C" uint64_t fc_record_bytes(uint64_t n) { return (uint64_t)FC_RECORD_BYTES * n; }
+
+extern "C" fc_status fc_store_prepare_records(const uint16_t* tokens, const uint32_t* sa, uint64_t n, void* rec_out,
+                                              hipStream_t stream) {
+  if (n >= 0xFFFFFFFFull) return FC_ERR_INVALID;
+  if (n == 0) return FC_OK;
+  if (!tokens || !sa || !rec_out || ((uintptr_t)rec_out & (FC_RECORD_BYTES - 1))) return FC_ERR_INVALID;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(k_records, dim3(fc::div_up(n, 256)), dim3(256), 0, stream, tokens, sa, (uint32_t)n,
+                     (uint4*)rec_out);
   FC_CHECK_LAUNCH();
   return FC_OK;
 }

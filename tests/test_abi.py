@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_status_strings(L):
-    assert L.fc_abi_version() == 1
+    assert L.fc_abi_version() == 2
     for code, name in fc.STATUS.items():
         assert L.fc_status_string(code).decode().startswith(name)
     assert L.fc_status_string(99).decode() == "FC_ERR_UNKNOWN"
@@ -84,6 +84,12 @@ def test_retrieve_rejects_null_outputs_and_big_store(L):
     args[0] = views
     assert L.fc_retrieve(*args) == 1
     views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, 1, 70000))  # pair vocabulary out of range
+    args[0] = views
+    assert L.fc_retrieve(*args) == 1
+    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, None, 0, 64))  # records without a two-token table
+    args[0] = views
+    assert L.fc_retrieve(*args) == 1
+    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, 1, 100, 48))  # records not 32-byte aligned
     args[0] = views
     assert L.fc_retrieve(*args) == 1
 
@@ -142,6 +148,18 @@ def test_pair_table_size_and_rejects(L):
     assert L.fc_store_prepare_pairs(one, one, 10, 65537, one, None) == 1
     assert L.fc_store_prepare_pairs(one, one, 10, 5, None, None) == 1
     assert L.fc_store_prepare_pairs(None, one, 10, 5, one, None) == 1
+
+
+def test_record_size_and_rejects(L):
+    assert L.fc_record_bytes(1_001_999_999) == 32 * 1_001_999_999
+    assert L.fc_record_bytes(0) == 0
+    one, aligned = ctypes.c_void_p(8), ctypes.c_void_p(64)
+    assert L.fc_store_prepare_records(one, one, 10, ctypes.c_void_p(48), None) == 1  # misaligned
+    assert L.fc_store_prepare_records(one, one, 10, None, None) == 1
+    assert L.fc_store_prepare_records(None, one, 10, aligned, None) == 1
+    assert L.fc_store_prepare_records(one, None, 10, aligned, None) == 1
+    assert L.fc_store_prepare_records(one, one, 1 << 32, aligned, None) == 1
+    assert L.fc_store_prepare_records(None, None, 0, None, None) == 0  # nothing to write
 
 
 def test_verify_and_build_reject(L):

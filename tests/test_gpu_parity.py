@@ -140,6 +140,23 @@ def test_pair_table():
         fc.fc_store_prepare_pairs(st.tokens, st.sa, 49)
 
 
+def test_records():
+    """Record i = {sa[i], T[sa[i]+2 .. sa[i]+16)} with 0 past the end."""
+    for seed, n in enumerate((1, 2, 17, 3000, 70001)):
+        t = synth.random_text(70 + seed, n, 500, 0.05)
+        say(f"records n={n}")
+        st = fc.Store(dev(t), pair_vocab=500, records=True)
+        torch.cuda.synchronize()
+        sa = host(st.sa).astype(np.int64)
+        rec = host(st.rec).view(np.uint32).reshape(n, 8)
+        assert (rec[:, 0] == sa).all()
+        padded = np.concatenate([t.astype(np.uint32), np.zeros(16, np.uint32)])
+        idx = sa[:, None] + 2 + np.arange(14)[None, :]
+        want = padded[idx]
+        got = np.stack([rec[:, 1:] & 0xFFFF, rec[:, 1:] >> 16], axis=2).reshape(n, 14)
+        assert (got == want).all()
+
+
 # --------------------------------------------------------------- retrieval --
 
 def test_first_workload_full_batch():
@@ -147,10 +164,12 @@ def test_first_workload_full_batch():
     ctx = synth.queries(1)
     st = gpu_store(t)
     st_pairs = fc.Store(st.tokens, st.sa, st.bucket, pair_vocab=synth.VOCAB)
+    st_rec = fc.Store(st.tokens, st.sa, st.bucket, pair_vocab=synth.VOCAB, records=True)
+    variants = {P["k"]: st_rec, 1000: st_pairs}
     for (k, m, c) in ((P["k"], P["m"], P["c"]), (1000, 10, 64), (257, 3, 5), (1200, 13, 40), (1, 1, 1)):
         say(f"workload 1: k={k} m={m} c={c}")
         p = dict(P, k=k, m=m)
-        g = gpu_pipeline([st_pairs if k == P["k"] else st], ctx, p, (1,), c)
+        g = gpu_pipeline([variants.get(k, st)], ctx, p, (1,), c)
         o = oracle_pipeline([t], ctx, p, (1,), c)
         compare_retrieve(g, o)
         compare_tree(g, o)
@@ -160,7 +179,7 @@ def test_first_workload_full_batch():
 def test_two_store_workload_full_batch():
     tp, tg = synth.store(2, "project"), synth.store(2, "general")
     ctx = synth.queries(2)
-    stores = [gpu_store(tp, synth.VOCAB), gpu_store(tg, synth.VOCAB)]
+    stores = [gpu_store(tp, synth.VOCAB, records=True), gpu_store(tg, synth.VOCAB, records=True)]
     say("workload 2: gpu")
     g = gpu_pipeline(stores, ctx, P, (1, 1), P["c"])
     say("workload 2: oracle")
@@ -168,6 +187,10 @@ def test_two_store_workload_full_batch():
     compare_retrieve(g, o)
     compare_tree(g, o)
     _check_accept(g, o, P["m"])
+    # two-token tables without records
+    plain = [fc.Store(x.tokens, x.sa, x.bucket, pair_vocab=synth.VOCAB) for x in stores]
+    g = gpu_pipeline(plain, ctx[:128], P, (1, 1), P["c"])
+    compare_retrieve(g, {f: v[:128] for f, v in o.items()})
     # unequal store weights, first-token tables only
     stores = [fc.Store(x.tokens, x.sa, x.bucket) for x in stores]
     g = gpu_pipeline(stores, ctx[:64], P, (3, 1), 32)
@@ -182,7 +205,7 @@ def test_headline_workload_sampled():
     tp, tg = synth.store(3, "project"), synth.store(3, "general")
     ctx = synth.queries(3)
     say("headline: building suffix arrays")
-    stores = [gpu_store(tp, synth.VOCAB), gpu_store(tg, synth.VOCAB)]
+    stores = [gpu_store(tp, synth.VOCAB, records=True), gpu_store(tg, synth.VOCAB, records=True)]
     torch.cuda.synchronize()
     say("headline: checking suffix arrays")
     for t, st in zip((tp, tg), stores):
@@ -257,7 +280,7 @@ def test_fuzz_small_stores(seed):
     if seed == 0:
         texts[0] = np.zeros(0, np.uint16)  # an empty store
     pv = vocab if seed % 2 else None
-    stores = [gpu_store(t, pv) if len(t) else fc.Store(dev(np.zeros(1, np.uint16))[:0],
+    stores = [gpu_store(t, pv, records=seed % 4 == 1) if len(t) else fc.Store(dev(np.zeros(1, np.uint16))[:0],
                                                     dev(np.zeros(1, np.uint32))[:0],
                                                     fc.fc_store_prepare(dev(np.zeros(1, np.uint16))[:0],
                                                                         dev(np.zeros(1, np.uint32))[:0]))
