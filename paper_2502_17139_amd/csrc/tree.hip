@@ -515,6 +515,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
                                                   int32_t* __restrict__ parent, uint32_t* __restrict__ weight,
                                                   int32_t* __restrict__ pos_ids, int32_t* __restrict__ mask) {
   constexpr int NW = NT / fc::kWave;
+  static_assert(NT >= FC_MAX_TREE_ROWS, "one thread per tree row");
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int s_seg[FC_MAX_SOURCES + 1];
   __shared__ int s_err;
@@ -526,6 +527,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   __shared__ uint16_t s_sel_p[FC_MAX_TREE_ROWS];
   __shared__ uint8_t s_sel_d[FC_MAX_TREE_ROWS];
   __shared__ int16_t s_par[FC_MAX_TREE_ROWS];
+  __shared__ uint64_t s_dball[FC_MAX_TREE_ROWS / fc::kWave][MAXM];
   __shared__ uint32_t s_pick[3];
 
   // This launch owns the queries in `list` (built by k_tree_classify);
@@ -939,11 +941,28 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     nsel = (int)(total_sel < (uint32_t)c ? total_sel : (uint32_t)c);
     if (tid == 0) s_sel_d[0] = 0;
     __syncthreads();
-    for (int r = tid + 1; r <= nsel; r += NT) {
-      const int d = s_sel_d[r];
-      int q = r - 1;
-      while (q > 0 && s_sel_d[q] != d - 1) --q;
-      s_par[r] = (int16_t)q;
+    // Parent of row r: the last row before it one level shallower (rows are
+    // in preorder and the kept set is ancestor-closed).  The first four
+    // waves hold one row per lane and publish, per depth, a ballot of their
+    // rows at that depth; row r then takes the highest such row below it,
+    // in its own wave or else in the nearest earlier one.
+    if (tid < FC_MAX_TREE_ROWS) {
+      const int g = tid / fc::kWave;
+      const int d = tid <= nsel ? (int)s_sel_d[tid] : -1;
+#pragma unroll
+      for (int D = 0; D < MAXM; ++D) {
+        const uint64_t bl = fc::ballot(d == D);
+        if (lane == 0) s_dball[g][D] = bl;
+      }
+    }
+    __syncthreads();
+    if (tid >= 1 && tid <= nsel) {
+      const int g = tid / fc::kWave;
+      const int D = (int)s_sel_d[tid] - 1;
+      uint64_t bl = s_dball[g][D] & fc::lanemask_lt();
+      int gg = g;
+      while (bl == 0 && gg > 0) bl = s_dball[--gg][D];
+      s_par[tid] = bl ? (int16_t)(gg * fc::kWave + 63 - __builtin_clzll(bl)) : (int16_t)0;
     }
     if (tid == 0) s_par[0] = -1;
     __syncthreads();
