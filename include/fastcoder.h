@@ -107,19 +107,24 @@ fc_status fc_store_prepare_pairs(const uint16_t* tokens, const uint32_t* sa, uin
                                  uint32_t* pair_out, hipStream_t stream);
 
 /*
- * Optional inline-prefix records of a store, for the searches that start
- * from the two-token table.  Record i is FC_RECORD_BYTES = 32 bytes: sa[i]
- * as a uint32, then the FC_RECORD_TOKENS = 14 tokens T[sa[i]+2 ..
- * sa[i]+16) as uint16 (0 for positions at or past n).  A suffix search of
- * Section III-A then reads one record per probe and decides the comparison
- * from it alone (the table fixes the first two tokens and n_max <= 16), so
- * a probe costs one memory round trip and no second, dependent read of the
- * text.  A 0 stored past the end compares exactly like the end itself:
- * query tokens are never 0.  rec_out is fc_record_bytes(n) bytes (32 GB at
- * n = 1e9), 32-byte aligned, written on `stream`.
+ * Optional inline-prefix records of a store.  Record i is FC_RECORD_BYTES =
+ * 64 bytes: sa[i] as a uint32, then the FC_RECORD_TOKENS = 30 tokens
+ * T[sa[i]+2 .. sa[i]+32) as uint16 (0 for positions at or past n).
+ * - A suffix search of Section III-A reads one record per probe and decides
+ *   the comparison from it alone (the two-token table fixes the first two
+ *   tokens and n_max <= 16), so a probe costs one memory round trip and no
+ *   second, dependent read of the text.  A 0 stored past the end compares
+ *   exactly like the end itself: query tokens are never 0.
+ * - The continuation gather of a match of length n >= 2 reads its m tokens
+ *   from the same record when they lie inside it (n + m <= 30 or so,
+ *   depending on alignment), so a kept slot costs one read of 64 contiguous
+ *   bytes at its suffix-array position instead of a suffix-array read
+ *   followed by a random read of the text.
+ * rec_out is fc_record_bytes(n) bytes (64 GB at n = 1e9, affordable in a
+ * 288 GB HBM part), 64-byte aligned, written on `stream`.
  */
-#define FC_RECORD_BYTES 32
-#define FC_RECORD_TOKENS 14
+#define FC_RECORD_BYTES 64
+#define FC_RECORD_TOKENS 30
 uint64_t fc_record_bytes(uint64_t n);
 fc_status fc_store_prepare_records(const uint16_t* tokens, const uint32_t* sa, uint64_t n, void* rec_out,
                                    hipStream_t stream);
@@ -153,7 +158,7 @@ typedef struct fc_retrieve_params {
  *
  * stores (host) [S] : store views, S in 1..FC_MAX_SOURCES.  A store with
  *                    records must also have a two-token table, and its
- *                    records must be 32-byte aligned (FC_ERR_INVALID).
+ *                    records must be 64-byte aligned (FC_ERR_INVALID).
  * ctx [B][L]        : the last L context tokens of each query.
  * For each query and store: n_hi = min(n_max, L, trailing non-zero tokens of
  * the context); for n = n_hi down to n_min the suffix q = ctx[L-n..L) is

@@ -178,7 +178,7 @@ def fc_record_bytes(n: int) -> int:
 
 def fc_store_prepare_records(tokens: torch.Tensor, sa: torch.Tensor, rec_out: torch.Tensor | None = None,
                              stream=None) -> torch.Tensor:
-    """Inline-prefix records (uint8[32*n]: sa[i] then T[sa[i]+2 .. sa[i]+16))."""
+    """Inline-prefix records (uint8[64*n]: sa[i] then T[sa[i]+2 .. sa[i]+32))."""
     if rec_out is None:
         rec_out = _empty(max(fc_record_bytes(tokens.numel()), 1), torch.uint8, tokens.device)
     _check("fc_store_prepare_records", lib().fc_store_prepare_records(_ptr(tokens), _ptr(sa), tokens.numel(),

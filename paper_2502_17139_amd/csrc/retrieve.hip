@@ -13,7 +13,7 @@
 // table read replaces the top ~25 levels of the search on a 1B-token store)
 // or else from its first-token bucket, and compares only the tokens the
 // table does not already fix.  With the store's inline-prefix records a
-// probe is one 32-byte record read and two levels are resolved per round
+// probe is one 32-byte read of a record and two levels are resolved per round
 // trip; without them each probe reads the suffix-array entry (prefetched a
 // level ahead) and then the text.  The wave then keeps, per store, the longest n whose range
 // is non-empty and fills the k slots in store priority order.
@@ -80,9 +80,13 @@ __device__ __forceinline__ int cmp_suffix(const uint16_t* __restrict__ T, uint32
 // token words (offset 2 + 2x in the low half of word x), each word rotated
 // by 16 bits so that one unsigned compare orders two tokens
 // lexicographically; positions at or past n are masked out on both sides.
+constexpr int kSearchWords = (FC_MAX_NMAX - 1) / 2;  // token words of offsets 2..15
+constexpr int kRecQuads = FC_RECORD_BYTES / 16;     // 16-byte pieces per record
+static_assert(2 + 2 * kSearchWords <= FC_RECORD_TOKENS + 2 && kSearchWords == 7, "search words");
+
 struct RecQuery {
-  uint32_t rot[FC_RECORD_TOKENS / 2];
-  uint32_t mask[FC_RECORD_TOKENS / 2];
+  uint32_t rot[kSearchWords];
+  uint32_t mask[kSearchWords];
 };
 
 __device__ __forceinline__ uint32_t rot16(uint32_t x) { return __builtin_amdgcn_alignbit(x, x, 16); }
@@ -90,7 +94,7 @@ __device__ __forceinline__ uint32_t rot16(uint32_t x) { return __builtin_amdgcn_
 __device__ __forceinline__ RecQuery rec_query(const uint16_t* q, int n) {
   RecQuery r;
 #pragma unroll
-  for (int x = 0; x < FC_RECORD_TOKENS / 2; ++x) {
+  for (int x = 0; x < kSearchWords; ++x) {
     const int o = 2 + 2 * x;
     const uint32_t a = o < n ? q[o] : 0u;
     const uint32_t b = o + 1 < n ? q[o + 1] : 0u;
@@ -100,13 +104,13 @@ __device__ __forceinline__ RecQuery rec_query(const uint16_t* q, int n) {
   return r;
 }
 
-// Record (two 16-byte halves) against the pattern: -1 below, 0 starts
-// with it, +1 above.  The first differing word decides.
+// A record's first 32 bytes (offsets 2..15 of its suffix) against the
+// pattern: -1 below, 0 starts with it, +1 above.  The first differing word decides.
 __device__ __forceinline__ int rec_cmp(const uint4& h0, const uint4& h1, const RecQuery& r) {
-  const uint32_t t[FC_RECORD_TOKENS / 2] = {h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+  const uint32_t t[kSearchWords] = {h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
   int res = 0;
 #pragma unroll
-  for (int x = FC_RECORD_TOKENS / 2 - 1; x >= 0; --x) {
+  for (int x = kSearchWords - 1; x >= 0; --x) {
     const uint32_t u = rot16(t[x] & r.mask[x]);
     res = u != r.rot[x] ? (u < r.rot[x] ? -1 : 1) : res;
   }
@@ -123,9 +127,9 @@ __device__ __forceinline__ uint32_t rec_search(const uint4* __restrict__ R, uint
     const uint32_t mid = lo + ((hi - lo) >> 1);
     const uint32_t lmid = lo < mid ? lo + ((mid - lo) >> 1) : mid;
     const uint32_t rmid = mid + 1 < hi ? (mid + 1) + ((hi - mid - 1) >> 1) : mid;
-    const uint4 m0 = R[2 * (uint64_t)mid], m1 = R[2 * (uint64_t)mid + 1];
-    const uint4 l0 = R[2 * (uint64_t)lmid], l1 = R[2 * (uint64_t)lmid + 1];
-    const uint4 r0 = R[2 * (uint64_t)rmid], r1 = R[2 * (uint64_t)rmid + 1];
+    const uint4 m0 = R[kRecQuads * (uint64_t)mid], m1 = R[kRecQuads * (uint64_t)mid + 1];
+    const uint4 l0 = R[kRecQuads * (uint64_t)lmid], l1 = R[kRecQuads * (uint64_t)lmid + 1];
+    const uint4 r0 = R[kRecQuads * (uint64_t)rmid], r1 = R[kRecQuads * (uint64_t)rmid + 1];
     const int c = rec_cmp(m0, m1, rq);
     const bool right = upper ? c <= 0 : c < 0;
     if (right) lo = mid + 1; else hi = mid;
@@ -293,26 +297,33 @@ __global__ void __launch_bounds__(kScanThreads) k_offsets(const int32_t* __restr
   if (threadIdx.x == 0) offsets[B] = total;
 }
 
-// Continuation tokens [start, start + MAXM) of one slot, all loads issued
-// together: 32-bit words from the aligned word at or before start.  Tokens
-// at or past N read as 0.
+// MAXM tokens from MAXM/2 + 1 consecutive 32-bit words holding two tokens
+// each (low half first), starting at the high half of the first word when
+// `odd`; every load is issued before any is used.
+template <int MAXM>
+__device__ __forceinline__ void words_window(const uint32_t* __restrict__ W, int odd, uint16_t (&v)[MAXM]) {
+  constexpr int kWords = MAXM / 2 + 1;
+  uint32_t wd[kWords];
+#pragma unroll
+  for (int u = 0; u < kWords; ++u) wd[u] = W[u];
+#pragma unroll
+  for (int x = 0; x < MAXM; ++x) {
+    const uint16_t even_v = (uint16_t)(wd[x >> 1] >> (16 * (x & 1)));
+    const uint16_t odd_v = (uint16_t)(wd[(x + 1) >> 1] >> (16 * ((x + 1) & 1)));
+    v[x] = odd ? odd_v : even_v;
+  }
+}
+
+// Continuation tokens [start, start + MAXM) of one slot from the text: the
+// words from the aligned word at or before start.  Tokens at or past N
+// read as 0.
 template <int MAXM>
 __device__ __forceinline__ void load_window(const uint16_t* __restrict__ T, uint64_t N, uint64_t start,
                                            uint16_t (&v)[MAXM]) {
   constexpr int kWords = MAXM / 2 + 1;
   const uint64_t w0 = start >> 1;
-  const int odd = (int)(start & 1);
   if (2 * (w0 + kWords) <= N) {
-    const uint32_t* W = (const uint32_t*)T + w0;
-    uint32_t wd[kWords];
-#pragma unroll
-    for (int u = 0; u < kWords; ++u) wd[u] = W[u];
-#pragma unroll
-    for (int x = 0; x < MAXM; ++x) {
-      const uint16_t even_v = (uint16_t)(wd[x >> 1] >> (16 * (x & 1)));
-      const uint16_t odd_v = (uint16_t)(wd[(x + 1) >> 1] >> (16 * ((x + 1) & 1)));
-      v[x] = odd ? odd_v : even_v;
-    }
+    words_window<MAXM>((const uint32_t*)T + w0, (int)(start & 1), v);
   } else {
 #pragma unroll
     for (int x = 0; x < MAXM; ++x) v[x] = (start + x < N) ? T[start + x] : (uint16_t)0;
@@ -365,15 +376,27 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
     const uint64_t budget = (uint64_t)((int64_t)k - before);
     const uint64_t local = (uint64_t)(i - before);
     const uint64_t off = cnt > budget ? (local * cnt) / budget : local;
-    const uint32_t j = st.sa[s][(uint64_t)range_lo[o] + off];
-    const uint64_t start = (uint64_t)j + (uint64_t)match_n[o];
+    const uint64_t idx = (uint64_t)range_lo[o] + off;
+    const int n = match_n[o];
     const uint64_t N = st.n[s];
     uint16_t v[MAXM];
-    if (words) load_window<MAXM>(st.tok[s], N, start, v);
-    else {
+    uint32_t j;
+    // the window's words (token n - 2 onward) inside the record: no text read
+    const int t0 = n - 2;
+    if (st.rec[s] != nullptr && t0 >= 0 && (t0 >> 1) + MAXM / 2 <= FC_RECORD_TOKENS / 2 - 1) {
+      const uint32_t* W = (const uint32_t*)(st.rec[s] + kRecQuads * idx);
+      j = W[0];
+      words_window<MAXM>(W + 1 + (t0 >> 1), t0 & 1, v);
+    } else {
+      j = st.sa[s][idx];
+      const uint64_t start = (uint64_t)j + (uint64_t)n;
+      if (words) load_window<MAXM>(st.tok[s], N, start, v);
+      else {
 #pragma unroll
-      for (int x = 0; x < MAXM; ++x) v[x] = (start + x < N) ? st.tok[s][start + x] : (uint16_t)0;
+        for (int x = 0; x < MAXM; ++x) v[x] = (start + x < N) ? st.tok[s][start + x] : (uint16_t)0;
+      }
     }
+    const uint64_t start = (uint64_t)j + (uint64_t)n;
     int len = m;
 #pragma unroll
     for (int x = MAXM - 1; x >= 0; --x)

@@ -430,13 +430,14 @@ __global__ void __launch_bounds__(256) k_pairs(const uint16_t* __restrict__ tok,
 }
 
 // Inline-prefix records: one thread per suffix-array position writes
-// {sa[i], T[sa[i]+2 .. sa[i]+16)} as two 16-byte stores (0 past the end).
+// {sa[i], T[sa[i]+2 .. sa[i]+32)} as four 16-byte stores (0 past the end).
 __global__ void __launch_bounds__(256) k_records(const uint16_t* __restrict__ tok, const uint32_t* __restrict__ sa,
                                                  uint32_t n, uint4* __restrict__ rec) {
+  static_assert(FC_RECORD_BYTES == 64 && FC_RECORD_TOKENS == 30, "record layout");
   const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const uint32_t j = sa[i];
-  uint32_t w[8];
+  uint32_t w[16];
   w[0] = j;
 #pragma unroll
   for (int x = 0; x < FC_RECORD_TOKENS / 2; ++x) {
@@ -445,8 +446,8 @@ __global__ void __launch_bounds__(256) k_records(const uint16_t* __restrict__ to
     const uint32_t b = p + 1 < n ? tok[p + 1] : 0u;
     w[1 + x] = a | (b << 16);
   }
-  rec[2 * i] = make_uint4(w[0], w[1], w[2], w[3]);
-  rec[2 * i + 1] = make_uint4(w[4], w[5], w[6], w[7]);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) rec[4 * i + u] = make_uint4(w[4 * u], w[4 * u + 1], w[4 * u + 2], w[4 * u + 3]);
 }
 
 struct BuildWs {

@@ -89,7 +89,7 @@ def test_retrieve_rejects_null_outputs_and_big_store(L):
     views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, None, 0, 64))  # records without a two-token table
     args[0] = views
     assert L.fc_retrieve(*args) == 1
-    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, 1, 100, 48))  # records not 32-byte aligned
+    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, 1, 100, 48))  # records not 64-byte aligned
     args[0] = views
     assert L.fc_retrieve(*args) == 1
 
@@ -151,7 +151,7 @@ def test_pair_table_size_and_rejects(L):
 
 
 def test_record_size_and_rejects(L):
-    assert L.fc_record_bytes(1_001_999_999) == 32 * 1_001_999_999
+    assert L.fc_record_bytes(1_001_999_999) == 64 * 1_001_999_999
     assert L.fc_record_bytes(0) == 0
     one, aligned = ctypes.c_void_p(8), ctypes.c_void_p(64)
     assert L.fc_store_prepare_records(one, one, 10, ctypes.c_void_p(48), None) == 1  # misaligned

@@ -141,19 +141,19 @@ def test_pair_table():
 
 
 def test_records():
-    """Record i = {sa[i], T[sa[i]+2 .. sa[i]+16)} with 0 past the end."""
+    """Record i = {sa[i], T[sa[i]+2 .. sa[i]+32)} with 0 past the end."""
     for seed, n in enumerate((1, 2, 17, 3000, 70001)):
         t = synth.random_text(70 + seed, n, 500, 0.05)
         say(f"records n={n}")
         st = fc.Store(dev(t), pair_vocab=500, records=True)
         torch.cuda.synchronize()
         sa = host(st.sa).astype(np.int64)
-        rec = host(st.rec).view(np.uint32).reshape(n, 8)
+        rec = host(st.rec).view(np.uint32).reshape(n, 16)
         assert (rec[:, 0] == sa).all()
-        padded = np.concatenate([t.astype(np.uint32), np.zeros(16, np.uint32)])
-        idx = sa[:, None] + 2 + np.arange(14)[None, :]
+        padded = np.concatenate([t.astype(np.uint32), np.zeros(32, np.uint32)])
+        idx = sa[:, None] + 2 + np.arange(30)[None, :]
         want = padded[idx]
-        got = np.stack([rec[:, 1:] & 0xFFFF, rec[:, 1:] >> 16], axis=2).reshape(n, 14)
+        got = np.stack([rec[:, 1:] & 0xFFFF, rec[:, 1:] >> 16], axis=2).reshape(n, 30)
         assert (got == want).all()
 
 
@@ -165,7 +165,7 @@ def test_first_workload_full_batch():
     st = gpu_store(t)
     st_pairs = fc.Store(st.tokens, st.sa, st.bucket, pair_vocab=synth.VOCAB)
     st_rec = fc.Store(st.tokens, st.sa, st.bucket, pair_vocab=synth.VOCAB, records=True)
-    variants = {P["k"]: st_rec, 1000: st_pairs}
+    variants = {P["k"]: st_rec, 1000: st_pairs, 1200: st_rec}
     for (k, m, c) in ((P["k"], P["m"], P["c"]), (1000, 10, 64), (257, 3, 5), (1200, 13, 40), (1, 1, 1)):
         say(f"workload 1: k={k} m={m} c={c}")
         p = dict(P, k=k, m=m)
