@@ -330,12 +330,37 @@ __device__ __forceinline__ void load_window(const uint16_t* __restrict__ T, uint
   }
 }
 
+// The per-store fields of one query's row that its slots need.
+struct RowMeta {
+  int32_t taken[FC_MAX_SOURCES];
+  uint32_t cnt[FC_MAX_SOURCES], lo[FC_MAX_SOURCES];
+  int32_t n[FC_MAX_SOURCES];
+};
+
+__device__ __forceinline__ RowMeta load_meta(const int32_t* __restrict__ taken, const uint32_t* __restrict__ range_cnt,
+                                             const uint32_t* __restrict__ range_lo,
+                                             const int32_t* __restrict__ match_n, int64_t row, int S) {
+  RowMeta r;
+#pragma unroll
+  for (int u = 0; u < FC_MAX_SOURCES; ++u) {
+    const int64_t o = row * S + u;
+    r.taken[u] = u < S ? taken[o] : 0;
+    r.cnt[u] = u < S ? range_cnt[o] : 0u;
+    r.lo[u] = u < S ? range_lo[o] : 0u;
+    r.n[u] = u < S ? match_n[o] : 0;
+  }
+  return r;
+}
+
 // Kept slots of the whole batch as one flat range, split evenly over a
 // persistent grid: slot g belongs to the query b with offsets[b] <= g <
-// offsets[b+1] (binary search in an LDS copy of the offsets).  For each slot
-// the suffix-array entry is read (consecutive slots of a store read
-// consecutive entries when the whole range is kept), then the continuation
-// window with a few wide loads, cut at the first 0 in registers.
+// offsets[b+1] (binary search in an LDS copy of the offsets).  A wave whose
+// slots all belong to one query (the common case) reads that query's
+// per-store fields with scalar loads.  Each slot reads its inline-prefix
+// record (or else its suffix-array entry and then the text) at consecutive
+// positions when the whole range is kept, cuts the window at the first 0 in
+// registers and writes the tokens two per 32-bit store when rows are
+// 4-byte aligned.
 template <int MAXM>
 __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, int B, int k, int m,
                                                            const int32_t* __restrict__ match_n,
@@ -343,8 +368,8 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
                                                            const uint32_t* __restrict__ range_cnt,
                                                            const int32_t* __restrict__ taken,
                                                            const uint32_t* __restrict__ offsets, int words,
-                                                           const int32_t* __restrict__ rows, int n_rows,
-                                                           uint32_t* __restrict__ cont_pos,
+                                                           int out_words, const int32_t* __restrict__ rows,
+                                                           int n_rows, uint32_t* __restrict__ cont_pos,
                                                            uint8_t* __restrict__ cont_src,
                                                            uint8_t* __restrict__ cont_len,
                                                            uint16_t* __restrict__ cont_tok) {
@@ -364,20 +389,29 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
     const int b = lo;
     const int row = fc::map_row(rows, n_rows, b);  // >= 0: a skipped query owns no slots
     const int i = (int)(g - off_tab[b]);
+    const int rf = __builtin_amdgcn_readfirstlane(row);
+    const RowMeta meta = fc::ballot(row != rf) == 0 ? load_meta(taken, range_cnt, range_lo, match_n, rf, S)
+                                                    : load_meta(taken, range_cnt, range_lo, match_n, row, S);
+    // the slot's store: stores before it fill the first slots
     int s = 0;
     int64_t before = 0;
-    for (; s + 1 < S; ++s) {
-      const int64_t t = taken[(int64_t)row * S + s];
-      if (i < before + t) break;
-      before += t;
+    uint64_t cnt = meta.cnt[0], rlo = meta.lo[0];
+    int n = meta.n[0];
+#pragma unroll
+    for (int u = 1; u < FC_MAX_SOURCES; ++u) {
+      const int64_t nb = before + meta.taken[u - 1];
+      if (u < S && s == u - 1 && i >= nb) {
+        s = u;
+        before = nb;
+        cnt = meta.cnt[u];
+        rlo = meta.lo[u];
+        n = meta.n[u];
+      }
     }
-    const int64_t o = (int64_t)row * S + s;
-    const uint64_t cnt = range_cnt[o];
     const uint64_t budget = (uint64_t)((int64_t)k - before);
     const uint64_t local = (uint64_t)(i - before);
     const uint64_t off = cnt > budget ? (local * cnt) / budget : local;
-    const uint64_t idx = (uint64_t)range_lo[o] + off;
-    const int n = match_n[o];
+    const uint64_t idx = rlo + off;
     const uint64_t N = st.n[s];
     uint16_t v[MAXM];
     uint32_t j;
@@ -403,9 +437,19 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
       if (x < m && v[x] == 0) len = x;
     const int64_t slot = (int64_t)row * k + i;
     uint16_t* out = cont_tok + slot * m;
+    if (out_words) {
+      uint32_t* out32 = (uint32_t*)out;
 #pragma unroll
-    for (int x = 0; x < MAXM; ++x)
-      if (x < m) out[x] = x < len ? v[x] : (uint16_t)0;
+      for (int x = 0; x < MAXM / 2; ++x) {
+        const uint32_t a = 2 * x < len ? v[2 * x] : 0u;
+        const uint32_t c2 = 2 * x + 1 < len ? v[2 * x + 1] : 0u;
+        if (2 * x < m) out32[x] = a | (c2 << 16);
+      }
+    } else {
+#pragma unroll
+      for (int x = 0; x < MAXM; ++x)
+        if (x < m) out[x] = x < len ? v[x] : (uint16_t)0;
+    }
     cont_pos[slot] = (uint32_t)start;
     cont_src[slot] = (uint8_t)s;
     cont_len[slot] = (uint8_t)len;
@@ -514,15 +558,16 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
     FC_CHECK_LAUNCH();
     int words = 1;
     for (int s = 0; s < S; ++s) words &= (((uintptr_t)st.tok[s]) & 3) == 0;
+    const int out_words = (p.m % 2 == 0) && (((uintptr_t)cont_tok) & 3) == 0;
     const uint64_t want = ((uint64_t)B * p.k + kGatherThreads - 1) / kGatherThreads;
     const uint32_t blocks = (uint32_t)(want < (uint64_t)kGatherBlocks ? want : (uint64_t)kGatherBlocks);
     if (p.m <= 10)
       hipLaunchKernelGGL(k_gather<10>, dim3(blocks), dim3(kGatherThreads), 0, stream, st, S, B, p.k, p.m, match_n,
-                         range_lo, range_cnt, taken, offsets, words, rows, n_rows, cont_pos, cont_src, cont_len,
+                         range_lo, range_cnt, taken, offsets, words, out_words, rows, n_rows, cont_pos, cont_src, cont_len,
                          cont_tok);
     else
       hipLaunchKernelGGL(k_gather<16>, dim3(blocks), dim3(kGatherThreads), 0, stream, st, S, B, p.k, p.m, match_n,
-                         range_lo, range_cnt, taken, offsets, words, rows, n_rows, cont_pos, cont_src, cont_len,
+                         range_lo, range_cnt, taken, offsets, words, out_words, rows, n_rows, cont_pos, cont_src, cont_len,
                          cont_tok);
   } else {
     hipLaunchKernelGGL(k_gather_any, dim3(B), dim3(kGatherThreads), 0, stream, st, S, p.k, p.m, match_n, range_lo,
