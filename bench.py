@@ -31,6 +31,48 @@ import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "build": 3, "copy": 0}
+# kernels each entry point launches (rocprofv3 kernel names start with these)
+ENTRY_KERNELS = {
+    "fc_retrieve": ("k_search", "k_offsets", "k_gather"),
+    "fc_build_tree": ("k_tree_classify", "k_tree_fast", "k_tree_any"),
+    "fc_verify_accept": ("k_verify",),
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_headline_10M_1B.txt")
+
+
+def kernel_source_hash() -> str:
+    """SHA-256 over the HIP sources and the ABI header: measured hardware
+    traffic is only reported for the sources it was measured on."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2502_17139_amd", "csrc")
+    files = sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h")) +
+                   glob.glob(os.path.join(csrc, "*.cpp"))) + [os.path.join(ROOT, "include", "fastcoder.h")]
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic() -> dict:
+    """HBM bytes per launch of each entry point from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy's readings),
+    or {} when it is missing or was taken on other kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            lines = f.read().splitlines()
+    except OSError:
+        return {}
+    out, sha = {}, None
+    for ln in lines:
+        parts = ln.split()
+        if len(parts) == 2 and parts[0] == "source_sha256":
+            sha = parts[1]
+        elif len(parts) == 4 and parts[0] == "entry" and parts[2] == "bytes":
+            out[parts[1]] = float(parts[3])
+    return out if sha == kernel_source_hash() else {}
 
 
 def log(*a):
@@ -228,10 +270,18 @@ def main():
     acc = aout["accept_len"].cpu().numpy()
     nb = algorithmic_bytes(taken, cont_len, match_n, n_hi_of(ctx_np, p["n_max"]), [len(t) for t in texts],
                            k, m, c, p["n_min"])
+    entry_bytes = {"fc_retrieve": nb["search"] + nb["gather"], "fc_build_tree": nb["tree"],
+                   "fc_verify_accept": nb["verify"]}
+    traffic = measured_traffic()
+    roofs = {}
+    for name, ms in phase_ms.items():
+        gbs = entry_bytes[name] / (ms * 1e-3) / 1e9
+        t = traffic.get(name)
+        roofs[name] = {"bound": "hbm", "kernel": name, "kernels": list(ENTRY_KERNELS[name]), "achieved": gbs,
+                       "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "traffic": t,
+                       "algorithmic_bytes": entry_bytes[name], "us_per_launch": ms * 1e3,
+                       "traffic_GBps": None if t is None else t / (ms * 1e-3) / 1e9}
     dominant = max(phase_ms, key=phase_ms.get)
-    dom_bytes = {"fc_retrieve": nb["search"] + nb["gather"], "fc_build_tree": nb["tree"],
-                 "fc_verify_accept": nb["verify"]}[dominant]
-    achieved = dom_bytes / (phase_ms[dominant] * 1e-3) / 1e9
     total_bytes = sum(nb.values())
 
     cpu = None
@@ -257,8 +307,8 @@ def main():
         "config": {"workload": synth.CONFIGS[cfg]["name"], "stores_tokens": [len(t) for t in texts],
                    "batch": B, "n_max": p["n_max"], "n_min": p["n_min"], "k": k, "m": m, "c": c,
                    "alpha": list(alpha), "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+        "roofline": roofs[dominant],
+        "roofline_by_entry": roofs,
         "cpu_baseline": cpu,
         "phases_ms": phase_ms,
         "algorithmic_bytes_per_step": nb,
