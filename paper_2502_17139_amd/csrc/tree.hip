@@ -38,7 +38,7 @@ namespace {
 
 constexpr int kTreeThreads = 512;
 constexpr int kMaskWords = FC_MAX_TREE_ROWS / 32;
-constexpr int kSmallClass = 1024;  // kept slots handled by the small-LDS launch
+constexpr int kSmallClass = 256;  // kept slots handled by the small-LDS launch (one per thread)
 
 struct Alpha {
   uint32_t a[FC_MAX_SOURCES];
@@ -1017,7 +1017,7 @@ fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint1
                       const TreeLayout& full, int32_t* num_nodes, int32_t* node_tok, int32_t* parent,
                       uint32_t* weight, int32_t* pos_ids, int32_t* mask, const int32_t* rows, int32_t n_rows, void* ws,
                       hipStream_t stream) {
-  // light queries (T <= 1024) in small-LDS workgroups, the rest in full-LDS
+  // light queries (T <= 256) in small-LDS workgroups, the rest in full-LDS
   // ones, each launch walking its own list of queries
   const int t_small = k < kSmallClass ? k : kSmallClass;
   int32_t* lists = (int32_t*)ws;
