@@ -575,7 +575,9 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     s_err = bad;
     s_pick[0] = 0;
     s_pick[1] = 0;
+    s_pick[2] = 0;
   }
+  for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
   __syncthreads();
   const int T = T_raw;
   // store boundaries in registers (no LDS round trip per lookup)
@@ -724,8 +726,9 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
       const uint32_t x = s_wsuf[w][d];
       if (d <= m && x < nh[d]) nh[d] = (uint16_t)x;
     }
-    // alpha prefix sums
-    {
+    // alpha prefix sums (with one weight for every store they are
+    // alpha * position and never stored)
+    if (!alpha_flat) {
       uint32_t run = a_ex;
       for (int p = p0; p < p1; ++p) {
         A[p] = run;
@@ -734,78 +737,65 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
       if (tid == 0) A[T] = a_tot;
     }
     __syncthreads();  // str is dead from here on: E reuses it
+    // alpha weight of merged positions [p, e)
+    auto wsum = [&](uint32_t e, uint32_t p) -> uint32_t {
+      return alpha_flat ? alpha.a[0] * (e - p) : A[e] - A[p];
+    };
 
-    // 4. run ends, right to left through the chunk.  The node weight
-    //    A[end] - A[q] is stored directly when every weight fits 16 bits
-    //    (weights never exceed the root's); otherwise the run end is stored
-    //    and the weight recomputed where needed.
+    // 4. run ends, right to left through the chunk, with the weight
+    //    histogram of the chunk's own nodes counted on the way.  The node
+    //    weight is stored directly when every weight fits 16 bits (weights
+    //    never exceed the root's); otherwise the run end is stored and the
+    //    weight recomputed where needed.
+    //    The histogram serves step 5: weights 1 and 2 (the bulk: unshared
+    //    continuation tails) are counted in registers, other weights below
+    //    256 with LDS atomics, heavier ones lumped.
     const bool wide = root_w > 0xFFFFu;
-    for (int q = p1 - 1; q >= p0; --q) {
-      const int l = lcp[q], ml = mlen[q];
-      const uint32_t aq = A[q];
+    {
+      uint32_t r1 = 0, r2 = 0, rbig = 0;
+      for (int q = p1 - 1; q >= p0; --q) {
+        const int l = lcp[q], ml = mlen[q];
+        const uint32_t aq = alpha_flat ? 0u : A[q];
 #pragma unroll
-      for (int d = 1; d <= MAXM; ++d) {
-        if (d > l && d <= ml)
-          E[q * m + d - 1] = wide ? nh[d] : alpha_flat ? (uint16_t)(alpha.a[0] * ((uint32_t)nh[d] - (uint32_t)q))
-                                                       : (uint16_t)(A[nh[d]] - aq);
-        if (d > l) nh[d] = (uint16_t)q;
+        for (int d = 1; d <= MAXM; ++d) {
+          if (d > l && d <= ml) {
+            const uint32_t W = alpha_flat ? alpha.a[0] * ((uint32_t)nh[d] - (uint32_t)q) : A[nh[d]] - aq;
+            E[q * m + d - 1] = wide ? nh[d] : (uint16_t)W;
+            r1 += W == 1u ? 1u : 0u;
+            r2 += W == 2u ? 1u : 0u;
+            rbig += W >= 256u ? 1u : 0u;
+            if (W != 1u && W != 2u && W < 256u) atomicAdd(&s_hist[W], 1u);
+          }
+          if (d > l) nh[d] = (uint16_t)q;
+        }
       }
+      const uint32_t x1 = fc::wave_sum_u32(r1), x2 = fc::wave_sum_u32(r2), xb = fc::wave_sum_u32(rbig);
+      if (lane == 0 && x1) atomicAdd(&s_hist[1], x1);
+      if (lane == 0 && x2) atomicAdd(&s_hist[2], x2);
+      if (lane == 0 && xb) atomicAdd(&s_pick[2], xb);
     }
     __syncthreads();
-    auto node_w = [&](int p, int d, uint32_t ap) -> uint32_t {
+    auto node_w = [&](int p, int d) -> uint32_t {
       const uint16_t e = E[p * m + d - 1];
-      return wide ? A[e] - ap : (uint32_t)e;
+      return wide ? wsum(e, (uint32_t)p) : (uint32_t)e;
     };
     // The weights of all depths of string p, fetched together (the depth
     // bound m is uniform, so every load issues before any is used); depths
     // that are not p's own nodes hold unused values.
     auto row_w = [&](int p, uint32_t (&wv)[MAXM + 1]) {
-      const uint32_t ap = wide ? A[p] : 0u;
 #pragma unroll
       for (int d = 1; d <= MAXM; ++d) wv[d] = d <= m ? (uint32_t)E[p * m + d - 1] : 0u;
       if (wide) {
 #pragma unroll
-        for (int d = 1; d <= MAXM; ++d) wv[d] = d <= m ? A[wv[d]] - ap : 0u;
+        for (int d = 1; d <= MAXM; ++d) wv[d] = d <= m ? wsum(wv[d], (uint32_t)p) : 0u;
       }
     };
 
     // 5. the need-th largest weight W* and how many nodes of weight W* to
-    //    take (in (p, d) order).  Most nodes are light, so weights below 8
-    //    are counted in registers, 8..255 in an LDS histogram, and heavier
-    //    ones lumped; only when W* itself is heavy does a radix select over
-    //    the (few) heavy nodes follow.
+    //    take (in (p, d) order), from the histogram; only when W* itself is
+    //    256 or more does a radix select over the (few) heavy nodes follow.
     const uint32_t need = n_tot < (uint32_t)c ? n_tot : (uint32_t)c;
     uint32_t prefix = 0, remaining = need;
-    for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
-    if (tid == 0) s_pick[2] = 0;
-    __syncthreads();
-    if (need > 0) {
-      // weights 1 and 2 (the bulk: unshared continuation tails) are counted
-      // in registers, other light weights with LDS atomics
-      uint32_t r1 = 0, r2 = 0, rbig = 0;
-      for (int p = p0; p < p1; ++p) {
-        const int l = lcp[p], ml = mlen[p];
-        uint32_t wv[MAXM + 1];
-        row_w(p, wv);
-#pragma unroll
-        for (int d = 1; d <= MAXM; ++d) {
-          const bool own = d > l && d <= ml;
-          const uint32_t W = wv[d];
-          r1 += (own && W == 1u) ? 1u : 0u;
-          r2 += (own && W == 2u) ? 1u : 0u;
-          rbig += (own && W >= 256u) ? 1u : 0u;
-          if (own && W != 1u && W != 2u && W < 256u) atomicAdd(&s_hist[W], 1u);
-        }
-      }
-      {
-        const uint32_t x1 = fc::wave_sum_u32(r1), x2 = fc::wave_sum_u32(r2);
-        if (lane == 0 && x1) atomicAdd(&s_hist[1], x1);
-        if (lane == 0 && x2) atomicAdd(&s_hist[2], x2);
-      }
-      const uint32_t xb = fc::wave_sum_u32(rbig);
-      if (lane == 0 && xb) atomicAdd(&s_pick[2], xb);
-    }
-    __syncthreads();
     const uint32_t n_heavy = s_pick[2];
     if (need > 0 && n_heavy < need) {
       // W* < 256: wave 0 walks the histogram from the top
@@ -844,7 +834,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
       for (int p = p0; p < p1; ++p) {
         const int d = lcp[p] + 1;  // the shallowest own node is the heaviest
         if (d <= mlen[p]) {
-          const uint32_t W = node_w(p, d, A[p]);
+          const uint32_t W = node_w(p, d);
           wmax = W > wmax ? W : wmax;
         }
       }
@@ -856,9 +846,8 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
         __syncthreads();
         const uint64_t hi_mask = shift + 8 >= 32 ? 0ull : (uint64_t)prefix >> (shift + 8);
         for (int p = p0; p < p1; ++p) {
-          const uint32_t ap = wide ? A[p] : 0u;
           for (int d = lcp[p] + 1; d <= mlen[p]; ++d) {
-            const uint32_t W = node_w(p, d, ap);
+            const uint32_t W = node_w(p, d);
             if (W < 256) break;  // own nodes get lighter with depth
             if ((shift + 8 >= 32 ? 0ull : (uint64_t)(W >> (shift + 8))) == hi_mask)
               atomicAdd(&s_hist[(W >> shift) & 0xFF], 1u);
