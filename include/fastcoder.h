@@ -202,6 +202,57 @@ fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, in
                       const int32_t* rows, int32_t n_rows, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* CACHE (Section IV-B)                                                      */
+/* ------------------------------------------------------------------------ */
+
+#define FC_MAX_CACHE_TOKENS 16384 /* longest CACHE text (sequences joined by 0) */
+
+/*
+ * Retrieval from the context- and LLM preference-aware CACHE of Section
+ * IV-B, which Alg. 1 searches before the datastores.  A CACHE's text is its
+ * sequences joined by single 0 tokens; it is searched exactly like a store
+ * (Section III-A), so the results equal those of fc_retrieve over one store
+ * holding that text: the same match length, range_lo (the suffix-array index
+ * of the first occurrence within the text), range_cnt, taken = min(k, cnt),
+ * strided selection beyond k, and continuations in suffix order (cont_src =
+ * 0).  No suffix array is needed: one workgroup per query holds the text in
+ * LDS.
+ *
+ * texts [n_texts][stride] : CACHE texts, row r holding text_len[r] tokens
+ *                           (clamped to [0, stride]); 1 <= stride <=
+ *                           FC_MAX_CACHE_TOKENS.
+ * text_row [B]            : the text query b searches (NULL: text b); a row
+ *                           outside [0, n_texts) reads as an empty text.
+ * ctx, B, L, p            : as fc_retrieve.
+ * outputs                 : as fc_retrieve with S = 1 (match_n, range_lo,
+ *                           range_cnt, taken [rows][1]; slots [rows][k]),
+ *                           including the optional row map rows/n_rows.
+ * The LDS needed is fc_cache_lds_bytes(stride) (96 KB at the maximum);
+ * FC_ERR_UNSUPPORTED when the device has less.
+ */
+size_t fc_cache_lds_bytes(int64_t stride);
+fc_status fc_cache_retrieve(const uint16_t* texts, int64_t stride, int32_t n_texts, const int32_t* text_len,
+                            const int32_t* text_row, const uint16_t* ctx, int32_t B, int32_t L, fc_retrieve_params p,
+                            int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt, int32_t* taken,
+                            uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len, uint16_t* cont_tok,
+                            const int32_t* rows, int32_t n_rows, hipStream_t stream);
+
+/*
+ * Batched CACHE update (Section IV-B: verified retrieved sequences and the
+ * LLM's output are added after each step).  Segment i copies src_len[i]
+ * tokens from src_tok + src_off[i] into text row dst_row[i] at offset
+ * dst_off[i] and sets text_len[dst_row[i]] = new_len[i] (clamped to [0,
+ * stride]); the caller lays out the appended sequences with their 0
+ * separators.  Segments of one row must not overlap; a row outside [0,
+ * n_texts) is skipped and tokens past the row's end are not written.  All
+ * arrays are device memory.
+ */
+fc_status fc_cache_write(uint16_t* texts, int64_t stride, int32_t n_texts, int32_t* text_len, int32_t n_seg,
+                         const int32_t* dst_row, const int32_t* dst_off, const int32_t* new_len,
+                         const int64_t* src_off, const int32_t* src_len, const uint16_t* src_tok,
+                         hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Draft tree                                                                */
 /* ------------------------------------------------------------------------ */
 

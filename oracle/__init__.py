@@ -168,8 +168,49 @@ def verify_accept(tree: dict, target, m: int = 10) -> dict:
     return out
 
 
+class Cache:
+    """The context- and LLM preference-aware CACHE of one stream (Section
+    IV-B), as the oracle keeps it.
+
+    It holds token sequences; `size` is their number.  Its text, the
+    sequences joined by single 0 tokens (the separator of a datastore), is
+    searched exactly like a store (Section III-A).  Reading for a bounded
+    device buffer: when adding a sequence would make the text longer than
+    `cap` tokens, the oldest sequences are dropped first (a sequence longer
+    than `cap` on its own is cut to its last `cap` tokens).
+    """
+
+    def __init__(self, cap: int):
+        self.cap = cap
+        self.seqs = []
+
+    @property
+    def size(self) -> int:
+        return len(self.seqs)
+
+    def text_len(self) -> int:
+        return sum(len(x) for x in self.seqs) + max(len(self.seqs) - 1, 0)
+
+    def add(self, seq) -> None:
+        seq = [int(x) for x in seq][-self.cap:]
+        if not seq:
+            return
+        self.seqs.append(seq)
+        while self.text_len() > self.cap:
+            self.seqs.pop(0)
+
+    def text(self) -> np.ndarray:
+        out = []
+        for i, x in enumerate(self.seqs):
+            if i:
+                out.append(0)
+            out.extend(x)
+        return np.array(out, dtype=np.uint16)
+
+
 def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int = 10, c: int = 64, alpha=(1, 1),
-           lru: int = 32, ctx_len: int = 16, max_steps: int = 512) -> dict:
+           lru: int = 32, ctx_len: int = 16, max_steps: int = 512, cache_l: int | None = None,
+           cache_every: int = 20, cache_cap: int = 16384) -> dict:
     """Decode-trace replay over known streams (reading of the average
     acceptance length setting, Section V-C eq. (7)).
 
@@ -180,9 +221,29 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
     recent; a miss retrieves, inserts as most recent and drops the least
     recent beyond `lru`); the draft tree is built; the target after tree row
     i is truth[p + pos_ids[i]] (-1 past the stream); the accepted length is
-    added to p.  Returns accept [steps][n_streams] (-1 for finished streams),
-    hits and lookups per stream, final positions, the mean accepted length
-    per live step, and the step count.
+    added to p.
+
+    With cache_l set, each stream also keeps the CACHE of Section IV-B and
+    follows the cache branch of Alg. 1:
+      - when the CACHE holds at least cache_l sequences (Alg. 1's test; the
+        prose says "exceeds", read as the listing's >=), the context is first
+        searched in the CACHE's text as a single store; a non-empty result is
+        the retrieval result R and the datastores are not consulted;
+      - otherwise (or on an empty CACHE result) the datastores are searched
+        as above (through the LRU);
+      - after verification, when R is non-empty and at least one draft token
+        was accepted, the context followed by the accepted draft tokens is
+        added to the CACHE (the verified retrieved sequence);
+      - the stream's output (every token accepted from p = ctx_len on,
+        bonus tokens included) is added in consecutive chunks of
+        cache_every tokens, each when it completes (the LLM output
+        truncated every 20 tokens, Section V-D).
+    The CACHE's trie uses weight 1 (one source).
+
+    Returns accept [steps][n_streams] (-1 for finished streams), hits and
+    lookups of the LRU per stream, cache_served (steps whose R came from the
+    CACHE) per stream, final positions, the mean accepted length per live
+    step, and the step count.
     """
     from collections import OrderedDict
 
@@ -192,6 +253,9 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
     caches = [OrderedDict() for _ in range(nseq)]
     hits = [0] * nseq
     lookups = [0] * nseq
+    served = [0] * nseq
+    cch = [Cache(cache_cap) for _ in range(nseq)] if cache_l is not None else None
+    chunks_done = [0] * nseq
     fields = ("taken", "cont_len", "cont_tok")
     steps = []
     for _ in range(max_steps):
@@ -199,9 +263,21 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
         if not act:
             break
         ctx = np.stack([truth[b, pos[b] - ctx_len:pos[b]] for b in act])
-        keys = [ctx[j].tobytes() for j in range(len(act))]
+        got = [None] * len(act)
+        from_cache = [False] * len(act)
+        if cch is not None:
+            for j, b in enumerate(act):
+                if cch[b].size >= cache_l:
+                    r = retrieve([cch[b].text()], ctx[j:j + 1], n_max=n_max, n_min=n_min, k=k, m=m)
+                    if int(r["taken"][0].sum()) > 0:
+                        got[j] = {f: r[f][0].copy() for f in fields}
+                        from_cache[j] = True
+                        served[b] += 1
+        need = [j for j in range(len(act)) if got[j] is None]
+        keys = {j: ctx[j].tobytes() for j in need}
         missing = []
-        for j, b in enumerate(act):
+        for j in need:
+            b = act[j]
             lookups[b] += 1
             if keys[j] in caches[b]:
                 caches[b].move_to_end(keys[j])
@@ -215,22 +291,42 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
                 if len(caches[b]) >= lru:
                     caches[b].popitem(last=False)
                 caches[b][keys[j]] = {f: r[f][i].copy() for f in fields}
-        got = [caches[b][keys[j]] for j, b in enumerate(act)]
-        tree = build_tree(np.stack([g["taken"] for g in got]), np.stack([g["cont_len"] for g in got]),
-                          np.stack([g["cont_tok"] for g in got]), ctx, c=c, alpha=alpha)
-        target = np.full(tree["node_tok"].shape, -1, np.int32)
-        for j, b in enumerate(act):
-            for i in range(int(tree["num_nodes"][j])):
-                at = pos[b] + int(tree["pos_ids"][j, i])
-                if at < tlen:
-                    target[j, i] = int(truth[b, at])
-        acc = verify_accept(tree, target, m=m)["accept_len"]
+        for j in need:
+            got[j] = caches[act[j]][keys[j]]
+        acc = np.zeros(len(act), np.int64)
+        depth = np.zeros(len(act), np.int64)
+        for group, al in ((True, (1,)), (False, tuple(alpha))):
+            idx = [j for j in range(len(act)) if from_cache[j] == group]
+            if not idx:
+                continue
+            tree = build_tree(np.stack([got[j]["taken"] for j in idx]), np.stack([got[j]["cont_len"] for j in idx]),
+                              np.stack([got[j]["cont_tok"] for j in idx]), ctx[idx], c=c, alpha=al)
+            target = np.full(tree["node_tok"].shape, -1, np.int32)
+            for i, j in enumerate(idx):
+                b = act[j]
+                for r_ in range(int(tree["num_nodes"][i])):
+                    at = pos[b] + int(tree["pos_ids"][i, r_])
+                    if at < tlen:
+                        target[i, r_] = int(truth[b, at])
+            va = verify_accept(tree, target, m=m)
+            for i, j in enumerate(idx):
+                acc[j] = int(va["accept_len"][i])
+                depth[j] = int(tree["pos_ids"][i, int(va["last_node"][i])])
         row = np.full(nseq, -1, np.int64)
         for j, b in enumerate(act):
+            if cch is not None:
+                if int(np.asarray(got[j]["taken"]).sum()) > 0 and depth[j] >= 1:
+                    cch[b].add(list(ctx[j]) + list(truth[b, pos[b]:pos[b] + depth[j]]))
             row[b] = int(acc[j])
             pos[b] += int(acc[j])
+            if cch is not None:
+                while ctx_len + cache_every * (chunks_done[b] + 1) <= min(pos[b], tlen):
+                    lo = ctx_len + cache_every * chunks_done[b]
+                    cch[b].add(list(truth[b, lo:lo + cache_every]))
+                    chunks_done[b] += 1
         steps.append(row)
     accept = np.stack(steps) if steps else np.zeros((0, nseq), np.int64)
     live = accept >= 0
     return dict(accept=accept, hits=np.array(hits), lookups=np.array(lookups), pos=np.array(pos),
-                acc_len=float(accept[live].sum() / max(live.sum(), 1)), steps=len(steps))
+                cache_served=np.array(served), acc_len=float(accept[live].sum() / max(live.sum(), 1)),
+                steps=len(steps))

@@ -23,6 +23,7 @@ FC_MAX_SOURCES = 4
 FC_MAX_NMAX = 16
 FC_MAX_TREE_ROWS = 256
 FC_BUCKETS = 65537
+FC_MAX_CACHE_TOKENS = 16384
 
 STATUS = {0: "FC_OK", 1: "FC_ERR_INVALID", 2: "FC_ERR_WORKSPACE", 3: "FC_ERR_DEVICE", 4: "FC_ERR_UNSUPPORTED"}
 
@@ -32,7 +33,7 @@ EXPORTS = (
     "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_store_prepare",
     "fc_pair_table_entries", "fc_store_prepare_pairs", "fc_record_bytes", "fc_store_prepare_records",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
-    "fc_verify_accept", "fc_targets_from_truth",
+    "fc_verify_accept", "fc_targets_from_truth", "fc_cache_lds_bytes", "fc_cache_retrieve", "fc_cache_write",
 )
 
 
@@ -90,6 +91,13 @@ def lib() -> ctypes.CDLL:
     L.fc_retrieve.restype = ctypes.c_int
     L.fc_retrieve.argtypes = [ctypes.POINTER(FcStore), i32, vp, i32, i32, FcRetrieveParams,
                               vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]
+    L.fc_cache_lds_bytes.restype = sz
+    L.fc_cache_lds_bytes.argtypes = [ctypes.c_int64]
+    L.fc_cache_retrieve.restype = ctypes.c_int
+    L.fc_cache_retrieve.argtypes = [vp, ctypes.c_int64, i32, vp, vp, vp, i32, i32, FcRetrieveParams,
+                                    vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp]
+    L.fc_cache_write.restype = ctypes.c_int
+    L.fc_cache_write.argtypes = [vp, ctypes.c_int64, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp]
     L.fc_build_tree_workspace_bytes.restype = sz
     L.fc_build_tree_workspace_bytes.argtypes = [i32]
     L.fc_build_tree.restype = ctypes.c_int
@@ -252,6 +260,42 @@ def fc_retrieve(stores, ctx: torch.Tensor, n_max: int = 16, n_min: int = 2, k: i
         views, S, _ptr(ctx), B, L, p, *[_ptr(out[f]) for f in RETRIEVE_FIELDS], _ptr(rows), n_rows,
         _ptr(workspace), 0 if workspace is None else workspace.numel(), _stream(stream)))
     return out
+
+
+# ---------------------------------------------------------------- CACHE ----
+
+def fc_cache_lds_bytes(stride: int) -> int:
+    return int(lib().fc_cache_lds_bytes(stride))
+
+
+def fc_cache_retrieve(texts: torch.Tensor, text_len: torch.Tensor, ctx: torch.Tensor, n_max: int = 16,
+                      n_min: int = 2, k: int = 5000, m: int = 10, text_row: torch.Tensor | None = None,
+                      out: dict | None = None, rows: torch.Tensor | None = None, stream=None) -> dict:
+    """Retrieval from CACHE texts (uint16 [n_texts][stride], lengths int32
+    [n_texts]) as single stores; outputs as fc_retrieve with S = 1."""
+    if texts.dtype != torch.uint16 or texts.dim() != 2 or text_len.dtype != torch.int32:
+        raise ValueError("texts must be 2-D uint16 and text_len int32")
+    if ctx.dtype != torch.uint16 or ctx.dim() != 2:
+        raise ValueError("ctx must be a 2-D uint16 tensor")
+    B, L = ctx.shape
+    n_texts, stride = texts.shape
+    if out is None:
+        out = retrieve_outputs(B, 1, k, m, ctx.device)
+    _check("fc_cache_retrieve", lib().fc_cache_retrieve(
+        _ptr(texts), stride, n_texts, _ptr(text_len), _ptr(text_row), _ptr(ctx), B, L,
+        FcRetrieveParams(n_max, n_min, k, m), *[_ptr(out[f]) for f in RETRIEVE_FIELDS], _ptr(rows),
+        out["taken"].shape[0], _stream(stream)))
+    return out
+
+
+def fc_cache_write(texts: torch.Tensor, text_len: torch.Tensor, dst_row: torch.Tensor, dst_off: torch.Tensor,
+                   new_len: torch.Tensor, src_off: torch.Tensor, src_len: torch.Tensor, src_tok: torch.Tensor,
+                   stream=None) -> None:
+    """Segment copies into CACHE texts (see include/fastcoder.h)."""
+    n_texts, stride = texts.shape
+    _check("fc_cache_write", lib().fc_cache_write(
+        _ptr(texts), stride, n_texts, _ptr(text_len), dst_row.numel(), _ptr(dst_row), _ptr(dst_off),
+        _ptr(new_len), _ptr(src_off), _ptr(src_len), _ptr(src_tok), _stream(stream)))
 
 
 # ----------------------------------------------------------------- tree ----

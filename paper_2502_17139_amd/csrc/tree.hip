@@ -993,9 +993,19 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   }
   __syncthreads();
   const int64_t mbase = (int64_t)b * R * R;
-  for (int e = tid; e < R * R; e += NT) {
-    const int i = e / R, j = e - (e / R) * R;
-    mask[mbase + e] = (i < num) ? (int32_t)((anc[i * words_per_row + (j >> 5)] >> (j & 31)) & 1u) : 0;
+  {
+    // element e = i*R + j, (i, j) stepped without a division per element
+    int i = tid / R, j = tid - (tid / R) * R;
+    const int di = NT / R, dj = NT - (NT / R) * R;
+    for (int e = tid; e < R * R; e += NT) {
+      mask[mbase + e] = (i < num) ? (int32_t)((anc[i * words_per_row + (j >> 5)] >> (j & 31)) & 1u) : 0;
+      i += di;
+      j += dj;
+      if (j >= R) {
+        j -= R;
+        ++i;
+      }
+    }
   }
   if (tid == 0) num_nodes[b] = err ? -1 : num;
 }

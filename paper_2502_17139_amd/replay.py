@@ -15,6 +15,17 @@ straight into their slot (fc_retrieve's row map) and the tree reads each
 stream's slot in place (fc_build_tree's row map), so cached results are
 never copied.  Only the cache keys and positions are kept on the host; one
 small copy of the accepted lengths comes back per step.
+
+With cache_l set, each stream also keeps the paper's CACHE (Section IV-B)
+and follows the cache branch of Alg. 1: once the CACHE holds cache_l
+sequences, the context is searched there first (fc_cache_retrieve) and a
+non-empty result replaces the datastore retrieval; after verification the
+context plus the accepted draft tokens, and every completed chunk of
+cache_every output tokens, are added.  The CACHE texts live on the GPU (one
+row of FC_MAX_CACHE_TOKENS tokens per stream, sequences joined by 0); the
+host keeps the sequence lists, decides evictions (oldest sequences first
+when a text would outgrow its row) and ships each step's appended tokens in
+one batched fc_cache_write.
 """
 from __future__ import annotations
 
@@ -23,16 +34,48 @@ from collections import OrderedDict
 import numpy as np
 import torch
 
-from . import (accept_outputs, fc_build_tree, fc_build_tree_workspace_bytes, fc_retrieve,
-               fc_retrieve_workspace_bytes, fc_targets_from_truth, fc_verify_accept, retrieve_outputs,
-               tree_outputs)
+from . import (FC_MAX_CACHE_TOKENS, accept_outputs, fc_build_tree, fc_build_tree_workspace_bytes,
+               fc_cache_retrieve, fc_cache_write, fc_retrieve, fc_retrieve_workspace_bytes, fc_targets_from_truth,
+               fc_verify_accept, retrieve_outputs, tree_outputs)
+
+
+class _Sequences:
+    """One stream's CACHE sequences and the text they make (joined by 0),
+    bounded by `cap` tokens: the oldest sequences go first."""
+
+    def __init__(self, cap: int):
+        self.cap = cap
+        self.seqs = []
+        self.tokens = 0  # text length, separators included
+
+    def add(self, seq) -> bool:
+        """Append a sequence; True when older sequences had to go."""
+        seq = [int(x) for x in seq][-self.cap:]
+        if not seq:
+            return False
+        self.seqs.append(seq)
+        self.tokens += len(seq) + (1 if len(self.seqs) > 1 else 0)
+        evicted = False
+        while self.tokens > self.cap:
+            first = self.seqs.pop(0)
+            self.tokens -= len(first) + (1 if self.seqs else 0)
+            evicted = True
+        return evicted
+
+    def text(self) -> list:
+        out = []
+        for i, x in enumerate(self.seqs):
+            if i:
+                out.append(0)
+            out.extend(x)
+        return out
 
 
 class GpuReplay:
     """Replay state for `truth` (uint16 [n_streams][length]) over `stores`."""
 
     def __init__(self, stores, truth: np.ndarray, n_max=16, n_min=2, k=5000, m=10, c=64, alpha=(1, 1), lru=32,
-                 ctx_len=16, device="cuda"):
+                 ctx_len=16, device="cuda", cache_l=None, cache_every=20, cache_cap=FC_MAX_CACHE_TOKENS):
         self.stores = stores
         self.truth_np = np.ascontiguousarray(truth, dtype=np.uint16)
         self.nseq, self.tlen = self.truth_np.shape
@@ -49,6 +92,11 @@ class GpuReplay:
         self.tout = tree_outputs(self.nseq, c, self.device)
         self.aout = accept_outputs(self.nseq, m, self.device)
         self.tgt = torch.empty((self.nseq, c + 1), dtype=torch.int32, device=self.device)
+        self.cache_l, self.cache_every, self.cache_cap = cache_l, cache_every, cache_cap
+        if cache_l is not None:
+            self.ctext = torch.zeros((self.nseq, cache_cap), dtype=torch.uint16, device=self.device)
+            self.clen = torch.zeros(self.nseq, dtype=torch.int32, device=self.device)
+            self.cres = retrieve_outputs(self.nseq, 1, k, m, self.device)
         self.reset()
 
     def reset(self):
@@ -56,6 +104,38 @@ class GpuReplay:
         self.lru_state = [OrderedDict() for _ in range(self.nseq)]
         self.hits = np.zeros(self.nseq, np.int64)
         self.lookups = np.zeros(self.nseq, np.int64)
+        self.served = np.zeros(self.nseq, np.int64)
+        if self.cache_l is not None:
+            self.seqs = [_Sequences(self.cache_cap) for _ in range(self.nseq)]
+            self.chunks = np.zeros(self.nseq, np.int64)
+            self.clen.zero_()
+
+    def _cache_upload(self, changed: dict) -> None:
+        """Ship the CACHE texts of the streams in `changed` (stream -> text
+        length on the device before this step's additions, or -1 when the
+        whole text must be rewritten) in one batched write."""
+        rows, offs, lens, src_off, src_len, parts = [], [], [], [], [], []
+        at = 0
+        for b, old in changed.items():
+            text = self.seqs[b].text()
+            start = 0 if old < 0 else old
+            piece = text[start:]
+            rows.append(b)
+            offs.append(start)
+            lens.append(len(text))
+            src_off.append(at)
+            src_len.append(len(piece))
+            parts.extend(piece)
+            at += len(piece)
+        if not rows:
+            return
+        dev = self.device
+
+        def d(x, dt):
+            return torch.from_numpy(np.asarray(x, dtype=dt)).to(dev)
+
+        fc_cache_write(self.ctext, self.clen, d(rows, np.int32), d(offs, np.int32), d(lens, np.int32),
+                       d(src_off, np.int64), d(src_len, np.int32), d(parts if parts else [0], np.uint16))
 
     def step(self) -> np.ndarray | None:
         """One step for every live stream; returns accepted lengths per stream
@@ -64,16 +144,31 @@ class GpuReplay:
         if len(act) == 0:
             return None
         L = self.ctx_len
+        dev = self.device
         ctx = np.stack([self.truth_np[b, self.pos[b] - L:self.pos[b]] for b in act])
-        slots = np.empty(len(act), np.int64)
+        ctx_d = torch.from_numpy(ctx).to(dev)
+        # Alg. 1: the CACHE first, once it holds cache_l sequences
+        served = np.zeros(len(act), bool)
+        if self.cache_l is not None:
+            elig = np.array([j for j, b in enumerate(act) if len(self.seqs[b].seqs) >= self.cache_l], np.int64)
+            if len(elig):
+                sid = torch.from_numpy(act[elig].astype(np.int32)).to(dev)
+                fc_cache_retrieve(self.ctext, self.clen, torch.from_numpy(ctx[elig]).to(dev), text_row=sid,
+                                  out=self.cres, rows=sid, **self.p)
+                tk = self.cres["taken"][sid.long(), 0].cpu().numpy()
+                served[elig[tk > 0]] = True
+        srv = np.nonzero(served)[0]
+        need = np.nonzero(~served)[0]
+        slots = np.empty(len(need), np.int64)
         miss = []
-        for j, b in enumerate(act):
+        for i, j in enumerate(need):
+            b = act[j]
             d = self.lru_state[b]
             key = ctx[j].tobytes()
             self.lookups[b] += 1
             if key in d:
                 d.move_to_end(key)
-                slots[j] = d[key]
+                slots[i] = d[key]
                 self.hits[b] += 1
             else:
                 if len(d) >= self.lru:
@@ -81,25 +176,55 @@ class GpuReplay:
                 else:
                     slot = len(d)
                 d[key] = slot
-                slots[j] = slot
-                miss.append(j)
-        rows = (act * self.lru + slots).astype(np.int32)
-        dev = self.device
+                slots[i] = slot
+                miss.append(i)
+        rows = (act[need] * self.lru + slots).astype(np.int32)
         if miss:
-            fc_retrieve(self.stores, torch.from_numpy(ctx[miss]).to(dev), out=self.cache, workspace=self.rws,
+            fc_retrieve(self.stores, torch.from_numpy(ctx[need[miss]]).to(dev), out=self.cache, workspace=self.rws,
                         rows=torch.from_numpy(rows[miss]).to(dev), **self.p)
-        B = len(act)
-        ctx_d = torch.from_numpy(ctx).to(dev)
+        # trees: CACHE-served streams first (one source), then the rest
+        order = np.concatenate([srv, need]).astype(np.int64)
+        B, Bs = len(order), len(srv)
         tree = {f: v[:B] for f, v in self.tout.items()}
-        fc_build_tree(self.cache["taken"], self.cache["cont_len"], self.cache["cont_tok"], ctx_d, c=self.c,
-                      alpha=self.alpha, out=tree, workspace=self.tws, rows=torch.from_numpy(rows).to(dev))
-        tgt = fc_targets_from_truth(self.truth, torch.from_numpy(self.pos[act].astype(np.int32)).to(dev), tree,
-                                    seq=torch.from_numpy(act.astype(np.int32)).to(dev), out=self.tgt[:B])
+        if Bs:
+            fc_build_tree(self.cres["taken"], self.cres["cont_len"], self.cres["cont_tok"],
+                          torch.from_numpy(ctx[srv]).to(dev), c=self.c, alpha=(1,),
+                          out={f: v[:Bs] for f, v in tree.items()}, workspace=self.tws,
+                          rows=torch.from_numpy(act[srv].astype(np.int32)).to(dev))
+        if len(need):
+            fc_build_tree(self.cache["taken"], self.cache["cont_len"], self.cache["cont_tok"],
+                          ctx_d if len(need) == len(act) else torch.from_numpy(ctx[need]).to(dev), c=self.c,
+                          alpha=self.alpha,
+                          out={f: v[Bs:] for f, v in tree.items()}, workspace=self.tws,
+                          rows=torch.from_numpy(rows).to(dev))
+        seq_o = act[order]
+        tgt = fc_targets_from_truth(self.truth, torch.from_numpy(self.pos[seq_o].astype(np.int32)).to(dev), tree,
+                                    seq=torch.from_numpy(seq_o.astype(np.int32)).to(dev), out=self.tgt[:B])
         acc = fc_verify_accept(tree, tgt, m=self.p["m"], out={f: v[:B] for f, v in self.aout.items()})
         a = acc["accept_len"].cpu().numpy().astype(np.int64)
         out = np.full(self.nseq, -1, np.int64)
-        out[act] = a
-        self.pos[act] += a
+        out[seq_o] = a
+        if self.cache_l is None:
+            self.pos[seq_o] += a
+            return out
+        last = acc["last_node"].long()
+        depth = tree["pos_ids"].gather(1, last[:, None])[:, 0].cpu().numpy().astype(np.int64)
+        self.served[act[srv]] += 1
+        changed = {}
+        for i, b in enumerate(seq_o):
+            p = int(self.pos[b])
+            old = int(self.seqs[b].tokens)
+            ev = False
+            if depth[i] >= 1:  # a verified draft (R non-empty)
+                ev |= self.seqs[b].add(list(self.truth_np[b, p - L:p]) + list(self.truth_np[b, p:p + depth[i]]))
+            self.pos[b] = p + a[i]
+            while L + self.cache_every * (self.chunks[b] + 1) <= min(self.pos[b], self.tlen):
+                lo = L + self.cache_every * int(self.chunks[b])
+                ev |= self.seqs[b].add(self.truth_np[b, lo:lo + self.cache_every])
+                self.chunks[b] += 1
+            if self.seqs[b].tokens != old or ev:
+                changed[int(b)] = -1 if ev else old
+        self._cache_upload(changed)
         return out
 
     def run(self, max_steps: int = 512) -> dict:
@@ -112,4 +237,5 @@ class GpuReplay:
         acc = np.stack(steps) if steps else np.zeros((0, self.nseq), np.int64)
         live = acc >= 0
         return dict(accept=acc, hits=self.hits.copy(), lookups=self.lookups.copy(), pos=self.pos.copy(),
-                    acc_len=float(acc[live].sum() / max(live.sum(), 1)), steps=len(steps))
+                    cache_served=self.served.copy(), acc_len=float(acc[live].sum() / max(live.sum(), 1)),
+                    steps=len(steps))

@@ -188,3 +188,25 @@ def test_binding_has_no_cpu_path(monkeypatch, tmp_path):
     finally:
         monkeypatch.undo()
         fc.lib.cache_clear()
+
+
+def test_cache_entry_points_reject(L):
+    assert L.fc_cache_lds_bytes(16384) == 32768 + 65536
+    assert L.fc_cache_lds_bytes(1) == 16 + 4
+    assert L.fc_cache_lds_bytes(0) == 0 and L.fc_cache_lds_bytes(16385) == 0
+    one = ctypes.c_void_p(8)
+    p = fc.FcRetrieveParams(16, 2, 5000, 10)
+
+    def call(stride=100, n_texts=2, B=1, L_=4, params=p, ctx=one):
+        return L.fc_cache_retrieve(one, stride, n_texts, one, None, ctx, B, L_, params, *([one] * 8), None, 0, None)
+
+    assert call(stride=0) == 1 and call(stride=16385) == 1 and call(n_texts=0) == 1
+    assert call(B=-1) == 1 and call(L_=0) == 1 and call(ctx=None) == 1
+    assert call(params=fc.FcRetrieveParams(17, 2, 10, 10)) == 1
+    assert call(params=fc.FcRetrieveParams(4, 2, 0, 10)) == 1
+    assert call(params=fc.FcRetrieveParams(4, 2, 10, 256)) == 1
+    assert call(B=0) == 0
+    assert L.fc_cache_write(one, 100, 2, one, -1, one, one, one, one, one, one, None) == 1
+    assert L.fc_cache_write(one, 0, 2, one, 1, one, one, one, one, one, one, None) == 1
+    assert L.fc_cache_write(None, 100, 2, one, 1, one, one, one, one, one, one, None) == 1
+    assert L.fc_cache_write(one, 100, 2, one, 0, one, one, one, one, one, one, None) == 0

@@ -341,3 +341,80 @@ def test_repeat_runs_are_identical():
         assert (a[f] == b[f]).all(), f
     sa2 = host(fc.fc_datastore_build(dev(t)))
     assert (sa2 == host(st.sa)).all()
+
+
+# ------------------------------------------------------------------- CACHE --
+
+def _cache_texts(seed: int, n_texts: int, vocab: int, max_len: int) -> list:
+    """Texts shaped like CACHE contents: short sequences of a small
+    vocabulary (long repeats, many ties) joined by single 0 tokens."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for t in range(n_texts):
+        target = int(rng.integers(0, max_len + 1))
+        toks = []
+        while len(toks) < target:
+            n = int(rng.integers(3, 30))
+            seq = synth.random_text(1000 * seed + 17 * t + len(toks), n, vocab).tolist()
+            toks += ([0] if toks else []) + seq
+        out.append(np.array(toks[:target], np.uint16))
+    return out
+
+
+def test_cache_retrieve_matches_oracle():
+    """fc_cache_retrieve equals the oracle's retrieval over a one-store
+    datastore holding each CACHE text, field by field: empty texts, texts at
+    the 16,384-token limit, more occurrences than k (strided), short and
+    long contexts, a text row map and an output row map."""
+    stride = fc.FC_MAX_CACHE_TOKENS
+    for seed, (vocab, max_len, k, m, n_max, n_min) in enumerate([
+            (4, 400, 30, 4, 16, 2), (9, 3000, 5000, 10, 16, 2), (3, stride, 200, 10, 16, 2),
+            (50, stride, 5000, 16, 8, 1), (6, 800, 7, 3, 5, 3)]):
+        texts = _cache_texts(seed, 6, vocab, max_len)
+        if seed == 0:
+            texts[0] = np.zeros(0, np.uint16)
+        if seed == 2:
+            texts[1] = np.resize(synth.random_text(5, 50, vocab), stride).astype(np.uint16)  # full and periodic
+        buf = np.zeros((len(texts), stride), np.uint16)
+        lens = np.zeros(len(texts), np.int32)
+        for i, t in enumerate(texts):
+            buf[i, :len(t)] = t
+            lens[i] = len(t)
+        rng = np.random.default_rng(100 + seed)
+        B, Lq = 40, 16
+        trow = rng.integers(0, len(texts), size=B).astype(np.int32)
+        ctx = np.zeros((B, Lq), np.uint16)
+        for b in range(B):
+            t = texts[trow[b]]
+            if len(t) > Lq and rng.random() < 0.8:
+                j = int(rng.integers(0, len(t) - Lq))
+                ctx[b] = t[j:j + Lq]
+            else:
+                ctx[b] = rng.integers(1, vocab, size=Lq)
+        out_rows = rng.permutation(B + 5)[:B].astype(np.int32)  # results land in a larger buffer
+        say(f"cache retrieve seed={seed} vocab={vocab} k={k} m={m} n={n_max}..{n_min}")
+        out = fc.retrieve_outputs(B + 5, 1, k, m, torch.device("cuda"))
+        fc.fc_cache_retrieve(dev(buf), dev(lens), dev(ctx), n_max=n_max, n_min=n_min, k=k, m=m,
+                             text_row=dev(trow), out=out, rows=dev(out_rows))
+        torch.cuda.synchronize()
+        g = {f: host(v) for f, v in out.items()}
+        for b in range(B):
+            o = oracle.retrieve([texts[trow[b]]], ctx[b:b + 1], n_max=n_max, n_min=n_min, k=k, m=m)
+            compare_retrieve(g, o, rows=[int(out_rows[b])])
+
+
+@pytest.mark.parametrize("cache_l,cap", [(50, fc.FC_MAX_CACHE_TOKENS), (4, 300)])
+def test_replay_with_cache_matches_oracle(cache_l, cap):
+    """Decode-trace replay with the CACHE branch of Alg. 1: every accepted
+    length, final position, LRU count and CACHE-served count equal the
+    oracle's; the small-cap case evicts and rewrites CACHE texts."""
+    tp, t1 = synth.store(3, "project"), synth.store(1, "single")
+    truth = synth.truth(n_seq=12, length=500)
+    stores = [gpu_store(tp, synth.VOCAB, records=True), gpu_store(t1)]
+    say(f"replay+cache l={cache_l} cap={cap}: gpu")
+    g = GpuReplay(stores, truth, cache_l=cache_l, cache_cap=cap, **P).run(max_steps=400)
+    say(f"replay+cache l={cache_l} cap={cap}: oracle")
+    o = oracle.replay([tp, t1], truth, cache_l=cache_l, cache_cap=cap, **P, max_steps=400)
+    for f in ("accept", "hits", "lookups", "pos", "cache_served"):
+        assert (g[f] == o[f]).all(), f
+    assert g["cache_served"].sum() > 0

@@ -70,3 +70,107 @@ def test_replay_periodic_stream_lru_counts():
     r = oracle.replay([store], t, m=4, k=50, c=8, alpha=(1,), lru=10, max_steps=1000)
     assert r["hits"][0] == 0
     assert r["acc_len"] == 1.0
+
+
+# ------------------------------------------------------------------ CACHE ---
+
+def _brute_cache_replay(texts, truth, n_max, n_min, k, m, c, alpha, ctx_len, cache_l, every, cap, max_steps):
+    """Alg. 1's cache branch and the CACHE updates of Section IV-B, restated
+    with the brute-force retrieval, trie and acceptance (no LRU: it never
+    changes what is accepted)."""
+    import brute
+
+    nseq, tlen = truth.shape
+    pos = [ctx_len] * nseq
+    seqs = [[] for _ in range(nseq)]
+    done = [0] * nseq
+    served = [0] * nseq
+
+    def text(b):
+        out = []
+        for i, x in enumerate(seqs[b]):
+            out += ([0] if i else []) + x
+        return out
+
+    def add(b, seq):
+        seq = [int(x) for x in seq][-cap:]
+        if seq:
+            seqs[b].append(seq)
+            while sum(len(x) for x in seqs[b]) + len(seqs[b]) - 1 > cap:
+                seqs[b].pop(0)
+
+    steps = []
+    for _ in range(max_steps):
+        act = [b for b in range(nseq) if pos[b] < tlen]
+        if not act:
+            break
+        row = [-1] * nseq
+        for b in act:
+            p = pos[b]
+            ctx = [int(x) for x in truth[b, p - ctx_len:p]]
+            r, al = None, tuple(alpha)
+            if len(seqs[b]) >= cache_l:
+                rc = brute.retrieve([text(b)], ctx, n_max, n_min, k, m)
+                if sum(rc["taken"]) > 0:
+                    r, al = rc, (1,)
+                    served[b] += 1
+            if r is None:
+                r = brute.retrieve(texts, ctx, n_max, n_min, k, m)
+            conts = [(s, cont) for s, _, cont in r["slots"]]
+            t = brute.draft_tree(conts, al, c, ctx[-1])
+            target = [int(truth[b, p + d]) if p + d < tlen else -1 for (_, _, _, d) in t["rows"]]
+            acc, _, u = brute.accept(t["rows"], target)
+            depth = t["rows"][u][3]
+            if sum(r["taken"]) > 0 and depth >= 1:
+                add(b, ctx + [int(x) for x in truth[b, p:p + depth]])
+            row[b] = acc
+            pos[b] += acc
+            while ctx_len + every * (done[b] + 1) <= min(pos[b], tlen):
+                lo = ctx_len + every * done[b]
+                add(b, truth[b, lo:lo + every])
+                done[b] += 1
+        steps.append(row)
+    return np.array(steps), np.array(pos), np.array(served)
+
+
+def test_cache_text_and_eviction():
+    c = oracle.Cache(cap=10)
+    assert c.size == 0 and len(c.text()) == 0
+    c.add([1, 2, 3])
+    c.add([4, 5])
+    assert c.text().tolist() == [1, 2, 3, 0, 4, 5] and c.size == 2
+    c.add([6, 7, 8])  # 10 tokens with separators: fits exactly
+    assert c.text().tolist() == [1, 2, 3, 0, 4, 5, 0, 6, 7, 8]
+    c.add([9])  # 12 > 10: the oldest sequence goes
+    assert c.text().tolist() == [4, 5, 0, 6, 7, 8, 0, 9] and c.size == 3
+    c.add(list(range(1, 15)))  # longer than the cap alone: its last 10 tokens, everything else dropped
+    assert c.text().tolist() == list(range(5, 15)) and c.size == 1
+    c.add([])
+    assert c.size == 1
+
+
+def test_cache_replay_matches_brute_force():
+    """Tiny vocabularies make long repeats, so the CACHE activates, serves
+    steps, fills past its cap and evicts; every accepted length, final
+    position and cache-served count must equal an independent restatement."""
+    for seed, (vocab, cache_l, every, cap) in enumerate([(5, 2, 7, 60), (7, 1, 5, 40), (4, 3, 9, 200)]):
+        store = synth.random_text(300 + seed, 250, vocab, 0.03)
+        truth = np.stack([synth.random_text(400 + 10 * seed + i, 90, vocab) for i in range(3)])
+        kw = dict(n_max=6, n_min=2, k=20, m=4, c=8, alpha=(1,))
+        r = oracle.replay([store], truth, lru=4, ctx_len=6, max_steps=200, cache_l=cache_l, cache_every=every,
+                          cache_cap=cap, **kw)
+        acc, pos, served = _brute_cache_replay([store], truth, ctx_len=6, cache_l=cache_l, every=every, cap=cap,
+                                               max_steps=200, **kw)
+        assert (r["accept"] == acc).all(), seed
+        assert (r["pos"] == pos).all() and (r["cache_served"] == served).all()
+        assert served.sum() > 0  # the cache branch was exercised
+
+
+def test_cache_inactive_is_plain_replay():
+    texts, truth = _setup()
+    kw = dict(m=6, k=300, c=16, alpha=(1,), lru=4, max_steps=120)
+    base = oracle.replay(texts, truth, **kw)
+    never = oracle.replay(texts, truth, cache_l=10 ** 9, **kw)
+    for f in ("accept", "hits", "lookups", "pos"):
+        assert (base[f] == never[f]).all(), f
+    assert (never["cache_served"] == 0).all()
