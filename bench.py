@@ -30,7 +30,7 @@ if ROOT not in sys.path:
 import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
-WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "build": 3, "copy": 0}
+WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "replay-cache": 3, "build": 3, "copy": 0}
 # kernels each entry point launches (rocprofv3 kernel names start with these)
 ENTRY_KERNELS = {
     "fc_retrieve": ("k_search", "k_offsets", "k_gather"),
@@ -177,8 +177,8 @@ def main():
     import paper_2502_17139_amd as fc
     import synth
 
-    if args.workload == "replay":
-        return run_replay(args)
+    if args.workload in ("replay", "replay-cache"):
+        return run_replay(args, cache=args.workload == "replay-cache")
     if args.workload == "build":
         return run_build(args)
     if args.workload == "copy":
@@ -333,9 +333,12 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def run_replay(args):
+def run_replay(args, cache: bool = False):
     """Decode-trace replay: 128 streams of 4096 tokens drawn like the 10M-token
-    project store, over the 10M + 1B stores, up to 512 steps, LRU(32)."""
+    project store, over the 10M + 1B stores, up to 512 steps, LRU(32).  With
+    cache, each stream also keeps the CACHE of Section IV-B (activation at
+    l = 50 sequences, output added every 20 tokens, Section V-D) and Alg. 1
+    searches it first."""
     import torch
     import paper_2502_17139_amd as fc
     from paper_2502_17139_amd.replay import GpuReplay
@@ -347,7 +350,8 @@ def run_replay(args):
     texts = [synth.store(3, r) for r in synth.store_roles(3)]
     stores = [fc.Store(torch.from_numpy(t).to(dev), pair_vocab=synth.VOCAB, records=True) for t in texts]
     truth = synth.truth()
-    rp = GpuReplay(stores, truth, **p)
+    ckw = dict(cache_l=50, cache_every=20) if cache else {}
+    rp = GpuReplay(stores, truth, **p, **ckw)
     rp.run(max_steps=args.warmup)  # warm-up steps, then a fresh replay is timed
     rp.reset()
     torch.cuda.synchronize()
@@ -358,18 +362,23 @@ def run_replay(args):
     live = res["accept"] >= 0
     tokens = int(res["accept"][live].sum())
     line = {
-        "metric": "decode-trace replay steps/sec (128 streams; retrieve + tree + accept per step)",
+        "metric": ("decode-trace replay with CACHE steps/sec (128 streams; CACHE or datastore retrieval + tree + "
+                   "accept per step)" if cache else
+                   "decode-trace replay steps/sec (128 streams; retrieve + tree + accept per step)"),
         "value": res["steps"] / wall, "unit": "steps/s", "n_gpus": 1, "steps": res["steps"], "warmup": args.warmup,
         "ms_per_step": 1e3 * wall / max(res["steps"], 1), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "u16/u32 (integer)",
         "data": "synthetic (seeded streams from the project pool; no dataset)",
-        "config": {"workload": "replay over project 10M + general 1B", "streams": int(truth.shape[0]),
-                   "stream_len": int(truth.shape[1]), "lru": 32, **{kk: p[kk] for kk in ("n_max", "n_min", "k", "m", "c")}},
+        "config": {"workload": "replay over project 10M + general 1B" + (" with CACHE (l=50, every 20)" if cache else ""),
+                   "streams": int(truth.shape[0]), "stream_len": int(truth.shape[1]), "lru": 32,
+                   **{kk: p[kk] for kk in ("n_max", "n_min", "k", "m", "c")}},
         "roofline": None,
         "accepted_tokens_per_s": tokens / wall,
         "acc_len": res["acc_len"],
         "lru_hit_rate": float(res["hits"].sum() / max(res["lookups"].sum(), 1)),
         "retrievals": int(res["lookups"].sum() - res["hits"].sum()),
+        "cache_served": int(res["cache_served"].sum()),
+        "cache_served_share": float(res["cache_served"].sum() / max(res["cache_served"].sum() + res["lookups"].sum(), 1)),
     }
     print(json.dumps(line), flush=True)
 

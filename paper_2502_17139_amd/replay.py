@@ -41,34 +41,36 @@ from . import (FC_MAX_CACHE_TOKENS, accept_outputs, fc_build_tree, fc_build_tree
 
 class _Sequences:
     """One stream's CACHE sequences and the text they make (joined by 0),
-    bounded by `cap` tokens: the oldest sequences go first."""
+    bounded by `cap` tokens: the oldest sequences go first.  The text is
+    kept as one flat list, so an append costs its own length."""
 
     def __init__(self, cap: int):
         self.cap = cap
-        self.seqs = []
-        self.tokens = 0  # text length, separators included
+        self.lens = []  # sequence lengths, oldest first
+        self.flat = []  # the text
+
+    @property
+    def tokens(self) -> int:
+        return len(self.flat)
 
     def add(self, seq) -> bool:
         """Append a sequence; True when older sequences had to go."""
         seq = [int(x) for x in seq][-self.cap:]
         if not seq:
             return False
-        self.seqs.append(seq)
-        self.tokens += len(seq) + (1 if len(self.seqs) > 1 else 0)
-        evicted = False
-        while self.tokens > self.cap:
-            first = self.seqs.pop(0)
-            self.tokens -= len(first) + (1 if self.seqs else 0)
-            evicted = True
-        return evicted
+        if self.flat:
+            self.flat.append(0)
+        self.flat.extend(seq)
+        self.lens.append(len(seq))
+        cut = 0
+        while len(self.flat) - cut > self.cap:
+            cut += self.lens.pop(0) + 1  # the sequence and the separator after it
+        if cut:
+            self.flat = self.flat[cut:]
+        return cut > 0
 
     def text(self) -> list:
-        out = []
-        for i, x in enumerate(self.seqs):
-            if i:
-                out.append(0)
-            out.extend(x)
-        return out
+        return self.flat
 
 
 class GpuReplay:
@@ -150,7 +152,7 @@ class GpuReplay:
         # Alg. 1: the CACHE first, once it holds cache_l sequences
         served = np.zeros(len(act), bool)
         if self.cache_l is not None:
-            elig = np.array([j for j, b in enumerate(act) if len(self.seqs[b].seqs) >= self.cache_l], np.int64)
+            elig = np.array([j for j, b in enumerate(act) if len(self.seqs[b].lens) >= self.cache_l], np.int64)
             if len(elig):
                 sid = torch.from_numpy(act[elig].astype(np.int32)).to(dev)
                 fc_cache_retrieve(self.ctext, self.clen, torch.from_numpy(ctx[elig]).to(dev), text_row=sid,
