@@ -30,7 +30,8 @@ if ROOT not in sys.path:
 import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
-WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "replay-cache": 3, "build": 3, "copy": 0}
+WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "replay-cache": 3, "replay-control": 3,
+             "build": 3, "copy": 0}
 # kernels each entry point launches (rocprofv3 kernel names start with these)
 ENTRY_KERNELS = {
     "fc_retrieve": ("k_search", "k_offsets", "k_gather"),
@@ -177,8 +178,8 @@ def main():
     import paper_2502_17139_amd as fc
     import synth
 
-    if args.workload in ("replay", "replay-cache"):
-        return run_replay(args, cache=args.workload == "replay-cache")
+    if args.workload in ("replay", "replay-cache", "replay-control"):
+        return run_replay(args, cache=args.workload != "replay", control=args.workload == "replay-control")
     if args.workload == "build":
         return run_build(args)
     if args.workload == "copy":
@@ -333,12 +334,15 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def run_replay(args, cache: bool = False):
+def run_replay(args, cache: bool = False, control: bool = False):
     """Decode-trace replay: 128 streams of 4096 tokens drawn like the 10M-token
     project store, over the 10M + 1B stores, up to 512 steps, LRU(32).  With
     cache, each stream also keeps the CACHE of Section IV-B (activation at
     l = 50 sequences, output added every 20 tokens, Section V-D) and Alg. 1
-    searches it first."""
+    searches it first.  With control, Alg. 1's missing table and skip gate
+    (p = 0.5) are on too; the synthetic streams have no line breaks, so the
+    skip token is their most frequent token and the gate's draws come from
+    the seeded generator."""
     import torch
     import paper_2502_17139_amd as fc
     from paper_2502_17139_amd.replay import GpuReplay
@@ -351,6 +355,10 @@ def run_replay(args, cache: bool = False):
     stores = [fc.Store(torch.from_numpy(t).to(dev), pair_vocab=synth.VOCAB, records=True) for t in texts]
     truth = synth.truth()
     ckw = dict(cache_l=50, cache_every=20) if cache else {}
+    if control:
+        tok = int(np.bincount(truth.ravel()).argmax())
+        draws = np.stack([synth.uniform(31, 30, step, truth.shape[0], 0, 2 ** 31 - 1) for step in range(1024)])
+        ckw.update(missing=True, skip_tok=tok, skip_p=0.5, skip_draws=draws)
     rp = GpuReplay(stores, truth, **p, **ckw)
     rp.run(max_steps=args.warmup)  # warm-up steps, then a fresh replay is timed
     rp.reset()
@@ -362,7 +370,9 @@ def run_replay(args, cache: bool = False):
     live = res["accept"] >= 0
     tokens = int(res["accept"][live].sum())
     line = {
-        "metric": ("decode-trace replay with CACHE steps/sec (128 streams; CACHE or datastore retrieval + tree + "
+        "metric": ("decode-trace replay with Alg. 1 (CACHE, missing table, skip gate) steps/sec (128 streams)"
+                   if control else
+                   "decode-trace replay with CACHE steps/sec (128 streams; CACHE or datastore retrieval + tree + "
                    "accept per step)" if cache else
                    "decode-trace replay steps/sec (128 streams; retrieve + tree + accept per step)"),
         "value": res["steps"] / wall, "unit": "steps/s", "n_gpus": 1, "steps": res["steps"], "warmup": args.warmup,
@@ -379,6 +389,8 @@ def run_replay(args, cache: bool = False):
         "retrievals": int(res["lookups"].sum() - res["hits"].sum()),
         "cache_served": int(res["cache_served"].sum()),
         "cache_served_share": float(res["cache_served"].sum() / max(res["cache_served"].sum() + res["lookups"].sum(), 1)),
+        "missing_skips": int(res["missing_skips"].sum()),
+        "gate_skips": int(res["gate_skips"].sum()),
     }
     print(json.dumps(line), flush=True)
 

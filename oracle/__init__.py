@@ -210,7 +210,8 @@ class Cache:
 
 def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int = 10, c: int = 64, alpha=(1, 1),
            lru: int = 32, ctx_len: int = 16, max_steps: int = 512, cache_l: int | None = None,
-           cache_every: int = 20, cache_cap: int = 16384) -> dict:
+           cache_every: int = 20, cache_cap: int = 16384, missing: bool = False, skip_tok: int | None = None,
+           skip_p: float = 0.5, skip_draws=None) -> dict:
     """Decode-trace replay over known streams (reading of the average
     acceptance length setting, Section V-C eq. (7)).
 
@@ -240,10 +241,24 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
         truncated every 20 tokens, Section V-D).
     The CACHE's trie uses weight 1 (one source).
 
+    Alg. 1's retrieval-timing control, for a context that the CACHE did not
+    serve:
+      - missing=True keeps a missing table M per stream: a context whose
+        datastore retrieval found no occurrence in any store is added to M
+        (the prose's reading: only an actual, empty retrieval adds), and a
+        context found in M later is not retrieved at all;
+      - skip_tok set enables the skip gate: when the context ends with
+        skip_tok, the datastores are searched only when the step's draw
+        skip_draws[step][stream] (uniform integers in [0, 2^31)) is below
+        skip_p * 2^31;
+      - a context that is not retrieved gets an empty R: a bare root, so the
+        step accepts the target model's own token only.
+
     Returns accept [steps][n_streams] (-1 for finished streams), hits and
     lookups of the LRU per stream, cache_served (steps whose R came from the
-    CACHE) per stream, final positions, the mean accepted length per live
-    step, and the step count.
+    CACHE), missing_skips and gate_skips (contexts not retrieved because of
+    M or of the gate) per stream, final positions, the mean accepted length
+    per live step, and the step count.
     """
     from collections import OrderedDict
 
@@ -254,11 +269,14 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
     hits = [0] * nseq
     lookups = [0] * nseq
     served = [0] * nseq
+    m_skips = [0] * nseq
+    g_skips = [0] * nseq
+    mtab = [set() for _ in range(nseq)]
     cch = [Cache(cache_cap) for _ in range(nseq)] if cache_l is not None else None
     chunks_done = [0] * nseq
     fields = ("taken", "cont_len", "cont_tok")
     steps = []
-    for _ in range(max_steps):
+    for step in range(max_steps):
         act = [b for b in range(nseq) if pos[b] < tlen]
         if not act:
             break
@@ -273,9 +291,24 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
                         got[j] = {f: r[f][0].copy() for f in fields}
                         from_cache[j] = True
                         served[b] += 1
-        need = [j for j in range(len(act)) if got[j] is None]
+        need = []
+        empty = {"taken": np.zeros(len(texts), np.int32), "cont_len": np.zeros(k, np.uint8),
+                 "cont_tok": np.zeros((k, m), np.uint16)}
+        for j in range(len(act)):
+            if got[j] is not None:
+                continue
+            b = act[j]
+            if missing and ctx[j].tobytes() in mtab[b]:
+                got[j] = empty
+                m_skips[b] += 1
+            elif (skip_tok is not None and int(ctx[j][-1]) == skip_tok
+                  and not int(skip_draws[step][b]) < int(skip_p * 2 ** 31)):
+                got[j] = empty
+                g_skips[b] += 1
+            else:
+                need.append(j)
         keys = {j: ctx[j].tobytes() for j in need}
-        missing = []
+        misses = []
         for j in need:
             b = act[j]
             lookups[b] += 1
@@ -283,16 +316,18 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
                 caches[b].move_to_end(keys[j])
                 hits[b] += 1
             else:
-                missing.append(j)
-        if missing:
-            r = retrieve(texts, ctx[missing], n_max=n_max, n_min=n_min, k=k, m=m)
-            for i, j in enumerate(missing):
+                misses.append(j)
+        if misses:
+            r = retrieve(texts, ctx[misses], n_max=n_max, n_min=n_min, k=k, m=m)
+            for i, j in enumerate(misses):
                 b = act[j]
                 if len(caches[b]) >= lru:
                     caches[b].popitem(last=False)
                 caches[b][keys[j]] = {f: r[f][i].copy() for f in fields}
         for j in need:
             got[j] = caches[act[j]][keys[j]]
+            if missing and int(np.asarray(got[j]["taken"]).sum()) == 0:
+                mtab[act[j]].add(keys[j])
         acc = np.zeros(len(act), np.int64)
         depth = np.zeros(len(act), np.int64)
         for group, al in ((True, (1,)), (False, tuple(alpha))):
@@ -328,5 +363,5 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
     accept = np.stack(steps) if steps else np.zeros((0, nseq), np.int64)
     live = accept >= 0
     return dict(accept=accept, hits=np.array(hits), lookups=np.array(lookups), pos=np.array(pos),
-                cache_served=np.array(served), acc_len=float(accept[live].sum() / max(live.sum(), 1)),
-                steps=len(steps))
+                cache_served=np.array(served), missing_skips=np.array(m_skips), gate_skips=np.array(g_skips),
+                acc_len=float(accept[live].sum() / max(live.sum(), 1)), steps=len(steps))

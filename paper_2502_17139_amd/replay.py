@@ -26,6 +26,14 @@ row of FC_MAX_CACHE_TOKENS tokens per stream, sequences joined by 0); the
 host keeps the sequence lists, decides evictions (oldest sequences first
 when a text would outgrow its row) and ships each step's appended tokens in
 one batched fc_cache_write.
+
+Alg. 1's retrieval-timing control (for contexts the CACHE did not serve):
+with missing=True a per-stream missing table holds the contexts whose
+datastore retrieval found nothing, and such a context is not retrieved
+again; with skip_tok set, a context ending with skip_tok is retrieved only
+when the step's draw (skip_draws[step][stream], uniform in [0, 2^31)) is
+below skip_p * 2^31.  A context that is not retrieved gets an empty result
+(a bare root).  Both tables are host-side sets next to the LRU keys.
 """
 from __future__ import annotations
 
@@ -77,7 +85,8 @@ class GpuReplay:
     """Replay state for `truth` (uint16 [n_streams][length]) over `stores`."""
 
     def __init__(self, stores, truth: np.ndarray, n_max=16, n_min=2, k=5000, m=10, c=64, alpha=(1, 1), lru=32,
-                 ctx_len=16, device="cuda", cache_l=None, cache_every=20, cache_cap=FC_MAX_CACHE_TOKENS):
+                 ctx_len=16, device="cuda", cache_l=None, cache_every=20, cache_cap=FC_MAX_CACHE_TOKENS,
+                 missing=False, skip_tok=None, skip_p=0.5, skip_draws=None):
         self.stores = stores
         self.truth_np = np.ascontiguousarray(truth, dtype=np.uint16)
         self.nseq, self.tlen = self.truth_np.shape
@@ -86,7 +95,11 @@ class GpuReplay:
         self.c, self.alpha, self.lru, self.ctx_len = c, tuple(alpha)[:len(stores)], lru, ctx_len
         self.device = torch.device(device)
         S = len(stores)
-        self.cache = retrieve_outputs(self.nseq * lru, S, k, m, self.device)
+        # LRU slots, plus one last row that stays empty (taken 0): the input
+        # row of contexts that are not retrieved
+        self.cache = retrieve_outputs(self.nseq * lru + 1, S, k, m, self.device)
+        self.cache["taken"][-1].zero_()
+        self.empty_row = self.nseq * lru
         self.rws = torch.empty(max(fc_retrieve_workspace_bytes(self.nseq, S, n_max, n_min, k, m), 1),
                                dtype=torch.uint8, device=self.device)
         self.tws = torch.empty(max(fc_build_tree_workspace_bytes(self.nseq), 1), dtype=torch.uint8,
@@ -95,6 +108,9 @@ class GpuReplay:
         self.aout = accept_outputs(self.nseq, m, self.device)
         self.tgt = torch.empty((self.nseq, c + 1), dtype=torch.int32, device=self.device)
         self.cache_l, self.cache_every, self.cache_cap = cache_l, cache_every, cache_cap
+        self.missing, self.skip_tok = missing, skip_tok
+        self.skip_thr = int(skip_p * 2 ** 31)
+        self.skip_draws = None if skip_draws is None else np.asarray(skip_draws)
         if cache_l is not None:
             self.ctext = torch.zeros((self.nseq, cache_cap), dtype=torch.uint16, device=self.device)
             self.clen = torch.zeros(self.nseq, dtype=torch.int32, device=self.device)
@@ -107,6 +123,10 @@ class GpuReplay:
         self.hits = np.zeros(self.nseq, np.int64)
         self.lookups = np.zeros(self.nseq, np.int64)
         self.served = np.zeros(self.nseq, np.int64)
+        self.m_skips = np.zeros(self.nseq, np.int64)
+        self.g_skips = np.zeros(self.nseq, np.int64)
+        self.mtab = [set() for _ in range(self.nseq)]
+        self.step_i = 0
         if self.cache_l is not None:
             self.seqs = [_Sequences(self.cache_cap) for _ in range(self.nseq)]
             self.chunks = np.zeros(self.nseq, np.int64)
@@ -159,8 +179,24 @@ class GpuReplay:
                                   out=self.cres, rows=sid, **self.p)
                 tk = self.cres["taken"][sid.long(), 0].cpu().numpy()
                 served[elig[tk > 0]] = True
+        # Alg. 1's timing control for the rest: the missing table, then the
+        # skip gate
+        skip = np.zeros(len(act), bool)
+        if self.missing or self.skip_tok is not None:
+            for j, b in enumerate(act):
+                if served[j]:
+                    continue
+                if self.missing and ctx[j].tobytes() in self.mtab[b]:
+                    skip[j] = True
+                    self.m_skips[b] += 1
+                elif (self.skip_tok is not None and int(ctx[j][-1]) == self.skip_tok
+                      and not int(self.skip_draws[self.step_i][b]) < self.skip_thr):
+                    skip[j] = True
+                    self.g_skips[b] += 1
+        self.step_i += 1
         srv = np.nonzero(served)[0]
-        need = np.nonzero(~served)[0]
+        need = np.nonzero(~served & ~skip)[0]
+        skp = np.nonzero(skip)[0]
         slots = np.empty(len(need), np.int64)
         miss = []
         for i, j in enumerate(need):
@@ -184,7 +220,15 @@ class GpuReplay:
         if miss:
             fc_retrieve(self.stores, torch.from_numpy(ctx[need[miss]]).to(dev), out=self.cache, workspace=self.rws,
                         rows=torch.from_numpy(rows[miss]).to(dev), **self.p)
-        # trees: CACHE-served streams first (one source), then the rest
+        if self.missing and len(need):
+            tot = self.cache["taken"][torch.from_numpy(rows).long().to(dev)].sum(1).cpu().numpy()
+            for i, j in enumerate(need):
+                if tot[i] == 0:
+                    self.mtab[act[j]].add(ctx[j].tobytes())
+        # trees: CACHE-served streams first (one source), then the rest, the
+        # contexts that were not retrieved reading the empty row
+        rows = np.concatenate([rows, np.full(len(skp), self.empty_row, np.int32)])
+        need = np.concatenate([need, skp]).astype(np.int64)
         order = np.concatenate([srv, need]).astype(np.int64)
         B, Bs = len(order), len(srv)
         tree = {f: v[:B] for f, v in self.tout.items()}
@@ -195,8 +239,8 @@ class GpuReplay:
                           rows=torch.from_numpy(act[srv].astype(np.int32)).to(dev))
         if len(need):
             fc_build_tree(self.cache["taken"], self.cache["cont_len"], self.cache["cont_tok"],
-                          ctx_d if len(need) == len(act) else torch.from_numpy(ctx[need]).to(dev), c=self.c,
-                          alpha=self.alpha,
+                          ctx_d if np.array_equal(need, np.arange(len(act))) else torch.from_numpy(ctx[need]).to(dev),
+                          c=self.c, alpha=self.alpha,
                           out={f: v[Bs:] for f, v in tree.items()}, workspace=self.tws,
                           rows=torch.from_numpy(rows).to(dev))
         seq_o = act[order]
@@ -239,5 +283,6 @@ class GpuReplay:
         acc = np.stack(steps) if steps else np.zeros((0, self.nseq), np.int64)
         live = acc >= 0
         return dict(accept=acc, hits=self.hits.copy(), lookups=self.lookups.copy(), pos=self.pos.copy(),
-                    cache_served=self.served.copy(), acc_len=float(acc[live].sum() / max(live.sum(), 1)),
+                    cache_served=self.served.copy(), missing_skips=self.m_skips.copy(),
+                    gate_skips=self.g_skips.copy(), acc_len=float(acc[live].sum() / max(live.sum(), 1)),
                     steps=len(steps))

@@ -418,3 +418,32 @@ def test_replay_with_cache_matches_oracle(cache_l, cap):
     for f in ("accept", "hits", "lookups", "pos", "cache_served"):
         assert (g[f] == o[f]).all(), f
     assert g["cache_served"].sum() > 0
+
+
+@pytest.mark.parametrize("case", ["project-streams", "recurring-misses"])
+def test_replay_with_retrieval_control_matches_oracle(case):
+    """Alg. 1 in full (CACHE branch, missing table, skip gate with p = 0.5
+    on the streams' most frequent token): every accepted length, position
+    and branch count equal the oracle's.  The second case replays periodic
+    streams over stores they rarely match, so failed contexts recur and the
+    missing table bypasses them."""
+    if case == "project-streams":
+        texts = [synth.store(3, "project"), synth.store(1, "single")]
+        truth = synth.truth(n_seq=12, length=500)
+        stores = [gpu_store(texts[0], synth.VOCAB, records=True), gpu_store(texts[1])]
+    else:
+        texts = [synth.random_text(41, 200_000, synth.VOCAB, 0.01), synth.store(1, "single")]
+        truth = np.stack([np.resize(synth.random_text(50 + i, 37, synth.VOCAB), 400) for i in range(8)])
+        stores = [gpu_store(texts[0], synth.VOCAB, records=True), gpu_store(texts[1])]
+    tok = int(np.bincount(truth.ravel()).argmax())
+    draws = np.stack([synth.uniform(31, 30, step, truth.shape[0], 0, 2 ** 31 - 1) for step in range(400)])
+    kw = dict(cache_l=50, missing=True, skip_tok=tok, skip_p=0.5, skip_draws=draws)
+    say(f"replay+control {case}: gpu")
+    g = GpuReplay(stores, truth, **kw, **P).run(max_steps=400)
+    say(f"replay+control {case}: oracle")
+    o = oracle.replay(texts, truth, **kw, **P, max_steps=400)
+    for f in ("accept", "hits", "lookups", "pos", "cache_served", "missing_skips", "gate_skips"):
+        assert (g[f] == o[f]).all(), f
+    assert g["gate_skips"].sum() > 0
+    if case == "recurring-misses":
+        assert g["missing_skips"].sum() > 0

@@ -74,10 +74,12 @@ def test_replay_periodic_stream_lru_counts():
 
 # ------------------------------------------------------------------ CACHE ---
 
-def _brute_cache_replay(texts, truth, n_max, n_min, k, m, c, alpha, ctx_len, cache_l, every, cap, max_steps):
-    """Alg. 1's cache branch and the CACHE updates of Section IV-B, restated
-    with the brute-force retrieval, trie and acceptance (no LRU: it never
-    changes what is accepted)."""
+def _brute_cache_replay(texts, truth, n_max, n_min, k, m, c, alpha, ctx_len, cache_l, every, cap, max_steps,
+                        missing=False, skip_tok=None, skip_p=0.5, draws=None):
+    """Alg. 1 (the CACHE branch, the missing table and the skip gate) and
+    the CACHE updates of Section IV-B, restated with the brute-force
+    retrieval, trie and acceptance (no LRU: it never changes what is
+    accepted)."""
     import brute
 
     nseq, tlen = truth.shape
@@ -85,6 +87,8 @@ def _brute_cache_replay(texts, truth, n_max, n_min, k, m, c, alpha, ctx_len, cac
     seqs = [[] for _ in range(nseq)]
     done = [0] * nseq
     served = [0] * nseq
+    mtab = [set() for _ in range(nseq)]
+    skips = [0, 0]
 
     def text(b):
         out = []
@@ -100,7 +104,7 @@ def _brute_cache_replay(texts, truth, n_max, n_min, k, m, c, alpha, ctx_len, cac
                 seqs[b].pop(0)
 
     steps = []
-    for _ in range(max_steps):
+    for step in range(max_steps):
         act = [b for b in range(nseq) if pos[b] < tlen]
         if not act:
             break
@@ -115,7 +119,16 @@ def _brute_cache_replay(texts, truth, n_max, n_min, k, m, c, alpha, ctx_len, cac
                     r, al = rc, (1,)
                     served[b] += 1
             if r is None:
-                r = brute.retrieve(texts, ctx, n_max, n_min, k, m)
+                if missing and tuple(ctx) in mtab[b]:
+                    r = dict(taken=[0], slots=[])
+                    skips[0] += 1
+                elif skip_tok is not None and ctx[-1] == skip_tok and draws[step][b] >= skip_p * 2 ** 31:
+                    r = dict(taken=[0], slots=[])
+                    skips[1] += 1
+                else:
+                    r = brute.retrieve(texts, ctx, n_max, n_min, k, m)
+                    if missing and sum(r["taken"]) == 0:
+                        mtab[b].add(tuple(ctx))
             conts = [(s, cont) for s, _, cont in r["slots"]]
             t = brute.draft_tree(conts, al, c, ctx[-1])
             target = [int(truth[b, p + d]) if p + d < tlen else -1 for (_, _, _, d) in t["rows"]]
@@ -130,7 +143,7 @@ def _brute_cache_replay(texts, truth, n_max, n_min, k, m, c, alpha, ctx_len, cac
                 add(b, truth[b, lo:lo + every])
                 done[b] += 1
         steps.append(row)
-    return np.array(steps), np.array(pos), np.array(served)
+    return np.array(steps), np.array(pos), np.array(served), skips
 
 
 def test_cache_text_and_eviction():
@@ -159,8 +172,8 @@ def test_cache_replay_matches_brute_force():
         kw = dict(n_max=6, n_min=2, k=20, m=4, c=8, alpha=(1,))
         r = oracle.replay([store], truth, lru=4, ctx_len=6, max_steps=200, cache_l=cache_l, cache_every=every,
                           cache_cap=cap, **kw)
-        acc, pos, served = _brute_cache_replay([store], truth, ctx_len=6, cache_l=cache_l, every=every, cap=cap,
-                                               max_steps=200, **kw)
+        acc, pos, served, _ = _brute_cache_replay([store], truth, ctx_len=6, cache_l=cache_l, every=every, cap=cap,
+                                                  max_steps=200, **kw)
         assert (r["accept"] == acc).all(), seed
         assert (r["pos"] == pos).all() and (r["cache_served"] == served).all()
         assert served.sum() > 0  # the cache branch was exercised
@@ -174,3 +187,68 @@ def test_cache_inactive_is_plain_replay():
     for f in ("accept", "hits", "lookups", "pos"):
         assert (base[f] == never[f]).all(), f
     assert (never["cache_served"] == 0).all()
+
+
+
+# ---------------------------------------------- missing table, skip gate ---
+
+def _draws(n_steps: int, n_seq: int, seed: int = 9) -> np.ndarray:
+    return np.stack([synth.uniform(seed, 30, step, n_seq, 0, 2 ** 31 - 1) for step in range(n_steps)])
+
+
+def test_missing_table_closed_form():
+    """A store that never matches a periodic stream: each of the 20
+    contexts is retrieved once, fails, enters M, and is never retrieved
+    again."""
+    store = np.full(5000, 7, np.uint16)
+    period = (np.arange(20) * 13 % 97 + 100).astype(np.uint16)
+    t = np.tile(period, 12)[None, :]
+    steps = t.shape[1] - 16
+    r = oracle.replay([store], t, m=4, k=50, c=8, alpha=(1,), lru=32, max_steps=1000, missing=True)
+    assert (r["accept"][:, 0] == 1).all()
+    assert r["lookups"][0] == 20 and r["missing_skips"][0] == steps - 20 and r["gate_skips"][0] == 0
+
+
+def test_skip_gate_closed_form():
+    """p = 0 skips every context ending with the skip token, p = 1 none; with
+    a store that never matches every step advances one token, so the
+    skipped count is the number of such contexts."""
+    store = np.full(5000, 7, np.uint16)
+    period = (np.arange(20) * 13 % 97 + 100).astype(np.uint16)
+    t = np.tile(period, 12)[None, :]
+    tok = int(period[5])
+    draws = _draws(300, 1)
+    want = int(sum(1 for p in range(16, t.shape[1]) if t[0, p - 1] == tok))
+    kw = dict(m=4, k=50, c=8, alpha=(1,), lru=32, max_steps=1000, skip_tok=tok, skip_draws=draws)
+    r0 = oracle.replay([store], t, skip_p=0.0, **kw)
+    r1 = oracle.replay([store], t, skip_p=1.0, **kw)
+    assert r0["gate_skips"][0] == want and r1["gate_skips"][0] == 0
+    assert r0["lookups"][0] == t.shape[1] - 16 - want and r1["lookups"][0] == t.shape[1] - 16
+
+
+def test_control_replay_matches_brute_force():
+    """CACHE, missing table and skip gate together against the independent
+    restatement: every accepted length, position, CACHE-served count and
+    skip count equal."""
+    tot = np.zeros(3, np.int64)
+    for seed, (vocab, cache_l, every, cap, period) in enumerate([(5, 3, 7, 80, 0), (8, 2, 5, 120, 0),
+                                                                 (40, 6, 9, 100, 23), (30, 50, 20, 400, 17)]):
+        store = synth.random_text(600 + seed, 200, vocab, 0.05)
+        if period:  # recurring contexts that the store rarely matches: the missing table's case
+            truth = np.stack([np.resize(synth.random_text(700 + 10 * seed + i, period, vocab), 100)
+                              for i in range(3)])
+        else:
+            truth = np.stack([synth.random_text(700 + 10 * seed + i, 100, vocab) for i in range(3)])
+        draws = _draws(250, 3, seed=20 + seed)
+        tok = int(truth[0, 3])
+        kw = dict(n_max=6, n_min=2, k=20, m=4, c=8, alpha=(1,))
+        r = oracle.replay([store], truth, lru=4, ctx_len=6, max_steps=250, cache_l=cache_l, cache_every=every,
+                          cache_cap=cap, missing=True, skip_tok=tok, skip_p=0.5, skip_draws=draws, **kw)
+        acc, pos, served, skips = _brute_cache_replay([store], truth, ctx_len=6, cache_l=cache_l, every=every,
+                                                      cap=cap, max_steps=250, missing=True, skip_tok=tok,
+                                                      skip_p=0.5, draws=draws, **kw)
+        assert (r["accept"] == acc).all(), seed
+        assert (r["pos"] == pos).all() and (r["cache_served"] == served).all()
+        assert r["missing_skips"].sum() == skips[0] and r["gate_skips"].sum() == skips[1]
+        tot += [served.sum(), skips[0], skips[1]]
+    assert (tot > 0).all()  # every branch of Alg. 1 was exercised
