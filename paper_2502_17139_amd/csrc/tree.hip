@@ -45,12 +45,14 @@ struct Alpha {
 };
 
 struct TreeLayout {
-  size_t str, A, perm, len, lcp, mlen, total;
+  size_t str, A, perm, len, lcp, mlen, E, total;
 };
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-__host__ __device__ inline TreeLayout tree_layout(int k, int m) {
+// sep_e: the run ends E get a region of their own instead of reusing the
+// strings' (the strings then stay readable until the rows are written).
+__host__ __device__ inline TreeLayout tree_layout(int k, int m, bool sep_e = false) {
   TreeLayout t;
   size_t o = 0;
   t.str = o;  // k*m uint16 tokens (by slot); later run ends E[p][d-1]; later mask bitsets
@@ -68,6 +70,11 @@ __host__ __device__ inline TreeLayout tree_layout(int k, int m) {
   o = align_up(o + (size_t)k, 16);
   t.mlen = o;  // k uint8 by merged position
   o = align_up(o + (size_t)k, 16);
+  t.E = t.str;
+  if (sep_e) {
+    t.E = o;  // k*m uint16 run ends / weights
+    o = align_up(o + (size_t)k * m * 2, 16);
+  }
   t.total = o;
   return t;
 }
@@ -526,15 +533,18 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   __shared__ uint32_t s_sel_w[FC_MAX_TREE_ROWS];
   __shared__ uint16_t s_sel_p[FC_MAX_TREE_ROWS];
   __shared__ uint8_t s_sel_d[FC_MAX_TREE_ROWS];
+  __shared__ uint16_t s_sel_t[FC_MAX_TREE_ROWS];  // token of a kept node (light launch)
   __shared__ int16_t s_par[FC_MAX_TREE_ROWS];
   __shared__ uint64_t s_dball[FC_MAX_TREE_ROWS / fc::kWave][MAXM];
   __shared__ uint32_t s_pick[3];
 
   // This launch owns the queries in `list` (built by k_tree_classify);
   // workgroups past the list's length leave at once, after every real one
-  // has been dispatched.
+  // has been dispatched.  (list has B entries: reading it before the count
+  // check saves a round trip.)
+  const int b_raw = list[blockIdx.x];
   if ((int)blockIdx.x >= *list_count) return;
-  const int b = list[blockIdx.x];
+  const int b = b_raw;
   const int tid = threadIdx.x;
   const int lane = fc::lane_id();
   const int w = tid / fc::kWave;
@@ -542,21 +552,30 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   const int in_row = fc::map_row(rows, n_rows, b);
   const int64_t row0 = (int64_t)(in_row < 0 ? 0 : in_row) * k;
 
+  // The light launch keeps the strings next to the run ends, so kept
+  // nodes take their tokens from LDS.
+  constexpr bool kSepE = NT < 1024;
+  const uint16_t root_tok = ctx[(int64_t)b * L + L - 1];  // issued early, used at the end
   // Malformed rows (a row outside the map's range, a negative count or more
   // than k slots) count as T = 0 and are reported with num_nodes = -1.
   int T_raw = 0, bad = in_row < 0;
-  for (int s = 0; s < S && in_row >= 0; ++s) {
-    const int t = taken[(int64_t)in_row * S + s];
-    bad |= t < 0;
-    T_raw += t > 0 ? t : 0;
+  int tk_s[FC_MAX_SOURCES] = {0, 0, 0, 0};
+#pragma unroll
+  for (int s = 0; s < FC_MAX_SOURCES; ++s) {
+    if (s < S && in_row >= 0) {
+      const int t = taken[(int64_t)in_row * S + s];
+      tk_s[s] = t;
+      bad |= t < 0;
+      T_raw += t > 0 ? t : 0;
+    }
   }
   bad |= T_raw > k;
   bad |= T_raw > t_hi;  // cannot happen: k_tree_classify routes queries by T
   if (bad) T_raw = 0;
 
-  const TreeLayout lay = tree_layout(t_hi, m);
+  const TreeLayout lay = tree_layout(t_hi, m, kSepE);
   uint16_t* str = (uint16_t*)(smem + lay.str);
-  uint16_t* E = str;
+  uint16_t* E = (uint16_t*)(smem + lay.E);
   uint32_t* anc = (uint32_t*)(smem + lay.str);
   uint32_t* A = (uint32_t*)(smem + lay.A);
   uint16_t* perm = (uint16_t*)(smem + lay.perm);
@@ -566,10 +585,12 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
 
   if (tid == 0) {
     int acc = 0;
-    for (int s = 0; s < S; ++s) {
-      s_seg[s] = acc;
-      const int t = bad ? 0 : taken[(int64_t)in_row * S + s];
-      acc += t;
+#pragma unroll
+    for (int s = 0; s < FC_MAX_SOURCES; ++s) {
+      if (s < S) {
+        s_seg[s] = acc;
+        acc += bad ? 0 : tk_s[s];
+      }
     }
     s_seg[S] = acc;
     s_err = bad;
@@ -736,7 +757,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
       }
       if (tid == 0) A[T] = a_tot;
     }
-    __syncthreads();  // str is dead from here on: E reuses it
+    __syncthreads();  // in the heavy launch str is dead from here on: E reuses it
     // alpha weight of merged positions [p, e)
     auto wsum = [&](uint32_t e, uint32_t p) -> uint32_t {
       return alpha_flat ? alpha.a[0] * (e - p) : A[e] - A[p];
@@ -921,6 +942,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
             s_sel_p[o] = (uint16_t)p;
             s_sel_d[o] = (uint8_t)d;
             s_sel_w[o] = W;
+            if (kSepE) s_sel_t[o] = str[perm[p] * m + d - 1];
             ++o;
           }
         }
@@ -965,12 +987,12 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     uint32_t wt = 0;
     if (r < num) {
       if (r == 0) {
-        tk = ctx[(int64_t)b * L + L - 1];
+        tk = root_tok;
         wt = root_w;
       } else {
         const int p = s_sel_p[r];
         const int d = s_sel_d[r];
-        tk = cont_tok[(row0 + perm[p]) * m + d - 1];
+        tk = kSepE ? s_sel_t[r] : cont_tok[(row0 + perm[p]) * m + d - 1];
         pr = s_par[r];
         wt = s_sel_w[r];
         ps = d;
@@ -1029,7 +1051,7 @@ fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint1
   int words = 0;
   if ((((uintptr_t)cont_tok) & 15) == 0 && ((size_t)k * m) % 8 == 0) words = 2;
   else if ((((uintptr_t)cont_tok) & 3) == 0 && ((size_t)k * m) % 2 == 0) words = 1;
-  const TreeLayout small = tree_layout(t_small, m);
+  const TreeLayout small = tree_layout(t_small, m, true);
   if (small.total > 64 * 1024)
     (void)hipFuncSetAttribute((const void*)k_tree_fast<256, MAXM>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)small.total);
