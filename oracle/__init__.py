@@ -365,3 +365,61 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
     return dict(accept=accept, hits=np.array(hits), lookups=np.array(lookups), pos=np.array(pos),
                 cache_served=np.array(served), missing_skips=np.array(m_skips), gate_skips=np.array(g_skips),
                 acc_len=float(accept[live].sum() / max(live.sum(), 1)), steps=len(steps))
+
+
+def rope(x: np.ndarray, positions: np.ndarray, base: float) -> np.ndarray:
+    """Rotary position embedding, rotate-half form: for d < D/2 the pair
+    (x_d, x_{d+D/2}) is rotated by the angle position * base^(-2d/D).
+    x [..., n, D] (float64), positions [n]."""
+    x = np.asarray(x, dtype=np.float64)
+    D = x.shape[-1]
+    half = D // 2
+    inv = base ** (-2.0 * np.arange(half) / D)
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * inv[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = x[..., :half], x[..., half:]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+def tree_attention(q, k_tree, v_tree, k_cache, v_cache, prefix_len, num_nodes, mask, pos_ids,
+                   rope_base: float = 10000.0) -> np.ndarray:
+    """Attention of a draft tree's rows in one target-model forward (Section
+    IV-D, eq. (4)): row i of tree b sits at position prefix_len[b] +
+    pos_ids[b][i] (the root, depth 0, right after the cached prefix) and
+    attends to every cached prefix token and to the tree rows j with
+    mask[b][i][j] = 1.  Queries and tree keys are rotated by their
+    positions (rotary embedding, rotate-half form); cached keys are stored
+    rotated.  Scores are q.k / sqrt(D); the output is the softmax-weighted
+    sum of values.  Rows at or past num_nodes[b] are 0.
+
+    q [B][R][H][D], k_tree/v_tree [B][R][Hkv][D], k_cache/v_cache
+    [B][Pmax][Hkv][D] (any float dtype; computed in float64), prefix_len and
+    num_nodes [B], mask [B][R][R], pos_ids [B][R]; query head h reads key
+    head h // (H // Hkv).  Returns float64 [B][R][H][D].
+    """
+    q = np.asarray(q, dtype=np.float64)
+    B, R, H, D = q.shape
+    Hkv = k_tree.shape[2]
+    grp = H // Hkv
+    out = np.zeros((B, R, H, D), np.float64)
+    for b in range(B):
+        P = int(prefix_len[b])
+        n = int(num_nodes[b])
+        if n <= 0:
+            continue
+        pos = P + np.asarray(pos_ids[b][:n], dtype=np.int64)
+        for h in range(H):
+            g = h // grp
+            qh = rope(q[b, :n, h, :], pos, rope_base)
+            kt = rope(np.asarray(k_tree[b, :n, g, :], dtype=np.float64), pos, rope_base)
+            vt = np.asarray(v_tree[b, :n, g, :], dtype=np.float64)
+            kc = np.asarray(k_cache[b, :P, g, :], dtype=np.float64)
+            vc = np.asarray(v_cache[b, :P, g, :], dtype=np.float64)
+            keys = np.concatenate([kc, kt], axis=0)
+            vals = np.concatenate([vc, vt], axis=0)
+            for i in range(n):
+                allowed = np.concatenate([np.ones(P, bool), np.asarray(mask[b][i][:n]) == 1])
+                s = keys[allowed] @ qh[i] / np.sqrt(D)
+                w = np.exp(s - s.max())
+                out[b, i, h] = (w / w.sum()) @ vals[allowed]
+    return out
