@@ -321,6 +321,43 @@ fc_status fc_verify_accept(const int32_t* num_nodes, const int32_t* node_tok, co
                            int32_t* accept_len, int32_t* accept_tok, int32_t* last_node, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Tree attention (verification of the draft tree)                           */
+/* ------------------------------------------------------------------------ */
+
+#define FC_TREE_ATTN_HEAD_DIM 128 /* head dimension this build supports */
+
+/*
+ * The attention step of the target model's forward pass over a draft tree
+ * (Section IV-D, eq. (4): one pass verifies every draft sequence, each row
+ * attending to its ancestors through the tree mask, at the positions the
+ * position ids give).  Row i of tree b sits at position prefix_len[b] +
+ * pos_ids[b][i] (the root, depth 0, right after the cached prefix) and
+ * attends to the prefix_len[b] cached tokens and to the tree rows j with
+ * mask[b][i][j] = 1 (fc_build_tree's mask, pos_ids and num_nodes).  Queries
+ * and the tree's keys are rotated by their positions (rotary embedding,
+ * rotate-half form: the pair (d, d + D/2) turns by position *
+ * rope_base^(-2d/D)); cached keys are stored already rotated.  Scores are
+ * q.k / sqrt(D), softmax in fp32; out = softmax-weighted sum of values.
+ * Rows at or past num_nodes[b] (and every row of a tree with num_nodes < 1)
+ * are 0.  Query head h reads key/value head h / (H / Hkv).
+ *
+ * q [B][R][H][D], k_tree, v_tree [B][R][Hkv][D], k_cache, v_cache
+ * [B][Pmax][Hkv][D]: bf16 bit patterns as uint16, 16-byte aligned;
+ * prefix_len, num_nodes [B] and pos_ids [B][R], mask [B][R][R]: int32
+ * (device lengths are clamped to [0, Pmax] and [0, R]); out [B][R][H][D]
+ * fp32, 16-byte aligned.  D must be FC_TREE_ATTN_HEAD_DIM
+ * (FC_ERR_UNSUPPORTED otherwise); 1 <= R <= FC_MAX_TREE_ROWS, H % Hkv == 0,
+ * rope_base > 1.  The products run on bf16 matrix cores: rotated queries
+ * and keys and the softmax weights are rounded to bf16, accumulations are
+ * fp32.
+ */
+fc_status fc_tree_attention(const uint16_t* q, const uint16_t* k_tree, const uint16_t* v_tree,
+                            const uint16_t* k_cache, const uint16_t* v_cache, const int32_t* prefix_len,
+                            const int32_t* num_nodes, const int32_t* mask, const int32_t* pos_ids, int32_t B,
+                            int32_t R, int32_t H, int32_t Hkv, int32_t D, int32_t Pmax, float rope_base, float* out,
+                            hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Decode-trace replay                                                       */
 /* ------------------------------------------------------------------------ */
 

@@ -24,6 +24,7 @@ FC_MAX_NMAX = 16
 FC_MAX_TREE_ROWS = 256
 FC_BUCKETS = 65537
 FC_MAX_CACHE_TOKENS = 16384
+FC_TREE_ATTN_HEAD_DIM = 128
 
 STATUS = {0: "FC_OK", 1: "FC_ERR_INVALID", 2: "FC_ERR_WORKSPACE", 3: "FC_ERR_DEVICE", 4: "FC_ERR_UNSUPPORTED"}
 
@@ -34,6 +35,7 @@ EXPORTS = (
     "fc_pair_table_entries", "fc_store_prepare_pairs", "fc_record_bytes", "fc_store_prepare_records",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
     "fc_verify_accept", "fc_targets_from_truth", "fc_cache_lds_bytes", "fc_cache_retrieve", "fc_cache_write",
+    "fc_tree_attention",
 )
 
 
@@ -98,6 +100,8 @@ def lib() -> ctypes.CDLL:
                                     vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp]
     L.fc_cache_write.restype = ctypes.c_int
     L.fc_cache_write.argtypes = [vp, ctypes.c_int64, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp]
+    L.fc_tree_attention.restype = ctypes.c_int
+    L.fc_tree_attention.argtypes = [vp] * 9 + [i32] * 6 + [ctypes.c_float, vp, vp]
     L.fc_build_tree_workspace_bytes.restype = sz
     L.fc_build_tree_workspace_bytes.argtypes = [i32]
     L.fc_build_tree.restype = ctypes.c_int
@@ -296,6 +300,28 @@ def fc_cache_write(texts: torch.Tensor, text_len: torch.Tensor, dst_row: torch.T
     _check("fc_cache_write", lib().fc_cache_write(
         _ptr(texts), stride, n_texts, _ptr(text_len), dst_row.numel(), _ptr(dst_row), _ptr(dst_off),
         _ptr(new_len), _ptr(src_off), _ptr(src_len), _ptr(src_tok), _stream(stream)))
+
+
+# ------------------------------------------------------- tree attention ----
+
+def fc_tree_attention(q: torch.Tensor, k_tree: torch.Tensor, v_tree: torch.Tensor, k_cache: torch.Tensor,
+                      v_cache: torch.Tensor, prefix_len: torch.Tensor, tree: dict, rope_base: float = 10000.0,
+                      out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Tree attention (bf16 q [B][R][H][D], k/v_tree [B][R][Hkv][D],
+    k/v_cache [B][Pmax][Hkv][D]) with the tree's num_nodes, mask and pos_ids;
+    returns fp32 [B][R][H][D]."""
+    for t in (q, k_tree, v_tree, k_cache, v_cache):
+        if t.dtype != torch.bfloat16 or t.dim() != 4:
+            raise ValueError("q, k_tree, v_tree, k_cache, v_cache must be 4-D bfloat16")
+    B, R, H, D = q.shape
+    Hkv, Pmax = k_tree.shape[2], k_cache.shape[1]
+    if out is None:
+        out = _empty((B, R, H, D), torch.float32, q.device)
+    u16 = lambda t: _ptr(t.view(torch.uint16))  # noqa: E731
+    _check("fc_tree_attention", lib().fc_tree_attention(
+        u16(q), u16(k_tree), u16(v_tree), u16(k_cache), u16(v_cache), _ptr(prefix_len), _ptr(tree["num_nodes"]),
+        _ptr(tree["mask"]), _ptr(tree["pos_ids"]), B, R, H, Hkv, D, Pmax, rope_base, _ptr(out), _stream(stream)))
+    return out
 
 
 # ----------------------------------------------------------------- tree ----

@@ -447,3 +447,96 @@ def test_replay_with_retrieval_control_matches_oracle(case):
     assert g["gate_skips"].sum() > 0
     if case == "recurring-misses":
         assert g["missing_skips"].sum() > 0
+
+
+# ---------------------------------------------------------- tree attention --
+
+def _bf16(rng, *shape, scale=1.0):
+    return torch.from_numpy(rng.uniform(-scale, scale, size=shape)).to(torch.bfloat16)
+
+
+def _attention_bound(q, kt, kc, vt, vc, P, tree, base):
+    """Per-row error bound of the bf16 matrix-core evaluation against the
+    exact result on the same inputs: rotated queries and keys are rounded to
+    bf16 (relative 2^-9 each), so a score moves by at most
+    2^-8 * sum_d |q_d k_d| / sqrt(D) (plus fp32 accumulation, < 1e-5); a
+    softmax whose scores move by at most delta moves its weighted mean by at
+    most 2*delta*max|v|; the bf16 weights in the value product add 2^-8 *
+    max|v|."""
+    B, R, H, D = q.shape
+    Hkv = kt.shape[2]
+    bound = np.zeros((B, R, H))
+    for b in range(B):
+        n = int(tree["num_nodes"][b])
+        p = int(P[b])
+        if n <= 0:
+            continue
+        pos = p + tree["pos_ids"][b][:n].astype(np.int64)
+        for h in range(H):
+            g = h // (H // Hkv)
+            qh = np.abs(oracle.rope(q[b, :n, h], pos, base))
+            keys = np.abs(np.concatenate([kc[b, :p, g], oracle.rope(kt[b, :n, g], pos, base)]))
+            vmax = max(np.abs(vc[b, :p, g]).max() if p else 0.0, np.abs(vt[b, :n, g]).max())
+            for i in range(n):
+                allowed = np.concatenate([np.ones(p, bool), tree["mask"][b][i][:n] == 1])
+                delta = 2.0 ** -8 * (keys[allowed] @ qh[i]).max() / np.sqrt(D) + 1e-5
+                bound[b, i, h] = 2 * delta * vmax + 2.0 ** -8 * vmax + 1e-6
+    return bound
+
+
+def _tree_attention_case(trees: dict, rows, H, Hkv, P, Pmax, seed, base=10000.0, qscale=1.0):
+    rng = np.random.default_rng(seed)
+    B = len(rows)
+    R = trees["mask"].shape[1]
+    D = fc.FC_TREE_ATTN_HEAD_DIM
+    tsub = {f: np.ascontiguousarray(trees[f][rows]) for f in ("num_nodes", "mask", "pos_ids")}
+    q = _bf16(rng, B, R, H, D, scale=qscale)
+    kt, vt = _bf16(rng, B, R, Hkv, D), _bf16(rng, B, R, Hkv, D)
+    kc, vc = _bf16(rng, B, max(Pmax, 1), Hkv, D), _bf16(rng, B, max(Pmax, 1), Hkv, D)
+    Pn = np.asarray(P, np.int32)
+    g = fc.fc_tree_attention(q.cuda(), kt.cuda(), vt.cuda(), kc.cuda(), vc.cuda(), dev(Pn),
+                             {f: dev(v) for f, v in tsub.items()}, rope_base=base)
+    torch.cuda.synchronize()
+    g = host(g).astype(np.float64)
+    f64 = lambda t: t.float().numpy().astype(np.float64)  # noqa: E731
+    o = oracle.tree_attention(f64(q), f64(kt), f64(vt), f64(kc), f64(vc), Pn, tsub["num_nodes"], tsub["mask"],
+                              tsub["pos_ids"], rope_base=base)
+    bound = _attention_bound(f64(q), f64(kt), f64(kc), f64(vt), f64(vc), Pn, tsub, base)
+    err = np.abs(g - o).max(axis=3)
+    assert (err <= bound).all(), (err.max(), float((err - bound).max()))
+    for b in range(B):  # rows past the tree are exactly zero
+        assert (g[b, max(int(tsub["num_nodes"][b]), 0):] == 0).all()
+    return err, bound
+
+
+def test_tree_attention_matches_oracle():
+    """Tree attention on real draft trees (the 1M-token workload's batch):
+    prefixes of 0 to 300 cached tokens across block edges, multi-head and
+    grouped heads, every output within the derived bf16 bound of the exact
+    result, rows past the tree zero."""
+    t = synth.store(1, "single")
+    ctx = synth.queries(1)
+    st = gpu_store(t)
+    for c in (64, 8):
+        g = gpu_pipeline([st], ctx, P, (1,), c)
+        trees = {f: g[f] for f in ("num_nodes", "mask", "pos_ids")}
+        for (B, H, Hkv, seed) in ((16, 4, 4, 1), (16, 4, 2, 2), (3, 3, 1, 3)):
+            rows = list(range(3 * seed, 3 * seed + B))
+            P_ = [(0, 1, 31, 32, 33, 100, 300)[i % 7] for i in range(B)]
+            say(f"tree attention c={c} B={B} H={H} Hkv={Hkv}")
+            err, bound = _tree_attention_case(trees, rows, H, Hkv, P_, 320, seed)
+            assert err.mean() < 0.25 * bound.mean()  # typical error well inside the bound
+
+
+def test_tree_attention_masks_and_edge_cases():
+    """No prefix and sharp scores, so every row attends to a handful of its
+    ancestors and a wrong mask entry would move it far outside the bound; a
+    malformed tree (num_nodes = -1) gives zeros; large positions."""
+    t = synth.store(1, "single")
+    ctx = synth.queries(1)
+    g = gpu_pipeline([gpu_store(t)], ctx, P, (1,), 64)
+    trees = {f: g[f].copy() for f in ("num_nodes", "mask", "pos_ids")}
+    trees["num_nodes"][5] = -1
+    err, bound = _tree_attention_case(trees, list(range(0, 24)), 2, 2, [0] * 24, 0, 11, qscale=3.0)
+    assert (err[5] == 0).all()
+    err, bound = _tree_attention_case(trees, list(range(24, 32)), 2, 1, [4000] * 8, 4000, 12, base=1e6)
