@@ -31,7 +31,7 @@ import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "replay-cache": 3, "replay-control": 3,
-             "build": 3, "copy": 0}
+             "build": 3, "copy": 0, "tree-attention": 1}
 # kernels each entry point launches (rocprofv3 kernel names start with these)
 ENTRY_KERNELS = {
     "fc_retrieve": ("k_search", "k_offsets", "k_gather"),
@@ -182,6 +182,8 @@ def main():
         return run_replay(args, cache=args.workload != "replay", control=args.workload == "replay-control")
     if args.workload == "build":
         return run_build(args)
+    if args.workload == "tree-attention":
+        return run_tree_attention(args)
     if args.workload == "copy":
         return run_copy(args)
     cfg = WORKLOADS[args.workload]
@@ -432,6 +434,78 @@ def run_build(args):
         "config": {"workload": "SA build, 1B general + 10M project stores"}, "roofline": None, "builds": out,
     }
     print(json.dumps(line), flush=True)
+
+
+def run_tree_attention(args):
+    """One layer's attention step over 64 draft trees (the 1M-token
+    workload's batch, c = 64, so 65 rows each) after a 2,048-token cached
+    prefix, 32 heads of 128 dims (a 7B-class code model's attention shape),
+    bf16 inputs from a seeded generator."""
+    import torch
+    import paper_2502_17139_amd as fc
+    import synth
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    p = dict(synth.PARAMS)
+    t = synth.store(1, "single")
+    ctx = torch.from_numpy(synth.queries(1)).to(dev)
+    st = fc.Store(torch.from_numpy(t).to(dev), pair_vocab=synth.VOCAB, records=True)
+    r = fc.fc_retrieve([st], ctx, n_max=p["n_max"], n_min=p["n_min"], k=p["k"], m=p["m"])
+    tree = fc.fc_build_tree(r["taken"], r["cont_len"], r["cont_tok"], ctx, c=p["c"], alpha=(1,))
+    B, R = tree["mask"].shape[0], tree["mask"].shape[1]
+    H, Hkv, D, Pn = 32, 32, fc.FC_TREE_ATTN_HEAD_DIM, 2048
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5)
+    rnd = lambda *shape: (torch.rand(*shape, generator=gen, device=dev) * 2 - 1).to(torch.bfloat16)  # noqa: E731
+    q, kt, vt = rnd(B, R, H, D), rnd(B, R, Hkv, D), rnd(B, R, Hkv, D)
+    kc, vc = rnd(B, Pn, Hkv, D), rnd(B, Pn, Hkv, D)
+    prefix = torch.full((B,), Pn, dtype=torch.int32, device=dev)
+    out = torch.empty((B, R, H, D), dtype=torch.float32, device=dev)
+    run = lambda: fc.fc_tree_attention(q, kt, vt, kc, vc, prefix, tree, out=out)  # noqa: E731
+    for _ in range(max(args.warmup, 1)):
+        run()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    K = args.steps
+    e0.record(stream)
+    for _ in range(K):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    nn = tree["num_nodes"].cpu().numpy()
+    rows = int(nn.sum())
+    # algorithmic bytes: each head reads its queries, its key/value head's
+    # prefix and tree rows, the mask once per tree, and writes its outputs
+    hb = R * D * 2 + (Pn + R) * D * 2 * 2 + R * D * 4
+    byts = B * H * hb + B * R * R * 4 + B * R * 4
+    flops = float(sum(4 * int(n) * (Pn + int(n)) * D for n in nn)) * H
+    gbs = byts / (ms * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        f64 = lambda x: x[:1].float().cpu().numpy().astype(np.float64)  # noqa: E731
+        t0 = time.perf_counter()
+        oracle.tree_attention(f64(q), f64(kt), f64(vt), f64(kc), f64(vc), np.array([Pn], np.int32), nn[:1],
+                              tree["mask"][:1].cpu().numpy(), tree["pos_ids"][:1].cpu().numpy())
+        spent = time.perf_counter() - t0
+        cpu = {"value": int(nn[0]) * H / spent, "unit": "row-heads/s", "cores": 1, "kind": "oracle",
+               "sample": f"tree 0 ({int(nn[0])} rows x {H} heads), {spent:.1f} s"}
+    print(json.dumps({
+        "metric": "tree-attention row-heads/sec (64 trees x 65 rows, 2,048-token prefix, 32 heads x 128)",
+        "value": rows * H / (ms * 1e-3), "unit": "row-heads/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded bf16 tensors; trees from the 1M-token workload)",
+        "config": {"workload": "tree attention, 64 trees, prefix 2048, H 32, Hkv 32, D 128", "trees": B, "rows": R,
+                   "prefix": Pn, "heads": H, "kv_heads": Hkv, "head_dim": D},
+        "roofline": {"bound": "hbm", "kernel": "fc_tree_attention", "achieved": gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes": byts, "mfma_tflops": flops / (ms * 1e-3) / 1e12,
+                     "mfma_frac_bf16": flops / (ms * 1e-3) / 2.5e15},
+        "cpu_baseline": cpu,
+    }), flush=True)
 
 
 def run_copy(args):

@@ -72,8 +72,9 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
     const int32_t* __restrict__ prefix_len, const int32_t* __restrict__ num_nodes, const int32_t* __restrict__ mask,
     const int32_t* __restrict__ pos_ids, int B, int R, int H, int Hkv, int Pmax, double log2_base,
     float* __restrict__ out) {
-  __shared__ __align__(16) __bf16 s_k[kBlock * kKStride];
-  __shared__ __align__(16) __bf16 s_vt[kD * kVStride];
+  // two buffers: the next block is staged while the current one is used
+  __shared__ __align__(16) __bf16 s_k[2][kBlock * kKStride];
+  __shared__ __align__(16) __bf16 s_vt[2][kD * kVStride];
 
   // workgroup -> (tree, head): consecutive ids on one XCD when the count
   // divides evenly, so the heads of one key head share an L2
@@ -128,64 +129,121 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
   const float scale = 1.0f / sqrtf((float)kD);
 
   const int n_pre = (P + kBlock - 1) / kBlock, n_tree = (n + kBlock - 1) / kBlock;
-  for (int blk = 0; blk < n_pre + n_tree; ++blk) {
-    const bool tree = blk >= n_pre;
-    const int base = (tree ? blk - n_pre : blk) * kBlock;
-    const int lim = tree ? n : P;
-    // stage keys (rotated for tree rows) and transposed values
-    for (int it = tid; it < kBlock * (kD / 16); it += nt) {
-      const int kk = it / (kD / 16), c = it - kk * (kD / 16);  // key, pair of 8-dim chunks c and c + D/16
+  const int nb = n_pre + n_tree;
+
+  // Staging (at least 256 threads): a block's keys are 512 chunks of 8 dims
+  // (two per thread), its values 128 quads of 4 keys x 8 dims (one per
+  // thread below 128), transposed into s_vt as 8-byte rows of 4 keys.
+  constexpr int kKChunks = kBlock * (kD / 8);
+  uint4 pk[2], pv[4];
+  auto fetch_prefix = [&](int blk) {  // global loads of a cached block into registers
+    const int base = blk * kBlock;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int it = tid + u * nt;
+      const int kk = it / (kD / 8), c = it - kk * (kD / 8);
+      pk[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (it < kKChunks && base + kk < P)
+        pk[u] = *(const uint4*)(k_cache + (((int64_t)b * Pmax + base + kk) * Hkv + g_kv) * kD + 8 * c);
+    }
+    const int kq = tid / (kD / 8), c = tid - kq * (kD / 8);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = base + 4 * kq + r;
+      pv[r] = make_uint4(0u, 0u, 0u, 0u);
+      if (tid < kBlock / 4 * (kD / 8) && j < P)
+        pv[r] = *(const uint4*)(v_cache + (((int64_t)b * Pmax + j) * Hkv + g_kv) * kD + 8 * c);
+    }
+  };
+  auto put_values = [&](int buf) {  // pv (4 keys x 8 dims) -> s_vt, transposed
+    if (tid < kBlock / 4 * (kD / 8)) {
+      const int kq = tid / (kD / 8), c = tid - kq * (kD / 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        uint32_t hw[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t word = (e >> 1) == 0 ? pv[r].x : (e >> 1) == 1 ? pv[r].y : (e >> 1) == 2 ? pv[r].z : pv[r].w;
+          hw[r] = (word >> (16 * (e & 1))) & 0xFFFFu;
+        }
+        *(uint2*)&s_vt[buf][(8 * c + e) * kVStride + 4 * kq] = make_uint2(hw[0] | (hw[1] << 16), hw[2] | (hw[3] << 16));
+      }
+    }
+  };
+  auto put_prefix = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int it = tid + u * nt;
+      const int kk = it / (kD / 8), c = it - kk * (kD / 8);
+      if (it < kKChunks) *(uint4*)&s_k[buf][kk * kKStride + 8 * c] = pk[u];
+    }
+    put_values(buf);
+  };
+  auto stage_tree = [&](int tb, int buf) {  // a block of tree rows, keys rotated
+    const int base = tb * kBlock;
+    if (tid < kBlock * (kD / 16)) {
+      const int kk = tid / (kD / 16), c = tid - kk * (kD / 16);  // key, chunks c and c + D/16
       const int j = base + kk;
       float a[8], bb[8];
-      if (j < lim) {
-        const uint16_t* src = tree ? k_tree + (((int64_t)b * R + j) * Hkv + g_kv) * kD
-                                   : k_cache + (((int64_t)b * Pmax + j) * Hkv + g_kv) * kD;
+      if (j < n) {
+        const uint16_t* src = k_tree + (((int64_t)b * R + j) * Hkv + g_kv) * kD;
         load8(src + 8 * c, a);
         load8(src + kD / 2 + 8 * c, bb);
-        if (tree) {
-          const int pos = P + pos_ids[(int64_t)b * R + j];
+        const int pos = P + pos_ids[(int64_t)b * R + j];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            float s, cs;
-            rope_sincos(pos, 8 * c + e, log2_base, s, cs);
-            const float x0 = a[e], x1 = bb[e];
-            a[e] = x0 * cs - x1 * s;
-            bb[e] = x1 * cs + x0 * s;
-          }
+        for (int e = 0; e < 8; ++e) {
+          float sn, cs;
+          rope_sincos(pos, 8 * c + e, log2_base, sn, cs);
+          const float x0 = a[e], x1 = bb[e];
+          a[e] = x0 * cs - x1 * sn;
+          bb[e] = x1 * cs + x0 * sn;
         }
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) a[e] = bb[e] = 0.0f;
       }
+      bf16x8 pa, pbb;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        s_k[kk * kKStride + 8 * c + e] = f2bf(a[e]);
-        s_k[kk * kKStride + kD / 2 + 8 * c + e] = f2bf(bb[e]);
+        pa[e] = f2bf(a[e]);
+        pbb[e] = f2bf(bb[e]);
       }
+      *(bf16x8*)&s_k[buf][kk * kKStride + 8 * c] = pa;
+      *(bf16x8*)&s_k[buf][kk * kKStride + kD / 2 + 8 * c] = pbb;
     }
-    for (int it = tid; it < kBlock * (kD / 8); it += nt) {
-      const int kk = it / (kD / 8), c = it - kk * (kD / 8);
-      const int j = base + kk;
-      float v[8];
-      if (j < lim) {
-        const uint16_t* src = tree ? v_tree + (((int64_t)b * R + j) * Hkv + g_kv) * kD
-                                   : v_cache + (((int64_t)b * Pmax + j) * Hkv + g_kv) * kD;
-        load8(src + 8 * c, v);
-      } else {
+    const int kq = tid / (kD / 8), c = tid - kq * (kD / 8);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = 0.0f;
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s_vt[(8 * c + e) * kVStride + kk] = f2bf(v[e]);
+    for (int r = 0; r < 4; ++r) {
+      const int j = base + 4 * kq + r;
+      pv[r] = make_uint4(0u, 0u, 0u, 0u);
+      if (tid < kBlock / 4 * (kD / 8) && j < n)
+        pv[r] = *(const uint4*)(v_tree + (((int64_t)b * R + j) * Hkv + g_kv) * kD + 8 * c);
     }
-    __syncthreads();
+    put_values(buf);
+  };
+
+  if (n_pre > 0) {
+    fetch_prefix(0);
+    put_prefix(0);
+  } else if (n_tree > 0) {
+    stage_tree(0, 0);
+  }
+  __syncthreads();
+  for (int blk = 0; blk < nb; ++blk) {
+    const int cur = blk & 1;
+    const bool tree = blk >= n_pre;
+    const int base = (tree ? blk - n_pre : blk) * kBlock;
+    const int lim = tree ? n : P;
+    const bool next_pre = blk + 1 < n_pre;
+    if (next_pre) fetch_prefix(blk + 1);  // in flight during this block's products
 
     // S^T for keys 0..15 and 16..31 of the block
+    const __bf16* sk = s_k[cur];
     floatx4 st0 = {0.0f, 0.0f, 0.0f, 0.0f}, st1 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int kc = 0; kc < kDSteps; ++kc) {
-      const bf16x8 a0 = *(const bf16x8*)&s_k[lc * kKStride + 32 * kc + 8 * lg];
-      const bf16x8 a1 = *(const bf16x8*)&s_k[(16 + lc) * kKStride + 32 * kc + 8 * lg];
+      const bf16x8 a0 = *(const bf16x8*)&sk[lc * kKStride + 32 * kc + 8 * lg];
+      const bf16x8 a1 = *(const bf16x8*)&sk[(16 + lc) * kKStride + 32 * kc + 8 * lg];
       st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[kc], st0, 0, 0, 0);
       st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qf[kc], st1, 0, 0, 0);
     }
@@ -212,16 +270,17 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
     float ps = 0.0f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float p = none ? 0.0f : __expf(sv[e] - m_new);
-      ps += p;
-      pb[e] = f2bf(p);
+      const float pe = none ? 0.0f : __expf(sv[e] - m_new);
+      ps += pe;
+      pb[e] = f2bf(pe);
     }
     m_run = m_new;
     l_run = l_run * alpha + ps;
+    const __bf16* svt = s_vt[cur];
 #pragma unroll
     for (int t = 0; t < kDTiles; ++t) {
       o[t] *= alpha;
-      const __bf16* vrow = &s_vt[(16 * t + lc) * kVStride];
+      const __bf16* vrow = &svt[(16 * t + lc) * kVStride];
       bf16x8 a;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -230,7 +289,13 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
       }
       o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[t], 0, 0, 0);
     }
-    __syncthreads();  // the next block overwrites the staged keys and values
+    // stage the next block into the other buffer (its last readers passed
+    // the previous barrier)
+    if (blk + 1 < nb) {
+      if (next_pre) put_prefix(cur ^ 1);
+      else stage_tree(blk + 1 - n_pre, cur ^ 1);
+    }
+    __syncthreads();
   }
 
   // normalise by the row's total weight (summed over the four lane groups)
@@ -264,7 +329,8 @@ extern "C" fc_status fc_tree_attention(const uint16_t* q, const uint16_t* k_tree
   const uintptr_t al = (uintptr_t)q | (uintptr_t)k_tree | (uintptr_t)v_tree | (uintptr_t)out |
                        (Pmax > 0 ? ((uintptr_t)k_cache | (uintptr_t)v_cache) : 0);
   if (al & 15) return FC_ERR_INVALID;
-  const int waves = (R + 15) / 16;
+  const int rows_waves = (R + 15) / 16;
+  const int waves = rows_waves < 4 ? 4 : rows_waves;  // at least 256 threads stage a block
   const dim3 grid((uint32_t)B * (uint32_t)H), block(waves * fc::kWave);
   (void)hipGetLastError();
   // trees of up to 128 rows (c <= 127) in workgroups of at most 8 waves,
