@@ -601,6 +601,40 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
   __syncthreads();
   const int T = T_raw;
+
+  // At most one kept continuation: the tree is the chain of its first
+  // min(len, c) tokens, every node of that store's weight alpha, so the
+  // general passes are skipped (same rows, weights and mask).
+  const int len0 = (!bad && T == 1) ? (int)cont_len[row0] : 0;
+  if (!bad && T <= 1 && len0 <= m) {
+    int s0 = 0;
+#pragma unroll
+    for (int s = FC_MAX_SOURCES - 1; s >= 0; --s)
+      if (s < S && tk_s[s] > 0) s0 = s;
+    const uint32_t a0 = alpha_of(alpha, s0);
+    const int num = 1 + (len0 < c ? len0 : c);
+    for (int r = tid; r < R; r += NT) {
+      const int64_t o = (int64_t)b * R + r;
+      node_tok[o] = r == 0 ? (int32_t)root_tok : (r < num ? (int32_t)cont_tok[row0 * m + r - 1] : 0);
+      parent[o] = (r >= 1 && r < num) ? r - 1 : -1;
+      weight[o] = r == 0 ? (len0 > 0 ? a0 : 0u) : (r < num ? a0 : 0u);
+      pos_ids[o] = r < num ? r : 0;
+    }
+    const int64_t mb = (int64_t)b * R * R;
+    int i = tid / R, j = tid - (tid / R) * R;
+    const int di = NT / R, dj = NT - (NT / R) * R;
+    for (int e = tid; e < R * R; e += NT) {
+      mask[mb + e] = (i < num && j <= i) ? 1 : 0;
+      i += di;
+      j += dj;
+      if (j >= R) {
+        j -= R;
+        ++i;
+      }
+    }
+    if (tid == 0) num_nodes[b] = num;
+    return;
+  }
   // store boundaries in registers (no LDS round trip per lookup)
   const int seg1 = s_seg[1 < S ? 1 : S], seg2 = s_seg[2 < S ? 2 : S], seg3 = s_seg[3 < S ? 3 : S];
   auto store_of = [&](int i) -> int { return (S > 1 && i >= seg1) + (S > 2 && i >= seg2) + (S > 3 && i >= seg3); };
