@@ -517,7 +517,7 @@ def test_tree_attention_matches_oracle():
     t = synth.store(1, "single")
     ctx = synth.queries(1)
     st = gpu_store(t)
-    for c in (64, 8):
+    for c in (64, 8, 200):  # 200: the 1024-thread instance (more than 128 rows)
         g = gpu_pipeline([st], ctx, P, (1,), c)
         trees = {f: g[f] for f in ("num_nodes", "mask", "pos_ids")}
         for (B, H, Hkv, seed) in ((16, 4, 4, 1), (16, 4, 2, 2), (3, 3, 1, 3)):
