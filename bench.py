@@ -31,7 +31,7 @@ import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "replay-cache": 3, "replay-control": 3,
-             "build": 3, "copy": 0, "tree-attention": 1}
+             "build": 3, "build-repos": 0, "copy": 0, "tree-attention": 1}
 # kernels each entry point launches (rocprofv3 kernel names start with these)
 ENTRY_KERNELS = {
     "fc_retrieve": ("k_search", "k_offsets", "k_gather"),
@@ -171,7 +171,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "single-GPU path only (no sharded stores); --gpus must be 1", "n_gpus": args.gpus}))
         sys.exit(2)
 
     import torch
@@ -182,6 +182,8 @@ def main():
         return run_replay(args, cache=args.workload != "replay", control=args.workload == "replay-control")
     if args.workload == "build":
         return run_build(args)
+    if args.workload == "build-repos":
+        return run_build_repos(args)
     if args.workload == "tree-attention":
         return run_tree_attention(args)
     if args.workload == "copy":
@@ -432,6 +434,59 @@ def run_build(args):
         "ms_per_step": 1e3 * out["general"]["seconds"], "higher_is_better": False, "scaling": "weak",
         "vs_baseline": None, "dtype": "u16/u32/u64 (integer)", "data": "synthetic (seeded store; no dataset)",
         "config": {"workload": "SA build, 1B general + 10M project stores"}, "roofline": None, "builds": out,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def run_build_repos(args):
+    """Per-repository stores: 64 repositories of 60..2000 files each
+    (log-uniform, 16.9M tokens in all) built by one batched call, against one
+    fc_datastore_build call per repository on the same stream."""
+    import torch
+    import paper_2502_17139_amd as fc
+    import synth
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    t, off = synth.repos(12, 64, 60, 2000)
+    n, R = len(t), len(off) - 1
+    tok = torch.from_numpy(t).to(dev)
+    sa = torch.empty(n, dtype=torch.uint32, device=dev)
+    ws = torch.empty(fc.fc_datastore_build_batched_workspace_bytes(n, R), dtype=torch.uint8, device=dev)
+    lens = np.diff(off).astype(np.int64)
+
+    def batched():
+        fc.fc_datastore_build_batched(tok, off, sa_out=sa, workspace=ws)
+
+    def per_repo():
+        for r in range(R):
+            a, b = int(off[r]), int(off[r + 1])
+            if b > a:
+                fc.fc_datastore_build(tok[a:b], sa_out=sa[a:b], workspace=ws)
+
+    def timed(fn):
+        times = []
+        for i in range(max(args.warmup, 1) + args.steps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            if i >= max(args.warmup, 1):
+                times.append(time.perf_counter() - t0)
+        return float(np.median(times))
+
+    sec_b = timed(batched)
+    sec_p = timed(per_repo)
+    line = {
+        "metric": "per-repository store build seconds (64 repositories, batched)", "value": sec_b, "unit": "s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": 1e3 * sec_b,
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "u16/u32/u64 (integer)",
+        "data": "synthetic (seeded repositories; no dataset)",
+        "config": {"workload": "SA builds of 64 repositories, 60..2000 files, 16.9M tokens", "tokens": n,
+                   "repositories": R, "smallest": int(lens.min()), "largest": int(lens.max())},
+        "roofline": None,
+        "per_repository_calls_s": sec_p, "speedup_vs_per_repository": sec_p / sec_b,
+        "tokens_per_s": n / sec_b,
     }
     print(json.dumps(line), flush=True)
 

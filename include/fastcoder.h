@@ -81,6 +81,24 @@ fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint32_t* sa_ou
                              hipStream_t stream);
 
 /*
+ * Batched construction of many small stores (per-repository stores, Section
+ * IV-A: the repository store is built per repository, offline, Section
+ * V-D).  tokens holds n_seg stores back to back, store r at
+ * [seg_off[r], seg_off[r+1]) (seg_off on the host: seg_off[0] = 0,
+ * non-decreasing, total n = seg_off[n_seg] < 2^32 - 1; empty stores
+ * allowed).  On return sa_out[seg_off[r] .. seg_off[r+1]) is exactly the
+ * suffix array fc_datastore_build gives for store r alone, with positions
+ * local to that store.  One prefix-doubling build covers every store: the
+ * store index leads each suffix's first key and a suffix ends at its own
+ * store's end.  Workspace of fc_datastore_build_batched_workspace_bytes(n,
+ * n_seg) bytes; synchronises `stream` once per doubling round, as
+ * fc_datastore_build does.
+ */
+size_t fc_datastore_build_batched_workspace_bytes(uint64_t n, int32_t n_seg);
+fc_status fc_datastore_build_batched(const uint16_t* tokens, const uint64_t* seg_off, int32_t n_seg,
+                                     uint32_t* sa_out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * First-token table of a store: bucket_out[t] (t = 0..65536) = number of
  * suffixes whose first token is below t, i.e. the suffix-array index where
  * suffixes starting with token t begin (the bucket table Manber and Myers

@@ -14,6 +14,7 @@ import ctypes
 import functools
 import os
 
+import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -31,7 +32,8 @@ STATUS = {0: "FC_OK", 1: "FC_ERR_INVALID", 2: "FC_ERR_WORKSPACE", 3: "FC_ERR_DEV
 # Names of every entry point the header declares.
 EXPORTS = (
     "fc_abi_version", "fc_status_string",
-    "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_store_prepare",
+    "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_datastore_build_batched_workspace_bytes",
+    "fc_datastore_build_batched", "fc_store_prepare",
     "fc_pair_table_entries", "fc_store_prepare_pairs", "fc_record_bytes", "fc_store_prepare_records",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
     "fc_verify_accept", "fc_targets_from_truth", "fc_cache_lds_bytes", "fc_cache_retrieve", "fc_cache_write",
@@ -78,6 +80,10 @@ def lib() -> ctypes.CDLL:
     L.fc_datastore_build_workspace_bytes.argtypes = [u64]
     L.fc_datastore_build.restype = ctypes.c_int
     L.fc_datastore_build.argtypes = [vp, u64, vp, vp, sz, vp]
+    L.fc_datastore_build_batched_workspace_bytes.restype = sz
+    L.fc_datastore_build_batched_workspace_bytes.argtypes = [u64, i32]
+    L.fc_datastore_build_batched.restype = ctypes.c_int
+    L.fc_datastore_build_batched.argtypes = [vp, vp, i32, vp, vp, sz, vp]
     L.fc_store_prepare.restype = ctypes.c_int
     L.fc_store_prepare.argtypes = [vp, vp, u64, vp, vp]
     L.fc_pair_table_entries.restype = u64
@@ -144,6 +150,10 @@ def fc_datastore_build_workspace_bytes(n: int) -> int:
     return int(lib().fc_datastore_build_workspace_bytes(n))
 
 
+def fc_datastore_build_batched_workspace_bytes(n: int, n_seg: int) -> int:
+    return int(lib().fc_datastore_build_batched_workspace_bytes(n, n_seg))
+
+
 def fc_datastore_build(tokens: torch.Tensor, sa_out: torch.Tensor | None = None,
                        workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """Suffix array (uint32[n]) of a uint16 token tensor on the GPU."""
@@ -157,6 +167,26 @@ def fc_datastore_build(tokens: torch.Tensor, sa_out: torch.Tensor | None = None,
         workspace = _empty(max(need, 1), torch.uint8, tokens.device)
     _check("fc_datastore_build", lib().fc_datastore_build(_ptr(tokens), n, _ptr(sa_out), _ptr(workspace),
                                                          workspace.numel(), _stream(stream)))
+    return sa_out
+
+
+def fc_datastore_build_batched(tokens: torch.Tensor, seg_off, sa_out: torch.Tensor | None = None,
+                               workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Suffix arrays of many stores laid back to back in `tokens` (store r
+    at [seg_off[r], seg_off[r+1])), each local to its store, in one build."""
+    if tokens.dtype != torch.uint16 or tokens.dim() != 1:
+        raise ValueError("tokens must be a 1-D uint16 tensor")
+    off = np.ascontiguousarray(seg_off, dtype=np.uint64)
+    R = len(off) - 1
+    n = tokens.numel()
+    if sa_out is None:
+        sa_out = _empty(n, torch.uint32, tokens.device)
+    need = fc_datastore_build_batched_workspace_bytes(n, R) if R >= 1 else 0
+    if workspace is None:
+        workspace = _empty(max(need, 1), torch.uint8, tokens.device)
+    _check("fc_datastore_build_batched", lib().fc_datastore_build_batched(
+        _ptr(tokens), ctypes.c_void_p(off.ctypes.data), R, _ptr(sa_out), _ptr(workspace), workspace.numel(),
+        _stream(stream)))
     return sa_out
 
 

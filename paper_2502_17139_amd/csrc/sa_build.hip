@@ -83,6 +83,54 @@ __global__ void __launch_bounds__(256) k_pair_keys(const uint32_t* __restrict__ 
   keys[r] = (hi << sb) | lo;
 }
 
+// Batched build: position i belongs to the segment r with off[r] <= i <
+// off[r+1] (the last r with off[r] <= i, so empty segments are skipped).
+__device__ __forceinline__ uint32_t segment_of(const uint64_t* __restrict__ off, uint32_t R, uint64_t i) {
+  uint32_t lo = 0, hi = R - 1;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Round 0 of a batched build: key = (segment, first two tokens as token+1,
+// 0 past the segment's end), so suffixes of different segments never share
+// a group and every suffix ends at its own segment's end.
+__global__ void __launch_bounds__(256) k_init_keys_seg(const uint16_t* __restrict__ tok, uint32_t n,
+                                                         const uint64_t* __restrict__ off, uint32_t R,
+                                                         uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                                         uint32_t* __restrict__ end_of) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t r = segment_of(off, R, i);
+  const uint32_t end = (uint32_t)off[r + 1];
+  const uint64_t a = (uint64_t)tok[i] + 1;
+  const uint64_t b = (i + 1 < end) ? (uint64_t)tok[i + 1] + 1 : 0;
+  keys[i] = ((uint64_t)r << 34) | (a << 17) | b;
+  vals[i] = i;
+  end_of[i] = end;
+}
+
+__global__ void __launch_bounds__(256) k_pair_keys_seg(const uint32_t* __restrict__ vals, uint32_t U,
+                                                         const uint32_t* __restrict__ rank,
+                                                         const uint32_t* __restrict__ end_of, uint64_t h,
+                                                         uint32_t sb, uint64_t* __restrict__ keys) {
+  const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= U) return;
+  const uint32_t i = vals[r];
+  const uint64_t hi = rank[i];
+  const uint64_t lo = ((uint64_t)i + h < end_of[i]) ? (uint64_t)rank[i + h] + 1 : 0;
+  keys[r] = (hi << sb) | lo;
+}
+
+// Segment-major suffix array -> positions local to each segment.
+__global__ void __launch_bounds__(256) k_localize_sa(uint32_t* __restrict__ sa, uint32_t n,
+                                                       const uint64_t* __restrict__ off, uint32_t R) {
+  const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r < n) sa[r] -= (uint32_t)off[segment_of(off, R, r)];
+}
+
 __global__ void __launch_bounds__(256) k_scatter_sa(const uint32_t* __restrict__ rank, uint32_t n,
                                                       uint32_t* __restrict__ sa) {
   uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -460,9 +508,11 @@ struct BuildWs {
   uint32_t* offsets;
   uint32_t* tickets;
   uint32_t* misc;  // [0] error flag, [1] next U, [2..9] trivial digit flags
+  uint32_t* end_of;   // batched build: end of each position's segment
+  uint64_t* seg_off;  // batched build: segment offsets (device copy)
 };
 
-size_t carve_build(void* p, uint64_t n, BuildWs* w) {
+size_t carve_build(void* p, uint64_t n, BuildWs* w, uint32_t n_seg = 0) {
   fc::Carver c(p);
   const uint64_t tiles = (n + kSortTile - 1) / kSortTile;
   const uint64_t seg_tiles = (n + kSegTile - 1) / kSegTile;
@@ -480,6 +530,8 @@ size_t carve_build(void* p, uint64_t n, BuildWs* w) {
   tmp.offsets = c.take<uint32_t>(kMaxDigits * kRadix);
   tmp.tickets = c.take<uint32_t>(kMaxPasses);
   tmp.misc = c.take<uint32_t>(16);
+  tmp.end_of = n_seg ? c.take<uint32_t>(n) : nullptr;
+  tmp.seg_off = n_seg ? c.take<uint64_t>((size_t)n_seg + 1) : nullptr;
   if (w) *w = tmp;
   return c.used + 256;
 }
@@ -529,19 +581,11 @@ fc_status radix_sort(BuildWs& w, int src, uint32_t U, int key_bits, SortState& s
   return FC_OK;
 }
 
-}  // namespace
-
-extern "C" size_t fc_datastore_build_workspace_bytes(uint64_t n) { return carve_build(nullptr, n, nullptr); }
-
-extern "C" fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint32_t* sa_out, void* ws,
-                                        size_t ws_bytes, hipStream_t stream) {
-  if (n >= 0xFFFFFFFFull) return FC_ERR_INVALID;
-  if (n == 0) return FC_OK;
-  if (!tokens || !sa_out) return FC_ERR_INVALID;
-  if (!ws || ws_bytes < fc_datastore_build_workspace_bytes(n)) return FC_ERR_WORKSPACE;
-  (void)hipGetLastError();
-  BuildWs w;
-  carve_build(ws, n, &w);
+// Prefix doubling over all n suffixes (n_seg = 0) or over the suffixes of
+// n_seg segments at once, each ending at its segment's end (n_seg >= 1,
+// offsets already in w.seg_off).
+fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& w, uint32_t* sa_out,
+                   hipStream_t stream) {
   const uint32_t N = (uint32_t)n;
   const uint64_t tiles = (n + kSortTile - 1) / kSortTile;
   FC_CHECK_HIP(hipMemsetAsync(w.status, 0, sizeof(uint64_t) * tiles * kRadix, stream));
@@ -550,21 +594,36 @@ extern "C" fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint
 
   const uint32_t sb = (uint32_t)bit_length(n);  // every rank + 1 <= n fits in sb bits
   SortState st;
-  hipLaunchKernelGGL(k_init_keys, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, tokens, N, w.keys[0], w.vals[0]);
+  uint64_t h;
+  int key0_bits;
+  if (n_seg == 0) {
+    hipLaunchKernelGGL(k_init_keys, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, tokens, N, w.keys[0],
+                       w.vals[0]);
+    h = 3;
+    key0_bits = 51;
+  } else {
+    hipLaunchKernelGGL(k_init_keys_seg, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, tokens, N, w.seg_off, n_seg,
+                       w.keys[0], w.vals[0], w.end_of);
+    h = 2;
+    key0_bits = 34 + bit_length(n_seg - 1);
+  }
   FC_CHECK_LAUNCH();
   uint32_t U = N;
   int vin = 0;  // buffer holding the suffixes to sort
-  uint64_t h = 3;
   for (int round = 0;; ++round) {
     if (round >= kMaxRounds) return FC_ERR_DEVICE;
     if (round > 0) {
-      hipLaunchKernelGGL(k_pair_keys, dim3(fc::div_up(U, 256)), dim3(256), 0, stream, w.vals[vin], U, w.rank, N,
-                         h, sb, w.keys[vin]);
+      if (n_seg == 0)
+        hipLaunchKernelGGL(k_pair_keys, dim3(fc::div_up(U, 256)), dim3(256), 0, stream, w.vals[vin], U, w.rank, N,
+                           h, sb, w.keys[vin]);
+      else
+        hipLaunchKernelGGL(k_pair_keys_seg, dim3(fc::div_up(U, 256)), dim3(256), 0, stream, w.vals[vin], U, w.rank,
+                           w.end_of, h, sb, w.keys[vin]);
       FC_CHECK_LAUNCH();
       h *= 2;
     }
     int res = vin;
-    fc_status s = radix_sort(w, vin, U, round == 0 ? 51 : (int)(2 * sb), st, stream, &res);
+    fc_status s = radix_sort(w, vin, U, round == 0 ? key0_bits : (int)(2 * sb), st, stream, &res);
     if (s != FC_OK) return s;
     const uint32_t seg_tiles = fc::div_up(U, kSegTile);
     hipLaunchKernelGGL(k_seg_partials, dim3(seg_tiles), dim3(kSegThreads), 0, stream, w.keys[res], U, sb,
@@ -586,7 +645,50 @@ extern "C" fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint
   }
   hipLaunchKernelGGL(k_scatter_sa, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, w.rank, N, sa_out);
   FC_CHECK_LAUNCH();
+  if (n_seg > 0) {
+    hipLaunchKernelGGL(k_localize_sa, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, sa_out, N, w.seg_off, n_seg);
+    FC_CHECK_LAUNCH();
+  }
   return FC_OK;
+}
+
+}  // namespace
+
+extern "C" size_t fc_datastore_build_workspace_bytes(uint64_t n) { return carve_build(nullptr, n, nullptr); }
+
+extern "C" fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint32_t* sa_out, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+  if (n >= 0xFFFFFFFFull) return FC_ERR_INVALID;
+  if (n == 0) return FC_OK;
+  if (!tokens || !sa_out) return FC_ERR_INVALID;
+  if (!ws || ws_bytes < fc_datastore_build_workspace_bytes(n)) return FC_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  BuildWs w;
+  carve_build(ws, n, &w);
+  return build_sa(tokens, n, 0, w, sa_out, stream);
+}
+
+extern "C" size_t fc_datastore_build_batched_workspace_bytes(uint64_t n, int32_t n_seg) {
+  return n_seg >= 1 ? carve_build(nullptr, n, nullptr, (uint32_t)n_seg) : 0;
+}
+
+extern "C" fc_status fc_datastore_build_batched(const uint16_t* tokens, const uint64_t* seg_off, int32_t n_seg,
+                                                uint32_t* sa_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (n_seg < 1 || !seg_off) return FC_ERR_INVALID;
+  if (seg_off[0] != 0) return FC_ERR_INVALID;
+  for (int32_t r = 0; r < n_seg; ++r)
+    if (seg_off[r + 1] < seg_off[r]) return FC_ERR_INVALID;
+  const uint64_t n = seg_off[n_seg];
+  if (n >= 0xFFFFFFFFull || 34 + bit_length((uint64_t)n_seg - 1) > 64) return FC_ERR_INVALID;
+  if (n == 0) return FC_OK;
+  if (!tokens || !sa_out) return FC_ERR_INVALID;
+  if (!ws || ws_bytes < fc_datastore_build_batched_workspace_bytes(n, n_seg)) return FC_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  BuildWs w;
+  carve_build(ws, n, &w, (uint32_t)n_seg);
+  FC_CHECK_HIP(hipMemcpyAsync(w.seg_off, seg_off, sizeof(uint64_t) * ((size_t)n_seg + 1), hipMemcpyHostToDevice,
+                              stream));
+  return build_sa(tokens, n, (uint32_t)n_seg, w, sa_out, stream);
 }
 
 extern "C" fc_status fc_store_prepare(const uint16_t* tokens, const uint32_t* sa, uint64_t n, uint32_t* bucket_out,

@@ -32,6 +32,7 @@ CTX_LEN = 16
 ROLE_QUERY = 10
 ROLE_SHUFFLE = 11
 ROLE_FRESH = 12
+ROLE_REPOS = 13
 
 # Workload configurations.  A store is (seed, n_templates, zipf_s, n_files).
 CONFIGS = {
@@ -228,6 +229,23 @@ def truth(n_seq: int | None = None, length: int | None = None) -> np.ndarray:
     _, seed, nt, s = t["pool"]
     flat = pool(seed, nt, s).files(t["seed"], 0, n_seq, length, sep=False)
     return flat.reshape(n_seq, length)
+
+
+def repos(seed: int, n_repos: int, min_files: int, max_files: int, n_templates: int = 2000,
+          zipf_s: float = 1.2) -> tuple:
+    """Many per-repository stores laid back to back: repository r holds a
+    log-uniform number of files in [min_files, max_files] (FILE_LEN tokens
+    each, joined by 0 tokens), drawn from one template pool shared by every
+    repository (common library code), each with its own file seed.  Returns
+    (tokens, offsets) with repository r at tokens[offsets[r]:offsets[r+1]]."""
+    u = uniform(seed, ROLE_REPOS, 0, n_repos, 0, 999_999).astype(np.float64) / 1e6
+    lo, hi = np.log(min_files), np.log(max_files + 1)
+    n_files = np.minimum(np.exp(lo + u * (hi - lo)).astype(np.int64), max_files)
+    p = pool(seed, n_templates, zipf_s)
+    parts = [p.files(seed * 1_000_003 + r, 0, int(f), FILE_LEN, sep=True) for r, f in enumerate(n_files)]
+    off = np.zeros(n_repos + 1, np.uint64)
+    off[1:] = np.cumsum([len(x) for x in parts])
+    return (np.concatenate(parts) if parts else np.zeros(0, np.uint16)), off
 
 
 def random_text(seed: int, n: int, vocab: int, sep_prob: float = 0.0) -> np.ndarray:

@@ -210,3 +210,17 @@ def test_cache_entry_points_reject(L):
     assert L.fc_cache_write(one, 0, 2, one, 1, one, one, one, one, one, one, None) == 1
     assert L.fc_cache_write(None, 100, 2, one, 1, one, one, one, one, one, one, None) == 1
     assert L.fc_cache_write(one, 100, 2, one, 0, one, one, one, one, one, one, None) == 0
+
+
+def test_batched_build_rejects(L):
+    one = ctypes.c_void_p(8)
+    off = lambda *v: (ctypes.c_uint64 * len(v))(*v)  # noqa: E731
+    assert L.fc_datastore_build_batched(one, off(0, 5), 0, one, one, 1 << 30, None) == 1   # no segment
+    assert L.fc_datastore_build_batched(one, None, 1, one, one, 1 << 30, None) == 1
+    assert L.fc_datastore_build_batched(one, off(1, 5), 1, one, one, 1 << 30, None) == 1   # must start at 0
+    assert L.fc_datastore_build_batched(one, off(0, 5, 3), 2, one, one, 1 << 30, None) == 1  # decreasing
+    assert L.fc_datastore_build_batched(one, off(0, 1 << 32), 1, one, one, 1 << 30, None) == 1
+    assert L.fc_datastore_build_batched(one, off(0, 5), 1, one, one, 8, None) == 2  # workspace too small
+    assert L.fc_datastore_build_batched(None, off(0, 0, 0), 2, None, None, 0, None) == 0  # nothing to build
+    assert (L.fc_datastore_build_batched_workspace_bytes(1000, 3) >
+            L.fc_datastore_build_workspace_bytes(1000))

@@ -100,6 +100,67 @@ def test_sa_two_store_workload():
     assert oracle.check_sa(g, sa) == (0, 0)
 
 
+def _batched_case(tok: np.ndarray, off: np.ndarray, full: bool = True):
+    """Batched build: store r's slice of the output is the suffix array of
+    store r alone (oracle comparison sort, or the linear-time checker)."""
+    g = host(fc.fc_datastore_build_batched(dev(tok), off))
+    torch.cuda.synchronize()
+    for r in range(len(off) - 1):
+        a, b = int(off[r]), int(off[r + 1])
+        if full:
+            assert (g[a:b] == oracle.suffix_array(tok[a:b])).all(), (r, a, b)
+        else:
+            assert oracle.check_sa(tok[a:b], g[a:b]) == (0, 0), (r, a, b)
+
+
+def _concat(parts):
+    off = np.zeros(len(parts) + 1, np.uint64)
+    off[1:] = np.cumsum([len(x) for x in parts])
+    return np.concatenate([np.asarray(x, np.uint16) for x in parts]), off
+
+
+@pytest.mark.parametrize("vocab", [2, 4, 32256])
+def test_sa_batched_ragged_stores(vocab):
+    lens = [0, 1, 2, 3, 0, 7, 64, 4095, 4096, 4097, 0, 9000, 5]
+    say(f"sa batched vocab={vocab} lens={lens}")
+    _batched_case(*_concat([synth.random_text(5000 * vocab + i, n, vocab, sep_prob=0.03 if i % 2 else 0.0)
+                            for i, n in enumerate(lens)]))
+
+
+def test_sa_batched_stores_do_not_see_each_other():
+    # equal stores back to back: a suffix that ran on into the next store
+    # would sort differently from the same suffix of a store built alone
+    for t in (np.full(1000, 7, np.uint16), synth.random_text(3, 2500, 2), np.zeros(300, np.uint16),
+              (np.arange(3000) % 3).astype(np.uint16)):
+        say(f"sa batched repeated n={len(t)}")
+        _batched_case(*_concat([t] * 5))
+        _batched_case(*_concat([t, t[: len(t) // 2], t, t[:1]]))
+
+
+def test_sa_batched_single_store_equals_plain_build():
+    t = synth.random_text(77, 20011, 4, sep_prob=0.01)
+    g = host(fc.fc_datastore_build_batched(dev(t), np.array([0, len(t)], np.uint64)))
+    torch.cuda.synchronize()
+    assert (g == host(fc.fc_datastore_build(dev(t)))).all()
+    assert (g == oracle.suffix_array(t)).all()
+
+
+def test_sa_batched_many_tiny_stores():
+    lens = synth.uniform(9, 30, 0, 3000, 0, 50)
+    say(f"sa batched {len(lens)} tiny stores")
+    _batched_case(*_concat([synth.random_text(90_000 + i, int(n), 4) for i, n in enumerate(lens)]))
+    _batched_case(np.zeros(0, np.uint16), np.zeros(4, np.uint64))   # only empty stores
+
+
+def test_sa_batched_repository_set():
+    tok, off = synth.repos(11, 48, 2, 400)
+    say(f"sa batched repositories n={len(tok)}")
+    _batched_case(tok, off)
+    tok, off = synth.repos(12, 64, 60, 2000)   # the benchmark's repository set
+    say(f"sa batched benchmark repositories n={len(tok)}")
+    _batched_case(tok, off, full=False)
+
+
 def test_bucket_table():
     for t in (synth.random_text(5, 5000, 300, 0.02), synth.store(1, "single"), np.zeros(0, np.uint16)):
         st = gpu_store(t) if len(t) else None
