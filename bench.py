@@ -31,7 +31,7 @@ import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "replay-cache": 3, "replay-control": 3,
-             "build": 3, "build-repos": 0, "copy": 0, "tree-attention": 1}
+             "build": 3, "build-repos": 0, "extend": 3, "copy": 0, "tree-attention": 1}
 # kernels each entry point launches (rocprofv3 kernel names start with these)
 ENTRY_KERNELS = {
     "fc_retrieve": ("k_search", "k_offsets", "k_gather"),
@@ -184,6 +184,8 @@ def main():
         return run_build(args)
     if args.workload == "build-repos":
         return run_build_repos(args)
+    if args.workload == "extend":
+        return run_extend(args)
     if args.workload == "tree-attention":
         return run_tree_attention(args)
     if args.workload == "copy":
@@ -487,6 +489,68 @@ def run_build_repos(args):
         "roofline": None,
         "per_repository_calls_s": sec_p, "speedup_vs_per_repository": sec_p / sec_b,
         "tokens_per_s": n / sec_b,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def run_extend(args):
+    """New files in front of an existing store (fc_datastore_extend) against
+    a full rebuild of the grown store: 1 and 200 new files on the 10M-token
+    project store, 2,000 new files (1M tokens) on the 1B-token general store.
+    The new files are the store's next files (same template pool, later file
+    indexes), so they share its code; each case is timed with the inverse
+    computed inside the call and with a kept inverse."""
+    import torch
+    import paper_2502_17139_amd as fc
+    import synth
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    def timed(fn):
+        times = []
+        for i in range(max(args.warmup, 1) + args.steps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            if i >= max(args.warmup, 1):
+                times.append(time.perf_counter() - t0)
+        return float(np.median(times))
+
+    spec = {r: (seed, nt, zs, nf) for r, seed, nt, zs, nf in synth.CONFIGS[3]["stores"]}
+    cases = []
+    for role, files in (("project", 1), ("project", 200), ("general", 2000)):
+        seed, nt, zs, nf = spec[role]
+        old = synth.store(3, role)
+        new = synth.pool(seed, nt, zs).files(seed, nf, files, synth.FILE_LEN, sep=True)
+        t = np.concatenate([new, np.zeros(1, np.uint16), old])
+        n, n_new = len(t), len(new) + 1
+        tt = torch.from_numpy(t).to(dev)
+        old_sa = fc.fc_datastore_build(tt[n_new:])
+        old_isa = torch.empty(n - n_new, dtype=torch.uint32, device=dev)
+        fc.fc_datastore_extend(tt[n_new:], 0, old_sa, isa_out=old_isa)   # the old store's inverse
+        sa = torch.empty(n, dtype=torch.uint32, device=dev)
+        isa = torch.empty(n, dtype=torch.uint32, device=dev)
+        ws = torch.empty(max(fc.fc_datastore_extend_workspace_bytes(n, n_new),
+                             fc.fc_datastore_build_workspace_bytes(n)), dtype=torch.uint8, device=dev)
+        sec_e = timed(lambda: fc.fc_datastore_extend(tt, n_new, old_sa, sa_out=sa, workspace=ws))
+        sec_k = timed(lambda: fc.fc_datastore_extend(tt, n_new, old_sa, old_isa=old_isa, sa_out=sa, isa_out=isa,
+                                                     workspace=ws))
+        sec_b = timed(lambda: fc.fc_datastore_build(tt, sa_out=sa, workspace=ws))
+        cases.append({"store": role, "old_tokens": n - n_new, "new_files": files, "new_tokens": n_new,
+                      "extend_s": sec_e, "extend_kept_inverse_s": sec_k, "rebuild_s": sec_b,
+                      "speedup": sec_b / sec_e, "speedup_kept_inverse": sec_b / sec_k})
+        del tt, old_sa, old_isa, sa, isa, ws
+        torch.cuda.empty_cache()
+    big = cases[-1]
+    line = {
+        "metric": "store extension seconds (2,000 new files on the 1B-token store)", "value": big["extend_s"],
+        "unit": "s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": 1e3 * big["extend_s"],
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "u16/u32/u64 (integer)",
+        "data": "synthetic (seeded stores and their next files; no dataset)",
+        "config": {"workload": "SA extension: new files in front of the 10M project and 1B general stores"},
+        "roofline": None, "cases": cases,
     }
     print(json.dumps(line), flush=True)
 

@@ -99,6 +99,42 @@ fc_status fc_datastore_build_batched(const uint16_t* tokens, const uint64_t* seg
                                      uint32_t* sa_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Extension of a store by new files without a full rebuild (a repository
+ * store grows as its files are written, Section IV-A; the suffix array is
+ * the Section III-A index).  The new files go in FRONT of the old store:
+ * tokens[n] = new[n_new] . old[n - n_new], where new already ends with the
+ * 0 token that joins it to the old store's first file.  Every suffix of the
+ * old store is then a suffix of the new text, so its order is kept and
+ * only the n_new new suffixes are sorted: each is first placed among the
+ * old suffixes by doubling over the old array and its inverse, then the
+ * new suffixes are ordered among themselves by prefix doubling, and the two
+ * lists are merged.
+ *
+ * old_sa [n - n_new]  : suffix array of tokens[n_new .. n) alone (as
+ *                       fc_datastore_build gives it; positions local to the
+ *                       old store).  Read only.
+ * old_isa [n - n_new] : optional (NULL: computed in the workspace, one
+ *                       random-write pass over the old store): its inverse,
+ *                       old_isa[old_sa[j]] = j.  A store that keeps its
+ *                       inverse (isa_out of its last extension) skips that
+ *                       pass.
+ * sa_out [n]          : receives exactly what fc_datastore_build(tokens, n)
+ *                       would.
+ * isa_out [n]         : optional: receives the inverse of sa_out.
+ * No output may overlap an input.  Workspace of
+ * fc_datastore_extend_workspace_bytes(n, n_new, old_isa != NULL) bytes
+ * (without old_isa it holds the inverse: 4 bytes per old token).
+ * n_new == 0 copies old_sa (and inverts it into isa_out); n == n_new is a
+ * plain build.  Requires n < 2^32 - 1 and n_new <= n.  Synchronises
+ * `stream` once per doubling round.  If old_sa (or old_isa) is not the old
+ * store's array the result is unspecified (no access leaves the buffers).
+ */
+size_t fc_datastore_extend_workspace_bytes(uint64_t n, uint64_t n_new, int32_t isa_given);
+fc_status fc_datastore_extend(const uint16_t* tokens, uint64_t n, uint64_t n_new, const uint32_t* old_sa,
+                              const uint32_t* old_isa, uint32_t* sa_out, uint32_t* isa_out, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
+
+/*
  * First-token table of a store: bucket_out[t] (t = 0..65536) = number of
  * suffixes whose first token is below t, i.e. the suffix-array index where
  * suffixes starting with token t begin (the bucket table Manber and Myers

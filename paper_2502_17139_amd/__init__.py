@@ -33,7 +33,7 @@ STATUS = {0: "FC_OK", 1: "FC_ERR_INVALID", 2: "FC_ERR_WORKSPACE", 3: "FC_ERR_DEV
 EXPORTS = (
     "fc_abi_version", "fc_status_string",
     "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_datastore_build_batched_workspace_bytes",
-    "fc_datastore_build_batched", "fc_store_prepare",
+    "fc_datastore_build_batched", "fc_datastore_extend_workspace_bytes", "fc_datastore_extend", "fc_store_prepare",
     "fc_pair_table_entries", "fc_store_prepare_pairs", "fc_record_bytes", "fc_store_prepare_records",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
     "fc_verify_accept", "fc_targets_from_truth", "fc_cache_lds_bytes", "fc_cache_retrieve", "fc_cache_write",
@@ -84,6 +84,10 @@ def lib() -> ctypes.CDLL:
     L.fc_datastore_build_batched_workspace_bytes.argtypes = [u64, i32]
     L.fc_datastore_build_batched.restype = ctypes.c_int
     L.fc_datastore_build_batched.argtypes = [vp, vp, i32, vp, vp, sz, vp]
+    L.fc_datastore_extend_workspace_bytes.restype = sz
+    L.fc_datastore_extend_workspace_bytes.argtypes = [u64, u64, i32]
+    L.fc_datastore_extend.restype = ctypes.c_int
+    L.fc_datastore_extend.argtypes = [vp, u64, u64, vp, vp, vp, vp, vp, sz, vp]
     L.fc_store_prepare.restype = ctypes.c_int
     L.fc_store_prepare.argtypes = [vp, vp, u64, vp, vp]
     L.fc_pair_table_entries.restype = u64
@@ -187,6 +191,33 @@ def fc_datastore_build_batched(tokens: torch.Tensor, seg_off, sa_out: torch.Tens
     _check("fc_datastore_build_batched", lib().fc_datastore_build_batched(
         _ptr(tokens), ctypes.c_void_p(off.ctypes.data), R, _ptr(sa_out), _ptr(workspace), workspace.numel(),
         _stream(stream)))
+    return sa_out
+
+
+def fc_datastore_extend_workspace_bytes(n: int, n_new: int, isa_given: bool = False) -> int:
+    return int(lib().fc_datastore_extend_workspace_bytes(n, n_new, 1 if isa_given else 0))
+
+
+def fc_datastore_extend(tokens: torch.Tensor, n_new: int, old_sa: torch.Tensor, old_isa: torch.Tensor | None = None,
+                        sa_out: torch.Tensor | None = None, isa_out: torch.Tensor | None = None,
+                        workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Suffix array of tokens = new (n_new tokens, ending with the joining 0)
+    followed by an old store whose suffix array is old_sa (and, optionally,
+    whose inverse is old_isa); isa_out, if given, receives the new inverse."""
+    if tokens.dtype != torch.uint16 or tokens.dim() != 1:
+        raise ValueError("tokens must be a 1-D uint16 tensor")
+    n = tokens.numel()
+    for name, t in (("old_sa", old_sa), ("old_isa", old_isa)):
+        if t is not None and (t.dtype != torch.uint32 or t.numel() != n - n_new):
+            raise ValueError(f"{name} must be a uint32 tensor of n - n_new entries")
+    if sa_out is None:
+        sa_out = _empty(n, torch.uint32, tokens.device)
+    if workspace is None:
+        need = fc_datastore_extend_workspace_bytes(n, n_new, old_isa is not None)
+        workspace = _empty(max(need, 1), torch.uint8, tokens.device)
+    _check("fc_datastore_extend", lib().fc_datastore_extend(
+        _ptr(tokens), n, n_new, _ptr(old_sa), _ptr(old_isa), _ptr(sa_out), _ptr(isa_out), _ptr(workspace),
+        workspace.numel(), _stream(stream)))
     return sa_out
 
 

@@ -140,6 +140,283 @@ __global__ void __launch_bounds__(256) k_scatter_sa(const uint32_t* __restrict__
   }
 }
 
+// ------------------------------------------------------------ extension --
+//
+// fc_datastore_extend: text = X . T, X the o new tokens in front of the old
+// store T (n_old tokens) whose suffix array is known.  Suffixes of T are
+// suffixes of the new text, so their order is kept.  For each new suffix p
+// the build finds ins(p) = the number of old suffixes smaller than it, then
+// orders the new suffixes among themselves, and merges.
+
+// inverse of the old suffix array
+__global__ void __launch_bounds__(256) k_isa(const uint32_t* __restrict__ sa, uint32_t n_old,
+                                               uint32_t* __restrict__ isa) {
+  const uint32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j < n_old) {
+    const uint32_t q = sa[j];
+    if (q < n_old) isa[q] = j;  // a malformed array cannot write out of bounds
+  }
+}
+
+// ins by doubling over h = 64, 128, ...: [lo, hi) is the suffix-array range
+// of the old suffixes whose first h tokens equal those of new suffix p.
+// Inside such a range the old suffixes are ordered by what follows their
+// first h tokens, i.e. by isa[q + h] (0 for an empty rest, isa + 1 else),
+// so the next range is found by two binary searches against p + h's range
+// (or, once p + h lies in T, against the single old suffix there).  An
+// empty range is final: its start is ins(p).
+
+// First ranges, for h = kExtFirst tokens at once: a binary search of the
+// new suffix's first kExtFirst tokens over the old array, comparing token by
+// token from the common prefix both bounds share (Manber and Myers' search).
+// Most new suffixes of real text are placed here; only those sharing more
+// than kExtFirst tokens with an old suffix go on to the doubling rounds.
+constexpr uint32_t kExtFirst = 64;
+
+// sign of (new suffix p, at most kExtFirst tokens) - (old suffix q), from
+// offset d on; *lcp receives the common length, capped at kExtFirst
+__device__ __forceinline__ int ext_cmp(const uint16_t* __restrict__ tok, uint32_t o, uint64_t n, uint32_t n_old,
+                                       uint32_t p, uint32_t q, uint32_t d, uint32_t* lcp) {
+  for (; d < kExtFirst; ++d) {
+    if ((uint64_t)q + d >= n_old) { *lcp = d; return 1; }   // the old suffix ended first
+    if ((uint64_t)p + d >= n) { *lcp = d; return -1; }
+    const uint32_t a = tok[p + d], b = tok[(uint64_t)o + q + d];
+    if (a != b) { *lcp = d; return a > b ? 1 : -1; }
+  }
+  *lcp = kExtFirst;
+  return 0;
+}
+
+__global__ void __launch_bounds__(256) k_ext_init(const uint16_t* __restrict__ tok, uint32_t o, uint64_t n,
+                                                    const uint32_t* __restrict__ sa, uint32_t n_old,
+                                                    uint32_t* __restrict__ lo0, uint32_t* __restrict__ hi0,
+                                                    uint32_t* __restrict__ lo1, uint32_t* __restrict__ hi1,
+                                                    uint32_t* __restrict__ active, uint32_t* __restrict__ count) {
+  const uint32_t p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= o) return;
+  auto old_at = [&](uint32_t r) -> uint32_t {
+    const uint32_t q = sa[r];
+    return q < n_old ? q : n_old;  // a malformed array reads as an ended suffix
+  };
+  // lower end: first r whose suffix is >= the new suffix's first tokens
+  uint32_t a = 0, b = n_old, la = 0, lb = 0;
+  while (a < b) {
+    const uint32_t mid = (a + b) >> 1;
+    uint32_t l;
+    const int c = ext_cmp(tok, o, n, n_old, p, old_at(mid), la < lb ? la : lb, &l);
+    if (c > 0) { a = mid + 1; la = l; } else { b = mid; lb = l; }
+  }
+  // upper end: first r whose suffix is > them (the search resumes from a,
+  // whose left neighbour shares la tokens)
+  uint32_t e = a, f = n_old, le = la, lf = 0;
+  while (e < f) {
+    const uint32_t mid = (e + f) >> 1;
+    uint32_t l;
+    const int c = ext_cmp(tok, o, n, n_old, p, old_at(mid), le < lf ? le : lf, &l);
+    if (c >= 0) { e = mid + 1; le = l; } else { f = mid; lf = l; }
+  }
+  lo0[p] = lo1[p] = a;
+  hi0[p] = hi1[p] = e;
+  if (a < e) active[atomicAdd(count, 1u)] = p;
+}
+
+__device__ __forceinline__ uint32_t ext_key(const uint32_t* __restrict__ sa, const uint32_t* __restrict__ isa,
+                                            uint32_t n_old, uint64_t h, uint32_t r) {
+  const uint64_t q = (uint64_t)sa[r] + h;
+  return q < n_old ? isa[q] + 1 : 0u;
+}
+
+__global__ void __launch_bounds__(256) k_ext_round(uint32_t o, uint64_t n, uint32_t n_old,
+                                                     const uint32_t* __restrict__ sa,
+                                                     const uint32_t* __restrict__ isa, uint64_t h,
+                                                     const uint32_t* __restrict__ clo,
+                                                     const uint32_t* __restrict__ chi, uint32_t* __restrict__ nlo,
+                                                     uint32_t* __restrict__ nhi, const uint32_t* __restrict__ act,
+                                                     const uint32_t* __restrict__ n_act,
+                                                     uint32_t* __restrict__ act_out,
+                                                     uint32_t* __restrict__ done_out,
+                                                     uint32_t* __restrict__ counts) {
+  const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= *n_act) return;
+  const uint32_t p = act[t];
+  const uint32_t lo = clo[p], hi = chi[p];
+  const uint64_t z = (uint64_t)p + h;
+  uint32_t a, b;
+  if (z < o) {
+    a = clo[z] + 1;
+    b = chi[z] + 1;
+  } else if (z < n) {
+    a = b = isa[z - o] + 1;
+  } else {
+    a = b = 0;
+  }
+  uint32_t x = lo, y = hi;
+  while (x < y) {
+    const uint32_t mid = (x + y) >> 1;
+    if (ext_key(sa, isa, n_old, h, mid) < a) x = mid + 1; else y = mid;
+  }
+  const uint32_t nl = x;
+  if (a != b) {
+    y = hi;
+    while (x < y) {
+      const uint32_t mid = (x + y) >> 1;
+      if (ext_key(sa, isa, n_old, h, mid) < b) x = mid + 1; else y = mid;
+    }
+  }
+  nlo[p] = nl;
+  nhi[p] = x;
+  if (nl < x) act_out[atomicAdd(&counts[0], 1u)] = p;
+  else done_out[atomicAdd(&counts[1], 1u)] = p;
+}
+
+// a range that became final this round is copied into the other buffer
+// (no other work of the next round touches it)
+__global__ void __launch_bounds__(256) k_ext_fix(const uint32_t* __restrict__ done,
+                                                   const uint32_t* __restrict__ n_done,
+                                                   const uint32_t* __restrict__ nlo, uint32_t* __restrict__ olo,
+                                                   uint32_t* __restrict__ ohi) {
+  const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= *n_done) return;
+  const uint32_t p = done[t];
+  olo[p] = ohi[p] = nlo[p];
+}
+
+// Ordering the new suffixes: prefix doubling as in the plain build, over the
+// o new positions only, with ins(p) as the most significant field of round
+// 0's key.  A new suffix's group label is ins(p) + rank[p] and an old
+// suffix's is its final index isa + (new suffixes with ins <= isa): both are
+// positions in the final array's order, so the rank of whatever follows the
+// first h tokens can be either kind.
+__global__ void __launch_bounds__(256) k_init_keys_ext(const uint16_t* __restrict__ tok, uint32_t o, uint64_t n,
+                                                         const uint32_t* __restrict__ ins, int two,
+                                                         uint64_t* __restrict__ keys, uint32_t* __restrict__ vals) {
+  const uint32_t p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= o) return;
+  const uint64_t a = (uint64_t)tok[p] + 1;
+  const uint64_t b = ((uint64_t)p + 1 < n) ? (uint64_t)tok[p + 1] + 1 : 0;
+  keys[p] = two ? (((uint64_t)ins[p] << 34) | (a << 17) | b) : (((uint64_t)ins[p] << 17) | a);
+  vals[p] = p;
+}
+
+__global__ void __launch_bounds__(256) k_ins_sorted(const uint64_t* __restrict__ keys, uint32_t o, int shift,
+                                                      uint32_t* __restrict__ out) {
+  const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r < o) out[r] = (uint32_t)(keys[r] >> shift);
+}
+
+// number of s[0..len) that are <= j (s non-decreasing)
+__device__ __forceinline__ uint32_t count_le(const uint32_t* __restrict__ s, uint32_t len, uint32_t j) {
+  uint32_t a = 0, b = len;
+  while (a < b) {
+    const uint32_t mid = (a + b) >> 1;
+    if (s[mid] <= j) a = mid + 1; else b = mid;
+  }
+  return a;
+}
+
+__global__ void __launch_bounds__(256) k_pair_keys_ext(const uint32_t* __restrict__ vals, uint32_t U,
+                                                         const uint32_t* __restrict__ rank,
+                                                         const uint32_t* __restrict__ ins,
+                                                         const uint32_t* __restrict__ isa,
+                                                         const uint32_t* __restrict__ ins_sorted, uint32_t o,
+                                                         uint64_t n, uint64_t h, uint32_t sb,
+                                                         uint64_t* __restrict__ keys) {
+  const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= U) return;
+  const uint32_t p = vals[r];
+  const uint64_t z = (uint64_t)p + h;
+  uint64_t lo;
+  if (z < o) {
+    lo = (uint64_t)rank[z] + ins[z] + 1;
+  } else if (z < n) {
+    const uint32_t j = isa[z - o];
+    lo = (uint64_t)j + count_le(ins_sorted, o, j) + 1;
+  } else {
+    lo = 0;
+  }
+  keys[r] = ((uint64_t)rank[p] << sb) | lo;
+}
+
+// merge: new suffix p goes to ins(p) + rank[p], old suffix at index j to
+// j + (new suffixes with ins <= j), at position sa[j] + o
+__global__ void __launch_bounds__(256) k_ext_new_out(const uint32_t* __restrict__ rank,
+                                                       const uint32_t* __restrict__ ins, uint32_t o,
+                                                       uint32_t* __restrict__ out) {
+  const uint32_t p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p < o) out[rank[p] + ins[p]] = p;
+}
+
+constexpr int kOldItems = 8;
+constexpr int kCountShift = 11;  // one coarse count per 2048 old indexes (256 threads x kOldItems)
+static_assert((256 * kOldItems) == (1 << kCountShift), "a merge workgroup covers one coarse block");
+
+// coarse[b] = number of new suffixes with ins < b * 2048, b = 0 .. n_old/2048 + 1
+__global__ void __launch_bounds__(256) k_ext_coarse(const uint32_t* __restrict__ ins_sorted, uint32_t o,
+                                                      uint32_t nb, uint32_t* __restrict__ coarse) {
+  const uint32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb) return;
+  const uint64_t v = (uint64_t)b << kCountShift;
+  uint32_t x = 0, y = o;
+  while (x < y) {
+    const uint32_t mid = (x + y) >> 1;
+    if (ins_sorted[mid] < v) x = mid + 1; else y = mid;
+  }
+  coarse[b] = x;
+}
+
+// number of new suffixes with ins <= j, from the coarse table
+__device__ __forceinline__ uint32_t count_new_le(const uint32_t* __restrict__ ins_sorted,
+                                                 const uint32_t* __restrict__ coarse, uint32_t j) {
+  const uint32_t b = j >> kCountShift;
+  uint32_t x = coarse[b], y = coarse[b + 1];
+  while (x < y) {
+    const uint32_t mid = (x + y) >> 1;
+    if (ins_sorted[mid] <= j) x = mid + 1; else y = mid;
+  }
+  return x;
+}
+
+__global__ void __launch_bounds__(256) k_ext_old_out(const uint32_t* __restrict__ sa, uint32_t n_old,
+                                                       const uint32_t* __restrict__ ins_sorted,
+                                                       const uint32_t* __restrict__ coarse, uint32_t o,
+                                                       uint32_t* __restrict__ out) {
+  // workgroup b covers old indexes [2048 b, 2048 (b + 1)): one coarse block,
+  // whose few inserted suffixes every thread searches; j = base + t + 256 i
+  // keeps each step's reads and writes coalesced
+  const uint32_t base = blockIdx.x << kCountShift;
+  const uint32_t c0 = o ? coarse[blockIdx.x] : 0u, c1 = o ? coarse[blockIdx.x + 1] : 0u;
+  for (int i = 0; i < kOldItems; ++i) {
+    const uint32_t j = base + threadIdx.x + 256 * i;
+    if (j >= n_old) break;
+    uint32_t x = c0, y = c1;
+    while (x < y) {
+      const uint32_t mid = (x + y) >> 1;
+      if (ins_sorted[mid] <= j) x = mid + 1; else y = mid;
+    }
+    out[j + x] = sa[j] + o;
+  }
+}
+
+// inverse of the result: new position p at ins(p) + rank[p]; old position q
+// (now q + o) at isa[q] + (new suffixes with ins <= isa[q])
+__global__ void __launch_bounds__(256) k_ext_isa_new(const uint32_t* __restrict__ rank,
+                                                       const uint32_t* __restrict__ ins, uint32_t o,
+                                                       uint32_t* __restrict__ isa_out) {
+  const uint32_t p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p < o) isa_out[p] = rank[p] + ins[p];
+}
+
+__global__ void __launch_bounds__(256) k_ext_isa_old(const uint32_t* __restrict__ isa, uint32_t n_old,
+                                                       const uint32_t* __restrict__ ins_sorted,
+                                                       const uint32_t* __restrict__ coarse, uint32_t o,
+                                                       uint32_t* __restrict__ isa_out) {
+  const uint32_t q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= n_old) return;
+  uint32_t j = isa[q];
+  j = j < n_old ? j : n_old - 1;  // a malformed inverse cannot read out of bounds
+  isa_out[q + o] = j + (o ? count_new_le(ins_sorted, coarse, j) : 0u);
+}
+
 // ------------------------------------------------------------ histogram ---
 
 __global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys, uint32_t U, int digits,
@@ -581,22 +858,41 @@ fc_status radix_sort(BuildWs& w, int src, uint32_t U, int key_bits, SortState& s
   return FC_OK;
 }
 
-// Prefix doubling over all n suffixes (n_seg = 0) or over the suffixes of
+// The new suffixes of an extension (see k_init_keys_ext).
+struct ExtendArgs {
+  const uint32_t* ins;  // per new position
+  const uint32_t* isa;  // inverse of the old suffix array
+  uint32_t* ins_sorted; // ins in the sorted order of the new suffixes
+  uint64_t n;           // whole text
+  int n_old_bits;
+};
+
+// Prefix doubling over all n suffixes (n_seg = 0), over the suffixes of
 // n_seg segments at once, each ending at its segment's end (n_seg >= 1,
-// offsets already in w.seg_off).
+// offsets already in w.seg_off), or over the n new suffixes of an extension
+// (ext; leaves their ranks in w.rank and writes no suffix array).
 fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& w, uint32_t* sa_out,
-                   hipStream_t stream) {
+                   hipStream_t stream, const ExtendArgs* ext = nullptr) {
   const uint32_t N = (uint32_t)n;
   const uint64_t tiles = (n + kSortTile - 1) / kSortTile;
   FC_CHECK_HIP(hipMemsetAsync(w.status, 0, sizeof(uint64_t) * tiles * kRadix, stream));
   FC_CHECK_HIP(hipMemsetAsync(w.tickets, 0, sizeof(uint32_t) * kMaxPasses, stream));
   FC_CHECK_HIP(hipMemsetAsync(w.misc, 0, sizeof(uint32_t) * 16, stream));
 
-  const uint32_t sb = (uint32_t)bit_length(n);  // every rank + 1 <= n fits in sb bits
+  // every rank + 1 <= n (an extension's labels: <= the whole text) fits in sb bits
+  const uint32_t sb = (uint32_t)bit_length(ext ? ext->n : n);
   SortState st;
   uint64_t h;
   int key0_bits;
-  if (n_seg == 0) {
+  int ext_shift = 0;
+  if (ext) {
+    const int two = ext->n_old_bits + 34 <= 64;
+    ext_shift = two ? 34 : 17;
+    hipLaunchKernelGGL(k_init_keys_ext, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, tokens, N, ext->n,
+                       ext->ins, two, w.keys[0], w.vals[0]);
+    h = two ? 2 : 1;
+    key0_bits = ext_shift + ext->n_old_bits;
+  } else if (n_seg == 0) {
     hipLaunchKernelGGL(k_init_keys, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, tokens, N, w.keys[0],
                        w.vals[0]);
     h = 3;
@@ -613,7 +909,10 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
   for (int round = 0;; ++round) {
     if (round >= kMaxRounds) return FC_ERR_DEVICE;
     if (round > 0) {
-      if (n_seg == 0)
+      if (ext)
+        hipLaunchKernelGGL(k_pair_keys_ext, dim3(fc::div_up(U, 256)), dim3(256), 0, stream, w.vals[vin], U, w.rank,
+                           ext->ins, ext->isa, ext->ins_sorted, N, ext->n, h, sb, w.keys[vin]);
+      else if (n_seg == 0)
         hipLaunchKernelGGL(k_pair_keys, dim3(fc::div_up(U, 256)), dim3(256), 0, stream, w.vals[vin], U, w.rank, N,
                            h, sb, w.keys[vin]);
       else
@@ -625,6 +924,11 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
     int res = vin;
     fc_status s = radix_sort(w, vin, U, round == 0 ? key0_bits : (int)(2 * sb), st, stream, &res);
     if (s != FC_OK) return s;
+    if (ext && round == 0) {
+      hipLaunchKernelGGL(k_ins_sorted, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, w.keys[res], N, ext_shift,
+                         ext->ins_sorted);
+      FC_CHECK_LAUNCH();
+    }
     const uint32_t seg_tiles = fc::div_up(U, kSegTile);
     hipLaunchKernelGGL(k_seg_partials, dim3(seg_tiles), dim3(kSegThreads), 0, stream, w.keys[res], U, sb,
                        round == 0 ? 1 : 0, w.part_h, w.part_g, w.part_k);
@@ -643,6 +947,7 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
     vin = res ^ 1;
     if (U == 0) break;
   }
+  if (ext) return FC_OK;
   hipLaunchKernelGGL(k_scatter_sa, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, w.rank, N, sa_out);
   FC_CHECK_LAUNCH();
   if (n_seg > 0) {
@@ -689,6 +994,129 @@ extern "C" fc_status fc_datastore_build_batched(const uint16_t* tokens, const ui
   FC_CHECK_HIP(hipMemcpyAsync(w.seg_off, seg_off, sizeof(uint64_t) * ((size_t)n_seg + 1), hipMemcpyHostToDevice,
                               stream));
   return build_sa(tokens, n, (uint32_t)n_seg, w, sa_out, stream);
+}
+
+namespace {
+
+struct ExtendWs {
+  uint32_t* isa;  // inverse of the old array, unless the caller passes it
+  uint32_t *lo[2], *hi[2];
+  uint32_t *act[2], *done;
+  uint32_t* counts;  // [0] still ranged, [1] final this round, [2] active now
+  uint32_t* ins_sorted;
+  uint32_t* coarse;
+  BuildWs b;
+};
+
+uint32_t coarse_entries(uint64_t n_old) { return (uint32_t)((n_old + (1u << kCountShift) - 1) >> kCountShift) + 1; }
+
+size_t carve_extend(void* p, uint64_t n, uint64_t o, bool isa_given, ExtendWs* w) {
+  fc::Carver c(p);
+  ExtendWs t;
+  t.isa = c.take<uint32_t>(isa_given ? 0 : n - o);
+  for (int i = 0; i < 2; ++i) {
+    t.lo[i] = c.take<uint32_t>(o);
+    t.hi[i] = c.take<uint32_t>(o);
+    t.act[i] = c.take<uint32_t>(o);
+  }
+  t.done = c.take<uint32_t>(o);
+  t.counts = c.take<uint32_t>(4);
+  t.ins_sorted = c.take<uint32_t>(o);
+  t.coarse = c.take<uint32_t>(coarse_entries(n - o));
+  char* rest = p ? (char*)p + ((c.used + 255) & ~(size_t)255) : nullptr;
+  const size_t head = (c.used + 255) & ~(size_t)255;
+  const size_t tail = o ? carve_build(rest, o, &t.b) : 0;
+  if (w) *w = t;
+  return head + tail;
+}
+
+}  // namespace
+
+extern "C" size_t fc_datastore_extend_workspace_bytes(uint64_t n, uint64_t n_new, int32_t isa_given) {
+  return n_new <= n && n < 0xFFFFFFFFull ? carve_extend(nullptr, n, n_new, isa_given != 0, nullptr) : 0;
+}
+
+extern "C" fc_status fc_datastore_extend(const uint16_t* tokens, uint64_t n, uint64_t n_new, const uint32_t* old_sa,
+                                         const uint32_t* old_isa, uint32_t* sa_out, uint32_t* isa_out, void* ws,
+                                         size_t ws_bytes, hipStream_t stream) {
+  if (n >= 0xFFFFFFFFull || n_new > n) return FC_ERR_INVALID;
+  if (n == 0) return FC_OK;
+  const uint32_t o = (uint32_t)n_new, n_old = (uint32_t)(n - n_new);
+  if (!tokens || !sa_out || (n_old > 0 && !old_sa)) return FC_ERR_INVALID;
+  const bool isa_given = old_isa != nullptr;
+  if (!ws || ws_bytes < fc_datastore_extend_workspace_bytes(n, n_new, isa_given ? 1 : 0)) return FC_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  ExtendWs w;
+  carve_extend(ws, n, n_new, isa_given, &w);
+  const uint32_t* isa = isa_given ? old_isa : w.isa;
+  const bool need_isa = n_old > 0 && (o > 0 || isa_out);
+  if (need_isa && !isa_given) {
+    hipLaunchKernelGGL(k_isa, dim3(fc::div_up(n_old, 256)), dim3(256), 0, stream, old_sa, n_old, w.isa);
+    FC_CHECK_LAUNCH();
+  }
+  if (o > 0) {
+    FC_CHECK_HIP(hipMemsetAsync(w.counts, 0, sizeof(uint32_t) * 4, stream));
+    hipLaunchKernelGGL(k_ext_init, dim3(fc::div_up(o, 256)), dim3(256), 0, stream, tokens, o, (uint64_t)n, old_sa,
+                       n_old, w.lo[0], w.hi[0], w.lo[1], w.hi[1], w.act[0], w.counts + 2);
+    FC_CHECK_LAUNCH();
+    uint32_t n_act = 0;
+    FC_CHECK_HIP(hipMemcpyAsync(&n_act, w.counts + 2, sizeof(uint32_t), hipMemcpyDeviceToHost, stream));
+    FC_CHECK_HIP(hipStreamSynchronize(stream));
+    int cur = 0;
+    uint32_t* act_in = w.act[0];
+    uint32_t* act_out = w.act[1];
+    for (uint64_t h = kExtFirst; n_act > 0; h *= 2) {
+      if (h > 2 * n) return FC_ERR_DEVICE;  // every new suffix is final once p + h reaches the old text
+      FC_CHECK_HIP(hipMemsetAsync(w.counts, 0, sizeof(uint32_t) * 2, stream));
+      hipLaunchKernelGGL(k_ext_round, dim3(fc::div_up(n_act, 256)), dim3(256), 0, stream, o, (uint64_t)n, n_old,
+                         old_sa, isa, h, w.lo[cur], w.hi[cur], w.lo[cur ^ 1], w.hi[cur ^ 1], act_in,
+                         w.counts + 2, act_out, w.done, w.counts);
+      FC_CHECK_LAUNCH();
+      hipLaunchKernelGGL(k_ext_fix, dim3(fc::div_up(n_act, 256)), dim3(256), 0, stream, w.done, w.counts + 1,
+                         w.lo[cur ^ 1], w.lo[cur], w.hi[cur]);
+      FC_CHECK_LAUNCH();
+      FC_CHECK_HIP(hipMemcpyAsync(w.counts + 2, w.counts, sizeof(uint32_t), hipMemcpyDeviceToDevice, stream));
+      FC_CHECK_HIP(hipMemcpyAsync(&n_act, w.counts, sizeof(uint32_t), hipMemcpyDeviceToHost, stream));
+      FC_CHECK_HIP(hipStreamSynchronize(stream));
+      uint32_t* t = act_in;
+      act_in = act_out;
+      act_out = t;
+      cur ^= 1;
+    }
+    // every range is final and in both buffers: w.lo[0] holds ins
+    ExtendArgs ea;
+    ea.ins = w.lo[0];
+    ea.isa = isa;
+    ea.ins_sorted = w.ins_sorted;
+    ea.n = n;
+    ea.n_old_bits = bit_length(n_old);
+    fc_status s = build_sa(tokens, o, 0, w.b, nullptr, stream, &ea);
+    if (s != FC_OK) return s;
+    hipLaunchKernelGGL(k_ext_new_out, dim3(fc::div_up(o, 256)), dim3(256), 0, stream, w.b.rank, w.lo[0], o, sa_out);
+    FC_CHECK_LAUNCH();
+    if (isa_out) {
+      hipLaunchKernelGGL(k_ext_isa_new, dim3(fc::div_up(o, 256)), dim3(256), 0, stream, w.b.rank, w.lo[0], o,
+                         isa_out);
+      FC_CHECK_LAUNCH();
+    }
+  }
+  if (n_old > 0) {
+    const uint32_t nc = coarse_entries(n_old);
+    if (o > 0) {
+      hipLaunchKernelGGL(k_ext_coarse, dim3(fc::div_up(nc, 256)), dim3(256), 0, stream, w.ins_sorted, o, nc,
+                         w.coarse);
+      FC_CHECK_LAUNCH();
+    }
+    hipLaunchKernelGGL(k_ext_old_out, dim3(nc - 1), dim3(256), 0, stream, old_sa, n_old, w.ins_sorted, w.coarse, o,
+                       sa_out);
+    FC_CHECK_LAUNCH();
+    if (isa_out) {
+      hipLaunchKernelGGL(k_ext_isa_old, dim3(fc::div_up(n_old, 256)), dim3(256), 0, stream, isa, n_old, w.ins_sorted,
+                         w.coarse, o, isa_out);
+      FC_CHECK_LAUNCH();
+    }
+  }
+  return FC_OK;
 }
 
 extern "C" fc_status fc_store_prepare(const uint16_t* tokens, const uint32_t* sa, uint64_t n, uint32_t* bucket_out,

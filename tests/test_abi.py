@@ -224,3 +224,19 @@ def test_batched_build_rejects(L):
     assert L.fc_datastore_build_batched(None, off(0, 0, 0), 2, None, None, 0, None) == 0  # nothing to build
     assert (L.fc_datastore_build_batched_workspace_bytes(1000, 3) >
             L.fc_datastore_build_workspace_bytes(1000))
+
+
+def test_extend_rejects(L):
+    one = ctypes.c_void_p(8)
+    big = 1 << 34
+    assert L.fc_datastore_extend(one, 10, 11, one, None, one, None, one, big, None) == 1   # more new than all
+    assert L.fc_datastore_extend(one, 1 << 32, 5, one, None, one, None, one, big, None) == 1
+    assert L.fc_datastore_extend(one, 10, 4, None, None, one, None, one, big, None) == 1   # old store, no array
+    assert L.fc_datastore_extend(None, 10, 4, one, None, one, None, one, big, None) == 1
+    assert L.fc_datastore_extend(one, 10, 4, one, None, None, None, one, big, None) == 1   # no output
+    assert L.fc_datastore_extend(one, 10, 4, one, None, one, None, one, 8, None) == 2      # workspace too small
+    assert L.fc_datastore_extend(None, 0, 0, None, None, None, None, None, 0, None) == 0   # nothing to build
+    assert L.fc_datastore_extend_workspace_bytes(10, 11, 0) == 0
+    # without a given inverse the workspace holds one: 4 bytes per old token
+    assert (L.fc_datastore_extend_workspace_bytes(1_000_000, 1000, 0) -
+            L.fc_datastore_extend_workspace_bytes(1_000_000, 1000, 1)) >= 4 * 999_000

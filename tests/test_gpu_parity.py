@@ -161,6 +161,80 @@ def test_sa_batched_repository_set():
     _batched_case(tok, off, full=False)
 
 
+def _inverse(sa: np.ndarray) -> np.ndarray:
+    inv = np.empty(len(sa), np.uint32)
+    inv[sa.astype(np.int64)] = np.arange(len(sa), dtype=np.uint32)
+    return inv
+
+
+def _extend_case(new: np.ndarray, old: np.ndarray, full: bool = True):
+    """Extension: the new files in front of an old store, from the old
+    store's suffix array (with and without its inverse); must equal the
+    suffix array of the whole text, and isa_out its inverse."""
+    t = np.concatenate([np.asarray(new, np.uint16), np.asarray(old, np.uint16)])
+    o_sa = oracle.suffix_array(old) if full else host(fc.fc_datastore_build(dev(old)))
+    want = oracle.suffix_array(t) if full else None
+    for give_isa in (False, True):
+        isa_out = torch.empty(len(t), dtype=torch.uint32, device="cuda")
+        g = host(fc.fc_datastore_extend(dev(t), len(new), dev(o_sa), old_isa=dev(_inverse(o_sa)) if give_isa else None,
+                                        isa_out=isa_out))
+        torch.cuda.synchronize()
+        if full:
+            assert (g == want).all(), (len(new), len(old), give_isa)
+        else:
+            assert oracle.check_sa(t, g) == (0, 0), (len(new), len(old), give_isa)
+        assert (host(isa_out) == _inverse(g)).all(), (len(new), len(old), give_isa)
+
+
+@pytest.mark.parametrize("vocab", [2, 4, 32256])
+def test_sa_extend_small_texts(vocab):
+    for seed, (n_new, n_old) in enumerate([(0, 5), (5, 0), (1, 1), (1, 4096), (4097, 1), (3, 9000), (9000, 3),
+                                           (4095, 4097), (20011, 7000), (64, 64)]):
+        say(f"sa extend vocab={vocab} new={n_new} old={n_old}")
+        new = synth.random_text(7000 * vocab + seed, n_new, vocab, sep_prob=0.03 if seed % 2 else 0.0)
+        old = synth.random_text(8000 * vocab + seed, n_old, vocab, sep_prob=0.03 if seed % 2 else 0.0)
+        _extend_case(new, old)
+
+
+def test_sa_extend_degenerate_texts():
+    for n_new, n_old in ((1, 5000), (5000, 1), (3000, 3000)):
+        say(f"sa extend degenerate new={n_new} old={n_old}")
+        _extend_case(np.full(n_new, 7, np.uint16), np.full(n_old, 7, np.uint16))   # one long run
+        _extend_case(np.zeros(n_new, np.uint16), np.zeros(n_old, np.uint16))
+        _extend_case(np.full(n_new, 65535, np.uint16), np.full(n_old, 1, np.uint16))
+    old = synth.random_text(31, 6000, 3)
+    _extend_case(np.concatenate([old, [0]]), old)                                  # new files repeat the old store
+    _extend_case(np.concatenate([old[:2500], [0], old[:2500], [0]]), old)
+    _extend_case((np.arange(5000) % 2).astype(np.uint16), (np.arange(7000) % 2).astype(np.uint16))
+
+
+def test_sa_extend_twice_with_kept_inverse():
+    # a store grows twice; the second extension takes the first's inverse
+    a, b, c = (synth.random_text(600 + i, n, 5, sep_prob=0.02) for i, n in enumerate((3000, 5000, 8000)))
+    t1 = np.concatenate([b, c])
+    isa1 = torch.empty(len(t1), dtype=torch.uint32, device="cuda")
+    sa1 = fc.fc_datastore_extend(dev(t1), len(b), dev(oracle.suffix_array(c)), isa_out=isa1)
+    t2 = np.concatenate([a, t1])
+    sa2 = fc.fc_datastore_extend(dev(t2), len(a), sa1, old_isa=isa1)
+    torch.cuda.synchronize()
+    assert (host(sa2) == oracle.suffix_array(t2)).all()
+
+
+def test_sa_extend_repository_files():
+    # a repository's new files (own seed, shared templates) in front of the
+    # 1M-token single store, and in front of the 2M project store
+    for cfg, role in ((1, "single"), (2, "project")):
+        old = synth.store(cfg, role)
+        tok, off = synth.repos(40 + cfg, 1, 20, 200)
+        new = np.concatenate([tok, [0]]).astype(np.uint16)
+        say(f"sa extend {role} by {len(new)} tokens")
+        _extend_case(new, old, full=False)
+        t = np.concatenate([new, old])
+        ext = host(fc.fc_datastore_extend(dev(t), len(new), fc.fc_datastore_build(dev(old))))
+        torch.cuda.synchronize()
+        assert (ext == host(fc.fc_datastore_build(dev(t)))).all()
+
+
 def test_bucket_table():
     for t in (synth.random_text(5, 5000, 300, 0.02), synth.store(1, "single"), np.zeros(0, np.uint16)):
         st = gpu_store(t) if len(t) else None
