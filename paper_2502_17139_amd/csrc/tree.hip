@@ -473,50 +473,15 @@ struct Scan2 {
   }
 };
 
-// Splits the batch into light (T <= t_small kept slots; malformed rows too)
-// and heavy queries, each list in query order: lists[0..B) light ids,
-// lists[B..2B) heavy ids, counts[0], counts[1] their lengths.
-__global__ void __launch_bounds__(1024) k_tree_classify(const int32_t* __restrict__ taken, int B, int S, int k,
-                                                        int t_small, const int32_t* __restrict__ rows, int n_rows,
-                                                        int32_t* __restrict__ lists,
-                                                        int32_t* __restrict__ counts) {
-  __shared__ uint32_t s_a[1024 / fc::kWave + 1], s_b[1024 / fc::kWave + 1];
-  const int per = (B + 1023) / 1024;
-  const int b0 = (int)threadIdx.x * per;
-  const int b1 = b0 + per < B ? b0 + per : B;
-  auto heavy = [&](int b) {
-    const int r = fc::map_row(rows, n_rows, b);
-    if (r < 0) return false;  // reported as malformed by the light launch
-    int T = 0, bad = 0;
-    for (int s = 0; s < S; ++s) {
-      const int t = taken[(int64_t)r * S + s];
-      bad |= t < 0;
-      T += t > 0 ? t : 0;
-    }
-    return !bad && T <= k && T > t_small;
-  };
-  uint32_t nh = 0;
-  for (int b = b0; b < b1; ++b) nh += heavy(b) ? 1u : 0u;
-  const uint32_t nl = (uint32_t)(b1 > b0 ? b1 - b0 : 0) - nh;
-  uint32_t el, eh, tl, th;
-  Scan2<1024>::run(nl, nh, s_a, s_b, &el, &eh, &tl, &th);
-  for (int b = b0; b < b1; ++b) {
-    if (heavy(b)) lists[B + (eh++)] = b;
-    else lists[el++] = b;
-  }
-  if (threadIdx.x == 0) {
-    counts[0] = (int32_t)tl;
-    counts[1] = (int32_t)th;
-  }
-}
-
 template <int NT, int MAXM>
 __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__ taken,
                                                   const uint8_t* __restrict__ cont_len,
                                                   const uint16_t* __restrict__ cont_tok,
                                                   const uint16_t* __restrict__ ctx, int L, int S, int k, int m, int c,
                                                   Alpha alpha, const int32_t* __restrict__ list,
-                                                  const int32_t* __restrict__ list_count, int t_hi, int words,
+                                                  const int32_t* __restrict__ list_count,
+                                                  int32_t* __restrict__ heavy_list, int32_t* __restrict__ heavy_count,
+                                                  int B, int t_hi, int words,
                                                   const int32_t* __restrict__ rows, int n_rows,
                                                   int32_t* __restrict__ num_nodes, int32_t* __restrict__ node_tok,
                                                   int32_t* __restrict__ parent, uint32_t* __restrict__ weight,
@@ -537,15 +502,60 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   __shared__ int16_t s_par[FC_MAX_TREE_ROWS];
   __shared__ uint64_t s_dball[FC_MAX_TREE_ROWS / fc::kWave][MAXM];
   __shared__ uint32_t s_pick[3];
+  __shared__ int s_query;
 
-  // This launch owns the queries in `list` (built by k_tree_classify);
-  // workgroups past the list's length leave at once, after every real one
-  // has been dispatched.  (list has B entries: reading it before the count
-  // check saves a round trip.)
-  const int b_raw = list[blockIdx.x];
-  if ((int)blockIdx.x >= *list_count) return;
-  const int b = b_raw;
   const int tid = threadIdx.x;
+  int b;
+  if (list) {
+    // This launch owns the queries in `list` (written by the light launch);
+    // workgroups past the list's length leave at once, after every real
+    // one has been dispatched.  (list has B entries: reading it before the
+    // count check saves a round trip.)
+    const int b_raw = list[blockIdx.x];
+    if ((int)blockIdx.x >= *list_count) return;
+    b = b_raw;
+  } else {
+    // The light launch: its queries are those with T <= t_hi kept slots
+    // (malformed rows too), in query order, and workgroup x takes the x-th.
+    // Every workgroup finds it with one scan over the batch; workgroup 0
+    // also writes the list of the others (the heavy launch's).
+    auto heavy = [&](int q) {
+      const int r = fc::map_row(rows, n_rows, q);
+      if (r < 0) return false;
+      int T = 0, bad = 0;
+      for (int u = 0; u < S; ++u) {
+        const int t = taken[(int64_t)r * S + u];
+        bad |= t < 0;
+        T += t > 0 ? t : 0;
+      }
+      return !bad && T <= k && T > t_hi;
+    };
+    const int per = (B + NT - 1) / NT;
+    const int q0 = tid * per < B ? tid * per : B;
+    const int q1 = q0 + per < B ? q0 + per : B;
+    uint32_t nh = 0;
+    for (int q = q0; q < q1; ++q) nh += heavy(q) ? 1u : 0u;
+    const uint32_t nl = (uint32_t)(q1 - q0) - nh;
+    uint32_t el, eh, tl, th;
+    Scan2<NT>::run(nl, nh, s_x, s_y, &el, &eh, &tl, &th);
+    if (blockIdx.x == 0) {
+      for (int q = q0; q < q1; ++q)
+        if (heavy(q)) heavy_list[eh++] = q;
+      if (tid == 0) *heavy_count = (int32_t)th;
+    }
+    const uint32_t target = blockIdx.x;
+    if (target >= tl) return;
+    if (target >= el && target < el + nl) {
+      uint32_t x = el;
+      for (int q = q0; q < q1; ++q) {
+        if (heavy(q)) continue;
+        if (x == target) s_query = q;
+        ++x;
+      }
+    }
+    __syncthreads();
+    b = s_query;
+  }
   const int lane = fc::lane_id();
   const int w = tid / fc::kWave;
   const int R = c + 1;
@@ -570,7 +580,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     }
   }
   bad |= T_raw > k;
-  bad |= T_raw > t_hi;  // cannot happen: k_tree_classify routes queries by T
+  bad |= T_raw > t_hi;  // cannot happen: the light launch routes queries by T
   if (bad) T_raw = 0;
 
   const TreeLayout lay = tree_layout(t_hi, m, kSepE);
@@ -1077,9 +1087,6 @@ fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint1
   const int t_small = k < kSmallClass ? k : kSmallClass;
   int32_t* lists = (int32_t*)ws;
   int32_t* counts = lists + 2 * (size_t)B;
-  hipLaunchKernelGGL(k_tree_classify, dim3(1), dim3(1024), 0, stream, taken, B, S, k, t_small, rows, n_rows, lists,
-                     counts);
-  FC_CHECK_LAUNCH();
   // row loads: 16-byte vectors when every query's row is 16-byte aligned,
   // else 32-bit words when 4-byte aligned, else single tokens
   int words = 0;
@@ -1091,8 +1098,8 @@ fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint1
                               (int)small.total);
   (void)hipGetLastError();
   hipLaunchKernelGGL((k_tree_fast<256, MAXM>), dim3(B), dim3(256), small.total, stream, taken, cont_len, cont_tok,
-                     ctx, L, S, k, m, t.c, a, lists, counts, t_small, words, rows, n_rows, num_nodes, node_tok, parent,
-                     weight, pos_ids, mask);
+                     ctx, L, S, k, m, t.c, a, nullptr, nullptr, lists + B, counts + 1, B, t_small, words, rows,
+                     n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
   FC_CHECK_LAUNCH();
   if (k > t_small) {
     if (full.total > 64 * 1024)
@@ -1100,8 +1107,8 @@ fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint1
                                 (int)full.total);
     (void)hipGetLastError();
     hipLaunchKernelGGL((k_tree_fast<1024, MAXM>), dim3(B), dim3(1024), full.total, stream, taken, cont_len, cont_tok,
-                       ctx, L, S, k, m, t.c, a, lists + B, counts + 1, k, words, rows, n_rows, num_nodes, node_tok,
-                       parent, weight, pos_ids, mask);
+                       ctx, L, S, k, m, t.c, a, lists + B, counts + 1, nullptr, nullptr, B, k, words, rows, n_rows,
+                       num_nodes, node_tok, parent, weight, pos_ids, mask);
     FC_CHECK_LAUNCH();
   }
   return FC_OK;
