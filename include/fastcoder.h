@@ -431,6 +431,86 @@ fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_
                                 const int32_t* start, const int32_t* num_nodes, const int32_t* pos_ids, int32_t B,
                                 int32_t c, int32_t* target, hipStream_t stream);
 
+/*
+ * Device-resident replay engine: the whole decode-trace replay above (the
+ * average acceptance length of Section V-C, eq. (7)) with every per-step
+ * decision on the GPU.  Each step, for every stream b with pos[b] <
+ * truth_len: its context truth[b][pos[b]-ctx_len .. pos[b]) is looked up in
+ * an LRU of `lru` recent retrievals keyed by the exact context (a hit
+ * becomes most recent; a miss takes the next free slot, or the least
+ * recently used one when all are taken, and is retrieved into it); the
+ * draft tree is built from the slot (fc_build_tree), the true tokens are
+ * its targets (fc_targets_from_truth), acceptance is greedy
+ * (fc_verify_accept) and pos[b] advances by the accepted length.  A step is
+ * a fixed chain of launches on `stream` with no host round trip.
+ *
+ * All pointers are device memory owned by the caller:
+ *   pos, lru_count, hits, lookups, rows_retrieve, rows_tree [n_streams];
+ *   lru_key [n_streams][lru][ctx_len]; lru_used [n_streams][lru];
+ *   ctx [n_streams][ctx_len]; live [1]: streams still live after the last
+ *   step; history [max_steps][n_streams]: the accepted length of each
+ *   stream at each step, -1 once the stream is finished;
+ *   retrieval outputs (fc_retrieve's, with n_streams * lru rows: row
+ *   b * lru + slot is stream b's slot) and workspace for a batch of
+ *   n_streams; tree outputs, target [n_streams][c+1] and acceptance
+ *   outputs for n_streams.
+ * Limits: 1 <= ctx_len <= 64 (also fc_retrieve's n_max <= ctx_len is the
+ * caller's choice), 1 <= lru <= 64, truth_stride >= truth_len.
+ * fc_replay_init sets pos = ctx_len, empties every LRU and zeroes the
+ * counters.  fc_replay_run runs steps first_step .. first_step + n_steps - 1
+ * (their history rows), first_step + n_steps <= max_steps; read `live`
+ * between calls to stop once it is 0.  Errors of the calls it makes are
+ * returned as they come.
+ */
+typedef struct fc_replay {
+  const uint16_t* truth;
+  int64_t truth_stride;
+  int32_t truth_len;
+  int32_t n_streams;
+  int32_t ctx_len;
+  int32_t lru;
+  int32_t max_steps;
+  fc_retrieve_params rp;
+  fc_tree_params tp;
+  int32_t* pos;
+  uint16_t* lru_key;
+  int32_t* lru_used;
+  int32_t* lru_count;
+  int32_t* hits;
+  int32_t* lookups;
+  uint16_t* ctx;
+  int32_t* rows_retrieve;
+  int32_t* rows_tree;
+  int32_t* live;
+  int32_t* history;
+  int32_t* match_n;
+  uint32_t* range_lo;
+  uint32_t* range_cnt;
+  int32_t* taken;
+  uint32_t* cont_pos;
+  uint8_t* cont_src;
+  uint8_t* cont_len;
+  uint16_t* cont_tok;
+  void* retrieve_ws;
+  size_t retrieve_ws_bytes;
+  int32_t* num_nodes;
+  int32_t* node_tok;
+  int32_t* parent;
+  uint32_t* weight;
+  int32_t* pos_ids;
+  int32_t* mask;
+  void* tree_ws;
+  size_t tree_ws_bytes;
+  int32_t* target;
+  int32_t* accept_len;
+  int32_t* accept_tok;
+  int32_t* last_node;
+} fc_replay;
+
+fc_status fc_replay_init(fc_replay* r, hipStream_t stream);
+fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_replay* r, int32_t first_step, int32_t n_steps,
+                        hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

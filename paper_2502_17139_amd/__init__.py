@@ -37,7 +37,7 @@ EXPORTS = (
     "fc_pair_table_entries", "fc_store_prepare_pairs", "fc_record_bytes", "fc_store_prepare_records",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
     "fc_verify_accept", "fc_targets_from_truth", "fc_cache_lds_bytes", "fc_cache_retrieve", "fc_cache_write",
-    "fc_tree_attention",
+    "fc_tree_attention", "fc_replay_init", "fc_replay_run",
 )
 
 
@@ -61,6 +61,22 @@ class FcRetrieveParams(ctypes.Structure):
 
 class FcTreeParams(ctypes.Structure):
     _fields_ = [("c", ctypes.c_int32), ("alpha", ctypes.c_uint32 * FC_MAX_SOURCES)]
+
+
+_P = ctypes.c_void_p
+
+
+class FcReplay(ctypes.Structure):
+    _fields_ = [("truth", _P), ("truth_stride", ctypes.c_int64), ("truth_len", ctypes.c_int32),
+                ("n_streams", ctypes.c_int32), ("ctx_len", ctypes.c_int32), ("lru", ctypes.c_int32),
+                ("max_steps", ctypes.c_int32), ("rp", FcRetrieveParams), ("tp", FcTreeParams)] + [
+        (f, _P) for f in ("pos", "lru_key", "lru_used", "lru_count", "hits", "lookups", "ctx", "rows_retrieve",
+                          "rows_tree", "live", "history", "match_n", "range_lo", "range_cnt", "taken", "cont_pos",
+                          "cont_src", "cont_len", "cont_tok", "retrieve_ws")] + [
+        ("retrieve_ws_bytes", ctypes.c_size_t)] + [
+        (f, _P) for f in ("num_nodes", "node_tok", "parent", "weight", "pos_ids", "mask", "tree_ws")] + [
+        ("tree_ws_bytes", ctypes.c_size_t)] + [
+        (f, _P) for f in ("target", "accept_len", "accept_tok", "last_node")]
 
 
 @functools.lru_cache(maxsize=1)
@@ -119,6 +135,10 @@ def lib() -> ctypes.CDLL:
                                 vp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]
     L.fc_verify_accept.restype = ctypes.c_int
     L.fc_verify_accept.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp]
+    L.fc_replay_init.restype = ctypes.c_int
+    L.fc_replay_init.argtypes = [ctypes.POINTER(FcReplay), vp]
+    L.fc_replay_run.restype = ctypes.c_int
+    L.fc_replay_run.argtypes = [ctypes.POINTER(FcStore), i32, ctypes.POINTER(FcReplay), i32, i32, vp]
     L.fc_targets_from_truth.restype = ctypes.c_int
     L.fc_targets_from_truth.argtypes = [vp, i32, ctypes.c_int64, vp, vp, vp, vp, i32, i32, vp, vp]
     return L
@@ -457,3 +477,67 @@ def fc_targets_from_truth(truth: torch.Tensor, start: torch.Tensor, tree: dict, 
         _ptr(truth), truth.shape[1], truth.stride(0), _ptr(seq), _ptr(start), _ptr(tree["num_nodes"]),
         _ptr(tree["pos_ids"]), B, R - 1, _ptr(out), _stream(stream)))
     return out
+
+
+class ReplayEngine:
+    """Device-resident decode-trace replay (fc_replay_init / fc_replay_run):
+    owns the device state for `truth` (uint16 [n_streams][length] on the
+    GPU) over `stores`; run() replays until every stream is finished."""
+
+    def __init__(self, stores, truth: torch.Tensor, n_max=16, n_min=2, k=5000, m=10, c=64, alpha=(1, 1), lru=32,
+                 ctx_len=16, max_steps=512, chunk=16):
+        if truth.dtype != torch.uint16 or truth.dim() != 2 or not truth.is_contiguous():
+            raise ValueError("truth must be a contiguous 2-D uint16 tensor")
+        dev = truth.device
+        self.stores, self.truth, self.chunk = stores, truth, chunk
+        n, tlen = truth.shape
+        S = len(stores)
+        self.views = (FcStore * S)(*[st.view() for st in stores])
+        i32 = torch.int32
+        self.t = dict(pos=_empty(n, i32, dev), lru_key=_empty((n, lru, ctx_len), torch.uint16, dev),
+                      lru_used=_empty((n, lru), i32, dev), lru_count=_empty(n, i32, dev), hits=_empty(n, i32, dev),
+                      lookups=_empty(n, i32, dev), ctx=_empty((n, ctx_len), torch.uint16, dev),
+                      rows_retrieve=_empty(n, i32, dev), rows_tree=_empty(n, i32, dev), live=_empty(1, i32, dev),
+                      history=_empty((max_steps, n), i32, dev), target=_empty((n, c + 1), i32, dev))
+        self.t.update(retrieve_outputs(n * lru, S, k, m, dev))
+        self.t.update(tree_outputs(n, c, dev))
+        self.t.update(accept_outputs(n, m, dev))
+        rp = FcRetrieveParams(n_max, n_min, k, m)
+        self.rws = _empty(max(int(lib().fc_retrieve_workspace_bytes(n, S, rp)), 1), torch.uint8, dev)
+        self.tws = _empty(max(fc_build_tree_workspace_bytes(n), 1), torch.uint8, dev)
+        al = (ctypes.c_uint32 * FC_MAX_SOURCES)(*([int(a) for a in tuple(alpha)[:S]] + [0] * (FC_MAX_SOURCES - S)))
+        r = FcReplay()
+        r.truth, r.truth_stride, r.truth_len = truth.data_ptr(), truth.stride(0), tlen
+        r.n_streams, r.ctx_len, r.lru, r.max_steps = n, ctx_len, lru, max_steps
+        r.rp, r.tp = rp, FcTreeParams(c, al)
+        for f, v in self.t.items():
+            setattr(r, f, v.data_ptr())
+        r.retrieve_ws, r.retrieve_ws_bytes = self.rws.data_ptr(), self.rws.numel()
+        r.tree_ws, r.tree_ws_bytes = self.tws.data_ptr(), self.tws.numel()
+        self.r, self.max_steps = r, max_steps
+
+    def run(self, limit: int | None = None, stream=None) -> dict:
+        """Replays from the start for at most `limit` (default max_steps)
+        steps; returns the per-step accepted lengths ([steps][n_streams], -1
+        for finished streams), LRU hits and lookups, final positions and the
+        mean accepted length."""
+        st = _stream(stream)
+        cap = self.max_steps if limit is None else min(limit, self.max_steps)
+        _check("fc_replay_init", lib().fc_replay_init(ctypes.byref(self.r), st))
+        step = 0
+        while step < cap:
+            n = min(self.chunk, cap - step)
+            _check("fc_replay_run", lib().fc_replay_run(self.views, len(self.stores), ctypes.byref(self.r), step, n,
+                                                        st))
+            step += n
+            if int(self.t["live"].item()) == 0:
+                break
+        hist = self.t["history"][:step].cpu().numpy().astype(np.int64)
+        live_rows = (hist >= 0).any(axis=1)
+        steps = int(live_rows.sum())
+        acc = hist[:steps]
+        live = acc >= 0
+        return dict(accept=acc, hits=self.t["hits"].cpu().numpy().astype(np.int64),
+                    lookups=self.t["lookups"].cpu().numpy().astype(np.int64),
+                    pos=self.t["pos"].cpu().numpy().astype(np.int64),
+                    acc_len=float(acc[live].sum() / max(live.sum(), 1)), steps=steps)

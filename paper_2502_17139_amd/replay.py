@@ -27,6 +27,11 @@ host keeps the sequence lists, decides evictions (oldest sequences first
 when a text would outgrow its row) and ships each step's appended tokens in
 one batched fc_cache_write.
 
+Without the CACHE and the timing control, run() hands the whole replay to
+the device-resident engine (ReplayEngine: fc_replay_init / fc_replay_run),
+which takes the same decisions on the GPU with no host round trip per step;
+step() is this module's own host-driven loop, used for the other modes.
+
 Alg. 1's retrieval-timing control (for contexts the CACHE did not serve):
 with missing=True a per-stream missing table holds the contexts whose
 datastore retrieval found nothing, and such a context is not retrieved
@@ -42,7 +47,7 @@ from collections import OrderedDict
 import numpy as np
 import torch
 
-from . import (FC_MAX_CACHE_TOKENS, accept_outputs, fc_build_tree, fc_build_tree_workspace_bytes,
+from . import (FC_MAX_CACHE_TOKENS, ReplayEngine, accept_outputs, fc_build_tree, fc_build_tree_workspace_bytes,
                fc_cache_retrieve, fc_cache_write, fc_retrieve, fc_retrieve_workspace_bytes, fc_targets_from_truth,
                fc_verify_accept, retrieve_outputs, tree_outputs)
 
@@ -88,6 +93,7 @@ class GpuReplay:
                  ctx_len=16, device="cuda", cache_l=None, cache_every=20, cache_cap=FC_MAX_CACHE_TOKENS,
                  missing=False, skip_tok=None, skip_p=0.5, skip_draws=None):
         self.stores = stores
+        self.kw = dict(n_max=n_max, n_min=n_min, k=k, m=m, c=c, alpha=alpha, lru=lru, ctx_len=ctx_len)
         self.truth_np = np.ascontiguousarray(truth, dtype=np.uint16)
         self.nseq, self.tlen = self.truth_np.shape
         self.truth = torch.from_numpy(self.truth_np).to(device)
@@ -273,7 +279,27 @@ class GpuReplay:
         self._cache_upload(changed)
         return out
 
-    def run(self, max_steps: int = 512) -> dict:
+    @property
+    def plain(self) -> bool:
+        """No CACHE and no timing control: the device engine's mode."""
+        return self.cache_l is None and not self.missing and self.skip_tok is None
+
+    def run(self, max_steps: int = 512, native: bool | None = None) -> dict:
+        """Replays from the current state (the engine always from the start)
+        for at most max_steps steps.  native: None picks the device engine
+        for the plain mode, True requires it, False uses step()."""
+        if native is None:
+            native = self.plain
+        if native:
+            if not self.plain:
+                raise ValueError("the device engine runs the plain replay only (no CACHE, no timing control)")
+            if not hasattr(self, "_engine") or self._engine.max_steps < max_steps:
+                self._engine = ReplayEngine(self.stores, self.truth, max_steps=max(max_steps, 512), **self.kw)
+            g = self._engine.run(limit=max_steps)
+            n = self.nseq
+            g.update(cache_served=np.zeros(n, np.int64), missing_skips=np.zeros(n, np.int64),
+                     gate_skips=np.zeros(n, np.int64))
+            return g
         steps = []
         for _ in range(max_steps):
             a = self.step()

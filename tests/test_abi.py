@@ -240,3 +240,35 @@ def test_extend_rejects(L):
     # without a given inverse the workspace holds one: 4 bytes per old token
     assert (L.fc_datastore_extend_workspace_bytes(1_000_000, 1000, 0) -
             L.fc_datastore_extend_workspace_bytes(1_000_000, 1000, 1)) >= 4 * 999_000
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """The binding's ctypes structs have the header's field offsets (a C
+    program built against include/fastcoder.h prints them)."""
+    import shutil
+    import subprocess
+    import paper_2502_17139_amd as fc
+    if shutil.which("gcc") is None:
+        pytest.skip("no C compiler")
+    structs = {"fc_replay": fc.FcReplay, "fc_store": fc.FcStore, "fc_retrieve_params": fc.FcRetrieveParams,
+               "fc_tree_params": fc.FcTreeParams}
+    lines = ["#include <stdio.h>", '#include "fastcoder.h"', "int main(void) {"]
+    for name, cls in structs.items():
+        lines.append(f'  printf("{name} sizeof %zu\\n", sizeof({name}));')
+        for f, _ in cls._fields_:
+            lines.append(f'  printf("{name} {f} %zu\\n", offsetof({name}, {f}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-I" + os.path.join(root, "include"),
+                    str(src), "-o", str(exe)], check=True)
+    got = {}
+    for line in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.splitlines():
+        name, f, v = line.split()
+        got[(name, f)] = int(v)
+    for name, cls in structs.items():
+        assert got[(name, "sizeof")] == ctypes.sizeof(cls), name
+        for f, _ in cls._fields_:
+            assert got[(name, f)] == getattr(cls, f).offset, (name, f)

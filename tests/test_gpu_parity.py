@@ -372,15 +372,17 @@ def test_headline_workload_sampled():
 
 # ------------------------------------------------------------------ replay --
 
-def test_replay_matches_oracle():
-    """Decode-trace replay: 16 streams from the project pool, 10M-token
-    project store + 1M-token store, first 60 steps; every accepted length,
-    cache hit and final position equal."""
+@pytest.mark.parametrize("native", [True, False], ids=["engine", "driver"])
+def test_replay_matches_oracle(native):
+    """Decode-trace replay, by the device engine and by the host-driven
+    loop: 16 streams from the project pool, 10M-token project store +
+    1M-token store, first 60 steps; every accepted length, cache hit and
+    final position equal."""
     tp, t1 = synth.store(3, "project"), synth.store(1, "single")
     truth = synth.truth(n_seq=16, length=600)
     stores = [gpu_store(tp, synth.VOCAB), gpu_store(t1)]
-    say("replay: gpu")
-    g = GpuReplay(stores, truth, **P).run(max_steps=60)
+    say(f"replay: gpu native={native}")
+    g = GpuReplay(stores, truth, **P).run(max_steps=60, native=native)
     say("replay: oracle")
     o = oracle.replay([tp, t1], truth, **P, max_steps=60)
     for f in ("accept", "hits", "lookups", "pos"):
@@ -388,16 +390,18 @@ def test_replay_matches_oracle():
     assert g["acc_len"] == o["acc_len"] and g["acc_len"] > 2.0
 
 
-def test_replay_cache_eviction():
+@pytest.mark.parametrize("native", [True, False], ids=["engine", "driver"])
+def test_replay_cache_eviction(native):
     """Periodic streams that never match: one token per step, contexts cycle
-    through 20 keys; LRU sizes above and below the cycle."""
+    through 20 keys; LRU sizes above and below the cycle (device engine and
+    host-driven loop)."""
     store = np.full(5000, 7, np.uint16)
     period = (np.arange(20) * 13 % 97 + 100).astype(np.uint16)
     truth = np.stack([np.tile(np.roll(period, r), 12) for r in range(3)])
     st = gpu_store(store)
     for lru in (10, 20, 32):
         p = dict(n_max=16, n_min=2, k=50, m=4, c=8, alpha=(1,))
-        g = GpuReplay([st], truth, lru=lru, **p).run(max_steps=1000)
+        g = GpuReplay([st], truth, lru=lru, **p).run(max_steps=1000, native=native)
         o = oracle.replay([store], truth, lru=lru, **p, max_steps=1000)
         for f in ("accept", "hits", "lookups", "pos"):
             assert (g[f] == o[f]).all(), (lru, f)
