@@ -410,6 +410,28 @@ def test_replay_cache_eviction(native):
 
 # -------------------------------------------------------------- edge cases --
 
+def test_large_batch():
+    """4,200 queries: the kept-slot offsets no longer fit the gather's LDS
+    table (a scan kernel of its own) and the light launch scans 17 queries
+    per thread; random contexts match short and fill the heavy class."""
+    texts = [synth.random_text(7, 20000, 8, 0.02), synth.random_text(8, 30000, 8, 0.02)]
+    rng = np.random.default_rng(1)
+    B = 4200
+    # windows of the stores match long (light); a token the stores lack then
+    # a pair of theirs matches two tokens only, with ~1,000 occurrences
+    ctx = np.stack([texts[b % 2][j:j + 12] if b % 5 else
+                    np.concatenate([np.full(10, 39, np.uint16), rng.integers(1, 8, 2).astype(np.uint16)])
+                    for b, j in enumerate(rng.integers(0, 19000, B))])
+    p = dict(n_max=12, n_min=2, k=400, m=10)
+    say(f"large batch B={B}")
+    g = gpu_pipeline([gpu_store(t) for t in texts], ctx, p, (1, 2), 16)
+    o = oracle_pipeline(texts, ctx, p, (1, 2), 16)
+    assert (o["taken"].sum(1) > 256).sum() > 100  # the heavy launch has work
+    compare_retrieve(g, o)
+    compare_tree(g, o)
+    _check_accept(g, o, p["m"], 5)
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_fuzz_small_stores(seed):
     rng = np.random.default_rng(seed)
