@@ -16,8 +16,18 @@
 // dims.  Working on the transposes keeps every operand in the lane layout
 // the MFMA wants: a lane's eight scores are exactly its eight probabilities
 // of the value product, so nothing is shuffled between the two products.
-// Workgroups are numbered so that the query heads sharing a key head run on
-// the same XCD and its L2 serves their shared key/value reads.
+//
+// The cached prefix moves straight from HBM into LDS with buffer loads that
+// write LDS (16 bytes a lane, no registers), through a ring of four blocks,
+// so three blocks are in flight while one is used; the loads of rows past
+// the prefix fall outside the buffer's range and read as zeros.  Rows sit in
+// LDS as written (key-major), each 16-byte chunk XOR-swizzled by the row, so
+// the score product reads K rows without bank conflicts and the value
+// product takes V^T with the transposing LDS read (ds_read_b64_tr_b16),
+// which hands each lane four keys of one output dim.  The tree's own keys
+// are rotated on the way in, through registers.  Workgroups are numbered so
+// that the query heads sharing a key head run on the same XCD and its L2
+// serves their shared key/value reads.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -28,19 +38,26 @@
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef int int32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-constexpr int kD = FC_TREE_ATTN_HEAD_DIM;  // 128
-constexpr int kBlock = 32;                 // keys per block
-constexpr int kKStride = kD + 8;           // bf16 per key row in LDS (padded)
-constexpr int kVStride = kBlock + 8;       // bf16 per value column in LDS (padded)
-constexpr int kDTiles = kD / 16;           // output tiles of 16 dims
-constexpr int kDSteps = kD / 32;           // 32-dim steps of the score product
+constexpr int kD = FC_TREE_ATTN_HEAD_DIM;   // 128
+constexpr int kBlock = 32;                  // keys per block
+constexpr int kRowBytes = kD * 2;           // 256: one key row
+constexpr int kPart = kBlock * kRowBytes;   // 8 KB: a block's keys (or values)
+constexpr int kStage = 2 * kPart;           // keys then values
+constexpr int kStages = 4;                  // ring depth
+constexpr int kDTiles = kD / 16;            // output tiles of 16 dims
+constexpr int kDSteps = kD / 32;            // 32-dim steps of the score product
+constexpr int kDmaWaves = 4;                // waves issuing a block's 16 loads, 4 each
 constexpr int kXcds = 8;
 
-__device__ __forceinline__ float bf2f(uint16_t x) { return __uint_as_float((uint32_t)x << 16); }
-
 __device__ __forceinline__ __bf16 f2bf(float x) { return (__bf16)x; }
+
+// byte offset inside a block part of 16-byte chunk c of row r (swizzled)
+__device__ __forceinline__ uint32_t chunk_at(int r, int c) { return (uint32_t)(r * kRowBytes + ((c ^ (r & 15)) << 4)); }
 
 // sin and cos of the rotary angle position * base^(-2d/D) of the pair (d,
 // d + D/2).  The angle is taken in revolutions and reduced to [0, 1) in
@@ -65,6 +82,28 @@ __device__ __forceinline__ void load8(const uint16_t* __restrict__ p, float (&v)
   }
 }
 
+// Buffer resource over `bytes` bytes at p (raw, no stride): loads at or past
+// `bytes` return zeros.
+__device__ __forceinline__ int32x4 buffer_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = (uint64_t)p;
+  int32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r.y = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xFFFFu));
+  r.z = __builtin_amdgcn_readfirstlane((int)bytes);
+  r.w = 0x00020000;
+  return r;
+}
+
+// One wave loads 64 x 16 bytes from the buffer at byte offsets voff (one per
+// lane) into LDS bytes [lds, lds + 1024), lane L at lds + 16 L.  The load is
+// counted by vmcnt like any vector load; the compiler does not track it.
+__device__ __forceinline__ void lds_load16(uint32_t lds, uint32_t voff, int32x4 rsrc) {
+  asm volatile("s_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds"
+               :
+               : "v"(voff), "s"(__builtin_amdgcn_readfirstlane((int)lds)), "s"(rsrc)
+               : "memory");
+}
+
 template <int MAXT>
 __global__ void __launch_bounds__(MAXT) k_tree_attn(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_tree, const uint16_t* __restrict__ v_tree,
@@ -72,9 +111,7 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
     const int32_t* __restrict__ prefix_len, const int32_t* __restrict__ num_nodes, const int32_t* __restrict__ mask,
     const int32_t* __restrict__ pos_ids, int B, int R, int H, int Hkv, int Pmax, double log2_base,
     float* __restrict__ out) {
-  // two buffers: the next block is staged while the current one is used
-  __shared__ __align__(16) __bf16 s_k[2][kBlock * kKStride];
-  __shared__ __align__(16) __bf16 s_vt[2][kD * kVStride];
+  __shared__ __align__(16) uint8_t s_ring[kStages * kStage];
 
   // workgroup -> (tree, head): consecutive ids on one XCD when the count
   // divides evenly, so the heads of one key head share an L2
@@ -90,6 +127,30 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
   // num_nodes = -1, has no rows)
   const int P = prefix_len[b] < 0 ? 0 : (prefix_len[b] > Pmax ? Pmax : prefix_len[b]);
   const int n = num_nodes[b] < 0 ? 0 : (num_nodes[b] > R ? R : num_nodes[b]);
+  const uint32_t ring = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)s_ring;
+
+  // Prefix block loads: load u (0..15) of a block covers rows 4(u%8) ..
+  // 4(u%8)+3 of the keys (u < 8) or values; lane L takes row 4(u%8) + L/16
+  // and fills physical chunk L%16, i.e. logical chunk (L%16) ^ (row%16).
+  // Waves 0..3 issue loads w, w+4, w+8, w+12 of every block.
+  const int64_t row_stride = (int64_t)Hkv * kD * 2;  // bytes between consecutive keys
+  const uint32_t pre_bytes = P > 0 ? (uint32_t)((int64_t)(P - 1) * row_stride + kRowBytes) : 0u;
+  const int32x4 rk = buffer_rsrc(k_cache + ((int64_t)b * Pmax * Hkv + g_kv) * kD, pre_bytes);
+  const int32x4 rv = buffer_rsrc(v_cache + ((int64_t)b * Pmax * Hkv + g_kv) * kD, pre_bytes);
+  const bool dma_wave = w < kDmaWaves;
+  auto issue_block = [&](int blk) {  // rows past P (also whole blocks past the prefix) read as zeros
+    if (!dma_wave) return;
+    const uint32_t slot = ring + (uint32_t)((blk % kStages) * kStage);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int u = w + kDmaWaves * i;
+      const int r = 4 * (u & 7) + (lane >> 4);
+      const int c = (lane & 15) ^ (r & 15);
+      const int64_t key = (int64_t)blk * kBlock + r;
+      const uint32_t voff = key < P ? (uint32_t)(key * row_stride + 16 * c) : pre_bytes;
+      lds_load16(slot + (u < 8 ? 0u : (uint32_t)kPart) + (uint32_t)(u & 7) * 1024u, voff, u < 8 ? rk : rv);
+    }
+  };
 
   // this lane's query row and its rotated dims as the B operand of S^T
   const int qr = w * 16 + lc;
@@ -128,122 +189,16 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
   float m_run = -INFINITY, l_run = 0.0f;
   const float scale = 1.0f / sqrtf((float)kD);
 
-  const int n_pre = (P + kBlock - 1) / kBlock, n_tree = (n + kBlock - 1) / kBlock;
-  const int nb = n_pre + n_tree;
-
-  // Staging (at least 256 threads): a block's keys are 512 chunks of 8 dims
-  // (two per thread), its values 128 quads of 4 keys x 8 dims (one per
-  // thread below 128), transposed into s_vt as 8-byte rows of 4 keys.
-  constexpr int kKChunks = kBlock * (kD / 8);
-  uint4 pk[2], pv[4];
-  auto fetch_prefix = [&](int blk) {  // global loads of a cached block into registers
-    const int base = blk * kBlock;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int it = tid + u * nt;
-      const int kk = it / (kD / 8), c = it - kk * (kD / 8);
-      pk[u] = make_uint4(0u, 0u, 0u, 0u);
-      if (it < kKChunks && base + kk < P)
-        pk[u] = *(const uint4*)(k_cache + (((int64_t)b * Pmax + base + kk) * Hkv + g_kv) * kD + 8 * c);
-    }
-    const int kq = tid / (kD / 8), c = tid - kq * (kD / 8);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int j = base + 4 * kq + r;
-      pv[r] = make_uint4(0u, 0u, 0u, 0u);
-      if (tid < kBlock / 4 * (kD / 8) && j < P)
-        pv[r] = *(const uint4*)(v_cache + (((int64_t)b * Pmax + j) * Hkv + g_kv) * kD + 8 * c);
-    }
-  };
-  auto put_values = [&](int buf) {  // pv (4 keys x 8 dims) -> s_vt, transposed
-    if (tid < kBlock / 4 * (kD / 8)) {
-      const int kq = tid / (kD / 8), c = tid - kq * (kD / 8);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        uint32_t hw[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const uint32_t word = (e >> 1) == 0 ? pv[r].x : (e >> 1) == 1 ? pv[r].y : (e >> 1) == 2 ? pv[r].z : pv[r].w;
-          hw[r] = (word >> (16 * (e & 1))) & 0xFFFFu;
-        }
-        *(uint2*)&s_vt[buf][(8 * c + e) * kVStride + 4 * kq] = make_uint2(hw[0] | (hw[1] << 16), hw[2] | (hw[3] << 16));
-      }
-    }
-  };
-  auto put_prefix = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int it = tid + u * nt;
-      const int kk = it / (kD / 8), c = it - kk * (kD / 8);
-      if (it < kKChunks) *(uint4*)&s_k[buf][kk * kKStride + 8 * c] = pk[u];
-    }
-    put_values(buf);
-  };
-  auto stage_tree = [&](int tb, int buf) {  // a block of tree rows, keys rotated
-    const int base = tb * kBlock;
-    if (tid < kBlock * (kD / 16)) {
-      const int kk = tid / (kD / 16), c = tid - kk * (kD / 16);  // key, chunks c and c + D/16
-      const int j = base + kk;
-      float a[8], bb[8];
-      if (j < n) {
-        const uint16_t* src = k_tree + (((int64_t)b * R + j) * Hkv + g_kv) * kD;
-        load8(src + 8 * c, a);
-        load8(src + kD / 2 + 8 * c, bb);
-        const int pos = P + pos_ids[(int64_t)b * R + j];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          float sn, cs;
-          rope_sincos(pos, 8 * c + e, log2_base, sn, cs);
-          const float x0 = a[e], x1 = bb[e];
-          a[e] = x0 * cs - x1 * sn;
-          bb[e] = x1 * cs + x0 * sn;
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) a[e] = bb[e] = 0.0f;
-      }
-      bf16x8 pa, pbb;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pa[e] = f2bf(a[e]);
-        pbb[e] = f2bf(bb[e]);
-      }
-      *(bf16x8*)&s_k[buf][kk * kKStride + 8 * c] = pa;
-      *(bf16x8*)&s_k[buf][kk * kKStride + kD / 2 + 8 * c] = pbb;
-    }
-    const int kq = tid / (kD / 8), c = tid - kq * (kD / 8);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int j = base + 4 * kq + r;
-      pv[r] = make_uint4(0u, 0u, 0u, 0u);
-      if (tid < kBlock / 4 * (kD / 8) && j < n)
-        pv[r] = *(const uint4*)(v_tree + (((int64_t)b * R + j) * Hkv + g_kv) * kD + 8 * c);
-    }
-    put_values(buf);
-  };
-
-  if (n_pre > 0) {
-    fetch_prefix(0);
-    put_prefix(0);
-  } else if (n_tree > 0) {
-    stage_tree(0, 0);
-  }
-  __syncthreads();
-  for (int blk = 0; blk < nb; ++blk) {
-    const int cur = blk & 1;
-    const bool tree = blk >= n_pre;
-    const int base = (tree ? blk - n_pre : blk) * kBlock;
-    const int lim = tree ? n : P;
-    const bool next_pre = blk + 1 < n_pre;
-    if (next_pre) fetch_prefix(blk + 1);  // in flight during this block's products
-
-    // S^T for keys 0..15 and 16..31 of the block
-    const __bf16* sk = s_k[cur];
+  // One block of the two products from the K and V parts at slot_off (a byte
+  // offset in s_ring); `tree` blocks take the mask, prefix blocks only the
+  // prefix bound.
+  auto consume = [&](uint32_t slot_off, int base, int lim, bool tree) {
+    const uint8_t* sk = s_ring + slot_off;
     floatx4 st0 = {0.0f, 0.0f, 0.0f, 0.0f}, st1 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int kc = 0; kc < kDSteps; ++kc) {
-      const bf16x8 a0 = *(const bf16x8*)&sk[lc * kKStride + 32 * kc + 8 * lg];
-      const bf16x8 a1 = *(const bf16x8*)&sk[(16 + lc) * kKStride + 32 * kc + 8 * lg];
+      const bf16x8 a0 = *(const bf16x8*)(sk + chunk_at(lc, 4 * kc + lg));
+      const bf16x8 a1 = *(const bf16x8*)(sk + chunk_at(16 + lc, 4 * kc + lg));
       st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[kc], st0, 0, 0, 0);
       st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qf[kc], st1, 0, 0, 0);
     }
@@ -276,25 +231,85 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
     }
     m_run = m_new;
     l_run = l_run * alpha + ps;
-    const __bf16* svt = s_vt[cur];
+    // V^T for output tile t: a transposing read gives lane (lg, lc) dims
+    // 16t + lc of keys 4lg + e (first read) and 16 + 4lg + e (second); the
+    // addressing lane (lg, 4e + i) points at dims 16t + 4i of that key
+    const uint32_t vbase = ring + slot_off + (uint32_t)kPart;
+    const int vr0 = 4 * lg + (lc >> 2), vr1 = 16 + 4 * lg + (lc >> 2), vq = lc & 3;
 #pragma unroll
     for (int t = 0; t < kDTiles; ++t) {
       o[t] *= alpha;
-      const __bf16* vrow = &svt[(16 * t + lc) * kVStride];
-      bf16x8 a;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        a[e] = vrow[4 * lg + e];
-        a[4 + e] = vrow[16 + 4 * lg + e];
-      }
+      const int cc = 2 * t + (vq >> 1);
+      const uint32_t half = (uint32_t)(vq & 1) * 8u;
+      const bf16x4 lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+          (lds_bf16x4*)(uintptr_t)(vbase + chunk_at(vr0, cc) + half));
+      const bf16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+          (lds_bf16x4*)(uintptr_t)(vbase + chunk_at(vr1, cc) + half));
+      const bf16x8 a = {lo4[0], lo4[1], lo4[2], lo4[3], hi4[0], hi4[1], hi4[2], hi4[3]};
       o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[t], 0, 0, 0);
     }
-    // stage the next block into the other buffer (its last readers passed
-    // the previous barrier)
-    if (blk + 1 < nb) {
-      if (next_pre) put_prefix(cur ^ 1);
-      else stage_tree(blk + 1 - n_pre, cur ^ 1);
+  };
+
+  // the cached prefix: a ring of kStages blocks, kStages - 1 in flight
+  const int n_pre = (P + kBlock - 1) / kBlock, n_tree = (n + kBlock - 1) / kBlock;
+#pragma unroll
+  for (int blk = 0; blk < kStages - 1; ++blk) issue_block(blk);
+  for (int blk = 0; blk < n_pre; ++blk) {
+    // this wave's loads of block blk are done once at most the loads of the
+    // kStages - 2 later blocks (4 each) are outstanding; the barrier makes every
+    // wave's visible, and frees the slot the next issue overwrites
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(4 * (kStages - 2)) : "memory");
+    __syncthreads();
+    issue_block(blk + kStages - 1);
+    consume((uint32_t)((blk % kStages) * kStage), blk * kBlock, P, false);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  // the tree's rows: keys rotated by their positions, values as they are,
+  // staged through registers into slot 0
+  for (int tb = 0; tb < n_tree; ++tb) {
+    const int base = tb * kBlock;
+    uint8_t* sk = s_ring;
+    for (int it = tid; it < kBlock * (kD / 16); it += nt) {
+      const int kk = it / (kD / 16), c = it - kk * (kD / 16);  // key, chunks c and c + D/16
+      const int j = base + kk;
+      float a[8], bb[8];
+      if (j < n) {
+        const uint16_t* src = k_tree + (((int64_t)b * R + j) * Hkv + g_kv) * kD;
+        load8(src + 8 * c, a);
+        load8(src + kD / 2 + 8 * c, bb);
+        const int pos = P + pos_ids[(int64_t)b * R + j];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float sn, cs;
+          rope_sincos(pos, 8 * c + e, log2_base, sn, cs);
+          const float x0 = a[e], x1 = bb[e];
+          a[e] = x0 * cs - x1 * sn;
+          bb[e] = x1 * cs + x0 * sn;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a[e] = bb[e] = 0.0f;
+      }
+      bf16x8 pa, pbb;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        pa[e] = f2bf(a[e]);
+        pbb[e] = f2bf(bb[e]);
+      }
+      *(bf16x8*)(sk + chunk_at(kk, c)) = pa;
+      *(bf16x8*)(sk + chunk_at(kk, c + kD / 16)) = pbb;
     }
+    for (int it = tid; it < kBlock * (kD / 8); it += nt) {
+      const int kk = it / (kD / 8), c = it - kk * (kD / 8);
+      const int j = base + kk;
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      if (j < n) v = *(const uint4*)(v_tree + (((int64_t)b * R + j) * Hkv + g_kv) * kD + 8 * c);
+      *(uint4*)(sk + kPart + chunk_at(kk, c)) = v;
+    }
+    __syncthreads();
+    consume(0u, base, n, true);
     __syncthreads();
   }
 
@@ -329,6 +344,8 @@ extern "C" fc_status fc_tree_attention(const uint16_t* q, const uint16_t* k_tree
   const uintptr_t al = (uintptr_t)q | (uintptr_t)k_tree | (uintptr_t)v_tree | (uintptr_t)out |
                        (Pmax > 0 ? ((uintptr_t)k_cache | (uintptr_t)v_cache) : 0);
   if (al & 15) return FC_ERR_INVALID;
+  // the prefix of one (tree, key head) is read with 32-bit byte offsets
+  if ((int64_t)Pmax * Hkv * D * 2 >= (int64_t)1 << 32) return FC_ERR_UNSUPPORTED;
   const int rows_waves = (R + 15) / 16;
   const int waves = rows_waves < 4 ? 4 : rows_waves;  // at least 256 threads stage a block
   const dim3 grid((uint32_t)B * (uint32_t)H), block(waves * fc::kWave);
