@@ -281,6 +281,27 @@ def main():
     phase_ms = {name: float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)]))
                 for j, name in enumerate(("fc_retrieve", "fc_build_tree", "fc_verify_accept"))}
 
+    # single-query latency (B = 1): one query's retrieve + tree + accept on
+    # its own, event-timed, over the batch's first queries
+    r1 = fc.retrieve_outputs(1, len(stores), k, m, dev)
+    rws1 = torch.empty(max(fc.fc_retrieve_workspace_bytes(1, len(stores), p["n_max"], p["n_min"], k, m), 1),
+                       dtype=torch.uint8, device=dev)
+    t1o = fc.tree_outputs(1, c, dev)
+    tws1 = torch.empty(max(fc.fc_build_tree_workspace_bytes(1), 1), dtype=torch.uint8, device=dev)
+    a1o = fc.accept_outputs(1, m, dev)
+    lat = []
+    for qi in range(min(64, B) + 3):
+        cq, tq = ctx[qi % B:qi % B + 1], target[qi % B:qi % B + 1]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fc.fc_retrieve(stores, cq, n_max=p["n_max"], n_min=p["n_min"], k=k, m=m, out=r1, workspace=rws1)
+        fc.fc_build_tree(r1["taken"], r1["cont_len"], r1["cont_tok"], cq, c=c, alpha=alpha, out=t1o, workspace=tws1)
+        fc.fc_verify_accept(t1o, tq, m=m, out=a1o)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if qi >= 3:  # the first three warm up
+            lat.append(e0.elapsed_time(e1))
+
     # outputs of the batch, for the byte model and the acceptance statistic
     taken = rout["taken"].cpu().numpy()
     cont_len = rout["cont_len"].cpu().numpy()
@@ -329,6 +350,8 @@ def main():
         "roofline_by_entry": roofs,
         "cpu_baseline": cpu,
         "phases_ms": phase_ms,
+        "single_query_latency_ms": {"median": float(np.median(lat)), "p90": float(np.percentile(lat, 90)),
+                                    "queries": len(lat)},
         "ms_per_step_with_phase_events": float(sum(phase_ms.values())),
         "algorithmic_bytes_per_step": nb,
         "step_GBps_algorithmic": total_bytes / (ms_step * 1e-3) / 1e9,
