@@ -456,11 +456,39 @@ fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_
  *   outputs for n_streams.
  * Limits: 1 <= ctx_len <= 64 (also fc_retrieve's n_max <= ctx_len is the
  * caller's choice), 1 <= lru <= 64, truth_stride >= truth_len.
- * fc_replay_init sets pos = ctx_len, empties every LRU and zeroes the
- * counters.  fc_replay_run runs steps first_step .. first_step + n_steps - 1
- * (their history rows), first_step + n_steps <= max_steps; read `live`
- * between calls to stop once it is 0.  Errors of the calls it makes are
- * returned as they come.
+ *
+ * Optionally the CACHE of Section IV-B with Alg. 1's cache branch
+ * (cache_l >= 0) and Alg. 1's retrieval-timing control (missing != 0:
+ * contexts whose datastore retrieval found nothing are not retrieved again;
+ * skip_tok >= 0: a context ending with skip_tok is retrieved only when the
+ * step's draw skip_draws[step][b] is below skip_thr).  Per step, for a live
+ * stream whose CACHE holds at least cache_l sequences the context is first
+ * searched in the CACHE's text (fc_cache_retrieve, results in the c_*
+ * arrays, row b); a non-empty result is "served": its tree is built from
+ * it alone (one source, weight 1) and the datastores are not touched.
+ * Otherwise the missing table and then the skip gate may skip the context
+ * (its tree is the bare root read from retrieval row n_streams * lru, which
+ * fc_replay_init empties), else the LRU step above runs and, with the
+ * missing table on, a context whose result is empty is added to it.  After
+ * acceptance the CACHE gets the context plus the accepted draft tokens
+ * (when the draft contributed any) and every completed chunk of
+ * cache_every output tokens; a sequence longer than cache_cap keeps its
+ * last cache_cap tokens, and the oldest sequences go when the text (the
+ * sequences joined by 0 tokens) would outgrow cache_cap.
+ * Extra device arrays (caller-owned): ctext [n_streams][cache_cap], clen,
+ * seq_head, seq_count, chunks, served, rows_cache, state [n_streams],
+ * seq_len [n_streams][max_seqs] (max_seqs >= (cache_cap + 1) / 2 + 1); CACHE
+ * retrieval outputs (S = 1) and a second set of tree outputs for
+ * n_streams; miss_key [n_streams][miss_cap][ctx_len], miss_used
+ * [n_streams][miss_cap] (miss_cap a power of two above max_steps), m_skips,
+ * g_skips [n_streams]; skip_draws [max_steps][n_streams].  With the
+ * control on, the retrieval outputs need n_streams * lru + 1 rows.
+ *
+ * fc_replay_init sets pos = ctx_len, empties every LRU, CACHE and missing
+ * table and zeroes the counters.  fc_replay_run runs steps first_step ..
+ * first_step + n_steps - 1 (their history rows), first_step + n_steps <=
+ * max_steps; read `live` between calls to stop once it is 0.  Errors of the
+ * calls it makes are returned as they come.
  */
 typedef struct fc_replay {
   const uint16_t* truth;
@@ -505,6 +533,44 @@ typedef struct fc_replay {
   int32_t* accept_len;
   int32_t* accept_tok;
   int32_t* last_node;
+  /* CACHE (cache_l < 0: off) */
+  int32_t cache_l;
+  int32_t cache_every;
+  int32_t cache_cap;
+  int32_t max_seqs;
+  uint16_t* ctext;
+  int32_t* clen;
+  int32_t* seq_len;
+  int32_t* seq_head;
+  int32_t* seq_count;
+  int32_t* chunks;
+  int32_t* served;
+  int32_t* rows_cache;
+  int32_t* state;
+  int32_t* c_match_n;
+  uint32_t* c_range_lo;
+  uint32_t* c_range_cnt;
+  int32_t* c_taken;
+  uint32_t* c_cont_pos;
+  uint8_t* c_cont_src;
+  uint8_t* c_cont_len;
+  uint16_t* c_cont_tok;
+  int32_t* c_num_nodes;
+  int32_t* c_node_tok;
+  int32_t* c_parent;
+  uint32_t* c_weight;
+  int32_t* c_pos_ids;
+  int32_t* c_mask;
+  /* Alg. 1's retrieval-timing control */
+  int32_t missing;
+  int32_t miss_cap;
+  uint16_t* miss_key;
+  uint8_t* miss_used;
+  int32_t* m_skips;
+  int32_t skip_tok;
+  uint32_t skip_thr;
+  const int32_t* skip_draws;
+  int32_t* g_skips;
 } fc_replay;
 
 fc_status fc_replay_init(fc_replay* r, hipStream_t stream);

@@ -76,7 +76,15 @@ class FcReplay(ctypes.Structure):
         ("retrieve_ws_bytes", ctypes.c_size_t)] + [
         (f, _P) for f in ("num_nodes", "node_tok", "parent", "weight", "pos_ids", "mask", "tree_ws")] + [
         ("tree_ws_bytes", ctypes.c_size_t)] + [
-        (f, _P) for f in ("target", "accept_len", "accept_tok", "last_node")]
+        (f, _P) for f in ("target", "accept_len", "accept_tok", "last_node")] + [
+        (f, ctypes.c_int32) for f in ("cache_l", "cache_every", "cache_cap", "max_seqs")] + [
+        (f, _P) for f in ("ctext", "clen", "seq_len", "seq_head", "seq_count", "chunks", "served", "rows_cache",
+                          "state", "c_match_n", "c_range_lo", "c_range_cnt", "c_taken", "c_cont_pos", "c_cont_src",
+                          "c_cont_len", "c_cont_tok", "c_num_nodes", "c_node_tok", "c_parent", "c_weight",
+                          "c_pos_ids", "c_mask")] + [
+        ("missing", ctypes.c_int32), ("miss_cap", ctypes.c_int32), ("miss_key", _P), ("miss_used", _P),
+        ("m_skips", _P), ("skip_tok", ctypes.c_int32), ("skip_thr", ctypes.c_uint32), ("skip_draws", _P),
+        ("g_skips", _P)]
 
 
 @functools.lru_cache(maxsize=1)
@@ -482,10 +490,14 @@ def fc_targets_from_truth(truth: torch.Tensor, start: torch.Tensor, tree: dict, 
 class ReplayEngine:
     """Device-resident decode-trace replay (fc_replay_init / fc_replay_run):
     owns the device state for `truth` (uint16 [n_streams][length] on the
-    GPU) over `stores`; run() replays until every stream is finished."""
+    GPU) over `stores`; run() replays until every stream is finished.  With
+    cache_l, the CACHE of Section IV-B comes first (Alg. 1's cache branch);
+    missing and skip_tok switch on Alg. 1's retrieval-timing control, with
+    the gate's draws from skip_draws (int [>= max_steps][n_streams])."""
 
     def __init__(self, stores, truth: torch.Tensor, n_max=16, n_min=2, k=5000, m=10, c=64, alpha=(1, 1), lru=32,
-                 ctx_len=16, max_steps=512, chunk=16):
+                 ctx_len=16, max_steps=512, chunk=16, cache_l=None, cache_every=20, cache_cap=FC_MAX_CACHE_TOKENS,
+                 missing=False, skip_tok=None, skip_p=0.5, skip_draws=None):
         if truth.dtype != torch.uint16 or truth.dim() != 2 or not truth.is_contiguous():
             raise ValueError("truth must be a contiguous 2-D uint16 tensor")
         dev = truth.device
@@ -498,10 +510,35 @@ class ReplayEngine:
                       lru_used=_empty((n, lru), i32, dev), lru_count=_empty(n, i32, dev), hits=_empty(n, i32, dev),
                       lookups=_empty(n, i32, dev), ctx=_empty((n, ctx_len), torch.uint16, dev),
                       rows_retrieve=_empty(n, i32, dev), rows_tree=_empty(n, i32, dev), live=_empty(1, i32, dev),
-                      history=_empty((max_steps, n), i32, dev), target=_empty((n, c + 1), i32, dev))
-        self.t.update(retrieve_outputs(n * lru, S, k, m, dev))
+                      history=_empty((max_steps, n), i32, dev), target=_empty((n, c + 1), i32, dev),
+                      state=_empty(n, i32, dev))
+        # the LRU slots plus one empty row (the bare root of skipped contexts)
+        self.t.update(retrieve_outputs(n * lru + 1, S, k, m, dev))
         self.t.update(tree_outputs(n, c, dev))
         self.t.update(accept_outputs(n, m, dev))
+        self.cache_on = cache_l is not None
+        self.control_on = bool(missing) or skip_tok is not None
+        if self.cache_on:
+            max_seqs = (cache_cap + 1) // 2 + 1
+            self.t.update(ctext=_empty((n, cache_cap), torch.uint16, dev), clen=_empty(n, i32, dev),
+                          seq_len=_empty((n, max_seqs), i32, dev), seq_head=_empty(n, i32, dev),
+                          seq_count=_empty(n, i32, dev), chunks=_empty(n, i32, dev), served=_empty(n, i32, dev),
+                          rows_cache=_empty(n, i32, dev))
+            self.t.update({"c_" + f: v for f, v in retrieve_outputs(n, 1, k, m, dev).items()})
+            self.t.update({"c_" + f: v for f, v in tree_outputs(n, c, dev).items()})
+        miss_cap = 64
+        while miss_cap <= max_steps:
+            miss_cap *= 2
+        if missing:
+            self.t.update(miss_key=_empty((n, miss_cap, ctx_len), torch.uint16, dev),
+                          miss_used=_empty((n, miss_cap), torch.uint8, dev))
+        if self.control_on:
+            self.t.update(m_skips=_empty(n, i32, dev), g_skips=_empty(n, i32, dev))
+        if skip_tok is not None:
+            d = np.ascontiguousarray(np.asarray(skip_draws)[:max_steps], dtype=np.int32)
+            if d.shape != (max_steps, n):
+                raise ValueError("skip_draws must hold max_steps rows of n_streams draws")
+            self.t["skip_draws"] = torch.from_numpy(d).to(dev)
         rp = FcRetrieveParams(n_max, n_min, k, m)
         self.rws = _empty(max(int(lib().fc_retrieve_workspace_bytes(n, S, rp)), 1), torch.uint8, dev)
         self.tws = _empty(max(fc_build_tree_workspace_bytes(n), 1), torch.uint8, dev)
@@ -514,13 +551,19 @@ class ReplayEngine:
             setattr(r, f, v.data_ptr())
         r.retrieve_ws, r.retrieve_ws_bytes = self.rws.data_ptr(), self.rws.numel()
         r.tree_ws, r.tree_ws_bytes = self.tws.data_ptr(), self.tws.numel()
+        r.cache_l = -1 if cache_l is None else int(cache_l)
+        r.cache_every, r.cache_cap = int(cache_every), int(cache_cap)
+        r.max_seqs = (int(cache_cap) + 1) // 2 + 1
+        r.missing, r.miss_cap = (1 if missing else 0), miss_cap
+        r.skip_tok = -1 if skip_tok is None else int(skip_tok)
+        r.skip_thr = int(skip_p * 2 ** 31)
         self.r, self.max_steps = r, max_steps
 
     def run(self, limit: int | None = None, stream=None) -> dict:
         """Replays from the start for at most `limit` (default max_steps)
         steps; returns the per-step accepted lengths ([steps][n_streams], -1
-        for finished streams), LRU hits and lookups, final positions and the
-        mean accepted length."""
+        for finished streams), LRU hits and lookups, final positions, the
+        mean accepted length and the CACHE / timing-control counters."""
         st = _stream(stream)
         cap = self.max_steps if limit is None else min(limit, self.max_steps)
         _check("fc_replay_init", lib().fc_replay_init(ctypes.byref(self.r), st))
@@ -533,11 +576,14 @@ class ReplayEngine:
             if int(self.t["live"].item()) == 0:
                 break
         hist = self.t["history"][:step].cpu().numpy().astype(np.int64)
-        live_rows = (hist >= 0).any(axis=1)
-        steps = int(live_rows.sum())
+        steps = int((hist >= 0).any(axis=1).sum())
         acc = hist[:steps]
         live = acc >= 0
-        return dict(accept=acc, hits=self.t["hits"].cpu().numpy().astype(np.int64),
-                    lookups=self.t["lookups"].cpu().numpy().astype(np.int64),
-                    pos=self.t["pos"].cpu().numpy().astype(np.int64),
-                    acc_len=float(acc[live].sum() / max(live.sum(), 1)), steps=steps)
+        nn = self.r.n_streams
+
+        def host(name):
+            return self.t[name].cpu().numpy().astype(np.int64) if name in self.t else np.zeros(nn, np.int64)
+
+        return dict(accept=acc, hits=host("hits"), lookups=host("lookups"), pos=host("pos"),
+                    acc_len=float(acc[live].sum() / max(live.sum(), 1)), steps=steps, cache_served=host("served"),
+                    missing_skips=host("m_skips"), gate_skips=host("g_skips"))

@@ -6,19 +6,25 @@
 // context up in an LRU of its recent retrievals, retrieves on a miss
 // (Section III-A over the stores in priority order), builds its draft tree
 // (Section IV-D), takes the true next tokens as the target model's outputs,
-// accepts greedily and advances by the accepted length.
+// accepts greedily and advances by the accepted length.  Optionally the
+// CACHE of Section IV-B comes first (Alg. 1's cache branch) and Alg. 1's
+// retrieval-timing control (missing table, skip gate) may skip a retrieval.
 //
 // Everything a step decides lives on the GPU, so a step is a fixed chain of
 // launches on one stream with no host round trip:
-//   k_replay_prepare   one wave per stream: the context from the stream, the
-//                      LRU probe (keys compared by the lanes, least recent
-//                      slot by a wave minimum), the row maps;
-//   fc_retrieve        every stream, misses into their LRU slot (hits and
-//                      finished streams have no row and are skipped);
-//   fc_build_tree      every live stream from its slot;
+//   k_replay_context   (CACHE on) the context and the CACHE row map;
+//   fc_cache_retrieve  (CACHE on) streams whose CACHE is old enough;
+//   k_replay_decide    one wave per stream: served by the CACHE, else the
+//                      missing table and the skip gate, else the LRU probe
+//                      (keys compared by the lanes, the least recent slot
+//                      by a wave minimum); the row maps;
+//   fc_retrieve        misses into their LRU slot (everything else skipped);
+//   k_replay_missing   (table on) empty results enter the missing table;
+//   fc_build_tree      from the datastore slots (and, CACHE on, a second one
+//                      from the CACHE results, merged by k_replay_merge);
 //   fc_targets_from_truth, fc_verify_accept;
-//   k_replay_advance   one thread per stream: position += accepted length,
-//                      the step's history row and the live count.
+//   k_replay_advance   position += accepted length, the step's history row,
+//                      the live count and (CACHE on) the CACHE additions.
 // The LRU keeps the exact semantics of an ordered map: slots fill in order,
 // a hit becomes most recent, a miss in a full table replaces the least
 // recently used slot (last-use steps are distinct per stream).
@@ -34,20 +40,92 @@ namespace {
 constexpr int kPrepThreads = 256;
 constexpr int kStreamsPerBlock = kPrepThreads / fc::kWave;
 
-__global__ void __launch_bounds__(256) k_replay_init(int32_t n, int32_t L, int32_t* __restrict__ pos,
-                                                     int32_t* __restrict__ lru_count, int32_t* __restrict__ hits,
-                                                     int32_t* __restrict__ lookups, int32_t* __restrict__ live,
-                                                     int32_t truth_len) {
+enum StreamState : int32_t { kNeed = 0, kServed = 1, kSkipped = 2, kDone = -1 };
+
+__device__ __forceinline__ bool cache_on(const fc_replay& r) { return r.cache_l >= 0; }
+__device__ __forceinline__ bool control_on(const fc_replay& r) { return r.missing || r.skip_tok >= 0; }
+
+__global__ void __launch_bounds__(256) k_replay_init(fc_replay r) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b == 0) *live = L < truth_len ? n : 0;
-  if (b >= n) return;
-  pos[b] = L;
-  lru_count[b] = 0;
-  hits[b] = 0;
-  lookups[b] = 0;
+  if (b == 0) *r.live = r.ctx_len < r.truth_len ? r.n_streams : 0;
+  if (b >= r.n_streams) return;
+  r.pos[b] = r.ctx_len;
+  r.lru_count[b] = 0;
+  r.hits[b] = 0;
+  r.lookups[b] = 0;
+  if (cache_on(r)) {
+    r.clen[b] = 0;
+    r.seq_head[b] = 0;
+    r.seq_count[b] = 0;
+    r.chunks[b] = 0;
+    r.served[b] = 0;
+  }
+  if (control_on(r)) {
+    r.m_skips[b] = 0;
+    r.g_skips[b] = 0;
+  }
 }
 
-__global__ void __launch_bounds__(kPrepThreads) k_replay_prepare(fc_replay r, int32_t step) {
+// empties the missing tables and the skipped contexts' retrieval row
+__global__ void __launch_bounds__(256) k_replay_init_tables(fc_replay r, int32_t S) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < S) r.taken[(int64_t)r.n_streams * r.lru * S + i] = 0;
+  if (r.missing && i < (int64_t)r.n_streams * r.miss_cap) r.miss_used[i] = 0;
+}
+
+// The context (the L tokens before the position) of every live stream, and
+// (CACHE on) which streams search their CACHE this step.
+__global__ void __launch_bounds__(256) k_replay_context(fc_replay r) {
+  const int b = blockIdx.x;
+  const int L = r.ctx_len;
+  const int p = r.pos[b];
+  const bool live = p < r.truth_len;
+  if (threadIdx.x == 0) r.rows_cache[b] = (live && r.seq_count[b] >= r.cache_l) ? b : -1;
+  if (live && (int)threadIdx.x < L)
+    r.ctx[(int64_t)b * L + threadIdx.x] = r.truth[(int64_t)b * r.truth_stride + (p - L) + threadIdx.x];
+}
+
+__device__ __forceinline__ uint32_t ctx_hash(const uint16_t* c, int L) {
+  uint32_t h = 2166136261u;  // FNV-1a over the tokens
+  for (int t = 0; t < L; ++t) {
+    h = (h ^ (uint32_t)(c[t] & 0xFF)) * 16777619u;
+    h = (h ^ (uint32_t)(c[t] >> 8)) * 16777619u;
+  }
+  return h;
+}
+
+// Missing table of stream b: open addressing over miss_cap slots, probed 64
+// at a time by the wave.  Returns the slot holding ctx, or -1 - (first free
+// slot) when it is absent.  The table never fills (miss_cap > max_steps >=
+// insertions), so the probe ends.
+__device__ int miss_find(const fc_replay& r, int b, const uint16_t* ctx) {
+  const int L = r.ctx_len, lane = fc::lane_id();
+  const uint32_t mask = (uint32_t)r.miss_cap - 1u;
+  const uint32_t h = ctx_hash(ctx, L);
+  const uint16_t* keys = r.miss_key + (int64_t)b * r.miss_cap * L;
+  const uint8_t* used = r.miss_used + (int64_t)b * r.miss_cap;
+  for (uint32_t base = 0; base < (uint32_t)r.miss_cap; base += fc::kWave) {
+    const uint32_t slot = (h + base + (uint32_t)lane) & mask;
+    const bool u = used[slot] != 0;
+    bool eq = u;
+    if (u) {
+      const uint16_t* key = keys + (int64_t)slot * L;
+      for (int t = 0; t < L; ++t) eq &= key[t] == ctx[t];
+    }
+    const uint64_t hit = fc::ballot(eq), empty = fc::ballot(!u);
+    // the first slot in probe order that matches or is empty decides
+    const uint64_t any = hit | empty;
+    if (any) {
+      const int first = __builtin_ctzll(any);
+      const int s = __shfl((int)slot, first);
+      return ((hit >> first) & 1ull) ? s : -1 - s;
+    }
+  }
+  return -1 - (int)(h & mask);  // not reached
+}
+
+// One wave per stream: the step's decision and its row maps.
+__global__ void __launch_bounds__(kPrepThreads) k_replay_decide(fc_replay r, int32_t step, int32_t S) {
   const int lane = fc::lane_id();
   const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
   if (blockIdx.x == 0 && threadIdx.x == 0) *r.live = 0;
@@ -58,15 +136,47 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_prepare(fc_replay r, in
     if (lane == 0) {
       r.rows_retrieve[b] = -1;
       r.rows_tree[b] = -1;
+      if (cache_on(r)) r.rows_cache[b] = -1;
+      r.state[b] = kDone;
     }
     return;
   }
-  // the context: the L tokens before the position
   const uint16_t* src = r.truth + (int64_t)b * r.truth_stride + (p - L);
   uint16_t* ctx = r.ctx + (int64_t)b * L;
   const uint16_t tok = lane < L ? src[lane] : (uint16_t)0;
   if (lane < L) ctx[lane] = tok;
-  // probe: lane e compares slot e's key with the context
+  // Alg. 1: the CACHE first
+  if (cache_on(r)) {
+    const bool served = r.rows_cache[b] >= 0 && r.c_taken[b] > 0;
+    if (served) {
+      if (lane == 0) {
+        r.rows_retrieve[b] = -1;
+        r.rows_tree[b] = -1;
+        r.state[b] = kServed;
+      }
+      return;
+    }
+    if (lane == 0) r.rows_cache[b] = -1;
+  }
+  // the timing control: the missing table, then the skip gate
+  bool skip = false;
+  if (r.missing && miss_find(r, b, src) >= 0) {
+    skip = true;
+    if (lane == 0) r.m_skips[b] += 1;
+  } else if (r.skip_tok >= 0 && (int)src[L - 1] == r.skip_tok &&
+             !((uint32_t)r.skip_draws[(int64_t)step * r.n_streams + b] < r.skip_thr)) {
+    skip = true;
+    if (lane == 0) r.g_skips[b] += 1;
+  }
+  if (skip) {
+    if (lane == 0) {
+      r.rows_retrieve[b] = -1;
+      r.rows_tree[b] = r.n_streams * lru;  // the empty row: a bare root
+      r.state[b] = kSkipped;
+    }
+    return;
+  }
+  // the LRU probe: lane e compares slot e's key with the context
   const int count = r.lru_count[b];
   const uint16_t* keys = r.lru_key + (int64_t)b * lru * L;
   int32_t* used = r.lru_used + (int64_t)b * lru;
@@ -105,63 +215,233 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_prepare(fc_replay r, in
     const int row = b * lru + slot;
     r.rows_retrieve[b] = hit_mask ? -1 : row;
     r.rows_tree[b] = row;
+    r.state[b] = kNeed;
   }
+  (void)S;
 }
 
-__global__ void __launch_bounds__(256) k_replay_advance(fc_replay r, int32_t step) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+// One wave per stream: a looked-up context whose result is empty enters the
+// missing table.
+__global__ void __launch_bounds__(kPrepThreads) k_replay_missing(fc_replay r, int32_t S) {
+  const int lane = fc::lane_id();
+  const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
+  if (b >= r.n_streams || r.state[b] != kNeed) return;
+  const int row = r.rows_tree[b];
+  int tot = 0;
+  for (int s = 0; s < S; ++s) tot += r.taken[(int64_t)row * S + s];
+  if (tot != 0) return;
+  const int L = r.ctx_len;
+  const uint16_t* ctx = r.ctx + (int64_t)b * L;
+  const int f = miss_find(r, b, ctx);
+  if (f >= 0) return;
+  const int slot = -1 - f;
+  if (lane < L) r.miss_key[((int64_t)b * r.miss_cap + slot) * L + lane] = ctx[lane];
+  if (lane == 0) r.miss_used[(int64_t)b * r.miss_cap + slot] = 1;
+}
+
+// One workgroup per stream: a served stream's tree comes from the CACHE's.
+__global__ void __launch_bounds__(256) k_replay_merge(fc_replay r, int32_t R) {
+  const int b = blockIdx.x;
+  if (r.state[b] != kServed) return;
+  const int64_t o = (int64_t)b * R;
+  for (int i = threadIdx.x; i < R; i += blockDim.x) {
+    r.node_tok[o + i] = r.c_node_tok[o + i];
+    r.parent[o + i] = r.c_parent[o + i];
+    r.weight[o + i] = r.c_weight[o + i];
+    r.pos_ids[o + i] = r.c_pos_ids[o + i];
+  }
+  const int64_t mo = (int64_t)b * R * R;
+  for (int i = threadIdx.x; i < R * R; i += blockDim.x) r.mask[mo + i] = r.c_mask[mo + i];
+  if (threadIdx.x == 0) r.num_nodes[b] = r.c_num_nodes[b];
+}
+
+// A stream's CACHE bookkeeping, held in registers (the same in every lane)
+// while one wave adds its sequences.
+struct CacheState {
+  int len, head, cnt;
+};
+
+// Adds seq[0 .. len) to stream b's CACHE (one wave): the sequence keeps its
+// last cache_cap tokens; the oldest sequences go while the text, the
+// sequences joined by 0, would be longer than cache_cap.  Lane 0 keeps the
+// ring of sequence lengths; a workgroup fence at the end makes this
+// addition's writes visible to every lane before the next one reads them.
+__device__ void cache_add(const fc_replay& r, int b, CacheState& st, const uint16_t* seq, int len) {
+  const int lane = fc::lane_id();
+  const int cap = r.cache_cap;
+  if (len > cap) {
+    seq += len - cap;
+    len = cap;
+  }
+  if (len <= 0) return;
+  uint16_t* text = r.ctext + (int64_t)b * cap;
+  int* lens = r.seq_len + (int64_t)b * r.max_seqs;
+  const int old = st.len;
+  const int total = old + (st.cnt > 0 ? 1 : 0) + len;
+  int cut = 0;
+  while (total - cut > cap) {  // only old sequences go: the new one fits alone
+    cut += lens[st.head] + 1;
+    st.head = st.head + 1 == r.max_seqs ? 0 : st.head + 1;
+    --st.cnt;
+  }
+  const int keep = old - cut;  // -1 when every old sequence went (with the separator)
+  if (cut > 0 && keep > 0) {
+    // move the kept text to the front, 64 tokens a pass in increasing order
+    // (a pass's loads complete before its stores, and later passes read
+    // above what earlier ones wrote)
+    for (int i = 0; i < keep; i += fc::kWave) {
+      const int j = i + lane;
+      const uint16_t v = j < keep ? text[cut + j] : (uint16_t)0;
+      if (j < keep) text[j] = v;
+    }
+  }
+  const int start = keep > 0 ? keep + 1 : 0;
+  if (keep > 0 && lane == 0) text[keep] = 0;
+  for (int i = lane; i < len; i += fc::kWave) text[start + i] = seq[i];
+  if (lane == 0) lens[(st.head + st.cnt) % r.max_seqs] = len;
+  st.cnt += 1;
+  st.len = start + len;
+  __threadfence_block();
+}
+
+// One wave per stream: the history row, the new position, the live count
+// and (CACHE on) the CACHE additions of this step.
+__global__ void __launch_bounds__(kPrepThreads) k_replay_advance(fc_replay r, int32_t step) {
+  const int lane = fc::lane_id();
+  const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
   if (b >= r.n_streams) return;
   int32_t* hist = r.history + (int64_t)step * r.n_streams;
   const int p = r.pos[b];
-  if (p >= r.truth_len) {
-    hist[b] = -1;
+  const int tlen = r.truth_len, L = r.ctx_len;
+  if (p >= tlen) {
+    if (lane == 0) hist[b] = -1;
     return;
   }
   const int a = r.accept_len[b];
-  hist[b] = a;
-  r.pos[b] = p + a;
-  if (p + a < r.truth_len) atomicAdd(r.live, 1);
+  const int np = p + a;
+  if (cache_on(r)) {
+    const int R = r.tp.c + 1;
+    const uint16_t* row = r.truth + (int64_t)b * r.truth_stride;
+    if (lane == 0 && r.state[b] == kServed) r.served[b] += 1;
+    const int last = r.last_node[b];
+    const int depth = (last >= 0 && last < R) ? r.pos_ids[(int64_t)b * R + last] : 0;
+    CacheState st = {r.clen[b], r.seq_head[b], r.seq_count[b]};
+    if (depth >= 1) {  // a verified draft: the context and its accepted tokens
+      const int end = p + depth < tlen ? p + depth : tlen;
+      cache_add(r, b, st, row + (p - L), end - (p - L));
+    }
+    int ch = r.chunks[b];
+    const int lim = np < tlen ? np : tlen;
+    while (L + r.cache_every * (ch + 1) <= lim) {  // every completed output chunk
+      cache_add(r, b, st, row + L + r.cache_every * ch, r.cache_every);
+      ++ch;
+    }
+    if (lane == 0) {
+      r.chunks[b] = ch;
+      r.clen[b] = st.len;
+      r.seq_head[b] = st.head;
+      r.seq_count[b] = st.cnt;
+    }
+  }
+  if (lane == 0) {
+    hist[b] = a;
+    r.pos[b] = np;
+    if (np < tlen) atomicAdd(r.live, 1);
+  }
+}
+
+fc_status check_replay(const fc_replay* r) {
+  if (!r || r->n_streams < 1 || r->ctx_len < 1 || r->ctx_len > fc::kWave || r->lru < 1 || r->lru > fc::kWave)
+    return FC_ERR_INVALID;
+  if (r->truth_len < 0 || r->truth_stride < r->truth_len || !r->truth || r->max_steps < 0) return FC_ERR_INVALID;
+  if ((int64_t)r->n_streams * r->lru + 1 > 0x7FFFFFFF) return FC_ERR_INVALID;
+  if (!r->pos || !r->lru_key || !r->lru_used || !r->lru_count || !r->hits || !r->lookups || !r->ctx ||
+      !r->rows_retrieve || !r->rows_tree || !r->live || !r->history || !r->taken || !r->state)
+    return FC_ERR_INVALID;
+  if (r->cache_l >= 0) {
+    if (r->cache_every < 1 || r->cache_cap < 1 || r->cache_cap > FC_MAX_CACHE_TOKENS ||
+        r->max_seqs < (r->cache_cap + 1) / 2 + 1)
+      return FC_ERR_INVALID;
+    if (!r->ctext || !r->clen || !r->seq_len || !r->seq_head || !r->seq_count || !r->chunks || !r->served ||
+        !r->rows_cache || !r->c_match_n || !r->c_range_lo || !r->c_range_cnt || !r->c_taken || !r->c_cont_pos ||
+        !r->c_cont_src || !r->c_cont_len || !r->c_cont_tok || !r->c_num_nodes || !r->c_node_tok || !r->c_parent ||
+        !r->c_weight || !r->c_pos_ids || !r->c_mask)
+      return FC_ERR_INVALID;
+  }
+  if (r->missing) {
+    if (r->miss_cap < 1 || (r->miss_cap & (r->miss_cap - 1)) || r->miss_cap <= r->max_steps || !r->miss_key ||
+        !r->miss_used)
+      return FC_ERR_INVALID;
+  }
+  if ((r->missing || r->skip_tok >= 0) && (!r->m_skips || !r->g_skips)) return FC_ERR_INVALID;
+  if (r->skip_tok >= 0 && !r->skip_draws) return FC_ERR_INVALID;
+  return FC_OK;
 }
 
 }  // namespace
 
 extern "C" fc_status fc_replay_init(fc_replay* r, hipStream_t stream) {
-  if (!r || r->n_streams < 1 || r->ctx_len < 1 || r->ctx_len > fc::kWave || r->lru < 1 || r->lru > fc::kWave)
-    return FC_ERR_INVALID;
-  if (!r->pos || !r->lru_count || !r->hits || !r->lookups || !r->live) return FC_ERR_INVALID;
+  fc_status s = check_replay(r);
+  if (s != FC_OK) return s;
   (void)hipGetLastError();
-  hipLaunchKernelGGL(k_replay_init, dim3(fc::div_up(r->n_streams, 256)), dim3(256), 0, stream, r->n_streams,
-                     r->ctx_len, r->pos, r->lru_count, r->hits, r->lookups, r->live, r->truth_len);
+  hipLaunchKernelGGL(k_replay_init, dim3(fc::div_up(r->n_streams, 256)), dim3(256), 0, stream, *r);
   FC_CHECK_LAUNCH();
   return FC_OK;
 }
 
 extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_replay* r, int32_t first_step,
                                    int32_t n_steps, hipStream_t stream) {
-  if (!r || !stores || S < 1 || S > FC_MAX_SOURCES) return FC_ERR_INVALID;
-  if (r->n_streams < 1 || r->ctx_len < 1 || r->ctx_len > fc::kWave || r->lru < 1 || r->lru > fc::kWave)
-    return FC_ERR_INVALID;
-  if (r->truth_len < 0 || r->truth_stride < r->truth_len || !r->truth) return FC_ERR_INVALID;
+  if (!stores || S < 1 || S > FC_MAX_SOURCES) return FC_ERR_INVALID;
+  fc_status s = check_replay(r);
+  if (s != FC_OK) return s;
   if (first_step < 0 || n_steps < 0 || (int64_t)first_step + n_steps > r->max_steps) return FC_ERR_INVALID;
-  if ((int64_t)r->n_streams * r->lru > 0x7FFFFFFF) return FC_ERR_INVALID;
-  if (!r->pos || !r->lru_key || !r->lru_used || !r->lru_count || !r->hits || !r->lookups || !r->ctx ||
-      !r->rows_retrieve || !r->rows_tree || !r->live || !r->history)
-    return FC_ERR_INVALID;
-  const int32_t B = r->n_streams, n_rows = r->n_streams * r->lru;
+  const int32_t B = r->n_streams, n_rows = r->n_streams * r->lru + 1;
+  const bool cache = r->cache_l >= 0, control = r->missing || r->skip_tok >= 0;
+  const int32_t R = r->tp.c + 1;
+  if (first_step == 0 && control) {  // a replay's first call: the empty row and the missing tables
+    const int64_t tab = r->missing ? (int64_t)B * r->miss_cap : 0;
+    const int64_t work = tab > S ? tab : (int64_t)S;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_replay_init_tables, dim3((uint32_t)((work + 255) / 256)), dim3(256), 0, stream, *r, S);
+    FC_CHECK_LAUNCH();
+  }
+  fc_tree_params ctp = r->tp;
+  for (int i = 0; i < FC_MAX_SOURCES; ++i) ctp.alpha[i] = i == 0 ? 1u : 0u;
   for (int32_t i = 0; i < n_steps; ++i) {
     const int32_t step = first_step + i;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_replay_prepare, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
-                       step);
+    if (cache) {
+      hipLaunchKernelGGL(k_replay_context, dim3(B), dim3(fc::kWave), 0, stream, *r);
+      FC_CHECK_LAUNCH();
+      s = fc_cache_retrieve(r->ctext, r->cache_cap, B, r->clen, nullptr, r->ctx, B, r->ctx_len, r->rp, r->c_match_n,
+                            r->c_range_lo, r->c_range_cnt, r->c_taken, r->c_cont_pos, r->c_cont_src, r->c_cont_len,
+                            r->c_cont_tok, r->rows_cache, B, stream);
+      if (s != FC_OK) return s;
+    }
+    hipLaunchKernelGGL(k_replay_decide, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
+                       step, S);
     FC_CHECK_LAUNCH();
-    fc_status s = fc_retrieve(stores, S, r->ctx, B, r->ctx_len, r->rp, r->match_n, r->range_lo, r->range_cnt,
-                              r->taken, r->cont_pos, r->cont_src, r->cont_len, r->cont_tok, r->rows_retrieve, n_rows,
-                              r->retrieve_ws, r->retrieve_ws_bytes, stream);
+    s = fc_retrieve(stores, S, r->ctx, B, r->ctx_len, r->rp, r->match_n, r->range_lo, r->range_cnt, r->taken,
+                    r->cont_pos, r->cont_src, r->cont_len, r->cont_tok, r->rows_retrieve, n_rows, r->retrieve_ws,
+                    r->retrieve_ws_bytes, stream);
     if (s != FC_OK) return s;
+    if (r->missing) {
+      hipLaunchKernelGGL(k_replay_missing, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream,
+                         *r, S);
+      FC_CHECK_LAUNCH();
+    }
     s = fc_build_tree(r->taken, r->cont_len, r->cont_tok, r->ctx, B, r->ctx_len, S, r->rp.k, r->rp.m, r->tp,
                       r->num_nodes, r->node_tok, r->parent, r->weight, r->pos_ids, r->mask, r->rows_tree, n_rows,
                       r->tree_ws, r->tree_ws_bytes, stream);
     if (s != FC_OK) return s;
+    if (cache) {
+      s = fc_build_tree(r->c_taken, r->c_cont_len, r->c_cont_tok, r->ctx, B, r->ctx_len, 1, r->rp.k, r->rp.m, ctp,
+                        r->c_num_nodes, r->c_node_tok, r->c_parent, r->c_weight, r->c_pos_ids, r->c_mask,
+                        r->rows_cache, B, r->tree_ws, r->tree_ws_bytes, stream);
+      if (s != FC_OK) return s;
+      hipLaunchKernelGGL(k_replay_merge, dim3(B), dim3(256), 0, stream, *r, R);
+      FC_CHECK_LAUNCH();
+    }
     s = fc_targets_from_truth(r->truth, r->truth_len, r->truth_stride, nullptr, r->pos, r->num_nodes, r->pos_ids, B,
                               r->tp.c, r->target, stream);
     if (s != FC_OK) return s;
@@ -169,7 +449,8 @@ extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_r
                          r->accept_len, r->accept_tok, r->last_node, stream);
     if (s != FC_OK) return s;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_replay_advance, dim3(fc::div_up(B, 256)), dim3(256), 0, stream, *r, step);
+    hipLaunchKernelGGL(k_replay_advance, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
+                       step);
     FC_CHECK_LAUNCH();
   }
   return FC_OK;

@@ -27,10 +27,10 @@ host keeps the sequence lists, decides evictions (oldest sequences first
 when a text would outgrow its row) and ships each step's appended tokens in
 one batched fc_cache_write.
 
-Without the CACHE and the timing control, run() hands the whole replay to
-the device-resident engine (ReplayEngine: fc_replay_init / fc_replay_run),
-which takes the same decisions on the GPU with no host round trip per step;
-step() is this module's own host-driven loop, used for the other modes.
+run() hands the whole replay to the device-resident engine (ReplayEngine:
+fc_replay_init / fc_replay_run), which takes the same decisions on the GPU
+with no host round trip per step; step() is this module's own host-driven
+loop (run(native=False)), kept as a second implementation.
 
 Alg. 1's retrieval-timing control (for contexts the CACHE did not serve):
 with missing=True a per-stream missing table holds the contexts whose
@@ -115,7 +115,7 @@ class GpuReplay:
         self.tgt = torch.empty((self.nseq, c + 1), dtype=torch.int32, device=self.device)
         self.cache_l, self.cache_every, self.cache_cap = cache_l, cache_every, cache_cap
         self.missing, self.skip_tok = missing, skip_tok
-        self.skip_thr = int(skip_p * 2 ** 31)
+        self.skip_p, self.skip_thr = skip_p, int(skip_p * 2 ** 31)
         self.skip_draws = None if skip_draws is None else np.asarray(skip_draws)
         if cache_l is not None:
             self.ctext = torch.zeros((self.nseq, cache_cap), dtype=torch.uint16, device=self.device)
@@ -279,27 +279,24 @@ class GpuReplay:
         self._cache_upload(changed)
         return out
 
-    @property
-    def plain(self) -> bool:
-        """No CACHE and no timing control: the device engine's mode."""
-        return self.cache_l is None and not self.missing and self.skip_tok is None
-
-    def run(self, max_steps: int = 512, native: bool | None = None) -> dict:
-        """Replays from the current state (the engine always from the start)
-        for at most max_steps steps.  native: None picks the device engine
-        for the plain mode, True requires it, False uses step()."""
-        if native is None:
-            native = self.plain
+    def run(self, max_steps: int = 512, native: bool = True) -> dict:
+        """Replays for at most max_steps steps: from the start on the device
+        engine (native), or from the current state with step()."""
         if native:
-            if not self.plain:
-                raise ValueError("the device engine runs the plain replay only (no CACHE, no timing control)")
             if not hasattr(self, "_engine") or self._engine.max_steps < max_steps:
-                self._engine = ReplayEngine(self.stores, self.truth, max_steps=max(max_steps, 512), **self.kw)
-            g = self._engine.run(limit=max_steps)
-            n = self.nseq
-            g.update(cache_served=np.zeros(n, np.int64), missing_skips=np.zeros(n, np.int64),
-                     gate_skips=np.zeros(n, np.int64))
-            return g
+                steps = max(max_steps, 512)
+                ckw = {}
+                if self.cache_l is not None:
+                    ckw.update(cache_l=self.cache_l, cache_every=self.cache_every, cache_cap=self.cache_cap)
+                if self.missing:
+                    ckw.update(missing=True)
+                if self.skip_tok is not None:
+                    draws = np.zeros((steps, self.nseq), np.int64)
+                    have = min(steps, len(self.skip_draws))
+                    draws[:have] = np.asarray(self.skip_draws)[:have, :self.nseq]
+                    ckw.update(skip_tok=self.skip_tok, skip_p=self.skip_p, skip_draws=draws)
+                self._engine = ReplayEngine(self.stores, self.truth, max_steps=steps, **self.kw, **ckw)
+            return self._engine.run(limit=max_steps)
         steps = []
         for _ in range(max_steps):
             a = self.step()

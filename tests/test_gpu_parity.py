@@ -564,8 +564,9 @@ def test_cache_retrieve_matches_oracle():
             compare_retrieve(g, o, rows=[int(out_rows[b])])
 
 
+@pytest.mark.parametrize("native", [True, False], ids=["engine", "driver"])
 @pytest.mark.parametrize("cache_l,cap", [(50, fc.FC_MAX_CACHE_TOKENS), (4, 300)])
-def test_replay_with_cache_matches_oracle(cache_l, cap):
+def test_replay_with_cache_matches_oracle(cache_l, cap, native):
     """Decode-trace replay with the CACHE branch of Alg. 1: every accepted
     length, final position, LRU count and CACHE-served count equal the
     oracle's; the small-cap case evicts and rewrites CACHE texts."""
@@ -573,7 +574,7 @@ def test_replay_with_cache_matches_oracle(cache_l, cap):
     truth = synth.truth(n_seq=12, length=500)
     stores = [gpu_store(tp, synth.VOCAB, records=True), gpu_store(t1)]
     say(f"replay+cache l={cache_l} cap={cap}: gpu")
-    g = GpuReplay(stores, truth, cache_l=cache_l, cache_cap=cap, **P).run(max_steps=400)
+    g = GpuReplay(stores, truth, cache_l=cache_l, cache_cap=cap, **P).run(max_steps=400, native=native)
     say(f"replay+cache l={cache_l} cap={cap}: oracle")
     o = oracle.replay([tp, t1], truth, cache_l=cache_l, cache_cap=cap, **P, max_steps=400)
     for f in ("accept", "hits", "lookups", "pos", "cache_served"):
@@ -581,8 +582,9 @@ def test_replay_with_cache_matches_oracle(cache_l, cap):
     assert g["cache_served"].sum() > 0
 
 
+@pytest.mark.parametrize("native", [True, False], ids=["engine", "driver"])
 @pytest.mark.parametrize("case", ["project-streams", "recurring-misses"])
-def test_replay_with_retrieval_control_matches_oracle(case):
+def test_replay_with_retrieval_control_matches_oracle(case, native):
     """Alg. 1 in full (CACHE branch, missing table, skip gate with p = 0.5
     on the streams' most frequent token): every accepted length, position
     and branch count equal the oracle's.  The second case replays periodic
@@ -600,7 +602,7 @@ def test_replay_with_retrieval_control_matches_oracle(case):
     draws = np.stack([synth.uniform(31, 30, step, truth.shape[0], 0, 2 ** 31 - 1) for step in range(400)])
     kw = dict(cache_l=50, missing=True, skip_tok=tok, skip_p=0.5, skip_draws=draws)
     say(f"replay+control {case}: gpu")
-    g = GpuReplay(stores, truth, **kw, **P).run(max_steps=400)
+    g = GpuReplay(stores, truth, **kw, **P).run(max_steps=400, native=native)
     say(f"replay+control {case}: oracle")
     o = oracle.replay(texts, truth, **kw, **P, max_steps=400)
     for f in ("accept", "hits", "lookups", "pos", "cache_served", "missing_skips", "gate_skips"):
