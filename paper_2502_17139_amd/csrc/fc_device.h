@@ -250,4 +250,29 @@ __device__ __forceinline__ int map_row(const int32_t* rows, int n_rows, int b) {
   return (r >= 0 && r < n_rows) ? r : -1;
 }
 
+typedef int int32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource over `bytes` bytes at p (raw, no stride): loads at or past
+// `bytes` return zeros.
+__device__ __forceinline__ int32x4 buffer_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = (uint64_t)p;
+  int32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r.y = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xFFFFu));
+  r.z = __builtin_amdgcn_readfirstlane((int)bytes);
+  r.w = 0x00020000;
+  return r;
+}
+
+// One wave loads 64 x 16 bytes from the buffer at byte offsets voff (one per
+// lane) into LDS bytes [lds, lds + 1024), lane L at lds + 16 L.  The load is
+// counted by vmcnt like any vector load; the compiler does not track it.
+__device__ __forceinline__ void lds_load16(uint32_t lds, uint32_t voff, int32x4 rsrc) {
+  asm volatile("s_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds"
+               :
+               : "v"(voff), "s"(__builtin_amdgcn_readfirstlane((int)lds)), "s"(rsrc)
+               : "memory");
+}
+
+
 }  // namespace fc

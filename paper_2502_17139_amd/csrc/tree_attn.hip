@@ -40,7 +40,6 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef int int32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr int kD = FC_TREE_ATTN_HEAD_DIM;   // 128
@@ -82,28 +81,6 @@ __device__ __forceinline__ void load8(const uint16_t* __restrict__ p, float (&v)
   }
 }
 
-// Buffer resource over `bytes` bytes at p (raw, no stride): loads at or past
-// `bytes` return zeros.
-__device__ __forceinline__ int32x4 buffer_rsrc(const void* p, uint32_t bytes) {
-  const uint64_t a = (uint64_t)p;
-  int32x4 r;
-  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
-  r.y = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xFFFFu));
-  r.z = __builtin_amdgcn_readfirstlane((int)bytes);
-  r.w = 0x00020000;
-  return r;
-}
-
-// One wave loads 64 x 16 bytes from the buffer at byte offsets voff (one per
-// lane) into LDS bytes [lds, lds + 1024), lane L at lds + 16 L.  The load is
-// counted by vmcnt like any vector load; the compiler does not track it.
-__device__ __forceinline__ void lds_load16(uint32_t lds, uint32_t voff, int32x4 rsrc) {
-  asm volatile("s_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds"
-               :
-               : "v"(voff), "s"(__builtin_amdgcn_readfirstlane((int)lds)), "s"(rsrc)
-               : "memory");
-}
-
 template <int MAXT>
 __global__ void __launch_bounds__(MAXT) k_tree_attn(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_tree, const uint16_t* __restrict__ v_tree,
@@ -135,8 +112,8 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
   // Waves 0..3 issue loads w, w+4, w+8, w+12 of every block.
   const int64_t row_stride = (int64_t)Hkv * kD * 2;  // bytes between consecutive keys
   const uint32_t pre_bytes = P > 0 ? (uint32_t)((int64_t)(P - 1) * row_stride + kRowBytes) : 0u;
-  const int32x4 rk = buffer_rsrc(k_cache + ((int64_t)b * Pmax * Hkv + g_kv) * kD, pre_bytes);
-  const int32x4 rv = buffer_rsrc(v_cache + ((int64_t)b * Pmax * Hkv + g_kv) * kD, pre_bytes);
+  const fc::int32x4 rk = fc::buffer_rsrc(k_cache + ((int64_t)b * Pmax * Hkv + g_kv) * kD, pre_bytes);
+  const fc::int32x4 rv = fc::buffer_rsrc(v_cache + ((int64_t)b * Pmax * Hkv + g_kv) * kD, pre_bytes);
   const bool dma_wave = w < kDmaWaves;
   auto issue_block = [&](int blk) {  // rows past P (also whole blocks past the prefix) read as zeros
     if (!dma_wave) return;
@@ -148,7 +125,7 @@ __global__ void __launch_bounds__(MAXT) k_tree_attn(
       const int c = (lane & 15) ^ (r & 15);
       const int64_t key = (int64_t)blk * kBlock + r;
       const uint32_t voff = key < P ? (uint32_t)(key * row_stride + 16 * c) : pre_bytes;
-      lds_load16(slot + (u < 8 ? 0u : (uint32_t)kPart) + (uint32_t)(u & 7) * 1024u, voff, u < 8 ? rk : rv);
+      fc::lds_load16(slot + (u < 8 ? 0u : (uint32_t)kPart) + (uint32_t)(u & 7) * 1024u, voff, u < 8 ? rk : rv);
     }
   };
 
