@@ -169,6 +169,8 @@ def main():
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="headline")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-latency", action="store_true",
+                    help="skip the single-query latency runs (profiles then hold batch dispatches only)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "single-GPU path only (no sharded stores); --gpus must be 1", "n_gpus": args.gpus}))
@@ -290,7 +292,7 @@ def main():
     tws1 = torch.empty(max(fc.fc_build_tree_workspace_bytes(1), 1), dtype=torch.uint8, device=dev)
     a1o = fc.accept_outputs(1, m, dev)
     lat = []
-    for qi in range(min(64, B) + 3):
+    for qi in range(0 if args.no_latency else min(64, B) + 3):
         cq, tq = ctx[qi % B:qi % B + 1], target[qi % B:qi % B + 1]
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
@@ -350,8 +352,8 @@ def main():
         "roofline_by_entry": roofs,
         "cpu_baseline": cpu,
         "phases_ms": phase_ms,
-        "single_query_latency_ms": {"median": float(np.median(lat)), "p90": float(np.percentile(lat, 90)),
-                                    "queries": len(lat)},
+        "single_query_latency_ms": None if not lat else {
+            "median": float(np.median(lat)), "p90": float(np.percentile(lat, 90)), "queries": len(lat)},
         "ms_per_step_with_phase_events": float(sum(phase_ms.values())),
         "algorithmic_bytes_per_step": nb,
         "step_GBps_algorithmic": total_bytes / (ms_step * 1e-3) / 1e9,
