@@ -502,7 +502,6 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   __shared__ int16_t s_par[FC_MAX_TREE_ROWS];
   __shared__ uint64_t s_dball[FC_MAX_TREE_ROWS / fc::kWave][MAXM];
   __shared__ uint32_t s_pick[3];
-  __shared__ int s_query;
 
   const int tid = threadIdx.x;
   int b;
@@ -515,10 +514,10 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     if ((int)blockIdx.x >= *list_count) return;
     b = b_raw;
   } else {
-    // The light launch: its queries are those with T <= t_hi kept slots
-    // (malformed rows too), in query order, and workgroup x takes the x-th.
-    // Every workgroup finds it with one scan over the batch; workgroup 0
-    // also writes the list of the others (the heavy launch's).
+    // The light launch: workgroup q takes query q when it has T <= t_hi
+    // kept slots (malformed rows too) and leaves at once otherwise; one
+    // extra workgroup (q = B) writes the list of the others, in query order,
+    // for the heavy launch.
     auto heavy = [&](int q) {
       const int r = fc::map_row(rows, n_rows, q);
       if (r < 0) return false;
@@ -530,31 +529,21 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
       }
       return !bad && T <= k && T > t_hi;
     };
-    const int per = (B + NT - 1) / NT;
-    const int q0 = tid * per < B ? tid * per : B;
-    const int q1 = q0 + per < B ? q0 + per : B;
-    uint32_t nh = 0;
-    for (int q = q0; q < q1; ++q) nh += heavy(q) ? 1u : 0u;
-    const uint32_t nl = (uint32_t)(q1 - q0) - nh;
-    uint32_t el, eh, tl, th;
-    Scan2<NT>::run(nl, nh, s_x, s_y, &el, &eh, &tl, &th);
-    if (blockIdx.x == 0) {
+    if ((int)blockIdx.x == B) {
+      const int per = (B + NT - 1) / NT;
+      const int q0 = tid * per < B ? tid * per : B;
+      const int q1 = q0 + per < B ? q0 + per : B;
+      uint32_t nh = 0;
+      for (int q = q0; q < q1; ++q) nh += heavy(q) ? 1u : 0u;
+      uint32_t eh, dummy, th, dummy2;
+      Scan2<NT>::run(nh, 0u, s_x, s_y, &eh, &dummy, &th, &dummy2);
       for (int q = q0; q < q1; ++q)
         if (heavy(q)) heavy_list[eh++] = q;
       if (tid == 0) *heavy_count = (int32_t)th;
+      return;
     }
-    const uint32_t target = blockIdx.x;
-    if (target >= tl) return;
-    if (target >= el && target < el + nl) {
-      uint32_t x = el;
-      for (int q = q0; q < q1; ++q) {
-        if (heavy(q)) continue;
-        if (x == target) s_query = q;
-        ++x;
-      }
-    }
-    __syncthreads();
-    b = s_query;
+    b = (int)blockIdx.x;
+    if (heavy(b)) return;
   }
   const int lane = fc::lane_id();
   const int w = tid / fc::kWave;
@@ -1097,7 +1086,7 @@ fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint1
     (void)hipFuncSetAttribute((const void*)k_tree_fast<256, MAXM>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)small.total);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((k_tree_fast<256, MAXM>), dim3(B), dim3(256), small.total, stream, taken, cont_len, cont_tok,
+  hipLaunchKernelGGL((k_tree_fast<256, MAXM>), dim3(B + 1), dim3(256), small.total, stream, taken, cont_len, cont_tok,
                      ctx, L, S, k, m, t.c, a, nullptr, nullptr, lists + B, counts + 1, B, t_small, words, rows,
                      n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
   FC_CHECK_LAUNCH();
