@@ -756,6 +756,9 @@ __global__ void __launch_bounds__(256) k_pairs(const uint16_t* __restrict__ tok,
 
 // Inline-prefix records: one thread per suffix-array position writes
 // {sa[i], T[sa[i]+2 .. sa[i]+32)} as four 16-byte stores (0 past the end).
+// The 60 text bytes come from five aligned 16-byte loads (the 80 bytes from
+// the 16-byte boundary at or below the first token), re-aligned in
+// registers; suffixes whose window would leave the text take token loads.
 __global__ void __launch_bounds__(256) k_records(const uint16_t* __restrict__ tok, const uint32_t* __restrict__ sa,
                                                  uint32_t n, uint4* __restrict__ rec) {
   static_assert(FC_RECORD_BYTES == 64 && FC_RECORD_TOKENS == 30, "record layout");
@@ -764,12 +767,36 @@ __global__ void __launch_bounds__(256) k_records(const uint16_t* __restrict__ to
   const uint32_t j = sa[i];
   uint32_t w[16];
   w[0] = j;
+  const uintptr_t base = (uintptr_t)tok;
+  const uintptr_t first = base + 2 * ((uint64_t)j + 2);
+  const uintptr_t lo = first & ~(uintptr_t)15;
+  if (lo >= base && lo + 80 <= base + 2 * (uint64_t)n) {
+    uint32_t d[20];
 #pragma unroll
-  for (int x = 0; x < FC_RECORD_TOKENS / 2; ++x) {
-    const uint64_t p = (uint64_t)j + 2 + 2 * x;
-    const uint32_t a = p < n ? tok[p] : 0u;
-    const uint32_t b = p + 1 < n ? tok[p + 1] : 0u;
-    w[1 + x] = a | (b << 16);
+    for (int u = 0; u < 5; ++u) {
+      const uint4 v = ((const uint4*)lo)[u];
+      d[4 * u] = v.x;
+      d[4 * u + 1] = v.y;
+      d[4 * u + 2] = v.z;
+      d[4 * u + 3] = v.w;
+    }
+    const uint32_t off = (uint32_t)(first - lo);  // 0, 2, .., 14 bytes
+    const uint32_t q = off >> 2, half = off & 2;
+#pragma unroll
+    for (int x = 0; x < FC_RECORD_TOKENS / 2; ++x) {
+      // the dword starting at byte off + 4x: dwords q + x and q + x + 1
+      const uint32_t a0 = q == 0 ? d[x] : q == 1 ? d[x + 1] : q == 2 ? d[x + 2] : d[x + 3];
+      const uint32_t a1 = q == 0 ? d[x + 1] : q == 1 ? d[x + 2] : q == 2 ? d[x + 3] : d[x + 4];
+      w[1 + x] = half ? __builtin_amdgcn_alignbyte(a1, a0, 2) : a0;
+    }
+  } else {
+#pragma unroll
+    for (int x = 0; x < FC_RECORD_TOKENS / 2; ++x) {
+      const uint64_t p = (uint64_t)j + 2 + 2 * x;
+      const uint32_t a = p < n ? tok[p] : 0u;
+      const uint32_t b = p + 1 < n ? tok[p + 1] : 0u;
+      w[1 + x] = a | (b << 16);
+    }
   }
 #pragma unroll
   for (int u = 0; u < 4; ++u) rec[4 * i + u] = make_uint4(w[4 * u], w[4 * u + 1], w[4 * u + 2], w[4 * u + 3]);
