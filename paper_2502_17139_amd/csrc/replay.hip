@@ -125,7 +125,7 @@ __device__ int miss_find(const fc_replay& r, int b, const uint16_t* ctx) {
 }
 
 // One wave per stream: the step's decision and its row maps.
-__global__ void __launch_bounds__(kPrepThreads) k_replay_decide(fc_replay r, int32_t step, int32_t S) {
+__global__ void __launch_bounds__(kPrepThreads) k_replay_decide(fc_replay r, int32_t step) {
   const int lane = fc::lane_id();
   const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
   if (blockIdx.x == 0 && threadIdx.x == 0) *r.live = 0;
@@ -217,7 +217,6 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_decide(fc_replay r, int
     r.rows_tree[b] = row;
     r.state[b] = kNeed;
   }
-  (void)S;
 }
 
 // One wave per stream: a looked-up context whose result is empty enters the
@@ -419,7 +418,7 @@ extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_r
       if (s != FC_OK) return s;
     }
     hipLaunchKernelGGL(k_replay_decide, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
-                       step, S);
+                       step);
     FC_CHECK_LAUNCH();
     s = fc_retrieve(stores, S, r->ctx, B, r->ctx_len, r->rp, r->match_n, r->range_lo, r->range_cnt, r->taken,
                     r->cont_pos, r->cont_src, r->cont_len, r->cont_tok, r->rows_retrieve, n_rows, r->retrieve_ws,
