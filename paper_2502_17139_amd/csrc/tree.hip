@@ -941,11 +941,14 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     const uint32_t wstar = prefix;
     const uint32_t take_eq = remaining;
 
-    // 6. kept nodes in (p, d) order = preorder
+    // 6. kept nodes in (p, d) order = preorder.  A string's own nodes get
+    //    lighter with depth, so a string whose shallowest own node is below
+    //    W* has none to keep and is passed over after one read.
     uint32_t gt = 0, eq = 0;
     if (need > 0) {
       for (int p = p0; p < p1; ++p) {
         const int l = lcp[p], ml = mlen[p];
+        if (l >= ml || node_w(p, l + 1) < wstar) continue;
         uint32_t wv[MAXM + 1];
         row_w(p, wv);
 #pragma unroll
@@ -963,6 +966,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
       uint32_t r = eq_ex;
       for (int p = p0; p < p1; ++p) {
         const int l = lcp[p], ml = mlen[p];
+        if (l >= ml || node_w(p, l + 1) < wstar) continue;
         uint32_t wv[MAXM + 1];
         row_w(p, wv);
 #pragma unroll
