@@ -612,6 +612,38 @@ def test_replay_with_retrieval_control_matches_oracle(case, native):
         assert g["missing_skips"].sum() > 0
 
 
+@pytest.mark.parametrize("mode", ["lru1", "tiny-cache", "cache0-control"])
+def test_replay_engine_edge_cases(mode):
+    """The device engine against the oracle replay on small-vocabulary
+    stores and streams (long matches, many ties): an LRU of one slot, a
+    40-token CACHE of 3-token chunks that evicts almost every step, and a
+    CACHE searched from the first step (cache_l = 0, empty texts) with the
+    missing table and the skip gate on."""
+    texts = [synth.random_text(71, 3000, 6, 0.01), synth.random_text(72, 5000, 6, 0.01)]
+    # random streams, one repeating a single token (the same context every
+    # step: LRU hits), one of a token the stores lack (empty results: the
+    # missing table), one of period 3
+    truth = np.stack([synth.random_text(80 + i, 120, 6) for i in range(4)] +
+                     [np.full(120, 3, np.uint16), np.full(120, 9, np.uint16),
+                      np.resize(np.array([2, 4, 1], np.uint16), 120)])
+    p = dict(n_max=8, n_min=1, k=40, m=4, c=12, alpha=(1, 2), ctx_len=8)
+    kw = {"lru1": dict(lru=1),
+          "tiny-cache": dict(lru=3, cache_l=2, cache_every=3, cache_cap=40),
+          "cache0-control": dict(lru=3, cache_l=0, cache_every=5, cache_cap=200, missing=True,
+                                 skip_tok=int(np.bincount(truth.ravel()).argmax()), skip_p=0.5,
+                                 skip_draws=np.stack([synth.uniform(33, 30, st, truth.shape[0], 0, 2 ** 31 - 1)
+                                                      for st in range(300)]))}[mode]
+    say(f"replay engine edge case {mode}")
+    g = GpuReplay([gpu_store(t) for t in texts], truth, **kw, **p).run(max_steps=300)
+    o = oracle.replay(texts, truth, **kw, **p, max_steps=300)
+    for f in ("accept", "hits", "lookups", "pos", "cache_served", "missing_skips", "gate_skips"):
+        assert (g[f] == o[f]).all(), (mode, f)
+    assert g["steps"] == o["accept"].shape[0]
+    assert g["hits"].sum() > 0
+    if mode == "cache0-control":
+        assert g["missing_skips"].sum() > 0 and g["gate_skips"].sum() > 0
+
+
 # ---------------------------------------------------------- tree attention --
 
 def _bf16(rng, *shape, scale=1.0):
