@@ -440,9 +440,10 @@ fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_
  * becomes most recent; a miss takes the next free slot, or the least
  * recently used one when all are taken, and is retrieved into it); the
  * draft tree is built from the slot (fc_build_tree), the true tokens are
- * its targets (fc_targets_from_truth), acceptance is greedy
- * (fc_verify_accept) and pos[b] advances by the accepted length.  A step is
- * a fixed chain of launches on `stream` with no host round trip.
+ * its targets (as fc_targets_from_truth gives them), acceptance is greedy
+ * (as fc_verify_accept; both in one pass here, into accept_len, accept_tok
+ * and last_node) and pos[b] advances by the accepted length.  A step is a
+ * fixed chain of launches on `stream` with no host round trip.
  *
  * All pointers are device memory owned by the caller:
  *   pos, lru_count, hits, lookups, rows_retrieve, rows_tree [n_streams];
@@ -452,8 +453,8 @@ fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_
  *   stream at each step, -1 once the stream is finished;
  *   retrieval outputs (fc_retrieve's, with n_streams * lru rows: row
  *   b * lru + slot is stream b's slot) and workspace for a batch of
- *   n_streams; tree outputs, target [n_streams][c+1] and acceptance
- *   outputs for n_streams.
+ *   n_streams; tree outputs and acceptance outputs for n_streams (`target`
+ *   is not used and may be NULL).
  * Limits: 1 <= ctx_len <= 64 (also fc_retrieve's n_max <= ctx_len is the
  * caller's choice), 1 <= lru <= 64, truth_stride >= truth_len.
  *

@@ -275,4 +275,49 @@ __device__ __forceinline__ void lds_load16(uint32_t lds, uint32_t voff, int32x4 
 }
 
 
+// Greedy acceptance walk of one draft tree by one wave (Section IV-D):
+// from the root, step to the child whose token equals target(u) while one
+// exists; the target at the stopping row is accepted too.  Rows 1..n-1 of
+// the tree (n clamped to [1, R]) are held four per lane; each step is one
+// ballot per 64 rows.  Writes the accepted tokens (m + 1 slots, -1 past the
+// end) and returns the accepted length and the last row in len and u.
+template <int MAXROWS, typename Target>
+__device__ __forceinline__ void accept_walk(int n, const int32_t* __restrict__ node_tok,
+                                            const int32_t* __restrict__ parent, int R, int m, Target target,
+                                            int32_t* __restrict__ out, int& len, int& u) {
+  constexpr int kChunks = MAXROWS / kWave;
+  const int lane = lane_id();
+  n = n < 1 ? 1 : (n > R ? R : n);
+  int32_t par[kChunks], tok[kChunks];
+#pragma unroll
+  for (int h = 0; h < kChunks; ++h) {
+    const int v = lane + h * kWave;
+    const bool in = v >= 1 && v < n;
+    par[h] = in ? parent[v] : -2;
+    tok[h] = in ? node_tok[v] : -1;
+  }
+  u = 0;
+  len = 0;
+  for (;;) {
+    const int32_t want = target(u);
+    if (want < 0 || len >= m + 1) break;
+    int next = -1;
+#pragma unroll
+    for (int h = 0; h < kChunks; ++h) {
+      const uint64_t hit = ballot(par[h] == u && tok[h] == want);
+      if (next < 0 && hit) next = h * kWave + (int)__builtin_ctzll(hit);
+    }
+    if (next < 0) break;
+    if (lane == 0) out[len] = want;
+    ++len;
+    u = next;
+  }
+  const int32_t bonus = target(u);
+  if (bonus >= 0 && len < m + 1) {
+    if (lane == 0) out[len] = bonus;
+    ++len;
+  }
+  for (int x = len + lane; x < m + 1; x += kWave) out[x] = -1;
+}
+
 }  // namespace fc

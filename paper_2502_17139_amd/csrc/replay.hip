@@ -22,9 +22,11 @@
 //   k_replay_missing   (table on) empty results enter the missing table;
 //   fc_build_tree      from the datastore slots (and, CACHE on, a second one
 //                      from the CACHE results, merged by k_replay_merge);
-//   fc_targets_from_truth, fc_verify_accept;
-//   k_replay_advance   position += accepted length, the step's history row,
-//                      the live count and (CACHE on) the CACHE additions.
+//   k_replay_finish    one wave per stream: the acceptance walk with the
+//                      true tokens as targets (fc_targets_from_truth and
+//                      fc_verify_accept in one pass), position += accepted
+//                      length, the step's history row, the live count and
+//                      (CACHE on) the CACHE additions.
 // The LRU keeps the exact semantics of an ordered map: slots fill in order,
 // a hit becomes most recent, a miss in a full table replaces the least
 // recently used slot (last-use steps are distinct per stream).
@@ -303,9 +305,11 @@ __device__ void cache_add(const fc_replay& r, int b, CacheState& st, const uint1
   __threadfence_block();
 }
 
-// One wave per stream: the history row, the new position, the live count
-// and (CACHE on) the CACHE additions of this step.
-__global__ void __launch_bounds__(kPrepThreads) k_replay_advance(fc_replay r, int32_t step) {
+// One wave per stream: acceptance (the target after row i is the true token
+// at pos + pos_ids[i], -1 past the stream or for rows past num_nodes), the
+// history row, the new position, the live count and (CACHE on) the CACHE
+// additions of this step.
+__global__ void __launch_bounds__(kPrepThreads) k_replay_finish(fc_replay r, int32_t step) {
   const int lane = fc::lane_id();
   const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
   if (b >= r.n_streams) return;
@@ -316,14 +320,29 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_advance(fc_replay r, in
     if (lane == 0) hist[b] = -1;
     return;
   }
-  const int a = r.accept_len[b];
+  const int R = r.tp.c + 1;
+  const int64_t row = (int64_t)b * R;
+  const int nn = r.num_nodes[b];
+  const uint16_t* srow = r.truth + (int64_t)b * r.truth_stride;
+  const int32_t* pid = r.pos_ids + row;
+  int a, last;
+  fc::accept_walk<FC_MAX_TREE_ROWS>(
+      nn, r.node_tok + row, r.parent + row, R, r.rp.m,
+      [&](int v) -> int32_t {
+        if (v >= nn) return -1;
+        const int64_t q = (int64_t)p + pid[v];
+        return (q >= 0 && q < tlen) ? (int32_t)srow[q] : -1;
+      },
+      r.accept_tok + (int64_t)b * (r.rp.m + 1), a, last);
+  if (lane == 0) {
+    r.accept_len[b] = a;
+    r.last_node[b] = last;
+  }
   const int np = p + a;
   if (cache_on(r)) {
-    const int R = r.tp.c + 1;
-    const uint16_t* row = r.truth + (int64_t)b * r.truth_stride;
+    const uint16_t* row = srow;
     if (lane == 0 && r.state[b] == kServed) r.served[b] += 1;
-    const int last = r.last_node[b];
-    const int depth = (last >= 0 && last < R) ? r.pos_ids[(int64_t)b * R + last] : 0;
+    const int depth = (last >= 0 && last < R) ? pid[last] : 0;
     CacheState st = {r.clen[b], r.seq_head[b], r.seq_count[b]};
     if (depth >= 1) {  // a verified draft: the context and its accepted tokens
       const int end = p + depth < tlen ? p + depth : tlen;
@@ -355,7 +374,8 @@ fc_status check_replay(const fc_replay* r) {
   if (r->truth_len < 0 || r->truth_stride < r->truth_len || !r->truth || r->max_steps < 0) return FC_ERR_INVALID;
   if ((int64_t)r->n_streams * r->lru + 1 > 0x7FFFFFFF) return FC_ERR_INVALID;
   if (!r->pos || !r->lru_key || !r->lru_used || !r->lru_count || !r->hits || !r->lookups || !r->ctx ||
-      !r->rows_retrieve || !r->rows_tree || !r->live || !r->history || !r->taken || !r->state)
+      !r->rows_retrieve || !r->rows_tree || !r->live || !r->history || !r->taken || !r->state || !r->accept_len ||
+      !r->accept_tok || !r->last_node)
     return FC_ERR_INVALID;
   if (r->cache_l >= 0) {
     if (r->cache_every < 1 || r->cache_cap < 1 || r->cache_cap > FC_MAX_CACHE_TOKENS ||
@@ -441,14 +461,8 @@ extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_r
       hipLaunchKernelGGL(k_replay_merge, dim3(B), dim3(256), 0, stream, *r, R);
       FC_CHECK_LAUNCH();
     }
-    s = fc_targets_from_truth(r->truth, r->truth_len, r->truth_stride, nullptr, r->pos, r->num_nodes, r->pos_ids, B,
-                              r->tp.c, r->target, stream);
-    if (s != FC_OK) return s;
-    s = fc_verify_accept(r->num_nodes, r->node_tok, r->parent, r->pos_ids, r->target, B, r->tp.c, r->rp.m,
-                         r->accept_len, r->accept_tok, r->last_node, stream);
-    if (s != FC_OK) return s;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_replay_advance, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
+    hipLaunchKernelGGL(k_replay_finish, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
                        step);
     FC_CHECK_LAUNCH();
   }

@@ -18,9 +18,8 @@ namespace {
 constexpr int kVerifyThreads = 256;
 constexpr int kQueriesPerBlock = kVerifyThreads / fc::kWave;
 
-// One wave per query.  Lane l holds rows l, l+64, l+128, l+192 (parent and
-// token); each step is one ballot over "my row is a child of u carrying the
-// target token", so a path of depth d costs d ballots.
+// One wave per query (the walk in fc_device.h: lane l holds rows l, l+64,
+// l+128, l+192; a path of depth d costs d ballots per 64 rows).
 __global__ void __launch_bounds__(kVerifyThreads) k_verify(const int32_t* __restrict__ num_nodes,
                                                            const int32_t* __restrict__ node_tok,
                                                            const int32_t* __restrict__ parent,
@@ -28,44 +27,15 @@ __global__ void __launch_bounds__(kVerifyThreads) k_verify(const int32_t* __rest
                                                            int32_t* __restrict__ accept_len,
                                                            int32_t* __restrict__ accept_tok,
                                                            int32_t* __restrict__ last_node) {
-  constexpr int kChunks = FC_MAX_TREE_ROWS / fc::kWave;
   const int b = blockIdx.x * kQueriesPerBlock + (int)(threadIdx.x / fc::kWave);
   const int lane = fc::lane_id();
   if (b >= B) return;  // whole wave leaves together
   const int R = c + 1;
   const int64_t row = (int64_t)b * R;
-  int n = num_nodes[b];
-  n = n < 1 ? 1 : (n > R ? R : n);
-  int32_t par[kChunks], tok[kChunks];
-#pragma unroll
-  for (int h = 0; h < kChunks; ++h) {
-    const int v = lane + h * fc::kWave;
-    const bool in = v >= 1 && v < n;
-    par[h] = in ? parent[row + v] : -2;
-    tok[h] = in ? node_tok[row + v] : -1;
-  }
-  int32_t* out = accept_tok + (int64_t)b * (m + 1);
-  int u = 0, len = 0;
-  for (;;) {
-    const int32_t want = target[row + u];
-    if (want < 0 || len >= m + 1) break;
-    int next = -1;
-#pragma unroll
-    for (int h = 0; h < kChunks; ++h) {
-      const uint64_t hit = fc::ballot(par[h] == u && tok[h] == want);
-      if (next < 0 && hit) next = h * fc::kWave + (int)__builtin_ctzll(hit);
-    }
-    if (next < 0) break;
-    if (lane == 0) out[len] = want;
-    ++len;
-    u = next;
-  }
-  const int32_t bonus = target[row + u];
-  if (bonus >= 0 && len < m + 1) {
-    if (lane == 0) out[len] = bonus;
-    ++len;
-  }
-  for (int x = len + lane; x < m + 1; x += fc::kWave) out[x] = -1;
+  const int32_t* tgt = target + row;
+  int len, u;
+  fc::accept_walk<FC_MAX_TREE_ROWS>(num_nodes[b], node_tok + row, parent + row, R, m,
+                                     [&](int v) { return tgt[v]; }, accept_tok + (int64_t)b * (m + 1), len, u);
   if (lane == 0) {
     accept_len[b] = len;
     last_node[b] = u;
