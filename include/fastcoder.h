@@ -41,7 +41,7 @@ typedef enum fc_status {
   FC_ERR_INVALID = 1,     /* null pointer, size or parameter out of range */
   FC_ERR_WORKSPACE = 2,   /* workspace pointer null or smaller than required */
   FC_ERR_DEVICE = 3,      /* HIP launch/runtime error, or a device-side check failed */
-  FC_ERR_UNSUPPORTED = 4  /* valid request outside what this build handles */
+  FC_ERR_UNSUPPORTED = 4  /* valid request outside what the library handles */
 } fc_status;
 
 #define FC_MAX_SOURCES 4     /* stores per retrieval */
@@ -378,7 +378,7 @@ fc_status fc_verify_accept(const int32_t* num_nodes, const int32_t* node_tok, co
 /* Tree attention (verification of the draft tree)                           */
 /* ------------------------------------------------------------------------ */
 
-#define FC_TREE_ATTN_HEAD_DIM 128 /* head dimension this build supports */
+#define FC_TREE_ATTN_HEAD_DIM 128 /* head dimension the library supports */
 
 /*
  * The attention step of the target model's forward pass over a draft tree
