@@ -448,8 +448,8 @@ fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_
  * All pointers are device memory owned by the caller:
  *   pos, lru_count, hits, lookups, rows_retrieve, rows_tree [n_streams];
  *   lru_key [n_streams][lru][ctx_len]; lru_used [n_streams][lru];
- *   ctx [n_streams][ctx_len]; live [1]: streams still live after the last
- *   step; history [max_steps][n_streams]: the accepted length of each
+ *   ctx [n_streams][ctx_len]; live [2]: live[s & 1] counts the streams
+ *   still live after step s; history [max_steps][n_streams]: the accepted length of each
  *   stream at each step, -1 once the stream is finished;
  *   retrieval outputs (fc_retrieve's, with n_streams * lru rows: row
  *   b * lru + slot is stream b's slot) and workspace for a batch of
@@ -488,8 +488,8 @@ fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_
  * fc_replay_init sets pos = ctx_len, empties every LRU, CACHE and missing
  * table and zeroes the counters.  fc_replay_run runs steps first_step ..
  * first_step + n_steps - 1 (their history rows), first_step + n_steps <=
- * max_steps; read `live` between calls to stop once it is 0.  Errors of the
- * calls it makes are returned as they come.
+ * max_steps; read live[(last step) & 1] between calls to stop once it is
+ * 0.  Errors of the calls it makes are returned as they come.
  */
 typedef struct fc_replay {
   const uint16_t* truth;

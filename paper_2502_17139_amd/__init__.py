@@ -509,7 +509,7 @@ class ReplayEngine:
         self.t = dict(pos=_empty(n, i32, dev), lru_key=_empty((n, lru, ctx_len), torch.uint16, dev),
                       lru_used=_empty((n, lru), i32, dev), lru_count=_empty(n, i32, dev), hits=_empty(n, i32, dev),
                       lookups=_empty(n, i32, dev), ctx=_empty((n, ctx_len), torch.uint16, dev),
-                      rows_retrieve=_empty(n, i32, dev), rows_tree=_empty(n, i32, dev), live=_empty(1, i32, dev),
+                      rows_retrieve=_empty(n, i32, dev), rows_tree=_empty(n, i32, dev), live=_empty(2, i32, dev),
                       history=_empty((max_steps, n), i32, dev), target=_empty((n, c + 1), i32, dev),
                       state=_empty(n, i32, dev))
         # the LRU slots plus one empty row (the bare root of skipped contexts)
@@ -573,7 +573,7 @@ class ReplayEngine:
             _check("fc_replay_run", lib().fc_replay_run(self.views, len(self.stores), ctypes.byref(self.r), step, n,
                                                         st))
             step += n
-            if int(self.t["live"].item()) == 0:
+            if int(self.t["live"][(step - 1) & 1].item()) == 0:
                 break
         hist = self.t["history"][:step].cpu().numpy().astype(np.int64)
         steps = int((hist >= 0).any(axis=1).sum())

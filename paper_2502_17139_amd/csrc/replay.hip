@@ -26,7 +26,9 @@
 //                      true tokens as targets (fc_targets_from_truth and
 //                      fc_verify_accept in one pass), position += accepted
 //                      length, the step's history row, the live count and
-//                      (CACHE on) the CACHE additions.
+//                      (CACHE on) the CACHE additions; without the CACHE it
+//                      also takes the next step's decision (no separate
+//                      k_replay_decide launch).
 // The LRU keeps the exact semantics of an ordered map: slots fill in order,
 // a hit becomes most recent, a miss in a full table replaces the least
 // recently used slot (last-use steps are distinct per stream).
@@ -49,7 +51,7 @@ __device__ __forceinline__ bool control_on(const fc_replay& r) { return r.missin
 
 __global__ void __launch_bounds__(256) k_replay_init(fc_replay r) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b == 0) *r.live = r.ctx_len < r.truth_len ? r.n_streams : 0;
+  if (b == 0) r.live[0] = r.live[1] = 0;
   if (b >= r.n_streams) return;
   r.pos[b] = r.ctx_len;
   r.lru_count[b] = 0;
@@ -126,14 +128,10 @@ __device__ int miss_find(const fc_replay& r, int b, const uint16_t* ctx) {
   return -1 - (int)(h & mask);  // not reached
 }
 
-// One wave per stream: the step's decision and its row maps.
-__global__ void __launch_bounds__(kPrepThreads) k_replay_decide(fc_replay r, int32_t step) {
+// One wave: stream b's decision for `step` at position p, and its row maps.
+__device__ void decide_stream(const fc_replay& r, int b, int32_t step, int p) {
   const int lane = fc::lane_id();
-  const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
-  if (blockIdx.x == 0 && threadIdx.x == 0) *r.live = 0;
-  if (b >= r.n_streams) return;
   const int L = r.ctx_len, lru = r.lru;
-  const int p = r.pos[b];
   if (p >= r.truth_len) {  // finished: no retrieval, no tree row
     if (lane == 0) {
       r.rows_retrieve[b] = -1;
@@ -219,6 +217,11 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_decide(fc_replay r, int
     r.rows_tree[b] = row;
     r.state[b] = kNeed;
   }
+}
+
+__global__ void __launch_bounds__(kPrepThreads) k_replay_decide(fc_replay r, int32_t step) {
+  const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
+  if (b < r.n_streams) decide_stream(r, b, step, r.pos[b]);
 }
 
 // One wave per stream: a looked-up context whose result is empty enters the
@@ -309,15 +312,20 @@ __device__ void cache_add(const fc_replay& r, int b, CacheState& st, const uint1
 // at pos + pos_ids[i], -1 past the stream or for rows past num_nodes), the
 // history row, the new position, the live count and (CACHE on) the CACHE
 // additions of this step.
-__global__ void __launch_bounds__(kPrepThreads) k_replay_finish(fc_replay r, int32_t step) {
+// With decide_next (no CACHE), the same wave then takes the next step's
+// decision for its stream.  live[step & 1] counts the streams live after
+// the step; this launch clears the other counter for the next step.
+__global__ void __launch_bounds__(kPrepThreads) k_replay_finish(fc_replay r, int32_t step, int decide_next) {
   const int lane = fc::lane_id();
   const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
+  if (blockIdx.x == 0 && threadIdx.x == 0) r.live[(step + 1) & 1] = 0;
   if (b >= r.n_streams) return;
   int32_t* hist = r.history + (int64_t)step * r.n_streams;
   const int p = r.pos[b];
   const int tlen = r.truth_len, L = r.ctx_len;
   if (p >= tlen) {
     if (lane == 0) hist[b] = -1;
+    if (decide_next) decide_stream(r, b, step + 1, p);
     return;
   }
   const int R = r.tp.c + 1;
@@ -364,8 +372,9 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_finish(fc_replay r, int
   if (lane == 0) {
     hist[b] = a;
     r.pos[b] = np;
-    if (np < tlen) atomicAdd(r.live, 1);
+    if (np < tlen) atomicAdd(&r.live[step & 1], 1);
   }
+  if (decide_next) decide_stream(r, b, step + 1, np);
 }
 
 fc_status check_replay(const fc_replay* r) {
@@ -437,9 +446,11 @@ extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_r
                             r->c_cont_tok, r->rows_cache, B, stream);
       if (s != FC_OK) return s;
     }
-    hipLaunchKernelGGL(k_replay_decide, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
-                       step);
-    FC_CHECK_LAUNCH();
+    if (cache || i == 0) {  // otherwise the previous step's finish took this step's decision
+      hipLaunchKernelGGL(k_replay_decide, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
+                         step);
+      FC_CHECK_LAUNCH();
+    }
     s = fc_retrieve(stores, S, r->ctx, B, r->ctx_len, r->rp, r->match_n, r->range_lo, r->range_cnt, r->taken,
                     r->cont_pos, r->cont_src, r->cont_len, r->cont_tok, r->rows_retrieve, n_rows, r->retrieve_ws,
                     r->retrieve_ws_bytes, stream);
@@ -463,7 +474,7 @@ extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_r
     }
     (void)hipGetLastError();
     hipLaunchKernelGGL(k_replay_finish, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
-                       step);
+                       step, (!cache && i + 1 < n_steps) ? 1 : 0);
     FC_CHECK_LAUNCH();
   }
   return FC_OK;
