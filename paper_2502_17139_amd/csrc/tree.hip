@@ -473,7 +473,10 @@ struct Scan2 {
   }
 };
 
-template <int NT, int MAXM>
+// NARROW: every store has the same alpha and alpha * k fits 16 bits, so the
+// alpha prefix sums are linear and every node weight is stored as is; the
+// hot loops are compiled without the general paths.
+template <int NT, int MAXM, bool NARROW>
 __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__ taken,
                                                   const uint8_t* __restrict__ cont_len,
                                                   const uint16_t* __restrict__ cont_tok,
@@ -638,7 +641,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   const int seg1 = s_seg[1 < S ? 1 : S], seg2 = s_seg[2 < S ? 2 : S], seg3 = s_seg[3 < S ? 3 : S];
   auto store_of = [&](int i) -> int { return (S > 1 && i >= seg1) + (S > 2 && i >= seg2) + (S > 3 && i >= seg3); };
   // with one weight for every store the alpha prefix sum is linear
-  const bool alpha_flat = (S < 2 || alpha.a[1] == alpha.a[0]) && (S < 3 || alpha.a[2] == alpha.a[0]) &&
+  const bool alpha_flat = NARROW || (S < 2 || alpha.a[1] == alpha.a[0]) && (S < 3 || alpha.a[2] == alpha.a[0]) &&
                           (S < 4 || alpha.a[3] == alpha.a[0]);
   const bool even_m = (m & 1) == 0;  // rows are 4-byte aligned in LDS
   auto rcmp = [&](int i, int j) -> int {
@@ -804,7 +807,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     //    The histogram serves step 5: weights 1 and 2 (the bulk: unshared
     //    continuation tails) are counted in registers, other weights below
     //    256 with LDS atomics, heavier ones lumped.
-    const bool wide = root_w > 0xFFFFu;
+    const bool wide = !NARROW && root_w > 0xFFFFu;
     {
       uint32_t r1 = 0, r2 = 0, rbig = 0;
       for (int q = p1 - 1; q >= p0; --q) {
@@ -1069,7 +1072,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   if (tid == 0) num_nodes[b] = err ? -1 : num;
 }
 
-template <int MAXM>
+template <int MAXM, bool NARROW>
 fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok, const uint16_t* ctx,
                       int32_t B, int32_t L, int32_t S, int32_t k, int32_t m, fc_tree_params t, Alpha a,
                       const TreeLayout& full, int32_t* num_nodes, int32_t* node_tok, int32_t* parent,
@@ -1087,21 +1090,21 @@ fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint1
   else if ((((uintptr_t)cont_tok) & 3) == 0 && ((size_t)k * m) % 2 == 0) words = 1;
   const TreeLayout small = tree_layout(t_small, m, true);
   if (small.total > 64 * 1024)
-    (void)hipFuncSetAttribute((const void*)k_tree_fast<256, MAXM>, hipFuncAttributeMaxDynamicSharedMemorySize,
+    (void)hipFuncSetAttribute((const void*)k_tree_fast<256, MAXM, NARROW>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)small.total);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((k_tree_fast<256, MAXM>), dim3(B + 1), dim3(256), small.total, stream, taken, cont_len, cont_tok,
-                     ctx, L, S, k, m, t.c, a, nullptr, nullptr, lists + B, counts + 1, B, t_small, words, rows,
-                     n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
+  hipLaunchKernelGGL((k_tree_fast<256, MAXM, NARROW>), dim3(B + 1), dim3(256), small.total, stream, taken, cont_len,
+                     cont_tok, ctx, L, S, k, m, t.c, a, nullptr, nullptr, lists + B, counts + 1, B, t_small, words,
+                     rows, n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
   FC_CHECK_LAUNCH();
   if (k > t_small) {
     if (full.total > 64 * 1024)
-      (void)hipFuncSetAttribute((const void*)k_tree_fast<1024, MAXM>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)full.total);
+      (void)hipFuncSetAttribute((const void*)k_tree_fast<1024, MAXM, NARROW>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)full.total);
     (void)hipGetLastError();
-    hipLaunchKernelGGL((k_tree_fast<1024, MAXM>), dim3(B), dim3(1024), full.total, stream, taken, cont_len, cont_tok,
-                       ctx, L, S, k, m, t.c, a, lists + B, counts + 1, nullptr, nullptr, B, k, words, rows, n_rows,
-                       num_nodes, node_tok, parent, weight, pos_ids, mask);
+    hipLaunchKernelGGL((k_tree_fast<1024, MAXM, NARROW>), dim3(B), dim3(1024), full.total, stream, taken, cont_len,
+                       cont_tok, ctx, L, S, k, m, t.c, a, lists + B, counts + 1, nullptr, nullptr, B, k, words, rows,
+                       n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
     FC_CHECK_LAUNCH();
   }
   return FC_OK;
@@ -1137,10 +1140,20 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
   const TreeLayout full = tree_layout(k, m);
   if (full.total + static_lds > (size_t)max_lds) return FC_ERR_UNSUPPORTED;
   (void)hipGetLastError();
-  if (m <= 10) return launch_fast<10>(taken, cont_len, cont_tok, ctx, B, L, S, k, m, t, a, full, num_nodes, node_tok,
-                                      parent, weight, pos_ids, mask, rows, n_rows, ws, stream);
-  if (m <= 16) return launch_fast<16>(taken, cont_len, cont_tok, ctx, B, L, S, k, m, t, a, full, num_nodes, node_tok,
-                                      parent, weight, pos_ids, mask, rows, n_rows, ws, stream);
+  bool narrow = (uint64_t)t.alpha[0] * (uint64_t)k <= 0xFFFFull;
+  for (int s = 1; s < S; ++s) narrow = narrow && t.alpha[s] == t.alpha[0];
+#define FC_FAST(MM, NN)                                                                                              \
+  return launch_fast<MM, NN>(taken, cont_len, cont_tok, ctx, B, L, S, k, m, t, a, full, num_nodes, node_tok, parent, \
+                             weight, pos_ids, mask, rows, n_rows, ws, stream)
+  if (m <= 10) {
+    if (narrow) FC_FAST(10, true);
+    FC_FAST(10, false);
+  }
+  if (m <= 16) {
+    if (narrow) FC_FAST(16, true);
+    FC_FAST(16, false);
+  }
+#undef FC_FAST
   if (full.total > 64 * 1024)
     (void)hipFuncSetAttribute((const void*)k_tree_any, hipFuncAttributeMaxDynamicSharedMemorySize, (int)full.total);
   (void)hipGetLastError();
