@@ -9,10 +9,12 @@
 // search of a one-store datastore holding that text:
 //   1. agreement: for every end position e, how many tokens before e agree
 //      with the end of the context (capped at n_hi); the longest agreement
-//      is the match length n, and the occurrences of the n-token suffix are
-//      the positions where it reaches n;
-//   2. range_lo: the number of suffixes of the text below the pattern;
-//   3. the occurrences, sorted into suffix order by a bitonic sort in LDS;
+//      is the match length n;
+//   2. one comparison of every suffix with the n-token pattern gives
+//      range_lo (the suffixes below it) and the occurrences (the suffixes
+//      that start with it), numbered in text order by a block scan;
+//   3. the occurrences in suffix order: ranks by counting pairwise
+//      comparisons when there are at most 32, else a bitonic sort in LDS;
 //   4. the kept ones (strided floor(i*cnt/k) beyond k) and their
 //      continuations, cut before a 0 and at the end of the text.
 #include <hip/hip_runtime.h>
@@ -35,14 +37,25 @@ __host__ __device__ inline uint32_t pow2_at_least(uint32_t x) {
 
 // Suffix a below suffix b of T[0..len), knowing their first `from` tokens
 // agree (a != b, so one is a proper prefix of the other or they differ).
+// Eight tokens of each are read per LDS round trip: CACHE texts repeat, so
+// suffixes that share q often agree far beyond it.
 __device__ __forceinline__ bool suffix_less(const uint16_t* T, uint32_t len, uint32_t a, uint32_t b, int from) {
   if (a == kNone) return false;
   if (b == kNone) return true;
-  for (uint32_t x = (uint32_t)from;; ++x) {
-    if (a + x == len) return true;   // a ends first: the shorter is smaller
-    if (b + x == len) return false;
-    const uint16_t ta = T[a + x], tb = T[b + x];
-    if (ta != tb) return ta < tb;
+  for (uint32_t x0 = (uint32_t)from;; x0 += 8) {
+    uint16_t ta[8], tb[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      ta[u] = a + x0 + u < len ? T[a + x0 + u] : (uint16_t)0;
+      tb[u] = b + x0 + u < len ? T[b + x0 + u] : (uint16_t)0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t x = x0 + (uint32_t)u;
+      if (a + x == len) return true;  // a ends first: the shorter is smaller
+      if (b + x == len) return false;
+      if (ta[u] != tb[u]) return ta[u] < tb[u];
+    }
   }
 }
 
@@ -69,7 +82,12 @@ __global__ void __launch_bounds__(kCacheThreads) k_cache_retrieve(
   uint32_t* occ = (uint32_t*)(smem + (((size_t)stride * 2 + 15) & ~(size_t)15));
 
   const uint16_t* src = texts + (int64_t)(have ? tr : 0) * stride;
-  for (uint32_t i = tid; i < len; i += kCacheThreads) T[i] = src[i];
+  uint32_t head = 0;  // tokens loaded 16 bytes at a time
+  if ((((uintptr_t)src) & 15) == 0) {
+    head = len & ~7u;
+    for (uint32_t v = tid; v < (head >> 3); v += kCacheThreads) ((uint4*)T)[v] = ((const uint4*)src)[v];
+  }
+  for (uint32_t i = head + tid; i < len; i += kCacheThreads) T[i] = src[i];
   const int nq = L < FC_MAX_NMAX ? L : FC_MAX_NMAX;
   if (tid < nq) s_q[FC_MAX_NMAX - nq + tid] = ctx[(int64_t)b * L + (L - nq + tid)];
   __syncthreads();
@@ -83,14 +101,29 @@ __global__ void __launch_bounds__(kCacheThreads) k_cache_retrieve(
   const int n_hi = s_nhi;
   const uint16_t* qend = s_q + FC_MAX_NMAX;  // qend[-1] is the last context token
 
-  // 1. longest agreement over every end position
+  // 1. longest agreement over every end position.  The token before e is
+  //    checked first; only where it equals the context's last token are the
+  //    tokens before it read, all at once.
   uint32_t best = 0;
-  if (n_hi >= n_min)
+  if (n_hi >= n_min) {
+    uint16_t qr[FC_MAX_NMAX];  // qr[l] = the l-th token from the end of the context
+#pragma unroll
+    for (int l = 0; l < FC_MAX_NMAX; ++l) qr[l] = l < n_hi ? qend[-1 - l] : (uint16_t)0;
     for (uint32_t e = tid + 1; e <= len; e += kCacheThreads) {
-      uint32_t l = 0;
-      while ((int)l < n_hi && l < e && T[e - 1 - l] == qend[-1 - (int)l]) ++l;
-      best = l > best ? l : best;
+      if (T[e - 1] != qr[0]) continue;
+      uint16_t t[FC_MAX_NMAX];
+#pragma unroll
+      for (int l = 1; l < FC_MAX_NMAX; ++l) t[l] = (l < n_hi && (uint32_t)l < e) ? T[e - 1 - l] : (uint16_t)0;
+      uint32_t a = 1;
+      bool on = true;
+#pragma unroll
+      for (int l = 1; l < FC_MAX_NMAX; ++l) {
+        on = on && l < n_hi && (uint32_t)l < e && t[l] == qr[l];
+        a += on ? 1u : 0u;
+      }
+      best = a > best ? a : best;
     }
+  }
   best = fc::block_max<uint32_t>(best, s_red);
   const int n = (n_hi >= n_min && (int)best >= n_min) ? (int)best : 0;
   const int64_t o = row;  // one source
@@ -103,61 +136,81 @@ __global__ void __launch_bounds__(kCacheThreads) k_cache_retrieve(
     }
     return;
   }
-  const uint16_t* q = qend - n;
 
-  // occurrences of q (start j: T[j..j+n) == q), compacted in text order
-  const uint32_t span = len >= (uint32_t)n ? len - (uint32_t)n + 1 : 0u;
-  const uint32_t per = (span + kCacheThreads - 1) / kCacheThreads;
-  const uint32_t j0 = tid * per < span ? tid * per : span;
-  const uint32_t j1 = j0 + per < span ? j0 + per : span;
-  auto is_occ = [&](uint32_t j) -> bool {
-    for (int x = 0; x < n; ++x)
-      if (T[j + x] != q[x]) return false;
-    return true;
-  };
-  uint32_t mine = 0;
-  for (uint32_t j = j0; j < j1; ++j) mine += is_occ(j) ? 1u : 0u;
-  uint32_t cnt;
-  uint32_t at = fc::block_excl_sum<uint32_t>(mine, s_red, &cnt);
-  for (uint32_t j = j0; j < j1; ++j)
-    if (is_occ(j)) occ[at++] = j;
-  const uint32_t Pc = pow2_at_least(cnt);
-  for (uint32_t i = cnt + tid; i < Pc; i += kCacheThreads) occ[i] = kNone;
-
-  // 2. suffixes of the text below q
-  uint32_t below = 0;
-  for (uint32_t i = tid; i < len; i += kCacheThreads) {
-    int c = 0;
-    for (int x = 0; x < n; ++x) {
-      if (i + x == len) {
-        c = -1;
-        break;
-      }
-      if (T[i + x] != q[x]) {
-        c = T[i + x] < q[x] ? -1 : 1;
-        break;
+  // 2. one pass over the suffixes, in contiguous chunks: each is compared
+  //    with the n-token pattern q (eight tokens per LDS round trip) and is
+  //    below it, starts with it (an occurrence) or is above it.  A chunk has
+  //    at most FC_MAX_CACHE_TOKENS / kCacheThreads = 16 suffixes, so its
+  //    occurrences fit a bit mask; one block scan of (below << 16 | occurrences)
+  //    numbers the occurrences in text order and totals both (each total is at
+  //    most 16,384, so the halves never carry into each other).
+  uint16_t qv[FC_MAX_NMAX];
+#pragma unroll
+  for (int x = 0; x < FC_MAX_NMAX; ++x) qv[x] = x < n ? qend[x - n] : (uint16_t)0;
+  auto cmp_q = [&](uint32_t i) -> int {
+#pragma unroll
+    for (int x0 = 0; x0 < FC_MAX_NMAX; x0 += 8) {
+      if (x0 >= n) return 0;
+      uint16_t t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = (x0 + u < n && i + x0 + u < len) ? T[i + x0 + u] : (uint16_t)0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int x = x0 + u;
+        if (x >= n) return 0;
+        if (i + x >= len) return -1;  // the suffix ends first: a proper prefix of q
+        if (t[u] != qv[x]) return t[u] < qv[x] ? -1 : 1;
       }
     }
-    below += c < 0 ? 1u : 0u;
+    return 0;
+  };
+  const uint32_t per = (len + kCacheThreads - 1) / kCacheThreads;
+  const uint32_t i0 = tid * per < len ? tid * per : len;
+  const uint32_t i1 = i0 + per < len ? i0 + per : len;
+  uint32_t occ_bits = 0, packed = 0;
+  for (uint32_t i = i0; i < i1; ++i) {
+    const int c = cmp_q(i);
+    packed += c < 0 ? (1u << 16) : (c == 0 ? 1u : 0u);
+    occ_bits |= c == 0 ? (1u << (i - i0)) : 0u;
   }
-  below = fc::block_sum<uint32_t>(below, s_red);
+  uint32_t tot;
+  uint32_t at = fc::block_excl_sum<uint32_t>(packed, s_red, &tot) & 0xFFFFu;
+  const uint32_t cnt = tot & 0xFFFFu, below = tot >> 16;
+  for (uint32_t bits = occ_bits; bits; bits &= bits - 1) occ[at++] = i0 + (uint32_t)__builtin_ctz(bits);
+  const uint32_t Pc = pow2_at_least(cnt);
+  for (uint32_t i = cnt + tid; i < Pc; i += kCacheThreads) occ[i] = kNone;
+  __syncthreads();
 
-  // 3. suffix order (every occurrence starts with q: compare from offset n)
-  for (uint32_t k2 = 2; k2 <= Pc; k2 <<= 1) {
-    for (uint32_t j2 = k2 >> 1; j2 > 0; j2 >>= 1) {
-      for (uint32_t i = tid; i < Pc; i += kCacheThreads) {
-        const uint32_t x = i ^ j2;
-        if (x > i) {
-          const uint32_t a = occ[i], c = occ[x];
-          const bool up = (i & k2) == 0;
-          const bool swap = up ? suffix_less(T, len, c, a, n) : suffix_less(T, len, a, c, n);
-          if (swap) {
-            occ[i] = c;
-            occ[x] = a;
+  // 3. suffix order (every occurrence starts with q: compare from offset n).
+  //    Up to 32 occurrences, thread (i, j) = (tid / 32, tid % 32) tells
+  //    whether occurrence j's suffix is below occurrence i's and a ballot
+  //    over i's 32 lanes gives i's rank; more take a bitonic sort.
+  if (cnt <= 32) {
+    const uint32_t i = (uint32_t)tid >> 5, j = (uint32_t)tid & 31u;
+    const bool lt = i < cnt && j < cnt && j != i && suffix_less(T, len, occ[j], occ[i], n);
+    const uint64_t bl = fc::ballot(lt);
+    const uint32_t rank = (uint32_t)__builtin_popcount((tid & 32) ? (uint32_t)(bl >> 32) : (uint32_t)bl);
+    const uint32_t mine = (i < cnt && j == 0) ? occ[i] : 0u;
+    __syncthreads();
+    if (i < cnt && j == 0) occ[rank] = mine;
+    __syncthreads();
+  } else {
+    for (uint32_t k2 = 2; k2 <= Pc; k2 <<= 1) {
+      for (uint32_t j2 = k2 >> 1; j2 > 0; j2 >>= 1) {
+        for (uint32_t i = tid; i < Pc; i += kCacheThreads) {
+          const uint32_t x = i ^ j2;
+          if (x > i) {
+            const uint32_t a = occ[i], c = occ[x];
+            const bool up = (i & k2) == 0;
+            const bool swap = up ? suffix_less(T, len, c, a, n) : suffix_less(T, len, a, c, n);
+            if (swap) {
+              occ[i] = c;
+              occ[x] = a;
+            }
           }
         }
+        __syncthreads();
       }
-      __syncthreads();
     }
   }
 
