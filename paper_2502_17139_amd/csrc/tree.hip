@@ -504,6 +504,8 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   __shared__ uint16_t s_sel_t[FC_MAX_TREE_ROWS];  // token of a kept node (light launch)
   __shared__ int16_t s_par[FC_MAX_TREE_ROWS];
   __shared__ uint64_t s_dball[FC_MAX_TREE_ROWS / fc::kWave][MAXM];
+  __shared__ uint64_t s_shallow[FC_MAX_TREE_ROWS / fc::kWave][MAXM + 1];
+  __shared__ int16_t s_end[FC_MAX_TREE_ROWS];
   __shared__ uint32_t s_pick[3];
 
   const int tid = threadIdx.x;
@@ -578,7 +580,6 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   const TreeLayout lay = tree_layout(t_hi, m, kSepE);
   uint16_t* str = (uint16_t*)(smem + lay.str);
   uint16_t* E = (uint16_t*)(smem + lay.E);
-  uint32_t* anc = (uint32_t*)(smem + lay.str);
   uint32_t* A = (uint32_t*)(smem + lay.A);
   uint16_t* perm = (uint16_t*)(smem + lay.perm);
   uint8_t* len = smem + lay.len;
@@ -1019,7 +1020,10 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     __syncthreads();
   }
 
-  // 7. rows, then the mask from ancestor bitsets (E is dead by now)
+  // 7. rows, then the mask.  Rows are in preorder and the kept set is
+  //    ancestor-closed, so row j's subtree is the run of rows from j up to
+  //    the next row at j's depth or shallower (end(j)), and A[i][j] = 1
+  //    exactly when j <= i < end(j).
   const int num = err ? 0 : 1 + nsel;
   for (int r = tid; r < R; r += NT) {
     const int64_t out = (int64_t)b * R + r;
@@ -1043,31 +1047,33 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
     weight[out] = wt;
     pos_ids[out] = ps;
   }
-  const int words_per_row = (R + 31) >> 5;
-  for (int i = tid; i < R * words_per_row; i += NT) anc[i] = 0;
-  __syncthreads();
-  for (int r = tid; r < num; r += NT) {
-    int j = r;
-    while (j >= 0) {
-      anc[r * words_per_row + (j >> 5)] |= 1u << (j & 31);
-      j = (j == 0) ? -1 : s_par[j];
+  // end(j) from one ballot per group of 64 rows and depth D of the rows at
+  // depth <= D: the first such row after j, in j's group or a later one.
+  for (int g = w; g * fc::kWave < num; g += NW) {
+    const int r = g * fc::kWave + lane;
+    const int d = r < num ? (int)s_sel_d[r] : MAXM + 1;
+#pragma unroll
+    for (int D = 0; D <= MAXM; ++D) {
+      const uint64_t bl = fc::ballot(d <= D);
+      if (lane == 0) s_shallow[g][D] = bl;
     }
   }
   __syncthreads();
+  for (int r = tid; r < num; r += NT) {
+    const int g = r / fc::kWave, d = s_sel_d[r];
+    uint64_t bl = s_shallow[g][d] & ~((2ull << (r % fc::kWave)) - 1ull);  // rows after r in its group
+    int gg = g;
+    while (bl == 0 && (gg + 1) * fc::kWave < num) bl = s_shallow[++gg][d];
+    s_end[r] = (int16_t)(bl ? gg * fc::kWave + __builtin_ctzll(bl) : num);
+  }
+  __syncthreads();
+  // each thread owns one column j (NT >= R) and every (NT / R)-th row of it
   const int64_t mbase = (int64_t)b * R * R;
-  {
-    // element e = i*R + j, (i, j) stepped without a division per element
-    int i = tid / R, j = tid - (tid / R) * R;
-    const int di = NT / R, dj = NT - (NT / R) * R;
-    for (int e = tid; e < R * R; e += NT) {
-      mask[mbase + e] = (i < num) ? (int32_t)((anc[i * words_per_row + (j >> 5)] >> (j & 31)) & 1u) : 0;
-      i += di;
-      j += dj;
-      if (j >= R) {
-        j -= R;
-        ++i;
-      }
-    }
+  const int col = tid % R, row_step = NT / R;
+  if (tid / R < row_step) {
+    const int end_j = col < num ? (int)s_end[col] : -1;
+    for (int i = tid / R; i < R; i += row_step)
+      mask[mbase + (int64_t)i * R + col] = (col <= i && i < end_j) ? 1 : 0;
   }
   if (tid == 0) num_nodes[b] = err ? -1 : num;
 }
