@@ -491,6 +491,84 @@ def test_unsorted_slots_are_flagged():
         assert (host(t[f])[1] == o[f][0]).all()
 
 
+def _sorted_slots(rng, T: int, m: int, vocab: int) -> tuple:
+    """T continuations of lengths 0..m over a small vocabulary (long shared
+    prefixes), in the order a store hands them over: lexicographic, a
+    prefix before its extensions."""
+    rows = []
+    for _ in range(T):
+        n = m if rng.random() < 0.7 else int(rng.integers(0, m + 1))
+        rows.append(tuple(int(x) for x in rng.integers(1, vocab + 1, size=n)))
+    rows.sort()
+    lens = np.array([len(r) for r in rows], np.uint8)
+    toks = np.zeros((T, m), np.uint16)
+    for i, r in enumerate(rows):
+        toks[i, :len(r)] = r
+    return lens, toks
+
+
+def _largest_k(m: int) -> int:
+    """The largest k whose LDS layout the tree kernels accept for m (found
+    through the entry point itself: past it the call is refused before any
+    launch)."""
+    def ok(k):
+        taken = dev(np.zeros((1, 1), np.int32))
+        try:
+            fc.fc_build_tree(taken, dev(np.zeros((1, k), np.uint8)), dev(np.zeros((1, k, m), np.uint16)),
+                             dev(np.ones((1, 2), np.uint16)), c=4, alpha=(1,))
+            return True
+        except fc.FcError as e:
+            assert "UNSUPPORTED" in str(e), e
+            return False
+    lo, hi = 1, 65535
+    assert ok(lo)
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        if ok(mid):
+            lo = mid
+        else:
+            hi = mid - 1
+    return lo
+
+
+@pytest.mark.parametrize("m", [2, 10, 255])
+def test_tree_at_maximum_sizes(m):
+    """c = 255 (256 rows: four row groups), k at the largest LDS layout the
+    kernels take for m (up to ~12,000 slots: a dozen positions per thread in
+    the heavy launch; m = 255 is the general kernel), two stores with
+    unequal weights and with equal ones; k + 1 is refused."""
+    torch.cuda.synchronize()
+    k = _largest_k(m)
+    say(f"tree maximum sizes m={m}: k={k}")
+    assert k >= 200
+    rng = np.random.default_rng(m)
+    c, S, B = 255, 2, 5
+    totals = [k, k - 1, min(k, 300), min(k, 257), 2]
+    taken = np.zeros((B, S), np.int32)
+    lens = np.zeros((B, k), np.uint8)
+    toks = np.zeros((B, k, m), np.uint16)
+    for b, T in enumerate(totals):
+        t0 = int(rng.integers(0, T + 1)) if b % 2 else T // 2
+        taken[b] = (t0, T - t0)
+        at = 0
+        for s in range(S):
+            ln, tk = _sorted_slots(rng, int(taken[b, s]), m, 3 if b < 2 else 5)
+            lens[b, at:at + len(ln)] = ln
+            toks[b, at:at + len(ln)] = tk
+            at += len(ln)
+    ctx = rng.integers(1, 6, size=(B, 4)).astype(np.uint16)
+    for alpha in ((1, 1), (3, 1)):
+        t = fc.fc_build_tree(dev(taken), dev(lens), dev(toks), dev(ctx), c=c, alpha=alpha)
+        torch.cuda.synchronize()
+        o = oracle.build_tree(taken, lens, toks, ctx, c=c, alpha=alpha)
+        compare_tree({f: host(v) for f, v in t.items()}, o)
+        if m >= 10:
+            assert (o["num_nodes"][:2] == c + 1).all()
+    with pytest.raises(fc.FcError):
+        fc.fc_build_tree(dev(np.zeros((1, 1), np.int32)), dev(np.zeros((1, k + 1), np.uint8)),
+                         dev(np.zeros((1, k + 1, m), np.uint16)), dev(np.ones((1, 2), np.uint16)), c=c, alpha=(1,))
+
+
 def test_repeat_runs_are_identical():
     """Same call twice gives the same bytes (no order-dependent races)."""
     t = synth.store(1, "single")
