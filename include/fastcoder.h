@@ -465,8 +465,12 @@ fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_
  * step's draw skip_draws[step][b] is below skip_thr).  Per step, for a live
  * stream whose CACHE holds at least cache_l sequences the context is first
  * searched in the CACHE's text (fc_cache_retrieve, results in the c_*
- * arrays, row b); a non-empty result is "served": its tree is built from
- * it alone (one source, weight 1) and the datastores are not touched.
+ * arrays, row b); a non-empty result is "served": it is copied into the
+ * stream's own retrieval row n_streams * lru + 1 + b as the first store's
+ * slots (the other stores' counts 0), its tree is built from it alone and
+ * the datastores are not touched.  A served tree's weights are therefore
+ * tp.alpha[0] per slot instead of 1 (the same nodes and order; tp.alpha[0]
+ * must not be 0 with the CACHE on).
  * Otherwise the missing table and then the skip gate may skip the context
  * (its tree is the bare root read from retrieval row n_streams * lru, which
  * fc_replay_init empties), else the LRU step above runs and, with the
@@ -479,11 +483,12 @@ fc_status fc_targets_from_truth(const uint16_t* truth, int32_t truth_len, int64_
  * Extra device arrays (caller-owned): ctext [n_streams][cache_cap], clen,
  * seq_head, seq_count, chunks, served, rows_cache, state [n_streams],
  * seq_len [n_streams][max_seqs] (max_seqs >= (cache_cap + 1) / 2 + 1); CACHE
- * retrieval outputs (S = 1) and a second set of tree outputs for
- * n_streams; miss_key [n_streams][miss_cap][ctx_len], miss_used
+ * retrieval outputs (S = 1) for n_streams (c_num_nodes .. c_mask are not
+ * used and may be NULL); miss_key [n_streams][miss_cap][ctx_len], miss_used
  * [n_streams][miss_cap] (miss_cap a power of two above max_steps), m_skips,
  * g_skips [n_streams]; skip_draws [max_steps][n_streams].  With the
- * control on, the retrieval outputs need n_streams * lru + 1 rows.
+ * control on, the retrieval outputs need n_streams * lru + 1 rows; with the
+ * CACHE on, n_streams * lru + 1 + n_streams.
  *
  * fc_replay_init sets pos = ctx_len, empties every LRU, CACHE and missing
  * table and zeroes the counters.  fc_replay_run runs steps first_step ..
@@ -556,7 +561,7 @@ typedef struct fc_replay {
   uint8_t* c_cont_src;
   uint8_t* c_cont_len;
   uint16_t* c_cont_tok;
-  int32_t* c_num_nodes;
+  int32_t* c_num_nodes; /* not used (may be NULL) */
   int32_t* c_node_tok;
   int32_t* c_parent;
   uint32_t* c_weight;

@@ -512,11 +512,12 @@ class ReplayEngine:
                       rows_retrieve=_empty(n, i32, dev), rows_tree=_empty(n, i32, dev), live=_empty(2, i32, dev),
                       history=_empty((max_steps, n), i32, dev), target=_empty((n, c + 1), i32, dev),
                       state=_empty(n, i32, dev))
-        # the LRU slots plus one empty row (the bare root of skipped contexts)
-        self.t.update(retrieve_outputs(n * lru + 1, S, k, m, dev))
+        self.cache_on = cache_l is not None
+        # the LRU slots, one empty row (the bare root of skipped contexts) and,
+        # with the CACHE, one row per stream for its served CACHE result
+        self.t.update(retrieve_outputs(n * lru + 1 + (n if self.cache_on else 0), S, k, m, dev))
         self.t.update(tree_outputs(n, c, dev))
         self.t.update(accept_outputs(n, m, dev))
-        self.cache_on = cache_l is not None
         self.control_on = bool(missing) or skip_tok is not None
         if self.cache_on:
             max_seqs = (cache_cap + 1) // 2 + 1
@@ -525,7 +526,6 @@ class ReplayEngine:
                           seq_count=_empty(n, i32, dev), chunks=_empty(n, i32, dev), served=_empty(n, i32, dev),
                           rows_cache=_empty(n, i32, dev))
             self.t.update({"c_" + f: v for f, v in retrieve_outputs(n, 1, k, m, dev).items()})
-            self.t.update({"c_" + f: v for f, v in tree_outputs(n, c, dev).items()})
         miss_cap = 64
         while miss_cap <= max_steps:
             miss_cap *= 2

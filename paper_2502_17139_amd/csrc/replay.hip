@@ -12,23 +12,26 @@
 //
 // Everything a step decides lives on the GPU, so a step is a fixed chain of
 // launches on one stream with no host round trip:
-//   k_replay_context   (CACHE on) the context and the CACHE row map;
+//   k_replay_context   (CACHE on, first step of a call) the context and the
+//                      CACHE row map;
 //   fc_cache_retrieve  (CACHE on) streams whose CACHE is old enough;
-//   k_replay_decide    one wave per stream: served by the CACHE, else the
-//                      missing table and the skip gate, else the LRU probe
-//                      (keys compared by the lanes, the least recent slot
-//                      by a wave minimum); the row maps;
+//   k_replay_decide    one wave per stream: served by the CACHE (its result
+//                      is copied into the stream's own row after the LRU
+//                      rows, so one tree call serves both kinds of
+//                      stream), else the missing table and the skip gate,
+//                      else the LRU probe (keys compared by the lanes, the
+//                      least recent slot by a wave minimum); the row maps;
 //   fc_retrieve        misses into their LRU slot (everything else skipped);
 //   k_replay_missing   (table on) empty results enter the missing table;
-//   fc_build_tree      from the datastore slots (and, CACHE on, a second one
-//                      from the CACHE results, merged by k_replay_merge);
+//   fc_build_tree      from the mapped rows;
 //   k_replay_finish    one wave per stream: the acceptance walk with the
 //                      true tokens as targets (fc_targets_from_truth and
 //                      fc_verify_accept in one pass), position += accepted
 //                      length, the step's history row, the live count and
-//                      (CACHE on) the CACHE additions; without the CACHE it
-//                      also takes the next step's decision (no separate
-//                      k_replay_decide launch).
+//                      (CACHE on) the CACHE additions; then, within a call,
+//                      the next step's context and CACHE row map (CACHE on)
+//                      or the next step's decision (CACHE off), so those
+//                      launches run only on a call's first step.
 // The LRU keeps the exact semantics of an ordered map: slots fill in order,
 // a hit becomes most recent, a miss in a full table replaces the least
 // recently used slot (last-use steps are distinct per stream).
@@ -129,7 +132,11 @@ __device__ int miss_find(const fc_replay& r, int b, const uint16_t* ctx) {
 }
 
 // One wave: stream b's decision for `step` at position p, and its row maps.
-__device__ void decide_stream(const fc_replay& r, int b, int32_t step, int p) {
+// Row of stream b's CACHE result in the retrieval outputs (CACHE on): after
+// the n_streams * lru LRU rows and the empty row.
+__device__ __forceinline__ int cache_row(const fc_replay& r, int b) { return r.n_streams * r.lru + 1 + b; }
+
+__device__ void decide_stream(const fc_replay& r, int S, int b, int32_t step, int p) {
   const int lane = fc::lane_id();
   const int L = r.ctx_len, lru = r.lru;
   if (p >= r.truth_len) {  // finished: no retrieval, no tree row
@@ -149,9 +156,21 @@ __device__ void decide_stream(const fc_replay& r, int b, int32_t step, int p) {
   if (cache_on(r)) {
     const bool served = r.rows_cache[b] >= 0 && r.c_taken[b] > 0;
     if (served) {
+      // the CACHE result as a retrieval row: all its slots from the first
+      // store (the CACHE is searched as one store), none from the others
+      const int row = cache_row(r, b);
+      const int T = r.c_taken[b];
+      const int k = r.rp.k, m = r.rp.m;
+      if (lane < S) r.taken[(int64_t)row * S + lane] = lane == 0 ? T : 0;
+      const uint8_t* sl = r.c_cont_len + (int64_t)b * k;
+      uint8_t* dl = r.cont_len + (int64_t)row * k;
+      for (int i = lane; i < T; i += fc::kWave) dl[i] = sl[i];
+      const uint16_t* stk = r.c_cont_tok + (int64_t)b * k * m;
+      uint16_t* dtk = r.cont_tok + (int64_t)row * k * m;
+      for (int64_t e = lane; e < (int64_t)T * m; e += fc::kWave) dtk[e] = stk[e];
       if (lane == 0) {
         r.rows_retrieve[b] = -1;
-        r.rows_tree[b] = -1;
+        r.rows_tree[b] = row;
         r.state[b] = kServed;
       }
       return;
@@ -219,9 +238,9 @@ __device__ void decide_stream(const fc_replay& r, int b, int32_t step, int p) {
   }
 }
 
-__global__ void __launch_bounds__(kPrepThreads) k_replay_decide(fc_replay r, int32_t step) {
+__global__ void __launch_bounds__(kPrepThreads) k_replay_decide(fc_replay r, int S, int32_t step) {
   const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
-  if (b < r.n_streams) decide_stream(r, b, step, r.pos[b]);
+  if (b < r.n_streams) decide_stream(r, S, b, step, r.pos[b]);
 }
 
 // One wave per stream: a looked-up context whose result is empty enters the
@@ -244,21 +263,6 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_missing(fc_replay r, in
 }
 
 // One workgroup per stream: a served stream's tree comes from the CACHE's.
-__global__ void __launch_bounds__(256) k_replay_merge(fc_replay r, int32_t R) {
-  const int b = blockIdx.x;
-  if (r.state[b] != kServed) return;
-  const int64_t o = (int64_t)b * R;
-  for (int i = threadIdx.x; i < R; i += blockDim.x) {
-    r.node_tok[o + i] = r.c_node_tok[o + i];
-    r.parent[o + i] = r.c_parent[o + i];
-    r.weight[o + i] = r.c_weight[o + i];
-    r.pos_ids[o + i] = r.c_pos_ids[o + i];
-  }
-  const int64_t mo = (int64_t)b * R * R;
-  for (int i = threadIdx.x; i < R * R; i += blockDim.x) r.mask[mo + i] = r.c_mask[mo + i];
-  if (threadIdx.x == 0) r.num_nodes[b] = r.c_num_nodes[b];
-}
-
 // A stream's CACHE bookkeeping, held in registers (the same in every lane)
 // while one wave adds its sequences.
 struct CacheState {
@@ -312,10 +316,13 @@ __device__ void cache_add(const fc_replay& r, int b, CacheState& st, const uint1
 // at pos + pos_ids[i], -1 past the stream or for rows past num_nodes), the
 // history row, the new position, the live count and (CACHE on) the CACHE
 // additions of this step.
-// With decide_next (no CACHE), the same wave then takes the next step's
-// decision for its stream.  live[step & 1] counts the streams live after
-// the step; this launch clears the other counter for the next step.
-__global__ void __launch_bounds__(kPrepThreads) k_replay_finish(fc_replay r, int32_t step, int decide_next) {
+// Then, within a call, the same wave prepares its stream's next step:
+// `next` = 1 takes the next step's decision (CACHE off), `next` = 2 writes
+// the next step's context and CACHE row map (CACHE on: the CACHE search
+// comes between them and the decision).  live[step & 1] counts the streams
+// live after the step; this launch clears the other counter for the next
+// step.
+__global__ void __launch_bounds__(kPrepThreads) k_replay_finish(fc_replay r, int S, int32_t step, int next) {
   const int lane = fc::lane_id();
   const int b = blockIdx.x * kStreamsPerBlock + (int)threadIdx.x / fc::kWave;
   if (blockIdx.x == 0 && threadIdx.x == 0) r.live[(step + 1) & 1] = 0;
@@ -325,7 +332,8 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_finish(fc_replay r, int
   const int tlen = r.truth_len, L = r.ctx_len;
   if (p >= tlen) {
     if (lane == 0) hist[b] = -1;
-    if (decide_next) decide_stream(r, b, step + 1, p);
+    if (next == 1) decide_stream(r, S, b, step + 1, p);
+    if (next == 2 && lane == 0) r.rows_cache[b] = -1;
     return;
   }
   const int R = r.tp.c + 1;
@@ -368,20 +376,25 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_finish(fc_replay r, int
       r.seq_head[b] = st.head;
       r.seq_count[b] = st.cnt;
     }
+    if (next == 2) {  // the next step's context and CACHE row map
+      const bool live = np < tlen;
+      if (lane == 0) r.rows_cache[b] = (live && st.cnt >= r.cache_l) ? b : -1;
+      if (live && lane < L) r.ctx[(int64_t)b * L + lane] = srow[(np - L) + lane];
+    }
   }
   if (lane == 0) {
     hist[b] = a;
     r.pos[b] = np;
     if (np < tlen) atomicAdd(&r.live[step & 1], 1);
   }
-  if (decide_next) decide_stream(r, b, step + 1, np);
+  if (next == 1) decide_stream(r, S, b, step + 1, np);
 }
 
 fc_status check_replay(const fc_replay* r) {
   if (!r || r->n_streams < 1 || r->ctx_len < 1 || r->ctx_len > fc::kWave || r->lru < 1 || r->lru > fc::kWave)
     return FC_ERR_INVALID;
   if (r->truth_len < 0 || r->truth_stride < r->truth_len || !r->truth || r->max_steps < 0) return FC_ERR_INVALID;
-  if ((int64_t)r->n_streams * r->lru + 1 > 0x7FFFFFFF) return FC_ERR_INVALID;
+  if ((int64_t)r->n_streams * (r->lru + 1) + 1 > 0x7FFFFFFF) return FC_ERR_INVALID;
   if (!r->pos || !r->lru_key || !r->lru_used || !r->lru_count || !r->hits || !r->lookups || !r->ctx ||
       !r->rows_retrieve || !r->rows_tree || !r->live || !r->history || !r->taken || !r->state || !r->accept_len ||
       !r->accept_tok || !r->last_node)
@@ -392,9 +405,9 @@ fc_status check_replay(const fc_replay* r) {
       return FC_ERR_INVALID;
     if (!r->ctext || !r->clen || !r->seq_len || !r->seq_head || !r->seq_count || !r->chunks || !r->served ||
         !r->rows_cache || !r->c_match_n || !r->c_range_lo || !r->c_range_cnt || !r->c_taken || !r->c_cont_pos ||
-        !r->c_cont_src || !r->c_cont_len || !r->c_cont_tok || !r->c_num_nodes || !r->c_node_tok || !r->c_parent ||
-        !r->c_weight || !r->c_pos_ids || !r->c_mask)
+        !r->c_cont_src || !r->c_cont_len || !r->c_cont_tok)
       return FC_ERR_INVALID;
+    if (r->tp.alpha[0] == 0) return FC_ERR_INVALID;  // a served tree is weighted by the first store's alpha
   }
   if (r->missing) {
     if (r->miss_cap < 1 || (r->miss_cap & (r->miss_cap - 1)) || r->miss_cap <= r->max_steps || !r->miss_key ||
@@ -425,7 +438,6 @@ extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_r
   if (first_step < 0 || n_steps < 0 || (int64_t)first_step + n_steps > r->max_steps) return FC_ERR_INVALID;
   const int32_t B = r->n_streams, n_rows = r->n_streams * r->lru + 1;
   const bool cache = r->cache_l >= 0, control = r->missing || r->skip_tok >= 0;
-  const int32_t R = r->tp.c + 1;
   if (first_step == 0 && control) {  // a replay's first call: the empty row and the missing tables
     const int64_t tab = r->missing ? (int64_t)B * r->miss_cap : 0;
     const int64_t work = tab > S ? tab : (int64_t)S;
@@ -433,14 +445,15 @@ extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_r
     hipLaunchKernelGGL(k_replay_init_tables, dim3((uint32_t)((work + 255) / 256)), dim3(256), 0, stream, *r, S);
     FC_CHECK_LAUNCH();
   }
-  fc_tree_params ctp = r->tp;
-  for (int i = 0; i < FC_MAX_SOURCES; ++i) ctp.alpha[i] = i == 0 ? 1u : 0u;
+  const int32_t tree_rows = n_rows + (cache ? B : 0);  // (CACHE on) one CACHE row per stream
   for (int32_t i = 0; i < n_steps; ++i) {
     const int32_t step = first_step + i;
     (void)hipGetLastError();
     if (cache) {
-      hipLaunchKernelGGL(k_replay_context, dim3(B), dim3(fc::kWave), 0, stream, *r);
-      FC_CHECK_LAUNCH();
+      if (i == 0) {  // otherwise the previous step's finish wrote the context
+        hipLaunchKernelGGL(k_replay_context, dim3(B), dim3(fc::kWave), 0, stream, *r);
+        FC_CHECK_LAUNCH();
+      }
       s = fc_cache_retrieve(r->ctext, r->cache_cap, B, r->clen, nullptr, r->ctx, B, r->ctx_len, r->rp, r->c_match_n,
                             r->c_range_lo, r->c_range_cnt, r->c_taken, r->c_cont_pos, r->c_cont_src, r->c_cont_len,
                             r->c_cont_tok, r->rows_cache, B, stream);
@@ -448,7 +461,7 @@ extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_r
     }
     if (cache || i == 0) {  // otherwise the previous step's finish took this step's decision
       hipLaunchKernelGGL(k_replay_decide, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
-                         step);
+                         S, step);
       FC_CHECK_LAUNCH();
     }
     s = fc_retrieve(stores, S, r->ctx, B, r->ctx_len, r->rp, r->match_n, r->range_lo, r->range_cnt, r->taken,
@@ -461,20 +474,12 @@ extern "C" fc_status fc_replay_run(const fc_store* stores, int32_t S, const fc_r
       FC_CHECK_LAUNCH();
     }
     s = fc_build_tree(r->taken, r->cont_len, r->cont_tok, r->ctx, B, r->ctx_len, S, r->rp.k, r->rp.m, r->tp,
-                      r->num_nodes, r->node_tok, r->parent, r->weight, r->pos_ids, r->mask, r->rows_tree, n_rows,
+                      r->num_nodes, r->node_tok, r->parent, r->weight, r->pos_ids, r->mask, r->rows_tree, tree_rows,
                       r->tree_ws, r->tree_ws_bytes, stream);
     if (s != FC_OK) return s;
-    if (cache) {
-      s = fc_build_tree(r->c_taken, r->c_cont_len, r->c_cont_tok, r->ctx, B, r->ctx_len, 1, r->rp.k, r->rp.m, ctp,
-                        r->c_num_nodes, r->c_node_tok, r->c_parent, r->c_weight, r->c_pos_ids, r->c_mask,
-                        r->rows_cache, B, r->tree_ws, r->tree_ws_bytes, stream);
-      if (s != FC_OK) return s;
-      hipLaunchKernelGGL(k_replay_merge, dim3(B), dim3(256), 0, stream, *r, R);
-      FC_CHECK_LAUNCH();
-    }
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_replay_finish, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r,
-                       step, (!cache && i + 1 < n_steps) ? 1 : 0);
+    hipLaunchKernelGGL(k_replay_finish, dim3(fc::div_up(B, kStreamsPerBlock)), dim3(kPrepThreads), 0, stream, *r, S,
+                       step, i + 1 < n_steps ? (cache ? 2 : 1) : 0);
     FC_CHECK_LAUNCH();
   }
   return FC_OK;
