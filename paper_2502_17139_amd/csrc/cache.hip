@@ -35,27 +35,51 @@ __host__ __device__ inline uint32_t pow2_at_least(uint32_t x) {
   return p;
 }
 
+// Tokens p .. p+15 of T[0..len) (T 4-byte aligned) as 8 words holding two
+// tokens each, the earlier in the high half, so that one unsigned compare
+// orders two tokens lexicographically; words at or past len read as 0 (the
+// caller bounds the compare by the lengths).
+__device__ __forceinline__ void token_pairs(const uint16_t* T, uint32_t len, uint32_t p, uint32_t (&w)[8]) {
+  const uint32_t* W = (const uint32_t*)T;
+  const uint32_t wi = p >> 1;
+  uint32_t r[9];
+#pragma unroll
+  for (int k = 0; k < 9; ++k) r[k] = 2 * (wi + k) < len ? W[wi + k] : 0u;
+  if (p & 1) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) w[k] = (r[k] & 0xFFFF0000u) | (r[k + 1] & 0xFFFFu);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) w[k] = __builtin_amdgcn_alignbit(r[k], r[k], 16);
+  }
+}
+
 // Suffix a below suffix b of T[0..len), knowing their first `from` tokens
 // agree (a != b, so one is a proper prefix of the other or they differ).
-// Eight tokens of each are read per LDS round trip: CACHE texts repeat, so
-// suffixes that share q often agree far beyond it.
+// Sixteen tokens of each are read per LDS round trip, as word pairs: CACHE
+// texts repeat, so suffixes that share q often agree far beyond it.
 __device__ __forceinline__ bool suffix_less(const uint16_t* T, uint32_t len, uint32_t a, uint32_t b, int from) {
   if (a == kNone) return false;
   if (b == kNone) return true;
-  for (uint32_t x0 = (uint32_t)from;; x0 += 8) {
-    uint16_t ta[8], tb[8];
+  for (uint32_t x0 = (uint32_t)from;; x0 += 16) {
+    uint32_t wa[8], wb[8];
+    token_pairs(T, len, a + x0, wa);
+    token_pairs(T, len, b + x0, wb);
+    const uint32_t ra = len - (a + x0), rb = len - (b + x0);  // tokens left (never both 0)
+    int d = 16;  // first differing token of the window
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      ta[u] = a + x0 + u < len ? T[a + x0 + u] : (uint16_t)0;
-      tb[u] = b + x0 + u < len ? T[b + x0 + u] : (uint16_t)0;
+    for (int k = 7; k >= 0; --k) {
+      const uint32_t x = wa[k] ^ wb[k];
+      if (x) d = 2 * k + ((x >> 16) ? 0 : 1);
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const uint32_t x = x0 + (uint32_t)u;
-      if (a + x == len) return true;  // a ends first: the shorter is smaller
-      if (b + x == len) return false;
-      if (ta[u] != tb[u]) return ta[u] < tb[u];
+    const uint32_t lim = ra < rb ? (ra < 16u ? ra : 16u) : (rb < 16u ? rb : 16u);
+    if ((uint32_t)d < lim) {
+      const int k = d >> 1;
+      const uint32_t ta = (d & 1) ? (wa[k] & 0xFFFFu) : (wa[k] >> 16);
+      const uint32_t tb = (d & 1) ? (wb[k] & 0xFFFFu) : (wb[k] >> 16);
+      return ta < tb;
     }
+    if (lim < 16u) return ra < rb;  // the shorter ends first and is smaller (ra != rb as a != b)
   }
 }
 
@@ -184,7 +208,9 @@ __global__ void __launch_bounds__(kCacheThreads) k_cache_retrieve(
   // 3. suffix order (every occurrence starts with q: compare from offset n).
   //    Up to 32 occurrences, thread (i, j) = (tid / 32, tid % 32) tells
   //    whether occurrence j's suffix is below occurrence i's and a ballot
-  //    over i's 32 lanes gives i's rank; more take a bitonic sort.
+  //    over i's 32 lanes gives i's rank; up to P = 64 or 128, i's G = 1024 / P
+  //    lanes (i, j0) = (tid / G, tid % G) compare j = j0, j0 + G, ... and add
+  //    their counts; more take a bitonic sort.
   if (cnt <= 32) {
     const uint32_t i = (uint32_t)tid >> 5, j = (uint32_t)tid & 31u;
     const bool lt = i < cnt && j < cnt && j != i && suffix_less(T, len, occ[j], occ[i], n);
@@ -193,6 +219,17 @@ __global__ void __launch_bounds__(kCacheThreads) k_cache_retrieve(
     const uint32_t mine = (i < cnt && j == 0) ? occ[i] : 0u;
     __syncthreads();
     if (i < cnt && j == 0) occ[rank] = mine;
+    __syncthreads();
+  } else if (cnt <= 128) {
+    const uint32_t G = cnt <= 64 ? 16u : 8u;  // lanes per occurrence i
+    const uint32_t i = (uint32_t)tid / G, j0 = (uint32_t)tid % G;
+    uint32_t rank = 0;
+    if (i < cnt)
+      for (uint32_t j = j0; j < cnt; j += G) rank += (j != i && suffix_less(T, len, occ[j], occ[i], n)) ? 1u : 0u;
+    for (uint32_t off = G >> 1; off >= 1; off >>= 1) rank += (uint32_t)__shfl_xor((int)rank, (int)off, (int)G);
+    const uint32_t mine = (i < cnt && j0 == 0) ? occ[i] : 0u;
+    __syncthreads();
+    if (i < cnt && j0 == 0) occ[rank] = mine;
     __syncthreads();
   } else {
     for (uint32_t k2 = 2; k2 <= Pc; k2 <<= 1) {

@@ -608,12 +608,23 @@ def test_cache_retrieve_matches_oracle():
     stride = fc.FC_MAX_CACHE_TOKENS
     for seed, (vocab, max_len, k, m, n_max, n_min) in enumerate([
             (4, 400, 30, 4, 16, 2), (9, 3000, 5000, 10, 16, 2), (3, stride, 200, 10, 16, 2),
-            (50, stride, 5000, 16, 8, 1), (6, 800, 7, 3, 5, 3)]):
+            (50, stride, 5000, 16, 8, 1), (6, 800, 7, 3, 5, 3), (7, 5000, 5000, 10, 16, 2)]):
         texts = _cache_texts(seed, 6, vocab, max_len)
         if seed == 0:
             texts[0] = np.zeros(0, np.uint16)
         if seed == 2:
             texts[1] = np.resize(synth.random_text(5, 50, vocab), stride).astype(np.uint16)  # full and periodic
+        if seed == 5:
+            # periodic texts whose patterns occur ~40 and ~80 times (the ranked
+            # tiers above 32 occurrences), one with sparse noise so that the
+            # occurrences' suffixes part at varied depths
+            rng5 = np.random.default_rng(55)
+            texts[0] = np.resize(synth.random_text(50, 60, vocab), 5000).astype(np.uint16)
+            texts[1] = np.resize(synth.random_text(51, 120, vocab), 5000).astype(np.uint16)
+            t2 = np.resize(synth.random_text(52, 70, vocab), 5600).astype(np.uint16)
+            flip = rng5.random(len(t2)) < 0.003
+            t2[flip] = rng5.integers(1, vocab, size=int(flip.sum()))
+            texts[2] = t2
         buf = np.zeros((len(texts), stride), np.uint16)
         lens = np.zeros(len(texts), np.int32)
         for i, t in enumerate(texts):
