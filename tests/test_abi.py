@@ -65,6 +65,11 @@ def test_retrieve_rejects(L, change, code):
     assert L.fc_retrieve(*_retrieve_args(**change)) == code
 
 
+def test_retrieve_rejects_batches_past_32_bit_slots(L):
+    # 900,000 queries x 5,000 slots numbers more than 2^32 slots
+    assert L.fc_retrieve(*_retrieve_args(B=900_000)) == 4
+
+
 def test_retrieve_rejects_missing_workspace(L):
     assert L.fc_retrieve(*_retrieve_args(ws_bytes=0)) == 2
     args = _retrieve_args(ws_bytes=4)  # 4*(B+1) = 8 needed
