@@ -248,8 +248,8 @@ typedef struct fc_retrieve_params {
  * ws, ws_bytes : workspace of at least fc_retrieve_workspace_bytes(B, S, p)
  *                (4*(B+1) bytes: the batch's slot offsets); its contents on
  *                entry do not matter.
- * B * k must stay below 2^32 (the batch's slots are numbered in 32 bits);
- * FC_ERR_UNSUPPORTED otherwise.
+ * B * k must not exceed 2^31 - 1 (the batch's slots are numbered in 32
+ * bits with room for the grid stride); FC_ERR_UNSUPPORTED otherwise.
  */
 size_t fc_retrieve_workspace_bytes(int32_t B, int32_t S, fc_retrieve_params p);
 fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,

@@ -528,7 +528,7 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
   if (p.n_max < 1 || p.n_max > FC_MAX_NMAX || p.n_min < 1 || p.n_min > p.n_max) return FC_ERR_INVALID;
   if (p.k < 1 || p.m < 1 || p.m > 255) return FC_ERR_INVALID;
   if ((int64_t)S * (p.n_max - p.n_min + 1) * 2 > 4 * fc::kWave) return FC_ERR_INVALID;
-  if ((uint64_t)B * (uint64_t)p.k > 0xFFFFFFFFull) return FC_ERR_UNSUPPORTED;  // slot numbers are 32-bit
+  if ((uint64_t)B * (uint64_t)p.k > 0x7FFFFFFFull) return FC_ERR_UNSUPPORTED;  // slot numbers stay below 2^31
   StoreArgs st = {};
   for (int s = 0; s < S; ++s) {
     const fc_store& x = stores[s];

@@ -65,9 +65,9 @@ def test_retrieve_rejects(L, change, code):
     assert L.fc_retrieve(*_retrieve_args(**change)) == code
 
 
-def test_retrieve_rejects_batches_past_32_bit_slots(L):
-    # 900,000 queries x 5,000 slots numbers more than 2^32 slots
-    assert L.fc_retrieve(*_retrieve_args(B=900_000)) == 4
+def test_retrieve_rejects_batches_past_31_bit_slots(L):
+    # 430,000 queries x 5,000 slots number more than 2^31
+    assert L.fc_retrieve(*_retrieve_args(B=430_000)) == 4
 
 
 def test_retrieve_rejects_missing_workspace(L):
