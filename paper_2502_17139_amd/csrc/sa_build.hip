@@ -424,7 +424,8 @@ __global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys,
   __shared__ uint32_t s[kMaxDigits][kRadix];
   for (int i = threadIdx.x; i < kMaxDigits * kRadix; i += blockDim.x) (&s[0][0])[i] = 0;
   __syncthreads();
-  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < U; i += gridDim.x * blockDim.x) {
+  // 64-bit index: U can come within a grid stride of 2^32
+  for (uint64_t i = blockIdx.x * blockDim.x + threadIdx.x; i < U; i += (uint64_t)gridDim.x * blockDim.x) {
     uint64_t k = keys[i];
     for (int d = 0; d < digits; ++d) atomicAdd(&s[d][(k >> (8 * d)) & 0xFF], 1u);
   }
@@ -712,7 +713,7 @@ __global__ void __launch_bounds__(256) k_bucket(const uint16_t* __restrict__ tok
 __global__ void __launch_bounds__(256) k_max_token(const uint16_t* __restrict__ tok, uint32_t n,
                                                    uint32_t* __restrict__ out) {
   uint32_t mx = 0;
-  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+  for (uint64_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
     mx = tok[i] > mx ? tok[i] : mx;
   mx = fc::wave_max(mx);
   if (fc::lane_id() == 0 && mx) atomicMax(out, mx);
