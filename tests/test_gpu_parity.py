@@ -671,6 +671,24 @@ def test_replay_with_cache_matches_oracle(cache_l, cap, native):
     assert g["cache_served"].sum() > 0
 
 
+def test_replay_cache_with_unequal_store_weights():
+    """The engine builds a served stream's tree from its CACHE result as the
+    first store's slots, weighted by that store's alpha (3 here) instead of
+    1: the same nodes in the same order, so every accepted length and count
+    still equals the oracle's."""
+    tp, t1 = synth.store(3, "project"), synth.store(1, "single")
+    truth = synth.truth(n_seq=8, length=400)
+    stores = [gpu_store(tp, synth.VOCAB, records=True), gpu_store(t1)]
+    kw = dict(P, alpha=(3, 1))
+    say("replay+cache alpha=(3, 1): gpu")
+    g = GpuReplay(stores, truth, cache_l=4, cache_cap=300, **kw).run(max_steps=300, native=True)
+    say("replay+cache alpha=(3, 1): oracle")
+    o = oracle.replay([tp, t1], truth, cache_l=4, cache_cap=300, **kw, max_steps=300)
+    for f in ("accept", "hits", "lookups", "pos", "cache_served"):
+        assert (g[f] == o[f]).all(), f
+    assert g["cache_served"].sum() > 0
+
+
 @pytest.mark.parametrize("native", [True, False], ids=["engine", "driver"])
 @pytest.mark.parametrize("case", ["project-streams", "recurring-misses"])
 def test_replay_with_retrieval_control_matches_oracle(case, native):
