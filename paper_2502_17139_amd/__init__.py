@@ -167,6 +167,33 @@ def _ptr(t: torch.Tensor | None) -> ctypes.c_void_p:
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _expect(name: str, t: torch.Tensor | None, dtype, shape=None, optional: bool = False) -> None:
+    """The library trusts the sizes it is given, so a tensor of the wrong
+    type or shape is refused here, before any launch."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, not {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(int(x) for x in shape):
+        raise ValueError(f"{name} must have shape {tuple(int(x) for x in shape)}, not {tuple(t.shape)}")
+
+
+def _expect_outputs(out: dict, fields, shapes: dict, dtypes: dict) -> None:
+    for f in fields:
+        _expect(f, out.get(f), dtypes[f], shapes[f])
+
+
+_RETRIEVE_DTYPES = dict(match_n=torch.int32, range_lo=torch.uint32, range_cnt=torch.uint32, taken=torch.int32,
+                        cont_pos=torch.uint32, cont_src=torch.uint8, cont_len=torch.uint8, cont_tok=torch.uint16)
+
+
+def _retrieve_shapes(n_rows: int, S: int, k: int, m: int) -> dict:
+    return dict(match_n=(n_rows, S), range_lo=(n_rows, S), range_cnt=(n_rows, S), taken=(n_rows, S),
+                cont_pos=(n_rows, k), cont_src=(n_rows, k), cont_len=(n_rows, k), cont_tok=(n_rows, k, m))
+
+
 def _stream(stream) -> ctypes.c_void_p:
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
@@ -345,10 +372,15 @@ def fc_retrieve(stores, ctx: torch.Tensor, n_max: int = 16, n_min: int = 2, k: i
     p = FcRetrieveParams(n_max, n_min, k, m)
     if out is None:
         out = retrieve_outputs(B, S, k, m, ctx.device)
+    n_rows = out["taken"].shape[0] if "taken" in out else B
+    if rows is None and n_rows != B:
+        raise ValueError("without a row map the outputs need one row per query")
+    _expect_outputs(out, RETRIEVE_FIELDS, _retrieve_shapes(n_rows, S, k, m), _RETRIEVE_DTYPES)
+    _expect("rows", rows, torch.int32, (B,), optional=True)
+    _expect("workspace", workspace, torch.uint8, optional=True)
     need = int(lib().fc_retrieve_workspace_bytes(B, S, p))
     if workspace is None and need > 0:
         workspace = _empty(need, torch.uint8, ctx.device)
-    n_rows = out["taken"].shape[0]
     _check("fc_retrieve", lib().fc_retrieve(
         views, S, _ptr(ctx), B, L, p, *[_ptr(out[f]) for f in RETRIEVE_FIELDS], _ptr(rows), n_rows,
         _ptr(workspace), 0 if workspace is None else workspace.numel(), _stream(stream)))
@@ -372,8 +404,15 @@ def fc_cache_retrieve(texts: torch.Tensor, text_len: torch.Tensor, ctx: torch.Te
         raise ValueError("ctx must be a 2-D uint16 tensor")
     B, L = ctx.shape
     n_texts, stride = texts.shape
+    _expect("text_len", text_len, torch.int32, (n_texts,))
+    _expect("text_row", text_row, torch.int32, (B,), optional=True)
     if out is None:
         out = retrieve_outputs(B, 1, k, m, ctx.device)
+    n_rows = out["taken"].shape[0] if "taken" in out else B
+    if rows is None and n_rows != B:
+        raise ValueError("without a row map the outputs need one row per query")
+    _expect_outputs(out, RETRIEVE_FIELDS, _retrieve_shapes(n_rows, 1, k, m), _RETRIEVE_DTYPES)
+    _expect("rows", rows, torch.int32, (B,), optional=True)
     _check("fc_cache_retrieve", lib().fc_cache_retrieve(
         _ptr(texts), stride, n_texts, _ptr(text_len), _ptr(text_row), _ptr(ctx), B, L,
         FcRetrieveParams(n_max, n_min, k, m), *[_ptr(out[f]) for f in RETRIEVE_FIELDS], _ptr(rows),
@@ -385,7 +424,16 @@ def fc_cache_write(texts: torch.Tensor, text_len: torch.Tensor, dst_row: torch.T
                    new_len: torch.Tensor, src_off: torch.Tensor, src_len: torch.Tensor, src_tok: torch.Tensor,
                    stream=None) -> None:
     """Segment copies into CACHE texts (see include/fastcoder.h)."""
+    if texts.dtype != torch.uint16 or texts.dim() != 2:
+        raise ValueError("texts must be a 2-D uint16 tensor")
     n_texts, stride = texts.shape
+    n_seg = dst_row.numel()
+    _expect("text_len", text_len, torch.int32, (n_texts,))
+    for name, t, dt in (("dst_row", dst_row, torch.int32), ("dst_off", dst_off, torch.int32),
+                        ("new_len", new_len, torch.int32), ("src_off", src_off, torch.int64),
+                        ("src_len", src_len, torch.int32)):
+        _expect(name, t, dt, (n_seg,))
+    _expect("src_tok", src_tok, torch.uint16)
     _check("fc_cache_write", lib().fc_cache_write(
         _ptr(texts), stride, n_texts, _ptr(text_len), dst_row.numel(), _ptr(dst_row), _ptr(dst_off),
         _ptr(new_len), _ptr(src_off), _ptr(src_len), _ptr(src_tok), _stream(stream)))
@@ -404,6 +452,14 @@ def fc_tree_attention(q: torch.Tensor, k_tree: torch.Tensor, v_tree: torch.Tenso
             raise ValueError("q, k_tree, v_tree, k_cache, v_cache must be 4-D bfloat16")
     B, R, H, D = q.shape
     Hkv, Pmax = k_tree.shape[2], k_cache.shape[1]
+    for name, t, shape in (("k_tree", k_tree, (B, R, Hkv, D)), ("v_tree", v_tree, (B, R, Hkv, D)),
+                           ("k_cache", k_cache, (B, Pmax, Hkv, D)), ("v_cache", v_cache, (B, Pmax, Hkv, D))):
+        _expect(name, t, torch.bfloat16, shape)
+    _expect("prefix_len", prefix_len, torch.int32, (B,))
+    _expect("num_nodes", tree["num_nodes"], torch.int32, (B,))
+    _expect("pos_ids", tree["pos_ids"], torch.int32, (B, R))
+    _expect("mask", tree["mask"], torch.int32, (B, R, R))
+    _expect("out", out, torch.float32, (B, R, H, D), optional=True)
     if out is None:
         out = _empty((B, R, H, D), torch.float32, q.device)
     u16 = lambda t: _ptr(t.view(torch.uint16))  # noqa: E731
@@ -434,16 +490,28 @@ def fc_build_tree(taken: torch.Tensor, cont_len: torch.Tensor, cont_tok: torch.T
                   rows: torch.Tensor | None = None, stream=None) -> dict:
     """Weighted draft trie pruned to c nodes, with mask and position ids.
     With rows (int32 [B]), query b reads row rows[b] of taken/cont_*."""
+    if taken.dim() != 2 or cont_tok.dim() != 3 or ctx.dim() != 2:
+        raise ValueError("taken [rows][S], cont_tok [rows][k][m] and ctx [B][L] expected")
     n_rows, S = taken.shape
     B = n_rows if rows is None else rows.numel()
     k, m = cont_tok.shape[1], cont_tok.shape[2]
     L = ctx.shape[1]
+    _expect("taken", taken, torch.int32)
+    _expect("cont_len", cont_len, torch.uint8, (n_rows, k))
+    _expect("cont_tok", cont_tok, torch.uint16, (n_rows, k, m))
+    _expect("ctx", ctx, torch.uint16, (B, L))
+    _expect("rows", rows, torch.int32, (B,), optional=True)
     a = list(alpha)[:S]
     if len(a) != S:
         raise ValueError("need one alpha per store")
     tp = FcTreeParams(c, (ctypes.c_uint32 * FC_MAX_SOURCES)(*(a + [0] * (FC_MAX_SOURCES - S))))
     if out is None:
         out = tree_outputs(B, c, ctx.device)
+    R = c + 1
+    _expect_outputs(out, TREE_FIELDS, dict(num_nodes=(B,), node_tok=(B, R), parent=(B, R), weight=(B, R),
+                                           pos_ids=(B, R), mask=(B, R, R)),
+                    dict(num_nodes=torch.int32, node_tok=torch.int32, parent=torch.int32, weight=torch.uint32,
+                         pos_ids=torch.int32, mask=torch.int32))
     need = fc_build_tree_workspace_bytes(B)
     if workspace is None and need > 0:
         workspace = _empty(need, torch.uint8, ctx.device)
@@ -467,6 +535,13 @@ def accept_outputs(B: int, m: int, device) -> dict:
 def fc_verify_accept(tree: dict, target: torch.Tensor, m: int = 10, out: dict | None = None, stream=None) -> dict:
     """Longest accepted root path against per-row target tokens ([B][c+1])."""
     B, R = tree["node_tok"].shape
+    _expect("num_nodes", tree["num_nodes"], torch.int32, (B,))
+    for f in ("node_tok", "parent", "pos_ids"):
+        _expect(f, tree[f], torch.int32, (B, R))
+    _expect("target", target, torch.int32, (B, R))
+    if out is not None:
+        _expect_outputs(out, ACCEPT_FIELDS, dict(accept_len=(B,), accept_tok=(B, m + 1), last_node=(B,)),
+                        dict(accept_len=torch.int32, accept_tok=torch.int32, last_node=torch.int32))
     if out is None:
         out = accept_outputs(B, m, target.device)
     _check("fc_verify_accept", lib().fc_verify_accept(
@@ -479,6 +554,13 @@ def fc_targets_from_truth(truth: torch.Tensor, start: torch.Tensor, tree: dict, 
                           out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """Target tokens [B][c+1] from true streams (uint16 [n_streams][len])."""
     B, R = tree["node_tok"].shape
+    if truth.dtype != torch.uint16 or truth.dim() != 2:
+        raise ValueError("truth must be a 2-D uint16 tensor")
+    _expect("start", start, torch.int32, (B,))
+    _expect("seq", seq, torch.int32, (B,), optional=True)
+    _expect("num_nodes", tree["num_nodes"], torch.int32, (B,))
+    _expect("pos_ids", tree["pos_ids"], torch.int32, (B, R))
+    _expect("out", out, torch.int32, (B, R), optional=True)
     if out is None:
         out = _empty((B, R), torch.int32, truth.device)
     _check("fc_targets_from_truth", lib().fc_targets_from_truth(
