@@ -321,6 +321,12 @@ class Store:
 
     def __init__(self, tokens: torch.Tensor, sa: torch.Tensor | None = None, bucket: torch.Tensor | None = None,
                  pair_vocab: int | None = None, records: bool = False, stream=None):
+        if tokens.dtype != torch.uint16 or tokens.dim() != 1 or not tokens.is_cuda or not tokens.is_contiguous():
+            raise ValueError("tokens must be a contiguous 1-D uint16 device tensor")
+        for name, t, shape in (("sa", sa, (tokens.numel(),)), ("bucket", bucket, (FC_BUCKETS,))):
+            _expect(name, t, torch.uint32, shape, optional=True)
+            if t is not None and (not t.is_cuda or not t.is_contiguous()):
+                raise ValueError(f"{name} must be a contiguous device tensor")
         self.tokens = tokens
         self.sa = fc_datastore_build(tokens, stream=stream) if sa is None else sa
         self.bucket = fc_store_prepare(tokens, self.sa, stream=stream) if bucket is None else bucket
@@ -580,8 +586,8 @@ class ReplayEngine:
     def __init__(self, stores, truth: torch.Tensor, n_max=16, n_min=2, k=5000, m=10, c=64, alpha=(1, 1), lru=32,
                  ctx_len=16, max_steps=512, chunk=16, cache_l=None, cache_every=20, cache_cap=FC_MAX_CACHE_TOKENS,
                  missing=False, skip_tok=None, skip_p=0.5, skip_draws=None):
-        if truth.dtype != torch.uint16 or truth.dim() != 2 or not truth.is_contiguous():
-            raise ValueError("truth must be a contiguous 2-D uint16 tensor")
+        if truth.dtype != torch.uint16 or truth.dim() != 2 or not truth.is_contiguous() or not truth.is_cuda:
+            raise ValueError("truth must be a contiguous 2-D uint16 device tensor")
         dev = truth.device
         self.stores, self.truth, self.chunk = stores, truth, chunk
         n, tlen = truth.shape
