@@ -1,7 +1,7 @@
 // C ABI housekeeping: version and status strings.
 #include "fastcoder.h"
 
-extern "C" int32_t fc_abi_version(void) { return 3; }
+extern "C" int32_t fc_abi_version(void) { return 4; }
 
 extern "C" const char* fc_status_string(fc_status s) {
   switch (s) {

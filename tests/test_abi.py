@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_status_strings(L):
-    assert L.fc_abi_version() == 3
+    assert L.fc_abi_version() == 4
     for code, name in fc.STATUS.items():
         assert L.fc_status_string(code).decode().startswith(name)
     assert L.fc_status_string(99).decode() == "FC_ERR_UNKNOWN"
