@@ -345,7 +345,7 @@ def main():
         "vs_baseline": None,
         "dtype": "u16/u32 (integer)",
         "data": "synthetic (seeded template/Zipf/noise token stores; no dataset)",
-        "config": {"workload": synth.CONFIGS[cfg]["name"], "stores_tokens": [len(t) for t in texts],
+        "config": {"workload": synth.WORKLOADS[cfg]["name"], "stores_tokens": [len(t) for t in texts],
                    "batch": B, "n_max": p["n_max"], "n_min": p["n_min"], "k": k, "m": m, "c": c,
                    "alpha": list(alpha), "parallelism": "none (1 GPU)"},
         "roofline": roofs[dominant],
@@ -543,7 +543,7 @@ def run_extend(args):
                 times.append(time.perf_counter() - t0)
         return float(np.median(times))
 
-    spec = {r: (seed, nt, zs, nf) for r, seed, nt, zs, nf in synth.CONFIGS[3]["stores"]}
+    spec = {r: (seed, nt, zs, nf) for r, seed, nt, zs, nf in synth.WORKLOADS[3]["stores"]}
     cases = []
     for role, files in (("project", 1), ("project", 200), ("general", 2000)):
         seed, nt, zs, nf = spec[role]

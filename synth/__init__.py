@@ -34,8 +34,8 @@ ROLE_SHUFFLE = 11
 ROLE_FRESH = 12
 ROLE_REPOS = 13
 
-# Workload configurations.  A store is (seed, n_templates, zipf_s, n_files).
-CONFIGS = {
+# Synthetic workloads by size.  A store is (seed, n_templates, zipf_s, n_files).
+WORKLOADS = {
     1: dict(name="single-source 1M", stores=[("single", 0, 5000, 1.2, 2000)],
             qseed=0, batch=64, project_share=None),
     2: dict(name="project 2M + general 100M",
@@ -130,7 +130,7 @@ def store(cfg: int, role: str) -> np.ndarray:
     """The store named `role` ('single', 'project' or 'general') of a configuration."""
     key = (cfg, role)
     if key not in _STORE_CACHE:
-        for r, seed, nt, s, nf in CONFIGS[cfg]["stores"]:
+        for r, seed, nt, s, nf in WORKLOADS[cfg]["stores"]:
             if r == role:
                 _STORE_CACHE[key] = make_store(seed, nt, s, nf)
                 break
@@ -141,7 +141,7 @@ def store(cfg: int, role: str) -> np.ndarray:
 
 def store_roles(cfg: int) -> list:
     """Store roles of a configuration in priority order (project first)."""
-    return [r for r, *_ in CONFIGS[cfg]["stores"]]
+    return [r for r, *_ in WORKLOADS[cfg]["stores"]]
 
 
 def drop_cache() -> None:
@@ -173,7 +173,7 @@ def query_plan(cfg: int) -> list:
     from the general store's; each group is half random, half fresh.  The
     order is a seeded shuffle.
     """
-    c = CONFIGS[cfg]
+    c = WORKLOADS[cfg]
     b = c["batch"]
     if c["project_share"] is None:
         groups = [(store_roles(cfg)[0], b)]
@@ -200,7 +200,7 @@ def queries(cfg: int, count: int | None = None, next_tokens: int = 0):
     window, 0-padded at the end of the store; the fresh file's continuation
     for a fresh one): the ground truth a target model would reproduce.
     """
-    c = CONFIGS[cfg]
+    c = WORKLOADS[cfg]
     plan = query_plan(cfg)
     if count is not None:
         plan = plan[:count]
