@@ -15,7 +15,7 @@ import torch
 import oracle
 import synth
 from gpu_pipeline import (compare_retrieve, compare_tree, dev, gpu_pipeline, gpu_store, host,
-                          oracle_pipeline, say)
+                          oracle_pipeline, say, targets_from_truth)
 
 pytestmark = pytest.mark.gpu
 
@@ -473,6 +473,29 @@ def test_fuzz_small_stores(seed):
         o = oracle_pipeline(texts, ctx[:, -L:], p, (1,) * S, 16)
         compare_retrieve(g, o)
         compare_tree(g, o)
+
+
+def test_targets_from_truth_edges():
+    """fc_targets_from_truth against its definition: a stream map that
+    permutes and repeats streams, starts at the stream's last token (every
+    deeper row falls past the end), at 0, in the middle, and malformed trees
+    (num_nodes -1) whose rows all read -1."""
+    t = synth.store(1, "single")
+    ctx = synth.queries(1)[:24]
+    st = gpu_store(t)
+    g = gpu_pipeline([st], ctx, P, (1,), 16)
+    num_nodes = g["num_nodes"].copy()
+    num_nodes[5] = -1
+    truth = synth.truth(n_seq=6, length=300)
+    rng = np.random.default_rng(9)
+    seq = rng.integers(0, truth.shape[0], size=ctx.shape[0]).astype(np.int32)
+    start = rng.integers(0, 300, size=ctx.shape[0]).astype(np.int32)
+    start[:4] = (299, 298, 0, 150)
+    tree = {"num_nodes": dev(num_nodes), "pos_ids": dev(g["pos_ids"]), "node_tok": dev(g["node_tok"])}
+    got = host(fc.fc_targets_from_truth(dev(truth), dev(start), tree, seq=dev(seq)))
+    want = targets_from_truth(g["pos_ids"], num_nodes, truth[seq], start)
+    assert (got == want).all()
+    assert (got[5] == -1).all() and (got[0, 1:] == -1).all()
 
 
 def test_unsorted_slots_are_flagged():
