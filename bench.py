@@ -18,6 +18,7 @@ line.  Timing uses HIP events on the stream the kernels run on.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -172,6 +173,9 @@ def main():
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the single-query latency runs (profiles then hold batch dispatches only)")
     args = ap.parse_args()
+    # No garbage-collector pauses inside timed regions: a pause stalls the
+    # host while the GPU drains its queue, and the stall would be timed.
+    gc.disable()
     if args.gpus != 1:
         print(json.dumps({"error": "single-GPU path only (no sharded stores); --gpus must be 1", "n_gpus": args.gpus}))
         sys.exit(2)
@@ -251,6 +255,7 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
+    gc.collect()
     # Timed region 1: K steps back to back, one event pair around them (an
     # event between entry points costs a few microseconds of queue time, so
     # the throughput is timed without them).
@@ -280,7 +285,8 @@ def main():
         verify()
         ev[i][3].record(stream)
     torch.cuda.synchronize()
-    phase_ms = {name: float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)]))
+    # median per launch: robust to a step where the host fell behind the GPU
+    phase_ms = {name: float(np.median([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)]))
                 for j, name in enumerate(("fc_retrieve", "fc_build_tree", "fc_verify_accept"))}
 
     # single-query latency (B = 1): one query's retrieve + tree + accept on

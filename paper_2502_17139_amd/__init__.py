@@ -176,7 +176,7 @@ def _expect(name: str, t: torch.Tensor | None, dtype, shape=None, optional: bool
         raise ValueError(f"{name} is required")
     if t.dtype != dtype:
         raise ValueError(f"{name} must be {dtype}, not {t.dtype}")
-    if shape is not None and tuple(t.shape) != tuple(int(x) for x in shape):
+    if shape is not None and t.shape != shape:
         raise ValueError(f"{name} must have shape {tuple(int(x) for x in shape)}, not {tuple(t.shape)}")
 
 
