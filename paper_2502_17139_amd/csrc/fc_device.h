@@ -278,9 +278,13 @@ __device__ __forceinline__ void lds_load16(uint32_t lds, uint32_t voff, int32x4 
 // Greedy acceptance walk of one draft tree by one wave (Section IV-D):
 // from the root, step to the child whose token equals target(u) while one
 // exists; the target at the stopping row is accepted too.  Rows 1..n-1 of
-// the tree (n clamped to [1, R]) are held four per lane; each step is one
-// ballot per 64 rows.  Writes the accepted tokens (m + 1 slots, -1 past the
-// end) and returns the accepted length and the last row in len and u.
+// the tree (n clamped to [1, R]) are held four per lane, with the targets of
+// rows 0..n-1 loaded beside them before the walk, so that each step is one
+// ballot per 64 rows and one lane shuffle instead of a dependent load.  The
+// row loads do not wait for n: every row v < R is read (target(v) is called
+// for each and must be safe for each) and rows at n or past it are masked.
+// Writes the accepted tokens (m + 1 slots, -1 past the end) and returns the
+// accepted length and the last row in len and u.
 template <int MAXROWS, typename Target>
 __device__ __forceinline__ void accept_walk(int n, const int32_t* __restrict__ node_tok,
                                             const int32_t* __restrict__ parent, int R, int m, Target target,
@@ -288,18 +292,32 @@ __device__ __forceinline__ void accept_walk(int n, const int32_t* __restrict__ n
   constexpr int kChunks = MAXROWS / kWave;
   const int lane = lane_id();
   n = n < 1 ? 1 : (n > R ? R : n);
-  int32_t par[kChunks], tok[kChunks];
+  int32_t par[kChunks], tok[kChunks], tgt[kChunks];
 #pragma unroll
   for (int h = 0; h < kChunks; ++h) {
     const int v = lane + h * kWave;
-    const bool in = v >= 1 && v < n;
-    par[h] = in ? parent[v] : -2;
-    tok[h] = in ? node_tok[v] : -1;
+    par[h] = v < R ? parent[v] : -2;
+    tok[h] = v < R ? node_tok[v] : -1;
+    tgt[h] = v < R ? target(v) : -1;
   }
+#pragma unroll
+  for (int h = 0; h < kChunks; ++h) {
+    const int v = lane + h * kWave;
+    if (v < 1 || v >= n) par[h] = -2, tok[h] = -1;
+    if (v >= n) tgt[h] = -1;
+  }
+  // target of row x < n (x wave-uniform): its chunk, then its lane.
+  const auto target_of = [&](int x) -> int32_t {
+    int32_t t = tgt[0];
+#pragma unroll
+    for (int h = 1; h < kChunks; ++h)
+      if (x / kWave == h) t = tgt[h];
+    return __shfl(t, x % kWave, kWave);
+  };
   u = 0;
   len = 0;
   for (;;) {
-    const int32_t want = target(u);
+    const int32_t want = target_of(u);
     if (want < 0 || len >= m + 1) break;
     int next = -1;
 #pragma unroll
@@ -312,7 +330,7 @@ __device__ __forceinline__ void accept_walk(int n, const int32_t* __restrict__ n
     ++len;
     u = next;
   }
-  const int32_t bonus = target(u);
+  const int32_t bonus = target_of(u);
   if (bonus >= 0 && len < m + 1) {
     if (lane == 0) out[len] = bonus;
     ++len;
