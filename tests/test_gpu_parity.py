@@ -498,6 +498,56 @@ def test_targets_from_truth_edges():
     assert (got[5] == -1).all() and (got[0, 1:] == -1).all()
 
 
+def _decoy_trees(rng, B: int, R: int, m: int) -> tuple:
+    """Random trees (depth <= m, distinct sibling tokens) whose rows at and
+    past num_nodes are decoys: each hangs under a live row u and carries a
+    fresh token that is also u's target, so a walk that reads a row past
+    the node count would step into it.  Node counts include 0, 1 and R."""
+    nn = rng.integers(0, R + 1, size=B).astype(np.int32)
+    nn[:4] = (0, 1, 2, R)
+    tok = np.full((B, R), 7, np.int32)
+    par = np.full((B, R), -1, np.int32)
+    pos = np.zeros((B, R), np.int32)
+    tgt = rng.integers(-1, 50, size=(B, R)).astype(np.int32)
+    for b in range(B):
+        n = max(int(nn[b]), 1)
+        used = {}
+        for v in range(1, n):
+            u = int(rng.integers(0, v))
+            while pos[b, u] >= m:
+                u = int(par[b, u])
+            t = int(rng.integers(0, 12))
+            while t in used.setdefault(u, set()):
+                t += 1
+            used[u].add(t)
+            par[b, v], tok[b, v], pos[b, v] = u, t, pos[b, u] + 1
+            if rng.random() < 0.7:  # follow this child from u
+                tgt[b, u] = t
+        for v in range(n, R):
+            u = int(rng.integers(0, n))
+            fresh = 1000 + v
+            par[b, v], tok[b, v], pos[b, v] = u, fresh, pos[b, u] + 1
+            tgt[b, u] = fresh if rng.random() < 0.5 else tgt[b, u]
+    return nn, tok, par, pos, tgt
+
+
+@pytest.mark.parametrize("m", [3, 10])
+def test_accept_ignores_rows_past_the_node_count(m):
+    """fc_verify_accept against the oracle on trees whose rows past
+    num_nodes (0, 1, 2, R and random counts) hold decoys that match the
+    targets: only live rows may be walked."""
+    rng = np.random.default_rng(40 + m)
+    B, R = 96, 65
+    nn, tok, par, pos, tgt = _decoy_trees(rng, B, R, m)
+    tree = {"num_nodes": dev(nn), "node_tok": dev(tok), "parent": dev(par), "pos_ids": dev(pos)}
+    got = fc.fc_verify_accept(tree, dev(tgt), m=m)
+    torch.cuda.synchronize()
+    want = oracle.verify_accept(dict(num_nodes=nn, node_tok=tok, parent=par, pos_ids=pos), tgt, m=m)
+    for f in ("accept_len", "accept_tok", "last_node"):
+        assert (host(got[f]) == want[f]).all(), f
+    assert (want["last_node"] < np.maximum(nn, 1)).all()
+
+
 def test_unsorted_slots_are_flagged():
     """A query whose store slots are out of order gets num_nodes = -1 and
     padding rows; the other queries are unaffected."""
