@@ -382,7 +382,6 @@ def run_replay(args, cache: bool = False, control: bool = False):
     the seeded generator."""
     import torch
     import paper_2502_17139_amd as fc
-    from paper_2502_17139_amd.replay import GpuReplay
     import synth
 
     p = dict(synth.PARAMS)
@@ -396,12 +395,11 @@ def run_replay(args, cache: bool = False, control: bool = False):
         tok = int(np.bincount(truth.ravel()).argmax())
         draws = np.stack([synth.uniform(31, 30, step, truth.shape[0], 0, 2 ** 31 - 1) for step in range(1024)])
         ckw.update(missing=True, skip_tok=tok, skip_p=0.5, skip_draws=draws)
-    rp = GpuReplay(stores, truth, **p, **ckw)
-    rp.run(max_steps=args.warmup)  # warm-up steps, then a fresh replay is timed
-    rp.reset()
+    eng = fc.ReplayEngine(stores, torch.from_numpy(truth).to(dev), max_steps=512, **p, **ckw)
+    eng.run(limit=args.warmup)  # warm-up steps; every run replays from the start
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    res = rp.run(max_steps=512)
+    res = eng.run(limit=512)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     live = res["accept"] >= 0

@@ -81,6 +81,27 @@ fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint32_t* sa_ou
                              hipStream_t stream);
 
 /*
+ * fc_datastore_build that also reports how the doubling went (host struct,
+ * filled when the call returns; stats may be NULL).  Round r sorted the
+ * sorted[r] suffixes still tied after round r - 1 by their first
+ * prefix_len[r] tokens, and left unresolved[r] of them tied.  The last
+ * round leaves none tied, so the longest common prefix of two suffixes is
+ * below prefix_len[rounds - 1] and, when rounds > 1, at least
+ * prefix_len[rounds - 2].  sort_passes counts the radix passes run (a pass
+ * per key byte that is not the same for every suffix).
+ */
+#define FC_MAX_BUILD_ROUNDS 40
+typedef struct fc_build_stats {
+  int32_t rounds;
+  int32_t sort_passes;
+  uint64_t prefix_len[FC_MAX_BUILD_ROUNDS];
+  uint64_t sorted[FC_MAX_BUILD_ROUNDS];
+  uint64_t unresolved[FC_MAX_BUILD_ROUNDS];
+} fc_build_stats;
+fc_status fc_datastore_build_stats(const uint16_t* tokens, uint64_t n, uint32_t* sa_out, void* ws, size_t ws_bytes,
+                                   fc_build_stats* stats, hipStream_t stream);
+
+/*
  * Batched construction of many small stores (per-repository stores, Section
  * IV-A: the repository store is built per repository, offline, Section
  * V-D).  tokens holds n_seg stores back to back, store r at

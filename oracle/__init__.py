@@ -46,6 +46,8 @@ def _lib():
     lib.oracle_retrieve.restype = None
     lib.oracle_retrieve.argtypes = [i32, vp, vp, vp, i32, i32, i32, i32, i32, i32,
                                     vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.oracle_retrieve_batched.restype = None
+    lib.oracle_retrieve_batched.argtypes = lib.oracle_retrieve.argtypes
     lib.oracle_build_tree.restype = None
     lib.oracle_build_tree.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32,
                                       vp, vp, vp, vp, vp, vp]
@@ -96,12 +98,18 @@ def check_sa(text, sa) -> tuple[int, int]:
     return int(code), int(where.value)
 
 
-def retrieve(texts, ctx, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int = 10) -> dict:
+def retrieve(texts, ctx, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int = 10,
+             batched: bool = False) -> dict:
     """Batched suffix-match retrieval over stores in priority order.
 
     texts: list of uint16 arrays (store 0 = repository store first);
     ctx: uint16 [B][L].  Returns dict of match_n, range_lo, range_cnt, taken
     ([B][S]) and cont_pos, cont_src, cont_len ([B][k]), cont_tok ([B][k][m]).
+
+    batched=False runs the definition query by query (three scans of every
+    store per query); batched=True computes the same result with each scan
+    shared by the whole batch (one pass over a store per scan), which the
+    tests pin against the per-query form.
     """
     ts = [_u16(t) for t in texts]
     S = len(ts)
@@ -116,9 +124,10 @@ def retrieve(texts, ctx, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
         range_cnt=np.zeros((B, S), np.uint32), taken=np.zeros((B, S), np.int32),
         cont_pos=np.zeros((B, k), np.uint32), cont_src=np.zeros((B, k), np.uint8),
         cont_len=np.zeros((B, k), np.uint8), cont_tok=np.zeros((B, k, m), np.uint16))
-    _lib().oracle_retrieve(S, ctypes.cast(ptrs, ctypes.c_void_p), _p(lens), _p(c), B, L, n_max, n_min, k, m,
-                           _p(out["match_n"]), _p(out["range_lo"]), _p(out["range_cnt"]), _p(out["taken"]),
-                           _p(out["cont_pos"]), _p(out["cont_src"]), _p(out["cont_len"]), _p(out["cont_tok"]))
+    fn = _lib().oracle_retrieve_batched if batched else _lib().oracle_retrieve
+    fn(S, ctypes.cast(ptrs, ctypes.c_void_p), _p(lens), _p(c), B, L, n_max, n_min, k, m,
+       _p(out["match_n"]), _p(out["range_lo"]), _p(out["range_cnt"]), _p(out["taken"]),
+       _p(out["cont_pos"]), _p(out["cont_src"]), _p(out["cont_len"]), _p(out["cont_tok"]))
     return out
 
 
@@ -318,7 +327,7 @@ def replay(texts, truth, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int 
             else:
                 misses.append(j)
         if misses:
-            r = retrieve(texts, ctx[misses], n_max=n_max, n_min=n_min, k=k, m=m)
+            r = retrieve(texts, ctx[misses], n_max=n_max, n_min=n_min, k=k, m=m, batched=True)
             for i, j in enumerate(misses):
                 b = act[j]
                 if len(caches[b]) >= lru:

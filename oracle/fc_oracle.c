@@ -263,6 +263,218 @@ void oracle_retrieve(int S, const uint16_t* const* texts, const uint64_t* lens, 
   }
 }
 
+/*
+ * The same retrieval as oracle_retrieve, computed with the text scans shared
+ * by the whole batch: each store is read by one pass per question instead of
+ * three passes per query, which makes batches of a thousand queries over a
+ * billion-token store practical on the CPU.  Every query's answer is the one
+ * oracle_retrieve defines, step for step:
+ *   1. its longest occurring suffix: the agreement of the context with the
+ *      text before every end position e, capped at n_hi; the queries are
+ *      listed by their last token, so at e only the queries whose last token
+ *      is T[e-1] are compared (for the others the agreement is 0);
+ *   2. for the chosen q_n, at every start j: when T[j] equals q_n's first
+ *      token, the suffix at j is compared with q_n (an occurrence, or below,
+ *      or above); a suffix whose first token is smaller than q_n's is below,
+ *      counted through the number of start positions per first token;
+ *   3. the occurrences in suffix order by the direct suffix comparison;
+ *   4. the budget fill, strided picks and continuation cut of
+ *      oracle_retrieve.
+ * Steps 1 and 2 split the text into chunks, one per thread, and add up
+ * per-thread results; nothing else is reordered.
+ */
+typedef struct {
+  uint32_t* v;
+  uint64_t n, cap;
+} u32_list;
+
+static void u32_push(u32_list* l, uint32_t x) {
+  if (l->n == l->cap) {
+    l->cap = l->cap ? 2 * l->cap : 16;
+    l->v = (uint32_t*)realloc(l->v, l->cap * sizeof(uint32_t));
+  }
+  l->v[l->n++] = x;
+}
+
+static int omp_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+static int omp_thread(void) {
+#ifdef _OPENMP
+  return omp_get_thread_num();
+#else
+  return 0;
+#endif
+}
+
+/* match_n, range_lo, occurrences (suffix order) of every query in one store */
+static void match_batch_one_source(const uint16_t* T, uint64_t N, const uint16_t* ctx, int B, int L, int n_max,
+                                   int n_min, source_match* out) {
+  const int nt = omp_threads();
+  int* n_hi = (int*)malloc((size_t)(B ? B : 1) * sizeof(int));
+  int* head = (int*)malloc(65536 * sizeof(int));
+  int* next = (int*)malloc((size_t)(B ? B : 1) * sizeof(int));
+  for (int b = 0; b < B; ++b) {
+    out[b].match_n = 0;
+    out[b].range_lo = 0;
+    out[b].range_cnt = 0;
+    out[b].occ = NULL;
+    n_hi[b] = query_limit(ctx + (size_t)b * L, L, n_max);
+  }
+  if (N > 0) {
+    /* step 1: longest agreement before every end position, per query */
+    for (int t = 0; t < 65536; ++t) head[t] = -1;
+    for (int b = B - 1; b >= 0; --b) {
+      if (n_hi[b] < n_min || n_hi[b] < 1) continue;
+      const uint16_t last = ctx[(size_t)b * L + L - 1];
+      next[b] = head[last];
+      head[last] = b;
+    }
+    int* best = (int*)calloc((size_t)nt * (B ? B : 1), sizeof(int));
+#pragma omp parallel
+    {
+      int* mine = best + (size_t)omp_thread() * (B ? B : 1);
+#pragma omp for schedule(static)
+      for (uint64_t e = 1; e <= N; ++e) {
+        for (int b = head[T[e - 1]]; b >= 0; b = next[b]) {
+          const uint16_t* end = ctx + (size_t)b * L + L;
+          int l = 0;
+          while (l < n_hi[b] && (uint64_t)l < e && T[e - 1 - l] == end[-1 - l]) ++l;
+          if (l > mine[b]) mine[b] = l;
+        }
+      }
+    }
+    for (int b = 0; b < B; ++b) {
+      int l = 0;
+      for (int t = 0; t < nt; ++t)
+        if (best[(size_t)t * B + b] > l) l = best[(size_t)t * B + b];
+      out[b].match_n = l >= n_min ? l : 0;
+    }
+    free(best);
+
+    /* step 2: occurrences and the suffixes below q_n, per query */
+    {
+      uint64_t* first = (uint64_t*)calloc(65536, sizeof(uint64_t)); /* start positions per first token */
+      for (int t = 0; t < 65536; ++t) head[t] = -1;
+      for (int b = B - 1; b >= 0; --b) {
+        const int n = out[b].match_n;
+        if (n == 0) continue;
+        const uint16_t q0 = ctx[(size_t)b * L + L - n];
+        next[b] = head[q0];
+        head[q0] = b;
+      }
+      uint64_t* below = (uint64_t*)calloc((size_t)nt * (B ? B : 1), sizeof(uint64_t));
+      u32_list* occ = (u32_list*)calloc((size_t)nt * (B ? B : 1), sizeof(u32_list));
+      uint64_t* first_t = (uint64_t*)calloc((size_t)nt * 65536, sizeof(uint64_t));
+#pragma omp parallel
+      {
+        const int me = omp_thread();
+        uint64_t* my_below = below + (size_t)me * (B ? B : 1);
+        u32_list* my_occ = occ + (size_t)me * (B ? B : 1);
+        uint64_t* my_first = first_t + (size_t)me * 65536;
+#pragma omp for schedule(static)
+        for (uint64_t j = 0; j < N; ++j) {
+          my_first[T[j]]++;
+          for (int b = head[T[j]]; b >= 0; b = next[b]) {
+            const int n = out[b].match_n;
+            const int c = cmp_suffix_pattern(T, N, j, ctx + (size_t)b * L + L - n, n);
+            if (c < 0) my_below[b]++;
+            else if (c == 0) u32_push(&my_occ[b], (uint32_t)j);
+          }
+        }
+      }
+      for (int t = 0; t < nt; ++t)
+        for (int x = 0; x < 65536; ++x) first[x] += first_t[(size_t)t * 65536 + x];
+#pragma omp parallel for schedule(dynamic, 1)
+      for (int b = 0; b < B; ++b) {
+        const int n = out[b].match_n;
+        if (n == 0) continue;
+        const uint16_t q0 = ctx[(size_t)b * L + L - n];
+        uint64_t lo = 0, cnt = 0;
+        for (int x = 0; x < q0; ++x) lo += first[x];
+        for (int t = 0; t < nt; ++t) {
+          lo += below[(size_t)t * B + b];
+          cnt += occ[(size_t)t * B + b].n;
+        }
+        uint32_t* all = (uint32_t*)malloc((size_t)(cnt ? cnt : 1) * sizeof(uint32_t));
+        uint64_t at = 0;
+        for (int t = 0; t < nt; ++t) {
+          u32_list* l = &occ[(size_t)t * B + b];
+          if (l->n) memcpy(all + at, l->v, l->n * sizeof(uint32_t));
+          at += l->n;
+          free(l->v);
+        }
+        /* step 3 */
+        text_ref tr = {T, N};
+        qsort_r(all, cnt, sizeof(uint32_t), cmp_sa_entries, &tr);
+        out[b].range_lo = (uint32_t)lo;
+        out[b].range_cnt = (uint32_t)cnt;
+        out[b].occ = all;
+      }
+      free(first_t);
+      free(occ);
+      free(below);
+      free(first);
+    }
+  }
+  free(next);
+  free(head);
+  free(n_hi);
+}
+
+void oracle_retrieve_batched(int S, const uint16_t* const* texts, const uint64_t* lens, const uint16_t* ctx, int B,
+                             int L, int n_max, int n_min, int k, int m, int32_t* match_n, uint32_t* range_lo,
+                             uint32_t* range_cnt, int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src,
+                             uint8_t* cont_len, uint16_t* cont_tok) {
+  source_match* sm = (source_match*)malloc((size_t)(B ? B : 1) * S * sizeof(source_match));
+  for (int s = 0; s < S; ++s) match_batch_one_source(texts[s], lens[s], ctx, B, L, n_max, n_min, sm + (size_t)s * B);
+  /* step 4: exactly the fill of oracle_retrieve */
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int b = 0; b < B; ++b) {
+    uint32_t* pos = cont_pos + (size_t)b * k;
+    uint8_t* src = cont_src + (size_t)b * k;
+    uint8_t* len = cont_len + (size_t)b * k;
+    uint16_t* tok = cont_tok + (size_t)b * k * m;
+    for (int i = 0; i < k; ++i) {
+      pos[i] = 0xFFFFFFFFu;
+      src[i] = 0xFF;
+      len[i] = 0;
+    }
+    memset(tok, 0, (size_t)k * m * sizeof(uint16_t));
+    int64_t used = 0;
+    for (int s = 0; s < S; ++s) {
+      const source_match* x = &sm[(size_t)s * B + b];
+      int64_t budget = k - used;
+      int64_t t = (int64_t)x->range_cnt < budget ? (int64_t)x->range_cnt : budget;
+      match_n[b * S + s] = x->match_n;
+      range_lo[b * S + s] = x->range_lo;
+      range_cnt[b * S + s] = x->range_cnt;
+      taken[b * S + s] = (int32_t)t;
+      for (int64_t i = 0; i < t; ++i) {
+        uint64_t off = ((int64_t)x->range_cnt > budget) ? (uint64_t)i * x->range_cnt / (uint64_t)budget : (uint64_t)i;
+        uint64_t start = (uint64_t)x->occ[off] + (uint64_t)x->match_n;
+        int64_t slot = used + i;
+        int l = 0;
+        while (l < m && start + l < lens[s] && texts[s][start + l] != 0) {
+          tok[slot * m + l] = texts[s][start + l];
+          ++l;
+        }
+        pos[slot] = (uint32_t)start;
+        src[slot] = (uint8_t)s;
+        len[slot] = (uint8_t)l;
+      }
+      used += t;
+    }
+  }
+  for (size_t i = 0; i < (size_t)B * S; ++i) free(sm[i].occ);
+  free(sm);
+}
+
 /* ------------------------------------------------------------------------- */
 /* Weighted trie, top-c selection, tree emission (Section IV-D, eq. (3)-(4)).  */
 /* ------------------------------------------------------------------------- */
@@ -458,6 +670,10 @@ void oracle_build_tree(int B, int S, int k, int m, int c, const uint32_t* alpha,
  * tokens).  accept_len = depth(u) + 1 (the path plus the target's own token
  * at u), or depth(u) when target[u] is -1.  accept_tok lists the path tokens
  * then target[u]; unused entries are -1.  last_node = u.
+ * Precondition: no row is deeper than m (every tree built from continuations
+ * of at most m tokens meets it).  accept_tok holds m + 1 tokens, so for a
+ * deeper tree the walk stops once m + 1 tokens are accepted (and the
+ * target's own token is then not added); nothing is written past m + 1.
  * Arrays: num_nodes [B]; node_tok, parent, pos_ids, target [B][c+1];
  * accept_len, last_node [B]; accept_tok [B][m+1].
  */
@@ -474,6 +690,7 @@ void oracle_verify_accept(int B, int c, int m, const int32_t* num_nodes, const i
     int32_t u = 0, n = num_nodes[b];
     int len = 0;
     for (;;) {
+      if (len == m + 1) break; /* accept_tok is full: only a tree deeper than m gets here */
       int32_t next = -1;
       if (tgt[u] >= 0)
         for (int32_t v = 1; v < n; ++v)
@@ -485,7 +702,7 @@ void oracle_verify_accept(int B, int c, int m, const int32_t* num_nodes, const i
       out[len++] = tok[next];
       u = next;
     }
-    if (tgt[u] >= 0) out[len++] = tgt[u];
+    if (tgt[u] >= 0 && len < m + 1) out[len++] = tgt[u];
     (void)pos_ids;
     accept_len[b] = len;
     last_node[b] = u;

@@ -38,6 +38,7 @@ EXPORTS = (
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
     "fc_verify_accept", "fc_targets_from_truth", "fc_cache_lds_bytes", "fc_cache_retrieve", "fc_cache_write",
     "fc_tree_attention", "fc_replay_init", "fc_replay_run",
+    "fc_datastore_build_stats",
 )
 
 
@@ -53,6 +54,15 @@ class FcStore(ctypes.Structure):
     _fields_ = [("tokens", ctypes.c_void_p), ("sa", ctypes.c_void_p), ("bucket", ctypes.c_void_p),
                 ("n", ctypes.c_uint64), ("pair", ctypes.c_void_p), ("pair_vocab", ctypes.c_uint32),
                 ("rec", ctypes.c_void_p)]
+
+
+FC_MAX_BUILD_ROUNDS = 40
+
+
+class FcBuildStats(ctypes.Structure):
+    _fields_ = [("rounds", ctypes.c_int32), ("sort_passes", ctypes.c_int32),
+                ("prefix_len", ctypes.c_uint64 * FC_MAX_BUILD_ROUNDS), ("sorted", ctypes.c_uint64 * FC_MAX_BUILD_ROUNDS),
+                ("unresolved", ctypes.c_uint64 * FC_MAX_BUILD_ROUNDS)]
 
 
 class FcRetrieveParams(ctypes.Structure):
@@ -104,6 +114,8 @@ def lib() -> ctypes.CDLL:
     L.fc_datastore_build_workspace_bytes.argtypes = [u64]
     L.fc_datastore_build.restype = ctypes.c_int
     L.fc_datastore_build.argtypes = [vp, u64, vp, vp, sz, vp]
+    L.fc_datastore_build_stats.restype = ctypes.c_int
+    L.fc_datastore_build_stats.argtypes = [vp, u64, vp, vp, sz, ctypes.POINTER(FcBuildStats), vp]
     L.fc_datastore_build_batched_workspace_bytes.restype = sz
     L.fc_datastore_build_batched_workspace_bytes.argtypes = [u64, i32]
     L.fc_datastore_build_batched.restype = ctypes.c_int
@@ -227,6 +239,26 @@ def fc_datastore_build(tokens: torch.Tensor, sa_out: torch.Tensor | None = None,
     _check("fc_datastore_build", lib().fc_datastore_build(_ptr(tokens), n, _ptr(sa_out), _ptr(workspace),
                                                          workspace.numel(), _stream(stream)))
     return sa_out
+
+
+def fc_datastore_build_stats(tokens: torch.Tensor, sa_out: torch.Tensor | None = None,
+                             workspace: torch.Tensor | None = None, stream=None) -> tuple:
+    """fc_datastore_build that also returns the doubling rounds: (sa, dict of
+    rounds, sort_passes and per-round prefix_len, sorted, unresolved)."""
+    if tokens.dtype != torch.uint16 or tokens.dim() != 1:
+        raise ValueError("tokens must be a 1-D uint16 tensor")
+    n = tokens.numel()
+    if sa_out is None:
+        sa_out = _empty(n, torch.uint32, tokens.device)
+    need = fc_datastore_build_workspace_bytes(n)
+    if workspace is None:
+        workspace = _empty(max(need, 1), torch.uint8, tokens.device)
+    st = FcBuildStats()
+    _check("fc_datastore_build_stats", lib().fc_datastore_build_stats(
+        _ptr(tokens), n, _ptr(sa_out), _ptr(workspace), workspace.numel(), ctypes.byref(st), _stream(stream)))
+    r = int(st.rounds)
+    return sa_out, dict(rounds=r, sort_passes=int(st.sort_passes), prefix_len=list(st.prefix_len[:r]),
+                        sorted=list(st.sorted[:r]), unresolved=list(st.unresolved[:r]))
 
 
 def fc_datastore_build_batched(tokens: torch.Tensor, seg_off, sa_out: torch.Tensor | None = None,

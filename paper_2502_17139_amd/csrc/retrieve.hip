@@ -518,18 +518,21 @@ extern "C" size_t fc_retrieve_workspace_bytes(int32_t B, int32_t S, fc_retrieve_
   return B > 0 ? ((size_t)B + 1) * sizeof(uint32_t) : 0;
 }
 
-extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
-                                 fc_retrieve_params p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
-                                 int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len,
-                                 uint16_t* cont_tok, const int32_t* rows, int32_t n_rows, void* ws,
-                                 size_t ws_bytes, hipStream_t stream) {
+namespace {
+
+// Host-side checks of fc_retrieve; fills the
+// kernels' store arguments.  Nothing touches the device.
+fc_status retrieve_check(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
+                         const fc_retrieve_params& p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
+                         int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len,
+                         uint16_t* cont_tok, const int32_t* rows, int32_t n_rows, StoreArgs& st) {
   if (!stores || S < 1 || S > FC_MAX_SOURCES) return FC_ERR_INVALID;
   if (B < 0 || L < 1) return FC_ERR_INVALID;
   if (p.n_max < 1 || p.n_max > FC_MAX_NMAX || p.n_min < 1 || p.n_min > p.n_max) return FC_ERR_INVALID;
   if (p.k < 1 || p.m < 1 || p.m > 255) return FC_ERR_INVALID;
   if ((int64_t)S * (p.n_max - p.n_min + 1) * 2 > 4 * fc::kWave) return FC_ERR_INVALID;
   if ((uint64_t)B * (uint64_t)p.k > 0x7FFFFFFFull) return FC_ERR_UNSUPPORTED;  // slot numbers stay below 2^31
-  StoreArgs st = {};
+  st = StoreArgs{};
   for (int s = 0; s < S; ++s) {
     const fc_store& x = stores[s];
     if (x.n >= 0xFFFFFFFFull) return FC_ERR_INVALID;
@@ -548,7 +551,15 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
   if (!ctx || !match_n || !range_lo || !range_cnt || !taken || !cont_pos || !cont_src || !cont_len || !cont_tok)
     return FC_ERR_INVALID;
   if (rows && n_rows < 1) return FC_ERR_INVALID;
-  if (!ws || ws_bytes < fc_retrieve_workspace_bytes(B, S, p)) return FC_ERR_WORKSPACE;
+  return FC_OK;
+}
+
+// The launches of one retrieval (after retrieve_check and with a workspace
+// of at least fc_retrieve_workspace_bytes bytes).
+fc_status retrieve_launch(const StoreArgs& st, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
+                          const fc_retrieve_params& p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
+                          int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len,
+                          uint16_t* cont_tok, const int32_t* rows, int32_t n_rows, void* ws, hipStream_t stream) {
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_search, dim3(fc::div_up(B, kQueriesPerBlock)), dim3(kSearchThreads), 0, stream, st, S, ctx,
                      B, L, p.n_max, p.n_min, p.k, rows, n_rows, match_n, range_lo, range_cnt, taken);
@@ -576,4 +587,20 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
   }
   FC_CHECK_LAUNCH();
   return FC_OK;
+}
+
+}  // namespace
+
+extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
+                                 fc_retrieve_params p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
+                                 int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len,
+                                 uint16_t* cont_tok, const int32_t* rows, int32_t n_rows, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+  StoreArgs st;
+  const fc_status e = retrieve_check(stores, S, ctx, B, L, p, match_n, range_lo, range_cnt, taken, cont_pos,
+                                     cont_src, cont_len, cont_tok, rows, n_rows, st);
+  if (e != FC_OK || B == 0) return e;
+  if (!ws || ws_bytes < fc_retrieve_workspace_bytes(B, S, p)) return FC_ERR_WORKSPACE;
+  return retrieve_launch(st, S, ctx, B, L, p, match_n, range_lo, range_cnt, taken, cont_pos, cont_src, cont_len,
+                         cont_tok, rows, n_rows, ws, stream);
 }

@@ -900,7 +900,7 @@ struct ExtendArgs {
 // offsets already in w.seg_off), or over the n new suffixes of an extension
 // (ext; leaves their ranks in w.rank and writes no suffix array).
 fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& w, uint32_t* sa_out,
-                   hipStream_t stream, const ExtendArgs* ext = nullptr) {
+                   hipStream_t stream, const ExtendArgs* ext = nullptr, fc_build_stats* stats = nullptr) {
   const uint32_t N = (uint32_t)n;
   const uint64_t tiles = (n + kSortTile - 1) / kSortTile;
   FC_CHECK_HIP(hipMemsetAsync(w.status, 0, sizeof(uint64_t) * tiles * kRadix, stream));
@@ -971,6 +971,13 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
     FC_CHECK_HIP(hipMemcpyAsync(host_misc, w.misc, sizeof(uint32_t) * 2, hipMemcpyDeviceToHost, stream));
     FC_CHECK_HIP(hipStreamSynchronize(stream));
     if (host_misc[0]) return FC_ERR_DEVICE;
+    if (stats && round < FC_MAX_BUILD_ROUNDS) {
+      stats->prefix_len[round] = h;
+      stats->sorted[round] = U;
+      stats->unresolved[round] = host_misc[1];
+      stats->rounds = round + 1;
+      stats->sort_passes = (int32_t)st.ticket;
+    }
     U = host_misc[1];
     vin = res ^ 1;
     if (U == 0) break;
@@ -989,16 +996,22 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
 
 extern "C" size_t fc_datastore_build_workspace_bytes(uint64_t n) { return carve_build(nullptr, n, nullptr); }
 
-extern "C" fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint32_t* sa_out, void* ws,
-                                        size_t ws_bytes, hipStream_t stream) {
+extern "C" fc_status fc_datastore_build_stats(const uint16_t* tokens, uint64_t n, uint32_t* sa_out, void* ws,
+                                              size_t ws_bytes, fc_build_stats* stats, hipStream_t stream) {
   if (n >= 0xFFFFFFFFull) return FC_ERR_INVALID;
+  if (stats) *stats = fc_build_stats{};
   if (n == 0) return FC_OK;
   if (!tokens || !sa_out) return FC_ERR_INVALID;
   if (!ws || ws_bytes < fc_datastore_build_workspace_bytes(n)) return FC_ERR_WORKSPACE;
   (void)hipGetLastError();
   BuildWs w;
   carve_build(ws, n, &w);
-  return build_sa(tokens, n, 0, w, sa_out, stream);
+  return build_sa(tokens, n, 0, w, sa_out, stream, nullptr, stats);
+}
+
+extern "C" fc_status fc_datastore_build(const uint16_t* tokens, uint64_t n, uint32_t* sa_out, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+  return fc_datastore_build_stats(tokens, n, sa_out, ws, ws_bytes, nullptr, stream);
 }
 
 extern "C" size_t fc_datastore_build_batched_workspace_bytes(uint64_t n, int32_t n_seg) {

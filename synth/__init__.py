@@ -163,7 +163,14 @@ def _window_fresh(p: Pool, qseed: int, q: int, extra: int) -> np.ndarray:
     return text[off:off + CTX_LEN + extra].copy()
 
 
-def query_plan(cfg: int) -> list:
+def query_seed(cfg: int, rotation: int = 0) -> int:
+    """Seed of a configuration's query batch; rotation r > 0 names the r-th
+    further batch drawn the same way (distinct windows of the same stores),
+    for timing over batches that do not repeat."""
+    return WORKLOADS[cfg]["qseed"] + 1_000_033 * rotation
+
+
+def query_plan(cfg: int, rotation: int = 0) -> list:
     """(kind, role) of every query, in batch order.
 
     kind is 'random' (a 16-token window at a uniform file and offset of the
@@ -185,15 +192,16 @@ def query_plan(cfg: int) -> list:
         n_rand = (g + 1) // 2
         plan += [("random", role)] * n_rand + [("fresh", role)] * (g - n_rand)
     # Fisher-Yates with the configuration's shuffle stream.
-    r = uniform(c["qseed"], ROLE_SHUFFLE, 0, len(plan), 0, 0x7FFFFFFF)
+    r = uniform(query_seed(cfg, rotation), ROLE_SHUFFLE, 0, len(plan), 0, 0x7FFFFFFF)
     for i in range(len(plan) - 1, 0, -1):
         j = int(r[i]) % (i + 1)
         plan[i], plan[j] = plan[j], plan[i]
     return plan
 
 
-def queries(cfg: int, count: int | None = None, next_tokens: int = 0):
-    """Query contexts, uint16 [B][16] (the first `count` of the batch if given).
+def queries(cfg: int, count: int | None = None, next_tokens: int = 0, rotation: int = 0):
+    """Query contexts, uint16 [B][16] (the first `count` of the batch if given;
+    batch `rotation` of the configuration, see query_seed).
 
     With next_tokens > 0 also returns the tokens that truly follow each
     window, uint16 [B][next_tokens] (the store's own text for a random
@@ -201,17 +209,18 @@ def queries(cfg: int, count: int | None = None, next_tokens: int = 0):
     for a fresh one): the ground truth a target model would reproduce.
     """
     c = WORKLOADS[cfg]
-    plan = query_plan(cfg)
+    plan = query_plan(cfg, rotation)
     if count is not None:
         plan = plan[:count]
+    qseed = query_seed(cfg, rotation)
     stores = {r: (seed, nt, s, nf) for r, seed, nt, s, nf in c["stores"]}
     out = np.empty((len(plan), CTX_LEN + next_tokens), dtype=np.uint16)
     for q, (kind, role) in enumerate(plan):
         seed, nt, s, nf = stores[role]
         if kind == "random":
-            out[q] = _window_random(nf, c["qseed"], q, store(cfg, role), next_tokens)
+            out[q] = _window_random(nf, qseed, q, store(cfg, role), next_tokens)
         else:
-            out[q] = _window_fresh(pool(seed, nt, s), c["qseed"], q, next_tokens)
+            out[q] = _window_fresh(pool(seed, nt, s), qseed, q, next_tokens)
     if next_tokens:
         return np.ascontiguousarray(out[:, :CTX_LEN]), np.ascontiguousarray(out[:, CTX_LEN:])
     return out

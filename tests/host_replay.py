@@ -1,20 +1,23 @@
-"""Decode-trace replay on the GPU.
+"""Decode-trace replay driven from the host: a second implementation of the
+replay, for the tests only.
 
-Drives the draft stage over known token streams as a stand-in for a
-decoding loop: every step each live stream retrieves (or reuses a cached
-retrieval for the same 16-token context), builds its draft tree, receives
-the true next tokens as the target model's outputs, and advances by the
-accepted length.  The mean advance per step is the paper's average
-acceptance length (Section V-C, eq. (7)).
+It drives the draft stage over known token streams as a stand-in for a
+decoding loop, through the library's entry points one call at a time: every
+step each live stream retrieves (or reuses a cached retrieval for the same
+16-token context), builds its draft tree, receives the true next tokens as
+the target model's outputs, and advances by the accepted length.  The mean
+advance per step is the paper's average acceptance length (Section V-C,
+eq. (7)).  The product's replay is the device-resident engine
+(paper_2502_17139_amd.ReplayEngine, fc_replay_init / fc_replay_run); the
+tests run both and compare each with the oracle.
 
 Per stream, an LRU cache of 32 recent retrievals is keyed by the exact
-16-token context; a hit reuses the stored retrieval and becomes most
-recent, a miss retrieves into the least recent slot.  The cache lives on the
-GPU: its slots are rows of the retrieval output arrays, misses are retrieved
-straight into their slot (fc_retrieve's row map) and the tree reads each
-stream's slot in place (fc_build_tree's row map), so cached results are
-never copied.  Only the cache keys and positions are kept on the host; one
-small copy of the accepted lengths comes back per step.
+16-token context; a hit reuses the stored retrieval and becomes most recent,
+a miss retrieves into the least recent slot.  The slots are rows of the
+retrieval output arrays on the GPU: misses are retrieved straight into their
+slot (fc_retrieve's row map) and the tree reads each stream's slot in place
+(fc_build_tree's row map).  The cache keys and positions are kept on the
+host; one small copy of the accepted lengths comes back per step.
 
 With cache_l set, each stream also keeps the paper's CACHE (Section IV-B)
 and follows the cache branch of Alg. 1: once the CACHE holds cache_l
@@ -27,11 +30,6 @@ host keeps the sequence lists, decides evictions (oldest sequences first
 when a text would outgrow its row) and ships each step's appended tokens in
 one batched fc_cache_write.
 
-run() hands the whole replay to the device-resident engine (ReplayEngine:
-fc_replay_init / fc_replay_run), which takes the same decisions on the GPU
-with no host round trip per step; step() is this module's own host-driven
-loop (run(native=False)), kept as a second implementation.
-
 Alg. 1's retrieval-timing control (for contexts the CACHE did not serve):
 with missing=True a per-stream missing table holds the contexts whose
 datastore retrieval found nothing, and such a context is not retrieved
@@ -39,6 +37,9 @@ again; with skip_tok set, a context ending with skip_tok is retrieved only
 when the step's draw (skip_draws[step][stream], uniform in [0, 2^31)) is
 below skip_p * 2^31.  A context that is not retrieved gets an empty result
 (a bare root).  Both tables are host-side sets next to the LRU keys.
+
+GpuReplay.run(native=True) hands the replay to the device engine with the
+same parameters; run(native=False) steps this loop.
 """
 from __future__ import annotations
 
@@ -47,9 +48,10 @@ from collections import OrderedDict
 import numpy as np
 import torch
 
-from . import (FC_MAX_CACHE_TOKENS, ReplayEngine, accept_outputs, fc_build_tree, fc_build_tree_workspace_bytes,
-               fc_cache_retrieve, fc_cache_write, fc_retrieve, fc_retrieve_workspace_bytes, fc_targets_from_truth,
-               fc_verify_accept, retrieve_outputs, tree_outputs)
+from paper_2502_17139_amd import (FC_MAX_CACHE_TOKENS, ReplayEngine, accept_outputs, fc_build_tree,
+                                  fc_build_tree_workspace_bytes, fc_cache_retrieve, fc_cache_write, fc_retrieve,
+                                  fc_retrieve_workspace_bytes, fc_targets_from_truth, fc_verify_accept,
+                                  retrieve_outputs, tree_outputs)
 
 
 class _Sequences:

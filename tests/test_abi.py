@@ -256,7 +256,7 @@ def test_struct_layouts_match_header(tmp_path):
     if shutil.which("gcc") is None:
         pytest.skip("no C compiler")
     structs = {"fc_replay": fc.FcReplay, "fc_store": fc.FcStore, "fc_retrieve_params": fc.FcRetrieveParams,
-               "fc_tree_params": fc.FcTreeParams}
+               "fc_tree_params": fc.FcTreeParams, "fc_build_stats": fc.FcBuildStats}
     lines = ["#include <stdio.h>", '#include "fastcoder.h"', "int main(void) {"]
     for name, cls in structs.items():
         lines.append(f'  printf("{name} sizeof %zu\\n", sizeof({name}));')

@@ -4,9 +4,12 @@ the oracle's bit for bit on the same seeded inputs.
 Sizes: tiny adversarial texts (small vocabularies force long repeats and
 ties) spanning several 4096-suffix sort tiles with ragged tails; the 1M-token
 single store of the first workload in full; the 2M + 100M two-store workload
-in full; and the 10M + 1B headline workload in the batch shape the benchmark
-launches, checked on sampled queries (the oracle scans 1B tokens per query)
-and on the suffix arrays by the linear-time checker.
+in full; the 10M + 1B headline workload in the batch shape the benchmark
+launches, every query of it (the oracle's batched form makes one pass over
+each store for the batch), with the suffix arrays by the linear-time
+checker; and the decode-trace replay on those stores, 128 streams for 32
+steps against the oracle run live and for the full 512 steps against the
+oracle's stored trace.
 """
 import numpy as np
 import pytest
@@ -23,7 +26,7 @@ if not torch.cuda.is_available():  # pragma: no cover - CPU container
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_2502_17139_amd as fc  # noqa: E402
-from paper_2502_17139_amd.replay import GpuReplay  # noqa: E402
+from host_replay import GpuReplay  # noqa: E402
 
 P = dict(synth.PARAMS)
 
@@ -333,41 +336,82 @@ def test_two_store_workload_full_batch():
     compare_tree(g, o)
 
 
-def test_headline_workload_sampled():
-    """10M + 1B stores, the full 1024-query batch in one launch; the oracle
-    recomputes a sample of queries one by one."""
+@pytest.fixture(scope="module")
+def headline():
+    """The 10M-token project store and the 1B-token general store, on the GPU
+    with two-token tables and records (as the benchmark runs them)."""
     say("headline: generating stores")
     tp, tg = synth.store(3, "project"), synth.store(3, "general")
-    ctx = synth.queries(3)
     say("headline: building suffix arrays")
     stores = [gpu_store(tp, synth.VOCAB, records=True), gpu_store(tg, synth.VOCAB, records=True)]
     torch.cuda.synchronize()
+    yield tp, tg, stores
+    del stores
+    synth.drop_cache()
+    torch.cuda.empty_cache()
+
+
+def test_headline_workload_full_batch(headline):
+    """10M + 1B stores: the whole 1,024-query batch in the launch shape the
+    benchmark times, every query compared with the oracle (its batched form,
+    one pass over each store for the batch); suffix arrays by the
+    linear-time checker."""
+    tp, tg, stores = headline
+    ctx = synth.queries(3)
     say("headline: checking suffix arrays")
     for t, st in zip((tp, tg), stores):
         assert oracle.check_sa(t, host(st.sa)) == (0, 0)
     say("headline: gpu pipeline")
     g = gpu_pipeline(stores, ctx, P, (1, 1), P["c"])
-    rows = list(range(0, 1024, 43))
-    say(f"headline: oracle on {len(rows)} queries")
-    o = oracle_pipeline([tp, tg], ctx[rows], P, (1, 1), P["c"])
-    compare_retrieve(g, o, rows)
-    compare_tree(g, o, rows)
-    tg_ = {f: g[f] for f in ("node_tok", "parent", "num_nodes")}
-    targets = _targets(tg_, 3)
-    ga = fc.fc_verify_accept(g["_tree_dev"], dev(targets), m=P["m"])
-    oa = oracle.verify_accept(o, _targets({f: o[f] for f in ("node_tok", "parent", "num_nodes")}, 3, rows),
-                              m=P["m"])
-    for i, b in enumerate(rows):
-        for f in ("accept_len", "accept_tok", "last_node"):
-            assert (host(ga[f])[b] == oa[f][i]).all(), (f, b)
-    # decode-trace replay over the same stores: a few streams, first steps
-    say("headline: replay")
-    truth = synth.truth(n_seq=4)
-    g = GpuReplay(stores, truth, **P).run(max_steps=6)
-    o = oracle.replay([tp, tg], truth, **P, max_steps=6)
+    say("headline: oracle on all 1024 queries")
+    r = oracle.retrieve([tp, tg], ctx, n_max=P["n_max"], n_min=P["n_min"], k=P["k"], m=P["m"], batched=True)
+    o = dict(r)
+    o.update(oracle.build_tree(r["taken"], r["cont_len"], r["cont_tok"], ctx, c=P["c"], alpha=(1, 1)))
+    say("headline: comparing")
+    compare_retrieve(g, o)
+    compare_tree(g, o)
+    assert int(o["taken"].sum()) > 800_000  # the batch keeps ~900k slots: the heavy paths run
+    _check_accept(g, o, P["m"], seed=3)
+
+
+def test_headline_replay_live(headline):
+    """Decode-trace replay on the 10M + 1B stores, all 128 streams, the
+    first 32 steps: the device engine against the oracle run now (every
+    accepted length, LRU hit and lookup, and position)."""
+    tp, tg, stores = headline
+    truth = synth.truth()
+    say("headline replay: engine, 128 streams x 32 steps")
+    eng = fc.ReplayEngine(stores, dev(truth), max_steps=512, **P)
+    g = eng.run(limit=32)
+    say("headline replay: oracle")
+    o = oracle.replay([tp, tg], truth, **P, max_steps=32)
+    assert g["steps"] == o["steps"] == 32
     for f in ("accept", "hits", "lookups", "pos"):
         assert (g[f] == o[f]).all(), f
-    synth.drop_cache()
+
+
+def test_headline_replay_golden(headline, golden):
+    """The full replay shape, 128 streams x 512 steps on the 10M + 1B
+    stores: the device engine against the oracle's trace stored in
+    tests/golden (written by make_replay_golden.py, which calls only the
+    oracle and the generator), after checking the inputs' SHA-256."""
+    import hashlib
+    tp, tg, stores = headline
+    truth = synth.truth()
+    gold = golden("replay_10M_1B_128x512.json")
+    sha = lambda a: hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()  # noqa: E731
+    assert gold["sha256"] == {"project": sha(tp), "general": sha(tg), "truth": sha(truth)}
+    assert gold["params"] == {kk: (list(v) if isinstance(v, tuple) else v) for kk, v in P.items()}
+    say("headline replay: engine, 128 streams x 512 steps")
+    eng = fc.ReplayEngine(stores, dev(truth), max_steps=512, lru=gold["lru"], **P)
+    g = eng.run(limit=gold["max_steps"])
+    digits = "0123456789abcdefghijklmnopqrstuvwxyz"
+    acc = np.array([[-1 if ch == "." else digits.index(ch) for ch in col] for col in gold["accept"]]).T
+    assert g["steps"] == gold["steps"] and g["accept"].shape == acc.shape
+    assert (g["accept"] == acc).all()
+    for f in ("hits", "lookups", "pos"):
+        assert g[f].tolist() == gold[f], f
+    assert abs(g["acc_len"] - gold["acc_len"]) < 1e-12
 
 
 # ------------------------------------------------------------------ replay --
@@ -546,6 +590,34 @@ def test_accept_ignores_rows_past_the_node_count(m):
     for f in ("accept_len", "accept_tok", "last_node"):
         assert (host(got[f]) == want[f]).all(), f
     assert (want["last_node"] < np.maximum(nn, 1)).all()
+
+
+@pytest.mark.parametrize("extra", [0, 1, 5])
+def test_accept_on_trees_deeper_than_m(extra):
+    """Chains of depth m + extra (a built tree is at most m deep) whose
+    targets follow them: the walk stops at m + 1 accepted tokens on both
+    sides and nothing is written past accept_tok's m + 1 entries."""
+    m, R = 4, 16
+    depth = m + extra
+    B = 3
+    nn = np.full(B, depth + 1, np.int32)
+    tok = np.zeros((B, R), np.int32)
+    par = np.full((B, R), -1, np.int32)
+    pos = np.zeros((B, R), np.int32)
+    tok[:, :depth + 1] = np.arange(10, 11 + depth)
+    par[:, 1:depth + 1] = np.arange(depth)
+    pos[:, :depth + 1] = np.arange(depth + 1)
+    tgt = np.full((B, R), -1, np.int32)
+    tgt[:, :depth] = np.arange(11, 11 + depth)
+    tgt[:, depth] = 99
+    tgt[1, 2] = 5  # the second tree stops at depth 2
+    tree = {"num_nodes": dev(nn), "node_tok": dev(tok), "parent": dev(par), "pos_ids": dev(pos)}
+    got = fc.fc_verify_accept(tree, dev(tgt), m=m)
+    torch.cuda.synchronize()
+    want = oracle.verify_accept(dict(num_nodes=nn, node_tok=tok, parent=par, pos_ids=pos), tgt, m=m)
+    for f in ("accept_len", "accept_tok", "last_node"):
+        assert (host(got[f]) == want[f]).all(), f
+    assert want["accept_len"].tolist() == [min(depth + 1, m + 1), 3, min(depth + 1, m + 1)]
 
 
 def test_unsorted_slots_are_flagged():

@@ -1,13 +1,13 @@
-"""Host-side logic of the product path, checked on the CPU against the
-oracle's independent implementation."""
+"""Host-side logic of the tests' host-driven replay, checked on the CPU
+against the oracle's independent implementation."""
 import random
 
 import oracle
-from paper_2502_17139_amd.replay import _Sequences
+from host_replay import _Sequences
 
 
 def test_replay_cache_text_matches_oracle_cache():
-    """The GPU replay's CACHE bookkeeping (a flat text with separators and
+    """The host-driven replay's CACHE bookkeeping (a flat text with separators and
     oldest-first eviction) gives the oracle CACHE's text after every add."""
     rng = random.Random(5)
     for _ in range(300):

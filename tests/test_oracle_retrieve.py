@@ -18,7 +18,12 @@ def _ctx_from(text, rng, L=16, fresh_prob=0.3, vocab=4):
 
 
 def _compare(texts, ctx, n_max, n_min, k, m):
-    got = oracle.retrieve(texts, ctx, n_max=n_max, n_min=n_min, k=k, m=m)
+    for batched in (False, True):
+        _compare_one(oracle.retrieve(texts, ctx, n_max=n_max, n_min=n_min, k=k, m=m, batched=batched),
+                     texts, ctx, n_max, n_min, k, m)
+
+
+def _compare_one(got, texts, ctx, n_max, n_min, k, m):
     for b in range(ctx.shape[0]):
         want = brute.retrieve(texts, ctx[b], n_max, n_min, k, m)
         for f in ("match_n", "range_lo", "range_cnt", "taken"):
@@ -136,8 +141,9 @@ def test_example_a(golden):
     t = np.array(g["text"], np.uint16)
     ctx = np.array([g["ctx"]], np.uint16)
     p = g["params"]
-    for k, key in ((2, "retrieve_k2"), (3, "retrieve_k3")):
-        r = oracle.retrieve([t], ctx, n_max=p["n_max"], n_min=p["n_min"], k=k, m=p["m"])
+    for k, key, batched in ((2, "retrieve_k2", False), (3, "retrieve_k3", False), (2, "retrieve_k2", True),
+                            (3, "retrieve_k3", True)):
+        r = oracle.retrieve([t], ctx, n_max=p["n_max"], n_min=p["n_min"], k=k, m=p["m"], batched=batched)
         w = g[key]
         assert r["match_n"][0, 0] == w["match_n"]
         assert r["range_lo"][0, 0] == w["range_lo"]
@@ -151,7 +157,52 @@ def test_example_a(golden):
 def test_example_b(golden):
     g = golden("example_b.json")
     p = g["params"]
-    r = oracle.retrieve([np.array(g["project"], np.uint16), np.array(g["general"], np.uint16)],
-                        np.array([g["ctx"]], np.uint16), n_max=p["n_max"], n_min=p["n_min"], k=p["k"], m=p["m"])
-    for f, v in g["retrieve"].items():
-        assert r[f][0].tolist() == v, f
+    for batched in (False, True):
+        r = oracle.retrieve([np.array(g["project"], np.uint16), np.array(g["general"], np.uint16)],
+                            np.array([g["ctx"]], np.uint16), n_max=p["n_max"], n_min=p["n_min"], k=p["k"], m=p["m"],
+                            batched=batched)
+        for f, v in g["retrieve"].items():
+            assert r[f][0].tolist() == v, f
+
+
+def _same(a: dict, b: dict) -> None:
+    for f in a:
+        assert a[f].shape == b[f].shape and (a[f] == b[f]).all(), f
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_batched_equals_definition(seed):
+    """The batch-shared scans give the per-query definition's answer on
+    every field, padding included: one to four stores (one empty), small
+    vocabularies (long repeats, many queries sharing a last or first
+    token), contexts with separators, of length 1..16, n_min 1..3 and
+    budgets below, at and above the counts."""
+    rng = np.random.default_rng(700 + seed)
+    vocab = [2, 3, 5, 16, 300, 32256][seed]
+    S = 1 + seed % 4
+    texts = [synth.random_text(40 * seed + s, int(rng.integers(0, 3000)) if s != 1 else 0, vocab,
+                               sep_prob=0.02 * (s % 2)) for s in range(S)]
+    for L, n_min in ((16, 2), (5, 1), (1, 1), (3, 3)):
+        rows = []
+        for _ in range(40):
+            src = texts[int(rng.integers(0, S))]
+            rows.append(_ctx_from(src, rng, L=L, fresh_prob=0.3, vocab=vocab))
+        ctx = np.stack(rows)
+        if L > 1:
+            ctx[::7, -2] = 0
+        ctx[::11, -1] = 0
+        for k, m in ((1, 1), (7, 3), (64, 10), (5000, 16)):
+            want = oracle.retrieve(texts, ctx, n_max=min(16, max(L, n_min)), n_min=n_min, k=k, m=m)
+            got = oracle.retrieve(texts, ctx, n_max=min(16, max(L, n_min)), n_min=n_min, k=k, m=m, batched=True)
+            _same(want, got)
+
+
+def test_batched_equals_definition_on_workload():
+    """The 1M-token store and its 64 queries, and the 2M project store with
+    the first 96 queries of the two-store batch: both forms agree."""
+    t = synth.store(1, "single")
+    ctx = synth.queries(1)
+    _same(oracle.retrieve([t], ctx), oracle.retrieve([t], ctx, batched=True))
+    tp = synth.store(2, "project")
+    ctx = synth.queries(2, count=96)
+    _same(oracle.retrieve([tp, t], ctx), oracle.retrieve([tp, t], ctx, batched=True))

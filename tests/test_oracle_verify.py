@@ -68,3 +68,25 @@ def test_root_only_and_exhausted_truth():
     assert got["accept_len"][0] == 1 and got["accept_tok"][0].tolist() == [9, -1, -1]
     got = oracle.verify_accept(tr, np.array([[-1, -1, -1]], np.int32), m=2)
     assert got["accept_len"][0] == 0 and got["last_node"][0] == 0
+
+
+@pytest.mark.parametrize("extra", [0, 1, 3])
+def test_tree_deeper_than_m_stops_at_m_plus_one(extra):
+    """A chain of depth m + extra whose every edge matches: the walk takes
+    m + 1 tokens at most and writes nothing past accept_tok's m + 1 slots
+    (a chain of depth m, extra = 0, is the deepest a built tree can be)."""
+    m = 4
+    depth = m + extra
+    R = depth + 1
+    tr = dict(num_nodes=np.array([R, R]), node_tok=np.tile(np.arange(10, 10 + R, dtype=np.int32), (2, 1)),
+              parent=np.tile(np.arange(-1, R - 1, dtype=np.int32), (2, 1)),
+              pos_ids=np.tile(np.arange(R, dtype=np.int32), (2, 1)))
+    target = np.tile(np.concatenate([np.arange(11, 10 + R, dtype=np.int32), [99]]), (2, 1))
+    got = oracle.verify_accept(tr, target, m=m)
+    want_path = min(depth, m + 1)
+    want_len = min(depth + 1, m + 1)
+    assert (got["accept_len"] == want_len).all()
+    assert (got["last_node"] == want_path).all()
+    toks = list(range(11, 11 + want_path)) + ([99] if depth < m + 1 else [])
+    assert got["accept_tok"][0, :want_len].tolist() == toks[:want_len]
+    assert (got["accept_tok"][:, want_len:] == -1).all()
