@@ -278,6 +278,26 @@ fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16_t* ctx, in
                       int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len, uint16_t* cont_tok,
                       const int32_t* rows, int32_t n_rows, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * fc_retrieve without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, outputs and checks as fc_retrieve;
+ * the workspace is a static device array of FC_RETRIEVE_NOALLOC_BYTES that
+ * the library holds on every GPU it runs on until the process ends.  The
+ * call allocates nothing.  Limit: fc_retrieve_workspace_bytes(B, S, p) must
+ * not exceed FC_RETRIEVE_NOALLOC_BYTES (FC_ERR_UNSUPPORTED otherwise, before
+ * anything touches the device).  Every call on one GPU uses that GPU's one
+ * array, so calls that overlap on the same GPU (different streams or host
+ * threads) race and must be serialised by the caller.  The first call on a
+ * device looks the array's address up (FC_ERR_DEVICE if that fails).
+ */
+#define FC_RETRIEVE_NOALLOC_BYTES (1u << 20)
+size_t fc_retrieve_noalloc_max_bytes(void);
+fc_status fc_retrieve_noalloc(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
+                              fc_retrieve_params p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
+                              int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len,
+                              uint16_t* cont_tok, const int32_t* rows, int32_t n_rows, hipStream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* CACHE (Section IV-B)                                                      */
 /* ------------------------------------------------------------------------ */

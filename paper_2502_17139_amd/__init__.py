@@ -37,7 +37,7 @@ EXPORTS = (
     "fc_pair_table_entries", "fc_store_prepare_pairs", "fc_record_bytes", "fc_store_prepare_records",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
     "fc_verify_accept", "fc_targets_from_truth", "fc_cache_lds_bytes", "fc_cache_retrieve", "fc_cache_write",
-    "fc_tree_attention", "fc_replay_init", "fc_replay_run",
+    "fc_tree_attention", "fc_replay_init", "fc_replay_run", "fc_retrieve_noalloc_max_bytes", "fc_retrieve_noalloc",
     "fc_datastore_build_stats",
 )
 
@@ -139,6 +139,11 @@ def lib() -> ctypes.CDLL:
     L.fc_retrieve.restype = ctypes.c_int
     L.fc_retrieve.argtypes = [ctypes.POINTER(FcStore), i32, vp, i32, i32, FcRetrieveParams,
                               vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]
+    L.fc_retrieve_noalloc_max_bytes.restype = sz
+    L.fc_retrieve_noalloc_max_bytes.argtypes = []
+    L.fc_retrieve_noalloc.restype = ctypes.c_int
+    L.fc_retrieve_noalloc.argtypes = [ctypes.POINTER(FcStore), i32, vp, i32, i32, FcRetrieveParams,
+                                      vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp]
     L.fc_cache_lds_bytes.restype = sz
     L.fc_cache_lds_bytes.argtypes = [ctypes.c_int64]
     L.fc_cache_retrieve.restype = ctypes.c_int
@@ -422,6 +427,34 @@ def fc_retrieve(stores, ctx: torch.Tensor, n_max: int = 16, n_min: int = 2, k: i
     _check("fc_retrieve", lib().fc_retrieve(
         views, S, _ptr(ctx), B, L, p, *[_ptr(out[f]) for f in RETRIEVE_FIELDS], _ptr(rows), n_rows,
         _ptr(workspace), 0 if workspace is None else workspace.numel(), _stream(stream)))
+    return out
+
+
+def fc_retrieve_noalloc_max_bytes() -> int:
+    return int(lib().fc_retrieve_noalloc_max_bytes())
+
+
+def fc_retrieve_noalloc(stores, ctx: torch.Tensor, n_max: int = 16, n_min: int = 2, k: int = 5000, m: int = 10,
+                        out: dict | None = None, rows: torch.Tensor | None = None, stream=None) -> dict:
+    """fc_retrieve with the library's static per-GPU workspace (no workspace
+    argument; the call allocates nothing when `out` is given).  Calls that
+    overlap on one GPU share that workspace and race."""
+    if ctx.dtype != torch.uint16 or ctx.dim() != 2:
+        raise ValueError("ctx must be a 2-D uint16 tensor")
+    B, L = ctx.shape
+    S = len(stores)
+    views = (FcStore * max(S, 1))(*[s.view() for s in stores])
+    p = FcRetrieveParams(n_max, n_min, k, m)
+    if out is None:
+        out = retrieve_outputs(B, S, k, m, ctx.device)
+    n_rows = out["taken"].shape[0] if "taken" in out else B
+    if rows is None and n_rows != B:
+        raise ValueError("without a row map the outputs need one row per query")
+    _expect_outputs(out, RETRIEVE_FIELDS, _retrieve_shapes(n_rows, S, k, m), _RETRIEVE_DTYPES)
+    _expect("rows", rows, torch.int32, (B,), optional=True)
+    _check("fc_retrieve_noalloc", lib().fc_retrieve_noalloc(
+        views, S, _ptr(ctx), B, L, p, *[_ptr(out[f]) for f in RETRIEVE_FIELDS], _ptr(rows), n_rows,
+        _stream(stream)))
     return out
 
 

@@ -26,6 +26,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "fastcoder.h"
 #include "fc_device.h"
 #include "fc_host.h"
@@ -520,7 +522,7 @@ extern "C" size_t fc_retrieve_workspace_bytes(int32_t B, int32_t S, fc_retrieve_
 
 namespace {
 
-// Host-side checks of fc_retrieve; fills the
+// Host-side checks shared by fc_retrieve and fc_retrieve_noalloc; fills the
 // kernels' store arguments.  Nothing touches the device.
 fc_status retrieve_check(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B, int32_t L,
                          const fc_retrieve_params& p, int32_t* match_n, uint32_t* range_lo, uint32_t* range_cnt,
@@ -601,6 +603,61 @@ extern "C" fc_status fc_retrieve(const fc_store* stores, int32_t S, const uint16
                                      cont_src, cont_len, cont_tok, rows, n_rows, st);
   if (e != FC_OK || B == 0) return e;
   if (!ws || ws_bytes < fc_retrieve_workspace_bytes(B, S, p)) return FC_ERR_WORKSPACE;
+  return retrieve_launch(st, S, ctx, B, L, p, match_n, range_lo, range_cnt, taken, cont_pos, cont_src, cont_len,
+                         cont_tok, rows, n_rows, ws, stream);
+}
+
+// ---------------------------------------------------------------------------
+// fc_retrieve_noalloc: fc_retrieve with its workspace in a static device
+// array instead of a caller buffer, for callers that cannot allocate.  Each
+// GPU holds its own copy of the array for the life of the process; its
+// device address is looked up once per device (hipGetSymbolAddress, with
+// that device current) and only that address is ever passed to kernels.
+// Calls on one GPU share the array, so calls that overlap on one GPU race.
+namespace {
+
+constexpr size_t kNoAllocBytes = FC_RETRIEVE_NOALLOC_BYTES;
+static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// The device address of the current GPU's scratch array, or null on failure.
+void* device_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" size_t fc_retrieve_noalloc_max_bytes(void) { return kNoAllocBytes; }
+
+extern "C" fc_status fc_retrieve_noalloc(const fc_store* stores, int32_t S, const uint16_t* ctx, int32_t B,
+                                         int32_t L, fc_retrieve_params p, int32_t* match_n, uint32_t* range_lo,
+                                         uint32_t* range_cnt, int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src,
+                                         uint8_t* cont_len, uint16_t* cont_tok, const int32_t* rows, int32_t n_rows,
+                                         hipStream_t stream) {
+  StoreArgs st;
+  const fc_status e = retrieve_check(stores, S, ctx, B, L, p, match_n, range_lo, range_cnt, taken, cont_pos,
+                                     cont_src, cont_len, cont_tok, rows, n_rows, st);
+  if (e != FC_OK || B == 0) return e;
+  if (fc_retrieve_workspace_bytes(B, S, p) > kNoAllocBytes) return FC_ERR_UNSUPPORTED;
+  void* ws = device_scratch();
+  if (!ws) return FC_ERR_DEVICE;
   return retrieve_launch(st, S, ctx, B, L, p, match_n, range_lo, range_cnt, taken, cont_pos, cont_src, cont_len,
                          cont_tok, rows, n_rows, ws, stream);
 }

@@ -70,6 +70,23 @@ def test_retrieve_rejects_batches_past_31_bit_slots(L):
     assert L.fc_retrieve(*_retrieve_args(B=430_000)) == 4
 
 
+def _noalloc_args(**change):
+    a = _retrieve_args(**change)
+    return a[:-3] + [a[-1]]  # fc_retrieve's arguments without the workspace pointer and size
+
+
+def test_retrieve_noalloc_rejects_on_the_host(L):
+    """The no-allocation retrieval takes fc_retrieve's checks, and refuses a
+    batch whose workspace exceeds its static array, before any device call."""
+    assert L.fc_retrieve_noalloc_max_bytes() == 1 << 20
+    for change, code in ((dict(S=0), 1), (dict(B=-1), 1), (dict(L_=0), 1), (dict(p=(4, 2, 10, 256)), 1),
+                         (dict(B=430_000), 4)):
+        assert L.fc_retrieve_noalloc(*_noalloc_args(**change)) == code
+    # 4 * (B + 1) bytes of offsets: 262,143 queries fit in 1 MiB, 262,144 do not
+    assert L.fc_retrieve_noalloc(*_noalloc_args(B=262_144, p=(16, 2, 8, 10))) == 4
+    assert L.fc_retrieve_noalloc(*_noalloc_args(B=0)) == 0  # nothing to do, no device call
+
+
 def test_retrieve_rejects_missing_workspace(L):
     assert L.fc_retrieve(*_retrieve_args(ws_bytes=0)) == 2
     args = _retrieve_args(ws_bytes=4)  # 4*(B+1) = 8 needed
