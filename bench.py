@@ -32,7 +32,7 @@ import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "replay-cache": 3, "replay-control": 3,
-             "build": 3, "build-repos": 0, "extend": 3, "copy": 0, "tree-attention": 1}
+             "build": 3, "build-repos": 0, "extend": 3, "copy": 0, "tree-attention": 1, "gather-probe": 0}
 # kernels each entry point launches (rocprofv3 kernel names start with these)
 ENTRY_KERNELS = {
     "fc_retrieve": ("k_search", "k_offsets", "k_gather"),
@@ -40,6 +40,7 @@ ENTRY_KERNELS = {
     "fc_verify_accept": ("k_verify",),
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_headline_10M_1B.txt")
+BUILD_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sa_build_1B_10M.txt")
 
 
 def kernel_source_hash() -> str:
@@ -58,12 +59,12 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic() -> dict:
-    """HBM bytes per launch of each entry point from the committed counter
-    summary (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy's readings),
-    or {} when it is missing or was taken on other kernel sources."""
+def measured_traffic(path: str) -> dict:
+    """HBM bytes per launch from a committed counter summary (FETCH_SIZE and
+    WRITE_SIZE, scaled by a plain copy's readings), or {} when it is missing
+    or was taken on other kernel sources."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             lines = f.read().splitlines()
     except OSError:
         return {}
@@ -81,14 +82,17 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(taken, cont_len, match_n, ctx_nhi, store_sizes, k, m, c, n_min):
+def algorithmic_bytes(taken, cont_len, match_n, ctx_nhi, store_sizes, k, m, c, n_min, L=16):
     """Bytes the method must move per launch, from the batch's own outputs.
 
-    search (per query, per store): for every suffix length tried, n_hi down
-    to the match (or n_min): one bucket read (8 B) and two binary searches of
-    ceil(log2(bucket size + 1)) probes, each probe a 4-byte suffix-array entry
-    plus up to 2n bytes of text; bucket sizes are taken as n_s / 32256.
-    Plus the context row (32 B) and the four per-store outputs (16 B).
+    search (per query, per store, for every suffix length tried - n_hi down
+    to the match, or down to n_min when nothing matches): two binary
+    searches over the whole suffix array, ceil(log2(N_s + 1)) probes each, a
+    probe being a 4-byte suffix-array entry plus up to 2n bytes of text.
+    `search_bucketed` is the same with the first-token bucket narrowing each
+    search first (8 bytes of table, ranges of N_s / 32256).
+    io (per query): the context (2L) read, the four per-store fields (16 per
+    store) written.
     gather (per kept slot): 4-byte suffix-array entry + 2*len text bytes
     read; 4 + 1 + 1 + 2*m bytes written.
     tree (per query): taken (4*S) + cont_len (1 per kept slot) + cont_tok
@@ -99,22 +103,26 @@ def algorithmic_bytes(taken, cont_len, match_n, ctx_nhi, store_sizes, k, m, c, n
     """
     B, S = taken.shape
     R = c + 1
-    search = 0.0
-    for b in range(B):
-        search += 32
-        for s in range(S):
-            lo_n = match_n[b, s] if match_n[b, s] > 0 else n_min
-            probes = int(np.ceil(np.log2(store_sizes[s] / 32256.0 + 1)))
-            for n in range(int(ctx_nhi[b]), int(lo_n) - 1, -1):
-                search += 8 + 2 * probes * (4 + 2 * n)
-            search += 16
+    search = search_b = 0.0
+    for s in range(S):
+        full = int(np.ceil(np.log2(store_sizes[s] + 1.0)))
+        buck = int(np.ceil(np.log2(store_sizes[s] / 32256.0 + 1)))
+        lo = np.where(match_n[:, s] > 0, match_n[:, s], n_min).astype(np.int64)
+        hi = ctx_nhi.astype(np.int64)
+        for n in range(n_min, 17):
+            tried = (hi >= n) & (lo <= n)
+            cnt = int(tried.sum())
+            search += cnt * 2 * full * (4 + 2 * n)
+            search_b += cnt * (8 + 2 * buck * (4 + 2 * n))
+    io = B * (2 * L + 16 * S)
     used = taken.sum(axis=1)
     kept = int(used.sum())
     lens = sum(int(cont_len[b, :used[b]].astype(np.int64).sum()) for b in range(B))
     gather = kept * (4 + 4 + 1 + 1 + 2 * m) + 2 * lens
     tree = B * (4 * S + 2) + kept * (1 + 2 * m) + B * (4 + 16 * R + 4 * R * R)
     verify = B * (4 + 12 * R + 4 + 4 * (m + 1) + 4)
-    return dict(search=search, gather=float(gather), tree=float(tree), verify=float(verify))
+    return dict(search=float(search), search_bucketed=float(search_b), io=float(io), gather=float(gather),
+                tree=float(tree), verify=float(verify), kept=kept)
 
 
 def n_hi_of(ctx: np.ndarray, n_max: int) -> np.ndarray:
@@ -125,28 +133,6 @@ def n_hi_of(ctx: np.ndarray, n_max: int) -> np.ndarray:
             t += 1
         out[b] = min(n_max, ctx.shape[1], t)
     return out
-
-
-def cpu_baseline(texts, ctx, nxt, p, alpha, c, budget_s):
-    """The oracle (test infrastructure) on a bounded sample of the batch."""
-    import oracle
-    B = ctx.shape[0]
-    n = 4
-    done, spent = 0, 0.0
-    while done < B:
-        q = min(n, B - done)
-        rows = slice(done, done + q)
-        t0 = time.perf_counter()
-        r = oracle.retrieve(texts, ctx[rows], n_max=p["n_max"], n_min=p["n_min"], k=p["k"], m=p["m"])
-        t = oracle.build_tree(r["taken"], r["cont_len"], r["cont_tok"], ctx[rows], c=c, alpha=alpha)
-        tgt = targets_for(t["pos_ids"], t["num_nodes"], nxt[rows])
-        oracle.verify_accept(t, tgt, m=p["m"])
-        spent += time.perf_counter() - t0
-        done += q
-        if spent >= budget_s:
-            break
-        n = min(2 * n, 64)
-    return done, spent
 
 
 def targets_for(pos_ids, num_nodes, nxt):
@@ -162,27 +148,239 @@ def targets_for(pos_ids, num_nodes, nxt):
     return out
 
 
+def host_info() -> dict:
+    """Cores this process may use, the oracle's thread count and the CPU model."""
+    import oracle
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"affinity_cores": len(os.sched_getaffinity(0)), "nproc": os.cpu_count(),
+            "oracle_threads": oracle.max_threads(), "cpu_model": model}
+
+
+def oracle_batch(texts, ctx, nxt, p, alpha, c):
+    """The oracle (test infrastructure) on a whole batch: retrieval (its
+    batched form), tree and acceptance; returns seconds."""
+    import oracle
+    t0 = time.perf_counter()
+    r = oracle.retrieve(texts, ctx, n_max=p["n_max"], n_min=p["n_min"], k=p["k"], m=p["m"], batched=True)
+    t = oracle.build_tree(r["taken"], r["cont_len"], r["cont_tok"], ctx, c=c, alpha=alpha)
+    oracle.verify_accept(t, targets_for(t["pos_ids"], t["num_nodes"], nxt), m=p["m"])
+    return time.perf_counter() - t0
+
+
+class Batch:
+    """One query batch resident on the GPU with its own output buffers."""
+
+    def __init__(self, fc, torch, dev, ctx_np, nxt_np, S, p, c):
+        B = ctx_np.shape[0]
+        self.B, self.ctx_np, self.nxt_np = B, ctx_np, nxt_np
+        self.ctx = torch.from_numpy(ctx_np).to(dev)
+        self.rout = fc.retrieve_outputs(B, S, p["k"], p["m"], dev)
+        self.tout = fc.tree_outputs(B, c, dev)
+        self.aout = fc.accept_outputs(B, p["m"], dev)
+        self.target = None
+
+
+def make_pipeline(fc, torch, dev, stores, p, alpha, c, Bmax):
+    rws = torch.empty(max(fc.fc_retrieve_workspace_bytes(Bmax, len(stores), p["n_max"], p["n_min"], p["k"], p["m"]),
+                          1), dtype=torch.uint8, device=dev)
+    tws = torch.empty(max(fc.fc_build_tree_workspace_bytes(Bmax), 1), dtype=torch.uint8, device=dev)
+
+    def retrieve(bt):
+        fc.fc_retrieve(stores, bt.ctx, n_max=p["n_max"], n_min=p["n_min"], k=p["k"], m=p["m"], out=bt.rout,
+                       workspace=rws)
+
+    def tree(bt):
+        fc.fc_build_tree(bt.rout["taken"], bt.rout["cont_len"], bt.rout["cont_tok"], bt.ctx, c=c, alpha=alpha,
+                         out=bt.tout, workspace=tws)
+
+    def verify(bt):
+        fc.fc_verify_accept(bt.tout, bt.target, m=p["m"], out=bt.aout)
+
+    return retrieve, tree, verify
+
+
+def prepare_targets(torch, dev, batches, retrieve, tree):
+    """First pass over every batch: its tree fixes the target tokens (the
+    target model's outputs: the true tokens after each row's path)."""
+    for bt in batches:
+        retrieve(bt)
+        tree(bt)
+    torch.cuda.synchronize()
+    for bt in batches:
+        tgt = targets_for(bt.tout["pos_ids"].cpu().numpy(), bt.tout["num_nodes"].cpu().numpy(), bt.nxt_np)
+        bt.target = torch.from_numpy(tgt).to(dev)
+
+
+def timed_steps(torch, stream, K, order, batches, fns):
+    """K steps back to back, step i on batches[order(i)]; one event pair."""
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(K):
+        bt = batches[order(i)]
+        for f in fns:
+            f(bt)
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end)
+
+
+def timed_phases(torch, stream, K, order, batches, fns):
+    """K steps with an event at every entry-point boundary; per-entry lists
+    of milliseconds per launch."""
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(K)]
+    torch.cuda.synchronize()
+    for i in range(K):
+        bt = batches[order(i)]
+        ev[i][0].record(stream)
+        for j, f in enumerate(fns):
+            f(bt)
+            ev[i][j + 1].record(stream)
+    torch.cuda.synchronize()
+    return [[ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)] for j in range(len(fns))]
+
+
+def small_config(args, cfg, fc, torch, synth, dev, p, c, with_oracle, retrieve_bytes=False):
+    """One of the smaller configurations (1M single store, 2M + 100M): the
+    whole step (retrieve + tree + accept) timed over K steps of its batch,
+    and the oracle on the same batch."""
+    roles = synth.store_roles(cfg)
+    alpha = tuple(p["alpha"])[:len(roles)]
+    texts = [synth.store(cfg, r) for r in roles]
+    ctx_np, nxt_np = synth.queries(cfg, next_tokens=p["m"] + 1)
+    stores = [fc.Store(torch.from_numpy(t).to(dev), pair_vocab=synth.VOCAB, records=True) for t in texts]
+    bt = Batch(fc, torch, dev, ctx_np, nxt_np, len(stores), p, c)
+    retrieve, tree, verify = make_pipeline(fc, torch, dev, stores, p, alpha, c, bt.B)
+    prepare_targets(torch, dev, [bt], retrieve, tree)
+    stream = torch.cuda.current_stream()
+    K = max(args.steps, 10)
+    for _ in range(args.warmup):
+        retrieve(bt), tree(bt), verify(bt)
+    ms = timed_steps(torch, stream, K, lambda i: 0, [bt], (retrieve, tree, verify))
+    ph = timed_phases(torch, stream, K, lambda i: 0, [bt], (retrieve, tree, verify))
+    out = {"workload": synth.WORKLOADS[cfg]["name"], "stores_tokens": [len(t) for t in texts], "batch": bt.B,
+           "retrievals_per_s": bt.B * K / (ms * 1e-3), "ms_per_step": ms / K,
+           "phases_ms_mean": {n: float(np.mean(v)) for n, v in zip(("fc_retrieve", "fc_build_tree",
+                                                                    "fc_verify_accept"), ph)},
+           "accept_len_mean": float(bt.aout["accept_len"].float().mean().item())}
+    if retrieve_bytes:
+        nb = algorithmic_bytes(bt.rout["taken"].cpu().numpy(), bt.rout["cont_len"].cpu().numpy(),
+                               bt.rout["match_n"].cpu().numpy(), n_hi_of(ctx_np, p["n_max"]), [len(t) for t in texts],
+                               p["k"], p["m"], c, p["n_min"])
+        rb = nb["search"] + nb["io"] + nb["gather"]
+        out["fc_retrieve_algorithmic_GBps"] = rb / (np.mean(ph[0]) * 1e-3) / 1e9
+        out["fc_retrieve_frac"] = out["fc_retrieve_algorithmic_GBps"] / HBM_PEAK_GBS
+    if with_oracle:
+        sec = oracle_batch(texts, ctx_np, nxt_np, p, alpha, c)
+        out["oracle"] = {"retrievals_per_s": bt.B / sec, "seconds": sec, "sample": f"the whole batch ({bt.B} queries)"}
+    del stores, bt
+    torch.cuda.empty_cache()
+    return out
+
+
+def replay_config(args, fc, torch, synth, dev, stores, texts, p, with_oracle):
+    """Decode-trace replay on the headline stores: 128 streams of 4,096
+    tokens, 512 steps, LRU of 32, on the device engine."""
+    truth = synth.truth()
+    eng = fc.ReplayEngine(stores, torch.from_numpy(truth).to(dev), max_steps=512, **p)
+    eng.run(limit=max(args.warmup, 1))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    res = eng.run(limit=512)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    live = res["accept"] >= 0
+    out = {"workload": "decode-trace replay, 128 streams x 4096 tokens over project 10M + general 1B, LRU 32",
+           "steps": res["steps"], "steps_per_s": res["steps"] / wall, "ms_per_step": 1e3 * wall / res["steps"],
+           "accepted_tokens_per_s": float(res["accept"][live].sum()) / wall, "acc_len": res["acc_len"],
+           "lru_hit_rate": float(res["hits"].sum() / max(res["lookups"].sum(), 1))}
+    if with_oracle:
+        import oracle
+        n = 4
+        t0 = time.perf_counter()
+        o = oracle.replay(texts, truth, **p, max_steps=n)
+        sec = time.perf_counter() - t0
+        out["oracle"] = {"steps_per_s": n / sec, "seconds": sec,
+                         "sample": f"the first {n} steps of all 128 streams (batched retrieval per step)",
+                         "acc_len_first_steps": o["acc_len"]}
+    return out
+
+
+def build_config(args, fc, torch, synth, dev, texts_by_role, with_oracle):
+    """Suffix-array builds of the 1B-token general store and the 10M-token
+    project store: seconds, doubling rounds, suffixes still tied after each
+    round, the longest common prefix bracket, and the floor bandwidth of any
+    build (read 2n, write 4n bytes)."""
+    out = {}
+    traffic = measured_traffic(BUILD_TRAFFIC_FILE)
+    for role in ("project", "general"):
+        t = texts_by_role[role]
+        n = len(t)
+        tok = torch.from_numpy(t).to(dev)
+        sa = torch.empty(n, dtype=torch.uint32, device=dev)
+        ws = torch.empty(fc.fc_datastore_build_workspace_bytes(n), dtype=torch.uint8, device=dev)
+        times, stats = [], None
+        for i in range(3):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            _, stats = fc.fc_datastore_build_stats(tok, sa_out=sa, workspace=ws)
+            torch.cuda.synchronize()
+            if i:
+                times.append(time.perf_counter() - t0)
+        sec = float(np.median(times))
+        pl = stats["prefix_len"]
+        rec = {"tokens": n, "seconds": sec, "floor_GBps": 6 * n / sec / 1e9, "rounds": stats["rounds"],
+               "sort_passes": stats["sort_passes"], "prefix_len": pl, "sorted_per_round": stats["sorted"],
+               "unresolved_per_round": stats["unresolved"],
+               "max_lcp": {"at_least": int(pl[-2]) if len(pl) > 1 else 0, "below": int(pl[-1])}}
+        tb = traffic.get(role)
+        rec["counter_bytes"] = tb
+        rec["counter_GBps"] = None if tb is None else tb / sec / 1e9
+        out[role] = rec
+        del ws, sa, tok
+        torch.cuda.empty_cache()
+    if with_oracle:
+        import oracle
+        t = texts_by_role["project"]
+        t0 = time.perf_counter()
+        oracle.suffix_array(t)
+        sec = time.perf_counter() - t0
+        n1 = len(texts_by_role["general"])
+        n0 = len(t)
+        out["oracle"] = {"project_seconds": sec, "threads": 1, "kind": "naive comparison sort",
+                         "general_seconds_extrapolated": sec * (n1 * np.log2(n1)) / (n0 * np.log2(n0)),
+                         "general_note": "not run: extrapolated from the 10M-token sort by n log n"}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="headline")
-    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--rotations", type=int, default=8, help="distinct query batches cycled by the timed steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the single-query latency runs (profiles then hold batch dispatches only)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="headline only: skip the other configurations' sub-records")
     args = ap.parse_args()
     # No garbage-collector pauses inside timed regions: a pause stalls the
     # host while the GPU drains its queue, and the stall would be timed.
     gc.disable()
     if args.gpus != 1:
-        print(json.dumps({"error": "single-GPU path only (no sharded stores); --gpus must be 1", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "this build runs on one GPU (no sharded stores or collectives); "
+                                   "--gpus must be 1", "n_gpus": args.gpus}))
         sys.exit(2)
-
-    import torch
-    import paper_2502_17139_amd as fc
-    import synth
 
     if args.workload in ("replay", "replay-cache", "replay-control"):
         return run_replay(args, cache=args.workload != "replay", control=args.workload == "replay-control")
@@ -196,6 +394,16 @@ def main():
         return run_tree_attention(args)
     if args.workload == "copy":
         return run_copy(args)
+    if args.workload == "gather-probe":
+        return run_gather_probe(args)
+    return run_headline(args)
+
+
+def run_headline(args):
+    import torch
+    import paper_2502_17139_amd as fc
+    import synth
+
     cfg = WORKLOADS[args.workload]
     p = dict(synth.PARAMS)
     c, alpha = p["c"], tuple(p["alpha"])
@@ -203,11 +411,14 @@ def main():
     alpha = alpha[:len(roles)]
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    k, m = p["k"], p["m"]
 
     t0 = time.perf_counter()
     texts = [synth.store(cfg, r) for r in roles]
-    ctx_np, nxt_np = synth.queries(cfg, next_tokens=p["m"] + 1)
-    log(f"generated stores {[len(t) for t in texts]} and {ctx_np.shape[0]} queries in {time.perf_counter() - t0:.1f}s")
+    R = max(args.rotations, 1)
+    qs = [synth.queries(cfg, next_tokens=m + 1, rotation=r) for r in range(R)]
+    log(f"generated stores {[len(t) for t in texts]} and {R} batches of {qs[0][0].shape[0]} queries "
+        f"in {time.perf_counter() - t0:.1f}s")
 
     stream = torch.cuda.current_stream()
     stores, build_s = [], []
@@ -221,122 +432,112 @@ def main():
         stores.append(st)
     log(f"suffix arrays + tables built in {[round(x, 3) for x in build_s]} s")
 
-    B = ctx_np.shape[0]
-    k, m = p["k"], p["m"]
-    ctx = torch.from_numpy(ctx_np).to(dev)
-    rout = fc.retrieve_outputs(B, len(stores), k, m, dev)
-    rws = torch.empty(max(fc.fc_retrieve_workspace_bytes(B, len(stores), p["n_max"], p["n_min"], k, m), 1),
-                      dtype=torch.uint8, device=dev)
-    tout = fc.tree_outputs(B, c, dev)
-    tws = torch.empty(max(fc.fc_build_tree_workspace_bytes(B), 1), dtype=torch.uint8, device=dev)
-    aout = fc.accept_outputs(B, m, dev)
-
-    def retrieve():
-        fc.fc_retrieve(stores, ctx, n_max=p["n_max"], n_min=p["n_min"], k=k, m=m, out=rout, workspace=rws)
-
-    def tree():
-        fc.fc_build_tree(rout["taken"], rout["cont_len"], rout["cont_tok"], ctx, c=c, alpha=alpha, out=tout,
-                         workspace=tws)
-
-    # first pass: its tree fixes the target tokens (the target model's outputs)
-    retrieve()
-    tree()
-    torch.cuda.synchronize()
-    tgt_np = targets_for(tout["pos_ids"].cpu().numpy(), tout["num_nodes"].cpu().numpy(), nxt_np)
-    target = torch.from_numpy(tgt_np).to(dev)
-
-    def verify():
-        fc.fc_verify_accept(tout, target, m=m, out=aout)
-
-    for _ in range(args.warmup):
-        retrieve()
-        tree()
-        verify()
+    batches = [Batch(fc, torch, dev, cq, nq, len(stores), p, c) for cq, nq in qs]
+    B = batches[0].B
+    retrieve, tree, verify = make_pipeline(fc, torch, dev, stores, p, alpha, c, B)
+    prepare_targets(torch, dev, batches, retrieve, tree)
+    fns = (retrieve, tree, verify)
+    rot = lambda i: i % R  # noqa: E731
+    same = lambda i: 0  # noqa: E731
+    for i in range(args.warmup):
+        for f in fns:
+            f(batches[rot(i)])
     torch.cuda.synchronize()
 
     K = args.steps
     gc.collect()
-    # Timed region 1: K steps back to back, one event pair around them (an
+    # Timed region 1: K steps back to back over the rotation of distinct
+    # batches (each step's contexts, continuations and trees live in buffers
+    # the previous R - 1 steps did not touch), one event pair around them; an
     # event between entry points costs a few microseconds of queue time, so
-    # the throughput is timed without them).
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
+    # the throughput is timed without them.  Then the same with one batch
+    # repeated (its lines stay warm in L2 and the MALL).
     wall0 = time.perf_counter()
-    start.record(stream)
-    for i in range(K):
-        retrieve()
-        tree()
-        verify()
-    end.record(stream)
-    torch.cuda.synchronize()
+    total_ms = timed_steps(torch, stream, K, rot, batches, fns)
     wall = time.perf_counter() - wall0
-    total_ms = start.elapsed_time(end)
-    ms_step = total_ms / K
-    # Timed region 2: K more steps with an event at every entry-point
-    # boundary, for each entry point's time per launch (the roofline).
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
-    torch.cuda.synchronize()
-    for i in range(K):
-        ev[i][0].record(stream)
-        retrieve()
-        ev[i][1].record(stream)
-        tree()
-        ev[i][2].record(stream)
-        verify()
-        ev[i][3].record(stream)
-    torch.cuda.synchronize()
-    # median per launch: robust to a step where the host fell behind the GPU
-    phase_ms = {name: float(np.median([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)]))
-                for j, name in enumerate(("fc_retrieve", "fc_build_tree", "fc_verify_accept"))}
+    repeat_ms = timed_steps(torch, stream, K, same, batches, fns)
+    # Timed region 2: K more rotating steps with an event at every
+    # entry-point boundary, for each entry point's time per launch.
+    ph = timed_phases(torch, stream, K, rot, batches, fns)
+    names = ("fc_retrieve", "fc_build_tree", "fc_verify_accept")
+    phase_mean = {n: float(np.mean(v)) for n, v in zip(names, ph)}
+    phase_med = {n: float(np.median(v)) for n, v in zip(names, ph)}
 
     # single-query latency (B = 1): one query's retrieve + tree + accept on
-    # its own, event-timed, over the batch's first queries
-    r1 = fc.retrieve_outputs(1, len(stores), k, m, dev)
-    rws1 = torch.empty(max(fc.fc_retrieve_workspace_bytes(1, len(stores), p["n_max"], p["n_min"], k, m), 1),
-                       dtype=torch.uint8, device=dev)
-    t1o = fc.tree_outputs(1, c, dev)
-    tws1 = torch.empty(max(fc.fc_build_tree_workspace_bytes(1), 1), dtype=torch.uint8, device=dev)
-    a1o = fc.accept_outputs(1, m, dev)
+    # its own, event-timed, over the first batch's first queries
     lat = []
-    for qi in range(0 if args.no_latency else min(64, B) + 3):
-        cq, tq = ctx[qi % B:qi % B + 1], target[qi % B:qi % B + 1]
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        fc.fc_retrieve(stores, cq, n_max=p["n_max"], n_min=p["n_min"], k=k, m=m, out=r1, workspace=rws1)
-        fc.fc_build_tree(r1["taken"], r1["cont_len"], r1["cont_tok"], cq, c=c, alpha=alpha, out=t1o, workspace=tws1)
-        fc.fc_verify_accept(t1o, tq, m=m, out=a1o)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        if qi >= 3:  # the first three warm up
-            lat.append(e0.elapsed_time(e1))
+    if not args.no_latency:
+        one = Batch(fc, torch, dev, qs[0][0][:1], qs[0][1][:1], len(stores), p, c)
+        r1, t1f, v1 = make_pipeline(fc, torch, dev, stores, p, alpha, c, 1)
+        for qi in range(min(64, B) + 3):
+            one.ctx.copy_(batches[0].ctx[qi % B:qi % B + 1])
+            one.target = batches[0].target[qi % B:qi % B + 1]
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            r1(one), t1f(one), v1(one)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            if qi >= 3:  # the first three warm up
+                lat.append(e0.elapsed_time(e1))
 
-    # outputs of the batch, for the byte model and the acceptance statistic
-    taken = rout["taken"].cpu().numpy()
-    cont_len = rout["cont_len"].cpu().numpy()
-    match_n = rout["match_n"].cpu().numpy()
-    acc = aout["accept_len"].cpu().numpy()
-    nb = algorithmic_bytes(taken, cont_len, match_n, n_hi_of(ctx_np, p["n_max"]), [len(t) for t in texts],
-                           k, m, c, p["n_min"])
-    entry_bytes = {"fc_retrieve": nb["search"] + nb["gather"], "fc_build_tree": nb["tree"],
+    # byte models per batch, averaged over the launches of the timed rotation
+    sizes = [len(t) for t in texts]
+    per = []
+    for bt in batches:
+        per.append(algorithmic_bytes(bt.rout["taken"].cpu().numpy(), bt.rout["cont_len"].cpu().numpy(),
+                                     bt.rout["match_n"].cpu().numpy(), n_hi_of(bt.ctx_np, p["n_max"]), sizes, k, m, c,
+                                     p["n_min"]))
+    w = np.bincount([rot(i) for i in range(K)], minlength=R) / K
+    nb = {key: float(sum(w[r] * per[r][key] for r in range(R))) for key in per[0]}
+    entry_bytes = {"fc_retrieve": nb["search"] + nb["io"] + nb["gather"], "fc_build_tree": nb["tree"],
                    "fc_verify_accept": nb["verify"]}
-    traffic = measured_traffic()
+    traffic = measured_traffic(TRAFFIC_FILE)
     roofs = {}
-    for name, ms in phase_ms.items():
+    for name in names:
+        ms = phase_mean[name]
         gbs = entry_bytes[name] / (ms * 1e-3) / 1e9
         t = traffic.get(name)
-        roofs[name] = {"bound": "hbm", "kernel": name, "kernels": list(ENTRY_KERNELS[name]), "achieved": gbs,
-                       "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "traffic": t,
+        roofs[name] = {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                       "frac": gbs / HBM_PEAK_GBS, "traffic": t, "kernel": name, "kernels": list(ENTRY_KERNELS[name]),
                        "algorithmic_bytes": entry_bytes[name], "us_per_launch": ms * 1e3,
+                       "us_per_launch_median": phase_med[name] * 1e3,
                        "traffic_GBps": None if t is None else t / (ms * 1e-3) / 1e9}
-    dominant = max(phase_ms, key=phase_ms.get)
-    total_bytes = sum(nb.values())
+    rr = roofs["fc_retrieve"]
+    rr["byte_model"] = ("search: 2*ceil(log2(N_s+1))*(4+2n) per store and tried n; io: context 2L + 16 per store; "
+                        "gather: 4 + 2*len read and 26 written per kept slot")
+    rr["algorithmic_bytes_bucketed_search"] = nb["search_bucketed"] + nb["io"] + nb["gather"]
+    rr["frac_bucketed_search"] = rr["algorithmic_bytes_bucketed_search"] / (phase_mean["fc_retrieve"] * 1e-3) / 1e9 / HBM_PEAK_GBS
 
+    footprint = sum(bt.ctx.numel() * 2 + sum(v.numel() * v.element_size() for v in bt.rout.values())
+                    + sum(v.numel() * v.element_size() for v in bt.tout.values()) for bt in batches)
+
+    with_oracle = not args.no_cpu_baseline
+    info = host_info() if with_oracle else None
     cpu = None
-    if not args.no_cpu_baseline:
-        import oracle
-        done, spent = cpu_baseline(texts, ctx_np, nxt_np, p, alpha, c, args.cpu_budget)
-        cpu = {"value": done / spent, "unit": "retrievals/s", "cores": oracle.max_threads(), "kind": "oracle",
-               "sample": f"first {done} of the {B} queries (retrieve + tree + accept), {spent:.1f} s"}
+    if with_oracle:
+        sec = oracle_batch(texts, batches[0].ctx_np, batches[0].nxt_np, p, alpha, c)
+        cpu = {"value": B / sec, "unit": "retrievals/s", "cores": info["oracle_threads"], "kind": "oracle",
+               "sample": f"the whole first batch ({B} queries: batched retrieval, tree, acceptance), {sec:.1f} s",
+               "host": info}
+
+    configs = None
+    if not args.no_configs:
+        configs = {}
+        log("configuration 4: replay")
+        configs["replay_128x4096"] = replay_config(args, fc, torch, synth, dev, stores, texts, p, with_oracle)
+        del stores, batches
+        torch.cuda.empty_cache()
+        log("configuration 5: builds")
+        configs["sa_build_1B_and_10M"] = build_config(args, fc, torch, synth, dev, dict(zip(roles, texts)), with_oracle)
+        synth.drop_cache()
+        del texts
+        log("configuration 1")
+        configs["single_1M"] = small_config(args, 1, fc, torch, synth, dev, p, c, with_oracle)
+        log("configuration 2")
+        configs["two_store_2M_100M"] = small_config(args, 2, fc, torch, synth, dev, p, c, with_oracle,
+                                                    retrieve_bytes=True)
+        synth.drop_cache()
 
     line = {
         "metric": "draft retrievals/sec (match+gather+trie) at 1B-token datastore; HBM GB/s vs peak",
@@ -345,28 +546,35 @@ def main():
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
-        "ms_per_step": ms_step,
+        "ms_per_step": total_ms / K,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u16/u32 (integer)",
         "data": "synthetic (seeded template/Zipf/noise token stores; no dataset)",
-        "config": {"workload": synth.WORKLOADS[cfg]["name"], "stores_tokens": [len(t) for t in texts],
-                   "batch": B, "n_max": p["n_max"], "n_min": p["n_min"], "k": k, "m": m, "c": c,
-                   "alpha": list(alpha), "parallelism": "none (1 GPU)"},
-        "roofline": roofs[dominant],
+        "config": {"workload": synth.WORKLOADS[cfg]["name"], "stores_tokens": sizes, "batch": B,
+                   "n_max": p["n_max"], "n_min": p["n_min"], "k": k, "m": m, "c": c, "alpha": list(alpha),
+                   "parallelism": "none (1 GPU)", "batches_rotated": R},
+        "cache_state": (f"value: steps cycle {R} distinct seeded batches, each with its own output buffers "
+                        f"({footprint / 1e9:.2f} GB of contexts and outputs in the rotation, above the 256 MB MALL); "
+                        "value_repeat_batch: one batch repeated (warm L2 and MALL)"),
+        "value_repeat_batch": B * K / (repeat_ms * 1e-3),
+        "ms_per_step_repeat_batch": repeat_ms / K,
+        "roofline": roofs["fc_retrieve"],
         "roofline_by_entry": roofs,
         "cpu_baseline": cpu,
-        "phases_ms": phase_ms,
+        "phases_ms": phase_mean,
+        "phases_ms_median": phase_med,
         "single_query_latency_ms": None if not lat else {
             "median": float(np.median(lat)), "p90": float(np.percentile(lat, 90)), "queries": len(lat)},
-        "ms_per_step_with_phase_events": float(sum(phase_ms.values())),
+        "ms_per_step_with_phase_events": float(sum(phase_mean.values())),
         "algorithmic_bytes_per_step": nb,
-        "step_GBps_algorithmic": total_bytes / (ms_step * 1e-3) / 1e9,
-        "accept_len_mean": float(acc.mean()),
-        "slots_kept_mean": float(taken.sum(axis=1).mean()),
+        "step_GBps_algorithmic": (nb["search"] + nb["io"] + nb["gather"] + nb["tree"] + nb["verify"])
+        / (total_ms / K * 1e-3) / 1e9,
+        "slots_kept_mean": nb["kept"] / B,
         "sa_build_s": build_s,
         "wall_s_timed": wall,
+        "configs": configs,
     }
     print(json.dumps(line), flush=True)
 
@@ -654,6 +862,43 @@ def run_tree_attention(args):
                      "mfma_frac_bf16": flops / (ms * 1e-3) / 2.5e15},
         "cpu_baseline": cpu,
     }), flush=True)
+
+
+def run_gather_probe(args):
+    """Known-bytes random reads for checking the traffic counters' scale on
+    the access pattern of the retrieval: rows of 64 bytes (then 32 bytes) at
+    uniformly random row indexes of a 64 GiB buffer, 4M rows per launch,
+    gathered into a dense output.  Per launch it reads 8 bytes of index and
+    one row per index, and writes one row per index."""
+    import torch
+
+    dev = torch.device("cuda", 0)
+    span = 64 << 30
+    buf = torch.empty(span // 4, dtype=torch.int32, device=dev)
+    rows = 4 << 20
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(11)
+    out = {}
+    for row_bytes in (64, 32):
+        src = buf.view(-1, row_bytes // 4)
+        idx = torch.randint(0, src.shape[0], (rows,), generator=gen, device=dev)
+        dst = torch.empty((rows, row_bytes // 4), dtype=torch.int32, device=dev)
+        for _ in range(max(args.warmup, 1)):
+            torch.index_select(src, 0, idx, out=dst)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            torch.index_select(src, 0, idx, out=dst)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / max(args.steps, 1)
+        read = rows * (8 + row_bytes)
+        out[f"rows_{row_bytes}B"] = {"rows": rows, "bytes_read": read, "bytes_written": rows * row_bytes,
+                                     "us_per_launch": ms * 1e3,
+                                     "GBps": (read + rows * row_bytes) / (ms * 1e-3) / 1e9}
+    print(json.dumps({"metric": "random row gather over a 64 GiB buffer (known bytes per launch)", "cases": out,
+                      "steps": args.steps, "warmup": args.warmup, "n_gpus": 1}), flush=True)
 
 
 def run_copy(args):

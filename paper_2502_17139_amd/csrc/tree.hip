@@ -30,6 +30,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+#include <type_traits>
+
 #include "fastcoder.h"
 #include "fc_device.h"
 #include "fc_host.h"
@@ -642,8 +645,8 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   const int seg1 = s_seg[1 < S ? 1 : S], seg2 = s_seg[2 < S ? 2 : S], seg3 = s_seg[3 < S ? 3 : S];
   auto store_of = [&](int i) -> int { return (S > 1 && i >= seg1) + (S > 2 && i >= seg2) + (S > 3 && i >= seg3); };
   // with one weight for every store the alpha prefix sum is linear
-  const bool alpha_flat = NARROW || (S < 2 || alpha.a[1] == alpha.a[0]) && (S < 3 || alpha.a[2] == alpha.a[0]) &&
-                          (S < 4 || alpha.a[3] == alpha.a[0]);
+  const bool alpha_flat = NARROW || ((S < 2 || alpha.a[1] == alpha.a[0]) && (S < 3 || alpha.a[2] == alpha.a[0]) &&
+                                     (S < 4 || alpha.a[3] == alpha.a[0]));
   const bool even_m = (m & 1) == 0;  // rows are 4-byte aligned in LDS
   auto rcmp = [&](int i, int j) -> int {
     return even_m ? row_cmp_w<MAXM / 2>(str + i * m, len[i], str + j * m, len[j])
@@ -1078,6 +1081,929 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
   if (tid == 0) num_nodes[b] = err ? -1 : num;
 }
 
+// ---------------------------------------------------------------------------
+// Flat path (m <= 16, every query unless its short lists are too long).  One
+// workgroup of kFlatThreads threads per query, and no continuation text in
+// LDS except the strings of the query's short stores: every store but the
+// one with the most kept slots (the long store), which in practice hold a
+// handful of strings beside thousands.  The long store's strings stay in
+// the retrieval output (L2-resident right after fc_retrieve) and are read
+// once, coalesced:
+//   1. each long string finds its place among the short strings by binary
+//      search in LDS; its merged position is its own index plus that rank,
+//      and its adjacent LCP comes from its neighbour in the long list (a
+//      lane shuffle) or from the short string just before it;
+//   2. the merged positions the long strings leave free are the short
+//      strings', in their own merged order;
+//   3. from the per-position LCP and length, the run ends, weights, top-c
+//      selection and emission of the trie follow as in the fast path, with
+//      every node weight recomputed from the per-depth next heads in each
+//      pass instead of being stored (that array was k*m*2 bytes).
+// LDS per query is then 3 bytes per kept slot plus the short strings, so two
+// queries of the largest size share a CU.
+// ---------------------------------------------------------------------------
+
+constexpr int kFlatThreads = 512;
+constexpr int kFlatRows = 4;       // long-string loads in flight per lane
+constexpr int kFlatShortCap = 256;  // short strings a query may keep in LDS
+constexpr int kFlatShared = 2048;   // shared trie nodes (two strings or more) listed in LDS
+constexpr int kFlatCand = 512;      // candidates of the list-based selection (one per thread)
+static_assert(kFlatCand <= kFlatThreads, "one candidate per thread");
+
+struct FlatLayout {
+  size_t perm, lm, A, sstr, slen, sidx, sh_key, sh_w, total;
+};
+
+// maxm: the instantiation's row width (rows of maxm/2 32-bit words);
+// cap: short strings held; with_A: alpha prefix sums (stores of different
+// weights); S > 2: the short strings' merged order needs its own index.
+__host__ __device__ inline FlatLayout flat_layout(int k, int maxm, int cap, int S, bool with_A) {
+  FlatLayout t;
+  size_t o = 0;
+  t.perm = o;  // k uint16: merged position -> slot
+  o = align_up(o + (size_t)k * 2, 16);
+  t.lm = o;  // k packed (lcp, merged length)
+  o = align_up(o + (size_t)k * (maxm <= 15 ? 1 : 2), 16);
+  t.A = o;  // k+1 uint32 alpha prefix sums
+  if (with_A) o = align_up(o + (size_t)(k + 1) * 4, 16);
+  t.sstr = o;  // cap rows of maxm/2 words; later the selection's candidates
+  const size_t rows = (size_t)cap * maxm * 2, cand = (size_t)kFlatCand * 8;
+  o = align_up(o + (rows > cand ? rows : cand), 16);
+  t.slen = o;  // cap uint8
+  o = align_up(o + (size_t)cap, 16);
+  t.sidx = o;  // cap uint16: short merged order -> LDS row
+  if (S > 2) o = align_up(o + (size_t)cap * 2, 16);
+  t.sh_key = o;  // shared trie nodes: (merged position, depth)
+  o = align_up(o + (size_t)kFlatShared * 4, 16);
+  t.sh_w = o;  // their weights (16 bits when no weight can exceed them)
+  o = align_up(o + (size_t)kFlatShared * (with_A ? 4 : 2), 16);
+  t.total = o;
+  return t;
+}
+
+// Per-store kept slots of query q, their total, the store with the most
+// slots (the lowest index on ties) and whether the row is malformed (outside
+// the row map's range, a negative count, or more than k slots in all;
+// malformed rows count as empty and are reported with num_nodes = -1).
+struct QueryShape {
+  int tk[FC_MAX_SOURCES];
+  int T, longest, n_long;  // n_long = tk[longest]
+  bool bad;
+};
+
+__device__ __forceinline__ QueryShape query_shape(const int32_t* __restrict__ taken, int S, int k,
+                                                  const int32_t* __restrict__ rows, int n_rows, int q) {
+  QueryShape r;
+  const int row = fc::map_row(rows, n_rows, q);
+  r.bad = row < 0;
+  r.T = 0;
+#pragma unroll
+  for (int s = 0; s < FC_MAX_SOURCES; ++s) {
+    r.tk[s] = (s < S && row >= 0) ? taken[(int64_t)row * S + s] : 0;
+    r.bad |= r.tk[s] < 0;
+    r.T += r.tk[s] > 0 ? r.tk[s] : 0;
+  }
+  r.bad |= r.T > k;
+  if (r.bad) {
+#pragma unroll
+    for (int s = 0; s < FC_MAX_SOURCES; ++s) r.tk[s] = 0;
+    r.T = 0;
+  }
+  r.longest = 0;
+  r.n_long = r.tk[0];
+#pragma unroll
+  for (int s = 1; s < FC_MAX_SOURCES; ++s)
+    if (r.tk[s] > r.n_long) r.longest = s, r.n_long = r.tk[s];
+  return r;
+}
+
+// Tokens [0, len) of a continuation row as MAXM/2 words (token 2x in the
+// low half of word x), zero past len.
+template <int MAXM>
+__device__ __forceinline__ void load_row_words(const uint16_t* __restrict__ src, int m, int len, bool words,
+                                               uint32_t (&v)[MAXM / 2]) {
+  if (words) {
+    const uint32_t* s32 = (const uint32_t*)src;
+#pragma unroll
+    for (int x = 0; x < MAXM / 2; ++x) v[x] = 2 * x < m ? s32[x] : 0u;
+  } else {
+#pragma unroll
+    for (int x = 0; x < MAXM / 2; ++x) {
+      const uint32_t a = 2 * x < m ? src[2 * x] : 0u;
+      const uint32_t b = 2 * x + 1 < m ? src[2 * x + 1] : 0u;
+      v[x] = a | (b << 16);
+    }
+  }
+#pragma unroll
+  for (int x = 0; x < MAXM / 2; ++x)
+    v[x] &= (2 * x < len ? 0xFFFFu : 0u) | (2 * x + 1 < len ? 0xFFFF0000u : 0u);
+}
+
+// LCP and order of two word rows (zero past their lengths).
+template <int W>
+__device__ __forceinline__ int lcp_words(const uint32_t (&a)[W], int la, const uint32_t (&b)[W], int lb) {
+  const int n = la < lb ? la : lb;
+  int first = 2 * W;
+#pragma unroll
+  for (int j = W - 1; j >= 0; --j) {
+    const uint32_t d = a[j] ^ b[j];
+    if (d) first = 2 * j + ((d & 0xFFFFu) == 0 ? 1 : 0);
+  }
+  return first < n ? first : n;
+}
+
+template <int W>
+__device__ __forceinline__ int cmp_words(const uint32_t (&a)[W], int la, const uint32_t (&b)[W], int lb) {
+  const int x = lcp_words<W>(a, la, b, lb);
+  const int n = la < lb ? la : lb;
+  if (x < n) {
+    uint32_t wa = 0, wb = 0;
+#pragma unroll
+    for (int j = 0; j < W; ++j)
+      if (j == (x >> 1)) wa = a[j], wb = b[j];
+    const uint32_t ta = (x & 1) ? wa >> 16 : wa & 0xFFFFu, tb = (x & 1) ? wb >> 16 : wb & 0xFFFFu;
+    return ta < tb ? -1 : 1;
+  }
+  return la < lb ? -1 : (la > lb ? 1 : 0);
+}
+
+template <int W>
+__device__ __forceinline__ void lds_row(const uint32_t* __restrict__ sstr, int ci, uint32_t (&v)[W]) {
+#pragma unroll
+  for (int x = 0; x < W; ++x) v[x] = sstr[ci * W + x];
+}
+
+// Strings of the LDS rows [lo, hi) that precede string (v, len) in merged
+// order: those <= it when their store comes first on ties (upper), those
+// < it otherwise.
+template <int W>
+__device__ __forceinline__ int count_before(const uint32_t* __restrict__ sstr, const uint8_t* __restrict__ slen, int lo,
+                                            int hi, const uint32_t (&v)[W], int len, bool upper) {
+  const int base = lo;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    uint32_t r[W];
+    lds_row<W>(sstr, mid, r);
+    const int cc = cmp_words<W>(r, slen[mid], v, len);
+    if (upper ? cc <= 0 : cc < 0) lo = mid + 1; else hi = mid;
+  }
+  return lo - base;
+}
+
+template <int MAXM, bool NARROW>
+__global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(const int32_t* __restrict__ taken,
+                                                            const uint8_t* __restrict__ cont_len,
+                                                            const uint16_t* __restrict__ cont_tok,
+                                                            const uint16_t* __restrict__ ctx, int L, int S, int k,
+                                                            int m, int c, Alpha alpha, int cap, int words,
+                                                            int32_t* __restrict__ defer_list,
+                                                            int32_t* __restrict__ defer_count, int B,
+                                                            const int32_t* __restrict__ rows, int n_rows,
+                                                            int32_t* __restrict__ num_nodes,
+                                                            int32_t* __restrict__ node_tok,
+                                                            int32_t* __restrict__ parent, uint32_t* __restrict__ weight,
+                                                            int32_t* __restrict__ pos_ids, int32_t* __restrict__ mask) {
+  constexpr int NT = kFlatThreads;
+  constexpr int NW = NT / fc::kWave;
+  constexpr int W = MAXM / 2;
+  using LMT = typename std::conditional<(MAXM <= 15), uint8_t, uint16_t>::type;
+  using SWT = typename std::conditional<NARROW, uint16_t, uint32_t>::type;  // NARROW: every weight < 2^16
+  constexpr int kSh = MAXM <= 15 ? 4 : 8;
+  constexpr uint32_t kLo = (1u << kSh) - 1u;
+  static_assert(NT >= FC_MAX_TREE_ROWS, "one thread per tree row");
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ int s_seg[FC_MAX_SOURCES + 1];
+  __shared__ int s_cs[FC_MAX_SOURCES + 1];
+  __shared__ int s_err;
+  __shared__ uint32_t s_x[NW + 1], s_y[NW + 1], s_z[NW + 1];
+  __shared__ uint16_t s_wmin[NW][MAXM + 1];
+  __shared__ uint16_t s_wsuf[NW][MAXM + 1];
+  __shared__ uint32_t s_hist[256];
+  __shared__ uint32_t s_sel_w[FC_MAX_TREE_ROWS];
+  __shared__ uint16_t s_sel_p[FC_MAX_TREE_ROWS];
+  __shared__ uint8_t s_sel_d[FC_MAX_TREE_ROWS];
+  __shared__ int16_t s_par[FC_MAX_TREE_ROWS];
+  __shared__ uint64_t s_dball[FC_MAX_TREE_ROWS / fc::kWave][MAXM];
+  __shared__ uint64_t s_shallow[FC_MAX_TREE_ROWS / fc::kWave][MAXM + 1];
+  __shared__ int16_t s_end[FC_MAX_TREE_ROWS];
+  __shared__ uint32_t s_pick[3];
+  __shared__ uint32_t s_nsh;
+  __shared__ uint32_t s_ncand;
+
+  const int tid = threadIdx.x;
+  const int lane = fc::lane_id();
+  const int w = tid / fc::kWave;
+  auto deferred = [&](const QueryShape& qs) { return !qs.bad && qs.T - qs.n_long > cap; };
+  if ((int)blockIdx.x == B) {
+    // the list of queries left to the general kernel, in query order
+    const int per = (B + NT - 1) / NT;
+    const int q0 = tid * per < B ? tid * per : B;
+    const int q1 = q0 + per < B ? q0 + per : B;
+    uint32_t nd = 0;
+    for (int q = q0; q < q1; ++q) nd += deferred(query_shape(taken, S, k, rows, n_rows, q)) ? 1u : 0u;
+    uint32_t ed, dummy, td, dummy2;
+    Scan2<NT>::run(nd, 0u, s_x, s_y, &ed, &dummy, &td, &dummy2);
+    for (int q = q0; q < q1; ++q)
+      if (deferred(query_shape(taken, S, k, rows, n_rows, q))) defer_list[ed++] = q;
+    if (tid == 0) *defer_count = (int32_t)td;
+    return;
+  }
+  const int b = (int)blockIdx.x;
+  const QueryShape qs = query_shape(taken, S, k, rows, n_rows, b);
+  if (deferred(qs)) return;
+  const int R = c + 1;
+  const int in_row = fc::map_row(rows, n_rows, b);
+  const int64_t row0 = (int64_t)(in_row < 0 ? 0 : in_row) * k;
+  const uint16_t root_tok = ctx[(int64_t)b * L + L - 1];  // issued early, used at the end
+  const int T = qs.T;
+  const int sL = qs.longest;
+  const int nL = qs.n_long;
+  const int n_short = T - nL;
+
+  if (tid == 0) {
+    int acc = 0, cacc = 0;
+#pragma unroll
+    for (int s = 0; s < FC_MAX_SOURCES; ++s) {
+      if (s < S) {
+        s_seg[s] = acc;
+        s_cs[s] = cacc;
+        acc += qs.tk[s];
+        cacc += s == sL ? 0 : qs.tk[s];
+      }
+    }
+    s_seg[S] = acc;
+    s_cs[S] = cacc;
+    s_err = qs.bad;
+    s_pick[0] = 0;
+    s_pick[1] = 0;
+    s_pick[2] = 0;
+  }
+  for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
+  __syncthreads();
+
+  // At most one kept continuation: the tree is the chain of its first
+  // min(len, c) tokens, every node of that store's weight alpha.
+  const int len0 = (!qs.bad && T == 1) ? (int)cont_len[row0] : 0;
+  if (!qs.bad && T <= 1 && len0 <= m) {
+    int s0 = 0;
+#pragma unroll
+    for (int s = FC_MAX_SOURCES - 1; s >= 0; --s)
+      if (s < S && qs.tk[s] > 0) s0 = s;
+    const uint32_t a0 = alpha_of(alpha, s0);
+    const int num = 1 + (len0 < c ? len0 : c);
+    for (int r = tid; r < R; r += NT) {
+      const int64_t o = (int64_t)b * R + r;
+      node_tok[o] = r == 0 ? (int32_t)root_tok : (r < num ? (int32_t)cont_tok[row0 * m + r - 1] : 0);
+      parent[o] = (r >= 1 && r < num) ? r - 1 : -1;
+      weight[o] = r == 0 ? (len0 > 0 ? a0 : 0u) : (r < num ? a0 : 0u);
+      pos_ids[o] = r < num ? r : 0;
+    }
+    const int64_t mb = (int64_t)b * R * R;
+    int i = tid / R, j = tid - (tid / R) * R;
+    const int di = NT / R, dj = NT - (NT / R) * R;
+    for (int e = tid; e < R * R; e += NT) {
+      mask[mb + e] = (i < num && j <= i) ? 1 : 0;
+      i += di;
+      j += dj;
+      if (j >= R) {
+        j -= R;
+        ++i;
+      }
+    }
+    if (tid == 0) num_nodes[b] = num;
+    return;
+  }
+
+  const FlatLayout lay = flat_layout(k, MAXM, cap, S, !NARROW);
+  uint16_t* perm = (uint16_t*)(smem + lay.perm);
+  LMT* lm = (LMT*)(smem + lay.lm);
+  uint32_t* A = (uint32_t*)(smem + lay.A);
+  uint32_t* sstr = (uint32_t*)(smem + lay.sstr);
+  uint8_t* slen = smem + lay.slen;
+  uint16_t* sidx = (uint16_t*)(smem + lay.sidx);
+  const int seg1 = s_seg[1 < S ? 1 : S], seg2 = s_seg[2 < S ? 2 : S], seg3 = s_seg[3 < S ? 3 : S];
+  auto store_of = [&](int slot) -> int {
+    return (S > 1 && slot >= seg1) + (S > 2 && slot >= seg2) + (S > 3 && slot >= seg3);
+  };
+  // the short store of LDS row ci, and that row's slot
+  auto short_store = [&](int ci) -> int {
+    int s = 0;
+#pragma unroll
+    for (int u = 0; u < FC_MAX_SOURCES; ++u)
+      if (u < S && u != sL && ci >= s_cs[u] && ci < s_cs[u] + qs.tk[u]) s = u;
+    return s;
+  };
+  auto short_slot = [&](int ci) -> int {
+    const int s = short_store(ci);
+    return s_seg[s] + (ci - s_cs[s]);
+  };
+  const bool alpha_flat = NARROW || ((S < 2 || alpha.a[1] == alpha.a[0]) && (S < 3 || alpha.a[2] == alpha.a[0]) &&
+                                     (S < 4 || alpha.a[3] == alpha.a[0]));
+
+  // 1. the short strings into LDS, each store's order checked; with three
+  //    or more stores, their merged order among themselves
+  for (int p = tid; p < T; p += NT) perm[p] = 0xFFFF;
+  if (S > 2)
+    for (int g = tid; g < n_short; g += NT) sidx[g] = 0;  // every entry valid even if unsorted input collides
+  for (int ci = tid; ci < n_short; ci += NT) {
+    const int slot = short_slot(ci);
+    int len = cont_len[row0 + slot];
+    if (len > m) s_err = 1;
+    len = len < m ? len : m;
+    uint32_t v[W];
+    load_row_words<MAXM>(cont_tok + (row0 + slot) * m, m, len, words != 0, v);
+#pragma unroll
+    for (int x = 0; x < W; ++x) sstr[ci * W + x] = v[x];
+    slen[ci] = (uint8_t)len;
+  }
+  __syncthreads();
+  for (int ci = tid; ci < n_short; ci += NT) {
+    const int s = short_store(ci);
+    const int i = ci - s_cs[s];
+    uint32_t v[W];
+    lds_row<W>(sstr, ci, v);
+    const int len = slen[ci];
+    if (i > 0) {
+      uint32_t pv[W];
+      lds_row<W>(sstr, ci - 1, pv);
+      if (cmp_words<W>(pv, slen[ci - 1], v, len) > 0) s_err = 1;
+    }
+    if (S > 2) {
+      int pos = i;
+#pragma unroll
+      for (int u = 0; u < FC_MAX_SOURCES; ++u)
+        if (u < S && u != sL && u != s && qs.tk[u] > 0)
+          pos += count_before<W>(sstr, slen, s_cs[u], s_cs[u] + qs.tk[u], v, len, u < s);
+      sidx[pos] = (uint16_t)ci;
+    }
+  }
+  __syncthreads();
+
+  // 2. long strings: rank among the short strings, merged position, LCP
+  //    with the merged predecessor when that is long (its neighbour in the
+  //    long list) or the short string just before.  Each wave takes 63
+  //    consecutive long strings per pass and its lane 0 the string before
+  //    them, so every predecessor comes from the lane below; kFlatRows
+  //    passes have their loads in flight together.
+  auto rank_short = [&](const uint32_t (&v)[W], int len) -> int {
+    int r = 0;
+#pragma unroll
+    for (int u = 0; u < FC_MAX_SOURCES; ++u)
+      if (u < S && u != sL && qs.tk[u] > 0)
+        r += count_before<W>(sstr, slen, s_cs[u], s_cs[u] + qs.tk[u], v, len, u < sL);
+    return r;
+  };
+  const int lslot0 = s_seg[sL];
+  constexpr int kPass = NW * (fc::kWave - 1);  // long strings per pass of the block
+  for (int j0 = 0; j0 < nL; j0 += kPass * kFlatRows) {
+    uint32_t v[kFlatRows][W];
+    int len[kFlatRows];
+#pragma unroll
+    for (int u = 0; u < kFlatRows; ++u) {
+      const int j = j0 + u * kPass + w * (fc::kWave - 1) + lane - 1;
+      len[u] = 0;
+      if (j >= 0 && j < nL) {
+        len[u] = cont_len[row0 + lslot0 + j];
+        const uint16_t* src = cont_tok + (row0 + lslot0 + j) * m;
+        if (words) {
+          const uint32_t* s32 = (const uint32_t*)src;
+#pragma unroll
+          for (int x = 0; x < W; ++x) v[u][x] = 2 * x < m ? s32[x] : 0u;
+        } else {
+#pragma unroll
+          for (int x = 0; x < W; ++x) {
+            const uint32_t a0 = 2 * x < m ? src[2 * x] : 0u;
+            const uint32_t a1 = 2 * x + 1 < m ? src[2 * x + 1] : 0u;
+            v[u][x] = a0 | (a1 << 16);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int x = 0; x < W; ++x) v[u][x] = 0u;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kFlatRows; ++u) {
+      const int j = j0 + u * kPass + w * (fc::kWave - 1) + lane - 1;
+      const bool have = j >= 0 && j < nL;
+      if (have && len[u] > m) s_err = 1;
+      const int ln = len[u] < m ? len[u] : m;
+#pragma unroll
+      for (int x = 0; x < W; ++x) v[u][x] &= (2 * x < ln ? 0xFFFFu : 0u) | (2 * x + 1 < ln ? 0xFFFF0000u : 0u);
+      const int r = have && n_short > 0 ? rank_short(v[u], ln) : 0;
+      uint32_t pv[W];
+#pragma unroll
+      for (int x = 0; x < W; ++x) pv[x] = (uint32_t)__shfl_up((int)v[u][x], 1, fc::kWave);
+      const int plen = __shfl_up(ln, 1, fc::kWave);
+      const int pr = __shfl_up(r, 1, fc::kWave);
+      if (have && lane > 0) {
+        if (j > 0 && cmp_words<W>(pv, plen, v[u], ln) > 0) s_err = 1;
+        int l = 0;
+        if (j > 0 && pr == r) {
+          l = lcp_words<W>(pv, plen, v[u], ln);
+        } else if (r > 0) {
+          const int ci = S > 2 ? (int)sidx[r - 1] : r - 1;
+          uint32_t sv[W];
+          lds_row<W>(sstr, ci, sv);
+          l = lcp_words<W>(sv, slen[ci], v[u], ln);
+        }
+        const int P = j + r;
+        perm[P] = (uint16_t)(lslot0 + j);
+        lm[P] = (LMT)((uint32_t)l | ((uint32_t)ln << kSh));
+      }
+    }
+  }
+  __syncthreads();
+
+  // 3. the free merged positions take the short strings in order
+  const int per = (T + NT - 1) / NT;
+  const int p0 = tid * per < T ? tid * per : T;
+  const int p1 = p0 + per < T ? p0 + per : T;
+  if (n_short > 0) {
+    uint32_t gaps = 0;
+    for (int p = p0; p < p1; ++p) gaps += perm[p] == 0xFFFF ? 1u : 0u;
+    // the predecessor of the chunk, read before anything is rewritten
+    const uint16_t before = p0 > 0 && p0 < p1 ? perm[p0 - 1] : (uint16_t)0;
+    const uint32_t before_lm = p0 > 0 && p0 < p1 ? (uint32_t)lm[p0 - 1] : 0u;
+    uint32_t g0, dummy, gtot, dummy2;
+    Scan2<NT>::run(gaps, 0u, s_x, s_y, &g0, &dummy, &gtot, &dummy2);
+    bool prev_gap = before == 0xFFFF;
+    uint16_t prev_slot = before;
+    uint32_t prev_len = before_lm >> kSh;
+    for (int p = p0; p < p1; ++p) {
+      const uint16_t cur = perm[p];
+      if (cur != 0xFFFF) {
+        prev_gap = false;
+        prev_slot = cur;
+        prev_len = (uint32_t)lm[p] >> kSh;
+        continue;
+      }
+      const int g = (int)g0++;
+      if (g >= n_short) {
+        s_err = 1;  // only unsorted input can leave more free positions than short strings
+        break;
+      }
+      const int ci = S > 2 ? (int)sidx[g] : g;
+      uint32_t v[W];
+      lds_row<W>(sstr, ci, v);
+      const int len = slen[ci];
+      int l = 0;
+      if (p > 0 && prev_gap) {
+        const int pci = S > 2 ? (int)sidx[g - 1] : g - 1;
+        uint32_t pv[W];
+        lds_row<W>(sstr, pci, pv);
+        l = lcp_words<W>(pv, slen[pci], v, len);
+      } else if (p > 0) {
+        uint32_t pv[W];
+        load_row_words<MAXM>(cont_tok + (row0 + prev_slot) * m, m, (int)prev_len, words != 0, pv);
+        l = lcp_words<W>(pv, (int)prev_len, v, len);
+      }
+      const uint16_t slot = (uint16_t)short_slot(ci);
+      perm[p] = slot;
+      lm[p] = (LMT)((uint32_t)l | ((uint32_t)len << kSh));
+      prev_gap = true;
+      prev_slot = slot;
+      prev_len = (uint32_t)len;
+    }
+  }
+  __syncthreads();
+  const bool err = s_err != 0;
+
+  int nsel = 0;
+  uint32_t root_w = 0;
+  if (!err) {
+    // 4. chunk sums: alpha, non-empty strings (root weight), nodes, and the
+    //    chunk's first head per depth (first q with lcp[q] < d), then the
+    //    next head per depth after the chunk
+    const uint32_t a0 = alpha.a[0];
+    uint32_t asum = 0, rw = 0, nodes = 0;
+    uint16_t f[MAXM + 1];
+#pragma unroll
+    for (int d = 0; d <= MAXM; ++d) f[d] = (uint16_t)T;
+    for (int p = p1 - 1; p >= p0; --p) {
+      const uint32_t x = lm[p];
+      const int l = (int)(x & kLo), li = (int)(x >> kSh);
+      const uint32_t a = alpha_flat ? a0 : alpha_of(alpha, store_of(perm[p]));
+      asum += a;
+      if (li > 0) rw += a;
+      nodes += (uint32_t)(li - l);
+#pragma unroll
+      for (int d = 1; d <= MAXM; ++d)
+        if (l < d) f[d] = (uint16_t)p;
+    }
+    uint32_t a_ex, dummy, a_tot, n_tot;
+    Scan2<NT>::run(asum, nodes, s_x, s_y, &a_ex, &dummy, &a_tot, &n_tot, rw, s_z, &root_w);
+    uint16_t nh[MAXM + 1];
+#pragma unroll
+    for (int d = 1; d <= MAXM; ++d) {
+      uint32_t wave_min = (uint32_t)T;
+      nh[d] = (uint16_t)T;
+      if (d <= m) nh[d] = (uint16_t)fc::wave_excl_suffix_min_u32(f[d], (uint32_t)T, &wave_min);
+      if (lane == 0) s_wmin[w][d] = (uint16_t)wave_min;
+    }
+    if (tid == 0) {
+      s_nsh = 0;
+      s_ncand = 0;
+    }
+    __syncthreads();
+    if (tid < NW * MAXM) {
+      const int w0 = tid / MAXM, d0 = tid % MAXM + 1;
+      uint32_t v = (uint32_t)T;
+#pragma unroll
+      for (int u = 0; u < NW; ++u) {
+        const uint32_t x = s_wmin[u][d0];
+        v = (u > w0 && x < v) ? x : v;
+      }
+      s_wsuf[w0][d0] = (uint16_t)v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int d = 1; d <= MAXM; ++d) {
+      const uint32_t x = s_wsuf[w][d];
+      if (d <= m && x < nh[d]) nh[d] = (uint16_t)x;
+    }
+    if (!alpha_flat) {
+      uint32_t run = a_ex;
+      for (int p = p0; p < p1; ++p) {
+        A[p] = run;
+        run += alpha_of(alpha, store_of(perm[p]));
+      }
+      if (tid == 0) A[T] = a_tot;
+      __syncthreads();
+    }
+    // The own nodes of the chunk, right to left and deepest first (the
+    // reverse of (p, d) order), with their weights: node (q, d) covers the
+    // run from q to the next head of depth d.  Below the next string's LCP
+    // (shared nodes, weight of two strings or more) the weight is that
+    // difference; past it (the string's own tail) the run is q alone and the
+    // weight is q's alpha, so tails are handed over as one range (tail(q,
+    // d_lo, d_hi, w): depths d_lo < d <= d_hi) and shared nodes one by one
+    // (shared(q, d, w)), tail first.
+    auto walk = [&](auto&& tail, auto&& shared) {
+      uint32_t h[MAXM + 1];
+#pragma unroll
+      for (int d = 1; d <= MAXM; ++d) h[d] = nh[d];
+      int l_next = p1 < T ? (int)((uint32_t)lm[p1] & kLo) : 0;
+      uint32_t a_next = alpha_flat ? 0u : A[p1];
+      for (int q = p1 - 1; q >= p0; --q) {
+        const uint32_t x = lm[q];
+        const int l = (int)(x & kLo), ml = (int)(x >> kSh);
+        const uint32_t aq = alpha_flat ? 0u : A[q];
+        const uint32_t wq = alpha_flat ? a0 : a_next - aq;
+        const int lo_t = l > l_next ? l : l_next;
+        if (ml > lo_t) tail(q, lo_t, ml, wq);
+        const int hi_s = ml < l_next ? ml : l_next;
+#pragma unroll
+        for (int d = MAXM; d >= 1; --d) {
+          if (d > l && d <= hi_s) {
+            const uint32_t Wt = alpha_flat ? a0 * (h[d] - (uint32_t)q) : A[h[d]] - aq;
+            shared(q, d, Wt);
+          }
+        }
+#pragma unroll
+        for (int d = 1; d <= MAXM; ++d)
+          if (d > l) h[d] = (uint32_t)q;
+        l_next = l;
+        a_next = aq;
+      }
+    };
+    uint32_t* sh_key = (uint32_t*)(smem + lay.sh_key);
+    SWT* sh_w = (SWT*)(smem + lay.sh_w);
+
+    // 5. weight histogram: 1 and 2 (the bulk) in registers, other weights
+    //    below 256 by LDS atomics, heavier ones only counted; the shared
+    //    nodes are listed on the way (while they fit) for the selection
+    {
+      uint32_t r1 = 0, r2 = 0, rbig = 0;
+      auto count = [&](uint32_t Wt, uint32_t n) {
+        r1 += Wt == 1u ? n : 0u;
+        r2 += Wt == 2u ? n : 0u;
+        rbig += Wt >= 256u ? n : 0u;
+        if (Wt != 1u && Wt != 2u && Wt < 256u) atomicAdd(&s_hist[Wt], n);
+      };
+      walk([&](int, int lo, int hi, uint32_t Wt) { count(Wt, (uint32_t)(hi - lo)); },
+           [&](int q, int d, uint32_t Wt) {
+             count(Wt, 1u);
+             const uint32_t o = atomicAdd(&s_nsh, 1u);
+             if (o < (uint32_t)kFlatShared) {
+               sh_key[o] = ((uint32_t)q << 5) | (uint32_t)d;
+               sh_w[o] = (SWT)Wt;
+             }
+           });
+      const uint32_t x1 = fc::wave_sum_u32(r1), x2 = fc::wave_sum_u32(r2), xb = fc::wave_sum_u32(rbig);
+      if (lane == 0 && x1) atomicAdd(&s_hist[1], x1);
+      if (lane == 0 && x2) atomicAdd(&s_hist[2], x2);
+      if (lane == 0 && xb) atomicAdd(&s_pick[2], xb);
+    }
+    __syncthreads();
+    const uint32_t n_shared = s_nsh;
+    const bool listed = n_shared <= (uint32_t)kFlatShared;
+
+    // 6. the need-th largest weight W* and how many nodes of weight W* to
+    //    take (in (p, d) order)
+    const uint32_t need = n_tot < (uint32_t)c ? n_tot : (uint32_t)c;
+    uint32_t prefix = 0, remaining = need;
+    const uint32_t n_heavy = s_pick[2];
+    auto pick_bin = [&](uint32_t want, uint32_t base_prefix, int shift) {
+      // wave 0: the bin holding the want-th largest, from the top
+      if (tid < fc::kWave) {
+        uint32_t cnt4[4];
+        uint32_t lsum = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          cnt4[u] = s_hist[255 - (lane * 4 + u)];
+          lsum += cnt4[u];
+        }
+        const uint32_t incl = fc::wave_incl_sum_u32(lsum);
+        const uint32_t before = incl - lsum;
+        if (before < want && incl >= want) {
+          uint32_t acc = before;
+          int bin = 0;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            if (acc + cnt4[u] >= want) {
+              bin = 255 - (lane * 4 + u);
+              break;
+            }
+            acc += cnt4[u];
+          }
+          s_pick[0] = base_prefix | ((uint32_t)bin << shift);
+          s_pick[1] = want - acc;
+        }
+      }
+      __syncthreads();
+    };
+    if (need > 0 && n_heavy < need) {
+      pick_bin(need - n_heavy, 0u, 0);
+      prefix = s_pick[0];
+      remaining = s_pick[1];
+    } else if (need > 0) {
+      // W* >= 256: radix select over the heavy nodes only
+      uint32_t wmax = 0;
+      auto top = [&](uint32_t Wt) { wmax = Wt > wmax ? Wt : wmax; };
+      walk([&](int, int, int, uint32_t Wt) { top(Wt); }, [&](int, int, uint32_t Wt) { top(Wt); });
+      wmax = fc::block_max<uint32_t>(wmax, s_z);
+      int bits = 0;
+      for (uint32_t x = wmax; x; x >>= 1) ++bits;
+      for (int shift = ((bits - 1) / 8) * 8; shift >= 0; shift -= 8) {
+        for (int i = tid; i < 256; i += NT) s_hist[i] = 0;
+        __syncthreads();
+        const uint64_t hi_mask = shift + 8 >= 32 ? 0ull : (uint64_t)prefix >> (shift + 8);
+        auto digit = [&](uint32_t Wt, uint32_t n) {
+          if (n && Wt >= 256u && (shift + 8 >= 32 ? 0ull : (uint64_t)(Wt >> (shift + 8))) == hi_mask)
+            atomicAdd(&s_hist[(Wt >> shift) & 0xFF], n);
+        };
+        walk([&](int, int lo, int hi, uint32_t Wt) { digit(Wt, (uint32_t)(hi - lo)); },
+             [&](int, int, uint32_t Wt) { digit(Wt, 1u); });
+        __syncthreads();
+        pick_bin(remaining, prefix, shift);
+        prefix = s_pick[0];
+        remaining = s_pick[1];
+      }
+    }
+    const uint32_t wstar = prefix;
+    const uint32_t take_eq = remaining;
+
+    // 7. kept nodes in (p, d) order = preorder.  When every tail is lighter
+    //    than W* (the usual case) the kept nodes are shared ones: they are
+    //    gathered as candidates (weight >= W*), each learns how many
+    //    candidates precede it, and the first take_eq of weight W* are kept.
+    //    Otherwise the chunks count their kept nodes and emit them in order.
+    uint32_t tail_max = a0;
+#pragma unroll
+    for (int u = 1; u < FC_MAX_SOURCES; ++u)
+      if (u < S && alpha.a[u] > tail_max) tail_max = alpha.a[u];
+    bool fast_emit = listed && need > 0 && wstar > tail_max;
+    uint32_t* cand_key = (uint32_t*)(smem + lay.sstr);
+    uint32_t* cand_w = cand_key + kFlatCand;
+    if (fast_emit) {
+      for (uint32_t i = tid; i < n_shared; i += NT) {
+        const uint32_t Wt = (uint32_t)sh_w[i];
+        if (Wt >= wstar) {
+          const uint32_t o = atomicAdd(&s_ncand, 1u);
+          if (o < (uint32_t)kFlatCand) {
+            cand_key[o] = sh_key[i];
+            cand_w[o] = Wt;
+          }
+        }
+      }
+      __syncthreads();
+      fast_emit = s_ncand <= (uint32_t)kFlatCand;
+    }
+    if (fast_emit) {
+      // one candidate per thread (kFlatCand <= NT): whether it is kept (an
+      // equal-weight one is kept when fewer than take_eq equal-weight
+      // candidates precede it), then its row among the kept ones
+      const uint32_t nc = s_ncand;
+      const uint32_t i = (uint32_t)tid;
+      const uint32_t key = i < nc ? cand_key[i] : 0u, Wt = i < nc ? cand_w[i] : 0u;
+      bool keep = i < nc && Wt > wstar;
+      if (i < nc && !keep) {
+        uint32_t before = 0;
+        for (uint32_t j = 0; j < nc; ++j) before += (cand_w[j] == wstar && cand_key[j] < key) ? 1u : 0u;
+        keep = before < take_eq;
+      }
+      __syncthreads();
+      if (keep) cand_key[i] = key | 0x80000000u;
+      __syncthreads();
+      if (keep) {
+        const uint32_t kf = key | 0x80000000u;
+        uint32_t o = 1;
+        for (uint32_t j = 0; j < nc; ++j) o += cand_key[j] < kf && (cand_key[j] & 0x80000000u) ? 1u : 0u;
+        if (o < (uint32_t)FC_MAX_TREE_ROWS) {
+          s_sel_p[o] = (uint16_t)(key >> 5);
+          s_sel_d[o] = (uint8_t)(key & 31u);
+          s_sel_w[o] = Wt;
+        }
+      }
+      nsel = (int)(need < (uint32_t)c ? need : (uint32_t)c);
+    } else {
+      uint32_t gt = 0, eq = 0;
+      if (need > 0)
+        walk(
+            [&](int, int lo, int hi, uint32_t Wt) {
+              gt += Wt > wstar ? (uint32_t)(hi - lo) : 0u;
+              eq += Wt == wstar ? (uint32_t)(hi - lo) : 0u;
+            },
+            [&](int, int, uint32_t Wt) {
+              gt += Wt > wstar ? 1u : 0u;
+              eq += Wt == wstar ? 1u : 0u;
+            });
+      uint32_t gt_ex, eq_ex, gt_tot, eq_tot;
+      Scan2<NT>::run(gt, eq, s_x, s_y, &gt_ex, &eq_ex, &gt_tot, &eq_tot);
+      if (need > 0 && (gt + eq) > 0) {
+        const uint32_t keq = take_eq > eq_ex ? (take_eq - eq_ex < eq ? take_eq - eq_ex : eq) : 0u;
+        uint32_t o = 1 + gt_ex + (eq_ex < take_eq ? eq_ex : take_eq) + gt + keq;
+        uint32_t eq_left = eq;
+        auto emit = [&](int q, int d, uint32_t Wt) {
+          bool keep = Wt > wstar;
+          if (Wt == wstar) keep = --eq_left < keq;
+          if (keep) {
+            --o;
+            if (o < (uint32_t)FC_MAX_TREE_ROWS) {
+              s_sel_p[o] = (uint16_t)q;
+              s_sel_d[o] = (uint8_t)d;
+              s_sel_w[o] = Wt;
+            }
+          }
+        };
+        walk(
+            [&](int q, int lo, int hi, uint32_t Wt) {
+              if (Wt >= wstar)
+                for (int d = hi; d > lo; --d) emit(q, d, Wt);
+            },
+            emit);
+      }
+      const uint32_t total_sel = need > 0 ? gt_tot + (eq_tot < take_eq ? eq_tot : take_eq) : 0;
+      nsel = (int)(total_sel < (uint32_t)c ? total_sel : (uint32_t)c);
+    }
+    if (tid == 0) s_sel_d[0] = 0;
+    __syncthreads();
+    // 8. parent of row r: the last row before it one level shallower (rows
+    //    are in preorder and the kept set is ancestor-closed), from per-depth
+    //    ballots of the first four waves' rows
+    if (tid < FC_MAX_TREE_ROWS) {
+      const int g = tid / fc::kWave;
+      const int d = tid <= nsel ? (int)s_sel_d[tid] : -1;
+#pragma unroll
+      for (int D = 0; D < MAXM; ++D) {
+        const uint64_t bl = fc::ballot(d == D);
+        if (lane == 0) s_dball[g][D] = bl;
+      }
+    }
+    __syncthreads();
+    if (tid >= 1 && tid <= nsel) {
+      const int g = tid / fc::kWave;
+      const int D = (int)s_sel_d[tid] - 1;
+      uint64_t bl = s_dball[g][D] & fc::lanemask_lt();
+      int gg = g;
+      while (bl == 0 && gg > 0) bl = s_dball[--gg][D];
+      s_par[tid] = bl ? (int16_t)(gg * fc::kWave + 63 - __builtin_clzll(bl)) : (int16_t)0;
+    }
+    if (tid == 0) s_par[0] = -1;
+    __syncthreads();
+  }
+
+  // 9. rows, then the mask: row j's subtree is the run of rows from j up to
+  //    the next row at j's depth or shallower, so A[i][j] = [j <= i < end(j)]
+  const int num = err ? 0 : 1 + nsel;
+  for (int r = tid; r < R; r += NT) {
+    const int64_t out = (int64_t)b * R + r;
+    int32_t tk = 0, pr = -1, ps = 0;
+    uint32_t wt = 0;
+    if (r < num) {
+      if (r == 0) {
+        tk = root_tok;
+        wt = root_w;
+      } else {
+        const int p = s_sel_p[r];
+        const int d = s_sel_d[r];
+        tk = cont_tok[(row0 + perm[p]) * m + d - 1];
+        pr = s_par[r];
+        wt = s_sel_w[r];
+        ps = d;
+      }
+    }
+    node_tok[out] = tk;
+    parent[out] = pr;
+    weight[out] = wt;
+    pos_ids[out] = ps;
+  }
+  for (int g = w; g * fc::kWave < num; g += NW) {
+    const int r = g * fc::kWave + lane;
+    const int d = r < num ? (int)s_sel_d[r] : MAXM + 1;
+#pragma unroll
+    for (int D = 0; D <= MAXM; ++D) {
+      const uint64_t bl = fc::ballot(d <= D);
+      if (lane == 0) s_shallow[g][D] = bl;
+    }
+  }
+  __syncthreads();
+  for (int r = tid; r < num; r += NT) {
+    const int g = r / fc::kWave, d = s_sel_d[r];
+    uint64_t bl = s_shallow[g][d] & ~((2ull << (r % fc::kWave)) - 1ull);
+    int gg = g;
+    while (bl == 0 && (gg + 1) * fc::kWave < num) bl = s_shallow[++gg][d];
+    s_end[r] = (int16_t)(bl ? gg * fc::kWave + __builtin_ctzll(bl) : num);
+  }
+  __syncthreads();
+  const int64_t mbase = (int64_t)b * R * R;
+  const int col = tid % R, row_step = NT / R;
+  if (tid / R < row_step) {
+    const int end_j = col < num ? (int)s_end[col] : -1;
+    for (int i = tid / R; i < R; i += row_step)
+      mask[mbase + (int64_t)i * R + col] = (col <= i && i < end_j) ? 1 : 0;
+  }
+  if (tid == 0) num_nodes[b] = err ? -1 : num;
+}
+
+// Per-device facts the launches need, looked up once per device: the LDS a
+// workgroup may use, and each kernel's own static LDS (the dynamic limit of
+// every kernel is raised once to what the device allows).
+struct TreeDevice {
+  bool ready = false;
+  int max_lds = 0;
+  size_t flat_static[2][2] = {{0, 0}, {0, 0}};  // [MAXM 10/16][NARROW]
+  size_t full_static[2][2] = {{0, 0}, {0, 0}};  // the full-LDS kernel, same indexes
+  size_t any_static = 0;
+};
+
+std::mutex g_tree_mu;
+TreeDevice g_tree_dev[64];
+
+template <typename K>
+size_t raise_lds(K kernel, int max_lds) {
+  hipFuncAttributes at{};
+  if (hipFuncGetAttributes(&at, (const void*)kernel) != hipSuccess) {
+    (void)hipGetLastError();
+    return (size_t)max_lds;
+  }
+  const int dyn = max_lds - (int)at.sharedSizeBytes;
+  if (dyn > 0) (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, dyn);
+  (void)hipGetLastError();
+  return at.sharedSizeBytes;
+}
+
+const TreeDevice* tree_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_tree_mu);
+  TreeDevice& d = g_tree_dev[dev];
+  if (!d.ready) {
+    if (hipDeviceGetAttribute(&d.max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    d.flat_static[0][1] = raise_lds(k_tree_flat<10, true>, d.max_lds);
+    d.flat_static[0][0] = raise_lds(k_tree_flat<10, false>, d.max_lds);
+    d.flat_static[1][1] = raise_lds(k_tree_flat<16, true>, d.max_lds);
+    d.flat_static[1][0] = raise_lds(k_tree_flat<16, false>, d.max_lds);
+    raise_lds(k_tree_fast<256, 10, true>, d.max_lds);
+    raise_lds(k_tree_fast<256, 10, false>, d.max_lds);
+    raise_lds(k_tree_fast<256, 16, true>, d.max_lds);
+    raise_lds(k_tree_fast<256, 16, false>, d.max_lds);
+    d.full_static[0][1] = raise_lds(k_tree_fast<1024, 10, true>, d.max_lds);
+    d.full_static[0][0] = raise_lds(k_tree_fast<1024, 10, false>, d.max_lds);
+    d.full_static[1][1] = raise_lds(k_tree_fast<1024, 16, true>, d.max_lds);
+    d.full_static[1][0] = raise_lds(k_tree_fast<1024, 16, false>, d.max_lds);
+    d.any_static = raise_lds(k_tree_any, d.max_lds);
+    d.ready = true;
+  }
+  return &d;
+}
+
+// Row loads of the two-launch path: 16-byte vectors when every query's
+// block of rows is 16-byte aligned, else 32-bit words when 4-byte aligned,
+// else single tokens.
+int block_words(const uint16_t* cont_tok, int32_t k, int32_t m) {
+  if ((((uintptr_t)cont_tok) & 15) == 0 && ((size_t)k * m) % 8 == 0) return 2;
+  if ((((uintptr_t)cont_tok) & 3) == 0 && ((size_t)k * m) % 2 == 0) return 1;
+  return 0;
+}
+
 template <int MAXM, bool NARROW>
 fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok, const uint16_t* ctx,
                       int32_t B, int32_t L, int32_t S, int32_t k, int32_t m, fc_tree_params t, Alpha a,
@@ -1089,28 +2015,58 @@ fc_status launch_fast(const int32_t* taken, const uint8_t* cont_len, const uint1
   const int t_small = k < kSmallClass ? k : kSmallClass;
   int32_t* lists = (int32_t*)ws;
   int32_t* counts = lists + 2 * (size_t)B;
-  // row loads: 16-byte vectors when every query's row is 16-byte aligned,
-  // else 32-bit words when 4-byte aligned, else single tokens
-  int words = 0;
-  if ((((uintptr_t)cont_tok) & 15) == 0 && ((size_t)k * m) % 8 == 0) words = 2;
-  else if ((((uintptr_t)cont_tok) & 3) == 0 && ((size_t)k * m) % 2 == 0) words = 1;
+  const int words = block_words(cont_tok, k, m);
   const TreeLayout small = tree_layout(t_small, m, true);
-  if (small.total > 64 * 1024)
-    (void)hipFuncSetAttribute((const void*)k_tree_fast<256, MAXM, NARROW>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)small.total);
   (void)hipGetLastError();
   hipLaunchKernelGGL((k_tree_fast<256, MAXM, NARROW>), dim3(B + 1), dim3(256), small.total, stream, taken, cont_len,
                      cont_tok, ctx, L, S, k, m, t.c, a, nullptr, nullptr, lists + B, counts + 1, B, t_small, words,
                      rows, n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
   FC_CHECK_LAUNCH();
   if (k > t_small) {
-    if (full.total > 64 * 1024)
-      (void)hipFuncSetAttribute((const void*)k_tree_fast<1024, MAXM, NARROW>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)full.total);
-    (void)hipGetLastError();
     hipLaunchKernelGGL((k_tree_fast<1024, MAXM, NARROW>), dim3(B), dim3(1024), full.total, stream, taken, cont_len,
                        cont_tok, ctx, L, S, k, m, t.c, a, lists + B, counts + 1, nullptr, nullptr, B, k, words, rows,
                        n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
+    FC_CHECK_LAUNCH();
+  }
+  return FC_OK;
+}
+
+// The flat path when its layout fits (with as many short strings as a query
+// can have, or else as many as fit, the rest of the queries going to the
+// full-LDS kernel through a list); returns FC_ERR_UNSUPPORTED when it does
+// not apply, before launching anything.
+template <int MAXM, bool NARROW>
+fc_status launch_flat(const int32_t* taken, const uint8_t* cont_len, const uint16_t* cont_tok, const uint16_t* ctx,
+                      int32_t B, int32_t L, int32_t S, int32_t k, int32_t m, fc_tree_params t, Alpha a,
+                      const TreeLayout& full, const TreeDevice& dv, int32_t* num_nodes, int32_t* node_tok,
+                      int32_t* parent, uint32_t* weight, int32_t* pos_ids, int32_t* mask, const int32_t* rows,
+                      int32_t n_rows, void* ws, hipStream_t stream) {
+  const size_t stat = dv.flat_static[MAXM == 10 ? 0 : 1][NARROW ? 1 : 0];
+  if (stat >= (size_t)dv.max_lds) return FC_ERR_UNSUPPORTED;
+  const size_t budget = (size_t)dv.max_lds - stat;
+  const int worst_short = k - (k + S - 1) / S;  // the long store holds at least ceil(T / S)
+  // LDS for every possible short list would cost occupancy for nothing:
+  // queries past the cap (none in typical batches: a second store's list
+  // is short) go to the full-LDS kernel
+  int cap = worst_short < kFlatShortCap ? worst_short : kFlatShortCap;
+  while (cap > 0 && flat_layout(k, MAXM, cap, S, !NARROW).total > budget) cap = cap * 7 / 8;
+  const FlatLayout lay = flat_layout(k, MAXM, cap, S, !NARROW);
+  if (lay.total > budget) return FC_ERR_UNSUPPORTED;
+  const bool defer = cap < worst_short;
+  if (defer && full.total + dv.full_static[MAXM == 10 ? 0 : 1][NARROW ? 1 : 0] > (size_t)dv.max_lds)
+    return FC_ERR_UNSUPPORTED;
+  int32_t* lists = (int32_t*)ws;
+  int32_t* counts = lists + 2 * (size_t)B;
+  const int words = ((((uintptr_t)cont_tok) & 3) == 0 && (m % 2) == 0) ? 1 : 0;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL((k_tree_flat<MAXM, NARROW>), dim3(B + (defer ? 1 : 0)), dim3(kFlatThreads), lay.total, stream,
+                     taken, cont_len, cont_tok, ctx, L, S, k, m, t.c, a, cap, words, lists, counts, B, rows, n_rows,
+                     num_nodes, node_tok, parent, weight, pos_ids, mask);
+  FC_CHECK_LAUNCH();
+  if (defer) {
+    hipLaunchKernelGGL((k_tree_fast<1024, MAXM, NARROW>), dim3(B), dim3(1024), full.total, stream, taken, cont_len,
+                       cont_tok, ctx, L, S, k, m, t.c, a, lists, counts, nullptr, nullptr, B, k,
+                       block_words(cont_tok, k, m), rows, n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
     FC_CHECK_LAUNCH();
   }
   return FC_OK;
@@ -1137,17 +2093,28 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
     return FC_ERR_INVALID;
   if (rows && n_rows < 1) return FC_ERR_INVALID;
   if (!ws || ws_bytes < fc_build_tree_workspace_bytes(B)) return FC_ERR_WORKSPACE;
-  int dev = 0, max_lds = 0;
-  FC_CHECK_HIP(hipGetDevice(&dev));
-  FC_CHECK_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
-  const size_t static_lds = 7 * 1024;
+  const TreeDevice* dv = tree_device();
+  if (!dv) return FC_ERR_DEVICE;
   Alpha a = {};
   for (int s = 0; s < S; ++s) a.a[s] = t.alpha[s];
   const TreeLayout full = tree_layout(k, m);
-  if (full.total + static_lds > (size_t)max_lds) return FC_ERR_UNSUPPORTED;
-  (void)hipGetLastError();
   bool narrow = (uint64_t)t.alpha[0] * (uint64_t)k <= 0xFFFFull;
   for (int s = 1; s < S; ++s) narrow = narrow && t.alpha[s] == t.alpha[0];
+  fc_status st = FC_ERR_UNSUPPORTED;
+#define FC_FLAT(MM, NN)                                                                                              \
+  st = launch_flat<MM, NN>(taken, cont_len, cont_tok, ctx, B, L, S, k, m, t, a, full, *dv, num_nodes, node_tok,      \
+                           parent, weight, pos_ids, mask, rows, n_rows, ws, stream)
+  if (m <= 10) {
+    if (narrow) FC_FLAT(10, true);
+    else FC_FLAT(10, false);
+  } else if (m <= 16) {
+    if (narrow) FC_FLAT(16, true);
+    else FC_FLAT(16, false);
+  }
+#undef FC_FLAT
+  if (st != FC_ERR_UNSUPPORTED) return st;
+  const size_t static_lds = m <= 16 ? dv->full_static[m <= 10 ? 0 : 1][narrow ? 1 : 0] : dv->any_static;
+  if (full.total + static_lds > (size_t)dv->max_lds) return FC_ERR_UNSUPPORTED;
 #define FC_FAST(MM, NN)                                                                                              \
   return launch_fast<MM, NN>(taken, cont_len, cont_tok, ctx, B, L, S, k, m, t, a, full, num_nodes, node_tok, parent, \
                              weight, pos_ids, mask, rows, n_rows, ws, stream)
@@ -1160,8 +2127,6 @@ extern "C" fc_status fc_build_tree(const int32_t* taken, const uint8_t* cont_len
     FC_FAST(16, false);
   }
 #undef FC_FAST
-  if (full.total > 64 * 1024)
-    (void)hipFuncSetAttribute((const void*)k_tree_any, hipFuncAttributeMaxDynamicSharedMemorySize, (int)full.total);
   (void)hipGetLastError();
   hipLaunchKernelGGL(k_tree_any, dim3(B), dim3(kTreeThreads), full.total, stream, taken, cont_len, cont_tok, ctx, L,
                      S, k, m, t.c, a, rows, n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);

@@ -652,15 +652,15 @@ def _sorted_slots(rng, T: int, m: int, vocab: int) -> tuple:
     return lens, toks
 
 
-def _largest_k(m: int) -> int:
-    """The largest k whose LDS layout the tree kernels accept for m (found
-    through the entry point itself: past it the call is refused before any
-    launch)."""
+def _largest_k(m: int, S: int, alpha) -> int:
+    """The largest k whose LDS layouts the tree kernels accept for m, S
+    stores and these store weights (found through the entry point itself:
+    past it the call is refused before any launch)."""
     def ok(k):
-        taken = dev(np.zeros((1, 1), np.int32))
+        taken = dev(np.zeros((1, S), np.int32))
         try:
             fc.fc_build_tree(taken, dev(np.zeros((1, k), np.uint8)), dev(np.zeros((1, k, m), np.uint16)),
-                             dev(np.ones((1, 2), np.uint16)), c=4, alpha=(1,))
+                             dev(np.ones((1, 2), np.uint16)), c=4, alpha=alpha)
             return True
         except fc.FcError as e:
             assert "UNSUPPORTED" in str(e), e
@@ -679,15 +679,18 @@ def _largest_k(m: int) -> int:
 @pytest.mark.parametrize("m", [2, 10, 255])
 def test_tree_at_maximum_sizes(m):
     """c = 255 (256 rows: four row groups), k at the largest LDS layout the
-    kernels take for m (up to ~12,000 slots: a dozen positions per thread in
-    the heavy launch; m = 255 is the general kernel), two stores with
-    unequal weights and with equal ones; k + 1 is refused."""
+    kernels take for m and two stores (about 12,000 slots; for m = 2 the
+    one-workgroup layout cannot hold half of them as short strings, so the
+    evenly split queries go to the full-LDS kernel through its list; m = 255
+    is the general kernel), with unequal weights and with equal ones (unequal
+    weights need a larger layout, so k is the largest they take); k + 1 is
+    refused."""
     torch.cuda.synchronize()
-    k = _largest_k(m)
+    c, S, B = 255, 2, 5
+    k = _largest_k(m, S, (3, 1))
     say(f"tree maximum sizes m={m}: k={k}")
     assert k >= 200
     rng = np.random.default_rng(m)
-    c, S, B = 255, 2, 5
     totals = [k, k - 1, min(k, 300), min(k, 257), 2]
     taken = np.zeros((B, S), np.int32)
     lens = np.zeros((B, k), np.uint8)
@@ -710,8 +713,8 @@ def test_tree_at_maximum_sizes(m):
         if m >= 10:
             assert (o["num_nodes"][:2] == c + 1).all()
     with pytest.raises(fc.FcError):
-        fc.fc_build_tree(dev(np.zeros((1, 1), np.int32)), dev(np.zeros((1, k + 1), np.uint8)),
-                         dev(np.zeros((1, k + 1, m), np.uint16)), dev(np.ones((1, 2), np.uint16)), c=c, alpha=(1,))
+        fc.fc_build_tree(dev(np.zeros((1, S), np.int32)), dev(np.zeros((1, k + 1), np.uint8)),
+                         dev(np.zeros((1, k + 1, m), np.uint16)), dev(np.ones((1, 2), np.uint16)), c=c, alpha=(3, 1))
 
 
 def test_repeat_runs_are_identical():
