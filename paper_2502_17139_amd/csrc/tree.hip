@@ -1227,6 +1227,18 @@ __device__ __forceinline__ int cmp_words(const uint32_t (&a)[W], int la, const u
   return la < lb ? -1 : (la > lb ? 1 : 0);
 }
 
+// A continuation row and its length straight from the retrieval output (the
+// rare case of a short list too long for LDS).
+template <int MAXM>
+__device__ __forceinline__ int global_row(const uint16_t* __restrict__ cont_tok,
+                                                    const uint8_t* __restrict__ cont_len, int64_t slot, int m,
+                                                    int words, uint32_t (&v)[MAXM / 2]) {
+  int len = cont_len[slot];
+  len = len < m ? len : m;
+  load_row_words<MAXM>(cont_tok + slot * m, m, len, words != 0, v);
+  return len;
+}
+
 template <int W>
 __device__ __forceinline__ void lds_row(const uint32_t* __restrict__ sstr, int ci, uint32_t (&v)[W]) {
 #pragma unroll
@@ -1236,18 +1248,64 @@ __device__ __forceinline__ void lds_row(const uint32_t* __restrict__ sstr, int c
 // Strings of the LDS rows [lo, hi) that precede string (v, len) in merged
 // order: those <= it when their store comes first on ties (upper), those
 // < it otherwise.
-template <int W>
-__device__ __forceinline__ int count_before(const uint32_t* __restrict__ sstr, const uint8_t* __restrict__ slen, int lo,
-                                            int hi, const uint32_t (&v)[W], int len, bool upper) {
+template <int W, typename Row>
+__device__ __forceinline__ int count_before(Row row, int lo, int hi, const uint32_t (&v)[W], int len, bool upper) {
   const int base = lo;
   while (lo < hi) {
     const int mid = (lo + hi) >> 1;
     uint32_t r[W];
-    lds_row<W>(sstr, mid, r);
-    const int cc = cmp_words<W>(r, slen[mid], v, len);
+    const int rl = row(mid, r);
+    const int cc = cmp_words<W>(r, rl, v, len);
     if (upper ? cc <= 0 : cc < 0) lo = mid + 1; else hi = mid;
   }
   return lo - base;
+}
+
+// The flat kernel's workgroup order: queries of 2,048 kept slots or more
+// first, then those above 256, then the rest, each class in query order, so
+// that the first round of workgroups spreads the heaviest queries over the
+// CUs instead of letting a few CUs draw several.  With three stores or more,
+// the queries whose short lists exceed the flat layout (cap) come last and
+// are also listed for the full-LDS kernel.
+constexpr int kPlanThreads = 1024;
+
+__global__ void __launch_bounds__(kPlanThreads) k_tree_plan(const int32_t* __restrict__ taken, int S, int k,
+                                                           const int32_t* __restrict__ rows, int n_rows, int B,
+                                                           int cap, int32_t* __restrict__ order,
+                                                           int32_t* __restrict__ defer_list,
+                                                           int32_t* __restrict__ defer_count) {
+  constexpr int NT = kPlanThreads;
+  constexpr int NW = NT / fc::kWave;
+  __shared__ uint32_t s_x[NW + 1], s_y[NW + 1];
+  const int tid = threadIdx.x;
+  auto cls = [&](int q) -> int {
+    const QueryShape qs = query_shape(taken, S, k, rows, n_rows, q);
+    if (S > 2 && !qs.bad && qs.T - qs.n_long > cap) return 3;
+    return qs.T >= 2048 ? 0 : qs.T > 256 ? 1 : 2;
+  };
+  const int per = (B + NT - 1) / NT;
+  const int q0 = tid * per < B ? tid * per : B;
+  const int q1 = q0 + per < B ? q0 + per : B;
+  uint32_t n[4] = {0, 0, 0, 0};
+  for (int q = q0; q < q1; ++q) {
+    const int c = cls(q);
+    n[0] += c == 0;
+    n[1] += c == 1;
+    n[2] += c == 2;
+    n[3] += c == 3;
+  }
+  uint32_t e[4], t[4];
+  Scan2<NT>::run(n[0], n[1], s_x, s_y, &e[0], &e[1], &t[0], &t[1]);
+  Scan2<NT>::run(n[2], n[3], s_x, s_y, &e[2], &e[3], &t[2], &t[3]);
+  uint32_t o[4] = {e[0], t[0] + e[1], t[0] + t[1] + e[2], t[0] + t[1] + t[2] + e[3]};
+  uint32_t d = e[3];
+  for (int q = q0; q < q1; ++q) {
+    const int c = cls(q);
+    const uint32_t at = c == 0 ? o[0]++ : c == 1 ? o[1]++ : c == 2 ? o[2]++ : o[3]++;
+    order[at] = q;
+    if (c == 3 && defer_list) defer_list[d++] = q;
+  }
+  if (tid == 0 && defer_count) *defer_count = (int32_t)t[3];
 }
 
 template <int MAXM, bool NARROW>
@@ -1256,8 +1314,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
                                                             const uint16_t* __restrict__ cont_tok,
                                                             const uint16_t* __restrict__ ctx, int L, int S, int k,
                                                             int m, int c, Alpha alpha, int cap, int words,
-                                                            int32_t* __restrict__ defer_list,
-                                                            int32_t* __restrict__ defer_count, int B,
+                                                            const int32_t* __restrict__ order, int B,
                                                             const int32_t* __restrict__ rows, int n_rows,
                                                             int32_t* __restrict__ num_nodes,
                                                             int32_t* __restrict__ node_tok,
@@ -1293,22 +1350,10 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   const int tid = threadIdx.x;
   const int lane = fc::lane_id();
   const int w = tid / fc::kWave;
-  auto deferred = [&](const QueryShape& qs) { return !qs.bad && qs.T - qs.n_long > cap; };
-  if ((int)blockIdx.x == B) {
-    // the list of queries left to the general kernel, in query order
-    const int per = (B + NT - 1) / NT;
-    const int q0 = tid * per < B ? tid * per : B;
-    const int q1 = q0 + per < B ? q0 + per : B;
-    uint32_t nd = 0;
-    for (int q = q0; q < q1; ++q) nd += deferred(query_shape(taken, S, k, rows, n_rows, q)) ? 1u : 0u;
-    uint32_t ed, dummy, td, dummy2;
-    Scan2<NT>::run(nd, 0u, s_x, s_y, &ed, &dummy, &td, &dummy2);
-    for (int q = q0; q < q1; ++q)
-      if (deferred(query_shape(taken, S, k, rows, n_rows, q))) defer_list[ed++] = q;
-    if (tid == 0) *defer_count = (int32_t)td;
-    return;
-  }
-  const int b = (int)blockIdx.x;
+  // with three stores or more, short lists past the LDS cap go to the
+  // full-LDS kernel; with two, they are searched in place (slower, rare)
+  auto deferred = [&](const QueryShape& qs) { return S > 2 && !qs.bad && qs.T - qs.n_long > cap; };
+  const int b = order ? order[blockIdx.x] : (int)blockIdx.x;
   const QueryShape qs = query_shape(taken, S, k, rows, n_rows, b);
   if (deferred(qs)) return;
   const int R = c + 1;
@@ -1399,6 +1444,16 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   };
   const bool alpha_flat = NARROW || ((S < 2 || alpha.a[1] == alpha.a[0]) && (S < 3 || alpha.a[2] == alpha.a[0]) &&
                                      (S < 4 || alpha.a[3] == alpha.a[0]));
+  // short string ci (its row as words and its length): from LDS, or, past
+  // the cap (two stores only), from the retrieval output itself
+  const bool in_lds = n_short <= cap;
+  auto srow = [&](int ci, uint32_t (&v)[W]) -> int {
+    if (in_lds) {
+      lds_row<W>(sstr, ci, v);
+      return slen[ci];
+    }
+    return global_row<MAXM>(cont_tok, cont_len, row0 + short_slot(ci), m, words, v);
+  };
 
   // 1. the short strings into LDS, each store's order checked; with three
   //    or more stores, their merged order among themselves
@@ -1409,6 +1464,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     const int slot = short_slot(ci);
     int len = cont_len[row0 + slot];
     if (len > m) s_err = 1;
+    if (!in_lds) continue;
     len = len < m ? len : m;
     uint32_t v[W];
     load_row_words<MAXM>(cont_tok + (row0 + slot) * m, m, len, words != 0, v);
@@ -1421,19 +1477,18 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     const int s = short_store(ci);
     const int i = ci - s_cs[s];
     uint32_t v[W];
-    lds_row<W>(sstr, ci, v);
-    const int len = slen[ci];
+    const int len = srow(ci, v);
     if (i > 0) {
       uint32_t pv[W];
-      lds_row<W>(sstr, ci - 1, pv);
-      if (cmp_words<W>(pv, slen[ci - 1], v, len) > 0) s_err = 1;
+      const int plen = srow(ci - 1, pv);
+      if (cmp_words<W>(pv, plen, v, len) > 0) s_err = 1;
     }
     if (S > 2) {
       int pos = i;
 #pragma unroll
       for (int u = 0; u < FC_MAX_SOURCES; ++u)
         if (u < S && u != sL && u != s && qs.tk[u] > 0)
-          pos += count_before<W>(sstr, slen, s_cs[u], s_cs[u] + qs.tk[u], v, len, u < s);
+          pos += count_before<W>(srow, s_cs[u], s_cs[u] + qs.tk[u], v, len, u < s);
       sidx[pos] = (uint16_t)ci;
     }
   }
@@ -1445,74 +1500,86 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   //    consecutive long strings per pass and its lane 0 the string before
   //    them, so every predecessor comes from the lane below; kFlatRows
   //    passes have their loads in flight together.
-  auto rank_short = [&](const uint32_t (&v)[W], int len) -> int {
-    int r = 0;
-#pragma unroll
-    for (int u = 0; u < FC_MAX_SOURCES; ++u)
-      if (u < S && u != sL && qs.tk[u] > 0)
-        r += count_before<W>(sstr, slen, s_cs[u], s_cs[u] + qs.tk[u], v, len, u < sL);
-    return r;
+  auto lds_srow = [&](int ci, uint32_t (&v)[W]) -> int {
+    lds_row<W>(sstr, ci, v);
+    return slen[ci];
   };
   const int lslot0 = s_seg[sL];
   constexpr int kPass = NW * (fc::kWave - 1);  // long strings per pass of the block
-  for (int j0 = 0; j0 < nL; j0 += kPass * kFlatRows) {
-    uint32_t v[kFlatRows][W];
-    int len[kFlatRows];
+  // one pass over the long strings with the short strings read through
+  // `row` (compiled twice, so the common LDS case carries no registers of
+  // the in-place one)
+  auto long_pass = [&](auto&& row) {
+    auto rank_short = [&](const uint32_t (&v)[W], int len) -> int {
+      int r = 0;
 #pragma unroll
-    for (int u = 0; u < kFlatRows; ++u) {
-      const int j = j0 + u * kPass + w * (fc::kWave - 1) + lane - 1;
-      len[u] = 0;
-      if (j >= 0 && j < nL) {
-        len[u] = cont_len[row0 + lslot0 + j];
-        const uint16_t* src = cont_tok + (row0 + lslot0 + j) * m;
-        if (words) {
-          const uint32_t* s32 = (const uint32_t*)src;
+      for (int u = 0; u < FC_MAX_SOURCES; ++u)
+        if (u < S && u != sL && qs.tk[u] > 0) r += count_before<W>(row, s_cs[u], s_cs[u] + qs.tk[u], v, len, u < sL);
+      return r;
+    };
+    for (int j0 = 0; j0 < nL; j0 += kPass * kFlatRows) {
+      uint32_t v[kFlatRows][W];
+      int len[kFlatRows];
 #pragma unroll
-          for (int x = 0; x < W; ++x) v[u][x] = 2 * x < m ? s32[x] : 0u;
+      for (int u = 0; u < kFlatRows; ++u) {
+        const int j = j0 + u * kPass + w * (fc::kWave - 1) + lane - 1;
+        len[u] = 0;
+        if (j >= 0 && j < nL) {
+          len[u] = cont_len[row0 + lslot0 + j];
+          const uint16_t* src = cont_tok + (row0 + lslot0 + j) * m;
+          if (words) {
+            const uint32_t* s32 = (const uint32_t*)src;
+#pragma unroll
+            for (int x = 0; x < W; ++x) v[u][x] = 2 * x < m ? s32[x] : 0u;
+          } else {
+#pragma unroll
+            for (int x = 0; x < W; ++x) {
+              const uint32_t a0 = 2 * x < m ? src[2 * x] : 0u;
+              const uint32_t a1 = 2 * x + 1 < m ? src[2 * x + 1] : 0u;
+              v[u][x] = a0 | (a1 << 16);
+            }
+          }
         } else {
 #pragma unroll
-          for (int x = 0; x < W; ++x) {
-            const uint32_t a0 = 2 * x < m ? src[2 * x] : 0u;
-            const uint32_t a1 = 2 * x + 1 < m ? src[2 * x + 1] : 0u;
-            v[u][x] = a0 | (a1 << 16);
+          for (int x = 0; x < W; ++x) v[u][x] = 0u;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kFlatRows; ++u) {
+        const int j = j0 + u * kPass + w * (fc::kWave - 1) + lane - 1;
+        const bool have = j >= 0 && j < nL;
+        if (have && len[u] > m) s_err = 1;
+        const int ln = len[u] < m ? len[u] : m;
+#pragma unroll
+        for (int x = 0; x < W; ++x) v[u][x] &= (2 * x < ln ? 0xFFFFu : 0u) | (2 * x + 1 < ln ? 0xFFFF0000u : 0u);
+        const int r = have && n_short > 0 ? rank_short(v[u], ln) : 0;
+        uint32_t pv[W];
+#pragma unroll
+        for (int x = 0; x < W; ++x) pv[x] = (uint32_t)__shfl_up((int)v[u][x], 1, fc::kWave);
+        const int plen = __shfl_up(ln, 1, fc::kWave);
+        const int pr = __shfl_up(r, 1, fc::kWave);
+        if (have && lane > 0) {
+          if (j > 0 && cmp_words<W>(pv, plen, v[u], ln) > 0) s_err = 1;
+          int l = 0;
+          if (j > 0 && pr == r) {
+            l = lcp_words<W>(pv, plen, v[u], ln);
+          } else if (r > 0) {
+            const int ci = S > 2 ? (int)sidx[r - 1] : r - 1;
+            uint32_t sv[W];
+            const int sl = row(ci, sv);
+            l = lcp_words<W>(sv, sl, v[u], ln);
           }
+          const int P = j + r;
+          perm[P] = (uint16_t)(lslot0 + j);
+          lm[P] = (LMT)((uint32_t)l | ((uint32_t)ln << kSh));
         }
-      } else {
-#pragma unroll
-        for (int x = 0; x < W; ++x) v[u][x] = 0u;
       }
     }
-#pragma unroll
-    for (int u = 0; u < kFlatRows; ++u) {
-      const int j = j0 + u * kPass + w * (fc::kWave - 1) + lane - 1;
-      const bool have = j >= 0 && j < nL;
-      if (have && len[u] > m) s_err = 1;
-      const int ln = len[u] < m ? len[u] : m;
-#pragma unroll
-      for (int x = 0; x < W; ++x) v[u][x] &= (2 * x < ln ? 0xFFFFu : 0u) | (2 * x + 1 < ln ? 0xFFFF0000u : 0u);
-      const int r = have && n_short > 0 ? rank_short(v[u], ln) : 0;
-      uint32_t pv[W];
-#pragma unroll
-      for (int x = 0; x < W; ++x) pv[x] = (uint32_t)__shfl_up((int)v[u][x], 1, fc::kWave);
-      const int plen = __shfl_up(ln, 1, fc::kWave);
-      const int pr = __shfl_up(r, 1, fc::kWave);
-      if (have && lane > 0) {
-        if (j > 0 && cmp_words<W>(pv, plen, v[u], ln) > 0) s_err = 1;
-        int l = 0;
-        if (j > 0 && pr == r) {
-          l = lcp_words<W>(pv, plen, v[u], ln);
-        } else if (r > 0) {
-          const int ci = S > 2 ? (int)sidx[r - 1] : r - 1;
-          uint32_t sv[W];
-          lds_row<W>(sstr, ci, sv);
-          l = lcp_words<W>(sv, slen[ci], v[u], ln);
-        }
-        const int P = j + r;
-        perm[P] = (uint16_t)(lslot0 + j);
-        lm[P] = (LMT)((uint32_t)l | ((uint32_t)ln << kSh));
-      }
-    }
-  }
+  };
+  if (in_lds) long_pass(lds_srow);
+  else long_pass([&](int ci, uint32_t (&v)[W]) -> int {
+    return global_row<MAXM>(cont_tok, cont_len, row0 + short_slot(ci), m, words, v);
+  });
   __syncthreads();
 
   // 3. the free merged positions take the short strings in order
@@ -1545,14 +1612,13 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       }
       const int ci = S > 2 ? (int)sidx[g] : g;
       uint32_t v[W];
-      lds_row<W>(sstr, ci, v);
-      const int len = slen[ci];
+      const int len = srow(ci, v);
       int l = 0;
       if (p > 0 && prev_gap) {
         const int pci = S > 2 ? (int)sidx[g - 1] : g - 1;
         uint32_t pv[W];
-        lds_row<W>(sstr, pci, pv);
-        l = lcp_words<W>(pv, slen[pci], v, len);
+        const int pl = srow(pci, pv);
+        l = lcp_words<W>(pv, pl, v, len);
       } else if (p > 0) {
         uint32_t pv[W];
         load_row_words<MAXM>(cont_tok + (row0 + prev_slot) * m, m, (int)prev_len, words != 0, pv);
@@ -1768,12 +1834,16 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     //    than W* (the usual case) the kept nodes are shared ones: they are
     //    gathered as candidates (weight >= W*), each learns how many
     //    candidates precede it, and the first take_eq of weight W* are kept.
-    //    Otherwise the chunks count their kept nodes and emit them in order.
+    //    With one store weight and W* equal to it, every shared node is kept
+    //    (its weight is at least twice that) and so are the first take_eq
+    //    tail nodes in (p, d) order, which join the candidates.  Otherwise
+    //    the chunks count their kept nodes and emit them in order.
     uint32_t tail_max = a0;
 #pragma unroll
     for (int u = 1; u < FC_MAX_SOURCES; ++u)
       if (u < S && alpha.a[u] > tail_max) tail_max = alpha.a[u];
-    bool fast_emit = listed && need > 0 && wstar > tail_max;
+    const bool tails_eq = alpha_flat && a0 > 0 && wstar == a0;
+    bool fast_emit = listed && need > 0 && (wstar > tail_max || tails_eq);
     uint32_t* cand_key = (uint32_t*)(smem + lay.sstr);
     uint32_t* cand_w = cand_key + kFlatCand;
     if (fast_emit) {
@@ -1784,6 +1854,36 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
           if (o < (uint32_t)kFlatCand) {
             cand_key[o] = sh_key[i];
             cand_w[o] = Wt;
+          }
+        }
+      }
+      if (tails_eq) {
+        // the first take_eq tail nodes: tails of position q are the depths
+        // past both its own LCP and the next string's
+        auto tails_of = [&](int q, int& lo, int& hi) {
+          const uint32_t x = lm[q];
+          const int l = (int)(x & kLo), ml = (int)(x >> kSh);
+          const int ln = q + 1 < T ? (int)((uint32_t)lm[q + 1] & kLo) : 0;
+          lo = l > ln ? l : ln;
+          hi = ml;
+        };
+        uint32_t nt = 0;
+        for (int q = p0; q < p1; ++q) {
+          int lo, hi;
+          tails_of(q, lo, hi);
+          nt += hi > lo ? (uint32_t)(hi - lo) : 0u;
+        }
+        uint32_t t_ex, dmy, t_tot, dmy2;
+        Scan2<NT>::run(nt, 0u, s_x, s_y, &t_ex, &dmy, &t_tot, &dmy2);
+        for (int q = p0; q < p1 && t_ex < take_eq; ++q) {
+          int lo, hi;
+          tails_of(q, lo, hi);
+          for (int d = lo + 1; d <= hi && t_ex < take_eq; ++d, ++t_ex) {
+            const uint32_t o = atomicAdd(&s_ncand, 1u);
+            if (o < (uint32_t)kFlatCand) {
+              cand_key[o] = ((uint32_t)q << 5) | (uint32_t)d;
+              cand_w[o] = a0;
+            }
           }
         }
       }
@@ -2045,27 +2145,35 @@ fc_status launch_flat(const int32_t* taken, const uint8_t* cont_len, const uint1
   if (stat >= (size_t)dv.max_lds) return FC_ERR_UNSUPPORTED;
   const size_t budget = (size_t)dv.max_lds - stat;
   const int worst_short = k - (k + S - 1) / S;  // the long store holds at least ceil(T / S)
-  // LDS for every possible short list would cost occupancy for nothing:
-  // queries past the cap (none in typical batches: a second store's list
-  // is short) go to the full-LDS kernel
+  // LDS for every possible short list would cost occupancy for nothing (in
+  // typical batches a second store's list holds a few strings)
   int cap = worst_short < kFlatShortCap ? worst_short : kFlatShortCap;
   while (cap > 0 && flat_layout(k, MAXM, cap, S, !NARROW).total > budget) cap = cap * 7 / 8;
   const FlatLayout lay = flat_layout(k, MAXM, cap, S, !NARROW);
   if (lay.total > budget) return FC_ERR_UNSUPPORTED;
-  const bool defer = cap < worst_short;
+  // with two stores a query's short list past the cap is searched in place;
+  // with more, such queries go to the full-LDS kernel
+  const bool defer = S > 2 && cap < worst_short;
   if (defer && full.total + dv.full_static[MAXM == 10 ? 0 : 1][NARROW ? 1 : 0] > (size_t)dv.max_lds)
     return FC_ERR_UNSUPPORTED;
-  int32_t* lists = (int32_t*)ws;
-  int32_t* counts = lists + 2 * (size_t)B;
+  int32_t* order = (int32_t*)ws;
+  int32_t* defer_list = order + B;
+  int32_t* counts = order + 2 * (size_t)B;
+  const bool plan = defer || B > 256;
   const int words = ((((uintptr_t)cont_tok) & 3) == 0 && (m % 2) == 0) ? 1 : 0;
   (void)hipGetLastError();
-  hipLaunchKernelGGL((k_tree_flat<MAXM, NARROW>), dim3(B + (defer ? 1 : 0)), dim3(kFlatThreads), lay.total, stream,
-                     taken, cont_len, cont_tok, ctx, L, S, k, m, t.c, a, cap, words, lists, counts, B, rows, n_rows,
+  if (plan) {
+    hipLaunchKernelGGL(k_tree_plan, dim3(1), dim3(kPlanThreads), 0, stream, taken, S, k, rows, n_rows, B, cap, order,
+                       defer ? defer_list : nullptr, defer ? counts : nullptr);
+    FC_CHECK_LAUNCH();
+  }
+  hipLaunchKernelGGL((k_tree_flat<MAXM, NARROW>), dim3(B), dim3(kFlatThreads), lay.total, stream, taken, cont_len,
+                     cont_tok, ctx, L, S, k, m, t.c, a, cap, words, plan ? order : nullptr, B, rows, n_rows,
                      num_nodes, node_tok, parent, weight, pos_ids, mask);
   FC_CHECK_LAUNCH();
   if (defer) {
     hipLaunchKernelGGL((k_tree_fast<1024, MAXM, NARROW>), dim3(B), dim3(1024), full.total, stream, taken, cont_len,
-                       cont_tok, ctx, L, S, k, m, t.c, a, lists, counts, nullptr, nullptr, B, k,
+                       cont_tok, ctx, L, S, k, m, t.c, a, defer_list, counts, nullptr, nullptr, B, k,
                        block_words(cont_tok, k, m), rows, n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
     FC_CHECK_LAUNCH();
   }
