@@ -5,24 +5,30 @@
 // what follows each occurrence (Section III-A; the repository store and the
 // common store are searched side by side, Section IV-A and Section IV-C).
 //
-// k_search: one wave per query.  The wave's lanes take the (store, n, bound)
-// triples - 2 stores x 15 lengths x {lower, upper} = 60 lanes at the paper's
-// n_max = 16, n_min = 2 - so every candidate length is searched at once and
-// the dependent probe chain is one binary search long instead of fifteen.
-// Each search starts from the store's two-token table when it has one (one
-// table read replaces the top ~25 levels of the search on a 1B-token store)
-// or else from its first-token bucket, and compares only the tokens the
-// table does not already fix.  With the store's inline-prefix records a
-// probe is one 32-byte read of a record and two levels are resolved per round
-// trip; without them each probe reads the suffix-array entry (prefetched a
-// level ahead) and then the text.  The wave then keeps, per store, the longest n whose range
-// is non-empty and fills the k slots in store priority order.
+// k_search: one workgroup per query.  Every (store, n, bound) search task -
+// 2 stores x 15 lengths x {lower, upper} = 60 at the paper's n_max = 16,
+// n_min = 2 - gets a group of G lanes (G = 4 in 256 threads), so every
+// candidate length is searched at once.  Each search starts from the store's
+// two-token table when it has one (one table read replaces the top ~25
+// levels of the search on a 1B-token store) or else from its first-token
+// bucket.  With the store's inline-prefix records the group reads the records
+// at 2G - 1 evenly spaced pivots of its range per round trip (a 2G-ary
+// search: log_2G of the range in dependent round trips), comparing only the
+// tokens the table does not already fix; without them each lane runs a
+// binary search over the suffix-array entries and the text.  The workgroup
+// then keeps, per store, the longest n whose range is non-empty and fills
+// the k slots in store priority order.
 //
-// k_offsets + k_gather: the kept slots of the whole batch are numbered
-// consecutively and spread evenly over a persistent grid.  A slot maps to its
-// store and range offset (strided floor(i*cnt/b) when the range exceeds the
-// store's budget b), reads the suffix-array entry and copies up to m
-// continuation tokens, cut before a 0 and at the end of the store.
+// k_gather: the kept slots of the whole batch are numbered consecutively and
+// cut into one contiguous piece per workgroup of a grid that is resident at
+// once; every workgroup numbers them itself (an exclusive scan of the
+// queries' kept counts into LDS), or, past 4,095 queries, reads the numbering
+// k_offsets wrote.  A slot maps to its store and range offset (strided
+// floor(i*cnt/b) when the range exceeds the store's budget b), reads the
+// record (or the suffix-array entry and then the text) and copies up to m
+// continuation tokens, cut before a 0 and at the end of the store.  Strided
+// samples of large ranges put every slot on a cache line of its own, so the
+// gather runs at the rate of scattered line reads, not of HBM streaming.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -35,11 +41,10 @@
 namespace {
 
 constexpr int kSearchThreads = 256;
-constexpr int kQueriesPerBlock = kSearchThreads / fc::kWave;
 constexpr int kGatherThreads = 256;
 constexpr int kScanThreads = 1024;
 constexpr int kOffsetsInLds = 4096;
-constexpr int kGatherBlocks = 2048;
+constexpr int kGatherBlocks = 1024;  // resident at once: 4 per CU
 
 struct StoreArgs {
   const uint16_t* tok[FC_MAX_SOURCES];
@@ -119,155 +124,196 @@ __device__ __forceinline__ int rec_cmp(const uint4& h0, const uint4& h1, const R
   return res;
 }
 
-// Lower (upper = false) or upper bound of the pattern in suffix-array range
-// [lo, hi) over the records: two levels of the binary search per memory
-// round trip, by loading the midpoint's record together with the records
-// of both possible next midpoints.
-__device__ __forceinline__ uint32_t rec_search(const uint4* __restrict__ R, uint32_t lo, uint32_t hi,
-                                               const RecQuery& rq, bool upper) {
-  while (lo < hi) {
-    const uint32_t mid = lo + ((hi - lo) >> 1);
-    const uint32_t lmid = lo < mid ? lo + ((mid - lo) >> 1) : mid;
-    const uint32_t rmid = mid + 1 < hi ? (mid + 1) + ((hi - mid - 1) >> 1) : mid;
-    const uint4 m0 = R[kRecQuads * (uint64_t)mid], m1 = R[kRecQuads * (uint64_t)mid + 1];
-    const uint4 l0 = R[kRecQuads * (uint64_t)lmid], l1 = R[kRecQuads * (uint64_t)lmid + 1];
-    const uint4 r0 = R[kRecQuads * (uint64_t)rmid], r1 = R[kRecQuads * (uint64_t)rmid + 1];
-    const int c = rec_cmp(m0, m1, rq);
-    const bool right = upper ? c <= 0 : c < 0;
-    if (right) lo = mid + 1; else hi = mid;
-    if (lo < hi) {
-      const uint32_t nm = right ? rmid : lmid;
-      const uint4 a0 = right ? r0 : l0, a1 = right ? r1 : l1;
-      const int c2 = rec_cmp(a0, a1, rq);
-      if (upper ? c2 <= 0 : c2 < 0) lo = nm + 1; else hi = nm;
-    }
-  }
-  return lo;
-}
-
-__global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, const uint16_t* __restrict__ ctx,
-                                                           int B, int L, int n_max, int n_min, int k,
-                                                           const int32_t* __restrict__ rows, int n_rows,
-                                                           int32_t* __restrict__ match_n,
-                                                           uint32_t* __restrict__ range_lo,
-                                                           uint32_t* __restrict__ range_cnt,
-                                                           int32_t* __restrict__ taken) {
-  __shared__ uint16_t s_q[kQueriesPerBlock][FC_MAX_NMAX];
-  __shared__ uint32_t s_lo[kQueriesPerBlock][FC_MAX_SOURCES][FC_MAX_NMAX];
-  __shared__ uint32_t s_hi[kQueriesPerBlock][FC_MAX_SOURCES][FC_MAX_NMAX];
-  __shared__ int s_nhi[kQueriesPerBlock];
-
-  const int w = threadIdx.x / fc::kWave;
+// Search of query b by the whole workgroup: s_lo / s_hi[s][n_max - n] get
+// the bounds of every tried (store, n); untried entries stay 0.
+__device__ __forceinline__ void search_query(const StoreArgs& st, int S, const uint16_t* __restrict__ ctx, int b,
+                                             int L, int n_max, int n_min, int G, int log2_2g, uint16_t* s_q,
+                                             uint32_t (*s_lo)[FC_MAX_NMAX], uint32_t (*s_hi)[FC_MAX_NMAX],
+                                             int* s_nhi) {
+  const int tid = (int)threadIdx.x;
   const int lane = fc::lane_id();
-  const int b = blockIdx.x * kQueriesPerBlock + w;
-  const bool active = b < B;
-  const int nq = L < FC_MAX_NMAX ? L : FC_MAX_NMAX;  // tokens of the context kept
-
-  if (active && lane < nq) s_q[w][FC_MAX_NMAX - nq + lane] = ctx[(int64_t)b * L + (L - nq + lane)];
-  if (active && lane < FC_MAX_SOURCES * FC_MAX_NMAX) {
-    (&s_lo[w][0][0])[lane] = 0;
-    (&s_hi[w][0][0])[lane] = 0;
+  const int nq = L < FC_MAX_NMAX ? L : FC_MAX_NMAX;
+  if (tid < nq) s_q[FC_MAX_NMAX - nq + tid] = ctx[(int64_t)b * L + (L - nq + tid)];
+  if (tid < FC_MAX_SOURCES * FC_MAX_NMAX) {
+    (&s_lo[0][0])[tid] = 0;
+    (&s_hi[0][0])[tid] = 0;
   }
   __syncthreads();
-  if (active && lane == 0) {
+  if (tid == 0) {
     int tail = 0;
-    while (tail < nq && s_q[w][FC_MAX_NMAX - 1 - tail] != 0) ++tail;
-    int h = n_max < L ? n_max : L;
-    s_nhi[w] = tail < h ? tail : h;
+    while (tail < nq && s_q[FC_MAX_NMAX - 1 - tail] != 0) ++tail;
+    const int h = n_max < L ? n_max : L;
+    *s_nhi = tail < h ? tail : h;
   }
   __syncthreads();
 
   const int NN = n_max - n_min + 1;
   const int tasks = S * NN * 2;
-  if (active) {
-    const int n_hi = s_nhi[w];
-    for (int t = lane; t < tasks; t += fc::kWave) {
-      const int s = t / (2 * NN);
-      const int rem = t - s * 2 * NN;
-      const int ni = rem >> 1;
-      const int upper = rem & 1;
-      const int n = n_max - ni;
-      if (n > n_hi || n < n_min) continue;
-      const uint16_t* q = &s_q[w][FC_MAX_NMAX - n];
+  const int task = tid / G;
+  const int gl = tid - task * G;
+  const int n_hi = *s_nhi;
+  int s = 0, ni = 0, upper = 0, n = 0;
+  bool act = task < tasks;
+  if (act) {
+    s = task / (2 * NN);
+    const int rem = task - s * 2 * NN;
+    ni = rem >> 1;
+    upper = rem & 1;
+    n = n_max - ni;
+    act = n <= n_hi && n >= n_min;
+  }
+  uint32_t lo = 0, hi = 0;
+  int from = 1;
+  const uint16_t* q = &s_q[FC_MAX_NMAX - (act ? n : 1)];
+  if (act && st.n[s] > 0) {
+    const uint32_t V = st.pair_vocab[s];
+    if (n >= 2 && st.pair[s] != nullptr && q[0] < V && q[1] < V) {
+      const uint64_t idx = (uint64_t)q[0] * (V + 1) + q[1] + 1;
+      lo = st.pair[s][idx];
+      hi = st.pair[s][idx + 1];
+      from = 2;
+    } else if (n >= 2 && st.pair[s] != nullptr) {
+      hi = lo = 0;  // a token >= V cannot occur in the store
+    } else {
+      lo = st.bucket[s][q[0]];
+      hi = st.bucket[s][q[0] + 1];
+    }
+  }
+  const bool kary = act && from < n && lo < hi && from == 2 && st.rec[s] != nullptr;
+  if (act && !kary) {
+    if (from < n && lo < hi) {
       const uint16_t* T = st.tok[s];
       const uint32_t* SA = st.sa[s];
       const uint32_t N = st.n[s];
-      uint32_t lo = 0, hi = 0;
-      int from = 1;
-      if (N > 0) {
-        const uint32_t V = st.pair_vocab[s];
-        if (n >= 2 && st.pair[s] != nullptr && q[0] < V && q[1] < V) {
-          // two-token table: the range of suffixes starting with q[0] q[1]
-          const uint64_t idx = (uint64_t)q[0] * (V + 1) + q[1] + 1;
-          lo = st.pair[s][idx];
-          hi = st.pair[s][idx + 1];
-          from = 2;
-        } else if (n >= 2 && st.pair[s] != nullptr) {
-          hi = lo = 0;  // a token >= V cannot occur in the store
+      uint32_t mid = lo + ((hi - lo) >> 1);
+      uint32_t j = SA[mid];
+      for (;;) {
+        const uint32_t lmid = lo + ((mid - lo) >> 1);
+        const uint32_t rmid = (mid + 1) + ((hi - mid - 1) >> 1);
+        const uint32_t jl = lo < mid ? SA[lmid] : 0u;
+        const uint32_t jr = mid + 1 < hi ? SA[rmid] : 0u;
+        const int c = cmp_suffix(T, N, j, q, n, from);
+        if (upper ? (c <= 0) : (c < 0)) {
+          lo = mid + 1;
+          mid = rmid;
+          j = jr;
         } else {
-          lo = st.bucket[s][q[0]];
-          hi = st.bucket[s][q[0] + 1];
+          hi = mid;
+          mid = lmid;
+          j = jl;
         }
+        if (lo >= hi) break;
       }
-      // Binary search, over the records when the store has them; else the
-      // suffix-array entries of both possible next midpoints are fetched
-      // together with the current probe's text, so each level costs one
-      // dependent round trip.  When the table already covers the whole
-      // pattern the range is final.
-      if (from < n && lo < hi && from == 2 && st.rec[s] != nullptr) {
-        lo = rec_search(st.rec[s], lo, hi, rec_query(q, n), upper);
-      } else if (from < n && lo < hi) {
-        uint32_t mid = lo + ((hi - lo) >> 1);
-        uint32_t j = SA[mid];
-        for (;;) {
-          const uint32_t lmid = lo + ((mid - lo) >> 1);
-          const uint32_t rmid = (mid + 1) + ((hi - mid - 1) >> 1);
-          const uint32_t jl = lo < mid ? SA[lmid] : 0u;
-          const uint32_t jr = mid + 1 < hi ? SA[rmid] : 0u;
-          const int c = cmp_suffix(T, N, j, q, n, from);
-          if (upper ? (c <= 0) : (c < 0)) {
-            lo = mid + 1;
-            mid = rmid;
-            j = jr;
-          } else {
-            hi = mid;
-            mid = lmid;
-            j = jl;
-          }
-          if (lo >= hi) break;
-        }
-      } else if (upper) {
-        lo = hi;  // range already final: its end is the upper bound
-      }
-      if (upper) s_hi[w][s][ni] = lo; else s_lo[w][s][ni] = lo;
+    } else if (upper) {
+      lo = hi;  // range already final: its end is the upper bound
     }
   }
-  __syncthreads();
-  const int row = active ? fc::map_row(rows, n_rows, b) : -1;
-  if (active && lane == 0 && row >= 0) {
-    const int n_hi = s_nhi[w];
-    int64_t used = 0;
-    for (int s = 0; s < S; ++s) {
-      int mn = 0;
-      uint32_t lo = 0, cnt = 0;
-      for (int n = n_hi; n >= n_min; --n) {
-        const int ni = n_max - n;
-        const uint32_t c = s_hi[w][s][ni] - s_lo[w][s][ni];
-        if (c > 0) {
-          mn = n;
-          lo = s_lo[w][s][ni];
-          cnt = c;
-          break;
+  {
+    const RecQuery rq = rec_query(q, act ? n : 2);
+    const uint4* R = st.rec[s];
+    const bool two = n > 8;  // tokens past offset 7 sit in the record's second quad
+    const int gbase = lane - gl;
+    const uint64_t gmask = G >= 64 ? ~0ull : ((1ull << G) - 1);
+    const int P = 2 * G - 1;  // pivots per round trip
+    bool searching = kary;
+    while (fc::ballot(searching) != 0) {
+      bool ca = false, cb = false;
+      if (searching) {
+        const uint64_t span = hi - lo;
+        const uint32_t pa = lo + (uint32_t)(((uint64_t)(2 * gl + 1) * span) >> log2_2g);
+        const bool vb = 2 * gl + 2 <= P;
+        const uint32_t pb = vb ? lo + (uint32_t)(((uint64_t)(2 * gl + 2) * span) >> log2_2g) : pa;
+        const uint4 a0 = R[kRecQuads * (uint64_t)pa];
+        const uint4 b0 = R[kRecQuads * (uint64_t)pb];
+        uint4 a1 = make_uint4(0, 0, 0, 0), b1 = a1;
+        if (two) {
+          a1 = R[kRecQuads * (uint64_t)pa + 1];
+          b1 = R[kRecQuads * (uint64_t)pb + 1];
         }
+        const int c1 = rec_cmp(a0, a1, rq);
+        const int c2 = rec_cmp(b0, b1, rq);
+        ca = upper ? c1 <= 0 : c1 < 0;
+        cb = vb && (upper ? c2 <= 0 : c2 < 0);
       }
-      const int64_t budget = (int64_t)k - used;
-      const int64_t tk = (int64_t)cnt < budget ? (int64_t)cnt : budget;
-      const int64_t o = (int64_t)row * S + s;
+      const uint64_t ba = fc::ballot(searching && ca);
+      const uint64_t bb = fc::ballot(searching && cb);
+      if (searching) {
+        // the pivots before the bound form a prefix of the 2G - 1 pivots
+        const int c = __popcll((ba >> gbase) & gmask) + __popcll((bb >> gbase) & gmask);
+        const uint64_t span = hi - lo;
+        const uint32_t plo = c > 0 ? lo + (uint32_t)(((uint64_t)c * span) >> log2_2g) + 1 : lo;
+        const uint32_t phi = c < P ? lo + (uint32_t)(((uint64_t)(c + 1) * span) >> log2_2g) : hi;
+        lo = plo;
+        hi = phi;
+        searching = lo < hi;
+      }
+    }
+  }
+  if (act && gl == 0) {
+    if (upper) s_hi[s][ni] = lo; else s_lo[s][ni] = lo;
+  }
+  __syncthreads();
+}
+
+// One query per workgroup: the 2G-ary search of every (store, n, bound),
+// then the kept ranges (the longest non-empty n per store, store priority
+// order) written to the query's row.
+__global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, const uint16_t* __restrict__ ctx,
+                                                           int L, int n_max, int n_min, int k, int G, int log2_2g,
+                                                           const int32_t* __restrict__ rows, int n_rows,
+                                                           int32_t* __restrict__ match_n,
+                                                           uint32_t* __restrict__ range_lo,
+                                                           uint32_t* __restrict__ range_cnt,
+                                                           int32_t* __restrict__ taken) {
+  __shared__ uint16_t s_q[FC_MAX_NMAX];
+  __shared__ uint32_t s_lo[FC_MAX_SOURCES][FC_MAX_NMAX];
+  __shared__ uint32_t s_hi[FC_MAX_SOURCES][FC_MAX_NMAX];
+  __shared__ int s_nhi;
+  const int b = (int)blockIdx.x;
+  const int row = fc::map_row(rows, n_rows, b);
+  if (row < 0) return;  // skipped query: the whole workgroup leaves
+  const int tid = (int)threadIdx.x;
+  const int lane = fc::lane_id();
+  search_query(st, S, ctx, b, L, n_max, n_min, G, log2_2g, s_q, s_lo, s_hi, &s_nhi);
+  if (tid < fc::kWave) {
+    const int NN = n_max - n_min + 1;
+    const int n_hi = s_nhi;
+    bool ne = false;
+    if (lane < S * NN) {
+      const int u = lane / NN, x = lane - (lane / NN) * NN;
+      const int nn = n_max - x;
+      ne = nn <= n_hi && nn >= n_min && s_hi[u][x] > s_lo[u][x];
+    }
+    const uint64_t bal = fc::ballot(ne);
+    if (lane < S) {
+      // store `lane`: its longest non-empty n, then the budget left by the
+      // stores before it
+      int used = 0, mine = 0;
+      int mn = 0;
+      uint32_t rlo = 0, cnt = 0;
+      for (int u = 0; u <= lane; ++u) {
+        const uint32_t bits = (uint32_t)(bal >> (u * NN)) & ((1u << NN) - 1u);
+        uint32_t c = 0;
+        int x = 0;
+        if (bits) {
+          x = __builtin_ctz(bits);
+          c = s_hi[u][x] - s_lo[u][x];
+        }
+        const int budget = k - used;
+        const int tk = (int64_t)c < (int64_t)budget ? (int)c : budget;
+        if (u == lane) {
+          mine = tk;
+          mn = bits ? n_max - x : 0;
+          rlo = bits ? s_lo[u][x] : 0u;
+          cnt = c;
+        }
+        used += tk;
+      }
+      const int64_t o = (int64_t)row * S + lane;
       match_n[o] = mn;
-      range_lo[o] = lo;
+      range_lo[o] = rlo;
       range_cnt[o] = cnt;
-      taken[o] = (int32_t)tk;
-      used += tk;
+      taken[o] = mine;
     }
   }
 }
@@ -332,37 +378,23 @@ __device__ __forceinline__ void load_window(const uint16_t* __restrict__ T, uint
   }
 }
 
-// The per-store fields of one query's row that its slots need.
-struct RowMeta {
-  int32_t taken[FC_MAX_SOURCES];
-  uint32_t cnt[FC_MAX_SOURCES], lo[FC_MAX_SOURCES];
-  int32_t n[FC_MAX_SOURCES];
-};
+// Kept slots of the whole batch as one flat range (slot g belongs to the
+// query b with offsets[b] <= g < offsets[b+1]), cut into one contiguous piece
+// per workgroup of a grid that fits on the GPU at once.  Every workgroup
+// numbers the slots itself: the queries' kept counts are loaded all at once
+// (one memory round trip) and scanned in LDS; past 4,095 queries it reads
+// the numbering k_offsets wrote.  The piece's queries (a contiguous run,
+// usually a handful) have their per-store fields copied into LDS once, so a
+// slot costs an LDS lookup and then one record read.  Each thread takes
+// kGatherUnroll slots at a time with all their reads issued before any is
+// used; consecutive lanes take consecutive slots, so a kept range is read at
+// consecutive records and the outputs are written contiguously.  The window
+// is cut at the first 0 in registers and written two tokens per 32-bit store
+// when rows are 4-byte aligned.
+constexpr int kGatherUnroll = 4;
+constexpr int kMetaQueries = 64;  // queries of a piece whose fields fit in LDS
+constexpr int kMaxPerThread = kOffsetsInLds / kGatherThreads;
 
-__device__ __forceinline__ RowMeta load_meta(const int32_t* __restrict__ taken, const uint32_t* __restrict__ range_cnt,
-                                             const uint32_t* __restrict__ range_lo,
-                                             const int32_t* __restrict__ match_n, int64_t row, int S) {
-  RowMeta r;
-#pragma unroll
-  for (int u = 0; u < FC_MAX_SOURCES; ++u) {
-    const int64_t o = row * S + u;
-    r.taken[u] = u < S ? taken[o] : 0;
-    r.cnt[u] = u < S ? range_cnt[o] : 0u;
-    r.lo[u] = u < S ? range_lo[o] : 0u;
-    r.n[u] = u < S ? match_n[o] : 0;
-  }
-  return r;
-}
-
-// Kept slots of the whole batch as one flat range, split evenly over a
-// persistent grid: slot g belongs to the query b with offsets[b] <= g <
-// offsets[b+1] (binary search in an LDS copy of the offsets).  A wave whose
-// slots all belong to one query (the common case) reads that query's
-// per-store fields with scalar loads.  Each slot reads its inline-prefix
-// record (or else its suffix-array entry and then the text) at consecutive
-// positions when the whole range is kept, cuts the window at the first 0 in
-// registers and writes the tokens two per 32-bit store when rows are
-// 4-byte aligned.
 template <int MAXM>
 __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, int B, int k, int m,
                                                            const int32_t* __restrict__ match_n,
@@ -376,85 +408,233 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
                                                            uint8_t* __restrict__ cont_len,
                                                            uint16_t* __restrict__ cont_tok) {
   __shared__ uint32_t s_off[kOffsetsInLds];
+  __shared__ uint32_t s_scan[kGatherThreads / fc::kWave + 1];
+  __shared__ int32_t s_taken[kMetaQueries][FC_MAX_SOURCES];
+  __shared__ uint32_t s_cnt[kMetaQueries][FC_MAX_SOURCES], s_lo[kMetaQueries][FC_MAX_SOURCES];
+  __shared__ int32_t s_n[kMetaQueries][FC_MAX_SOURCES];
+  __shared__ int s_row[kMetaQueries];
+  const int tid = (int)threadIdx.x;
   const bool in_lds = B + 1 <= kOffsetsInLds;
-  if (in_lds)
-    for (int i = (int)threadIdx.x; i <= B; i += kGatherThreads) s_off[i] = offsets[i];
+  if (in_lds) {
+    // kept slots of queries tid, tid + 256, ...: every load issued at once
+    uint32_t t[kMaxPerThread];
+#pragma unroll
+    for (int i = 0; i < kMaxPerThread; ++i) {
+      const int q = tid + i * kGatherThreads;
+      t[i] = 0;
+      if (q < B) {
+        const int r = fc::map_row(rows, n_rows, q);
+        if (r >= 0) {
+#pragma unroll
+          for (int u = 0; u < FC_MAX_SOURCES; ++u)
+            if (u < S) t[i] += (uint32_t)taken[(int64_t)r * S + u];
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kMaxPerThread; ++i) {
+      const int q = tid + i * kGatherThreads;
+      if (q < B) s_off[q] = t[i];
+    }
+    __syncthreads();
+    // exclusive scan: each thread a run of consecutive queries
+    const int per = (B + kGatherThreads - 1) / kGatherThreads;
+    const int b0 = tid * per;
+    const int b1 = b0 + per < B ? b0 + per : B;
+    uint32_t sum = 0;
+    for (int q = b0; q < b1; ++q) sum += s_off[q];
+    uint32_t all;
+    uint32_t run = fc::block_excl_sum<uint32_t>(sum, s_scan, &all);
+    for (int q = b0; q < b1; ++q) {
+      const uint32_t x = s_off[q];
+      s_off[q] = run;
+      run += x;
+    }
+    if (tid == 0) s_off[B] = all;
+  }
   __syncthreads();
   const uint32_t* off_tab = in_lds ? s_off : offsets;
   const uint32_t total = off_tab[B];
-  for (uint32_t g = blockIdx.x * kGatherThreads + threadIdx.x; g < total; g += gridDim.x * kGatherThreads) {
-    int lo = 0, hi = B;  // last b with offsets[b] <= g
+  const uint32_t a = (uint32_t)(((uint64_t)total * blockIdx.x) / gridDim.x);
+  const uint32_t e = (uint32_t)(((uint64_t)total * (blockIdx.x + 1)) / gridDim.x);
+  if (a >= e) return;
+  // last query with offsets <= g, searched in [lo, hi)
+  auto owner = [&](uint32_t g, int lo, int hi) {
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
       if (off_tab[mid] <= g) lo = mid; else hi = mid;
     }
-    const int b = lo;
-    const int row = fc::map_row(rows, n_rows, b);  // >= 0: a skipped query owns no slots
-    const int i = (int)(g - off_tab[b]);
-    const int rf = __builtin_amdgcn_readfirstlane(row);
-    const RowMeta meta = fc::ballot(row != rf) == 0 ? load_meta(taken, range_cnt, range_lo, match_n, rf, S)
-                                                    : load_meta(taken, range_cnt, range_lo, match_n, row, S);
-    // the slot's store: stores before it fill the first slots
-    int s = 0;
-    int64_t before = 0;
-    uint64_t cnt = meta.cnt[0], rlo = meta.lo[0];
-    int n = meta.n[0];
-#pragma unroll
-    for (int u = 1; u < FC_MAX_SOURCES; ++u) {
-      const int64_t nb = before + meta.taken[u - 1];
-      if (u < S && s == u - 1 && i >= nb) {
-        s = u;
-        before = nb;
-        cnt = meta.cnt[u];
-        rlo = meta.lo[u];
-        n = meta.n[u];
-      }
-    }
-    const uint64_t budget = (uint64_t)((int64_t)k - before);
-    const uint64_t local = (uint64_t)(i - before);
-    const uint64_t off = cnt > budget ? (local * cnt) / budget : local;
-    const uint64_t idx = rlo + off;
-    const uint64_t N = st.n[s];
-    uint16_t v[MAXM];
-    uint32_t j;
-    // the window's words (token n - 2 onward) inside the record: no text read
-    const int t0 = n - 2;
-    if (st.rec[s] != nullptr && t0 >= 0 && (t0 >> 1) + MAXM / 2 <= FC_RECORD_TOKENS / 2 - 1) {
-      const uint32_t* W = (const uint32_t*)(st.rec[s] + kRecQuads * idx);
-      j = W[0];
-      words_window<MAXM>(W + 1 + (t0 >> 1), t0 & 1, v);
+    return lo;
+  };
+  const int qa = owner(a, 0, B);
+  const int qb = owner(e - 1, qa, B);
+  const int nq = qb - qa + 1;
+  const bool meta_lds = nq <= kMetaQueries;
+  if (meta_lds && tid < nq * FC_MAX_SOURCES) {
+    const int x = tid / FC_MAX_SOURCES, u = tid - x * FC_MAX_SOURCES;
+    const int r = fc::map_row(rows, n_rows, qa + x);  // >= 0 for a query that owns slots
+    if (u == 0) s_row[x] = r;
+    if (u < S && r >= 0) {
+      const int64_t o = (int64_t)r * S + u;
+      s_taken[x][u] = taken[o];
+      s_cnt[x][u] = range_cnt[o];
+      s_lo[x][u] = range_lo[o];
+      s_n[x][u] = match_n[o];
     } else {
-      j = st.sa[s][idx];
-      const uint64_t start = (uint64_t)j + (uint64_t)n;
-      if (words) load_window<MAXM>(st.tok[s], N, start, v);
-      else {
+      s_taken[x][u] = 0;
+      s_cnt[x][u] = 0;
+      s_lo[x][u] = 0;
+      s_n[x][u] = 0;
+    }
+  }
+  __syncthreads();
+
+  constexpr int kWords = MAXM / 2 + 1;
+  for (uint32_t g0 = a + (uint32_t)tid; g0 < e; g0 += kGatherThreads * kGatherUnroll) {
+    uint32_t wd[kGatherUnroll][kWords];
+    uint32_t jv[kGatherUnroll];
+    int sv[kGatherUnroll], nv[kGatherUnroll], rowv[kGatherUnroll], iv[kGatherUnroll];
+    bool in_rec[kGatherUnroll];
 #pragma unroll
-        for (int x = 0; x < MAXM; ++x) v[x] = (start + x < N) ? st.tok[s][start + x] : (uint16_t)0;
+    for (int v = 0; v < kGatherUnroll; ++v) {
+      const uint32_t g = g0 + (uint32_t)(v * kGatherThreads);
+      sv[v] = 0;
+      nv[v] = 0;
+      rowv[v] = 0;
+      iv[v] = 0;
+      jv[v] = 0;
+      in_rec[v] = false;
+      if (g < e) {
+        const int q = owner(g, qa, qb + 1);
+        const int i = (int)(g - off_tab[q]);
+        int tk[FC_MAX_SOURCES], nn[FC_MAX_SOURCES];
+        uint32_t ct[FC_MAX_SOURCES], lw[FC_MAX_SOURCES];
+        int row;
+        if (meta_lds) {
+          const int x = q - qa;
+          row = s_row[x];
+#pragma unroll
+          for (int u = 0; u < FC_MAX_SOURCES; ++u) {
+            tk[u] = s_taken[x][u];
+            ct[u] = s_cnt[x][u];
+            lw[u] = s_lo[x][u];
+            nn[u] = s_n[x][u];
+          }
+        } else {
+          row = fc::map_row(rows, n_rows, q);
+#pragma unroll
+          for (int u = 0; u < FC_MAX_SOURCES; ++u) {
+            const int64_t o = (int64_t)row * S + u;
+            tk[u] = u < S ? taken[o] : 0;
+            ct[u] = u < S ? range_cnt[o] : 0u;
+            lw[u] = u < S ? range_lo[o] : 0u;
+            nn[u] = u < S ? match_n[o] : 0;
+          }
+        }
+        // the slot's store: stores before it fill the first slots
+        int s = 0;
+        int before = 0;
+        uint64_t cnt = ct[0], rlo = lw[0];
+        int n = nn[0];
+#pragma unroll
+        for (int u = 1; u < FC_MAX_SOURCES; ++u) {
+          const int nb = before + tk[u - 1];
+          if (u < S && s == u - 1 && i >= nb) {
+            s = u;
+            before = nb;
+            cnt = ct[u];
+            rlo = lw[u];
+            n = nn[u];
+          }
+        }
+        const uint64_t budget = (uint64_t)(k - before);
+        const uint64_t local = (uint64_t)(i - before);
+        const uint64_t idx = rlo + (cnt > budget ? (local * cnt) / budget : local);
+        sv[v] = s;
+        nv[v] = n;
+        rowv[v] = row;
+        iv[v] = i;
+        // the window's words (token n - 2 onward) inside the record: no text
+        // read.  The record is read as 16-byte quads - quad 0 (sa entry and
+        // tokens 2..7) and only the later quads the window reaches - so a
+        // slot costs two to four vector loads instead of one per word.
+        const int t0 = n - 2;
+        if (st.rec[s] != nullptr && t0 >= 0 && (t0 >> 1) + MAXM / 2 <= FC_RECORD_TOKENS / 2 - 1) {
+          const uint4* Q = st.rec[s] + kRecQuads * idx;
+          const int wf = 1 + (t0 >> 1);  // first window word
+          const int wl = wf + kWords - 1;  // last window word
+          const uint4 q0 = Q[0];
+          const uint4 q1 = Q[1];
+          uint4 q2 = make_uint4(0, 0, 0, 0), q3 = q2;
+          if (wl >= 8) q2 = Q[2];
+          if (wl >= 12) q3 = Q[3];
+          in_rec[v] = true;
+          jv[v] = q0.x;
+          uint32_t w[16] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w,
+                            q2.x, q2.y, q2.z, q2.w, q3.x, q3.y, q3.z, q3.w};
+          // words wf.. by a barrel shift of the 16 words (wf < 16)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const bool on = (wf >> b) & 1;
+#pragma unroll
+            for (int x = 0; x < 16; ++x) {
+              const int y = x + (1 << b);
+              w[x] = on ? (y < 16 ? w[y] : 0u) : w[x];
+            }
+          }
+#pragma unroll
+          for (int x = 0; x < kWords; ++x) wd[v][x] = w[x];
+        } else {
+          jv[v] = st.sa[s][idx];
+        }
       }
     }
-    const uint64_t start = (uint64_t)j + (uint64_t)n;
-    int len = m;
 #pragma unroll
-    for (int x = MAXM - 1; x >= 0; --x)
-      if (x < m && v[x] == 0) len = x;
-    const int64_t slot = (int64_t)row * k + i;
-    uint16_t* out = cont_tok + slot * m;
-    if (out_words) {
-      uint32_t* out32 = (uint32_t*)out;
+    for (int v = 0; v < kGatherUnroll; ++v) {
+      const uint32_t g = g0 + (uint32_t)(v * kGatherThreads);
+      if (g >= e) continue;
+      const int s = sv[v];
+      const int n = nv[v];
+      const uint64_t start = (uint64_t)jv[v] + (uint64_t)n;
+      uint16_t tok[MAXM];
+      if (in_rec[v]) {
+        const int odd = (n - 2) & 1;
 #pragma unroll
-      for (int x = 0; x < MAXM / 2; ++x) {
-        const uint32_t a = 2 * x < len ? v[2 * x] : 0u;
-        const uint32_t c2 = 2 * x + 1 < len ? v[2 * x + 1] : 0u;
-        if (2 * x < m) out32[x] = a | (c2 << 16);
+        for (int x = 0; x < MAXM; ++x) {
+          const uint16_t even_v = (uint16_t)(wd[v][x >> 1] >> (16 * (x & 1)));
+          const uint16_t odd_v = (uint16_t)(wd[v][(x + 1) >> 1] >> (16 * ((x + 1) & 1)));
+          tok[x] = odd ? odd_v : even_v;
+        }
+      } else if (words) {
+        load_window<MAXM>(st.tok[s], st.n[s], start, tok);
+      } else {
+        const uint64_t N = st.n[s];
+#pragma unroll
+        for (int x = 0; x < MAXM; ++x) tok[x] = (start + x < N) ? st.tok[s][start + x] : (uint16_t)0;
       }
-    } else {
+      int len = m;
 #pragma unroll
-      for (int x = 0; x < MAXM; ++x)
-        if (x < m) out[x] = x < len ? v[x] : (uint16_t)0;
+      for (int x = MAXM - 1; x >= 0; --x)
+        if (x < m && tok[x] == 0) len = x;
+      const int64_t slot = (int64_t)rowv[v] * k + iv[v];
+      uint16_t* out = cont_tok + slot * m;
+      if (out_words) {
+        uint32_t* out32 = (uint32_t*)out;
+#pragma unroll
+        for (int x = 0; x < MAXM / 2; ++x) {
+          const uint32_t lo16 = 2 * x < len ? tok[2 * x] : 0u;
+          const uint32_t hi16 = 2 * x + 1 < len ? tok[2 * x + 1] : 0u;
+          if (2 * x < m) out32[x] = lo16 | (hi16 << 16);
+        }
+      } else {
+#pragma unroll
+        for (int x = 0; x < MAXM; ++x)
+          if (x < m) out[x] = x < len ? tok[x] : (uint16_t)0;
+      }
+      cont_pos[slot] = (uint32_t)start;
+      cont_src[slot] = (uint8_t)s;
+      cont_len[slot] = (uint8_t)len;
     }
-    cont_pos[slot] = (uint32_t)start;
-    cont_src[slot] = (uint8_t)s;
-    cont_len[slot] = (uint8_t)len;
   }
 }
 
@@ -563,13 +743,21 @@ fc_status retrieve_launch(const StoreArgs& st, int32_t S, const uint16_t* ctx, i
                           int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len,
                           uint16_t* cont_tok, const int32_t* rows, int32_t n_rows, void* ws, hipStream_t stream) {
   (void)hipGetLastError();
-  hipLaunchKernelGGL(k_search, dim3(fc::div_up(B, kQueriesPerBlock)), dim3(kSearchThreads), 0, stream, st, S, ctx,
-                     B, L, p.n_max, p.n_min, p.k, rows, n_rows, match_n, range_lo, range_cnt, taken);
+  // lanes per search task: the largest power of two <= 16 that fits
+  const int tasks = S * (p.n_max - p.n_min + 1) * 2;
+  int G = 16;
+  while (G > 1 && G * tasks > kSearchThreads) G >>= 1;
+  int log2_2g = 1;
+  while ((1 << log2_2g) < 2 * G) ++log2_2g;
+  hipLaunchKernelGGL(k_search, dim3(B), dim3(kSearchThreads), 0, stream, st, S, ctx, L, p.n_max, p.n_min, p.k, G,
+                     log2_2g, rows, n_rows, match_n, range_lo, range_cnt, taken);
   FC_CHECK_LAUNCH();
   if (p.m <= 16) {
     uint32_t* offsets = (uint32_t*)ws;
-    hipLaunchKernelGGL(k_offsets, dim3(1), dim3(kScanThreads), 0, stream, taken, B, S, rows, n_rows, offsets);
-    FC_CHECK_LAUNCH();
+    if (B + 1 > kOffsetsInLds) {  // else every gather workgroup numbers the slots itself
+      hipLaunchKernelGGL(k_offsets, dim3(1), dim3(kScanThreads), 0, stream, taken, B, S, rows, n_rows, offsets);
+      FC_CHECK_LAUNCH();
+    }
     int words = 1;
     for (int s = 0; s < S; ++s) words &= (((uintptr_t)st.tok[s]) & 3) == 0;
     const int out_words = (p.m % 2 == 0) && (((uintptr_t)cont_tok) & 3) == 0;
