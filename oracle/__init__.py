@@ -20,7 +20,9 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# FC_ORACLE_LIB names another build of fc_oracle.c to load (e.g. one built
+# with -fsanitize=address,undefined for a checked run of the pins).
+_LIB_PATH = os.environ.get("FC_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 
 def build() -> None:

@@ -14,7 +14,7 @@
 //      range_lo (the suffixes below it) and the occurrences (the suffixes
 //      that start with it), numbered in text order by a block scan;
 //   3. the occurrences in suffix order: ranks by counting pairwise
-//      comparisons when there are at most 32, else a bitonic sort in LDS;
+//      comparisons when there are at most 128, else a bitonic sort in LDS;
 //   4. the kept ones (strided floor(i*cnt/k) beyond k) and their
 //      continuations, cut before a 0 and at the end of the text.
 #include <hip/hip_runtime.h>

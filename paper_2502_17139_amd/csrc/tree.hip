@@ -9,9 +9,9 @@
 // tree whose attention mask lets a token see only its own ancestors
 // (Section IV-D, eq. (4)).
 //
-// One workgroup per query, everything in LDS, no hash table and no pointer
-// chasing.  fc_retrieve hands each store's continuations over in suffix
-// order, i.e. already sorted lexicographically, so:
+// One workgroup per query, no hash table and no pointer chasing.
+// fc_retrieve hands each store's continuations over in suffix order, i.e.
+// already sorted lexicographically, so:
 //   1. the per-store sorted lists are merged into one sorted list (each
 //      string finds its merged position by binary search in the other
 //      stores' lists);
@@ -25,8 +25,16 @@
 //      lexicographic path order with a prefix before its extensions, and
 //      also preorder, so an ordered compaction emits the kept nodes already
 //      in output order;
-//   4. a node's parent is the nearest earlier kept node one level up; the
-//      mask rows are ancestor bitsets expanded into int32.
+//   4. a node's parent is the nearest earlier kept node one level up; in
+//      preorder a node's subtree is the run of rows from it to its subtree
+//      end (the first later row no deeper than it), so mask row j is set
+//      exactly at the ancestors of j: the rows i <= j whose subtree end lies
+//      past j.
+// Three kernels implement this: k_tree_flat (m <= 16: only the short stores'
+// strings in LDS, the long store's read in place), k_tree_fast (every kept
+// string in LDS, also for the short lists too long for the flat path) and
+// k_tree_any (any m).  k_tree_plan orders the queries heaviest first when
+// the batch is large enough for the order to matter.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 

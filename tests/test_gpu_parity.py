@@ -519,6 +519,98 @@ def test_fuzz_small_stores(seed):
         compare_tree(g, o)
 
 
+def test_fuzz_many_tiny_cases():
+    """About 1.2e4 query cases on tiny adversarial stores: 48 seeded store
+    sets (one to four stores, vocabularies of 2 to 300 tokens, empty and
+    one-token stores, with and without pair tables and records) x 64 queries
+    of 1 to 19 tokens x four parameter sets (the paper's n and budgets
+    scaled down, n_min = 1, m > 16 through the any-m gather and tree, and
+    k = m = c = 1).  Every retrieval, tree and acceptance output against the
+    oracle."""
+    params = ((16, 2, 64, 10, 16), (8, 1, 9, 4, 5), (5, 3, 300, 17, 40), (16, 2, 1, 1, 1))
+    cases = 0
+    for seed in range(48):
+        rng = np.random.default_rng(1000 + seed)
+        S = 1 + seed % 4
+        vocab = (2, 3, 5, 12, 40, 300)[seed % 6]
+        lens = [int(rng.integers(0, 800)) for _ in range(S)]
+        if seed % 7 == 0:
+            lens[0] = 1
+        texts = [synth.random_text(5000 + 10 * seed + s, n, vocab, 0.03) for s, n in enumerate(lens)]
+        stores = []
+        for t in texts:
+            if len(t) == 0:
+                t = np.zeros(0, np.uint16)
+                stores.append(fc.Store(dev(np.zeros(1, np.uint16))[:0], dev(np.zeros(1, np.uint32))[:0],
+                                       fc.fc_store_prepare(dev(np.zeros(1, np.uint16))[:0],
+                                                           dev(np.zeros(1, np.uint32))[:0])))
+            else:
+                stores.append(gpu_store(t, vocab if seed % 2 else None, records=seed % 4 == 1))
+        rows = []
+        for b in range(64):
+            src = texts[int(rng.integers(S))]
+            L = int(rng.integers(1, 20))
+            if len(src) > L and rng.random() < 0.7:
+                j = int(rng.integers(0, len(src) - L))
+                rows.append(src[j:j + L].copy())
+            else:
+                rows.append(rng.integers(0, vocab, size=L).astype(np.uint16))
+        ctx = np.stack([np.concatenate([np.full(19 - len(r), 1, np.uint16), r]) for r in rows])
+        alpha = (1, 2, 3, 5)[:S]
+        for (n_max, n_min, k, m, c) in params:
+            say(f"tiny fuzz seed={seed} S={S} vocab={vocab} n={n_max}..{n_min} k={k} m={m} c={c}")
+            p = dict(n_max=n_max, n_min=n_min, k=k, m=m)
+            g = gpu_pipeline(stores, ctx, p, alpha, c)
+            o = oracle_pipeline(texts, ctx, p, alpha, c)
+            compare_retrieve(g, o)
+            compare_tree(g, o)
+            _check_accept(g, o, m, seed)
+            cases += len(ctx)
+    assert cases >= 12000
+
+
+def test_results_do_not_depend_on_batching():
+    """The same queries give the same per-query bytes whatever launch shape
+    the batch leads to: one batch of 300 (the tree's heaviest-first planning
+    launch, a full gather grid), batches of 1, 7, 41 and 251 (other gather
+    grids and slot pieces, no planning launch), and the batch reversed
+    through a row map (other workgroup-to-query assignment)."""
+    t = synth.store(1, "single")
+    st = gpu_store(t, synth.VOCAB, records=True)
+    base = synth.queries(1)
+    rng = np.random.default_rng(3)
+    ctx = base[rng.integers(0, len(base), 300)]
+    p = dict(P)
+    fields = ("match_n", "range_lo", "range_cnt", "taken", "num_nodes", "node_tok", "parent", "weight",
+              "pos_ids", "mask")
+    ref = gpu_pipeline([st], ctx, p, (1,), p["c"])
+
+    def same(got, lo, hi):
+        for f in fields:
+            assert (got[f] == ref[f][lo:hi]).all(), (f, lo, hi)
+        for b in range(hi - lo):
+            used = int(ref["taken"][lo + b].sum())
+            for f in ("cont_pos", "cont_src", "cont_len", "cont_tok"):
+                assert (got[f][b, :used] == ref[f][lo + b, :used]).all(), (f, lo + b)
+
+    for size in (1, 7, 41, 251):
+        say(f"batching: batches of {size}")
+        for lo in range(0, 300, size):
+            hi = min(300, lo + size)
+            same(gpu_pipeline([st], ctx[lo:hi], p, (1,), p["c"]), lo, hi)
+    say("batching: reversed through a row map")
+    cx = dev(ctx[::-1].astype(np.uint16))
+    rows = dev(np.arange(299, -1, -1, dtype=np.int32))
+    r = fc.fc_retrieve([st], cx, n_max=p["n_max"], n_min=p["n_min"], k=p["k"], m=p["m"], rows=rows,
+                       out=fc.retrieve_outputs(300, 1, p["k"], p["m"], cx.device))
+    tr = fc.fc_build_tree(r["taken"], r["cont_len"], r["cont_tok"], dev(ctx.astype(np.uint16)), c=p["c"],
+                          alpha=(1,))
+    torch.cuda.synchronize()
+    got = {f: host(v) for f, v in r.items()}
+    got.update({f: host(v) for f, v in tr.items()})
+    same(got, 0, 300)
+
+
 def test_targets_from_truth_edges():
     """fc_targets_from_truth against its definition: a stream map that
     permutes and repeats streams, starts at the stream's last token (every
