@@ -14,7 +14,9 @@
 //            end), where rank[i] is the suffix-array index at which i's group
 //            of equal h-token prefixes starts (Larsson and Sadakane's group
 //            numbering).  Suffixes whose group becomes a singleton drop out.
-//   finally  sa[rank[i]] = i.
+//   a suffix whose group becomes a singleton has its final index, rank[i],
+//   and sa[rank[i]] = i is written in that round (in sorted order, so at
+//   nearly sequential addresses).
 //
 // Each radix sort is a global digit histogram followed by one "onesweep"
 // pass per 8-bit digit (Adinets and Merrill 2022): a workgroup takes a tile
@@ -27,6 +29,9 @@
 // After each sort, head flags of the new and old groups are turned into
 // group starts with a three-phase scan (tile partials, one-workgroup scan of
 // the partials, per-tile apply), which also compacts the still-tied suffixes.
+// Both tile passes run wave-striped (a wave takes 1,024 consecutive sorted
+// positions, 64 at a time), so every load and store of a wave is coalesced
+// except the rank scatter itself, which is indexed by suffix.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -129,15 +134,6 @@ __global__ void __launch_bounds__(256) k_localize_sa(uint32_t* __restrict__ sa, 
                                                        const uint64_t* __restrict__ off, uint32_t R) {
   const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r < n) sa[r] -= (uint32_t)off[segment_of(off, R, r)];
-}
-
-__global__ void __launch_bounds__(256) k_scatter_sa(const uint32_t* __restrict__ rank, uint32_t n,
-                                                      uint32_t* __restrict__ sa) {
-  uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) {
-    const uint32_t r = rank[i];
-    if (r < n) sa[r] = i;
-  }
 }
 
 // ------------------------------------------------------------ extension --
@@ -600,10 +596,10 @@ __global__ void __launch_bounds__(kSegThreads) k_seg_partials(const uint64_t* __
                                                                 uint32_t* __restrict__ part_g,
                                                                 uint32_t* __restrict__ part_k) {
   __shared__ uint32_t scratch[kSegThreads / fc::kWave + 1];
-  const uint32_t r0 = blockIdx.x * kSegTile + threadIdx.x * kSegItems;
+  const uint32_t r0 = blockIdx.x * kSegTile + threadIdx.x;
   uint32_t mh = 0, mg = 0, kc = 0;
   for (int j = 0; j < kSegItems; ++j) {
-    const uint32_t r = r0 + j;
+    const uint32_t r = r0 + (uint32_t)j * kSegThreads;  // coalesced; max and sum ignore the order
     if (r >= U) break;
     const SegFlags f = seg_flags(keys, U, r, sb, round0 != 0);
     if (f.new_head) mh = r;
@@ -653,7 +649,13 @@ __global__ void __launch_bounds__(kScanThreads) k_seg_scan(uint32_t* __restrict_
 }
 
 // Per element: new rank = old group start + (new head index - old head index)
-// in the sorted list; tied suffixes are compacted into vals_next.
+// in the sorted list; tied suffixes are compacted into vals_next.  A suffix
+// whose group is now a singleton has its final index, so its suffix array
+// entry is written here (sa_out, unless null), in sorted order.  Wave w of
+// the tile takes positions [w * 1024, (w + 1) * 1024) of it, 64 consecutive
+// ones per step: the running head indexes and the kept count are wave scans
+// carried from step to step, started from the earlier waves' totals and the
+// tile prefix.
 __global__ void __launch_bounds__(kSegThreads) k_seg_apply(const uint64_t* __restrict__ keys,
                                                              const uint32_t* __restrict__ vals, uint32_t U,
                                                              uint32_t sb, int round0,
@@ -661,35 +663,65 @@ __global__ void __launch_bounds__(kSegThreads) k_seg_apply(const uint64_t* __res
                                                              const uint32_t* __restrict__ pre_g,
                                                              const uint32_t* __restrict__ pre_k,
                                                              uint32_t* __restrict__ rank,
-                                                             uint32_t* __restrict__ vals_next) {
-  __shared__ uint32_t scratch[kSegThreads / fc::kWave + 1];
-  const uint32_t r0 = blockIdx.x * kSegTile + threadIdx.x * kSegItems;
+                                                             uint32_t* __restrict__ vals_next,
+                                                             uint32_t* __restrict__ sa_out) {
+  constexpr int kWaves = kSegThreads / fc::kWave;
+  constexpr uint32_t kPerWave = kSegTile / kWaves;
+  __shared__ uint32_t s_tot[3][kWaves];
+  const int w = (int)threadIdx.x / fc::kWave;
+  const uint32_t lane = (uint32_t)fc::lane_id();
+  const uint32_t base = blockIdx.x * kSegTile + (uint32_t)w * kPerWave;
+  const bool r0f = round0 != 0;
+  // the wave's totals
   uint32_t mh = 0, mg = 0, kc = 0;
   for (int j = 0; j < kSegItems; ++j) {
-    const uint32_t r = r0 + j;
-    if (r >= U) break;
-    const SegFlags f = seg_flags(keys, U, r, sb, round0 != 0);
-    if (f.new_head) mh = r;
-    if (f.old_head) mg = r;
-    kc += f.keep ? 1u : 0u;
+    const uint32_t r = base + (uint32_t)j * fc::kWave + lane;
+    if (r < U) {
+      const SegFlags f = seg_flags(keys, U, r, sb, r0f);
+      if (f.new_head) mh = r;
+      if (f.old_head) mg = r;
+      kc += f.keep ? 1u : 0u;
+    }
   }
-  uint32_t eh = fc::block_excl_max<uint32_t>(mh, 0u, scratch);
-  uint32_t eg = fc::block_excl_max<uint32_t>(mg, 0u, scratch);
-  uint32_t ek = fc::block_excl_sum<uint32_t>(kc, scratch, nullptr);
-  const uint32_t th = pre_h[blockIdx.x], tg = pre_g[blockIdx.x];
-  uint32_t hh = eh > th ? eh : th;
-  uint32_t gg = eg > tg ? eg : tg;
-  uint32_t out = pre_k[blockIdx.x] + ek;
+  mh = fc::wave_max<uint32_t>(mh);
+  mg = fc::wave_max<uint32_t>(mg);
+  kc = fc::wave_sum<uint32_t>(kc);
+  if (lane == 0) {
+    s_tot[0][w] = mh;
+    s_tot[1][w] = mg;
+    s_tot[2][w] = kc;
+  }
+  __syncthreads();
+  uint32_t hh = pre_h[blockIdx.x], gg = pre_g[blockIdx.x], out = pre_k[blockIdx.x];
+  for (int v = 0; v < w; ++v) {
+    hh = s_tot[0][v] > hh ? s_tot[0][v] : hh;
+    gg = s_tot[1][v] > gg ? s_tot[1][v] : gg;
+    out += s_tot[2][v];
+  }
   for (int j = 0; j < kSegItems; ++j) {
-    const uint32_t r = r0 + j;
-    if (r >= U) break;
-    const SegFlags f = seg_flags(keys, U, r, sb, round0 != 0);
-    if (f.new_head) hh = r;
-    if (f.old_head) gg = r;
-    const uint32_t start = round0 ? 0u : (uint32_t)(keys[r] >> sb);
-    const uint32_t i = vals[r];
-    rank[i] = start + (hh - gg);
-    if (f.keep) vals_next[out++] = i;
+    const uint32_t r = base + (uint32_t)j * fc::kWave + lane;
+    const bool valid = r < U;
+    SegFlags f{false, false, false};
+    if (valid) f = seg_flags(keys, U, r, sb, r0f);
+    uint32_t hr = fc::wave_incl_max<uint32_t>(f.new_head ? r : 0u);
+    uint32_t gr = fc::wave_incl_max<uint32_t>(f.old_head ? r : 0u);
+    const uint32_t kr = fc::wave_incl_sum_u32(f.keep ? 1u : 0u);
+    hr = hr > hh ? hr : hh;
+    gr = gr > gg ? gr : gg;
+    if (valid) {
+      const uint32_t start = r0f ? 0u : (uint32_t)(keys[r] >> sb);
+      const uint32_t i = vals[r];
+      const uint32_t rk = start + (hr - gr);
+      // in the first new group of its old group a suffix keeps its rank (the
+      // old group start, already in rank[i]): only round 0 and the later
+      // new groups write
+      if (r0f || hr != gr) rank[i] = rk;
+      if (f.keep) vals_next[out + kr - 1u] = i;
+      else if (sa_out) sa_out[rk] = i;  // a singleton group: rk is the suffix's final index
+    }
+    hh = __shfl(hr, fc::kWave - 1);
+    gg = __shfl(gr, fc::kWave - 1);
+    out += __shfl(kr, fc::kWave - 1);
   }
 }
 
@@ -965,7 +997,8 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
                        w.misc + 1);
     FC_CHECK_LAUNCH();
     hipLaunchKernelGGL(k_seg_apply, dim3(seg_tiles), dim3(kSegThreads), 0, stream, w.keys[res], w.vals[res], U, sb,
-                       round == 0 ? 1 : 0, w.part_h, w.part_g, w.part_k, w.rank, w.vals[res ^ 1]);
+                       round == 0 ? 1 : 0, w.part_h, w.part_g, w.part_k, w.rank, w.vals[res ^ 1],
+                       ext ? nullptr : sa_out);
     FC_CHECK_LAUNCH();
     uint32_t host_misc[2] = {0, 0};
     FC_CHECK_HIP(hipMemcpyAsync(host_misc, w.misc, sizeof(uint32_t) * 2, hipMemcpyDeviceToHost, stream));
@@ -983,8 +1016,8 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
     if (U == 0) break;
   }
   if (ext) return FC_OK;
-  hipLaunchKernelGGL(k_scatter_sa, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, w.rank, N, sa_out);
-  FC_CHECK_LAUNCH();
+  // every suffix array entry was written when its suffix's group became a
+  // singleton (k_seg_apply)
   if (n_seg > 0) {
     hipLaunchKernelGGL(k_localize_sa, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, sa_out, N, w.seg_off, n_seg);
     FC_CHECK_LAUNCH();
