@@ -36,7 +36,7 @@ WORKLOADS = {"headline": 3, "two-store": 2, "single": 1, "replay": 3, "replay-ca
 # kernels each entry point launches (rocprofv3 kernel names start with these)
 ENTRY_KERNELS = {
     "fc_retrieve": ("k_search", "k_offsets", "k_gather"),
-    "fc_build_tree": ("k_tree_fast", "k_tree_any"),
+    "fc_build_tree": ("k_tree_plan", "k_tree_flat", "k_tree_fast", "k_tree_any"),
     "fc_verify_accept": ("k_verify",),
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_headline_10M_1B.txt")
