@@ -125,11 +125,17 @@ __device__ __forceinline__ int rec_cmp(const uint4& h0, const uint4& h1, const R
 }
 
 // Search of query b by the whole workgroup: s_lo / s_hi[s][n_max - n] get
-// the bounds of every tried (store, n); untried entries stay 0.
+// the bounds of every tried (store, n) that can still matter; untried
+// entries stay 0.  Only the longest n with an occurrence counts per store,
+// so once both bounds of some n are known and enclose a non-empty range
+// (s_best[s] = n), the tasks of that store's shorter lengths stop at their
+// next round trip: those are the short suffixes whose two-token ranges are
+// the largest, and the slowest searches.  Their entries are left partial;
+// the keep step never looks below the longest non-empty n.
 __device__ __forceinline__ void search_query(const StoreArgs& st, int S, const uint16_t* __restrict__ ctx, int b,
                                              int L, int n_max, int n_min, int G, int log2_2g, uint16_t* s_q,
                                              uint32_t (*s_lo)[FC_MAX_NMAX], uint32_t (*s_hi)[FC_MAX_NMAX],
-                                             int* s_nhi) {
+                                             int* s_nhi, uint32_t (*s_done)[FC_MAX_NMAX], int* s_best) {
   const int tid = (int)threadIdx.x;
   const int lane = fc::lane_id();
   const int nq = L < FC_MAX_NMAX ? L : FC_MAX_NMAX;
@@ -137,7 +143,9 @@ __device__ __forceinline__ void search_query(const StoreArgs& st, int S, const u
   if (tid < FC_MAX_SOURCES * FC_MAX_NMAX) {
     (&s_lo[0][0])[tid] = 0;
     (&s_hi[0][0])[tid] = 0;
+    (&s_done[0][0])[tid] = 0;
   }
+  if (tid < FC_MAX_SOURCES) s_best[tid] = 0;
   __syncthreads();
   if (tid == 0) {
     int tail = 0;
@@ -208,6 +216,18 @@ __device__ __forceinline__ void search_query(const StoreArgs& st, int S, const u
       lo = hi;  // range already final: its end is the upper bound
     }
   }
+  // a task's final bound: recorded, and the second bound of a (store, n)
+  // to arrive raises the store's best n when the range is non-empty
+  auto finish = [&](uint32_t bound) {
+    if (gl != 0) return;
+    if (upper) s_hi[s][ni] = bound; else s_lo[s][ni] = bound;
+    if (atomicAdd(&s_done[s][ni], 1u) == 1u) {
+      const uint32_t a = *(volatile uint32_t*)&s_lo[s][ni];
+      const uint32_t z = *(volatile uint32_t*)&s_hi[s][ni];
+      if (z > a) atomicMax(&s_best[s], n);
+    }
+  };
+  if (act && !kary) finish(lo);
   {
     const RecQuery rq = rec_query(q, act ? n : 2);
     const uint4* R = st.rec[s];
@@ -218,6 +238,7 @@ __device__ __forceinline__ void search_query(const StoreArgs& st, int S, const u
     bool searching = kary;
     while (fc::ballot(searching) != 0) {
       bool ca = false, cb = false;
+      if (searching && n < *(volatile int*)&s_best[s]) searching = false;  // a longer n has occurrences
       if (searching) {
         const uint64_t span = hi - lo;
         const uint32_t pa = lo + (uint32_t)(((uint64_t)(2 * gl + 1) * span) >> log2_2g);
@@ -246,11 +267,9 @@ __device__ __forceinline__ void search_query(const StoreArgs& st, int S, const u
         lo = plo;
         hi = phi;
         searching = lo < hi;
+        if (!searching) finish(lo);
       }
     }
-  }
-  if (act && gl == 0) {
-    if (upper) s_hi[s][ni] = lo; else s_lo[s][ni] = lo;
   }
   __syncthreads();
 }
@@ -269,12 +288,14 @@ __global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, 
   __shared__ uint32_t s_lo[FC_MAX_SOURCES][FC_MAX_NMAX];
   __shared__ uint32_t s_hi[FC_MAX_SOURCES][FC_MAX_NMAX];
   __shared__ int s_nhi;
+  __shared__ uint32_t s_done[FC_MAX_SOURCES][FC_MAX_NMAX];
+  __shared__ int s_best[FC_MAX_SOURCES];
   const int b = (int)blockIdx.x;
   const int row = fc::map_row(rows, n_rows, b);
   if (row < 0) return;  // skipped query: the whole workgroup leaves
   const int tid = (int)threadIdx.x;
   const int lane = fc::lane_id();
-  search_query(st, S, ctx, b, L, n_max, n_min, G, log2_2g, s_q, s_lo, s_hi, &s_nhi);
+  search_query(st, S, ctx, b, L, n_max, n_min, G, log2_2g, s_q, s_lo, s_hi, &s_nhi, s_done, s_best);
   if (tid < fc::kWave) {
     const int NN = n_max - n_min + 1;
     const int n_hi = s_nhi;
