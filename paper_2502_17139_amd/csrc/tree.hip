@@ -1322,7 +1322,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
                                                             const uint16_t* __restrict__ cont_tok,
                                                             const uint16_t* __restrict__ ctx, int L, int S, int k,
                                                             int m, int c, Alpha alpha, int cap, int words,
-                                                            const int32_t* __restrict__ order, int B,
+                                                            const int32_t* __restrict__ order, int self_plan, int B,
                                                             const int32_t* __restrict__ rows, int n_rows,
                                                             int32_t* __restrict__ num_nodes,
                                                             int32_t* __restrict__ node_tok,
@@ -1361,7 +1361,52 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   // with three stores or more, short lists past the LDS cap go to the
   // full-LDS kernel; with two, they are searched in place (slower, rare)
   auto deferred = [&](const QueryShape& qs) { return S > 2 && !qs.bad && qs.T - qs.n_long > cap; };
-  const int b = order ? order[blockIdx.x] : (int)blockIdx.x;
+  // this workgroup's query: from the planning launch's order, from the same
+  // order worked out here (self_plan: every workgroup classifies the batch,
+  // scans the class counts and picks the query at its own position, which
+  // saves the planning launch when nothing is deferred), or by index
+  __shared__ int s_self_b;
+  int b = (int)blockIdx.x;
+  if (order) {
+    b = order[blockIdx.x];
+  } else if (self_plan) {
+    const int per = (B + NT - 1) / NT;
+    const int q0 = (int)threadIdx.x * per < B ? (int)threadIdx.x * per : B;
+    const int q1 = q0 + per < B ? q0 + per : B;
+    auto cls = [&](int q) {
+      const int T2 = query_shape(taken, S, k, rows, n_rows, q).T;
+      return T2 >= 2048 ? 0 : T2 > 256 ? 1 : 2;
+    };
+    uint32_t n0 = 0, n1 = 0, n2 = 0;
+    for (int q = q0; q < q1; ++q) {
+      const int cq = cls(q);
+      n0 += cq == 0;
+      n1 += cq == 1;
+      n2 += cq == 2;
+    }
+    if (threadIdx.x == 0) s_self_b = (int)blockIdx.x;  // overwritten below: every position has one query
+    uint32_t e0, e1, e2, ez, t0, t1, t2, tz;
+    Scan2<NT>::run(n0, n1, s_x, s_y, &e0, &e1, &t0, &t1);
+    Scan2<NT>::run(n2, 0u, s_x, s_y, &e2, &ez, &t2, &tz);
+    const uint32_t pos = blockIdx.x;
+    const int want = pos < t0 ? 0 : (pos < t0 + t1 ? 1 : 2);
+    const uint32_t r = want == 0 ? pos : (want == 1 ? pos - t0 : pos - t0 - t1);
+    const uint32_t e = want == 0 ? e0 : (want == 1 ? e1 : e2);
+    const uint32_t nn = want == 0 ? n0 : (want == 1 ? n1 : n2);
+    if (r >= e && r < e + nn) {
+      uint32_t seen = e;
+      for (int q = q0; q < q1; ++q) {
+        if (cls(q) != want) continue;
+        if (seen == r) {
+          s_self_b = q;
+          break;
+        }
+        ++seen;
+      }
+    }
+    __syncthreads();
+    b = s_self_b;
+  }
   const QueryShape qs = query_shape(taken, S, k, rows, n_rows, b);
   if (deferred(qs)) return;
   const int R = c + 1;
@@ -2167,7 +2212,8 @@ fc_status launch_flat(const int32_t* taken, const uint8_t* cont_len, const uint1
   int32_t* order = (int32_t*)ws;
   int32_t* defer_list = order + B;
   int32_t* counts = order + 2 * (size_t)B;
-  const bool plan = defer || B > 256;
+  const bool plan = defer;          // a planning launch (which also lists the deferred queries)
+  const int self_plan = !defer && B > 256;  // else the flat workgroups order themselves
   const int words = ((((uintptr_t)cont_tok) & 3) == 0 && (m % 2) == 0) ? 1 : 0;
   (void)hipGetLastError();
   if (plan) {
@@ -2176,7 +2222,8 @@ fc_status launch_flat(const int32_t* taken, const uint8_t* cont_len, const uint1
     FC_CHECK_LAUNCH();
   }
   hipLaunchKernelGGL((k_tree_flat<MAXM, NARROW>), dim3(B), dim3(kFlatThreads), lay.total, stream, taken, cont_len,
-                     cont_tok, ctx, L, S, k, m, t.c, a, cap, words, plan ? order : nullptr, B, rows, n_rows,
+                     cont_tok, ctx, L, S, k, m, t.c, a, cap, words, plan ? order : nullptr, self_plan, B, rows,
+                     n_rows,
                      num_nodes, node_tok, parent, weight, pos_ids, mask);
   FC_CHECK_LAUNCH();
   if (defer) {
