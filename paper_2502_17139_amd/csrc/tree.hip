@@ -1115,6 +1115,13 @@ constexpr int kFlatThreads = 512;
 constexpr int kFlatRows = 4;       // long-string loads in flight per lane
 constexpr int kFlatShortCap = 256;  // short strings a query may keep in LDS
 constexpr int kFlatShared = 2048;   // shared trie nodes (two strings or more) listed in LDS
+// The list is two halves: nodes of weight below kListHeavy fill it from the
+// bottom, heavier ones from the top.  The selection needs every node of
+// weight >= W*; when W* >= kListHeavy the top half alone serves, so a
+// query with thousands of light shared nodes (where W* is large) keeps the
+// list-based selection.
+constexpr uint32_t kListHeavy = 16;
+constexpr uint32_t kHalfShared = kFlatShared / 2;
 constexpr int kFlatCand = 512;      // candidates of the list-based selection (one per thread)
 static_assert(kFlatCand <= kFlatThreads, "one candidate per thread");
 
@@ -1352,7 +1359,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   __shared__ uint64_t s_shallow[FC_MAX_TREE_ROWS / fc::kWave][MAXM + 1];
   __shared__ int16_t s_end[FC_MAX_TREE_ROWS];
   __shared__ uint32_t s_pick[3];
-  __shared__ uint32_t s_nsh;
+  __shared__ uint32_t s_nsh, s_nsh_hi;
   __shared__ uint32_t s_ncand;
 
   const int tid = threadIdx.x;
@@ -1722,6 +1729,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     }
     if (tid == 0) {
       s_nsh = 0;
+      s_nsh_hi = 0;
       s_ncand = 0;
     }
     __syncthreads();
@@ -1803,10 +1811,12 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       walk([&](int, int lo, int hi, uint32_t Wt) { count(Wt, (uint32_t)(hi - lo)); },
            [&](int q, int d, uint32_t Wt) {
              count(Wt, 1u);
-             const uint32_t o = atomicAdd(&s_nsh, 1u);
-             if (o < (uint32_t)kFlatShared) {
-               sh_key[o] = ((uint32_t)q << 5) | (uint32_t)d;
-               sh_w[o] = (SWT)Wt;
+             const bool hv = Wt >= kListHeavy;
+             const uint32_t o = atomicAdd(hv ? &s_nsh_hi : &s_nsh, 1u);
+             if (o < kHalfShared) {
+               const uint32_t at = hv ? (uint32_t)kFlatShared - 1u - o : o;
+               sh_key[at] = ((uint32_t)q << 5) | (uint32_t)d;
+               sh_w[at] = (SWT)Wt;
              }
            });
       const uint32_t x1 = fc::wave_sum_u32(r1), x2 = fc::wave_sum_u32(r2), xb = fc::wave_sum_u32(rbig);
@@ -1815,8 +1825,10 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       if (lane == 0 && xb) atomicAdd(&s_pick[2], xb);
     }
     __syncthreads();
-    const uint32_t n_shared = s_nsh;
-    const bool listed = n_shared <= (uint32_t)kFlatShared;
+    const uint32_t n_lo = s_nsh, n_hi = s_nsh_hi;
+    const uint32_t n_shared = n_lo + n_hi;  // shared nodes seen (listed or not)
+    (void)n_shared;
+    const bool listed_hi = n_hi <= kHalfShared, listed_all = listed_hi && n_lo <= kHalfShared;
 
     // 6. the need-th largest weight W* and how many nodes of weight W* to
     //    take (in (p, d) order)
@@ -1896,14 +1908,25 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     for (int u = 1; u < FC_MAX_SOURCES; ++u)
       if (u < S && alpha.a[u] > tail_max) tail_max = alpha.a[u];
     const bool tails_eq = alpha_flat && a0 > 0 && wstar == a0;
+    const bool listed = wstar >= kListHeavy ? listed_hi : listed_all;
     bool fast_emit = listed && need > 0 && (wstar > tail_max || tails_eq);
     uint32_t* cand_key = (uint32_t*)(smem + lay.sstr);
     uint32_t* cand_w = cand_key + kFlatCand;
     if (fast_emit) {
-      for (uint32_t i = tid; i < n_shared; i += NT) {
-        const uint32_t Wt = (uint32_t)sh_w[i];
-        if (Wt >= wstar) {
-          const uint32_t o = atomicAdd(&s_ncand, 1u);
+      // the top half, and the bottom one when W* is below its weights; one
+      // LDS atomic per wave and pass: ballot, popcount, lane offsets
+      const uint32_t n_scan = n_hi + (wstar >= kListHeavy ? 0u : n_lo);
+      for (uint32_t i0 = 0; i0 < n_scan; i0 += NT) {
+        const uint32_t x = i0 + (uint32_t)tid;
+        const uint32_t i = x < n_hi ? (uint32_t)kFlatShared - 1u - x : x - n_hi;  // top half first
+        const uint32_t Wt = x < n_scan ? (uint32_t)sh_w[i] : 0u;
+        const bool take = x < n_scan && Wt >= wstar;
+        const uint64_t bl = fc::ballot(take);
+        uint32_t base = 0;
+        if (lane == 0 && bl) base = atomicAdd(&s_ncand, (uint32_t)__popcll(bl));
+        base = (uint32_t)__shfl((int)base, 0);
+        if (take) {
+          const uint32_t o = base + (uint32_t)__popcll(bl & fc::lanemask_lt());
           if (o < (uint32_t)kFlatCand) {
             cand_key[o] = sh_key[i];
             cand_w[o] = Wt;
@@ -1946,14 +1969,30 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     if (fast_emit) {
       // one candidate per thread (kFlatCand <= NT): whether it is kept (an
       // equal-weight one is kept when fewer than take_eq equal-weight
-      // candidates precede it), then its row among the kept ones
+      // candidates precede it), then its row among the kept ones.  The
+      // candidate list is padded to a multiple of four with keys that count
+      // for nothing, and both counts read it as 16-byte quads, four quads in
+      // flight, instead of one LDS round trip per candidate.
       const uint32_t nc = s_ncand;
+      const uint32_t nc4 = (nc + 3u) & ~3u;
       const uint32_t i = (uint32_t)tid;
+      if (i >= nc && i < nc4) {
+        cand_key[i] = 0xFFFFFFFFu;  // above every key, flagged or not
+        cand_w[i] = 0u;
+      }
+      __syncthreads();
+      const uint4* ck4 = (const uint4*)cand_key;
+      const uint4* cw4 = (const uint4*)cand_w;
       const uint32_t key = i < nc ? cand_key[i] : 0u, Wt = i < nc ? cand_w[i] : 0u;
       bool keep = i < nc && Wt > wstar;
       if (i < nc && !keep) {
         uint32_t before = 0;
-        for (uint32_t j = 0; j < nc; ++j) before += (cand_w[j] == wstar && cand_key[j] < key) ? 1u : 0u;
+#pragma unroll 4
+        for (uint32_t j = 0; j < nc4 / 4; ++j) {
+          const uint4 kk = ck4[j], ww = cw4[j];
+          before += (ww.x == wstar && kk.x < key) + (ww.y == wstar && kk.y < key) + (ww.z == wstar && kk.z < key) +
+                    (ww.w == wstar && kk.w < key);
+        }
         keep = before < take_eq;
       }
       __syncthreads();
@@ -1962,7 +2001,12 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       if (keep) {
         const uint32_t kf = key | 0x80000000u;
         uint32_t o = 1;
-        for (uint32_t j = 0; j < nc; ++j) o += cand_key[j] < kf && (cand_key[j] & 0x80000000u) ? 1u : 0u;
+#pragma unroll 4
+        for (uint32_t j = 0; j < nc4 / 4; ++j) {
+          const uint4 kk = ck4[j];
+          o += (kk.x < kf && (kk.x & 0x80000000u)) + (kk.y < kf && (kk.y & 0x80000000u)) +
+               (kk.z < kf && (kk.z & 0x80000000u)) + (kk.w < kf && (kk.w & 0x80000000u));
+        }
         if (o < (uint32_t)FC_MAX_TREE_ROWS) {
           s_sel_p[o] = (uint16_t)(key >> 5);
           s_sel_d[o] = (uint8_t)(key & 31u);
