@@ -204,6 +204,24 @@ uint64_t fc_record_bytes(uint64_t n);
 fc_status fc_store_prepare_records(const uint16_t* tokens, const uint32_t* sa, uint64_t n, void* rec_out,
                                    hipStream_t stream);
 
+/*
+ * Optional top-level sample of a store's records for the suffix search of
+ * Section III-A: entry t is the first FC_TOP_BYTES = 32 bytes of record
+ * t * FC_TOP_STRIDE (its suffix-array entry and tokens 2..15), for t = 0 ..
+ * ceil(n / FC_TOP_STRIDE) - 1.  A search whose two-token range spans more
+ * than two sample strides first narrows the range over the sample (a dense
+ * array of n / 8 bytes: 125 MB at n = 1e9, small enough to stay in the
+ * memory-side cache), then finishes inside one stride of the records, so
+ * most of its dependent round trips avoid the 64-byte-per-suffix records.
+ * Results are identical with or without it.
+ * top_out is fc_store_top_bytes(n) bytes, 32-byte aligned, written on
+ * `stream` from the store's records (rec, as from fc_store_prepare_records).
+ */
+#define FC_TOP_STRIDE 256
+#define FC_TOP_BYTES 32
+uint64_t fc_store_top_bytes(uint64_t n);
+fc_status fc_store_prepare_top(const void* rec, uint64_t n, void* top_out, hipStream_t stream);
+
 /* A read-only view of one store; all pointers are device pointers. */
 typedef struct fc_store {
   const uint16_t* tokens; /* [n] text */
@@ -213,6 +231,7 @@ typedef struct fc_store {
   const uint32_t* pair;   /* optional two-token table from fc_store_prepare_pairs, or NULL */
   uint32_t pair_vocab;    /* its V (ignored when pair is NULL) */
   const void* rec;        /* optional records from fc_store_prepare_records (needs pair), or NULL */
+  const void* top;        /* optional sample from fc_store_prepare_top (needs rec), or NULL */
 } fc_store;
 
 /* ------------------------------------------------------------------------ */

@@ -35,6 +35,7 @@ EXPORTS = (
     "fc_datastore_build_workspace_bytes", "fc_datastore_build", "fc_datastore_build_batched_workspace_bytes",
     "fc_datastore_build_batched", "fc_datastore_extend_workspace_bytes", "fc_datastore_extend", "fc_store_prepare",
     "fc_pair_table_entries", "fc_store_prepare_pairs", "fc_record_bytes", "fc_store_prepare_records",
+    "fc_store_top_bytes", "fc_store_prepare_top",
     "fc_retrieve_workspace_bytes", "fc_retrieve", "fc_build_tree_workspace_bytes", "fc_build_tree",
     "fc_verify_accept", "fc_targets_from_truth", "fc_cache_lds_bytes", "fc_cache_retrieve", "fc_cache_write",
     "fc_tree_attention", "fc_replay_init", "fc_replay_run", "fc_retrieve_noalloc_max_bytes", "fc_retrieve_noalloc",
@@ -53,7 +54,7 @@ class FcError(RuntimeError):
 class FcStore(ctypes.Structure):
     _fields_ = [("tokens", ctypes.c_void_p), ("sa", ctypes.c_void_p), ("bucket", ctypes.c_void_p),
                 ("n", ctypes.c_uint64), ("pair", ctypes.c_void_p), ("pair_vocab", ctypes.c_uint32),
-                ("rec", ctypes.c_void_p)]
+                ("rec", ctypes.c_void_p), ("top", ctypes.c_void_p)]
 
 
 FC_MAX_BUILD_ROUNDS = 40
@@ -134,6 +135,10 @@ def lib() -> ctypes.CDLL:
     L.fc_record_bytes.argtypes = [u64]
     L.fc_store_prepare_records.restype = ctypes.c_int
     L.fc_store_prepare_records.argtypes = [vp, vp, u64, vp, vp]
+    L.fc_store_top_bytes.restype = u64
+    L.fc_store_top_bytes.argtypes = [u64]
+    L.fc_store_prepare_top.restype = ctypes.c_int
+    L.fc_store_prepare_top.argtypes = [vp, u64, vp, vp]
     L.fc_retrieve_workspace_bytes.restype = sz
     L.fc_retrieve_workspace_bytes.argtypes = [i32, i32, FcRetrieveParams]
     L.fc_retrieve.restype = ctypes.c_int
@@ -351,13 +356,23 @@ def fc_store_prepare_records(tokens: torch.Tensor, sa: torch.Tensor, rec_out: to
     return rec_out
 
 
+def fc_store_prepare_top(rec: torch.Tensor, n: int, top_out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Top-level sample of the records (uint8[32 * ceil(n / 256)]): the first
+    32 bytes of every 256th record."""
+    if top_out is None:
+        top_out = _empty(max(int(lib().fc_store_top_bytes(n)), 1), torch.uint8, rec.device)
+    _check("fc_store_prepare_top", lib().fc_store_prepare_top(_ptr(rec), n, _ptr(top_out), _stream(stream)))
+    return top_out
+
+
 class Store:
     """A datastore resident on the GPU: tokens, suffix array, bucket table and,
     with pair_vocab = V, the optional two-token table; with records = True
-    (needs pair_vocab) also the inline-prefix records."""
+    (needs pair_vocab) also the inline-prefix records and, unless top = False,
+    their top-level sample."""
 
     def __init__(self, tokens: torch.Tensor, sa: torch.Tensor | None = None, bucket: torch.Tensor | None = None,
-                 pair_vocab: int | None = None, records: bool = False, stream=None):
+                 pair_vocab: int | None = None, records: bool = False, top: bool | None = None, stream=None):
         if tokens.dtype != torch.uint16 or tokens.dim() != 1 or not tokens.is_cuda or not tokens.is_contiguous():
             raise ValueError("tokens must be a contiguous 1-D uint16 device tensor")
         for name, t, shape in (("sa", sa, (tokens.numel(),)), ("bucket", bucket, (FC_BUCKETS,))):
@@ -373,6 +388,10 @@ class Store:
         if records and not pair_vocab:
             raise ValueError("records need the two-token table (pair_vocab)")
         self.rec = fc_store_prepare_records(tokens, self.sa, stream=stream) if records else None
+        if top and not records:
+            raise ValueError("the top-level sample needs the records")
+        use_top = records if top is None else top
+        self.top = fc_store_prepare_top(self.rec, self.n, stream=stream) if use_top and self.n > 0 else None
 
     @property
     def n(self) -> int:
@@ -381,7 +400,8 @@ class Store:
     def view(self) -> FcStore:
         return FcStore(self.tokens.data_ptr(), self.sa.data_ptr(), self.bucket.data_ptr(), self.n,
                        None if self.pair is None else self.pair.data_ptr(), self.pair_vocab,
-                       None if self.rec is None else self.rec.data_ptr())
+                       None if self.rec is None else self.rec.data_ptr(),
+                       None if self.top is None else self.top.data_ptr())
 
 
 # ------------------------------------------------------------ retrieval ----

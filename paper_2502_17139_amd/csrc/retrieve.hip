@@ -52,6 +52,7 @@ struct StoreArgs {
   const uint32_t* bucket[FC_MAX_SOURCES];
   const uint32_t* pair[FC_MAX_SOURCES];
   const uint4* rec[FC_MAX_SOURCES];
+  const uint4* top[FC_MAX_SOURCES];  // sample of every FC_TOP_STRIDE-th record's first 32 bytes, or null
   uint32_t n[FC_MAX_SOURCES];
   uint32_t pair_vocab[FC_MAX_SOURCES];
 };
@@ -231,25 +232,40 @@ __device__ __forceinline__ void search_query(const StoreArgs& st, int S, const u
   {
     const RecQuery rq = rec_query(q, act ? n : 2);
     const uint4* R = st.rec[s];
+    const uint4* TP = st.top[s];
     const bool two = n > 8;  // tokens past offset 7 sit in the record's second quad
     const int gbase = lane - gl;
     const uint64_t gmask = G >= 64 ? ~0ull : ((1ull << G) - 1);
     const int P = 2 * G - 1;  // pivots per round trip
     bool searching = kary;
+    // A range spanning two sample strides or more is first searched over the
+    // sample: the positions t * FC_TOP_STRIDE in [lo, hi) are t in [ta, tb),
+    // and the first t whose record is not below the bound brackets the bound
+    // within one stride of records.
+    uint32_t ta = 0, tb = 0;
+    bool in_top = false;
+    if (kary && TP != nullptr) {
+      ta = (uint32_t)(((uint64_t)lo + FC_TOP_STRIDE - 1) / FC_TOP_STRIDE);
+      tb = (uint32_t)(((uint64_t)hi + FC_TOP_STRIDE - 1) / FC_TOP_STRIDE);
+      in_top = tb > ta + 1;
+    }
+    uint32_t clo = in_top ? ta : lo, chi = in_top ? tb : hi;  // the interval of the current phase
     while (fc::ballot(searching) != 0) {
       bool ca = false, cb = false;
       if (searching && n < *(volatile int*)&s_best[s]) searching = false;  // a longer n has occurrences
       if (searching) {
-        const uint64_t span = hi - lo;
-        const uint32_t pa = lo + (uint32_t)(((uint64_t)(2 * gl + 1) * span) >> log2_2g);
+        const uint64_t span = chi - clo;
+        const uint32_t pa = clo + (uint32_t)(((uint64_t)(2 * gl + 1) * span) >> log2_2g);
         const bool vb = 2 * gl + 2 <= P;
-        const uint32_t pb = vb ? lo + (uint32_t)(((uint64_t)(2 * gl + 2) * span) >> log2_2g) : pa;
-        const uint4 a0 = R[kRecQuads * (uint64_t)pa];
-        const uint4 b0 = R[kRecQuads * (uint64_t)pb];
+        const uint32_t pb = vb ? clo + (uint32_t)(((uint64_t)(2 * gl + 2) * span) >> log2_2g) : pa;
+        const uint4* Qa = in_top ? TP + 2 * (uint64_t)pa : R + kRecQuads * (uint64_t)pa;
+        const uint4* Qb = in_top ? TP + 2 * (uint64_t)pb : R + kRecQuads * (uint64_t)pb;
+        const uint4 a0 = Qa[0];
+        const uint4 b0 = Qb[0];
         uint4 a1 = make_uint4(0, 0, 0, 0), b1 = a1;
         if (two) {
-          a1 = R[kRecQuads * (uint64_t)pa + 1];
-          b1 = R[kRecQuads * (uint64_t)pb + 1];
+          a1 = Qa[1];
+          b1 = Qb[1];
         }
         const int c1 = rec_cmp(a0, a1, rq);
         const int c2 = rec_cmp(b0, b1, rq);
@@ -261,13 +277,21 @@ __device__ __forceinline__ void search_query(const StoreArgs& st, int S, const u
       if (searching) {
         // the pivots before the bound form a prefix of the 2G - 1 pivots
         const int c = __popcll((ba >> gbase) & gmask) + __popcll((bb >> gbase) & gmask);
-        const uint64_t span = hi - lo;
-        const uint32_t plo = c > 0 ? lo + (uint32_t)(((uint64_t)c * span) >> log2_2g) + 1 : lo;
-        const uint32_t phi = c < P ? lo + (uint32_t)(((uint64_t)(c + 1) * span) >> log2_2g) : hi;
-        lo = plo;
-        hi = phi;
-        searching = lo < hi;
-        if (!searching) finish(lo);
+        const uint64_t span = chi - clo;
+        const uint32_t plo = c > 0 ? clo + (uint32_t)(((uint64_t)c * span) >> log2_2g) + 1 : clo;
+        const uint32_t phi = c < P ? clo + (uint32_t)(((uint64_t)(c + 1) * span) >> log2_2g) : chi;
+        clo = plo;
+        chi = phi;
+        if (clo >= chi && in_top) {
+          // sample t = clo is the first not below the bound (tb: none is):
+          // the bound lies in ((t - 1) * stride, t * stride]
+          const uint32_t t = clo;
+          clo = t > ta ? (t - 1) * FC_TOP_STRIDE + 1 : lo;
+          chi = t < tb ? t * FC_TOP_STRIDE : hi;
+          in_top = false;
+        }
+        searching = clo < chi;
+        if (!searching) finish(clo);
       }
     }
   }
@@ -749,6 +773,8 @@ fc_status retrieve_check(const fc_store* stores, int32_t S, const uint16_t* ctx,
     if (x.pair && (x.pair_vocab < 1 || x.pair_vocab > 65536)) return FC_ERR_INVALID;
     if (x.rec && (!x.pair || ((uintptr_t)x.rec & (FC_RECORD_BYTES - 1)))) return FC_ERR_INVALID;
     st.rec[s] = x.n > 0 ? (const uint4*)x.rec : nullptr;
+    if (x.top && (!x.rec || ((uintptr_t)x.top & (FC_TOP_BYTES - 1)))) return FC_ERR_INVALID;
+    st.top[s] = x.n > 0 ? (const uint4*)x.top : nullptr;
   }
   if (B == 0) return FC_OK;
   if (!ctx || !match_n || !range_lo || !range_cnt || !taken || !cont_pos || !cont_src || !cont_len || !cont_tok)

@@ -1235,6 +1235,37 @@ extern "C" fc_status fc_store_prepare_pairs(const uint16_t* tokens, const uint32
 
 extern "C" uint64_t fc_record_bytes(uint64_t n) { return (uint64_t)FC_RECORD_BYTES * n; }
 
+namespace {
+
+// entry t of the top-level sample: the first two 16-byte quads of record
+// t * FC_TOP_STRIDE
+__global__ void __launch_bounds__(256) k_top(const uint4* __restrict__ rec, uint64_t n_top,
+                                               uint4* __restrict__ top) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;  // one quad per thread
+  if (i >= 2 * n_top) return;
+  const uint64_t t = i >> 1, q = i & 1;
+  top[i] = rec[(t * FC_TOP_STRIDE) * (FC_RECORD_BYTES / 16) + q];
+}
+
+}  // namespace
+
+extern "C" uint64_t fc_store_top_bytes(uint64_t n) {
+  return ((n + FC_TOP_STRIDE - 1) / FC_TOP_STRIDE) * (uint64_t)FC_TOP_BYTES;
+}
+
+extern "C" fc_status fc_store_prepare_top(const void* rec, uint64_t n, void* top_out, hipStream_t stream) {
+  if (n >= 0xFFFFFFFFull) return FC_ERR_INVALID;
+  if (n == 0) return FC_OK;
+  if (!rec || !top_out || ((uintptr_t)rec & (FC_RECORD_BYTES - 1)) || ((uintptr_t)top_out & (FC_TOP_BYTES - 1)))
+    return FC_ERR_INVALID;
+  const uint64_t n_top = (n + FC_TOP_STRIDE - 1) / FC_TOP_STRIDE;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(k_top, dim3(fc::div_up(2 * n_top, 256)), dim3(256), 0, stream, (const uint4*)rec, n_top,
+                     (uint4*)top_out);
+  FC_CHECK_LAUNCH();
+  return FC_OK;
+}
+
 extern "C" fc_status fc_store_prepare_records(const uint16_t* tokens, const uint32_t* sa, uint64_t n, void* rec_out,
                                               hipStream_t stream) {
   if (n >= 0xFFFFFFFFull) return FC_ERR_INVALID;

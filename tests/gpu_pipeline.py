@@ -26,8 +26,9 @@ def host(t: torch.Tensor) -> np.ndarray:
     return t.cpu().numpy()
 
 
-def gpu_store(tokens: np.ndarray, pair_vocab: int | None = None, records: bool = False) -> fc.Store:
-    return fc.Store(dev(tokens.astype(np.uint16)), pair_vocab=pair_vocab, records=records)
+def gpu_store(tokens: np.ndarray, pair_vocab: int | None = None, records: bool = False,
+              top: bool | None = None) -> fc.Store:
+    return fc.Store(dev(tokens.astype(np.uint16)), pair_vocab=pair_vocab, records=records, top=top)
 
 
 def gpu_pipeline(stores, ctx: np.ndarray, p: dict, alpha, c: int) -> dict:

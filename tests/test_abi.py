@@ -114,6 +114,12 @@ def test_retrieve_rejects_null_outputs_and_big_store(L):
     views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, 1, 100, 48))  # records not 64-byte aligned
     args[0] = views
     assert L.fc_retrieve(*args) == 1
+    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, None, 0, None, 32))  # a sample without records
+    args[0] = views
+    assert L.fc_retrieve(*args) == 1
+    views = (fc.FcStore * 1)(fc.FcStore(1, 1, 1, 10, 1, 100, 64, 48))  # a sample not 32-byte aligned
+    args[0] = views
+    assert L.fc_retrieve(*args) == 1
 
 
 def _tree_args(B=1, L_=2, S=2, k=10, m=4, c=8, alpha=(1, 1, 0, 0)):
@@ -182,6 +188,19 @@ def test_record_size_and_rejects(L):
     assert L.fc_store_prepare_records(one, None, 10, aligned, None) == 1
     assert L.fc_store_prepare_records(one, one, 1 << 32, aligned, None) == 1
     assert L.fc_store_prepare_records(None, None, 0, None, None) == 0  # nothing to write
+
+
+def test_top_sample_size_and_rejects(L):
+    # one 32-byte entry per started stride of 256 suffixes
+    assert L.fc_store_top_bytes(1_001_999_999) == 32 * 3_914_063
+    assert L.fc_store_top_bytes(256) == 32 and L.fc_store_top_bytes(257) == 64 and L.fc_store_top_bytes(0) == 0
+    rec, top = ctypes.c_void_p(64), ctypes.c_void_p(32)
+    assert L.fc_store_prepare_top(None, 10, top, None) == 1
+    assert L.fc_store_prepare_top(rec, 10, None, None) == 1
+    assert L.fc_store_prepare_top(ctypes.c_void_p(32), 10, top, None) == 1  # records misaligned
+    assert L.fc_store_prepare_top(rec, 10, ctypes.c_void_p(16), None) == 1  # sample misaligned
+    assert L.fc_store_prepare_top(rec, 1 << 32, top, None) == 1
+    assert L.fc_store_prepare_top(None, 0, None, None) == 0  # nothing to write
 
 
 def test_verify_and_build_reject(L):

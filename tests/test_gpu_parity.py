@@ -303,7 +303,8 @@ def test_first_workload_full_batch():
     st = gpu_store(t)
     st_pairs = fc.Store(st.tokens, st.sa, st.bucket, pair_vocab=synth.VOCAB)
     st_rec = fc.Store(st.tokens, st.sa, st.bucket, pair_vocab=synth.VOCAB, records=True)
-    variants = {P["k"]: st_rec, 1000: st_pairs, 1200: st_rec}
+    st_rec_only = fc.Store(st.tokens, st.sa, st.bucket, pair_vocab=synth.VOCAB, records=True, top=False)
+    variants = {P["k"]: st_rec, 1000: st_pairs, 1200: st_rec, 257: st_rec_only}
     for (k, m, c) in ((P["k"], P["m"], P["c"]), (1000, 10, 64), (257, 3, 5), (1200, 13, 40), (1, 1, 1)):
         say(f"workload 1: k={k} m={m} c={c}")
         p = dict(P, k=k, m=m)
@@ -522,7 +523,8 @@ def test_fuzz_small_stores(seed):
 def test_fuzz_many_tiny_cases():
     """About 1.2e4 query cases on tiny adversarial stores: 48 seeded store
     sets (one to four stores, vocabularies of 2 to 300 tokens, empty and
-    one-token stores, with and without pair tables and records) x 64 queries
+    one-token stores, with and without pair tables, records and the records'
+    top-level sample) x 64 queries
     of 1 to 19 tokens x four parameter sets (the paper's n and budgets
     scaled down, n_min = 1, m > 16 through the any-m gather and tree, and
     k = m = c = 1).  Every retrieval, tree and acceptance output against the
@@ -545,7 +547,9 @@ def test_fuzz_many_tiny_cases():
                                        fc.fc_store_prepare(dev(np.zeros(1, np.uint16))[:0],
                                                            dev(np.zeros(1, np.uint32))[:0])))
             else:
-                stores.append(gpu_store(t, vocab if seed % 2 else None, records=seed % 4 == 1))
+                # records with their top-level sample (seed % 4 == 1) and without it (== 3)
+                stores.append(gpu_store(t, vocab if seed % 2 else None, records=seed % 2 == 1,
+                                        top=seed % 4 == 1 if seed % 2 else None))
         rows = []
         for b in range(64):
             src = texts[int(rng.integers(S))]
