@@ -1,21 +1,24 @@
 """Build libfastcoder.so (HIP for gfx950) in place.
 
 hipcc cross-compiles for gfx950 without a GPU present.  Every kernel source
-and the C ABI file go into one shared library next to this file.
+and the C ABI file are compiled to objects side by side (one hipcc process
+per source), then linked into one shared library next to this file.
 """
 from __future__ import annotations
 
 import glob
 import os
 import subprocess
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libfastcoder.so")
+OBJ_DIR = os.path.join(ROOT, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-Wall", "-Wno-unused-function",
     # keep the compiler from emitting packed FP32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -28,11 +31,24 @@ def sources() -> list:
     return src
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into libfastcoder.so; returns its path."""
+def build(verbose: bool = False, jobs: int | None = None) -> str:
+    """Compile every HIP source and link libfastcoder.so; returns its path."""
+    os.makedirs(OBJ_DIR, exist_ok=True)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc")]
+
+    def compile_one(src: str) -> str:
+        obj = os.path.join(OBJ_DIR, os.path.basename(src) + ".o")
+        cmd = [HIPCC, *FLAGS, *inc, "-c", src, "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.check_call(cmd)
+        return obj
+
+    src = sources()
+    with ThreadPoolExecutor(max_workers=jobs or min(len(src), os.cpu_count() or 1, 16)) as ex:
+        objs = list(ex.map(compile_one, src))
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
-           *sources(), "-o", tmp]
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)

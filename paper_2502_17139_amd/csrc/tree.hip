@@ -484,6 +484,44 @@ struct Scan2 {
   }
 };
 
+template <int NT>
+struct Scan3 {
+  // Exclusive prefix sums of v[0..3) over the block and their totals, plus
+  // the block total of z; two barriers.  s holds 4 x (NT/64) words.
+  __device__ __forceinline__ static void run(const uint32_t (&v)[3], uint32_t z, uint32_t* s, uint32_t (&ex)[3],
+                                             uint32_t (&tot)[3], uint32_t* tz) {
+    constexpr int NW = NT / fc::kWave;
+    const int w = (int)threadIdx.x / fc::kWave;
+    uint32_t inc[3];
+#pragma unroll
+    for (int u = 0; u < 3; ++u) inc[u] = fc::wave_incl_sum_u32(v[u]);
+    const uint32_t iz = fc::wave_sum_u32(z);
+    if (fc::lane_id() == fc::kWave - 1) {
+#pragma unroll
+      for (int u = 0; u < 3; ++u) s[u * NW + w] = inc[u];
+      s[3 * NW + w] = iz;
+    }
+    __syncthreads();
+    uint32_t az = 0;
+#pragma unroll
+    for (int u = 0; u < 3; ++u) {
+      uint32_t pre = 0, all = 0;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) {
+        const uint32_t x = s[u * NW + i];
+        pre += i < w ? x : 0u;
+        all += x;
+      }
+      ex[u] = pre + inc[u] - v[u];
+      tot[u] = all;
+    }
+#pragma unroll
+    for (int i = 0; i < NW; ++i) az += s[3 * NW + i];
+    *tz = az;
+    __syncthreads();
+  }
+};
+
 // NARROW: every store has the same alpha and alpha * k fits 16 bits, so the
 // alpha prefix sums are linear and every node weight is stored as is; the
 // hot loops are compiled without the general paths.
@@ -1114,16 +1152,7 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
 constexpr int kFlatThreads = 512;
 constexpr int kFlatRows = 4;       // long-string loads in flight per lane
 constexpr int kFlatShortCap = 256;  // short strings a query may keep in LDS
-constexpr int kFlatShared = 2048;   // shared trie nodes (two strings or more) listed in LDS
-// The list is two halves: nodes of weight below kListHeavy fill it from the
-// bottom, heavier ones from the top.  The selection needs every node of
-// weight >= W*; when W* >= kListHeavy the top half alone serves, so a
-// query with thousands of light shared nodes (where W* is large) keeps the
-// list-based selection.
-constexpr uint32_t kListHeavy = 16;
-constexpr uint32_t kHalfShared = kFlatShared / 2;
-constexpr int kFlatCand = 512;      // candidates of the list-based selection (one per thread)
-static_assert(kFlatCand <= kFlatThreads, "one candidate per thread");
+constexpr int kFlatList = 2048;     // shared trie nodes (two strings or more) listed in LDS
 
 struct FlatLayout {
   size_t perm, lm, A, sstr, slen, sidx, sh_key, sh_w, total;
@@ -1141,17 +1170,17 @@ __host__ __device__ inline FlatLayout flat_layout(int k, int maxm, int cap, int 
   o = align_up(o + (size_t)k * (maxm <= 15 ? 1 : 2), 16);
   t.A = o;  // k+1 uint32 alpha prefix sums
   if (with_A) o = align_up(o + (size_t)(k + 1) * 4, 16);
-  t.sstr = o;  // cap rows of maxm/2 words; later the selection's candidates
-  const size_t rows = (size_t)cap * maxm * 2, cand = (size_t)kFlatCand * 8;
-  o = align_up(o + (rows > cand ? rows : cand), 16);
+  t.sstr = o;  // cap rows of maxm/2 words; later the kept tail nodes
+  const size_t rows = (size_t)cap * maxm * 2, tails = (size_t)FC_MAX_TREE_ROWS * 4;
+  o = align_up(o + (rows > tails ? rows : tails), 16);
   t.slen = o;  // cap uint8
   o = align_up(o + (size_t)cap, 16);
   t.sidx = o;  // cap uint16: short merged order -> LDS row
   if (S > 2) o = align_up(o + (size_t)cap * 2, 16);
-  t.sh_key = o;  // shared trie nodes: (merged position, depth)
-  o = align_up(o + (size_t)kFlatShared * 4, 16);
+  t.sh_key = o;  // shared trie nodes in (position, depth) order: position << 5 | depth
+  o = align_up(o + (size_t)kFlatList * 4, 16);
   t.sh_w = o;  // their weights (16 bits when no weight can exceed them)
-  o = align_up(o + (size_t)kFlatShared * (with_A ? 4 : 2), 16);
+  o = align_up(o + (size_t)kFlatList * (with_A ? 4 : 2), 16);
   t.total = o;
   return t;
 }
@@ -1359,8 +1388,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   __shared__ uint64_t s_shallow[FC_MAX_TREE_ROWS / fc::kWave][MAXM + 1];
   __shared__ int16_t s_end[FC_MAX_TREE_ROWS];
   __shared__ uint32_t s_pick[3];
-  __shared__ uint32_t s_nsh, s_nsh_hi;
-  __shared__ uint32_t s_ncand;
+  __shared__ uint32_t s_scan4[4 * NW];
 
   const int tid = threadIdx.x;
   const int lane = fc::lane_id();
@@ -1701,11 +1729,15 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     // 4. chunk sums: alpha, non-empty strings (root weight), nodes, and the
     //    chunk's first head per depth (first q with lcp[q] < d), then the
     //    next head per depth after the chunk
+    //    and the chunk's shared nodes (depths past its own LCP, up to the
+    //    next string's), which fix where the chunk's part of the list of
+    //    shared nodes starts
     const uint32_t a0 = alpha.a[0];
-    uint32_t asum = 0, rw = 0, nodes = 0;
+    uint32_t asum = 0, rw = 0, nodes = 0, nsh = 0;
     uint16_t f[MAXM + 1];
 #pragma unroll
     for (int d = 0; d <= MAXM; ++d) f[d] = (uint16_t)T;
+    int l_after = p1 < T ? (int)((uint32_t)lm[p1] & kLo) : 0;
     for (int p = p1 - 1; p >= p0; --p) {
       const uint32_t x = lm[p];
       const int l = (int)(x & kLo), li = (int)(x >> kSh);
@@ -1713,12 +1745,25 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       asum += a;
       if (li > 0) rw += a;
       nodes += (uint32_t)(li - l);
+      const int top = li < l_after ? li : l_after;
+      nsh += top > l ? (uint32_t)(top - l) : 0u;
+      l_after = l;
 #pragma unroll
       for (int d = 1; d <= MAXM; ++d)
         if (l < d) f[d] = (uint16_t)p;
     }
-    uint32_t a_ex, dummy, a_tot, n_tot;
-    Scan2<NT>::run(asum, nodes, s_x, s_y, &a_ex, &dummy, &a_tot, &n_tot, rw, s_z, &root_w);
+    uint32_t a_ex, a_tot, n_tot, sh_ex, sh_tot;
+    {
+      const uint32_t v3[3] = {asum, nodes, nsh};
+      uint32_t ex3[3], tot3[3];
+      Scan3<NT>::run(v3, rw, s_scan4, ex3, tot3, &root_w);
+      a_ex = ex3[0];
+      sh_ex = ex3[2];
+      a_tot = tot3[0];
+      n_tot = tot3[1];
+      sh_tot = tot3[2];
+    }
+    const bool listed = sh_tot <= (uint32_t)kFlatList;
     uint16_t nh[MAXM + 1];
 #pragma unroll
     for (int d = 1; d <= MAXM; ++d) {
@@ -1726,11 +1771,6 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       nh[d] = (uint16_t)T;
       if (d <= m) nh[d] = (uint16_t)fc::wave_excl_suffix_min_u32(f[d], (uint32_t)T, &wave_min);
       if (lane == 0) s_wmin[w][d] = (uint16_t)wave_min;
-    }
-    if (tid == 0) {
-      s_nsh = 0;
-      s_nsh_hi = 0;
-      s_ncand = 0;
     }
     __syncthreads();
     if (tid < NW * MAXM) {
@@ -1798,9 +1838,13 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     SWT* sh_w = (SWT*)(smem + lay.sh_w);
 
     // 5. weight histogram: 1 and 2 (the bulk) in registers, other weights
-    //    below 256 by LDS atomics, heavier ones only counted; the shared
-    //    nodes are listed on the way (while they fit) for the selection
+    //    below 256 by LDS atomics, heavier ones only counted.  The shared
+    //    nodes go to the list on the way: the walk meets a chunk's shared
+    //    nodes in reverse (position, depth) order, so it fills the chunk's
+    //    part of the list from its end, and the list comes out in (position,
+    //    depth) order with no atomics.
     {
+      uint32_t at = sh_ex + nsh;
       uint32_t r1 = 0, r2 = 0, rbig = 0;
       auto count = [&](uint32_t Wt, uint32_t n) {
         r1 += Wt == 1u ? n : 0u;
@@ -1811,10 +1855,8 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       walk([&](int, int lo, int hi, uint32_t Wt) { count(Wt, (uint32_t)(hi - lo)); },
            [&](int q, int d, uint32_t Wt) {
              count(Wt, 1u);
-             const bool hv = Wt >= kListHeavy;
-             const uint32_t o = atomicAdd(hv ? &s_nsh_hi : &s_nsh, 1u);
-             if (o < kHalfShared) {
-               const uint32_t at = hv ? (uint32_t)kFlatShared - 1u - o : o;
+             if (listed) {
+               --at;
                sh_key[at] = ((uint32_t)q << 5) | (uint32_t)d;
                sh_w[at] = (SWT)Wt;
              }
@@ -1825,10 +1867,6 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       if (lane == 0 && xb) atomicAdd(&s_pick[2], xb);
     }
     __syncthreads();
-    const uint32_t n_lo = s_nsh, n_hi = s_nsh_hi;
-    const uint32_t n_shared = n_lo + n_hi;  // shared nodes seen (listed or not)
-    (void)n_shared;
-    const bool listed_hi = n_hi <= kHalfShared, listed_all = listed_hi && n_lo <= kHalfShared;
 
     // 6. the need-th largest weight W* and how many nodes of weight W* to
     //    take (in (p, d) order)
@@ -1895,122 +1933,96 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     const uint32_t wstar = prefix;
     const uint32_t take_eq = remaining;
 
-    // 7. kept nodes in (p, d) order = preorder.  When every tail is lighter
-    //    than W* (the usual case) the kept nodes are shared ones: they are
-    //    gathered as candidates (weight >= W*), each learns how many
-    //    candidates precede it, and the first take_eq of weight W* are kept.
-    //    With one store weight and W* equal to it, every shared node is kept
-    //    (its weight is at least twice that) and so are the first take_eq
-    //    tail nodes in (p, d) order, which join the candidates.  Otherwise
-    //    the chunks count their kept nodes and emit them in order.
+    // 7. kept nodes in (p, d) order = preorder.  The list of shared nodes
+    //    (weight of two strings or more) is already in that order.  When
+    //    every tail is lighter than W* (the usual case) the kept nodes are
+    //    the listed ones heavier than W* and the first take_eq of weight W*:
+    //    each thread counts both over a contiguous piece of the list, and
+    //    one scan gives every kept node its row.  With one store weight and
+    //    W* equal to it, every shared node is kept (its weight is at least
+    //    twice that) and so are the first take_eq tail nodes in (p, d)
+    //    order; the two ordered lists are merged by binary search.
+    //    Otherwise (a list that did not fit) the chunks count their kept
+    //    nodes in a walk and emit them in order.
     uint32_t tail_max = a0;
 #pragma unroll
     for (int u = 1; u < FC_MAX_SOURCES; ++u)
       if (u < S && alpha.a[u] > tail_max) tail_max = alpha.a[u];
     const bool tails_eq = alpha_flat && a0 > 0 && wstar == a0;
-    const bool listed = wstar >= kListHeavy ? listed_hi : listed_all;
     bool fast_emit = listed && need > 0 && (wstar > tail_max || tails_eq);
-    uint32_t* cand_key = (uint32_t*)(smem + lay.sstr);
-    uint32_t* cand_w = cand_key + kFlatCand;
-    if (fast_emit) {
-      // the top half, and the bottom one when W* is below its weights; one
-      // LDS atomic per wave and pass: ballot, popcount, lane offsets
-      const uint32_t n_scan = n_hi + (wstar >= kListHeavy ? 0u : n_lo);
-      for (uint32_t i0 = 0; i0 < n_scan; i0 += NT) {
-        const uint32_t x = i0 + (uint32_t)tid;
-        const uint32_t i = x < n_hi ? (uint32_t)kFlatShared - 1u - x : x - n_hi;  // top half first
-        const uint32_t Wt = x < n_scan ? (uint32_t)sh_w[i] : 0u;
-        const bool take = x < n_scan && Wt >= wstar;
-        const uint64_t bl = fc::ballot(take);
-        uint32_t base = 0;
-        if (lane == 0 && bl) base = atomicAdd(&s_ncand, (uint32_t)__popcll(bl));
-        base = (uint32_t)__shfl((int)base, 0);
-        if (take) {
-          const uint32_t o = base + (uint32_t)__popcll(bl & fc::lanemask_lt());
-          if (o < (uint32_t)kFlatCand) {
-            cand_key[o] = sh_key[i];
-            cand_w[o] = Wt;
-          }
+    if (fast_emit && !tails_eq) {
+      const uint32_t pl = (sh_tot + NT - 1) / NT;
+      const uint32_t e0 = (uint32_t)tid * pl < sh_tot ? (uint32_t)tid * pl : sh_tot;
+      const uint32_t e1 = e0 + pl < sh_tot ? e0 + pl : sh_tot;
+      uint32_t g = 0, e = 0;
+      for (uint32_t i = e0; i < e1; ++i) {
+        const uint32_t Wt = sh_w[i];
+        g += Wt > wstar ? 1u : 0u;
+        e += Wt == wstar ? 1u : 0u;
+      }
+      uint32_t gb, eb, gtot, etot;
+      Scan2<NT>::run(g, e, s_x, s_y, &gb, &eb, &gtot, &etot);
+      for (uint32_t i = e0; i < e1 && (g > 0 || eb < take_eq); ++i) {
+        const uint32_t Wt = sh_w[i];
+        uint32_t row = 0;
+        if (Wt > wstar) {
+          row = 1 + gb + (eb < take_eq ? eb : take_eq);
+          ++gb;
+          --g;
+        } else if (Wt == wstar && eb < take_eq) {
+          row = 1 + gb + eb;
+          ++eb;
+        }
+        if (row > 0 && row < (uint32_t)FC_MAX_TREE_ROWS) {
+          const uint32_t key = sh_key[i];
+          s_sel_p[row] = (uint16_t)(key >> 5);
+          s_sel_d[row] = (uint8_t)(key & 31u);
+          s_sel_w[row] = Wt;
         }
       }
-      if (tails_eq) {
-        // the first take_eq tail nodes: tails of position q are the depths
-        // past both its own LCP and the next string's
-        auto tails_of = [&](int q, int& lo, int& hi) {
-          const uint32_t x = lm[q];
-          const int l = (int)(x & kLo), ml = (int)(x >> kSh);
-          const int ln = q + 1 < T ? (int)((uint32_t)lm[q + 1] & kLo) : 0;
-          lo = l > ln ? l : ln;
-          hi = ml;
-        };
-        uint32_t nt = 0;
-        for (int q = p0; q < p1; ++q) {
-          int lo, hi;
-          tails_of(q, lo, hi);
-          nt += hi > lo ? (uint32_t)(hi - lo) : 0u;
-        }
-        uint32_t t_ex, dmy, t_tot, dmy2;
-        Scan2<NT>::run(nt, 0u, s_x, s_y, &t_ex, &dmy, &t_tot, &dmy2);
-        for (int q = p0; q < p1 && t_ex < take_eq; ++q) {
-          int lo, hi;
-          tails_of(q, lo, hi);
-          for (int d = lo + 1; d <= hi && t_ex < take_eq; ++d, ++t_ex) {
-            const uint32_t o = atomicAdd(&s_ncand, 1u);
-            if (o < (uint32_t)kFlatCand) {
-              cand_key[o] = ((uint32_t)q << 5) | (uint32_t)d;
-              cand_w[o] = a0;
-            }
-          }
-        }
+      nsel = (int)(need < (uint32_t)c ? need : (uint32_t)c);
+    } else if (fast_emit) {
+      // the first take_eq tail nodes, in (p, d) order: tails of position q
+      // are the depths past both its own LCP and the next string's
+      uint32_t* tail_key = (uint32_t*)(smem + lay.sstr);
+      auto tails_of = [&](int q, int& lo, int& hi) {
+        const uint32_t x = lm[q];
+        const int l = (int)(x & kLo), ml = (int)(x >> kSh);
+        const int ln = q + 1 < T ? (int)((uint32_t)lm[q + 1] & kLo) : 0;
+        lo = l > ln ? l : ln;
+        hi = ml;
+      };
+      uint32_t nt = 0;
+      for (int q = p0; q < p1; ++q) {
+        int lo, hi;
+        tails_of(q, lo, hi);
+        nt += hi > lo ? (uint32_t)(hi - lo) : 0u;
+      }
+      uint32_t t_ex, dmy, t_tot, dmy2;
+      Scan2<NT>::run(nt, 0u, s_x, s_y, &t_ex, &dmy, &t_tot, &dmy2);
+      for (int q = p0; q < p1 && t_ex < take_eq; ++q) {
+        int lo, hi;
+        tails_of(q, lo, hi);
+        for (int d = lo + 1; d <= hi && t_ex < take_eq; ++d, ++t_ex) tail_key[t_ex] = ((uint32_t)q << 5) | (uint32_t)d;
       }
       __syncthreads();
-      fast_emit = s_ncand <= (uint32_t)kFlatCand;
-    }
-    if (fast_emit) {
-      // one candidate per thread (kFlatCand <= NT): whether it is kept (an
-      // equal-weight one is kept when fewer than take_eq equal-weight
-      // candidates precede it), then its row among the kept ones.  The
-      // candidate list is padded to a multiple of four with keys that count
-      // for nothing, and both counts read it as 16-byte quads, four quads in
-      // flight, instead of one LDS round trip per candidate.
-      const uint32_t nc = s_ncand;
-      const uint32_t nc4 = (nc + 3u) & ~3u;
-      const uint32_t i = (uint32_t)tid;
-      if (i >= nc && i < nc4) {
-        cand_key[i] = 0xFFFFFFFFu;  // above every key, flagged or not
-        cand_w[i] = 0u;
-      }
-      __syncthreads();
-      const uint4* ck4 = (const uint4*)cand_key;
-      const uint4* cw4 = (const uint4*)cand_w;
-      const uint32_t key = i < nc ? cand_key[i] : 0u, Wt = i < nc ? cand_w[i] : 0u;
-      bool keep = i < nc && Wt > wstar;
-      if (i < nc && !keep) {
-        uint32_t before = 0;
-#pragma unroll 4
-        for (uint32_t j = 0; j < nc4 / 4; ++j) {
-          const uint4 kk = ck4[j], ww = cw4[j];
-          before += (ww.x == wstar && kk.x < key) + (ww.y == wstar && kk.y < key) + (ww.z == wstar && kk.z < key) +
-                    (ww.w == wstar && kk.w < key);
+      // a listed node's row: its list index plus the kept tails before it;
+      // a kept tail's: its index plus the listed nodes before it
+      for (uint32_t i = (uint32_t)tid; i < sh_tot + take_eq; i += NT) {
+        const bool is_tail = i >= sh_tot;
+        const uint32_t j = is_tail ? i - sh_tot : i;
+        const uint32_t key = is_tail ? tail_key[j] : sh_key[j];
+        const uint32_t* other = is_tail ? sh_key : tail_key;
+        uint32_t lo = 0, hi = is_tail ? sh_tot : take_eq;
+        while (lo < hi) {
+          const uint32_t mid = (lo + hi) >> 1;
+          if (other[mid] < key) lo = mid + 1; else hi = mid;
         }
-        keep = before < take_eq;
-      }
-      __syncthreads();
-      if (keep) cand_key[i] = key | 0x80000000u;
-      __syncthreads();
-      if (keep) {
-        const uint32_t kf = key | 0x80000000u;
-        uint32_t o = 1;
-#pragma unroll 4
-        for (uint32_t j = 0; j < nc4 / 4; ++j) {
-          const uint4 kk = ck4[j];
-          o += (kk.x < kf && (kk.x & 0x80000000u)) + (kk.y < kf && (kk.y & 0x80000000u)) +
-               (kk.z < kf && (kk.z & 0x80000000u)) + (kk.w < kf && (kk.w & 0x80000000u));
-        }
-        if (o < (uint32_t)FC_MAX_TREE_ROWS) {
-          s_sel_p[o] = (uint16_t)(key >> 5);
-          s_sel_d[o] = (uint8_t)(key & 31u);
-          s_sel_w[o] = Wt;
+        const uint32_t row = 1 + j + lo;
+        if (row < (uint32_t)FC_MAX_TREE_ROWS) {
+          s_sel_p[row] = (uint16_t)(key >> 5);
+          s_sel_d[row] = (uint8_t)(key & 31u);
+          s_sel_w[row] = is_tail ? a0 : (uint32_t)sh_w[j];
         }
       }
       nsel = (int)(need < (uint32_t)c ? need : (uint32_t)c);
