@@ -32,6 +32,12 @@ __device__ __forceinline__ uint32_t dpp_mov(uint32_t x) {
 constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
 constexpr int kRowShl1 = 0x101, kRowShl2 = 0x102, kRowShl4 = 0x104, kRowShl8 = 0x108;
 
+// The value of the lane below (lane 0 gets `fill`): one DPP wave shift
+// (wave_shr:1 crosses the rows of 16 lanes).
+__device__ __forceinline__ uint32_t wave_shr1(uint32_t x, uint32_t fill) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)fill, (int)x, 0x138, 0xF, 0xF, false);
+}
+
 // Inclusive prefix sum over the 64 lanes.
 __device__ __forceinline__ uint32_t wave_incl_sum_u32(uint32_t v) {
   const int r = lane_id() & 15;

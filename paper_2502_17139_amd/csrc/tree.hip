@@ -450,7 +450,8 @@ template <int NT>
 struct Scan2 {
   // Exclusive prefix sums of (x, y) over the block plus their totals, and
   // optionally the block total of z; two barriers.
-  __device__ static void run(uint32_t x, uint32_t y, uint32_t* sx, uint32_t* sy, uint32_t* ex, uint32_t* ey,
+  __device__ __forceinline__ static void run(uint32_t x, uint32_t y, uint32_t* sx, uint32_t* sy, uint32_t* ex,
+                                             uint32_t* ey,
                              uint32_t* tx, uint32_t* ty, uint32_t z = 0, uint32_t* sz = nullptr,
                              uint32_t* tz = nullptr) {
     constexpr int NW = NT / fc::kWave;
@@ -1405,6 +1406,9 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   if (order) {
     b = order[blockIdx.x];
   } else if (self_plan) {
+    // a thread's queries: the first kPlanRegs classes are kept in registers
+    // (all loads issued at once), later ones are classified again
+    constexpr int kPlanRegs = 4;
     const int per = (B + NT - 1) / NT;
     const int q0 = (int)threadIdx.x * per < B ? (int)threadIdx.x * per : B;
     const int q1 = q0 + per < B ? q0 + per : B;
@@ -1412,17 +1416,25 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       const int T2 = query_shape(taken, S, k, rows, n_rows, q).T;
       return T2 >= 2048 ? 0 : T2 > 256 ? 1 : 2;
     };
-    uint32_t n0 = 0, n1 = 0, n2 = 0;
-    for (int q = q0; q < q1; ++q) {
+    int creg[kPlanRegs];
+#pragma unroll
+    for (int i = 0; i < kPlanRegs; ++i) creg[i] = q0 + i < q1 ? cls(q0 + i) : 3;
+    uint32_t n0 = 0, n1 = 0;
+#pragma unroll
+    for (int i = 0; i < kPlanRegs; ++i) {
+      n0 += creg[i] == 0;
+      n1 += creg[i] == 1;
+    }
+    for (int q = q0 + kPlanRegs; q < q1; ++q) {
       const int cq = cls(q);
       n0 += cq == 0;
       n1 += cq == 1;
-      n2 += cq == 2;
     }
+    const uint32_t n2 = (uint32_t)(q1 - q0) - n0 - n1;
     if (threadIdx.x == 0) s_self_b = (int)blockIdx.x;  // overwritten below: every position has one query
-    uint32_t e0, e1, e2, ez, t0, t1, t2, tz;
+    uint32_t e0, e1, t0, t1;
     Scan2<NT>::run(n0, n1, s_x, s_y, &e0, &e1, &t0, &t1);
-    Scan2<NT>::run(n2, 0u, s_x, s_y, &e2, &ez, &t2, &tz);
+    const uint32_t e2 = (uint32_t)q0 - e0 - e1;  // queries before q0 of class 2
     const uint32_t pos = blockIdx.x;
     const int want = pos < t0 ? 0 : (pos < t0 + t1 ? 1 : 2);
     const uint32_t r = want == 0 ? pos : (want == 1 ? pos - t0 : pos - t0 - t1);
@@ -1431,7 +1443,12 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     if (r >= e && r < e + nn) {
       uint32_t seen = e;
       for (int q = q0; q < q1; ++q) {
-        if (cls(q) != want) continue;
+        int cq = 0;
+#pragma unroll
+        for (int i = 0; i < kPlanRegs; ++i)
+          if (q == q0 + i) cq = creg[i];
+        if (q >= q0 + kPlanRegs) cq = cls(q);
+        if (cq != want) continue;
         if (seen == r) {
           s_self_b = q;
           break;
@@ -1643,9 +1660,9 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
         const int r = have && n_short > 0 ? rank_short(v[u], ln) : 0;
         uint32_t pv[W];
 #pragma unroll
-        for (int x = 0; x < W; ++x) pv[x] = (uint32_t)__shfl_up((int)v[u][x], 1, fc::kWave);
-        const int plen = __shfl_up(ln, 1, fc::kWave);
-        const int pr = __shfl_up(r, 1, fc::kWave);
+        for (int x = 0; x < W; ++x) pv[x] = fc::wave_shr1(v[u][x], 0u);
+        const int plen = (int)fc::wave_shr1((uint32_t)ln, 0u);
+        const int pr = (int)fc::wave_shr1((uint32_t)r, 0u);
         if (have && lane > 0) {
           if (j > 0 && cmp_words<W>(pv, plen, v[u], ln) > 0) s_err = 1;
           int l = 0;
@@ -1725,13 +1742,13 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
 
   int nsel = 0;
   uint32_t root_w = 0;
+  uint16_t row_tok = 0;  // this thread's kept row's token (row tid)
   if (!err) {
-    // 4. chunk sums: alpha, non-empty strings (root weight), nodes, and the
-    //    chunk's first head per depth (first q with lcp[q] < d), then the
-    //    next head per depth after the chunk
-    //    and the chunk's shared nodes (depths past its own LCP, up to the
-    //    next string's), which fix where the chunk's part of the list of
-    //    shared nodes starts
+    // 4. chunk sums: alpha, non-empty strings (root weight), nodes, the
+    //    chunk's shared nodes (depths past its own LCP, up to the next
+    //    string's: they fix where the chunk's part of the list of shared
+    //    nodes starts) and the chunk's first head per depth (first q with
+    //    lcp[q] < d), then the next head per depth after the chunk
     const uint32_t a0 = alpha.a[0];
     uint32_t asum = 0, rw = 0, nodes = 0, nsh = 0;
     uint16_t f[MAXM + 1];
@@ -1842,7 +1859,9 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     //    nodes go to the list on the way: the walk meets a chunk's shared
     //    nodes in reverse (position, depth) order, so it fills the chunk's
     //    part of the list from its end, and the list comes out in (position,
-    //    depth) order with no atomics.
+    //    depth) order with no atomics.  With the list, the shared nodes'
+    //    weights are counted from it after the walk (each thread a contiguous
+    //    piece), so the walk itself has no LDS atomics for them to wait on.
     {
       uint32_t at = sh_ex + nsh;
       uint32_t r1 = 0, r2 = 0, rbig = 0;
@@ -1854,13 +1873,21 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       };
       walk([&](int, int lo, int hi, uint32_t Wt) { count(Wt, (uint32_t)(hi - lo)); },
            [&](int q, int d, uint32_t Wt) {
-             count(Wt, 1u);
              if (listed) {
                --at;
                sh_key[at] = ((uint32_t)q << 5) | (uint32_t)d;
                sh_w[at] = (SWT)Wt;
+             } else {
+               count(Wt, 1u);
              }
            });
+      if (listed) {
+        __syncthreads();
+        const uint32_t pl = (sh_tot + NT - 1) / NT;
+        const uint32_t e0 = (uint32_t)tid * pl < sh_tot ? (uint32_t)tid * pl : sh_tot;
+        const uint32_t e1 = e0 + pl < sh_tot ? e0 + pl : sh_tot;
+        for (uint32_t i = e0; i < e1; ++i) count((uint32_t)sh_w[i], 1u);
+      }
       const uint32_t x1 = fc::wave_sum_u32(r1), x2 = fc::wave_sum_u32(r2), xb = fc::wave_sum_u32(rbig);
       if (lane == 0 && x1) atomicAdd(&s_hist[1], x1);
       if (lane == 0 && x2) atomicAdd(&s_hist[2], x2);
@@ -2068,6 +2095,9 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     }
     if (tid == 0) s_sel_d[0] = 0;
     __syncthreads();
+    // the kept rows' tokens are loaded now and used when the rows are
+    // written, so the load overlaps the parent search
+    if (tid >= 1 && tid <= nsel) row_tok = cont_tok[(row0 + perm[s_sel_p[tid]]) * m + s_sel_d[tid] - 1];
     // 8. parent of row r: the last row before it one level shallower (rows
     //    are in preorder and the kept set is ancestor-closed), from per-depth
     //    ballots of the first four waves' rows
@@ -2107,7 +2137,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       } else {
         const int p = s_sel_p[r];
         const int d = s_sel_d[r];
-        tk = cont_tok[(row0 + perm[p]) * m + d - 1];
+        tk = r == tid ? row_tok : cont_tok[(row0 + perm[p]) * m + d - 1];
         pr = s_par[r];
         wt = s_sel_w[r];
         ps = d;
