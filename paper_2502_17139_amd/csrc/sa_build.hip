@@ -20,7 +20,7 @@
 //
 // Each radix sort is a global digit histogram followed by one "onesweep"
 // pass per 8-bit digit (Adinets and Merrill 2022): a workgroup takes a tile
-// of 4096 keys (its tile id from an atomic ticket, so tiles start in order),
+// of 4,096 keys (its tile id from an atomic ticket, so tiles start in order),
 // ranks them stably inside the tile with wave ballots, publishes per-digit
 // tile counts and resolves its global offsets by decoupled look-back over the
 // earlier tiles, stages the tile in LDS in digit order, and writes it out in
@@ -43,7 +43,7 @@ namespace {
 
 constexpr int kSortThreads = 256;
 constexpr int kSortItems = 16;
-constexpr int kSortTile = kSortThreads * kSortItems;  // 4096 keys per tile
+constexpr int kSortTile = kSortThreads * kSortItems;  // 4,096 keys per tile
 constexpr int kRadix = 256;
 constexpr int kMaxDigits = 8;
 constexpr int kSegThreads = 256;
@@ -54,6 +54,7 @@ constexpr int kMaxPasses = 1024;  // ticket counters per build
 constexpr int kMaxRounds = 40;
 constexpr int kHistBlocks = 1024;
 constexpr uint32_t kSpinLimit = 1u << 22;
+constexpr int kLookWindow = 8;  // earlier tiles examined per look-back step
 
 constexpr uint64_t kFlagAgg = 1ull << 46;
 constexpr uint64_t kFlagInc = 2ull << 46;
@@ -77,15 +78,17 @@ __global__ void __launch_bounds__(256) k_init_keys(const uint16_t* __restrict__ 
   vals[i] = i;
 }
 
+// The high half of each key (the suffix's own rank) was written in place by
+// the previous round's k_seg_apply, in this round's order, so only the rank
+// h positions on is gathered.
 __global__ void __launch_bounds__(256) k_pair_keys(const uint32_t* __restrict__ vals, uint32_t U,
                                                      const uint32_t* __restrict__ rank, uint32_t n, uint64_t h,
-                                                     uint32_t sb, uint64_t* __restrict__ keys) {
+                                                     uint64_t* __restrict__ keys) {
   uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= U) return;
   uint32_t i = vals[r];
-  uint64_t hi = rank[i];
   uint64_t lo = ((uint64_t)i + h < n) ? (uint64_t)rank[i + h] + 1 : 0;
-  keys[r] = (hi << sb) | lo;
+  keys[r] |= lo;
 }
 
 // Batched build: position i belongs to the segment r with off[r] <= i <
@@ -420,10 +423,25 @@ __global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys,
   __shared__ uint32_t s[kMaxDigits][kRadix];
   for (int i = threadIdx.x; i < kMaxDigits * kRadix; i += blockDim.x) (&s[0][0])[i] = 0;
   __syncthreads();
-  // 64-bit index: U can come within a grid stride of 2^32
-  for (uint64_t i = blockIdx.x * blockDim.x + threadIdx.x; i < U; i += (uint64_t)gridDim.x * blockDim.x) {
-    uint64_t k = keys[i];
-    for (int d = 0; d < digits; ++d) atomicAdd(&s[d][(k >> (8 * d)) & 0xFF], 1u);
+  // 64-bit index: U can come within a grid stride of 2^32.  The keys are in
+  // the previous round's sorted order, so a wave's 64 consecutive keys
+  // mostly share their high digits: a digit the whole wave agrees on is
+  // counted with one LDS atomic instead of 64 that collide on one bin.
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t i0 = blockIdx.x * blockDim.x + (threadIdx.x & ~(uint64_t)(fc::kWave - 1)); i0 < U; i0 += stride) {
+    const uint64_t i = i0 + (uint64_t)fc::lane_id();
+    const bool valid = i < U;
+    const uint64_t k = valid ? keys[i] : 0ull;
+    const uint64_t act = fc::ballot(valid);
+    for (int d = 0; d < digits; ++d) {
+      const uint32_t dig = (uint32_t)(k >> (8 * d)) & 0xFF;
+      const uint32_t first = (uint32_t)__builtin_amdgcn_readfirstlane((int)dig);
+      if (fc::ballot(valid && dig == first) == act) {
+        if (fc::lane_id() == 0) atomicAdd(&s[d][first], (uint32_t)__popcll(act));
+      } else if (valid) {
+        atomicAdd(&s[d][dig], 1u);
+      }
+    }
   }
   __syncthreads();
   for (int i = threadIdx.x; i < digits * kRadix; i += blockDim.x) {
@@ -457,8 +475,11 @@ __global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __res
                                                            uint64_t* status, uint32_t* ticket, uint32_t epoch,
                                                            uint32_t* err) {
   __shared__ uint32_t s_tile;
-  __shared__ uint32_t s_wcnt[kSortThreads / fc::kWave][kRadix];
-  __shared__ uint32_t s_dstart[kRadix];
+  // per-wave digit counts and then per-wave offsets (below kSortTile), 16
+  // bits each: with these the LDS of a tile fits three tiles per CU, which
+  // matters because a tile spends most of its time waiting
+  __shared__ uint16_t s_wcnt[kSortThreads / fc::kWave][kRadix];
+  __shared__ uint16_t s_dstart[kRadix];  // tile-local digit starts (below kSortTile)
   __shared__ uint32_t s_gbase[kRadix];
   __shared__ uint32_t s_scan[kSortThreads / fc::kWave + 1];
   __shared__ uint64_t s_keys[kSortTile];
@@ -499,7 +520,7 @@ __global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __res
     }
     const uint32_t below = (uint32_t)__popcll(peers & lt);
     const uint32_t old = s_wcnt[w][d];
-    if (valid && below == 0) s_wcnt[w][d] = old + (uint32_t)__popcll(peers);
+    if (valid && below == 0) s_wcnt[w][d] = (uint16_t)(old + (uint32_t)__popcll(peers));
     rk[j] = old + below;
   }
   __syncthreads();
@@ -510,41 +531,15 @@ __global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __res
 #pragma unroll
   for (int ww = 0; ww < kSortThreads / fc::kWave; ++ww) {
     uint32_t c = s_wcnt[ww][t];
-    s_wcnt[ww][t] = total;
+    s_wcnt[ww][t] = (uint16_t)total;
     total += c;
   }
   uint32_t tile_sum;
-  s_dstart[t] = fc::block_excl_sum<uint32_t>(total, s_scan, &tile_sum);
-
-  // Decoupled look-back for this digit's global offset.
-  uint64_t* mine = status + (uint64_t)tile * kRadix + t;
-  uint64_t excl = 0;
-  if (tile > 0) {
-    __hip_atomic_store(mine, pack_status(epoch, kFlagAgg, total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    int64_t p = (int64_t)tile - 1;
-    uint32_t spins = 0;
-    while (p >= 0) {
-      const uint64_t s = __hip_atomic_load(status + (uint64_t)p * kRadix + t, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-      const uint64_t fl = s & kFlagMask;
-      if ((uint32_t)(s >> 48) != epoch || fl == 0) {
-        if (++spins > kSpinLimit) {
-          atomicOr(err, 1u);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-        continue;
-      }
-      excl += s & kCountMask;
-      if (fl == kFlagInc) break;
-      --p;
-    }
-  }
-  __hip_atomic_store(mine, pack_status(epoch, kFlagInc, excl + total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  s_gbase[t] = digit_base[t] + (uint32_t)excl;
+  s_dstart[t] = (uint16_t)fc::block_excl_sum<uint32_t>(total, s_scan, &tile_sum);
   __syncthreads();
 
-  // Stage in LDS in digit order.
+  // Stage in LDS in digit order (before the look-back, so the keys leave
+  // the registers while the look-back runs).
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
     const uint32_t idx = (uint32_t)(w * kSortItems * fc::kWave + j * fc::kWave + lane);
@@ -555,7 +550,56 @@ __global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __res
       s_vals[pos] = v[j];
     }
   }
+
+  // Decoupled look-back for this digit's global offset, kLookWindow earlier
+  // tiles per step: their status words are loaded together (for the block,
+  // a contiguous run per tile), then taken nearest first - aggregates are
+  // added until an inclusive prefix ends the walk; a tile that has published
+  // nothing yet makes the walk wait and reload from there.  One round trip
+  // then covers as many tiles as the window instead of one.
+  uint64_t* mine = status + (uint64_t)tile * kRadix + t;
+  uint64_t excl = 0;
+  if (tile > 0) {
+    __hip_atomic_store(mine, pack_status(epoch, kFlagAgg, total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int64_t p = (int64_t)tile - 1;  // nearest tile not yet taken
+    uint32_t spins = 0;
+    bool done = false;
+    while (!done) {
+      uint64_t sw[kLookWindow];
+#pragma unroll
+      for (int i = 0; i < kLookWindow; ++i)
+        sw[i] = p - i >= 0 ? __hip_atomic_load(status + (uint64_t)(p - i) * kRadix + t, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT)
+                           : pack_status(epoch, kFlagInc, 0);  // before tile 0: an empty prefix
+      int taken = 0;
+      bool stalled = false;
+#pragma unroll
+      for (int i = 0; i < kLookWindow; ++i) {
+        if (done || stalled) continue;
+        const uint64_t s = sw[i];
+        const uint64_t fl = s & kFlagMask;
+        if ((uint32_t)(s >> 48) != epoch || fl == 0) {
+          stalled = true;
+          continue;
+        }
+        excl += s & kCountMask;
+        ++taken;
+        if (fl == kFlagInc) done = true;
+      }
+      p -= taken;
+      if (stalled && !done) {
+        if (++spins > kSpinLimit) {
+          atomicOr(err, 1u);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+  }
+  __hip_atomic_store(mine, pack_status(epoch, kFlagInc, excl + total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  s_gbase[t] = digit_base[t] + (uint32_t)excl;
   __syncthreads();
+
   for (uint32_t i = (uint32_t)tid; i < nvalid; i += kSortThreads) {
     const uint64_t key = s_keys[i];
     const uint32_t d = (uint32_t)(key >> shift) & 0xFF;
@@ -664,6 +708,7 @@ __global__ void __launch_bounds__(kSegThreads) k_seg_apply(const uint64_t* __res
                                                              const uint32_t* __restrict__ pre_k,
                                                              uint32_t* __restrict__ rank,
                                                              uint32_t* __restrict__ vals_next,
+                                                             uint64_t* __restrict__ hi_next,
                                                              uint32_t* __restrict__ sa_out) {
   constexpr int kWaves = kSegThreads / fc::kWave;
   constexpr uint32_t kPerWave = kSegTile / kWaves;
@@ -716,7 +761,10 @@ __global__ void __launch_bounds__(kSegThreads) k_seg_apply(const uint64_t* __res
       // old group start, already in rank[i]): only round 0 and the later
       // new groups write
       if (r0f || hr != gr) rank[i] = rk;
-      if (f.keep) vals_next[out + kr - 1u] = i;
+      if (f.keep) {
+        vals_next[out + kr - 1u] = i;
+        if (hi_next) hi_next[out + kr - 1u] = (uint64_t)rk << sb;  // the next round's key, high half
+      }
       else if (sa_out) sa_out[rk] = i;  // a singleton group: rk is the suffix's final index
     }
     hh = __shfl(hr, fc::kWave - 1);
@@ -974,7 +1022,7 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
                            ext->ins, ext->isa, ext->ins_sorted, N, ext->n, h, sb, w.keys[vin]);
       else if (n_seg == 0)
         hipLaunchKernelGGL(k_pair_keys, dim3(fc::div_up(U, 256)), dim3(256), 0, stream, w.vals[vin], U, w.rank, N,
-                           h, sb, w.keys[vin]);
+                           h, w.keys[vin]);
       else
         hipLaunchKernelGGL(k_pair_keys_seg, dim3(fc::div_up(U, 256)), dim3(256), 0, stream, w.vals[vin], U, w.rank,
                            w.end_of, h, sb, w.keys[vin]);
@@ -998,7 +1046,7 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
     FC_CHECK_LAUNCH();
     hipLaunchKernelGGL(k_seg_apply, dim3(seg_tiles), dim3(kSegThreads), 0, stream, w.keys[res], w.vals[res], U, sb,
                        round == 0 ? 1 : 0, w.part_h, w.part_g, w.part_k, w.rank, w.vals[res ^ 1],
-                       ext ? nullptr : sa_out);
+                       (ext || n_seg > 0) ? nullptr : w.keys[res ^ 1], ext ? nullptr : sa_out);
     FC_CHECK_LAUNCH();
     uint32_t host_misc[2] = {0, 0};
     FC_CHECK_HIP(hipMemcpyAsync(host_misc, w.misc, sizeof(uint32_t) * 2, hipMemcpyDeviceToHost, stream));
