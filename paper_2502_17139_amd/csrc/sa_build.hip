@@ -427,19 +427,33 @@ __global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys,
   // the previous round's sorted order, so a wave's 64 consecutive keys
   // mostly share their high digits: a digit the whole wave agrees on is
   // counted with one LDS atomic instead of 64 that collide on one bin.
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  for (uint64_t i0 = blockIdx.x * blockDim.x + (threadIdx.x & ~(uint64_t)(fc::kWave - 1)); i0 < U; i0 += stride) {
-    const uint64_t i = i0 + (uint64_t)fc::lane_id();
-    const bool valid = i < U;
-    const uint64_t k = valid ? keys[i] : 0ull;
-    const uint64_t act = fc::ballot(valid);
-    for (int d = 0; d < digits; ++d) {
-      const uint32_t dig = (uint32_t)(k >> (8 * d)) & 0xFF;
-      const uint32_t first = (uint32_t)__builtin_amdgcn_readfirstlane((int)dig);
-      if (fc::ballot(valid && dig == first) == act) {
-        if (fc::lane_id() == 0) atomicAdd(&s[d][first], (uint32_t)__popcll(act));
-      } else if (valid) {
-        atomicAdd(&s[d][dig], 1u);
+  // Each wave takes kHistRun runs of 64 consecutive keys per step, their
+  // loads issued together.
+  constexpr int kHistRun = 4;
+  const uint64_t wave0 = (uint64_t)blockIdx.x * blockDim.x * kHistRun + (threadIdx.x & ~(uint32_t)(fc::kWave - 1)) * kHistRun;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x * kHistRun;
+  for (uint64_t i0 = wave0; i0 < U; i0 += stride) {
+    uint64_t kv[kHistRun];
+#pragma unroll
+    for (int u = 0; u < kHistRun; ++u) {
+      const uint64_t i = i0 + (uint64_t)(u * fc::kWave + fc::lane_id());
+      kv[u] = i < U ? keys[i] : 0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < kHistRun; ++u) {
+      const uint64_t i = i0 + (uint64_t)(u * fc::kWave + fc::lane_id());
+      const bool valid = i < U;
+      const uint64_t k = kv[u];
+      const uint64_t act = fc::ballot(valid);
+      if (act == 0) continue;
+      for (int d = 0; d < digits; ++d) {
+        const uint32_t dig = (uint32_t)(k >> (8 * d)) & 0xFF;
+        const uint32_t first = (uint32_t)__builtin_amdgcn_readfirstlane((int)dig);
+        if (fc::ballot(valid && dig == first) == act) {
+          if (fc::lane_id() == 0) atomicAdd(&s[d][first], (uint32_t)__popcll(act));
+        } else if (valid) {
+          atomicAdd(&s[d][dig], 1u);
+        }
       }
     }
   }
@@ -661,35 +675,66 @@ __global__ void __launch_bounds__(kSegThreads) k_seg_partials(const uint64_t* __
 }
 
 // One workgroup: exclusive max / max / sum scans of the tile partials, in
-// place; *u_next receives the number kept.
+// place; *u_next receives the number kept.  The partials are taken in chunks
+// of kScanThreads * kScanRun, each thread a run of kScanRun consecutive ones
+// (so a wave's loads and stores cover contiguous memory), with the chunk
+// totals carried from chunk to chunk.
+constexpr int kScanRun = 8;
 __global__ void __launch_bounds__(kScanThreads) k_seg_scan(uint32_t* __restrict__ part_h,
                                                              uint32_t* __restrict__ part_g,
                                                              uint32_t* __restrict__ part_k, uint32_t ntiles,
                                                              uint32_t* __restrict__ u_next) {
   __shared__ uint32_t scratch[kScanThreads / fc::kWave + 1];
-  const uint32_t per = fc::div_up(ntiles, kScanThreads);
-  const uint32_t lo = threadIdx.x * per;
-  const uint32_t hi = lo + per < ntiles ? lo + per : ntiles;
-  uint32_t mh = 0, mg = 0, kc = 0;
-  for (uint32_t i = lo; i < hi; ++i) {
-    mh = part_h[i] > mh ? part_h[i] : mh;
-    mg = part_g[i] > mg ? part_g[i] : mg;
-    kc += part_k[i];
+  __shared__ uint32_t s_last[3];
+  uint32_t ch = 0, cg = 0, ck = 0;  // carries: maxima and sum over the earlier chunks
+  for (uint32_t c0 = 0; c0 < ntiles; c0 += kScanThreads * kScanRun) {
+    const uint32_t b0 = c0 + threadIdx.x * kScanRun;
+    uint32_t h[kScanRun], g[kScanRun], k[kScanRun];
+#pragma unroll
+    for (int j = 0; j < kScanRun; ++j) {
+      const uint32_t i = b0 + (uint32_t)j;
+      h[j] = i < ntiles ? part_h[i] : 0u;
+      g[j] = i < ntiles ? part_g[i] : 0u;
+      k[j] = i < ntiles ? part_k[i] : 0u;
+    }
+    uint32_t mh = 0, mg = 0, kc = 0;
+#pragma unroll
+    for (int j = 0; j < kScanRun; ++j) {
+      mh = h[j] > mh ? h[j] : mh;
+      mg = g[j] > mg ? g[j] : mg;
+      kc += k[j];
+    }
+    uint32_t total;
+    uint32_t eh = fc::block_excl_max<uint32_t>(mh, 0u, scratch);
+    uint32_t eg = fc::block_excl_max<uint32_t>(mg, 0u, scratch);
+    uint32_t ek = fc::block_excl_sum<uint32_t>(kc, scratch, &total);
+    eh = eh > ch ? eh : ch;
+    eg = eg > cg ? eg : cg;
+    ek += ck;
+#pragma unroll
+    for (int j = 0; j < kScanRun; ++j) {
+      const uint32_t i = b0 + (uint32_t)j;
+      if (i < ntiles) {
+        part_h[i] = eh;
+        part_g[i] = eg;
+        part_k[i] = ek;
+      }
+      eh = h[j] > eh ? h[j] : eh;
+      eg = g[j] > eg ? g[j] : eg;
+      ek += k[j];
+    }
+    if (threadIdx.x == kScanThreads - 1) {
+      s_last[0] = eh;
+      s_last[1] = eg;
+      s_last[2] = ek;
+    }
+    __syncthreads();
+    ch = s_last[0];
+    cg = s_last[1];
+    ck = s_last[2];
+    __syncthreads();
   }
-  uint32_t total;
-  uint32_t eh = fc::block_excl_max<uint32_t>(mh, 0u, scratch);
-  uint32_t eg = fc::block_excl_max<uint32_t>(mg, 0u, scratch);
-  uint32_t ek = fc::block_excl_sum<uint32_t>(kc, scratch, &total);
-  for (uint32_t i = lo; i < hi; ++i) {
-    const uint32_t h = part_h[i], g = part_g[i], kk = part_k[i];
-    part_h[i] = eh;
-    part_g[i] = eg;
-    part_k[i] = ek;
-    eh = h > eh ? h : eh;
-    eg = g > eg ? g : eg;
-    ek += kk;
-  }
-  if (threadIdx.x == 0) *u_next = total;
+  if (threadIdx.x == 0) *u_next = ck;
 }
 
 // Per element: new rank = old group start + (new head index - old head index)
