@@ -390,6 +390,20 @@ __global__ void __launch_bounds__(kScanThreads) k_offsets(const int32_t* __restr
   if (threadIdx.x == 0) offsets[B] = total;
 }
 
+// floor(local * cnt / budget), the strided pick of a range larger than its
+// budget: local < budget <= k < 2^31 and cnt < 2^32.  Below 2^53 the product
+// is exact in a double and the double quotient lies within a small fraction
+// of the true one, so its integer part is off by at most one, which one
+// integer check corrects; larger products take the 64-bit division.
+__device__ __forceinline__ uint64_t strided_pick(uint64_t local, uint64_t cnt, uint64_t budget) {
+  const uint64_t prod = local * cnt;
+  if (prod >= (1ull << 53)) return prod / budget;
+  uint64_t q = (uint64_t)((double)prod / (double)budget);
+  if (q * budget > prod) --q;
+  else if ((q + 1) * budget <= prod) ++q;
+  return q;
+}
+
 // MAXM tokens from MAXM/2 + 1 consecutive 32-bit words holding two tokens
 // each (low half first), starting at the high half of the first word when
 // `odd`; every load is issued before any is used.
@@ -594,7 +608,7 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
         }
         const uint64_t budget = (uint64_t)(k - before);
         const uint64_t local = (uint64_t)(i - before);
-        const uint64_t idx = rlo + (cnt > budget ? (local * cnt) / budget : local);
+        const uint64_t idx = rlo + (cnt > budget ? strided_pick(local, cnt, budget) : local);
         sv[v] = s;
         nv[v] = n;
         rowv[v] = row;
@@ -609,9 +623,9 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
           const int wf = 1 + (t0 >> 1);  // first window word
           const int wl = wf + kWords - 1;  // last window word
           const uint4 q0 = Q[0];
-          const uint4 q1 = Q[1];
-          uint4 q2 = make_uint4(0, 0, 0, 0), q3 = q2;
-          if (wl >= 8) q2 = Q[2];
+          uint4 q1 = make_uint4(0, 0, 0, 0), q2 = q1, q3 = q1;
+          if (wf <= 7) q1 = Q[1];
+          if (wf <= 11 && wl >= 8) q2 = Q[2];
           if (wl >= 12) q3 = Q[3];
           in_rec[v] = true;
           jv[v] = q0.x;
