@@ -1159,6 +1159,15 @@ struct FlatLayout {
   size_t perm, lm, A, sstr, slen, sidx, sh_key, sh_w, total;
 };
 
+// Head bits (one 64-bit word per 64 merged positions and depth, positions
+// 0..T) need every weight to be one store weight times a run length and one
+// byte per position's (LCP, length); at most kHeadWords words per depth.
+constexpr int kHeadWords = 192;
+__host__ __device__ inline int head_words(int T) { return (T + 1 + 63) / 64; }
+__host__ __device__ inline bool flat_masks(int k, int maxm, bool with_A) {
+  return !with_A && maxm <= 15 && head_words(k) <= kHeadWords;
+}
+
 // maxm: the instantiation's row width (rows of maxm/2 32-bit words);
 // cap: short strings held; with_A: alpha prefix sums (stores of different
 // weights); S > 2: the short strings' merged order needs its own index.
@@ -1171,9 +1180,12 @@ __host__ __device__ inline FlatLayout flat_layout(int k, int maxm, int cap, int 
   o = align_up(o + (size_t)k * (maxm <= 15 ? 1 : 2), 16);
   t.A = o;  // k+1 uint32 alpha prefix sums
   if (with_A) o = align_up(o + (size_t)(k + 1) * 4, 16);
-  t.sstr = o;  // cap rows of maxm/2 words; later the kept tail nodes
+  t.sstr = o;  // cap rows of maxm/2 words; later the head bits, then the kept tail nodes
   const size_t rows = (size_t)cap * maxm * 2, tails = (size_t)FC_MAX_TREE_ROWS * 4;
-  o = align_up(o + (rows > tails ? rows : tails), 16);
+  const size_t heads = flat_masks(k, maxm, with_A) ? (size_t)maxm * head_words(k) * 8 : 0;
+  size_t region = rows > tails ? rows : tails;
+  region = region > heads ? region : heads;
+  o = align_up(o + region, 16);
   t.slen = o;  // cap uint8
   o = align_up(o + (size_t)cap, 16);
   t.sidx = o;  // cap uint16: short merged order -> LDS row
@@ -1390,6 +1402,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   __shared__ int16_t s_end[FC_MAX_TREE_ROWS];
   __shared__ uint32_t s_pick[3];
   __shared__ uint32_t s_scan4[4 * NW];
+  __shared__ uint64_t s_nzw[MAXM][kHeadWords / 64];  // per depth: which head words are non-empty
 
   const int tid = threadIdx.x;
   const int lane = fc::lane_id();
@@ -1747,10 +1760,10 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     // 4. chunk sums: alpha, non-empty strings (root weight), nodes, the
     //    chunk's shared nodes (depths past its own LCP, up to the next
     //    string's: they fix where the chunk's part of the list of shared
-    //    nodes starts) and the chunk's first head per depth (first q with
-    //    lcp[q] < d), then the next head per depth after the chunk
+    //    nodes starts) and tail nodes (depths past both LCPs), and the
+    //    chunk's first head per depth (first q with lcp[q] < d)
     const uint32_t a0 = alpha.a[0];
-    uint32_t asum = 0, rw = 0, nodes = 0, nsh = 0;
+    uint32_t asum = 0, rw = 0, nodes = 0, nsh = 0, ntail = 0;
     uint16_t f[MAXM + 1];
 #pragma unroll
     for (int d = 0; d <= MAXM; ++d) f[d] = (uint16_t)T;
@@ -1764,10 +1777,48 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       nodes += (uint32_t)(li - l);
       const int top = li < l_after ? li : l_after;
       nsh += top > l ? (uint32_t)(top - l) : 0u;
+      const int lo_t = l > l_after ? l : l_after;
+      ntail += li > lo_t ? (uint32_t)(li - lo_t) : 0u;
       l_after = l;
 #pragma unroll
       for (int d = 1; d <= MAXM; ++d)
         if (l < d) f[d] = (uint16_t)p;
+    }
+    // With one store weight, shared node (q, d) weighs alpha times the
+    // distance from q to the next head of depth d (the next position whose
+    // LCP is below d, or T).  Per depth, one bit per position says whether
+    // it is a head (positions T and past are), so a node's weight is a bit
+    // search instead of the chunk walk below ("direct").  A head word is
+    // built by one thread from 64 (LCP, length) bytes, four at a time: with
+    // the LCP in a byte's low nibble, adding 16 - d sets the byte's bit 4
+    // exactly when LCP >= d.
+    const int nwd = head_words(T);
+    const bool direct = alpha_flat && flat_masks(k, MAXM, !NARROW) && m <= MAXM;
+    uint64_t* heads = (uint64_t*)(smem + lay.sstr);
+    if (direct) {
+      if (tid < MAXM * (kHeadWords / 64)) (&s_nzw[0][0])[tid] = 0ull;
+      __syncthreads();
+      for (int x = tid; x < m * nwd; x += NT) {
+        const int d = x / nwd + 1, wd = x - (x / nwd) * nwd;
+        const uint4* src = (const uint4*)(lm + wd * 64);
+        const uint32_t add = (uint32_t)(16 - d) * 0x01010101u;
+        uint64_t hb = 0;
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4) {
+          const uint4 v = src[c4];
+          const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const uint32_t ge = (((wv[u] & 0x0F0F0F0Fu) + add) >> 4) & 0x01010101u;  // bit 8i: LCP_i >= d
+            const uint32_t nib = (ge | (ge >> 7) | (ge >> 14) | (ge >> 21)) & 0xFu;
+            hb |= (uint64_t)(~nib & 0xFu) << (16 * c4 + 4 * u);
+          }
+        }
+        const int past = T - wd * 64;  // positions at or past T are heads
+        if (past < 64) hb |= past <= 0 ? ~0ull : (~0ull << past);
+        heads[(d - 1) * nwd + wd] = hb;
+        if (hb != 0ull) atomicOr((unsigned long long*)&s_nzw[d - 1][wd >> 6], 1ull << (wd & 63));
+      }
     }
     uint32_t a_ex, a_tot, n_tot, sh_ex, sh_tot;
     {
@@ -1781,40 +1832,49 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       sh_tot = tot3[2];
     }
     const bool listed = sh_tot <= (uint32_t)kFlatList;
+
+    // The walk's set-up, done once and only when a walk is needed: the next
+    // head per depth after each chunk, and the alpha prefix sums of stores
+    // of different weights.
     uint16_t nh[MAXM + 1];
+    bool walk_ready = false;
+    auto prepare_walk = [&]() {
+      if (walk_ready) return;
+      walk_ready = true;
 #pragma unroll
-    for (int d = 1; d <= MAXM; ++d) {
-      uint32_t wave_min = (uint32_t)T;
-      nh[d] = (uint16_t)T;
-      if (d <= m) nh[d] = (uint16_t)fc::wave_excl_suffix_min_u32(f[d], (uint32_t)T, &wave_min);
-      if (lane == 0) s_wmin[w][d] = (uint16_t)wave_min;
-    }
-    __syncthreads();
-    if (tid < NW * MAXM) {
-      const int w0 = tid / MAXM, d0 = tid % MAXM + 1;
-      uint32_t v = (uint32_t)T;
-#pragma unroll
-      for (int u = 0; u < NW; ++u) {
-        const uint32_t x = s_wmin[u][d0];
-        v = (u > w0 && x < v) ? x : v;
+      for (int d = 1; d <= MAXM; ++d) {
+        uint32_t wave_min = (uint32_t)T;
+        nh[d] = (uint16_t)T;
+        if (d <= m) nh[d] = (uint16_t)fc::wave_excl_suffix_min_u32(f[d], (uint32_t)T, &wave_min);
+        if (lane == 0) s_wmin[w][d] = (uint16_t)wave_min;
       }
-      s_wsuf[w0][d0] = (uint16_t)v;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int d = 1; d <= MAXM; ++d) {
-      const uint32_t x = s_wsuf[w][d];
-      if (d <= m && x < nh[d]) nh[d] = (uint16_t)x;
-    }
-    if (!alpha_flat) {
-      uint32_t run = a_ex;
-      for (int p = p0; p < p1; ++p) {
-        A[p] = run;
-        run += alpha_of(alpha, store_of(perm[p]));
-      }
-      if (tid == 0) A[T] = a_tot;
       __syncthreads();
-    }
+      if (tid < NW * MAXM) {
+        const int w0 = tid / MAXM, d0 = tid % MAXM + 1;
+        uint32_t v = (uint32_t)T;
+#pragma unroll
+        for (int u = 0; u < NW; ++u) {
+          const uint32_t x = s_wmin[u][d0];
+          v = (u > w0 && x < v) ? x : v;
+        }
+        s_wsuf[w0][d0] = (uint16_t)v;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int d = 1; d <= MAXM; ++d) {
+        const uint32_t x = s_wsuf[w][d];
+        if (d <= m && x < nh[d]) nh[d] = (uint16_t)x;
+      }
+      if (!alpha_flat) {
+        uint32_t run = a_ex;
+        for (int p = p0; p < p1; ++p) {
+          A[p] = run;
+          run += alpha_of(alpha, store_of(perm[p]));
+        }
+        if (tid == 0) A[T] = a_tot;
+        __syncthreads();
+      }
+    };
     // The own nodes of the chunk, right to left and deepest first (the
     // reverse of (p, d) order), with their weights: node (q, d) covers the
     // run from q to the next head of depth d.  Below the next string's LCP
@@ -1822,7 +1882,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     // difference; past it (the string's own tail) the run is q alone and the
     // weight is q's alpha, so tails are handed over as one range (tail(q,
     // d_lo, d_hi, w): depths d_lo < d <= d_hi) and shared nodes one by one
-    // (shared(q, d, w)), tail first.
+    // (shared(q, d, w)), tail first.  prepare_walk() must have run.
     auto walk = [&](auto&& tail, auto&& shared) {
       uint32_t h[MAXM + 1];
 #pragma unroll
@@ -1856,14 +1916,15 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
 
     // 5. weight histogram: 1 and 2 (the bulk) in registers, other weights
     //    below 256 by LDS atomics, heavier ones only counted.  The shared
-    //    nodes go to the list on the way: the walk meets a chunk's shared
-    //    nodes in reverse (position, depth) order, so it fills the chunk's
-    //    part of the list from its end, and the list comes out in (position,
-    //    depth) order with no atomics.  With the list, the shared nodes'
-    //    weights are counted from it after the walk (each thread a contiguous
-    //    piece), so the walk itself has no LDS atomics for them to wait on.
+    //    nodes are listed in (position, depth) order with no atomics: each
+    //    chunk fills its part of the list, which starts at its exclusive
+    //    count.  Direct: each chunk lists its shared nodes, then every
+    //    thread takes list entries one by one and finds their weights by
+    //    bit search.  Otherwise the walk, which meets a chunk's shared nodes
+    //    in reverse order, fills the chunk's part from its end with their
+    //    weights, and with the list the weights are counted from it
+    //    afterwards (so the walk has no LDS atomics to wait on).
     {
-      uint32_t at = sh_ex + nsh;
       uint32_t r1 = 0, r2 = 0, rbig = 0;
       auto count = [&](uint32_t Wt, uint32_t n) {
         r1 += Wt == 1u ? n : 0u;
@@ -1871,22 +1932,65 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
         rbig += Wt >= 256u ? n : 0u;
         if (Wt != 1u && Wt != 2u && Wt < 256u) atomicAdd(&s_hist[Wt], n);
       };
-      walk([&](int, int lo, int hi, uint32_t Wt) { count(Wt, (uint32_t)(hi - lo)); },
-           [&](int q, int d, uint32_t Wt) {
-             if (listed) {
-               --at;
-               sh_key[at] = ((uint32_t)q << 5) | (uint32_t)d;
-               sh_w[at] = (SWT)Wt;
-             } else {
-               count(Wt, 1u);
-             }
-           });
-      if (listed) {
+      if (direct && listed) {
+        uint32_t o = sh_ex;
+        uint32_t x = p0 < p1 ? (uint32_t)lm[p0] : 0u;
+        for (int q = p0; q < p1; ++q) {
+          const uint32_t xn = q + 1 < T ? (uint32_t)lm[q + 1] : 0u;
+          const int l = (int)(x & kLo), ml = (int)(x >> kSh), ln = (int)(xn & kLo);
+          const int hi = ml < ln ? ml : ln;
+          for (int d = l + 1; d <= hi; ++d) sh_key[o++] = ((uint32_t)q << 5) | (uint32_t)d;
+          x = xn;
+        }
+        count(a0, ntail);
         __syncthreads();
-        const uint32_t pl = (sh_tot + NT - 1) / NT;
-        const uint32_t e0 = (uint32_t)tid * pl < sh_tot ? (uint32_t)tid * pl : sh_tot;
-        const uint32_t e1 = e0 + pl < sh_tot ? e0 + pl : sh_tot;
-        for (uint32_t i = e0; i < e1; ++i) count((uint32_t)sh_w[i], 1u);
+        // (q, d) with d <= lcp(q + 1): the next head of depth d is past q + 1
+        for (uint32_t e = (uint32_t)tid; e < sh_tot; e += NT) {
+          const uint32_t key = sh_key[e];
+          const int q = (int)(key >> 5), d = (int)(key & 31u);
+          const uint64_t* hd = heads + (d - 1) * nwd;
+          const int p = q + 2;  // <= T: a shared node's string is not the last
+          const int j = p >> 6;
+          const uint64_t bits = hd[j] & (~0ull << (p & 63));
+          int nxt;
+          if (bits != 0ull) {
+            nxt = (j << 6) + __builtin_ctzll(bits);
+          } else {
+            // the first non-empty word after j (word nwd - 1 holds position T)
+            int j2 = -1;
+#pragma unroll
+            for (int c = kHeadWords / 64 - 1; c >= 0; --c) {
+              const int lo_bit = c * 64;
+              uint64_t z = s_nzw[d - 1][c];
+              if (j + 1 > lo_bit) z = (j + 1 - lo_bit) >= 64 ? 0ull : z & (~0ull << (j + 1 - lo_bit));
+              if (z != 0ull) j2 = lo_bit + __builtin_ctzll(z);
+            }
+            nxt = (j2 << 6) + __builtin_ctzll(hd[j2]);
+          }
+          const uint32_t Wt = a0 * (uint32_t)(nxt - q);
+          sh_w[e] = (SWT)Wt;
+          count(Wt, 1u);
+        }
+      } else {
+        prepare_walk();
+        uint32_t at = sh_ex + nsh;
+        walk([&](int, int lo, int hi, uint32_t Wt) { count(Wt, (uint32_t)(hi - lo)); },
+             [&](int q, int d, uint32_t Wt) {
+               if (listed) {
+                 --at;
+                 sh_key[at] = ((uint32_t)q << 5) | (uint32_t)d;
+                 sh_w[at] = (SWT)Wt;
+               } else {
+                 count(Wt, 1u);
+               }
+             });
+        if (listed) {
+          __syncthreads();
+          const uint32_t pl = (sh_tot + NT - 1) / NT;
+          const uint32_t e0 = (uint32_t)tid * pl < sh_tot ? (uint32_t)tid * pl : sh_tot;
+          const uint32_t e1 = e0 + pl < sh_tot ? e0 + pl : sh_tot;
+          for (uint32_t i = e0; i < e1; ++i) count((uint32_t)sh_w[i], 1u);
+        }
       }
       const uint32_t x1 = fc::wave_sum_u32(r1), x2 = fc::wave_sum_u32(r2), xb = fc::wave_sum_u32(rbig);
       if (lane == 0 && x1) atomicAdd(&s_hist[1], x1);
@@ -1935,6 +2039,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       remaining = s_pick[1];
     } else if (need > 0) {
       // W* >= 256: radix select over the heavy nodes only
+      prepare_walk();
       uint32_t wmax = 0;
       auto top = [&](uint32_t Wt) { wmax = Wt > wmax ? Wt : wmax; };
       walk([&](int, int, int, uint32_t Wt) { top(Wt); }, [&](int, int, uint32_t Wt) { top(Wt); });
@@ -2055,6 +2160,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       nsel = (int)(need < (uint32_t)c ? need : (uint32_t)c);
     } else {
       uint32_t gt = 0, eq = 0;
+      prepare_walk();
       if (need > 0)
         walk(
             [&](int, int lo, int hi, uint32_t Wt) {
