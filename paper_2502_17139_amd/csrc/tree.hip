@@ -485,27 +485,27 @@ struct Scan2 {
   }
 };
 
-template <int NT>
-struct Scan3 {
-  // Exclusive prefix sums of v[0..3) over the block and their totals, plus
-  // the block total of z; two barriers.  s holds 4 x (NT/64) words.
-  __device__ __forceinline__ static void run(const uint32_t (&v)[3], uint32_t z, uint32_t* s, uint32_t (&ex)[3],
-                                             uint32_t (&tot)[3], uint32_t* tz) {
+template <int NT, int K>
+struct ScanK {
+  // Exclusive prefix sums of v[0..K) over the block and their totals, plus
+  // the block total of z; two barriers.  s holds (K + 1) x (NT/64) words.
+  __device__ __forceinline__ static void run(const uint32_t (&v)[K], uint32_t z, uint32_t* s, uint32_t (&ex)[K],
+                                             uint32_t (&tot)[K], uint32_t* tz) {
     constexpr int NW = NT / fc::kWave;
     const int w = (int)threadIdx.x / fc::kWave;
-    uint32_t inc[3];
+    uint32_t inc[K];
 #pragma unroll
-    for (int u = 0; u < 3; ++u) inc[u] = fc::wave_incl_sum_u32(v[u]);
+    for (int u = 0; u < K; ++u) inc[u] = fc::wave_incl_sum_u32(v[u]);
     const uint32_t iz = fc::wave_sum_u32(z);
     if (fc::lane_id() == fc::kWave - 1) {
 #pragma unroll
-      for (int u = 0; u < 3; ++u) s[u * NW + w] = inc[u];
-      s[3 * NW + w] = iz;
+      for (int u = 0; u < K; ++u) s[u * NW + w] = inc[u];
+      s[K * NW + w] = iz;
     }
     __syncthreads();
     uint32_t az = 0;
 #pragma unroll
-    for (int u = 0; u < 3; ++u) {
+    for (int u = 0; u < K; ++u) {
       uint32_t pre = 0, all = 0;
 #pragma unroll
       for (int i = 0; i < NW; ++i) {
@@ -517,7 +517,7 @@ struct Scan3 {
       tot[u] = all;
     }
 #pragma unroll
-    for (int i = 0; i < NW; ++i) az += s[3 * NW + i];
+    for (int i = 0; i < NW; ++i) az += s[K * NW + i];
     *tz = az;
     __syncthreads();
   }
@@ -1403,6 +1403,8 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   __shared__ uint32_t s_pick[3];
   __shared__ uint32_t s_scan4[4 * NW];
   __shared__ uint64_t s_nzw[MAXM][kHeadWords / 64];  // per depth: which head words are non-empty
+  __shared__ int16_t s_runj[kFlatShortCap];  // first short string of a run: long strings before it (else -1)
+  __shared__ uint8_t s_plcp[kFlatShortCap];  // and its LCP with the long string just before it
 
   const int tid = threadIdx.x;
   const int lane = fc::lane_id();
@@ -1576,6 +1578,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   // 1. the short strings into LDS, each store's order checked; with three
   //    or more stores, their merged order among themselves
   for (int p = tid; p < T; p += NT) perm[p] = 0xFFFF;
+  for (int g = tid; g < n_short && g < kFlatShortCap; g += NT) s_runj[g] = -1;
   if (S > 2)
     for (int g = tid; g < n_short; g += NT) sidx[g] = 0;  // every entry valid even if unsorted input collides
   for (int ci = tid; ci < n_short; ci += NT) {
@@ -1635,6 +1638,8 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
         if (u < S && u != sL && qs.tk[u] > 0) r += count_before<W>(row, s_cs[u], s_cs[u] + qs.tk[u], v, len, u < sL);
       return r;
     };
+    // with every short string in LDS the long pass also places them
+    const bool place = in_lds && n_short > 0;
     for (int j0 = 0; j0 < nL; j0 += kPass * kFlatRows) {
       uint32_t v[kFlatRows][W];
       int len[kFlatRows];
@@ -1690,6 +1695,30 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
           const int P = j + r;
           perm[P] = (uint16_t)(lslot0 + j);
           lm[P] = (LMT)((uint32_t)l | ((uint32_t)ln << kSh));
+          // a run of short strings merged right after long j - 1 (in short
+          // order [pr, r); [0, r) before the first long) or after the last
+          // long ([r, n_short)): the run's first string records the number
+          // of long strings before it and its LCP with the long string just
+          // before it, whose row is in registers here
+          if (place) {
+            if (j == 0 ? r > 0 : pr < r) {
+              const int g = j == 0 ? 0 : pr;
+              s_runj[g] = (int16_t)j;
+              if (j > 0) {
+                const int ci = S > 2 ? (int)sidx[g] : g;
+                uint32_t sv[W];
+                const int sl = lds_srow(ci, sv);
+                s_plcp[g] = (uint8_t)lcp_words<W>(pv, plen, sv, sl);
+              }
+            }
+            if (j == nL - 1 && r < n_short) {
+              const int ci = S > 2 ? (int)sidx[r] : r;
+              uint32_t sv[W];
+              const int sl = lds_srow(ci, sv);
+              s_runj[r] = (int16_t)nL;
+              s_plcp[r] = (uint8_t)lcp_words<W>(v[u], ln, sv, sl);
+            }
+          }
         }
       }
     }
@@ -1700,11 +1729,35 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   });
   __syncthreads();
 
-  // 3. the free merged positions take the short strings in order
+  // 3. the free merged positions take the short strings in order: with the
+  //    short strings in LDS and long ones present, short g goes to g plus
+  //    the long strings before its run (recorded by the long pass), one
+  //    thread per short string; otherwise the chunks count their free
+  //    positions and fill them
   const int per = (T + NT - 1) / NT;
   const int p0 = tid * per < T ? tid * per : T;
   const int p1 = p0 + per < T ? p0 + per : T;
-  if (n_short > 0) {
+  if (n_short > 0 && in_lds && nL > 0) {
+    for (int g = tid; g < n_short; g += NT) {
+      int st = g;
+      while (st > 0 && s_runj[st] < 0) --st;
+      const int jb = s_runj[st] < 0 ? 0 : (int)s_runj[st];
+      const int ci = S > 2 ? (int)sidx[g] : g;
+      uint32_t v[W];
+      const int len = lds_srow(ci, v);
+      int l = 0;
+      if (st == g && jb > 0) {
+        l = s_plcp[g];  // right after a long string
+      } else if (g > 0) {
+        const int pci = S > 2 ? (int)sidx[g - 1] : g - 1;
+        uint32_t pv[W];
+        const int pl = lds_srow(pci, pv);
+        l = lcp_words<W>(pv, pl, v, len);
+      }
+      perm[g + jb] = (uint16_t)short_slot(ci);
+      lm[g + jb] = (LMT)((uint32_t)l | ((uint32_t)len << kSh));
+    }
+  } else if (n_short > 0) {
     uint32_t gaps = 0;
     for (int p = p0; p < p1; ++p) gaps += perm[p] == 0xFFFF ? 1u : 0u;
     // the predecessor of the chunk, read before anything is rewritten
@@ -1824,7 +1877,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     {
       const uint32_t v3[3] = {asum, nodes, nsh};
       uint32_t ex3[3], tot3[3];
-      Scan3<NT>::run(v3, rw, s_scan4, ex3, tot3, &root_w);
+      ScanK<NT, 3>::run(v3, rw, s_scan4, ex3, tot3, &root_w);
       a_ex = ex3[0];
       sh_ex = ex3[2];
       a_tot = tot3[0];
