@@ -2177,14 +2177,8 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
         lo = l > ln ? l : ln;
         hi = ml;
       };
-      uint32_t nt = 0;
-      for (int q = p0; q < p1; ++q) {
-        int lo, hi;
-        tails_of(q, lo, hi);
-        nt += hi > lo ? (uint32_t)(hi - lo) : 0u;
-      }
       uint32_t t_ex, dmy, t_tot, dmy2;
-      Scan2<NT>::run(nt, 0u, s_x, s_y, &t_ex, &dmy, &t_tot, &dmy2);
+      Scan2<NT>::run(ntail, 0u, s_x, s_y, &t_ex, &dmy, &t_tot, &dmy2);  // the chunk's tails, counted in pass 4
       for (int q = p0; q < p1 && t_ex < take_eq; ++q) {
         int lo, hi;
         tails_of(q, lo, hi);
