@@ -18,6 +18,10 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return (uint64_t)__ballot(p); }
 
+// Four 32-bit words at a 4-byte aligned address: one 16-byte load (the
+// hardware takes multi-dword loads at dword alignment).
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+
 // ---- DPP wave primitives (32-bit).  Within each row of 16 lanes values move
 // with DPP row shifts (plain VALU ops); rows are combined with readlane.
 // Lanes whose DPP source falls outside the row take the identity explicitly,

@@ -1650,7 +1650,20 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
         if (j >= 0 && j < nL) {
           len[u] = cont_len[row0 + lslot0 + j];
           const uint16_t* src = cont_tok + (row0 + lslot0 + j) * m;
-          if (words) {
+          if (words && m == MAXM) {
+            // a full row: 16-byte loads (dword-aligned) plus single words
+            const uint32_t* s32 = (const uint32_t*)src;
+#pragma unroll
+            for (int x = 0; x + 4 <= W; x += 4) {
+              const fc::u32x4_a4 q4 = *(const fc::u32x4_a4*)(s32 + x);
+              v[u][x] = q4.x;
+              v[u][x + 1] = q4.y;
+              v[u][x + 2] = q4.z;
+              v[u][x + 3] = q4.w;
+            }
+#pragma unroll
+            for (int x = W / 4 * 4; x < W; ++x) v[u][x] = s32[x];
+          } else if (words) {
             const uint32_t* s32 = (const uint32_t*)src;
 #pragma unroll
             for (int x = 0; x < W; ++x) v[u][x] = 2 * x < m ? s32[x] : 0u;
