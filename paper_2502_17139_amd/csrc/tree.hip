@@ -1576,8 +1576,12 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
   };
 
   // 1. the short strings into LDS, each store's order checked; with three
-  //    or more stores, their merged order among themselves
-  for (int p = tid; p < T; p += NT) perm[p] = 0xFFFF;
+  //    or more stores, their merged order among themselves.  Free merged
+  //    positions are marked only for the gap pass (short strings read in
+  //    place, or no long strings); with no short string at all the pass is
+  //    skipped, barriers included.
+  if (n_short > 0 && !(in_lds && nL > 0))
+    for (int p = tid; p < T; p += NT) perm[p] = 0xFFFF;
   for (int g = tid; g < n_short && g < kFlatShortCap; g += NT) s_runj[g] = -1;
   if (S > 2)
     for (int g = tid; g < n_short; g += NT) sidx[g] = 0;  // every entry valid even if unsorted input collides
@@ -1593,7 +1597,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
     for (int x = 0; x < W; ++x) sstr[ci * W + x] = v[x];
     slen[ci] = (uint8_t)len;
   }
-  __syncthreads();
+  if (n_short > 0) __syncthreads();
   for (int ci = tid; ci < n_short; ci += NT) {
     const int s = short_store(ci);
     const int i = ci - s_cs[s];
@@ -1613,7 +1617,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       sidx[pos] = (uint16_t)ci;
     }
   }
-  __syncthreads();
+  if (n_short > 0) __syncthreads();
 
   // 2. long strings: rank among the short strings, merged position, LCP
   //    with the merged predecessor when that is long (its neighbour in the
