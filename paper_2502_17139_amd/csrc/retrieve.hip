@@ -679,11 +679,30 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
       uint16_t* out = cont_tok + slot * m;
       if (out_words) {
         uint32_t* out32 = (uint32_t*)out;
+        uint32_t ow[MAXM / 2];
 #pragma unroll
         for (int x = 0; x < MAXM / 2; ++x) {
           const uint32_t lo16 = 2 * x < len ? tok[2 * x] : 0u;
           const uint32_t hi16 = 2 * x + 1 < len ? tok[2 * x + 1] : 0u;
-          if (2 * x < m) out32[x] = lo16 | (hi16 << 16);
+          ow[x] = lo16 | (hi16 << 16);
+        }
+        if (m == MAXM) {
+          // a full row: dword-aligned 16-byte stores plus single words
+#pragma unroll
+          for (int x = 0; x + 4 <= MAXM / 2; x += 4) {
+            fc::u32x4_a4 q4;
+            q4.x = ow[x];
+            q4.y = ow[x + 1];
+            q4.z = ow[x + 2];
+            q4.w = ow[x + 3];
+            *(fc::u32x4_a4*)(out32 + x) = q4;
+          }
+#pragma unroll
+          for (int x = MAXM / 2 / 4 * 4; x < MAXM / 2; ++x) out32[x] = ow[x];
+        } else {
+#pragma unroll
+          for (int x = 0; x < MAXM / 2; ++x)
+            if (2 * x < m) out32[x] = ow[x];
         }
       } else {
 #pragma unroll
