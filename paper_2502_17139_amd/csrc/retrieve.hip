@@ -655,37 +655,43 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
       const int s = sv[v];
       const int n = nv[v];
       const uint64_t start = (uint64_t)jv[v] + (uint64_t)n;
-      uint16_t tok[MAXM];
+      // the window as MAXM / 2 words of two tokens (token 2y in the low
+      // half of word y): from a record, each word is one funnel shift of
+      // two record words (or the word itself when the window starts on a
+      // word boundary)
+      uint32_t ow[MAXM / 2];
       if (in_rec[v]) {
-        const int odd = (n - 2) & 1;
+        const bool odd = ((n - 2) & 1) != 0;
 #pragma unroll
-        for (int x = 0; x < MAXM; ++x) {
-          const uint16_t even_v = (uint16_t)(wd[v][x >> 1] >> (16 * (x & 1)));
-          const uint16_t odd_v = (uint16_t)(wd[v][(x + 1) >> 1] >> (16 * ((x + 1) & 1)));
-          tok[x] = odd ? odd_v : even_v;
-        }
-      } else if (words) {
-        load_window<MAXM>(st.tok[s], st.n[s], start, tok);
+        for (int y = 0; y < MAXM / 2; ++y)
+          ow[y] = odd ? __builtin_amdgcn_alignbit(wd[v][y + 1], wd[v][y], 16) : wd[v][y];
       } else {
-        const uint64_t N = st.n[s];
+        uint16_t tok[MAXM];
+        if (words) {
+          load_window<MAXM>(st.tok[s], st.n[s], start, tok);
+        } else {
+          const uint64_t N = st.n[s];
 #pragma unroll
-        for (int x = 0; x < MAXM; ++x) tok[x] = (start + x < N) ? st.tok[s][start + x] : (uint16_t)0;
+          for (int x = 0; x < MAXM; ++x) tok[x] = (start + x < N) ? st.tok[s][start + x] : (uint16_t)0;
+        }
+#pragma unroll
+        for (int y = 0; y < MAXM / 2; ++y) ow[y] = (uint32_t)tok[2 * y] | ((uint32_t)tok[2 * y + 1] << 16);
       }
-      int len = m;
+      // cut before the first 0 (and at m): one bit per zero token
+      uint32_t zm = 1u << m;
 #pragma unroll
-      for (int x = MAXM - 1; x >= 0; --x)
-        if (x < m && tok[x] == 0) len = x;
+      for (int y = 0; y < MAXM / 2; ++y) {
+        zm |= (ow[y] & 0xFFFFu) == 0u ? 1u << (2 * y) : 0u;
+        zm |= (ow[y] >> 16) == 0u ? 2u << (2 * y) : 0u;
+      }
+      const int len = __builtin_ctz(zm);
+#pragma unroll
+      for (int y = 0; y < MAXM / 2; ++y)
+        ow[y] &= (2 * y < len ? 0xFFFFu : 0u) | (2 * y + 1 < len ? 0xFFFF0000u : 0u);
       const int64_t slot = (int64_t)rowv[v] * k + iv[v];
       uint16_t* out = cont_tok + slot * m;
       if (out_words) {
         uint32_t* out32 = (uint32_t*)out;
-        uint32_t ow[MAXM / 2];
-#pragma unroll
-        for (int x = 0; x < MAXM / 2; ++x) {
-          const uint32_t lo16 = 2 * x < len ? tok[2 * x] : 0u;
-          const uint32_t hi16 = 2 * x + 1 < len ? tok[2 * x + 1] : 0u;
-          ow[x] = lo16 | (hi16 << 16);
-        }
         if (m == MAXM) {
           // a full row: dword-aligned 16-byte stores plus single words
 #pragma unroll
@@ -707,7 +713,7 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
       } else {
 #pragma unroll
         for (int x = 0; x < MAXM; ++x)
-          if (x < m) out[x] = x < len ? tok[x] : (uint16_t)0;
+          if (x < m) out[x] = (uint16_t)(ow[x >> 1] >> (16 * (x & 1)));
       }
       cont_pos[slot] = (uint32_t)start;
       cont_src[slot] = (uint8_t)s;

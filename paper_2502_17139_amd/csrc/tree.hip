@@ -1869,7 +1869,8 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(
       if (tid < MAXM * (kHeadWords / 64)) (&s_nzw[0][0])[tid] = 0ull;
       __syncthreads();
       for (int x = tid; x < m * nwd; x += NT) {
-        const int d = x / nwd + 1, wd = x - (x / nwd) * nwd;
+        // consecutive threads take the depths of one word: same LDS bytes
+        const int wd = x / m, d = x - (x / m) * m + 1;
         const uint4* src = (const uint4*)(lm + wd * 64);
         const uint32_t add = (uint32_t)(16 - d) * 0x01010101u;
         uint64_t hb = 0;
