@@ -1366,7 +1366,7 @@ __global__ void __launch_bounds__(kPlanThreads) k_tree_plan(const int32_t* __res
 }
 
 template <int MAXM, bool NARROW>
-__global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 8 : 4) k_tree_flat(const int32_t* __restrict__ taken,
+__global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 6 : 4) k_tree_flat(const int32_t* __restrict__ taken,
                                                             const uint8_t* __restrict__ cont_len,
                                                             const uint16_t* __restrict__ cont_tok,
                                                             const uint16_t* __restrict__ ctx, int L, int S, int k,
