@@ -6,9 +6,10 @@
 // Myers' own construction does, with every round's sort done as an LSD radix
 // sort so it runs at HBM bandwidth:
 //
-//   round 0  key(i) = the first 3 tokens of suffix i, each as token+1 in 17
-//            bits with 0 past the end, so a suffix that ends first sorts
-//            first; all n suffixes are sorted.
+//   round 0  key(i) = the first 3 tokens of suffix i, each as token+1 in as
+//            many bits as the largest token + 1 needs (at most 17), with 0
+//            past the end, so a suffix that ends first sorts first; all n
+//            suffixes are sorted.
 //   round r  (h = 3 * 2^(r-1)) only suffixes still tied with another are
 //            re-sorted, by key(i) = (rank[i], rank[i+h] + 1, or 0 past the
 //            end), where rank[i] is the suffix-array index at which i's group
@@ -67,14 +68,14 @@ __device__ __forceinline__ uint64_t pack_status(uint32_t epoch, uint64_t flag, u
 
 // ---------------------------------------------------------------- keys ----
 
-__global__ void __launch_bounds__(256) k_init_keys(const uint16_t* __restrict__ tok, uint32_t n,
+__global__ void __launch_bounds__(256) k_init_keys(const uint16_t* __restrict__ tok, uint32_t n, int tb,
                                                      uint64_t* __restrict__ keys, uint32_t* __restrict__ vals) {
   uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   uint64_t a = (uint64_t)tok[i] + 1;
   uint64_t b = (i + 1 < n) ? (uint64_t)tok[i + 1] + 1 : 0;
   uint64_t c = (i + 2 < n) ? (uint64_t)tok[i + 2] + 1 : 0;
-  keys[i] = (a << 34) | (b << 17) | c;
+  keys[i] = (a << (2 * tb)) | (b << tb) | c;
   vals[i] = i;
 }
 
@@ -425,10 +426,10 @@ __global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys,
   __syncthreads();
   // 64-bit index: U can come within a grid stride of 2^32.  The keys are in
   // the previous round's sorted order, so a wave's 64 consecutive keys
-  // mostly share their high digits: a digit the whole wave agrees on is
-  // counted with one LDS atomic instead of 64 that collide on one bin.
-  // Each wave takes kHistRun runs of 64 consecutive keys per step, their
-  // loads issued together.
+  // mostly share their high digits, in runs: each run of equal digits in
+  // consecutive lanes is counted with one LDS atomic by its first lane
+  // (lanes colliding on one bin would serialise).  Each wave takes kHistRun
+  // runs of 64 consecutive keys per step, their loads issued together.
   constexpr int kHistRun = 4;
   const uint64_t wave0 = (uint64_t)blockIdx.x * blockDim.x * kHistRun + (threadIdx.x & ~(uint32_t)(fc::kWave - 1)) * kHistRun;
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x * kHistRun;
@@ -446,14 +447,14 @@ __global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys,
       const uint64_t k = kv[u];
       const uint64_t act = fc::ballot(valid);
       if (act == 0) continue;
+      const uint32_t cnt = (uint32_t)__popcll(act);  // the valid lanes are a prefix
+      const uint32_t lane = (uint32_t)fc::lane_id();
       for (int d = 0; d < digits; ++d) {
         const uint32_t dig = (uint32_t)(k >> (8 * d)) & 0xFF;
-        const uint32_t first = (uint32_t)__builtin_amdgcn_readfirstlane((int)dig);
-        if (fc::ballot(valid && dig == first) == act) {
-          if (fc::lane_id() == 0) atomicAdd(&s[d][first], (uint32_t)__popcll(act));
-        } else if (valid) {
-          atomicAdd(&s[d][dig], 1u);
-        }
+        const bool head = valid && dig != fc::wave_shr1(dig, ~0u);
+        const uint64_t after = fc::ballot(head) >> lane >> 1;  // heads above this lane
+        const uint32_t next = after ? lane + 1u + (uint32_t)__builtin_ctzll(after) : cnt;
+        if (head) atomicAdd(&s[d][dig], next - lane);
       }
     }
   }
@@ -937,7 +938,7 @@ struct BuildWs {
   uint32_t* hist;
   uint32_t* offsets;
   uint32_t* tickets;
-  uint32_t* misc;  // [0] error flag, [1] next U, [2..9] trivial digit flags
+  uint32_t* misc;  // [0] error flag, [1] next U, [2..9] trivial digit flags, [10] largest token
   uint32_t* end_of;   // batched build: end of each position's segment
   uint64_t* seg_off;  // batched build: segment offsets (device copy)
 };
@@ -1046,10 +1047,18 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
     h = two ? 2 : 1;
     key0_bits = ext_shift + ext->n_old_bits;
   } else if (n_seg == 0) {
-    hipLaunchKernelGGL(k_init_keys, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, tokens, N, w.keys[0],
+    // token + 1 in tb bits: the largest token decides tb (misc[10] is zero)
+    const uint32_t blocks = fc::div_up(N, 256) < 4096u ? fc::div_up(N, 256) : 4096u;
+    hipLaunchKernelGGL(k_max_token, dim3(blocks), dim3(256), 0, stream, tokens, N, w.misc + 10);
+    FC_CHECK_LAUNCH();
+    uint32_t mx = 0;
+    FC_CHECK_HIP(hipMemcpyAsync(&mx, w.misc + 10, sizeof(uint32_t), hipMemcpyDeviceToHost, stream));
+    FC_CHECK_HIP(hipStreamSynchronize(stream));
+    const int tb = bit_length((uint64_t)mx + 1);
+    hipLaunchKernelGGL(k_init_keys, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, tokens, N, tb, w.keys[0],
                        w.vals[0]);
     h = 3;
-    key0_bits = 51;
+    key0_bits = 3 * tb;
   } else {
     hipLaunchKernelGGL(k_init_keys_seg, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, tokens, N, w.seg_off, n_seg,
                        w.keys[0], w.vals[0], w.end_of);
