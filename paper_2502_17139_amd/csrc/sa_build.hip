@@ -32,7 +32,12 @@
 // the partials, per-tile apply), which also compacts the still-tied suffixes.
 // Both tile passes run wave-striped (a wave takes 1,024 consecutive sorted
 // positions, 64 at a time), so every load and store of a wave is coalesced
-// except the rank scatter itself, which is indexed by suffix.
+// except the rank scatter itself, which is indexed by suffix.  Where the
+// rank array outgrows the MALL (64M suffixes or more), a random 4-byte write
+// costs a 32-byte memory write, so the round's (suffix, rank) pairs are
+// written in sorted order instead, sorted by the suffix's top 16 bits (two
+// keys-only passes), and then stored one 64 KB window of the rank array
+// after another.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -419,8 +424,8 @@ __global__ void __launch_bounds__(256) k_ext_isa_old(const uint32_t* __restrict_
 
 // ------------------------------------------------------------ histogram ---
 
-__global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys, uint32_t U, int digits,
-                                                uint32_t* __restrict__ hist) {
+__global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys, uint32_t U, int shift0,
+                                                int digits, uint32_t* __restrict__ hist) {
   __shared__ uint32_t s[kMaxDigits][kRadix];
   for (int i = threadIdx.x; i < kMaxDigits * kRadix; i += blockDim.x) (&s[0][0])[i] = 0;
   __syncthreads();
@@ -450,7 +455,7 @@ __global__ void __launch_bounds__(256) k_hist(const uint64_t* __restrict__ keys,
       const uint32_t cnt = (uint32_t)__popcll(act);  // the valid lanes are a prefix
       const uint32_t lane = (uint32_t)fc::lane_id();
       for (int d = 0; d < digits; ++d) {
-        const uint32_t dig = (uint32_t)(k >> (8 * d)) & 0xFF;
+        const uint32_t dig = (uint32_t)(k >> (shift0 + 8 * d)) & 0xFF;
         const bool head = valid && dig != fc::wave_shr1(dig, ~0u);
         const uint64_t after = fc::ballot(head) >> lane >> 1;  // heads above this lane
         const uint32_t next = after ? lane + 1u + (uint32_t)__builtin_ctzll(after) : cnt;
@@ -482,7 +487,10 @@ __global__ void __launch_bounds__(256) k_hist_scan(const uint32_t* __restrict__ 
 
 // ------------------------------------------------------------- onesweep ---
 
-__global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __restrict__ kin,
+// kVals false: keys only (vin and vout unused), compiled for four waves per
+// SIMD, so four tiles share a CU.
+template <bool kVals>
+__global__ void __launch_bounds__(kSortThreads, kVals ? 1 : 4) k_onesweep(const uint64_t* __restrict__ kin,
                                                            const uint32_t* __restrict__ vin,
                                                            uint64_t* __restrict__ kout, uint32_t* __restrict__ vout,
                                                            uint32_t U, uint32_t shift,
@@ -498,7 +506,7 @@ __global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __res
   __shared__ uint32_t s_gbase[kRadix];
   __shared__ uint32_t s_scan[kSortThreads / fc::kWave + 1];
   __shared__ uint64_t s_keys[kSortTile];
-  __shared__ uint32_t s_vals[kSortTile];
+  __shared__ uint32_t s_vals[kVals ? kSortTile : 1];
 
   const int tid = threadIdx.x;
   const int w = tid / fc::kWave;
@@ -518,7 +526,7 @@ __global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __res
     const uint32_t idx = (uint32_t)(w * kSortItems * fc::kWave + j * fc::kWave + lane);
     const bool valid = idx < nvalid;
     k[j] = valid ? kin[base + idx] : ~0ull;
-    v[j] = valid ? vin[base + idx] : 0u;
+    v[j] = kVals && valid ? vin[base + idx] : 0u;
   }
   const uint64_t lt = fc::lanemask_lt();
 #pragma unroll
@@ -562,7 +570,7 @@ __global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __res
       const uint32_t d = (uint32_t)(k[j] >> shift) & 0xFF;
       const uint32_t pos = s_dstart[d] + s_wcnt[w][d] + rk[j];
       s_keys[pos] = k[j];
-      s_vals[pos] = v[j];
+      if (kVals) s_vals[pos] = v[j];
     }
   }
 
@@ -621,7 +629,7 @@ __global__ void __launch_bounds__(kSortThreads) k_onesweep(const uint64_t* __res
     const uint32_t dst = s_gbase[d] + (i - s_dstart[d]);
     if (dst < U) {  // always true unless a look-back gave up (then err is set)
       kout[dst] = key;
-      vout[dst] = s_vals[i];
+      if (kVals) vout[dst] = s_vals[i];
     }
   }
 }
@@ -741,7 +749,10 @@ __global__ void __launch_bounds__(kScanThreads) k_seg_scan(uint32_t* __restrict_
 // Per element: new rank = old group start + (new head index - old head index)
 // in the sorted list; tied suffixes are compacted into vals_next.  A suffix
 // whose group is now a singleton has its final index, so its suffix array
-// entry is written here (sa_out, unless null), in sorted order.  Wave w of
+// entry is written here (sa_out, unless null), in sorted order.  The ranks
+// go to rank[] directly (a random 4-byte write each), or, with pairs, as
+// (suffix << 32 | rank) at the element's own position, for k_rank_write
+// after a sort by suffix.  Wave w of
 // the tile takes positions [w * 1024, (w + 1) * 1024) of it, 64 consecutive
 // ones per step: the running head indexes and the kept count are wave scans
 // carried from step to step, started from the earlier waves' totals and the
@@ -753,6 +764,7 @@ __global__ void __launch_bounds__(kSegThreads) k_seg_apply(const uint64_t* __res
                                                              const uint32_t* __restrict__ pre_g,
                                                              const uint32_t* __restrict__ pre_k,
                                                              uint32_t* __restrict__ rank,
+                                                             uint64_t* __restrict__ pairs,
                                                              uint32_t* __restrict__ vals_next,
                                                              uint64_t* __restrict__ hi_next,
                                                              uint32_t* __restrict__ sa_out) {
@@ -805,8 +817,9 @@ __global__ void __launch_bounds__(kSegThreads) k_seg_apply(const uint64_t* __res
       const uint32_t rk = start + (hr - gr);
       // in the first new group of its old group a suffix keeps its rank (the
       // old group start, already in rank[i]): only round 0 and the later
-      // new groups write
-      if (r0f || hr != gr) rank[i] = rk;
+      // new groups write (a pair rewrites an unchanged rank with itself)
+      if (pairs) pairs[r] = ((uint64_t)i << 32) | rk;
+      else if (r0f || hr != gr) rank[i] = rk;
       if (f.keep) {
         vals_next[out + kr - 1u] = i;
         if (hi_next) hi_next[out + kr - 1u] = (uint64_t)rk << sb;  // the next round's key, high half
@@ -816,6 +829,31 @@ __global__ void __launch_bounds__(kSegThreads) k_seg_apply(const uint64_t* __res
     hh = __shfl(hr, fc::kWave - 1);
     gg = __shfl(gr, fc::kWave - 1);
     out += __shfl(kr, fc::kWave - 1);
+  }
+}
+
+// rank[i] = rk for a round's (i << 32 | rk) pairs, sorted by the high bits
+// of i so that each run of equal high bits covers one window of the rank
+// array (64 KB at most).  Workgroup w takes chunk (w % 8) * per_xcd + w / 8
+// of kRankChunk pairs: workgroups are dealt to the eight XCDs in turn, so
+// each XCD writes one contiguous eighth of the sorted pairs, and a window is
+// assembled in one L2 rather than written back in pieces from several.
+constexpr int kRankChunk = 4096;
+constexpr int kXcds = 8;
+constexpr int kRankSortBits = 16;  // high bits of the suffix index sorted on
+constexpr uint64_t kPairRanksMin = 1ull << 26;  // suffixes (4-byte ranks: 256 MB)
+__global__ void __launch_bounds__(256) k_rank_write(const uint64_t* __restrict__ pairs, uint32_t U,
+                                                    uint32_t per_xcd, uint32_t* __restrict__ rank) {
+  const uint32_t c = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  const uint64_t b = (uint64_t)c * kRankChunk;
+  if (b >= U) return;
+#pragma unroll 4
+  for (int j = 0; j < kRankChunk / 256; ++j) {
+    const uint64_t r = b + (uint64_t)j * 256 + threadIdx.x;
+    if (r < U) {
+      const uint64_t p = pairs[r];
+      rank[p >> 32] = (uint32_t)p;
+    }
   }
 }
 
@@ -939,6 +977,7 @@ struct BuildWs {
   uint32_t* offsets;
   uint32_t* tickets;
   uint32_t* misc;  // [0] error flag, [1] next U, [2..9] trivial digit flags, [10] largest token
+  uint64_t* pairs;    // plain build: a round's (suffix, rank) pairs
   uint32_t* end_of;   // batched build: end of each position's segment
   uint64_t* seg_off;  // batched build: segment offsets (device copy)
 };
@@ -963,6 +1002,7 @@ size_t carve_build(void* p, uint64_t n, BuildWs* w, uint32_t n_seg = 0) {
   tmp.misc = c.take<uint32_t>(16);
   tmp.end_of = n_seg ? c.take<uint32_t>(n) : nullptr;
   tmp.seg_off = n_seg ? c.take<uint64_t>((size_t)n_seg + 1) : nullptr;
+  tmp.pairs = n_seg == 0 && n >= kPairRanksMin ? c.take<uint64_t>(n) : nullptr;
   if (w) *w = tmp;
   return c.used + 256;
 }
@@ -981,14 +1021,16 @@ struct SortState {
   uint32_t ticket = 0;
 };
 
-// LSD radix sort of (keys, vals) over the low key_bits bits.  Returns the
-// buffer index (0 or 1) that holds the result.
-fc_status radix_sort(BuildWs& w, int src, uint32_t U, int key_bits, SortState& st, hipStream_t stream,
-                     int* result) {
+// LSD radix sort over key bits [shift0, shift0 + key_bits) of kb[src], with
+// vb[src] carried alongside unless vb is null, the passes alternating
+// between the two buffers.  *result is the index (0 or 1) of the buffer
+// that holds the result.
+fc_status radix_sort(BuildWs& w, uint64_t* const kb[2], uint32_t* const vb[2], int src, uint32_t U, int shift0,
+                     int key_bits, SortState& st, hipStream_t stream, int* result) {
   const int digits = (key_bits + 7) / 8;
   FC_CHECK_HIP(hipMemsetAsync(w.hist, 0, sizeof(uint32_t) * kMaxDigits * kRadix, stream));
   const uint32_t hist_blocks = fc::div_up(U, 256) < (uint32_t)kHistBlocks ? fc::div_up(U, 256) : kHistBlocks;
-  hipLaunchKernelGGL(k_hist, dim3(hist_blocks), dim3(256), 0, stream, w.keys[src], U, digits, w.hist);
+  hipLaunchKernelGGL(k_hist, dim3(hist_blocks), dim3(256), 0, stream, kb[src], U, shift0, digits, w.hist);
   FC_CHECK_LAUNCH();
   hipLaunchKernelGGL(k_hist_scan, dim3(1), dim3(256), 0, stream, w.hist, U, digits, w.offsets, w.misc + 2);
   FC_CHECK_LAUNCH();
@@ -1001,9 +1043,15 @@ fc_status radix_sort(BuildWs& w, int src, uint32_t U, int key_bits, SortState& s
     if (trivial[d]) continue;
     if (st.ticket >= (uint32_t)kMaxPasses) return FC_ERR_UNSUPPORTED;
     ++st.epoch;
-    hipLaunchKernelGGL(k_onesweep, dim3(tiles), dim3(kSortThreads), 0, stream, w.keys[cur], w.vals[cur],
-                       w.keys[cur ^ 1], w.vals[cur ^ 1], U, (uint32_t)(8 * d), w.offsets + d * kRadix, w.status,
-                       w.tickets + st.ticket, st.epoch, w.misc);
+    const uint32_t shift = (uint32_t)(shift0 + 8 * d);
+    if (vb)
+      hipLaunchKernelGGL(k_onesweep<true>, dim3(tiles), dim3(kSortThreads), 0, stream, kb[cur], vb[cur],
+                         kb[cur ^ 1], vb[cur ^ 1], U, shift, w.offsets + d * kRadix, w.status, w.tickets + st.ticket,
+                         st.epoch, w.misc);
+    else
+      hipLaunchKernelGGL(k_onesweep<false>, dim3(tiles), dim3(kSortThreads), 0, stream, kb[cur], nullptr,
+                         kb[cur ^ 1], nullptr, U, shift, w.offsets + d * kRadix, w.status, w.tickets + st.ticket,
+                         st.epoch, w.misc);
     FC_CHECK_LAUNCH();
     ++st.ticket;
     cur ^= 1;
@@ -1068,6 +1116,9 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
   FC_CHECK_LAUNCH();
   uint32_t U = N;
   int vin = 0;  // buffer holding the suffixes to sort
+  // ranks through k_rank_write when the rank array is at least the size of
+  // the 256 MB MALL; a smaller one takes the random writes in the MALL
+  const bool pair_ranks = !ext && n_seg == 0 && n >= kPairRanksMin;
   for (int round = 0;; ++round) {
     if (round >= kMaxRounds) return FC_ERR_DEVICE;
     if (round > 0) {
@@ -1084,7 +1135,8 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
       h *= 2;
     }
     int res = vin;
-    fc_status s = radix_sort(w, vin, U, round == 0 ? key0_bits : (int)(2 * sb), st, stream, &res);
+    fc_status s = radix_sort(w, w.keys, w.vals, vin, U, 0, round == 0 ? key0_bits : (int)(2 * sb), st, stream,
+                             &res);
     if (s != FC_OK) return s;
     if (ext && round == 0) {
       hipLaunchKernelGGL(k_ins_sorted, dim3(fc::div_up(N, 256)), dim3(256), 0, stream, w.keys[res], N, ext_shift,
@@ -1099,8 +1151,8 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
                        w.misc + 1);
     FC_CHECK_LAUNCH();
     hipLaunchKernelGGL(k_seg_apply, dim3(seg_tiles), dim3(kSegThreads), 0, stream, w.keys[res], w.vals[res], U, sb,
-                       round == 0 ? 1 : 0, w.part_h, w.part_g, w.part_k, w.rank, w.vals[res ^ 1],
-                       (ext || n_seg > 0) ? nullptr : w.keys[res ^ 1], ext ? nullptr : sa_out);
+                       round == 0 ? 1 : 0, w.part_h, w.part_g, w.part_k, w.rank, pair_ranks ? w.pairs : nullptr,
+                       w.vals[res ^ 1], (ext || n_seg > 0) ? nullptr : w.keys[res ^ 1], ext ? nullptr : sa_out);
     FC_CHECK_LAUNCH();
     uint32_t host_misc[2] = {0, 0};
     FC_CHECK_HIP(hipMemcpyAsync(host_misc, w.misc, sizeof(uint32_t) * 2, hipMemcpyDeviceToHost, stream));
@@ -1112,6 +1164,19 @@ fc_status build_sa(const uint16_t* tokens, uint64_t n, uint32_t n_seg, BuildWs& 
       stats->unresolved[round] = host_misc[1];
       stats->rounds = round + 1;
       stats->sort_passes = (int32_t)st.ticket;
+    }
+    if (pair_ranks && host_misc[1] > 0) {
+      // the round's ranks, for the next round's keys: the pairs sorted by the
+      // suffix's top kRankSortBits bits (the other sort buffer is free now),
+      // then written window by window
+      uint64_t* const pb[2] = {w.pairs, w.keys[res]};
+      const int hb = (int)sb < kRankSortBits ? (int)sb : kRankSortBits;
+      int pres = 0;
+      s = radix_sort(w, pb, nullptr, 0, U, 32 + (int)sb - hb, hb, st, stream, &pres);
+      if (s != FC_OK) return s;
+      const uint32_t per_xcd = fc::div_up(fc::div_up(U, kRankChunk), kXcds);
+      hipLaunchKernelGGL(k_rank_write, dim3(per_xcd * kXcds), dim3(256), 0, stream, pb[pres], U, per_xcd, w.rank);
+      FC_CHECK_LAUNCH();
     }
     U = host_misc[1];
     vin = res ^ 1;
