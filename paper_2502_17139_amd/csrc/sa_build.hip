@@ -35,9 +35,9 @@
 // except the rank scatter itself, which is indexed by suffix.  Where the
 // rank array outgrows the MALL (64M suffixes or more), a random 4-byte write
 // costs a 32-byte memory write, so the round's (suffix, rank) pairs are
-// written in sorted order instead, sorted by the suffix's top 16 bits (two
-// keys-only passes), and then stored one 64 KB window of the rank array
-// after another.
+// written in sorted order instead, sorted by the suffix's top 24 bits
+// (three keys-only passes), and then stored one small window of the rank
+// array after another, each wave's stores falling on a few cache lines.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -557,6 +557,11 @@ __global__ void __launch_bounds__(kSortThreads, kVals ? 1 : 4) k_onesweep(const 
     s_wcnt[ww][t] = (uint16_t)total;
     total += c;
   }
+  // publish this tile's digit count at once (tile 0: its inclusive prefix),
+  // before the tile-local scan and staging, so later tiles' look-backs find it
+  uint64_t* mine = status + (uint64_t)tile * kRadix + t;
+  __hip_atomic_store(mine, pack_status(epoch, tile > 0 ? kFlagAgg : kFlagInc, total), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
   uint32_t tile_sum;
   s_dstart[t] = (uint16_t)fc::block_excl_sum<uint32_t>(total, s_scan, &tile_sum);
   __syncthreads();
@@ -580,10 +585,8 @@ __global__ void __launch_bounds__(kSortThreads, kVals ? 1 : 4) k_onesweep(const 
   // added until an inclusive prefix ends the walk; a tile that has published
   // nothing yet makes the walk wait and reload from there.  One round trip
   // then covers as many tiles as the window instead of one.
-  uint64_t* mine = status + (uint64_t)tile * kRadix + t;
   uint64_t excl = 0;
   if (tile > 0) {
-    __hip_atomic_store(mine, pack_status(epoch, kFlagAgg, total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     int64_t p = (int64_t)tile - 1;  // nearest tile not yet taken
     uint32_t spins = 0;
     bool done = false;
@@ -619,7 +622,8 @@ __global__ void __launch_bounds__(kSortThreads, kVals ? 1 : 4) k_onesweep(const 
       }
     }
   }
-  __hip_atomic_store(mine, pack_status(epoch, kFlagInc, excl + total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tile > 0)
+    __hip_atomic_store(mine, pack_status(epoch, kFlagInc, excl + total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   s_gbase[t] = digit_base[t] + (uint32_t)excl;
   __syncthreads();
 
@@ -834,13 +838,14 @@ __global__ void __launch_bounds__(kSegThreads) k_seg_apply(const uint64_t* __res
 
 // rank[i] = rk for a round's (i << 32 | rk) pairs, sorted by the high bits
 // of i so that each run of equal high bits covers one window of the rank
-// array (64 KB at most).  Workgroup w takes chunk (w % 8) * per_xcd + w / 8
-// of kRankChunk pairs: workgroups are dealt to the eight XCDs in turn, so
-// each XCD writes one contiguous eighth of the sorted pairs, and a window is
+// array (256 bytes at 1G suffixes), and a wave's 64 stores fall on a few
+// cache lines.  Workgroup w takes chunk (w % 8) * per_xcd + w / 8 of
+// kRankChunk pairs: workgroups are dealt to the eight XCDs in turn, so each
+// XCD writes one contiguous eighth of the sorted pairs, and a line is
 // assembled in one L2 rather than written back in pieces from several.
 constexpr int kRankChunk = 4096;
 constexpr int kXcds = 8;
-constexpr int kRankSortBits = 16;  // high bits of the suffix index sorted on
+constexpr int kRankSortBits = 24;  // high bits of the suffix index sorted on
 constexpr uint64_t kPairRanksMin = 1ull << 26;  // suffixes (4-byte ranks: 256 MB)
 __global__ void __launch_bounds__(256) k_rank_write(const uint64_t* __restrict__ pairs, uint32_t U,
                                                     uint32_t per_xcd, uint32_t* __restrict__ rank) {
