@@ -69,7 +69,8 @@ const char* fc_status_string(fc_status s);
  *                token by token by numeric id, a suffix that ends first
  *                (a proper prefix) sorting lower.  The order is total, so the
  *                result is unique.
- * ws, ws_bytes : workspace of at least fc_datastore_build_workspace_bytes(n).
+ * ws, ws_bytes : workspace of at least fc_datastore_build_workspace_bytes(n)
+ *                (about 28.6 bytes per token, 36.6 from 2^26 tokens on).
  * Built by prefix doubling: suffixes are sorted by their first 3 tokens, then
  * by (rank of the first h tokens, rank of the h tokens after them) with h
  * doubling, each round an LSD radix sort restricted to still-tied suffixes.

@@ -42,9 +42,13 @@ def test_status_strings(L):
 
 def test_workspace_sizes(L):
     assert fc.fc_datastore_build_workspace_bytes(1000) < fc.fc_datastore_build_workspace_bytes(2000)
-    # about 28.6 bytes per token for the 1B-token store
-    n = 1_001_999_999
+    # about 28.6 bytes per token below 2^26 tokens (rank, two key and two
+    # value buffers, per-tile status); from 2^26 on, 8 more for the rank
+    # pairs (about 36.6 for the 1B-token store)
+    n = (1 << 26) - 1
     assert 28 * n < fc.fc_datastore_build_workspace_bytes(n) < 29 * n
+    n = 1_001_999_999
+    assert 36 * n < fc.fc_datastore_build_workspace_bytes(n) < 37 * n
     # the batch's slot offsets
     assert L.fc_retrieve_workspace_bytes(1024, 2, fc.FcRetrieveParams(16, 2, 5000, 10)) == 4 * 1025
     assert L.fc_retrieve_workspace_bytes(0, 2, fc.FcRetrieveParams(16, 2, 5000, 10)) == 0

@@ -103,6 +103,23 @@ def test_sa_two_store_workload():
     assert oracle.check_sa(g, sa) == (0, 0)
 
 
+def test_sa_large_texts_rank_pairs():
+    """Stores of 64M suffixes or more take their ranks through sorted
+    (suffix, rank) pairs instead of random writes: just past that size, with
+    a ragged last tile, a near-periodic text (about 25 doubling rounds,
+    nearly every rank rewritten in each) and a 4-token random text, each
+    checked by the linear-time checker."""
+    n = (1 << 26) + 4097
+    periodic = np.tile(np.array([5, 9, 5, 9, 1], np.uint16), n // 5 + 1)[:n].copy()
+    periodic[n // 3] = 7  # one break, so two long runs of the period
+    for name, t, min_rounds in (("near-periodic", periodic, 20), ("vocab 4", synth.random_text(4242, n, 4), 3)):
+        say(f"sa rank pairs: {name} n={n}")
+        sa, stats = fc.fc_datastore_build_stats(dev(t))
+        torch.cuda.synchronize()
+        assert stats["rounds"] >= min_rounds, (name, stats["rounds"])
+        assert oracle.check_sa(t, host(sa)) == (0, 0), name
+
+
 def _batched_case(tok: np.ndarray, off: np.ndarray, full: bool = True):
     """Batched build: store r's slice of the output is the suffix array of
     store r alone (oracle comparison sort, or the linear-time checker)."""
