@@ -44,7 +44,10 @@ constexpr int kSearchThreads = 256;
 constexpr int kGatherThreads = 256;
 constexpr int kScanThreads = 1024;
 constexpr int kOffsetsInLds = 4096;
-constexpr int kGatherBlocks = 1024;  // resident at once: 4 per CU
+// gather grids that are resident at once: five workgroups per CU for rows of
+// up to 10 tokens (90 VGPRs), four for up to 16 (108 VGPRs)
+constexpr int kGatherBlocks10 = 1280;
+constexpr int kGatherBlocks16 = 1024;
 
 struct StoreArgs {
   const uint16_t* tok[FC_MAX_SOURCES];
@@ -848,7 +851,8 @@ fc_status retrieve_launch(const StoreArgs& st, int32_t S, const uint16_t* ctx, i
     for (int s = 0; s < S; ++s) words &= (((uintptr_t)st.tok[s]) & 3) == 0;
     const int out_words = (p.m % 2 == 0) && (((uintptr_t)cont_tok) & 3) == 0;
     const uint64_t want = ((uint64_t)B * p.k + kGatherThreads - 1) / kGatherThreads;
-    const uint32_t blocks = (uint32_t)(want < (uint64_t)kGatherBlocks ? want : (uint64_t)kGatherBlocks);
+    const uint64_t cap = p.m <= 10 ? kGatherBlocks10 : kGatherBlocks16;
+    const uint32_t blocks = (uint32_t)(want < cap ? want : cap);
     if (p.m <= 10)
       hipLaunchKernelGGL(k_gather<10>, dim3(blocks), dim3(kGatherThreads), 0, stream, st, S, B, p.k, p.m, match_n,
                          range_lo, range_cnt, taken, offsets, words, out_words, rows, n_rows, cont_pos, cont_src, cont_len,

@@ -58,7 +58,7 @@ constexpr int kSegTile = kSegThreads * kSegItems;
 constexpr int kScanThreads = 1024;
 constexpr int kMaxPasses = 1024;  // ticket counters per build
 constexpr int kMaxRounds = 40;
-constexpr int kHistBlocks = 1024;
+constexpr int kHistBlocks = 2048;
 constexpr uint32_t kSpinLimit = 1u << 22;
 constexpr int kLookWindow = 8;  // earlier tiles examined per look-back step
 
