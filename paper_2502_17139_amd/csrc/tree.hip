@@ -1151,6 +1151,8 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
 // ---------------------------------------------------------------------------
 
 constexpr int kFlatThreads = 512;
+constexpr int kFlatWide = 1024;     // threads per query for batches of at most kFlatWideMaxB queries
+constexpr int kFlatWideMaxB = 256;
 constexpr int kFlatRows = 4;       // long-string loads in flight per lane
 constexpr int kFlatShortCap = 256;  // short strings a query may keep in LDS
 constexpr int kFlatList = 2048;     // shared trie nodes (two strings or more) listed in LDS
@@ -1365,8 +1367,8 @@ __global__ void __launch_bounds__(kPlanThreads) k_tree_plan(const int32_t* __res
   if (tid == 0 && defer_count) *defer_count = (int32_t)t[3];
 }
 
-template <int MAXM, bool NARROW>
-__global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 6 : 4) k_tree_flat(const int32_t* __restrict__ taken,
+template <int MAXM, bool NARROW, int NT_ = kFlatThreads>
+__global__ void __launch_bounds__(NT_, NT_ == kFlatThreads && MAXM <= 10 ? 6 : 4) k_tree_flat(const int32_t* __restrict__ taken,
                                                             const uint8_t* __restrict__ cont_len,
                                                             const uint16_t* __restrict__ cont_tok,
                                                             const uint16_t* __restrict__ ctx, int L, int S, int k,
@@ -1377,7 +1379,7 @@ __global__ void __launch_bounds__(kFlatThreads, MAXM <= 10 ? 6 : 4) k_tree_flat(
                                                             int32_t* __restrict__ node_tok,
                                                             int32_t* __restrict__ parent, uint32_t* __restrict__ weight,
                                                             int32_t* __restrict__ pos_ids, int32_t* __restrict__ mask) {
-  constexpr int NT = kFlatThreads;
+  constexpr int NT = NT_;
   constexpr int NW = NT / fc::kWave;
   constexpr int W = MAXM / 2;
   using LMT = typename std::conditional<(MAXM <= 15), uint8_t, uint16_t>::type;
@@ -2354,6 +2356,7 @@ struct TreeDevice {
   bool ready = false;
   int max_lds = 0;
   size_t flat_static[2][2] = {{0, 0}, {0, 0}};  // [MAXM 10/16][NARROW]
+  size_t wide_static[2] = {0, 0};                // the kFlatWide-thread flat kernel (MAXM 10), [NARROW]
   size_t full_static[2][2] = {{0, 0}, {0, 0}};  // the full-LDS kernel, same indexes
   size_t any_static = 0;
 };
@@ -2391,6 +2394,8 @@ const TreeDevice* tree_device() {
     d.flat_static[0][0] = raise_lds(k_tree_flat<10, false>, d.max_lds);
     d.flat_static[1][1] = raise_lds(k_tree_flat<16, true>, d.max_lds);
     d.flat_static[1][0] = raise_lds(k_tree_flat<16, false>, d.max_lds);
+    d.wide_static[1] = raise_lds(k_tree_flat<10, true, kFlatWide>, d.max_lds);
+    d.wide_static[0] = raise_lds(k_tree_flat<10, false, kFlatWide>, d.max_lds);
     raise_lds(k_tree_fast<256, 10, true>, d.max_lds);
     raise_lds(k_tree_fast<256, 10, false>, d.max_lds);
     raise_lds(k_tree_fast<256, 16, true>, d.max_lds);
@@ -2478,10 +2483,19 @@ fc_status launch_flat(const int32_t* taken, const uint8_t* cont_len, const uint1
                        defer ? defer_list : nullptr, defer ? counts : nullptr);
     FC_CHECK_LAUNCH();
   }
-  hipLaunchKernelGGL((k_tree_flat<MAXM, NARROW>), dim3(B), dim3(kFlatThreads), lay.total, stream, taken, cont_len,
-                     cont_tok, ctx, L, S, k, m, t.c, a, cap, words, plan ? order : nullptr, self_plan, B, rows,
-                     n_rows,
-                     num_nodes, node_tok, parent, weight, pos_ids, mask);
+  // a small batch leaves CUs idle: each query gets a workgroup twice as wide
+  bool wide = false;
+  if constexpr (MAXM == 10) {
+    wide = !plan && B <= kFlatWideMaxB && lay.total + dv.wide_static[NARROW ? 1 : 0] <= (size_t)dv.max_lds;
+    if (wide)
+      hipLaunchKernelGGL((k_tree_flat<MAXM, NARROW, kFlatWide>), dim3(B), dim3(kFlatWide), lay.total, stream, taken,
+                         cont_len, cont_tok, ctx, L, S, k, m, t.c, a, cap, words, nullptr, self_plan, B, rows, n_rows,
+                         num_nodes, node_tok, parent, weight, pos_ids, mask);
+  }
+  if (!wide)
+    hipLaunchKernelGGL((k_tree_flat<MAXM, NARROW>), dim3(B), dim3(kFlatThreads), lay.total, stream, taken, cont_len,
+                       cont_tok, ctx, L, S, k, m, t.c, a, cap, words, plan ? order : nullptr, self_plan, B, rows,
+                       n_rows, num_nodes, node_tok, parent, weight, pos_ids, mask);
   FC_CHECK_LAUNCH();
   if (defer) {
     hipLaunchKernelGGL((k_tree_fast<1024, MAXM, NARROW>), dim3(B), dim3(1024), full.total, stream, taken, cont_len,
