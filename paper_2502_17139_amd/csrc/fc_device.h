@@ -348,4 +348,52 @@ __device__ __forceinline__ void accept_walk(int n, const int32_t* __restrict__ n
   for (int x = len + lane; x < m + 1; x += kWave) out[x] = -1;
 }
 
+// accept_walk for targets that depend only on a row's depth (a replay's
+// ground truth: the target of a row at depth d is the truth token d places
+// after the stream's position).  A path row at depth d is reached after d
+// accepted tokens, so the walk takes its target from lane `len` of win
+// (lane d holds the target at depth d, or -1); requires m + 1 <= 64.
+template <int MAXROWS>
+__device__ __forceinline__ void accept_walk_depth(int n, const int32_t* __restrict__ node_tok,
+                                                  const int32_t* __restrict__ parent, int R, int m, int32_t win,
+                                                  int32_t* __restrict__ out, int& len, int& u) {
+  constexpr int kChunks = MAXROWS / kWave;
+  const int lane = lane_id();
+  n = n < 1 ? 1 : (n > R ? R : n);
+  int32_t par[kChunks], tok[kChunks];
+#pragma unroll
+  for (int h = 0; h < kChunks; ++h) {
+    const int v = lane + h * kWave;
+    par[h] = v < R ? parent[v] : -2;
+    tok[h] = v < R ? node_tok[v] : -1;
+  }
+#pragma unroll
+  for (int h = 0; h < kChunks; ++h) {
+    const int v = lane + h * kWave;
+    if (v < 1 || v >= n) par[h] = -2, tok[h] = -1;
+  }
+  u = 0;
+  len = 0;
+  for (;;) {
+    const int32_t want = len <= m ? __shfl(win, len, kWave) : -1;
+    if (want < 0) break;
+    int next = -1;
+#pragma unroll
+    for (int h = 0; h < kChunks; ++h) {
+      const uint64_t hit = ballot(par[h] == u && tok[h] == want);
+      if (next < 0 && hit) next = h * kWave + (int)__builtin_ctzll(hit);
+    }
+    if (next < 0) break;
+    if (lane == 0) out[len] = want;
+    ++len;
+    u = next;
+  }
+  const int32_t bonus = len <= m ? __shfl(win, len, kWave) : -1;
+  if (bonus >= 0) {
+    if (lane == 0) out[len] = bonus;
+    ++len;
+  }
+  for (int x = len + lane; x < m + 1; x += kWave) out[x] = -1;
+}
+
 }  // namespace fc

@@ -342,14 +342,22 @@ __global__ void __launch_bounds__(kPrepThreads) k_replay_finish(fc_replay r, int
   const uint16_t* srow = r.truth + (int64_t)b * r.truth_stride;
   const int32_t* pid = r.pos_ids + row;
   int a, last;
-  fc::accept_walk<FC_MAX_TREE_ROWS>(
-      nn, r.node_tok + row, r.parent + row, R, r.rp.m,
-      [&](int v) -> int32_t {
-        if (v >= nn) return -1;
-        const int64_t q = (int64_t)p + pid[v];
-        return (q >= 0 && q < tlen) ? (int32_t)srow[q] : -1;
-      },
-      r.accept_tok + (int64_t)b * (r.rp.m + 1), a, last);
+  if (r.rp.m + 1 <= fc::kWave) {
+    // a row's target is the truth token its depth places after p: the
+    // window p .. p + m, one token per lane, loaded with the tree rows
+    const int32_t win = (lane <= r.rp.m && p + lane < tlen) ? (int32_t)srow[p + lane] : -1;
+    fc::accept_walk_depth<FC_MAX_TREE_ROWS>(nn, r.node_tok + row, r.parent + row, R, r.rp.m, win,
+                                            r.accept_tok + (int64_t)b * (r.rp.m + 1), a, last);
+  } else {
+    fc::accept_walk<FC_MAX_TREE_ROWS>(
+        nn, r.node_tok + row, r.parent + row, R, r.rp.m,
+        [&](int v) -> int32_t {
+          if (v >= nn) return -1;
+          const int64_t q = (int64_t)p + pid[v];
+          return (q >= 0 && q < tlen) ? (int32_t)srow[q] : -1;
+        },
+        r.accept_tok + (int64_t)b * (r.rp.m + 1), a, last);
+  }
   if (lane == 0) {
     r.accept_len[b] = a;
     r.last_node[b] = last;
