@@ -41,6 +41,8 @@
 namespace {
 
 constexpr int kSearchThreads = 256;
+constexpr int kSearchWide = 512;      // threads per query for batches of at most kSearchWideMaxB
+constexpr int kSearchWideMaxB = 256;
 constexpr int kGatherThreads = 256;
 constexpr int kScanThreads = 1024;
 constexpr int kOffsetsInLds = 4096;
@@ -304,7 +306,8 @@ __device__ __forceinline__ void search_query(const StoreArgs& st, int S, const u
 // One query per workgroup: the 2G-ary search of every (store, n, bound),
 // then the kept ranges (the longest non-empty n per store, store priority
 // order) written to the query's row.
-__global__ void __launch_bounds__(kSearchThreads) k_search(StoreArgs st, int S, const uint16_t* __restrict__ ctx,
+template <int NT>
+__global__ void __launch_bounds__(NT) k_search(StoreArgs st, int S, const uint16_t* __restrict__ ctx,
                                                            int L, int n_max, int n_min, int k, int G, int log2_2g,
                                                            const int32_t* __restrict__ rows, int n_rows,
                                                            int32_t* __restrict__ match_n,
@@ -832,14 +835,21 @@ fc_status retrieve_launch(const StoreArgs& st, int32_t S, const uint16_t* ctx, i
                           int32_t* taken, uint32_t* cont_pos, uint8_t* cont_src, uint8_t* cont_len,
                           uint16_t* cont_tok, const int32_t* rows, int32_t n_rows, void* ws, hipStream_t stream) {
   (void)hipGetLastError();
-  // lanes per search task: the largest power of two <= 16 that fits
+  // lanes per search task: the largest power of two <= 16 that fits; a
+  // small batch leaves CUs idle, so its workgroups are twice as wide
+  const bool wide = B <= kSearchWideMaxB;
+  const int nt = wide ? kSearchWide : kSearchThreads;
   const int tasks = S * (p.n_max - p.n_min + 1) * 2;
   int G = 16;
-  while (G > 1 && G * tasks > kSearchThreads) G >>= 1;
+  while (G > 1 && G * tasks > nt) G >>= 1;
   int log2_2g = 1;
   while ((1 << log2_2g) < 2 * G) ++log2_2g;
-  hipLaunchKernelGGL(k_search, dim3(B), dim3(kSearchThreads), 0, stream, st, S, ctx, L, p.n_max, p.n_min, p.k, G,
-                     log2_2g, rows, n_rows, match_n, range_lo, range_cnt, taken);
+  if (wide)
+    hipLaunchKernelGGL(k_search<kSearchWide>, dim3(B), dim3(kSearchWide), 0, stream, st, S, ctx, L, p.n_max, p.n_min,
+                       p.k, G, log2_2g, rows, n_rows, match_n, range_lo, range_cnt, taken);
+  else
+    hipLaunchKernelGGL(k_search<kSearchThreads>, dim3(B), dim3(kSearchThreads), 0, stream, st, S, ctx, L, p.n_max,
+                       p.n_min, p.k, G, log2_2g, rows, n_rows, match_n, range_lo, range_cnt, taken);
   FC_CHECK_LAUNCH();
   if (p.m <= 16) {
     uint32_t* offsets = (uint32_t*)ws;
