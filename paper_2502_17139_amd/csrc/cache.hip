@@ -162,7 +162,8 @@ __global__ void __launch_bounds__(kCacheThreads) k_cache_retrieve(
   }
 
   // 2. one pass over the suffixes, in contiguous chunks: each is compared
-  //    with the n-token pattern q (eight tokens per LDS round trip) and is
+  //    with the n-token pattern q (its first token alone, then, where that
+  //    agrees, eight tokens per LDS round trip) and is
   //    below it, starts with it (an occurrence) or is above it.  A chunk has
   //    at most FC_MAX_CACHE_TOKENS / kCacheThreads = 16 suffixes, so its
   //    occurrences fit a bit mask; one block scan of (below << 16 | occurrences)
@@ -193,7 +194,9 @@ __global__ void __launch_bounds__(kCacheThreads) k_cache_retrieve(
   const uint32_t i1 = i0 + per < len ? i0 + per : len;
   uint32_t occ_bits = 0, packed = 0;
   for (uint32_t i = i0; i < i1; ++i) {
-    const int c = cmp_q(i);
+    // most suffixes differ from q at their first token: one LDS read decides
+    const uint16_t t0 = T[i];
+    const int c = t0 != qv[0] ? (t0 < qv[0] ? -1 : 1) : cmp_q(i);
     packed += c < 0 ? (1u << 16) : (c == 0 ? 1u : 0u);
     occ_bits |= c == 0 ? (1u << (i - i0)) : 0u;
   }
