@@ -14,7 +14,8 @@
 //      range_lo (the suffixes below it) and the occurrences (the suffixes
 //      that start with it), numbered in text order by a block scan;
 //   3. the occurrences in suffix order: ranks by counting pairwise
-//      comparisons when there are at most 128, else a bitonic sort in LDS;
+//      comparisons when there are at most 128 (beyond 32, each unordered
+//      pair compared once), else a bitonic sort in LDS;
 //   4. the kept ones (strided floor(i*cnt/k) beyond k) and their
 //      continuations, cut before a 0 and at the end of the text.
 #include <hip/hip_runtime.h>
@@ -222,6 +223,35 @@ __global__ void __launch_bounds__(kCacheThreads) k_cache_retrieve(
     const uint32_t mine = (i < cnt && j == 0) ? occ[i] : 0u;
     __syncthreads();
     if (i < cnt && j == 0) occ[rank] = mine;
+    __syncthreads();
+  } else if (cnt <= 128 && Pc + 4 * cnt <= pow2_at_least((uint32_t)stride)) {
+    // every unordered pair compared once, both answers kept in a bit matrix
+    // past the occurrence list: bit j of row i (4 words a row) says that
+    // occurrence j's suffix is below occurrence i's, and i's rank is its
+    // row's population count
+    uint32_t* lt = occ + Pc;
+    for (uint32_t x = (uint32_t)tid; x < 4 * cnt; x += kCacheThreads) lt[x] = 0;
+    __syncthreads();
+    const uint32_t npairs = cnt * (cnt - 1) / 2;
+    for (uint32_t q = (uint32_t)tid; q < npairs; q += kCacheThreads) {
+      // pair q is (i, j), i < j, with j(j - 1) / 2 <= q < j(j + 1) / 2
+      uint32_t j = (uint32_t)((sqrtf(8.0f * (float)q + 1.0f) + 1.0f) * 0.5f);
+      while (j * (j - 1) / 2 > q) --j;
+      while (j * (j + 1) / 2 <= q) ++j;
+      const uint32_t i = q - j * (j - 1) / 2;
+      if (suffix_less(T, len, occ[j], occ[i], n)) atomicOr(&lt[4 * i + (j >> 5)], 1u << (j & 31));
+      else atomicOr(&lt[4 * j + (i >> 5)], 1u << (i & 31));
+    }
+    __syncthreads();
+    const uint32_t i = (uint32_t)tid;
+    uint32_t rank = 0, mine = 0;
+    if (i < cnt) {
+      rank = (uint32_t)(__builtin_popcount(lt[4 * i]) + __builtin_popcount(lt[4 * i + 1]) +
+                        __builtin_popcount(lt[4 * i + 2]) + __builtin_popcount(lt[4 * i + 3]));
+      mine = occ[i];
+    }
+    __syncthreads();
+    if (i < cnt) occ[rank] = mine;
     __syncthreads();
   } else if (cnt <= 128) {
     const uint32_t G = cnt <= 64 ? 16u : 8u;  // lanes per occurrence i
