@@ -43,6 +43,8 @@ namespace {
 constexpr int kSearchThreads = 256;
 constexpr int kSearchWide = 512;      // threads per query for batches of at most kSearchWideMaxB
 constexpr int kSearchWideMaxB = 256;
+constexpr int kSearchWidest = 1024;   // and for batches of at most kSearchWidestMaxB
+constexpr int kSearchWidestMaxB = 128;
 constexpr int kGatherThreads = 256;
 constexpr int kScanThreads = 1024;
 constexpr int kOffsetsInLds = 4096;
@@ -836,15 +838,19 @@ fc_status retrieve_launch(const StoreArgs& st, int32_t S, const uint16_t* ctx, i
                           uint16_t* cont_tok, const int32_t* rows, int32_t n_rows, void* ws, hipStream_t stream) {
   (void)hipGetLastError();
   // lanes per search task: the largest power of two <= 16 that fits; a
-  // small batch leaves CUs idle, so its workgroups are twice as wide
-  const bool wide = B <= kSearchWideMaxB;
-  const int nt = wide ? kSearchWide : kSearchThreads;
+  // small batch leaves CUs idle, so its workgroups are two or four times as
+  // wide
+  const bool widest = B <= kSearchWidestMaxB, wide = B <= kSearchWideMaxB;
+  const int nt = widest ? kSearchWidest : wide ? kSearchWide : kSearchThreads;
   const int tasks = S * (p.n_max - p.n_min + 1) * 2;
   int G = 16;
   while (G > 1 && G * tasks > nt) G >>= 1;
   int log2_2g = 1;
   while ((1 << log2_2g) < 2 * G) ++log2_2g;
-  if (wide)
+  if (widest)
+    hipLaunchKernelGGL(k_search<kSearchWidest>, dim3(B), dim3(kSearchWidest), 0, stream, st, S, ctx, L, p.n_max,
+                       p.n_min, p.k, G, log2_2g, rows, n_rows, match_n, range_lo, range_cnt, taken);
+  else if (wide)
     hipLaunchKernelGGL(k_search<kSearchWide>, dim3(B), dim3(kSearchWide), 0, stream, st, S, ctx, L, p.n_max, p.n_min,
                        p.k, G, log2_2g, rows, n_rows, match_n, range_lo, range_cnt, taken);
   else
