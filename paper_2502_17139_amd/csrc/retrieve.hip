@@ -476,6 +476,7 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
                                                            uint16_t* __restrict__ cont_tok) {
   __shared__ uint32_t s_off[kOffsetsInLds];
   __shared__ uint32_t s_scan[kGatherThreads / fc::kWave + 1];
+  __shared__ int s_qab[2];  // the queries owning the piece's first and last slots
   __shared__ int32_t s_taken[kMetaQueries][FC_MAX_SOURCES];
   __shared__ uint32_t s_cnt[kMetaQueries][FC_MAX_SOURCES], s_lo[kMetaQueries][FC_MAX_SOURCES];
   __shared__ int32_t s_n[kMetaQueries][FC_MAX_SOURCES];
@@ -512,9 +513,15 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
     for (int q = b0; q < b1; ++q) sum += s_off[q];
     uint32_t all;
     uint32_t run = fc::block_excl_sum<uint32_t>(sum, s_scan, &all);
+    // this workgroup's piece, and the queries owning its first and last
+    // slots, found while the offsets are written (no search afterwards)
+    const uint32_t pa = (uint32_t)(((uint64_t)all * blockIdx.x) / gridDim.x);
+    const uint32_t pe = (uint32_t)(((uint64_t)all * (blockIdx.x + 1)) / gridDim.x);
     for (int q = b0; q < b1; ++q) {
       const uint32_t x = s_off[q];
       s_off[q] = run;
+      if (pa < pe && run <= pa && pa < run + x) s_qab[0] = q;
+      if (pa < pe && run <= pe - 1 && pe - 1 < run + x) s_qab[1] = q;
       run += x;
     }
     if (tid == 0) s_off[B] = all;
@@ -533,8 +540,8 @@ __global__ void __launch_bounds__(kGatherThreads) k_gather(StoreArgs st, int S, 
     }
     return lo;
   };
-  const int qa = owner(a, 0, B);
-  const int qb = owner(e - 1, qa, B);
+  const int qa = in_lds ? s_qab[0] : owner(a, 0, B);
+  const int qb = in_lds ? s_qab[1] : owner(e - 1, qa, B);
   const int nq = qb - qa + 1;
   const bool meta_lds = nq <= kMetaQueries;
   if (meta_lds && tid < nq * FC_MAX_SOURCES) {
