@@ -60,7 +60,8 @@ constexpr int kMaxPasses = 1024;  // ticket counters per build
 constexpr int kMaxRounds = 40;
 constexpr int kHistBlocks = 2048;
 constexpr uint32_t kSpinLimit = 1u << 22;
-constexpr int kLookWindow = 8;  // earlier tiles examined per look-back step
+constexpr int kLookWindow = 2;  // earlier tiles examined per look-back step (with the counts
+                                // published early, wider windows only add loads)
 
 constexpr uint64_t kFlagAgg = 1ull << 46;
 constexpr uint64_t kFlagInc = 2ull << 46;
