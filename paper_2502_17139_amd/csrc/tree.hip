@@ -1832,13 +1832,9 @@ __global__ void __launch_bounds__(NT_, NT_ == kFlatThreads && MAXM <= 10 ? 6 : 4
     // 4. chunk sums: alpha, non-empty strings (root weight), nodes, the
     //    chunk's shared nodes (depths past its own LCP, up to the next
     //    string's: they fix where the chunk's part of the list of shared
-    //    nodes starts) and tail nodes (depths past both LCPs), and the
-    //    chunk's first head per depth (first q with lcp[q] < d)
+    //    nodes starts) and tail nodes (depths past both LCPs)
     const uint32_t a0 = alpha.a[0];
     uint32_t asum = 0, rw = 0, nodes = 0, nsh = 0, ntail = 0;
-    uint16_t f[MAXM + 1];
-#pragma unroll
-    for (int d = 0; d <= MAXM; ++d) f[d] = (uint16_t)T;
     int l_after = p1 < T ? (int)((uint32_t)lm[p1] & kLo) : 0;
     for (int p = p1 - 1; p >= p0; --p) {
       const uint32_t x = lm[p];
@@ -1852,9 +1848,6 @@ __global__ void __launch_bounds__(NT_, NT_ == kFlatThreads && MAXM <= 10 ? 6 : 4
       const int lo_t = l > l_after ? l : l_after;
       ntail += li > lo_t ? (uint32_t)(li - lo_t) : 0u;
       l_after = l;
-#pragma unroll
-      for (int d = 1; d <= MAXM; ++d)
-        if (l < d) f[d] = (uint16_t)p;
     }
     // With one store weight, shared node (q, d) weighs alpha times the
     // distance from q to the next head of depth d (the next position whose
@@ -1914,6 +1907,17 @@ __global__ void __launch_bounds__(NT_, NT_ == kFlatThreads && MAXM <= 10 ? 6 : 4
     auto prepare_walk = [&]() {
       if (walk_ready) return;
       walk_ready = true;
+      // the chunk's first head per depth (first q with lcp[q] < d), from
+      // the LCPs again (not kept from the sums, whose hot path needs none)
+      uint16_t f[MAXM + 1];
+#pragma unroll
+      for (int d = 0; d <= MAXM; ++d) f[d] = (uint16_t)T;
+      for (int p = p1 - 1; p >= p0; --p) {
+        const int l = (int)((uint32_t)lm[p] & kLo);
+#pragma unroll
+        for (int d = 1; d <= MAXM; ++d)
+          if (l < d) f[d] = (uint16_t)p;
+      }
 #pragma unroll
       for (int d = 1; d <= MAXM; ++d) {
         uint32_t wave_min = (uint32_t)T;
