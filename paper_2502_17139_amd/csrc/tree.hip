@@ -1153,7 +1153,11 @@ __global__ void __launch_bounds__(NT, 4) k_tree_fast(const int32_t* __restrict__
 constexpr int kFlatThreads = 512;
 constexpr int kFlatWide = 1024;     // threads per query for batches of at most kFlatWideMaxB queries
 constexpr int kFlatWideMaxB = 256;
-constexpr int kFlatRows = 4;       // long-string loads in flight per lane
+// long-string rows in flight per lane: five for rows of up to 10 tokens (a
+// 5,000-string list in two passes of a 512-thread workgroup), four for up to
+// 16 (where a fifth would cost a wave per SIMD)
+template <int MAXM>
+constexpr int flat_rows() { return MAXM <= 10 ? 5 : 4; }
 constexpr int kFlatShortCap = 256;  // short strings a query may keep in LDS
 constexpr int kFlatList = 2048;     // shared trie nodes (two strings or more) listed in LDS
 
@@ -1646,6 +1650,7 @@ __global__ void __launch_bounds__(NT_, NT_ == kFlatThreads && MAXM <= 10 ? 6 : 4
     };
     // with every short string in LDS the long pass also places them
     const bool place = in_lds && n_short > 0;
+    constexpr int kFlatRows = flat_rows<MAXM>();
     for (int j0 = 0; j0 < nL; j0 += kPass * kFlatRows) {
       uint32_t v[kFlatRows][W];
       int len[kFlatRows];
